@@ -1,0 +1,239 @@
+/*
+ * leyline.h -- C ABI of the MI355X (gfx950) KV-cache splice library (libleyline.so).
+ *
+ * The library implements the data-parallel hot path of a policy-driven KV-cache edit:
+ * a directive replaces the cached token span [span_start, span_end) of a sequence by a
+ * replacement ("stub") of stub_len tokens whose K/V the caller has already computed at their
+ * final positions (the directive 4-tuple and its positional contract: paper Sec. 3.1; the
+ * tensor effect of each step: appendix "Kernel specification: tensors and composition").
+ * Every cached token downstream of the span moves by Delta = stub_len - (span_end - span_start);
+ * its rotary key band is re-anchored with the closed-form rotation k' = R(Delta) k
+ * (paper Eq. "rotate", Sec. 3.2), while non-rotary data (MLA latent c_kv / K_nope, GQA V) is
+ * moved bit-for-bit.  Several non-overlapping directives per call are applied left to right with
+ * a running (cumulative) shift of either sign; overlapping spans are rejected (appendix "Kernel
+ * specification", multiple directives).  RoPE pairs are interleaved (dims 2i, 2i+1) or half-split
+ * (dims i, i+d/2) per plane (Sec. 3.3 "RoPE pairing convention").  Rotation arithmetic is fp32
+ * with cos/sin of the exact integer shift times theta_i evaluated in fp64 once per call and
+ * directive; results are rounded to nearest-even into the storage dtype (Sec. 5.1 "bf16 K-storage
+ * precision floor").
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Return value: LEYLINE_OK (0) or a negative LEYLINE_E_* code; leyline_strerror() names it.
+ * - All arguments are validated before anything is enqueued: a call that returns an error has
+ *   not touched device memory (the per-call all-or-none rule).  A failure reported by the HIP
+ *   runtime after the first enqueue (LEYLINE_E_HIP) cannot be rolled back.
+ * - "device" pointers are HIP device memory owned by the caller; "host" pointers are ordinary
+ *   host memory read (or written) only during the call.  The library never allocates or frees
+ *   device memory and keeps no state between calls; it is re-entrant.
+ * - stream is a hipStream_t passed as void* (NULL = the default stream).  Device work is
+ *   asynchronous on it; host outputs are complete when the call returns.  The caller orders the
+ *   call against kernels that read the cache.
+ * - Element offsets and strides are counted in elements of the cache dtype.  Every device base
+ *   pointer must be 16-byte aligned and every row, stride, head and rotary band must span a
+ *   multiple of 16 bytes (rows are moved as 16-byte vectors); otherwise LEYLINE_E_INVAL.
+ */
+#ifndef LEYLINE_H
+#define LEYLINE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LEYLINE_ABI_VERSION 1
+#define LEYLINE_MAX_PLANES 4
+
+enum {
+    LEYLINE_OK = 0,
+    LEYLINE_E_INVAL = -1,     /* null pointer, bad descriptor, misaligned layout             */
+    LEYLINE_E_RANGE = -2,     /* span outside [0, seq_len], seq index out of range            */
+    LEYLINE_E_ORDER = -3,     /* directives not sorted by (seq, span_start)                   */
+    LEYLINE_E_OVERLAP = -4,   /* two spans of one sequence overlap                            */
+    LEYLINE_E_CAPACITY = -5,  /* new length > capacity, too few free pages, output too small  */
+    LEYLINE_E_MODE = -6,      /* FORGET requested: not a splice, the caller re-prefills       */
+    LEYLINE_E_WORKSPACE = -7, /* workspace missing or smaller than the query reported         */
+    LEYLINE_E_HIP = -8        /* the HIP runtime reported an error while enqueueing           */
+};
+
+/* Storage dtype of the whole cache (all planes). */
+enum { LEYLINE_BF16 = 0, LEYLINE_F32 = 1 };
+
+/* RoPE pairing of a plane's rotary bands (Sec. 3.3): interleaved pairs dims (2i, 2i+1) of the
+ * band; NEOX (half-split) pairs dims (i, i + rot_dim/2). */
+enum { LEYLINE_ROPE_INTERLEAVED = 0, LEYLINE_ROPE_NEOX = 1 };
+
+/* Directive mode (Sec. 3.1): AMORTIZE is the in-place splice; FORGET asks for true forgetting,
+ * which is a prefix-trimmed re-prefill and is refused here with LEYLINE_E_MODE. */
+enum { LEYLINE_AMORTIZE = 0, LEYLINE_FORGET = 1 };
+
+/* Device-side status bits a kernel may OR into the optional device_status word. */
+enum {
+    LEYLINE_STATUS_BAD_PAGE = 1,  /* a block-table or free-list entry was outside [0, capacity) */
+    LEYLINE_STATUS_BAD_ROW = 2    /* a row index given to leyline_rotate_delta was out of range  */
+};
+
+/*
+ * One tensor family stored per token and layer.  MLA caches have one plane (row = latent c_kv
+ * followed by K_pe); GQA caches have a K plane (rotated over whole heads) and a V plane (moved
+ * only).  Row r of layer l starts at element
+ *     contiguous cache: base + l*layer_stride + r*token_stride
+ *     paged cache:      base + l*layer_stride + page*page_stride + (r % page_size)*token_stride
+ * A row holds row_elems elements; head h < n_heads starts at h*head_stride within the row and
+ * carries rot_dim rotary elements starting at rot_offset within the head (rot_dim = 0: the plane
+ * is moved only).  Frequencies are theta_i = rope_base^(-2i/rot_dim) (RoFormer), or inv_freq[i]
+ * when inv_freq (host, rot_dim/2 doubles) is non-NULL.
+ */
+typedef struct leyline_plane {
+    void* base;             /* device */
+    int64_t layer_stride;   /* elements between layers */
+    int64_t token_stride;   /* elements between consecutive rows (within a page when paged) */
+    int64_t page_stride;    /* elements between physical pages (paged only; ignored otherwise) */
+    int32_t row_elems;
+    int32_t n_heads;        /* >= 1 when rot_dim > 0 */
+    int32_t head_stride;
+    int32_t rot_offset;
+    int32_t rot_dim;        /* even; 0 = no rotary band */
+    int32_t rope_style;     /* LEYLINE_ROPE_* */
+    double rope_base;
+    const double* inv_freq; /* host, nullable */
+} leyline_plane;
+
+typedef struct leyline_cache {
+    int32_t dtype;          /* LEYLINE_BF16 or LEYLINE_F32 */
+    int32_t n_layers;       /* >= 1 */
+    int32_t n_planes;       /* 1 .. LEYLINE_MAX_PLANES */
+    int32_t page_size;      /* 0: contiguous cache; > 0: tokens per page */
+    int64_t capacity;       /* contiguous: rows allocated per layer; paged: physical pages in the pool */
+    leyline_plane planes[LEYLINE_MAX_PLANES];
+} leyline_cache;
+
+/*
+ * A directive D = (span_start, span_end, R, mode) of Sec. 3.1, in the pre-call coordinates of
+ * sequence `seq` (0 for a contiguous cache).  stub[p] is the replacement's K/V for plane p:
+ * device memory, dense [n_layers][stub_len][row_elems] in the cache dtype, already RoPE'd at its
+ * final positions [span_start + running_shift, ... + stub_len); it is copied verbatim and never
+ * rotated.  stub[p] may be NULL only when stub_len == 0.  An empty span (pure insertion) and an
+ * empty stub (pure deletion) are both valid.
+ */
+typedef struct leyline_directive {
+    int32_t seq;
+    int32_t mode;           /* LEYLINE_AMORTIZE (LEYLINE_FORGET -> LEYLINE_E_MODE) */
+    int64_t span_start;
+    int64_t span_end;
+    int64_t stub_len;
+    const void* stub[LEYLINE_MAX_PLANES];
+} leyline_directive;
+
+/* Human-readable name of a return code (static storage). */
+const char* leyline_strerror(int code);
+
+/* LEYLINE_ABI_VERSION of the loaded library. */
+int leyline_abi_version(void);
+
+/*
+ * Contiguous in-place splice of one sequence (all layers and planes).
+ *
+ * cache->page_size must be 0; rows [0, seq_len) hold the sequence, capacity rows are allocated.
+ * dirs: host array of n_dirs >= 0 directives (seq = 0), sorted by span_start, non-overlapping
+ * (adjacent spans are allowed).  After the call, rows [0, *new_len_out) hold the spliced sequence:
+ * prefix rows untouched, each stub at its new position, each downstream row at its old position
+ * plus the running shift with its rotary bands rotated by that shift.  Rows [new_len, max(seq_len,
+ * new_len)) are left unspecified.  Source and destination ranges overlap; the library orders the
+ * moves so that every row is read before it is overwritten.
+ * Errors: E_INVAL, E_RANGE, E_ORDER, E_OVERLAP, E_CAPACITY (new length > capacity), E_MODE, E_HIP.
+ */
+int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len,
+                          const leyline_directive* dirs, int32_t n_dirs,
+                          int64_t* new_len_out, void* stream);
+
+/*
+ * Sizes of a paged splice, computed on the host from lengths and directives alone.
+ *
+ * cache: the paged cache the splice will run on (its plane layout sizes the cos/sin tables).
+ * seq_lens: host [n_seqs]; bt_stride: row length of the block tables; dirs: host, sorted by
+ * (seq, span_start).  Outputs (host, each nullable): new_seq_lens[n_seqs]; *n_fresh_needed =
+ * fresh pages the call will consume; *n_freed = pages the call will drop from block tables;
+ * *workspace_bytes = device workspace the call needs.
+ * Errors: as leyline_splice_paged's validation (E_CAPACITY when a new table exceeds bt_stride).
+ */
+int leyline_paged_query(const leyline_cache* cache, int32_t n_seqs, const int32_t* seq_lens,
+                        int32_t bt_stride, const leyline_directive* dirs, int32_t n_dirs,
+                        int32_t* new_seq_lens, int32_t* n_fresh_needed, int32_t* n_freed,
+                        int64_t* workspace_bytes);
+
+/* Page kinds of a paged plan. */
+enum { LEYLINE_PAGE_IDENTITY = 0, LEYLINE_PAGE_REMAP = 1, LEYLINE_PAGE_ASSEMBLE = 2, LEYLINE_PAGE_NONE = -1 };
+
+/*
+ * Symbolic page plan (host only), for schedulers and tests.  For new logical page k of sequence
+ * b (k < ceil(new_len/page_size)):
+ *   IDENTITY: every row comes from the same position of old logical page k, shift 0;
+ *             the physical page is kept and not touched.
+ *   REMAP:    every row comes from old logical page src at the same in-page offset with one
+ *             nonzero shift (a multiple of page_size); the physical page is re-used and only its
+ *             rotary bands are rotated in place.
+ *   ASSEMBLE: the rows are gathered into fresh page number src (fresh pages are numbered in
+ *             ascending (b, k) order and taken from free_pages in that order).
+ * Old logical pages referenced by neither IDENTITY nor REMAP are freed, listed in ascending
+ * (b, old page) order.  The paper describes no paging; this rule is the library's own.
+ *
+ * kind_out, src_out: host [n_seqs][bt_stride] (LEYLINE_PAGE_NONE / -1 past the new length);
+ * freed_seq_out, freed_page_out: host [freed_cap].  E_CAPACITY when bt_stride or freed_cap is
+ * too small.
+ */
+int leyline_paged_plan(int32_t page_size, int32_t n_seqs, const int32_t* seq_lens,
+                       const leyline_directive* dirs, int32_t n_dirs, int32_t bt_stride,
+                       int32_t* kind_out, int32_t* src_out,
+                       int32_t* freed_seq_out, int32_t* freed_page_out, int32_t freed_cap);
+
+/*
+ * Paged splice of a batch of sequences (all layers and planes), following the page plan above.
+ *
+ * cache->page_size > 0, cache->capacity = physical pages in the pool.
+ * seq_lens: host [n_seqs].  block_table_in / block_table_out: device int32 [n_seqs][bt_stride],
+ * must not alias; on completion block_table_out holds every sequence's new table and -1 past
+ * its last page.  free_pages: device int32 [n_free], consumed from index 0 by ASSEMBLE pages.
+ * freed_pages_out: device int32 [freed_cap], receives the dropped physical pages.
+ * Host outputs (nullable): new_seq_lens_out[n_seqs], *n_fresh_used_out, *n_freed_out.
+ * device_status: device int32, nullable; kernels OR LEYLINE_STATUS_* bits into it when a page
+ * index read from device memory is outside [0, capacity) (that row is then skipped).
+ * workspace: device, >= the size leyline_paged_query reports (the plan is uploaded into it with
+ * an asynchronous copy on `stream`; reuse it only after the stream has passed this call).
+ *
+ * Ownership: only ASSEMBLE pages (fresh) and REMAP pages (rotary bands, in place) are written.
+ * Pages holding the rows of a REMAP page must not be shared with another sequence.  Freed pages
+ * are not written; the caller may recycle them once the stream has passed this call.
+ * Errors: as leyline_splice_contig, plus E_CAPACITY (too few free pages, freed_cap or bt_stride
+ * too small) and E_WORKSPACE.
+ */
+int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, const int32_t* seq_lens,
+                         const int32_t* block_table_in, int32_t* block_table_out, int32_t bt_stride,
+                         const leyline_directive* dirs, int32_t n_dirs,
+                         const int32_t* free_pages, int32_t n_free,
+                         int32_t* freed_pages_out, int32_t freed_cap,
+                         int32_t* new_seq_lens_out, int32_t* n_fresh_used_out, int32_t* n_freed_out,
+                         int32_t* device_status,
+                         void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * In-place re-anchoring without movement: every rotary band of the given rows, in every layer,
+ * becomes R(delta) times itself (Eq. "rotate").  Non-rotary elements are not touched.
+ *
+ * Rows are physical: contiguous cache -> row index r < capacity; paged cache -> page*page_size +
+ * offset with page < capacity.  rows: device int64 [n_rows] (nullable: then rows row0 ..
+ * row0+n_rows-1).  Listed rows must be distinct.  device_status as above (out-of-range listed
+ * rows are skipped and flagged with LEYLINE_STATUS_BAD_ROW).
+ * Errors: E_INVAL, E_RANGE (row0 range outside the cache), E_HIP.
+ */
+int leyline_rotate_delta(const leyline_cache* cache, int64_t delta,
+                         const int64_t* rows, int64_t row0, int64_t n_rows,
+                         int32_t* device_status, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LEYLINE_H */

@@ -1,0 +1,154 @@
+// Plain-old-data parameter blocks shared by the host planner (built with the host compiler)
+// and the HIP kernels (built with hipcc).  Layouts must stay identical on both sides: only
+// fixed-width integers, floats and raw pointers.
+#pragma once
+
+#include <cstdint>
+
+#include "leyline.h"
+
+namespace leyline {
+
+// Rows are moved as 16-byte vectors ("chunks").  A work unit is one chunk, or for half-split
+// (NEOX) rotary bands a chunk of the low half together with its partner chunk half a band away.
+enum : int32_t { KROT_NONE = 0, KROT_INTERLEAVED = 1, KROT_NEOX = 2 };
+
+struct KPlane {
+    char* base;              // device
+    int64_t layer_stride;    // bytes
+    int64_t token_stride;    // bytes
+    int64_t page_stride;     // bytes (paged caches)
+    int32_t row_bytes;
+    int32_t row_chunks;      // row_bytes / 16
+    int32_t units;           // work units per row (all chunks)
+    int32_t rot_units;       // work units per row that touch a rotary band
+    int32_t rot;             // KROT_*
+    int32_t n_heads;
+    int32_t head_chunks;     // head stride in chunks
+    int32_t rot_lo;          // first rotary chunk within a head
+    int32_t rot_chunks;      // rotary band length in chunks (whole band, both halves)
+    int32_t cs_off;          // offset of this plane's pairs within one shift's cos/sin block
+};
+
+struct KCosSin {
+    float c, s;
+};
+
+// ------------------------------------------------------------------------------ contiguous --
+constexpr int KMAX_JOBS = 6;
+constexpr int KMAX_ITEMS = KMAX_JOBS * LEYLINE_MAX_PLANES;
+constexpr int KMAX_CS = 192;
+
+struct KContigJob {
+    int64_t src0;            // move: first source row
+    int64_t dst0;            // stub: first destination row
+    int64_t count;           // rows
+    int64_t delta;           // move: nonzero shift; stub: 0
+    int32_t chains;          // move: min(|delta|, count); stub: count
+    int32_t cs;              // move: first cos/sin entry of this shift (-1: no rotation)
+    int32_t is_stub;
+    int32_t pad;
+    const char* stub[LEYLINE_MAX_PLANES];   // stub: per plane, dense [layers][count][row]
+};
+
+struct KContigParams {
+    KPlane planes[LEYLINE_MAX_PLANES];
+    KContigJob jobs[KMAX_JOBS];
+    int32_t item_job[KMAX_ITEMS];
+    int32_t item_plane[KMAX_ITEMS];
+    int32_t item_block_end[KMAX_ITEMS];   // inclusive prefix sum of blocks per layer
+    int32_t n_items;
+    int32_t n_layers;
+    KCosSin cs[KMAX_CS];
+};
+
+// ------------------------------------------------------------------------------ rotate-only --
+struct KRotateParams {
+    KPlane planes[LEYLINE_MAX_PLANES];
+    int32_t n_planes;
+    int32_t n_layers;
+    int32_t page_size;       // 0: contiguous
+    int32_t pad;
+    int64_t total_rows;      // bound for listed rows
+    const int64_t* rows;     // device, nullable
+    int64_t row0;
+    int64_t n_rows;
+    int32_t* status;         // device, nullable
+    int32_t units_per_row;   // sum of rot_units over planes
+    int32_t pad2;
+    KCosSin cs[KMAX_CS];
+};
+
+// ----------------------------------------------------------------------------------- paged --
+struct KSeqEntry {
+    int32_t dir_begin, dir_count, old_len, new_len;
+};
+
+struct KDirEntry {
+    int64_t stub_start;      // new position of the replacement's first token
+    int64_t stub_len;
+    int64_t delta;           // cumulative shift of the segment that follows the replacement
+    int32_t cs;              // first cos/sin entry of that shift (-1: shift 0 or no rotary plane)
+    int32_t pad;
+    const char* stub[LEYLINE_MAX_PLANES];
+};
+
+struct KAssembleTask {
+    int32_t seq, k, fresh, pad;
+};
+
+struct KRemapTask {
+    int32_t seq, k, src_page, dir;
+};
+
+struct KPageEntry {
+    int32_t kind, src;       // LEYLINE_PAGE_*, old logical page or fresh ordinal
+};
+
+struct KFreedEntry {
+    int32_t seq, page;
+};
+
+// Byte offsets of the tables inside the workspace (converted to pointers at launch).
+struct KPagedTables {
+    int64_t off_seq, off_dir, off_cs, off_asm, off_remap, off_pages, off_freed, total;
+    int32_t n_seqs, n_dirs, n_cs, n_asm, n_remap, n_pages, n_freed, bt_stride;
+};
+
+struct KPagedParams {
+    KPlane planes[LEYLINE_MAX_PLANES];
+    int32_t n_planes;
+    int32_t n_layers;
+    int32_t page_size;
+    int32_t bt_stride;
+    int32_t n_asm;
+    int32_t n_remap;
+    int64_t capacity;                    // physical pages
+    const KSeqEntry* seqs;
+    const KDirEntry* dirs;
+    const KCosSin* cs;
+    const KAssembleTask* asm_tasks;
+    const KRemapTask* remap_tasks;
+    const int32_t* bt_in;
+    const int32_t* free_pages;
+    int32_t n_free;
+    int32_t pad;
+    int32_t* status;
+};
+
+struct KTableParams {
+    const KPageEntry* pages;   // [n_seqs * bt_stride]
+    const KFreedEntry* freed;  // [n_freed]
+    const int32_t* bt_in;
+    int32_t* bt_out;
+    const int32_t* free_pages;
+    int32_t* freed_out;
+    int32_t* status;
+    int64_t capacity;
+    int32_t n_pages;           // n_seqs * bt_stride
+    int32_t n_freed;
+    int32_t bt_stride;
+    int32_t n_free;
+};
+
+}  // namespace leyline

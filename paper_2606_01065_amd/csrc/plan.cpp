@@ -1,0 +1,482 @@
+// Host planner of the splice library: argument validation, ordering of overlapping in-place
+// moves, paged page plans and fp64 cos/sin tables.  No HIP calls: everything here runs and is
+// tested without a GPU.
+#include "plan.hpp"
+
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstring>
+
+namespace leyline {
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int elem_size(int32_t dtype) {
+    if (dtype == LEYLINE_BF16) return 2;
+    if (dtype == LEYLINE_F32) return 4;
+    return 0;
+}
+
+}  // namespace
+
+int describe_cache(const leyline_cache* cache, bool paged, KPlane out[LEYLINE_MAX_PLANES],
+                   int* n_planes) {
+    if (!cache) return LEYLINE_E_INVAL;
+    const int esz = elem_size(cache->dtype);
+    if (!esz || cache->n_layers < 1 || cache->n_layers > 65535 || cache->n_planes < 1 ||
+        cache->n_planes > LEYLINE_MAX_PLANES)
+        return LEYLINE_E_INVAL;
+    if (paged ? cache->page_size < 1 : cache->page_size != 0) return LEYLINE_E_INVAL;
+    if (cache->capacity < 0) return LEYLINE_E_INVAL;
+    int32_t cs_off = 0;
+    for (int p = 0; p < cache->n_planes; ++p) {
+        const leyline_plane& pl = cache->planes[p];
+        KPlane& k = out[p];
+        std::memset(&k, 0, sizeof(k));
+        if (!pl.base || !aligned16(pl.base) || pl.row_elems <= 0) return LEYLINE_E_INVAL;
+        const int64_t row_bytes = int64_t(pl.row_elems) * esz;
+        if (row_bytes % 16) return LEYLINE_E_INVAL;
+        if (pl.token_stride < pl.row_elems || pl.layer_stride < 0) return LEYLINE_E_INVAL;
+        if ((pl.token_stride * esz) % 16 || (pl.layer_stride * esz) % 16) return LEYLINE_E_INVAL;
+        if (cache->n_layers > 1 && pl.layer_stride == 0) return LEYLINE_E_INVAL;
+        if (paged) {
+            if (pl.page_stride < int64_t(cache->page_size) * pl.token_stride && cache->capacity > 1)
+                return LEYLINE_E_INVAL;
+            if ((pl.page_stride * esz) % 16) return LEYLINE_E_INVAL;
+        }
+        k.base = static_cast<char*>(pl.base);
+        k.layer_stride = pl.layer_stride * esz;
+        k.token_stride = pl.token_stride * esz;
+        k.page_stride = paged ? pl.page_stride * esz : 0;
+        k.row_bytes = int32_t(row_bytes);
+        k.row_chunks = int32_t(row_bytes / 16);
+        k.units = k.row_chunks;
+        k.rot = KROT_NONE;
+        if (pl.rot_dim != 0) {
+            if (pl.rot_dim < 0 || (pl.rot_dim & 1) || pl.n_heads < 1 || pl.head_stride <= 0 ||
+                pl.rot_offset < 0 || pl.rot_offset + pl.rot_dim > pl.head_stride ||
+                int64_t(pl.n_heads) * pl.head_stride > pl.row_elems)
+                return LEYLINE_E_INVAL;
+            if (pl.rope_style != LEYLINE_ROPE_INTERLEAVED && pl.rope_style != LEYLINE_ROPE_NEOX)
+                return LEYLINE_E_INVAL;
+            if (!pl.inv_freq && !(pl.rope_base > 0.0)) return LEYLINE_E_INVAL;
+            const bool neox = pl.rope_style == LEYLINE_ROPE_NEOX;
+            if ((int64_t(pl.head_stride) * esz) % 16 || (int64_t(pl.rot_offset) * esz) % 16)
+                return LEYLINE_E_INVAL;
+            if ((int64_t(neox ? pl.rot_dim / 2 : pl.rot_dim) * esz) % 16) return LEYLINE_E_INVAL;
+            k.rot = neox ? KROT_NEOX : KROT_INTERLEAVED;
+            k.n_heads = pl.n_heads;
+            k.head_chunks = int32_t(int64_t(pl.head_stride) * esz / 16);
+            k.rot_lo = int32_t(int64_t(pl.rot_offset) * esz / 16);
+            k.rot_chunks = int32_t(int64_t(pl.rot_dim) * esz / 16);
+            if (neox) {
+                k.units = k.row_chunks - k.n_heads * (k.rot_chunks / 2);
+                k.rot_units = k.n_heads * (k.rot_chunks / 2);
+            } else {
+                k.rot_units = k.n_heads * k.rot_chunks;
+            }
+            k.cs_off = cs_off;
+            cs_off += pl.rot_dim / 2;
+        }
+    }
+    if (cs_off > KMAX_CS) return LEYLINE_E_INVAL;
+    *n_planes = cache->n_planes;
+    return LEYLINE_OK;
+}
+
+int32_t cos_sin_per_shift(const leyline_cache* cache) {
+    int32_t n = 0;
+    for (int p = 0; p < cache->n_planes; ++p) n += cache->planes[p].rot_dim / 2;
+    return n;
+}
+
+int32_t append_cos_sin(const leyline_cache* cache, int64_t shift, std::vector<KCosSin>& table) {
+    const int32_t first = int32_t(table.size());
+    const double d = double(shift);   // exact: |shift| < 2^53
+    for (int p = 0; p < cache->n_planes; ++p) {
+        const leyline_plane& pl = cache->planes[p];
+        const int half = pl.rot_dim / 2;
+        for (int i = 0; i < half; ++i) {
+            // theta_i = base^(-2i/d_rot) (RoFormer), or the caller's table
+            const double theta = pl.inv_freq ? pl.inv_freq[i]
+                                             : std::pow(pl.rope_base, -2.0 * i / pl.rot_dim);
+            const double phi = d * theta;
+            table.push_back(KCosSin{float(std::cos(phi)), float(std::sin(phi))});
+        }
+    }
+    return first;
+}
+
+int check_sequence(int64_t seq_len, const leyline_directive* dirs, int32_t n_dirs,
+                   int32_t n_planes) {
+    if (n_dirs < 0 || (n_dirs > 0 && !dirs) || seq_len < 0) return LEYLINE_E_INVAL;
+    int64_t prev_start = 0, prev_end = 0;
+    for (int32_t j = 0; j < n_dirs; ++j) {
+        const leyline_directive& d = dirs[j];
+        if (d.mode == LEYLINE_FORGET) return LEYLINE_E_MODE;
+        if (d.mode != LEYLINE_AMORTIZE) return LEYLINE_E_INVAL;
+        if (d.span_start < 0 || d.span_start > d.span_end || d.span_end > seq_len || d.stub_len < 0)
+            return LEYLINE_E_RANGE;
+        if (j > 0 && d.span_start < prev_start) return LEYLINE_E_ORDER;
+        if (j > 0 && d.span_start < prev_end) return LEYLINE_E_OVERLAP;
+        if (d.stub_len > 0)
+            for (int p = 0; p < n_planes; ++p)
+                if (!d.stub[p] || !aligned16(d.stub[p])) return LEYLINE_E_INVAL;
+        prev_start = d.span_start;
+        prev_end = d.span_end;
+    }
+    return LEYLINE_OK;
+}
+
+// ------------------------------------------------------------------------------ contiguous --
+
+int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_directive* dirs,
+                int32_t n_dirs, ContigSchedule* out) {
+    KPlane planes[LEYLINE_MAX_PLANES];
+    int n_planes = 0;
+    int rc = describe_cache(cache, false, planes, &n_planes);
+    if (rc) return rc;
+    if (seq_len < 0 || seq_len > cache->capacity) return LEYLINE_E_RANGE;
+    for (int32_t j = 0; j < n_dirs; ++j)
+        if (dirs && dirs[j].seq != 0) return LEYLINE_E_RANGE;
+    rc = check_sequence(seq_len, dirs, n_dirs, n_planes);
+    if (rc) return rc;
+
+    int64_t new_len = seq_len;
+    for (int32_t j = 0; j < n_dirs; ++j) {
+        if (dirs[j].stub_len > cache->capacity) return LEYLINE_E_CAPACITY;
+        new_len += dirs[j].stub_len - (dirs[j].span_end - dirs[j].span_start);
+    }
+    if (new_len > cache->capacity) return LEYLINE_E_CAPACITY;
+    out->new_len = new_len;
+    out->launches.clear();
+
+    // Jobs: each downstream segment [e_j, s_{j+1}) moved by its running shift, each stub copied.
+    std::vector<ContigJobHost> jobs;
+    int64_t shift = 0;
+    for (int32_t j = 0; j < n_dirs; ++j) {
+        const leyline_directive& d = dirs[j];
+        if (d.stub_len > 0)
+            jobs.push_back(ContigJobHost{true, 0, d.span_start + shift, d.stub_len, 0, j});
+        shift += d.stub_len - (d.span_end - d.span_start);
+        const int64_t seg_end = (j + 1 < n_dirs) ? dirs[j + 1].span_start : seq_len;
+        const int64_t count = seg_end - d.span_end;
+        if (count > 0 && shift != 0)
+            jobs.push_back(ContigJobHost{false, d.span_end, 0, count, shift, j});
+    }
+    if (jobs.empty()) return LEYLINE_OK;
+
+    // Job a must finish before job b when b writes a row that a reads.  Within one job the
+    // overlap of its own source and destination is resolved by the kernel's chain order.  The
+    // resulting graph is acyclic: a left-moving segment can only wait for segments to its left,
+    // a right-moving one only for segments to its right, and a stub only for moves.
+    const size_t n = jobs.size();
+    auto dst_lo = [&](const ContigJobHost& x) { return x.is_stub ? x.dst0 : x.src0 + x.delta; };
+    std::vector<int> level(n, 0);
+    for (size_t iter = 0; iter < n; ++iter) {
+        bool changed = false;
+        for (size_t b = 0; b < n; ++b) {
+            const int64_t blo = dst_lo(jobs[b]), bhi = blo + jobs[b].count;
+            for (size_t a = 0; a < n; ++a) {
+                if (a == b || jobs[a].is_stub) continue;
+                const int64_t alo = jobs[a].src0, ahi = alo + jobs[a].count;
+                if (blo < ahi && alo < bhi && level[b] < level[a] + 1) {
+                    level[b] = level[a] + 1;
+                    changed = true;
+                }
+            }
+        }
+        if (!changed) break;
+    }
+    const int n_levels = *std::max_element(level.begin(), level.end()) + 1;
+    const int32_t cs_need = cos_sin_per_shift(cache);
+    for (int lv = 0; lv < n_levels; ++lv) {
+        std::vector<ContigJobHost> cur;
+        int32_t cs_used = 0;
+        for (size_t a = 0; a < n; ++a) {
+            if (level[a] != lv) continue;
+            const int32_t need = jobs[a].is_stub ? 0 : cs_need;
+            if (int(cur.size()) == KMAX_JOBS || cs_used + need > KMAX_CS) {
+                out->launches.push_back(cur);
+                cur.clear();
+                cs_used = 0;
+            }
+            cur.push_back(jobs[a]);
+            cs_used += need;
+        }
+        if (!cur.empty()) out->launches.push_back(cur);
+    }
+    return LEYLINE_OK;
+}
+
+// ----------------------------------------------------------------------------------- paged --
+
+namespace {
+
+struct Piece {                 // a run of new positions with one source
+    int64_t lo, hi;            // new positions [lo, hi)
+    bool stub;
+    int64_t shift;             // old row = new position - shift
+    int32_t dir;               // directive whose segment / stub this is (-1: prefix)
+};
+
+}  // namespace
+
+int plan_paged(int32_t page_size, int32_t n_seqs, const int32_t* seq_lens,
+               const leyline_directive* dirs, int32_t n_dirs, int32_t n_planes, PagedPlan* out) {
+    if (page_size < 1 || n_seqs < 0 || (n_seqs > 0 && !seq_lens) || n_dirs < 0 ||
+        (n_dirs > 0 && !dirs))
+        return LEYLINE_E_INVAL;
+    for (int32_t b = 0; b < n_seqs; ++b)
+        if (seq_lens[b] < 0) return LEYLINE_E_RANGE;
+    for (int32_t j = 0; j < n_dirs; ++j) {
+        if (dirs[j].seq < 0 || dirs[j].seq >= n_seqs) return LEYLINE_E_RANGE;
+        if (j > 0 && dirs[j].seq < dirs[j - 1].seq) return LEYLINE_E_ORDER;
+    }
+    out->page_size = page_size;
+    out->n_seqs = n_seqs;
+    out->new_lens.assign(n_seqs, 0);
+    out->page_seq.clear(); out->page_k.clear(); out->page_kind.clear();
+    out->page_src.clear(); out->page_dir.clear();
+    out->freed_seq.clear(); out->freed_page.clear();
+    out->n_fresh = out->n_assemble = out->n_remap = 0;
+
+    int32_t j0 = 0;
+    std::vector<Piece> pieces;
+    std::vector<char> kept;
+    for (int32_t b = 0; b < n_seqs; ++b) {
+        int32_t j1 = j0;
+        while (j1 < n_dirs && dirs[j1].seq == b) ++j1;
+        const int64_t n = seq_lens[b];
+        int rc = check_sequence(n, dirs + j0, j1 - j0, n_planes);
+        if (rc) return rc;
+        // pieces in new-position order
+        pieces.clear();
+        int64_t shift = 0, cursor = 0, pos = 0;
+        for (int32_t j = j0; j < j1; ++j) {
+            const leyline_directive& d = dirs[j];
+            if (d.span_start > cursor) {
+                pieces.push_back(Piece{pos, pos + d.span_start - cursor, false, shift, j > j0 ? j - 1 : -1});
+                pos += d.span_start - cursor;
+            }
+            if (d.stub_len > 0) {
+                pieces.push_back(Piece{pos, pos + d.stub_len, true, 0, j});
+                pos += d.stub_len;
+            }
+            shift += d.stub_len - (d.span_end - d.span_start);
+            cursor = d.span_end;
+            if (pos > INT32_MAX) return LEYLINE_E_CAPACITY;
+        }
+        if (n > cursor) {
+            pieces.push_back(Piece{pos, pos + n - cursor, false, shift, j1 > j0 ? j1 - 1 : -1});
+            pos += n - cursor;
+        }
+        if (pos > INT32_MAX) return LEYLINE_E_CAPACITY;
+        const int64_t n_new = pos;
+        out->new_lens[b] = int32_t(n_new);
+        const int64_t old_pages = (n + page_size - 1) / page_size;
+        const int64_t new_pages = (n_new + page_size - 1) / page_size;
+        kept.assign(size_t(old_pages), 0);
+        size_t pi = 0;
+        for (int64_t k = 0; k < new_pages; ++k) {
+            const int64_t lo = k * page_size, hi = std::min<int64_t>(lo + page_size, n_new);
+            while (pi < pieces.size() && pieces[pi].hi <= lo) ++pi;
+            // pieces[pi] is the first piece overlapping [lo, hi)
+            const Piece& p = pieces[pi];
+            const bool single = p.lo <= lo && p.hi >= hi;
+            int32_t kind = LEYLINE_PAGE_ASSEMBLE, src = -1, dir = -1;
+            if (single && !p.stub && p.shift == 0) {
+                kind = LEYLINE_PAGE_IDENTITY;
+                src = int32_t(k);
+            } else if (single && !p.stub && p.shift % page_size == 0) {
+                kind = LEYLINE_PAGE_REMAP;
+                src = int32_t(k - p.shift / page_size);
+                dir = p.dir;
+            }
+            if (kind == LEYLINE_PAGE_ASSEMBLE) {
+                src = out->n_fresh++;
+                ++out->n_assemble;
+            } else {
+                kept[size_t(src)] = 1;
+                if (kind == LEYLINE_PAGE_REMAP) ++out->n_remap;
+            }
+            out->page_seq.push_back(b);
+            out->page_k.push_back(int32_t(k));
+            out->page_kind.push_back(kind);
+            out->page_src.push_back(src);
+            out->page_dir.push_back(dir);
+        }
+        for (int64_t kp = 0; kp < old_pages; ++kp)
+            if (!kept[size_t(kp)]) {
+                out->freed_seq.push_back(b);
+                out->freed_page.push_back(int32_t(kp));
+            }
+        j0 = j1;
+    }
+    return LEYLINE_OK;
+}
+
+int build_paged_image(const leyline_cache* cache, const PagedPlan& plan, int32_t n_seqs,
+                      const leyline_directive* dirs, int32_t n_dirs, int32_t bt_stride,
+                      PagedImage* img) {
+    std::vector<KSeqEntry> seqs(static_cast<size_t>(n_seqs));
+    std::vector<KDirEntry> dtab(static_cast<size_t>(n_dirs));
+    std::vector<KCosSin> cs;
+    const bool any_rot = cos_sin_per_shift(cache) > 0;
+    int32_t j0 = 0;
+    for (int32_t b = 0; b < n_seqs; ++b) {
+        int32_t j1 = j0;
+        while (j1 < n_dirs && dirs[j1].seq == b) ++j1;
+        seqs[size_t(b)] = KSeqEntry{j0, j1 - j0, 0, plan.new_lens[size_t(b)]};
+        int64_t shift = 0;
+        for (int32_t j = j0; j < j1; ++j) {
+            const leyline_directive& d = dirs[j];
+            KDirEntry& e = dtab[size_t(j)];
+            std::memset(&e, 0, sizeof(e));
+            e.stub_start = d.span_start + shift;
+            e.stub_len = d.stub_len;
+            shift += d.stub_len - (d.span_end - d.span_start);
+            e.delta = shift;
+            e.cs = (shift != 0 && any_rot) ? append_cos_sin(cache, shift, cs) : -1;
+            for (int p = 0; p < cache->n_planes; ++p)
+                e.stub[p] = static_cast<const char*>(d.stub[p]);
+        }
+        j0 = j1;
+    }
+    std::vector<KAssembleTask> asm_tasks;
+    std::vector<KRemapTask> remap_tasks;
+    std::vector<KPageEntry> pages(size_t(n_seqs) * size_t(bt_stride), KPageEntry{LEYLINE_PAGE_NONE, -1});
+    for (size_t i = 0; i < plan.page_kind.size(); ++i) {
+        const int32_t b = plan.page_seq[i], k = plan.page_k[i];
+        if (k >= bt_stride) return LEYLINE_E_CAPACITY;
+        pages[size_t(b) * bt_stride + k] = KPageEntry{plan.page_kind[i], plan.page_src[i]};
+        if (plan.page_kind[i] == LEYLINE_PAGE_ASSEMBLE)
+            asm_tasks.push_back(KAssembleTask{b, k, plan.page_src[i], 0});
+        else if (plan.page_kind[i] == LEYLINE_PAGE_REMAP)
+            remap_tasks.push_back(KRemapTask{b, k, plan.page_src[i], plan.page_dir[i]});
+    }
+    std::vector<KFreedEntry> freed(plan.freed_seq.size());
+    for (size_t i = 0; i < freed.size(); ++i) freed[i] = KFreedEntry{plan.freed_seq[i], plan.freed_page[i]};
+
+    KPagedTables& t = img->tables;
+    std::memset(&t, 0, sizeof(t));
+    int64_t off = 0;
+    auto place = [&](size_t bytes) {
+        const int64_t at = off;
+        off += int64_t((bytes + 255) / 256 * 256);
+        return at;
+    };
+    t.off_seq = place(seqs.size() * sizeof(KSeqEntry));
+    t.off_dir = place(dtab.size() * sizeof(KDirEntry));
+    t.off_cs = place(cs.size() * sizeof(KCosSin));
+    t.off_asm = place(asm_tasks.size() * sizeof(KAssembleTask));
+    t.off_remap = place(remap_tasks.size() * sizeof(KRemapTask));
+    t.off_pages = place(pages.size() * sizeof(KPageEntry));
+    t.off_freed = place(freed.size() * sizeof(KFreedEntry));
+    t.total = off;
+    t.n_seqs = n_seqs; t.n_dirs = n_dirs; t.n_cs = int32_t(cs.size());
+    t.n_asm = int32_t(asm_tasks.size()); t.n_remap = int32_t(remap_tasks.size());
+    t.n_pages = int32_t(pages.size()); t.n_freed = int32_t(freed.size()); t.bt_stride = bt_stride;
+    img->bytes.assign(size_t(off), 0);
+    auto put = [&](int64_t at, const void* src, size_t bytes) {
+        if (bytes) std::memcpy(img->bytes.data() + at, src, bytes);
+    };
+    put(t.off_seq, seqs.data(), seqs.size() * sizeof(KSeqEntry));
+    put(t.off_dir, dtab.data(), dtab.size() * sizeof(KDirEntry));
+    put(t.off_cs, cs.data(), cs.size() * sizeof(KCosSin));
+    put(t.off_asm, asm_tasks.data(), asm_tasks.size() * sizeof(KAssembleTask));
+    put(t.off_remap, remap_tasks.data(), remap_tasks.size() * sizeof(KRemapTask));
+    put(t.off_pages, pages.data(), pages.size() * sizeof(KPageEntry));
+    put(t.off_freed, freed.data(), freed.size() * sizeof(KFreedEntry));
+    return LEYLINE_OK;
+}
+
+int check_table_width(const PagedPlan& plan, const int32_t* seq_lens, int32_t bt_stride) {
+    for (int32_t b = 0; b < plan.n_seqs; ++b) {
+        const int64_t old_pages = (int64_t(seq_lens[b]) + plan.page_size - 1) / plan.page_size;
+        const int64_t new_pages = (int64_t(plan.new_lens[size_t(b)]) + plan.page_size - 1) / plan.page_size;
+        if (old_pages > bt_stride || new_pages > bt_stride) return LEYLINE_E_CAPACITY;
+    }
+    return LEYLINE_OK;
+}
+
+}  // namespace leyline
+
+// ------------------------------------------------------------------------ host-only C ABI ---
+
+extern "C" const char* leyline_strerror(int code) {
+    switch (code) {
+        case LEYLINE_OK: return "ok";
+        case LEYLINE_E_INVAL: return "invalid argument or cache layout";
+        case LEYLINE_E_RANGE: return "span or sequence index out of range";
+        case LEYLINE_E_ORDER: return "directives not sorted by (seq, span_start)";
+        case LEYLINE_E_OVERLAP: return "directive spans overlap";
+        case LEYLINE_E_CAPACITY: return "capacity exceeded (rows, pages, block table or freed list)";
+        case LEYLINE_E_MODE: return "FORGET mode is a re-prefill, not a splice";
+        case LEYLINE_E_WORKSPACE: return "workspace missing or too small";
+        case LEYLINE_E_HIP: return "HIP runtime error";
+        default: return "unknown leyline status";
+    }
+}
+
+extern "C" int leyline_abi_version(void) { return LEYLINE_ABI_VERSION; }
+
+extern "C" int leyline_paged_query(const leyline_cache* cache, int32_t n_seqs,
+                                   const int32_t* seq_lens, int32_t bt_stride,
+                                   const leyline_directive* dirs, int32_t n_dirs,
+                                   int32_t* new_seq_lens, int32_t* n_fresh_needed, int32_t* n_freed,
+                                   int64_t* workspace_bytes) {
+    using namespace leyline;
+    KPlane planes[LEYLINE_MAX_PLANES];
+    int n_planes = 0;
+    int rc = describe_cache(cache, true, planes, &n_planes);
+    if (rc) return rc;
+    if (bt_stride < 0) return LEYLINE_E_INVAL;
+    PagedPlan plan;
+    rc = plan_paged(cache->page_size, n_seqs, seq_lens, dirs, n_dirs, n_planes, &plan);
+    if (rc) return rc;
+    rc = check_table_width(plan, seq_lens, bt_stride);
+    if (rc) return rc;
+    PagedImage img;
+    rc = build_paged_image(cache, plan, n_seqs, dirs, n_dirs, bt_stride, &img);
+    if (rc) return rc;
+    if (new_seq_lens)
+        for (int32_t b = 0; b < n_seqs; ++b) new_seq_lens[b] = plan.new_lens[size_t(b)];
+    if (n_fresh_needed) *n_fresh_needed = plan.n_fresh;
+    if (n_freed) *n_freed = int32_t(plan.freed_page.size());
+    if (workspace_bytes) *workspace_bytes = img.tables.total;
+    return LEYLINE_OK;
+}
+
+extern "C" int leyline_paged_plan(int32_t page_size, int32_t n_seqs, const int32_t* seq_lens,
+                                  const leyline_directive* dirs, int32_t n_dirs, int32_t bt_stride,
+                                  int32_t* kind_out, int32_t* src_out,
+                                  int32_t* freed_seq_out, int32_t* freed_page_out, int32_t freed_cap) {
+    using namespace leyline;
+    if (bt_stride < 0 || (n_seqs > 0 && (!kind_out || !src_out))) return LEYLINE_E_INVAL;
+    PagedPlan plan;
+    // stub pointers are not needed for a symbolic plan: validate them against zero planes
+    int rc = plan_paged(page_size, n_seqs, seq_lens, dirs, n_dirs, 0, &plan);
+    if (rc) return rc;
+    rc = check_table_width(plan, seq_lens, bt_stride);
+    if (rc) return rc;
+    if (int64_t(plan.freed_page.size()) > freed_cap) return LEYLINE_E_CAPACITY;
+    if (plan.freed_page.size() && (!freed_seq_out || !freed_page_out)) return LEYLINE_E_INVAL;
+    for (int64_t i = 0; i < int64_t(n_seqs) * bt_stride; ++i) {
+        kind_out[i] = LEYLINE_PAGE_NONE;
+        src_out[i] = -1;
+    }
+    for (size_t i = 0; i < plan.page_k.size(); ++i) {
+        const int64_t at = int64_t(plan.page_seq[i]) * bt_stride + plan.page_k[i];
+        kind_out[at] = plan.page_kind[i];
+        src_out[at] = plan.page_src[i];
+    }
+    for (size_t i = 0; i < plan.freed_page.size(); ++i) {
+        freed_seq_out[i] = plan.freed_seq[i];
+        freed_page_out[i] = plan.freed_page[i];
+    }
+    return LEYLINE_OK;
+}

@@ -1,0 +1,77 @@
+// Host-side planning for the splice kernels: validation of the C-ABI arguments, the order in
+// which overlapping contiguous moves may run, paged page plans, and the fp64 -> fp32 cos/sin
+// tables.  Pure C++ (no HIP calls) so that every rule here can be exercised without a GPU.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <vector>
+
+#include "leyline.h"
+#include "kparams.hpp"
+
+namespace leyline {
+
+// A validated plane, reduced to what the kernels need (byte strides, 16-byte chunk geometry).
+int describe_cache(const leyline_cache* cache, bool paged, KPlane out[LEYLINE_MAX_PLANES],
+                   int* n_planes);
+
+// Validation of one sequence's directives (already restricted to that sequence).
+int check_sequence(int64_t seq_len, const leyline_directive* dirs, int32_t n_dirs,
+                   int32_t n_planes);
+
+// cos/sin of (shift * theta_i), evaluated in fp64 and rounded to fp32, for every rotary pair of
+// every rotary plane, appended to `table`.  Returns the offset of the first entry.
+int32_t append_cos_sin(const leyline_cache* cache, int64_t shift, std::vector<KCosSin>& table);
+
+// Number of cos/sin entries one shift needs (sum over rotary planes of rot_dim / 2).
+int32_t cos_sin_per_shift(const leyline_cache* cache);
+
+// ------------------------------------------------------------------------------------------
+// Contiguous splice: a set of jobs (move a source range by a shift, or copy a stub) grouped
+// into launches so that no job of a launch overwrites a row another job of the same or a later
+// launch still has to read.
+struct ContigJobHost {
+    bool is_stub;
+    int64_t src0, dst0, count, delta;
+    int32_t dir;        // stub: directive index
+};
+
+struct ContigSchedule {
+    int64_t new_len = 0;
+    std::vector<std::vector<ContigJobHost>> launches;
+};
+
+int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_directive* dirs,
+                int32_t n_dirs, ContigSchedule* out);
+
+// ------------------------------------------------------------------------------------------
+// Paged splice.
+struct PagedPlan {
+    int32_t page_size = 0;
+    int32_t n_seqs = 0;
+    std::vector<int32_t> new_lens;
+    // per (seq, new logical page), in ascending order
+    std::vector<int32_t> page_seq, page_k, page_kind, page_src, page_dir;   // page_dir: remap shift's directive (-1: none)
+    std::vector<int32_t> freed_seq, freed_page;
+    int32_t n_fresh = 0;
+    int32_t n_assemble = 0, n_remap = 0;
+};
+
+int plan_paged(int32_t page_size, int32_t n_seqs, const int32_t* seq_lens,
+               const leyline_directive* dirs, int32_t n_dirs, int32_t n_planes, PagedPlan* out);
+
+// E_CAPACITY unless every sequence's old and new page count fits a block-table row.
+int check_table_width(const PagedPlan& plan, const int32_t* seq_lens, int32_t bt_stride);
+
+// Device-side image of a paged plan (built into the caller's workspace).
+struct PagedImage {
+    std::vector<unsigned char> bytes;   // contents to upload
+    KPagedTables tables;                // offsets into the workspace (pointers filled at launch)
+};
+
+int build_paged_image(const leyline_cache* cache, const PagedPlan& plan, int32_t n_seqs,
+                      const leyline_directive* dirs, int32_t n_dirs, int32_t bt_stride,
+                      PagedImage* img);
+
+}  // namespace leyline

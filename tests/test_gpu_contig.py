@@ -1,0 +1,206 @@
+"""GPU parity of the contiguous in-place splice and of the in-place rotation (through the C ABI)
+against the CPU oracle, on the same seeded inputs."""
+
+import random
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import splice_oracle as O
+from tests.parity_util import assert_rows_match, host, oracle_plane
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2606_01065_amd import leyline
+    return leyline
+
+
+def _specs(L, wl, tensors):
+    return [L.PlaneSpec(t, p.n_heads, p.head_stride or p.row_elems, p.rot_offset, p.rot_dim,
+                        p.style, p.base) for p, t in zip(wl.planes, tensors)]
+
+
+def _dir_dicts(wl, stubs):
+    return [dict(span_start=d.span_start, span_end=d.span_end, stub=stubs[j], seq=d.seq,
+                 stub_len=d.stub_len) for j, d in enumerate(wl.dirs)]
+
+
+def _run_and_check(L, wl, planes_dev, stubs_dev, label):
+    """Snapshot inputs, splice on the GPU, splice in the oracle, compare rows [0, n')."""
+    print(f"[case] {label}", flush=True)
+    before = [host(t) for t in planes_dev]
+    stubs_h = [[host(s) for s in per] for per in stubs_dev]
+    cache = L.make_cache(_specs(L, wl, planes_dev))
+    dirs = L.make_directives(_dir_dicts(wl, stubs_dev))
+    n = wl.seq_lens[0]
+    new_len = L.leyline_splice_contig(cache, n, dirs, len(wl.dirs))
+    torch.cuda.synchronize()
+    odirs = [O.Directive(d.span_start, d.span_end, d.stub_len) for d in wl.dirs]
+    assert new_len == O.new_length(n, odirs)
+    for pi, (desc, t) in enumerate(zip(wl.planes, planes_dev)):
+        plane = oracle_plane(desc)
+        got = host(t).reshape(wl.n_layers, wl.capacity, -1)
+        src = before[pi].reshape(wl.n_layers, wl.capacity, -1)
+        stubs = [s[pi].reshape(wl.n_layers, s[pi].shape[1], -1) for s in stubs_h]
+        want, _ = O.splice_contig(src, n, odirs, stubs, plane, wl.dtype)
+        assert_rows_match(got[:, :new_len], want[:, :new_len], plane, wl.dtype,
+                          inputs=_inputs_for_new_rows(src, n, odirs, stubs),
+                          what=f"{label} plane {pi}")
+    return new_len
+
+
+def _inputs_for_new_rows(src, n, dirs, stubs):
+    """The pre-rotation rows in new-position order (prefix, stub, downstream), per layer."""
+    pieces, cursor = [], 0
+    for j, d in enumerate(dirs):
+        pieces.append(src[:, cursor:d.span_start])
+        pieces.append(stubs[j])
+        cursor = d.span_end
+    pieces.append(src[:, cursor:n])
+    return np.concatenate(pieces, axis=1)
+
+
+def _small_workload(rng, kind, dtype, n_layers, n, dirs, extra=0):
+    if kind == "mla":
+        planes = [W.mla_plane()]
+    elif kind == "gqa":
+        planes = W.gqa_planes(heads=2, dim=128)
+    elif kind == "mla_neox":
+        planes = [W.PlaneDesc((576,), 1, 576, 512, 64, 1, 10000.0)]
+    else:  # several interleaved heads with a partial rotary band, and a move-only plane
+        planes = [W.PlaneDesc((4, 64), 4, 64, 32, 32, 0, 50000.0), W.PlaneDesc((128,))]
+    cap = n + max(0, sum(d.stub_len - (d.span_end - d.span_start) for d in dirs)) + extra
+    return W.Workload(f"small_{kind}", n_layers, dtype, planes, dirs, [n], capacity=max(cap, n),
+                      seed=rng.randint(0, 10 ** 6))
+
+
+def _random_dirs(rng, n, k):
+    cuts = sorted(rng.sample(range(n + 1), min(2 * k, n + 1)))
+    out = []
+    for i in range(0, len(cuts) - 1, 2):
+        s, e = cuts[i], cuts[i + 1]
+        r = rng.choice([0, 1, rng.randint(0, 2 * (e - s) + 4), e - s, max(0, e - s - 1), e - s + 1])
+        out.append(W.Dir(s, e, r))
+    return out
+
+
+def test_mla_1l_4k_f32_exact_recipe(L):
+    """Keys built exactly as described: raw N(0,1) K_pe RoPE'd at its position (theta 1e4,
+    interleaved); stub K_pe RoPE'd at 1024..1039.  After the splice every moved K_pe must match
+    a fresh RoPE of its raw key at the new position, and the whole cache must match the oracle."""
+    wl = W.mla_1l_4k_f32()
+    gen = torch.Generator().manual_seed(wl.seed)
+    cache = torch.randn((1, 4096, 576), generator=gen, dtype=torch.float32)
+    raw = torch.randn((4096, 64), generator=gen, dtype=torch.float64).numpy()
+    plane = oracle_plane(wl.planes[0])
+    f = plane.frequencies()
+    cache[0, :, 512:] = torch.from_numpy(O.encode(O.rope(raw, np.arange(4096), f, O.INTERLEAVED), O.F32))
+    stub = torch.randn((1, 16, 576), generator=gen, dtype=torch.float32)
+    stub_raw = torch.randn((16, 64), generator=gen, dtype=torch.float64).numpy()
+    stub[0, :, 512:] = torch.from_numpy(O.encode(O.rope(stub_raw, np.arange(1024, 1040), f, O.INTERLEAVED), O.F32))
+    planes_dev = [cache.to(DEV)]
+    stubs_dev = [[stub.to(DEV)]]
+    n_new = _run_and_check(L, wl, planes_dev, stubs_dev, "mla_1l_4k_f32")
+    assert n_new == 4096 - 496
+    got = host(planes_dev[0])[0]
+    fresh = O.rope(raw[1536:], np.arange(1536, 4096) - 496, f, O.INTERLEAVED)
+    err = np.abs(got[1040:n_new, 512:].astype(np.float64) - fresh)
+    assert err.max() < 2e-5, err.max()
+    assert np.array_equal(got[1024:1040], host(stub)[0])
+
+
+@pytest.mark.parametrize("kind,dtype", [("mla", "bf16"), ("mla", "f32"), ("gqa", "bf16"),
+                                        ("gqa", "f32"), ("mla_neox", "bf16"), ("heads", "bf16")])
+def test_small_random_splices(L, kind, dtype):
+    rng = random.Random(zlib.crc32(f"{kind}/{dtype}".encode()))
+    cases = []
+    for n in (1, 7, 64, 257, 600):
+        for k in (1, 2, 3):
+            cases.append((n, _random_dirs(rng, n, k)))
+    # edge cases: delete at the very end, insert at 0, |Delta| = 1 both signs, Delta = 0,
+    # empty stub, span bigger than the downstream, growth into spare capacity
+    cases += [
+        (300, [W.Dir(250, 300, 0)]),
+        (300, [W.Dir(0, 0, 5)]),
+        (300, [W.Dir(10, 11, 0)]),
+        (300, [W.Dir(10, 10, 1)]),
+        (300, [W.Dir(10, 20, 10)]),
+        (300, [W.Dir(0, 280, 3)]),
+        (300, [W.Dir(5, 6, 200)]),
+        (300, [W.Dir(3, 9, 1), W.Dir(9, 9, 4), W.Dir(100, 180, 120), W.Dir(200, 290, 0)]),
+        (0, [W.Dir(0, 0, 3)]),
+    ]
+    for ci, (n, dirs) in enumerate(cases):
+        wl = _small_workload(rng, kind, dtype, 3, n, dirs, extra=rng.randint(0, 9))
+        planes_dev, stubs_dev = W.alloc_contig(wl, DEV, seed=1000 + ci)
+        _run_and_check(L, wl, planes_dev, stubs_dev, f"{kind}/{dtype} case {ci} n={n} dirs={dirs}")
+
+
+def test_mla_dsv3_32k_full(L):
+    wl = W.mla_dsv3_32k()
+    planes_dev, stubs_dev = W.alloc_contig(wl, DEV)
+    n_new = _run_and_check(L, wl, planes_dev, stubs_dev, "mla_dsv3_32k")
+    assert n_new == 32768 - 4064
+
+
+def test_gqa_llama3_8b_16k_full(L):
+    wl = W.gqa_llama3_8b_16k()
+    planes_dev, stubs_dev = W.alloc_contig(wl, DEV)
+    n_new = _run_and_check(L, wl, planes_dev, stubs_dev, "gqa_llama3_8b_16k")
+    assert n_new == 16384 - 2024
+
+
+@pytest.mark.parametrize("paged", [False, True])
+@pytest.mark.parametrize("kind,dtype", [("mla", "bf16"), ("gqa", "f32"), ("heads", "bf16")])
+def test_rotate_delta(L, kind, dtype, paged):
+    rng = random.Random(7)
+    wl = _small_workload(rng, kind, dtype, 2, 512, [])
+    print(f"[case] rotate {kind}/{dtype} paged={paged}", flush=True)
+    planes_dev, _ = W.alloc_contig(wl, DEV, seed=3)
+    if paged:   # view [L, 512 rows] as [L, 32 pages, 16 rows]
+        planes_dev = [t.view((t.shape[0], 32, 16) + t.shape[2:]) for t in planes_dev]
+    before = [host(t) for t in planes_dev]
+    cache = L.make_cache(_specs(L, wl, planes_dev), paged=paged)
+    rows = np.array(sorted(rng.sample(range(512), 77)), dtype=np.int64)
+    for delta, use_list in ((-4064, True), (131071, False), (1, True)):
+        if use_list:
+            L.leyline_rotate_delta(cache, delta, rows=torch.from_numpy(rows).to(DEV))
+            sel = rows
+        else:
+            L.leyline_rotate_delta(cache, delta, row0=100, n_rows=300)
+            sel = np.arange(100, 400)
+        torch.cuda.synchronize()
+        for pi, desc in enumerate(wl.planes):
+            plane = oracle_plane(desc)
+            b = before[pi].reshape(2, 512, -1)
+            g = host(planes_dev[pi]).reshape(2, 512, -1)
+            want = b.copy()
+            for layer in range(2):
+                want[layer, sel] = O.rotate_rows(b[layer, sel], delta, plane, dtype)
+            assert_rows_match(g, want, plane, dtype, inputs=b, what=f"rotate {delta}")
+            before[pi] = g.reshape(before[pi].shape)
+
+
+def test_rotate_delta_flags_bad_rows(L):
+    wl = _small_workload(random.Random(1), "mla", "bf16", 1, 64, [])
+    planes_dev, _ = W.alloc_contig(wl, DEV, seed=4)
+    before = host(planes_dev[0])
+    cache = L.make_cache(_specs(L, wl, planes_dev))
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    rows = torch.tensor([3, 64, -1, 5], dtype=torch.int64, device=DEV)
+    L.leyline_rotate_delta(cache, 10, rows=rows, device_status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == L.STATUS_BAD_ROW
+    after = host(planes_dev[0])
+    plane = oracle_plane(wl.planes[0])
+    want = before.copy()
+    want[0, [3, 5]] = O.rotate_rows(before[0, [3, 5]], 10, plane, "bf16")
+    assert_rows_match(after, want, plane, "bf16")

@@ -1,0 +1,199 @@
+"""GPU parity of the paged splice (through the C ABI) against the CPU oracle: whole pools on
+small ragged cases, and block tables, freed lists and sampled rows at the full batched and
+multi-directive sizes."""
+
+import random
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import splice_oracle as O
+from tests.parity_util import assert_rows_match, host, oracle_plane
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2606_01065_amd import leyline
+    return leyline
+
+
+def _run_gpu(L, wl, pools, bt, free, stubs):
+    specs = [L.PlaneSpec(t, p.n_heads, p.head_stride or p.row_elems, p.rot_offset, p.rot_dim,
+                         p.style, p.base) for p, t in zip(wl.planes, pools)]
+    cache = L.make_cache(specs, paged=True)
+    dirs = L.make_directives([dict(span_start=d.span_start, span_end=d.span_end, stub=stubs[j],
+                                   seq=d.seq, stub_len=d.stub_len) for j, d in enumerate(wl.dirs)])
+    new_lens, fresh, n_freed, ws_bytes = L.leyline_paged_query(cache, wl.seq_lens, bt.shape[1], dirs,
+                                                                len(wl.dirs))
+    bt_out = torch.full_like(bt, -7)
+    freed = torch.full((max(1, n_freed),), -7, dtype=torch.int32, device=DEV)
+    ws = torch.empty(max(256, ws_bytes), dtype=torch.uint8, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    got_lens, got_fresh, got_freed = L.leyline_splice_paged(cache, wl.seq_lens, bt, bt_out, dirs,
+                                                            len(wl.dirs), free, freed, ws,
+                                                            device_status=status)
+    torch.cuda.synchronize()
+    assert (got_lens, got_fresh, got_freed) == (new_lens, fresh, n_freed)
+    assert int(status.item()) == 0
+    return bt_out, freed[:n_freed], new_lens
+
+
+def _odirs(wl):
+    return [O.Directive(d.span_start, d.span_end, d.stub_len, seq=d.seq) for d in wl.dirs]
+
+
+def _random_workload(rng, page, kind, dtype):
+    n_seqs = rng.randint(1, 4)
+    lens, dirs = [], []
+    for b in range(n_seqs):
+        n = rng.randint(0, 5 * page + 3)
+        lens.append(n)
+        k = rng.randint(0, 3)
+        cuts = sorted(rng.sample(range(n + 1), min(2 * k, n + 1)))
+        for i in range(0, len(cuts) - 1, 2):
+            s, e = cuts[i], cuts[i + 1]
+            r = rng.choice([0, 1, e - s, rng.randint(0, 2 * (e - s) + 3), max(0, e - s - page),
+                            e - s + page])
+            dirs.append(W.Dir(s, e, r, seq=b))
+    planes = [W.mla_plane()] if kind == "mla" else W.gqa_planes(heads=2, dim=128)
+    return W.Workload(f"paged_{kind}", 2, dtype, planes, dirs, lens, page_size=page,
+                      seed=rng.randint(0, 10 ** 6))
+
+
+@pytest.mark.parametrize("kind,dtype", [("mla", "bf16"), ("gqa", "bf16"), ("mla", "f32")])
+def test_small_random_paged_whole_pool(L, kind, dtype):
+    rng = random.Random(97 if kind == "mla" else 98)
+    for page in (1, 4, 16, 64):
+        for ci in range(8):
+            wl = _random_workload(rng, page, kind, dtype)
+            print(f"[case] paged {kind}/{dtype} page={page} case={ci} lens={wl.seq_lens} dirs={wl.dirs}",
+                  flush=True)
+            pools, bt, free, stubs = W.alloc_paged(wl, DEV, spare_pages=3)
+            before = [host(p) for p in pools]
+            bt_h, free_h = host(bt), host(free)
+            stubs_h = [[host(s).reshape(wl.n_layers, s.shape[1], -1) for s in per] for per in stubs]
+            bt_out, freed, new_lens = _run_gpu(L, wl, pools, bt, free, stubs)
+            planes = [oracle_plane(p) for p in wl.planes]
+            flat = [b.reshape(b.shape[0], b.shape[1], b.shape[2], -1) for b in before]
+            want, want_bt, want_lens, want_freed = O.splice_paged(
+                flat, planes, dtype, bt_h, wl.seq_lens, _odirs(wl), stubs_h, list(free_h), page)
+            assert new_lens == want_lens
+            assert np.array_equal(host(bt_out), want_bt)
+            assert list(host(freed)) == want_freed
+            for pi, plane in enumerate(planes):
+                got = host(pools[pi]).reshape(want[pi].shape)
+                assert_rows_match(got, want[pi], plane, dtype, what=f"page={page} case={ci} plane={pi}")
+
+
+def _sample_positions(rng, wl, b, new_len, extra=24):
+    """New positions to check in sequence b: boundaries of every stub and segment, the ends,
+    page edges around them, and random positions."""
+    pts = {0, new_len - 1}
+    shift = 0
+    for d in (d for d in wl.dirs if d.seq == b):
+        a = d.span_start + shift
+        for q in (a - 1, a, a + d.stub_len - 1, a + d.stub_len, a + d.stub_len + 1):
+            pts.add(q)
+            pts.add((q // wl.page_size) * wl.page_size)
+            pts.add((q // wl.page_size) * wl.page_size + wl.page_size - 1)
+        shift += d.stub_len - (d.span_end - d.span_start)
+    pts.update(rng.randrange(max(1, new_len)) for _ in range(extra))
+    return sorted(q for q in pts if 0 <= q < new_len)
+
+
+def _check_sampled(L, wl, seed):
+    rng = random.Random(seed)
+    print(f"[case] {wl.name}: allocating and filling the pool", flush=True)
+    pools, bt, free, stubs = W.alloc_paged(wl, DEV)
+    P = wl.page_size
+    odirs = _odirs(wl)
+    bt_h, free_h = host(bt), host(free)
+    want_bt, want_lens, want_freed, plans = O.paged_tables(bt_h, wl.seq_lens, odirs, list(free_h), P)
+    # sampled outputs and their sources (old rows read before the call)
+    samples = []   # (seq, new position, kind, source index, shift)
+    for b, n in enumerate(wl.seq_lens):
+        mine = [d for d in odirs if d.seq == b]
+        src = O.row_sources(n, mine)
+        for q in _sample_positions(rng, wl, b, want_lens[b]):
+            s = src[q]
+            samples.append((b, q) + tuple(s))
+    pages_old = torch.tensor([bt_h[b, a // P] if kind == "old" else 0 for b, q, kind, a, c in samples],
+                             dtype=torch.long, device=DEV)
+    offs_old = torch.tensor([a % P if kind == "old" else 0 for b, q, kind, a, c in samples],
+                            dtype=torch.long, device=DEV)
+    before = [host(p[:, pages_old, offs_old]) for p in pools]          # [L, S, *row]
+    stubs_h = [[host(s) for s in per] for per in stubs]
+    dir_index = {}
+    for j, d in enumerate(wl.dirs):
+        dir_index.setdefault(d.seq, []).append(j)
+    print(f"[case] {wl.name}: splicing on the GPU", flush=True)
+    bt_out, freed, new_lens = _run_gpu(L, wl, pools, bt, free, stubs)
+    assert new_lens == want_lens
+    assert np.array_equal(host(bt_out), want_bt)
+    assert list(host(freed)) == want_freed
+    referenced = host(bt_out)[host(bt_out) >= 0]
+    assert len(np.unique(referenced)) == len(referenced)
+    bt_out_h = host(bt_out)
+    pages_new = torch.tensor([bt_out_h[x[0], x[1] // P] for x in samples], dtype=torch.long, device=DEV)
+    offs_new = torch.tensor([x[1] % P for x in samples], dtype=torch.long, device=DEV)
+    print(f"[case] {wl.name}: comparing {len(samples)} sampled rows x {wl.n_layers} layers", flush=True)
+    for pi, desc in enumerate(wl.planes):
+        plane = oracle_plane(desc)
+        got = host(pools[pi][:, pages_new, offs_new]).reshape(wl.n_layers, len(samples), -1)
+        old = before[pi].reshape(wl.n_layers, len(samples), -1)
+        want = np.empty_like(got)
+        for i, (b, q, kind, a, c) in enumerate(samples):
+            if kind == "old":
+                want[:, i] = O.rotate_rows(old[:, i], c, plane, wl.dtype)
+            else:
+                j = dir_index[b][a]
+                want[:, i] = stubs_h[j][pi].reshape(wl.n_layers, -1, plane.row_elems)[:, c]
+        assert_rows_match(got, want, plane, wl.dtype, what=f"{wl.name} plane {pi}")
+    return pools, bt, bt_out, new_lens, plans
+
+
+def test_mla_dsv3_paged_b64_full(L):
+    wl = W.mla_dsv3_paged_b64()
+    pools, bt, bt_out, new_lens, plans = _check_sampled(L, wl, seed=11)
+    kinds = [k for p in plans for k in p.kinds]
+    print(f"[info] pages: identity={kinds.count(O.IDENTITY)} remap={kinds.count(O.REMAP)} "
+          f"assemble={kinds.count(O.ASSEMBLE)}", flush=True)
+
+
+def test_mla_dsv3_paged_131k_full_and_sequential(L):
+    """Eight directives in one call; sampled rows against the one-call oracle, and whole
+    sequences of two layers against sequential application of the directives."""
+    wl = W.mla_dsv3_paged_131k()
+    P = wl.page_size
+    # snapshot two layers of the logical sequence before the call
+    layers = (0, wl.n_layers - 1)
+    pools, bt, free, stubs = W.alloc_paged(wl, DEV)
+    n = wl.seq_lens[0]
+    idx = torch.arange(n, device=DEV)
+    bt_row = bt[0].long()
+    pages, offs = bt_row[idx // P], idx % P
+    logical_before = {l: host(pools[0][l, pages, offs]) for l in layers}
+    stubs_h = [host(s[0]) for s in stubs]
+    bt_out, freed, new_lens = _run_gpu(L, wl, pools, bt, free, stubs)
+    n_new = new_lens[0]
+    idx = torch.arange(n_new, device=DEV)
+    bt_row = bt_out[0].long()
+    plane = oracle_plane(wl.planes[0])
+    odirs = [O.Directive(d.span_start, d.span_end, d.stub_len) for d in wl.dirs]
+    for l in layers:
+        print(f"[case] sequential reference, layer {l}", flush=True)
+        got = host(pools[0][l, bt_row[idx // P], idx % P])
+        cache = logical_before[l][None]
+        st = [s[l][None] for s in stubs_h]
+        want, nw = O.splice_sequential(cache, n, odirs, st, plane, wl.dtype)
+        assert nw == n_new
+        assert_rows_match(got, want[0, :n_new], plane, wl.dtype, what=f"sequential layer {l}")
+    del pools
+    torch.cuda.empty_cache()
+    _check_sampled(L, wl, seed=13)

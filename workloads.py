@@ -1,0 +1,224 @@
+"""Seeded synthetic inputs shaped like the paper's splice workloads.
+
+Shared by the tests, the benchmark and the smoke check.  This module only draws directive
+positions (integers) and fills tensors with seeded N(0,1) values; it performs none of the
+splice's or RoPE's arithmetic.  Keys that the workloads describe as "RoPE'd at their original
+position" are drawn directly from N(0,1): a rotation of an isotropic Gaussian pair is again an
+isotropic Gaussian pair, so the stored values have the described distribution.  Tests that need
+the exact construction (raw key, then RoPE at its position) build it themselves.
+
+Workloads (MLA rows: latent c_kv[512] + K_pe[64]; GQA rows: 8 KV heads x 128):
+  mla_1l_4k_f32       1 layer, 4096 tokens, fp32, delete [1024,1536), 16-token stub
+  mla_dsv3_32k        61 layers, 32768 tokens, bf16, 4096-token span at a seeded start in
+                      [2048,16384), 32-token stub, contiguous in place
+  mla_dsv3_paged_b64  61 layers, 64-token pages, 64 sequences of U[2048,32768] tokens, one
+                      directive each (start in the first half, span U[64,4096], stub U[0,64])
+  gqa_llama3_8b_16k   32 layers, K and V 8x128 bf16, theta 5e5 half-split, 16384 tokens,
+                      delete [4096,6144), 24-token stub
+  mla_dsv3_paged_131k 61 layers, 64-token pages, one 131072-token sequence, 8 non-overlapping
+                      directives (spans U[256,8192], stubs U[0,64])
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Tuple
+
+import numpy as np
+import torch
+
+MLA_LATENT, MLA_ROPE = 512, 64
+
+
+@dataclass
+class PlaneDesc:
+    row_shape: Tuple[int, ...]
+    n_heads: int = 1
+    head_stride: int = 0
+    rot_offset: int = 0
+    rot_dim: int = 0
+    style: int = 0                # 0 interleaved, 1 half-split (NEOX)
+    base: float = 10000.0
+
+    @property
+    def row_elems(self) -> int:
+        return int(np.prod(self.row_shape))
+
+
+@dataclass
+class Dir:
+    span_start: int
+    span_end: int
+    stub_len: int
+    seq: int = 0
+
+
+@dataclass
+class Workload:
+    name: str
+    n_layers: int
+    dtype: str                    # "bf16" | "f32"
+    planes: List[PlaneDesc]
+    dirs: List[Dir]
+    seq_lens: List[int]
+    page_size: int = 0            # 0: contiguous
+    capacity: int = 0             # contiguous rows per layer
+    seed: int = 0
+    notes: dict = field(default_factory=dict)
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.dtype == "bf16" else torch.float32
+
+
+def mla_plane(base=10000.0) -> PlaneDesc:
+    row = MLA_LATENT + MLA_ROPE
+    return PlaneDesc((row,), 1, row, MLA_LATENT, MLA_ROPE, 0, base)
+
+
+def gqa_planes(heads=8, dim=128, base=500000.0) -> List[PlaneDesc]:
+    return [PlaneDesc((heads, dim), heads, dim, 0, dim, 1, base), PlaneDesc((heads, dim))]
+
+
+def mla_1l_4k_f32() -> Workload:
+    return Workload("mla_1l_4k_f32", 1, "f32", [mla_plane()], [Dir(1024, 1536, 16)], [4096],
+                    capacity=4096, seed=1)
+
+
+def mla_dsv3_32k(seed: int = 2) -> Workload:
+    rng = np.random.default_rng(seed)
+    s = int(rng.integers(2048, 16384))
+    return Workload("mla_dsv3_32k", 61, "bf16", [mla_plane()], [Dir(s, s + 4096, 32)], [32768],
+                    capacity=32768, seed=seed)
+
+
+def gqa_llama3_8b_16k() -> Workload:
+    return Workload("gqa_llama3_8b_16k", 32, "bf16", gqa_planes(), [Dir(4096, 6144, 24)], [16384],
+                    capacity=16384, seed=4)
+
+
+def mla_dsv3_paged_b64(seed: int = 3, n_seqs: int = 64, n_layers: int = 61) -> Workload:
+    rng = np.random.default_rng(seed)
+    lens, dirs = [], []
+    for b in range(n_seqs):
+        n = int(rng.integers(2048, 32769))
+        s = int(rng.integers(0, n // 2))
+        ln = int(rng.integers(64, 4097))
+        r = int(rng.integers(0, 65))
+        lens.append(n)
+        dirs.append(Dir(s, min(n, s + ln), r, seq=b))
+    return Workload("mla_dsv3_paged_b64", n_layers, "bf16", [mla_plane()], dirs, lens,
+                    page_size=64, seed=seed)
+
+
+def mla_dsv3_paged_131k(seed: int = 5, n_layers: int = 61) -> Workload:
+    rng = np.random.default_rng(seed)
+    n = 131072
+    spans: List[Tuple[int, int]] = []
+    while len(spans) < 8:
+        ln = int(rng.integers(256, 8193))
+        s = int(rng.integers(0, n - ln + 1))
+        if all(s + ln <= a or s >= b for a, b in spans):
+            spans.append((s, s + ln))
+    spans.sort()
+    dirs = [Dir(a, b, int(rng.integers(0, 65))) for a, b in spans]
+    return Workload("mla_dsv3_paged_131k", n_layers, "bf16", [mla_plane()], dirs, [n],
+                    page_size=64, seed=seed)
+
+
+WORKLOADS = {
+    "mla_1l_4k_f32": mla_1l_4k_f32,
+    "mla_dsv3_32k": mla_dsv3_32k,
+    "mla_dsv3_paged_b64": mla_dsv3_paged_b64,
+    "gqa_llama3_8b_16k": gqa_llama3_8b_16k,
+    "mla_dsv3_paged_131k": mla_dsv3_paged_131k,
+}
+
+
+# --------------------------------------------------------------------------------- filling ---
+
+def fill_normal(t: torch.Tensor, seed: int, chunk_elems: int = 1 << 27) -> torch.Tensor:
+    """Fill t (any float dtype, any device) with seeded N(0,1) values, generated in fp32 chunks
+    along the flattened leading dims and rounded to t's dtype."""
+    flat = t.view(-1)
+    g = torch.Generator(device=t.device)
+    g.manual_seed(seed)
+    for lo in range(0, flat.numel(), chunk_elems):
+        hi = min(flat.numel(), lo + chunk_elems)
+        flat[lo:hi] = torch.randn(hi - lo, generator=g, device=t.device, dtype=torch.float32).to(t.dtype)
+    return t
+
+
+def alloc_contig(w: Workload, device, seed: int = None, fill: bool = True):
+    """Returns (plane tensors [L, capacity, *row], stubs[j][plane] = [L, r_j, *row])."""
+    seed = w.seed if seed is None else seed
+    planes = []
+    for i, p in enumerate(w.planes):
+        t = torch.empty((w.n_layers, w.capacity) + p.row_shape, dtype=w.torch_dtype, device=device)
+        if fill:
+            fill_normal(t, seed * 1000 + i)
+        planes.append(t)
+    stubs = []
+    for j, d in enumerate(w.dirs):
+        per = []
+        for i, p in enumerate(w.planes):
+            t = torch.empty((w.n_layers, d.stub_len) + p.row_shape, dtype=w.torch_dtype, device=device)
+            fill_normal(t, seed * 1000 + 100 + 10 * j + i)
+            per.append(t)
+        stubs.append(per)
+    return planes, stubs
+
+
+def fresh_page_bound(w: Workload) -> int:
+    """Upper bound on fresh pages a paged splice can consume: every new page from the page of
+    the sequence's first span start onwards."""
+    P = w.page_size
+    total = 0
+    for b, n in enumerate(w.seq_lens):
+        mine = [d for d in w.dirs if d.seq == b]
+        if not mine:
+            continue
+        n_new = n + sum(d.stub_len - (d.span_end - d.span_start) for d in mine)
+        total += -(-n_new // P) - mine[0].span_start // P
+    return total
+
+
+def alloc_paged(w: Workload, device, seed: int = None, fill: bool = True, spare_pages: int = 8):
+    """Pool tensors [L, n_pool, P, *row] per plane; block table int32 [n_seqs, bt_stride] with the
+    sequences' pages drawn from a seeded permutation of the pool; the rest is the free list.
+    Only pages referenced by a block table are filled."""
+    seed = w.seed if seed is None else seed
+    P = w.page_size
+    rng = np.random.default_rng(seed + 77)
+    old_pages = [-(-n // P) for n in w.seq_lens]
+    new_lens = []
+    for b, n in enumerate(w.seq_lens):
+        new_lens.append(n + sum(d.stub_len - (d.span_end - d.span_start) for d in w.dirs if d.seq == b))
+    bt_stride = max(max(old_pages), max(-(-n // P) for n in new_lens))
+    n_used = sum(old_pages)
+    n_pool = n_used + fresh_page_bound(w) + spare_pages
+    perm = rng.permutation(n_pool).astype(np.int32)
+    bt = np.full((len(w.seq_lens), bt_stride), -1, dtype=np.int32)
+    c = 0
+    for b, k in enumerate(old_pages):
+        bt[b, :k] = perm[c:c + k]
+        c += k
+    free = perm[c:].copy()
+    pools = []
+    for i, p in enumerate(w.planes):
+        t = torch.empty((w.n_layers, n_pool, P) + p.row_shape, dtype=w.torch_dtype, device=device)
+        if fill:
+            gen_seed = seed * 1000 + i
+            # fill layer by layer (keeps the fp32 staging small for very large pools)
+            for layer in range(w.n_layers):
+                fill_normal(t[layer], gen_seed * 100 + layer)
+        pools.append(t)
+    stubs = []
+    for j, d in enumerate(w.dirs):
+        per = []
+        for i, p in enumerate(w.planes):
+            t = torch.empty((w.n_layers, d.stub_len) + p.row_shape, dtype=w.torch_dtype, device=device)
+            fill_normal(t, seed * 1000 + 500 + 10 * j + i)
+            per.append(t)
+        stubs.append(per)
+    return pools, torch.from_numpy(bt).to(device), torch.from_numpy(free).to(device), stubs
