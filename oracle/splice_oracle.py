@@ -430,6 +430,27 @@ def gather_logical(pool: np.ndarray, layer: int, bt_row: np.ndarray, n: int, pag
     return pool[layer, bt_row[idx // page], idx % page]
 
 
+def paged_tables(block_table: np.ndarray, seq_lens: Sequence[int], dirs: Sequence[Directive],
+                 free_pages: Sequence[int], page: int):
+    """New block table (entries past a sequence's last page = -1), new lengths, the freed
+    physical pages, and the plans, from the page plan and the old block table."""
+    plans = plan_paged(seq_lens, dirs, page)
+    bt_out = np.full_like(block_table, -1)
+    freed: List[int] = []
+    for b, plan in enumerate(plans):
+        if pages_for(plan.new_len, page) > block_table.shape[1]:
+            raise DirectiveError("block table row too short for the new length")
+        for k, (kind, srcp) in enumerate(zip(plan.kinds, plan.sources)):
+            if kind == ASSEMBLE:
+                if srcp >= len(free_pages):
+                    raise DirectiveError("not enough free pages")
+                bt_out[b, k] = free_pages[srcp]
+            else:
+                bt_out[b, k] = block_table[b, srcp]
+        freed.extend(int(block_table[b, kp]) for kp in plan.freed)
+    return bt_out, [p.new_len for p in plans], freed, plans
+
+
 def splice_paged(pools: Sequence[np.ndarray], planes: Sequence[Plane], dtype: str,
                  block_table: np.ndarray, seq_lens: Sequence[int], dirs: Sequence[Directive],
                  stubs: Sequence[Sequence[np.ndarray]], free_pages: Sequence[int], page: int):
@@ -443,24 +464,11 @@ def splice_paged(pools: Sequence[np.ndarray], planes: Sequence[Plane], dtype: st
     Returns (new pools, new block table (unused entries = -1), new lengths, freed physical pages).
     Rows at or past the new length inside the last page of a sequence are unspecified.
     """
-    plans = plan_paged(seq_lens, dirs, page)
-    n_seqs, bt_stride = block_table.shape
-    bt_out = np.full_like(block_table, -1)
-    freed: List[int] = []
+    bt_out, new_lens, freed, plans = paged_tables(block_table, seq_lens, dirs, free_pages, page)
     out = [np.array(p, copy=True) for p in pools]
     for b, plan in enumerate(plans):
         my_dirs = [d for d in dirs if d.seq == b]
         my_stubs = [stubs[i] for i, d in enumerate(dirs) if d.seq == b]
-        if pages_for(plan.new_len, page) > bt_stride:
-            raise DirectiveError("block table row too short for the new length")
-        for k, (kind, srcp) in enumerate(zip(plan.kinds, plan.sources)):
-            if kind == ASSEMBLE:
-                if srcp >= len(free_pages):
-                    raise DirectiveError("not enough free pages")
-                bt_out[b, k] = free_pages[srcp]
-            else:
-                bt_out[b, k] = block_table[b, srcp]
-        freed.extend(int(block_table[b, kp]) for kp in plan.freed)
         for pi, plane in enumerate(planes):
             for layer in range(pools[pi].shape[0]):
                 old_rows = gather_logical(pools[pi], layer, block_table[b], plan.old_len, page)
@@ -471,4 +479,4 @@ def splice_paged(pools: Sequence[np.ndarray], planes: Sequence[Plane], dtype: st
                         continue
                     lo, hi = k * page, min((k + 1) * page, plan.new_len)
                     out[pi][layer, bt_out[b, k], :hi - lo] = new_rows[lo:hi]
-    return out, bt_out, [p.new_len for p in plans], freed
+    return out, bt_out, new_lens, freed
