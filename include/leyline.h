@@ -133,6 +133,10 @@ const char* leyline_strerror(int code);
 /* LEYLINE_ABI_VERSION of the loaded library. */
 int leyline_abi_version(void);
 
+/* The HIP runtime's description of the error behind the last LEYLINE_E_HIP returned on the
+ * calling thread ("no error" if there was none).  Static storage. */
+const char* leyline_last_hip_error(void);
+
 /*
  * Contiguous in-place splice of one sequence (all layers and planes).
  *

@@ -441,10 +441,19 @@ __global__ __launch_bounds__(TPB) void paged_tables_kernel(const KTableParams P)
 
 namespace {
 
-int hip_status(hipError_t e) { return e == hipSuccess ? LEYLINE_OK : LEYLINE_E_HIP; }
+thread_local hipError_t g_last_hip_error = hipSuccess;
 
+int hip_status(hipError_t e) {
+    if (e == hipSuccess) return LEYLINE_OK;
+    g_last_hip_error = e;
+    return LEYLINE_E_HIP;
+}
+
+// Launch and report the launch's own status: an error left behind by an earlier, unrelated
+// runtime call on this thread is cleared first so it is not blamed on this launch.
 template <typename K, typename A>
 int launch(K kernel, dim3 grid, hipStream_t stream, const A& args) {
+    (void)hipGetLastError();
     hipLaunchKernelGGL(kernel, grid, dim3(TPB), 0, stream, args);
     return hip_status(hipGetLastError());
 }
@@ -454,6 +463,10 @@ int launch(K kernel, dim3 grid, hipStream_t stream, const A& args) {
 }  // namespace leyline
 
 using namespace leyline;
+
+extern "C" const char* leyline_last_hip_error(void) {
+    return hipGetErrorString(g_last_hip_error);
+}
 
 extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len,
                                      const leyline_directive* dirs, int32_t n_dirs,

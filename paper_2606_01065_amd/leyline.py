@@ -67,17 +67,36 @@ class leyline_directive(Structure):
 class LeylineError(RuntimeError):
     def __init__(self, code: int, where: str):
         self.code = code
-        super().__init__(f"{where}: {strerror(code)} ({code})")
+        detail = f": {_lib.leyline_last_hip_error().decode()}" if code == E_HIP else ""
+        super().__init__(f"{where}: {strerror(code)} ({code}){detail}")
+
+
+def _hip_runtimes_mapped():
+    try:
+        with open("/proc/self/maps") as f:
+            return sorted({ln.split()[-1] for ln in f if "libamdhip64" in ln})
+    except OSError:
+        return []
 
 
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_01065_amd.build`")
+    # torch ships its own HIP runtime.  It must be loaded before the library so that the
+    # library's HIP dependency resolves to that same copy: two HIP/HSA runtimes in one process
+    # cannot both open the GPU.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
+    runtimes = _hip_runtimes_mapped()
+    if len(runtimes) > 1:
+        raise ImportError("more than one HIP runtime is loaded in this process "
+                          f"({', '.join(runtimes)}); import torch before anything that loads "
+                          "another libamdhip64")
     P = POINTER
     sig = {
         "leyline_strerror": (ctypes.c_char_p, [c_int]),
         "leyline_abi_version": (c_int, []),
+        "leyline_last_hip_error": (ctypes.c_char_p, []),
         "leyline_splice_contig": (c_int, [P(leyline_cache), c_int64, P(leyline_directive), c_int32,
                                           P(c_int64), c_void_p]),
         "leyline_paged_query": (c_int, [P(leyline_cache), c_int32, P(c_int32), c_int32,
@@ -103,7 +122,7 @@ def _load():
 _lib = _load()
 
 #: every symbol the header declares (checked by tests against the loaded library)
-SYMBOLS = ("leyline_strerror", "leyline_abi_version", "leyline_splice_contig", "leyline_paged_query",
+SYMBOLS = ("leyline_strerror", "leyline_abi_version", "leyline_last_hip_error", "leyline_splice_contig", "leyline_paged_query",
            "leyline_paged_plan", "leyline_splice_paged", "leyline_rotate_delta")
 
 

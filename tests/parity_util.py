@@ -3,10 +3,14 @@ built from workload descriptions, and the tolerance checks.
 
 Tolerances (the bar of the splice's parity tests):
 * every non-rotary element and every index/table: bit-exact;
-* rotary elements stored in bf16: |gpu - oracle| <= 1 bf16 ulp of the oracle value (the GPU
-  rounds an fp32 result once, the oracle rounds the fp64 value once);
-* rotary elements stored in fp32: per rotary pair, ||gpu - oracle|| <= 2e-6 * ||input pair||
-  (rotations preserve the pair norm, so this is the relative error of the fp32 compute).
+* rotary elements, fp32 storage: per rotary pair, ||gpu - oracle|| <= 2e-6 * ||input pair||
+  (rotations preserve the pair norm, so this is the relative error of the fp32 compute);
+* rotary elements, bf16 storage: per element, |gpu - oracle| <= max(1 bf16 ulp of the oracle
+  value, 2e-6 * ||pair||).  The rotation is computed in fp32 and rounded once; the oracle is
+  exact and rounded once.  When a pair's rotated component nearly cancels (e.g. (0.32, -1.98)
+  turning into (-2.0, 1.4e-6)), the fp32 compute error (about 1e-7 of the pair norm) exceeds the
+  bf16 spacing of that tiny component, so the 2e-6-of-fp32-compute arm applies; everywhere else
+  the 1-ulp arm does.  The fraction of bf16 elements that are bit-identical is reported too.
 """
 
 import numpy as np
@@ -15,6 +19,20 @@ import torch
 from oracle import splice_oracle as O
 
 F32_PAIR_RTOL = 2e-6
+LAST_BF16_EXACT_FRACTION = None
+
+
+def pair_norms(vals: np.ndarray, plane: O.Plane, rot: np.ndarray) -> np.ndarray:
+    """For every rotary element (in the compressed rotary selection), the norm of its pair."""
+    out = np.empty_like(vals)
+    sel_all = np.flatnonzero(rot)
+    ia, ib = O.pair_dims(plane.rot_dim, plane.style)
+    for cols in plane.rotary_columns():
+        sel = np.searchsorted(sel_all, cols)
+        nrm = np.hypot(vals[..., sel[ia]], vals[..., sel[ib]])
+        out[..., sel[ia]] = nrm
+        out[..., sel[ib]] = nrm
+    return out
 
 
 def host(t: torch.Tensor) -> np.ndarray:
@@ -60,15 +78,18 @@ def assert_rows_match(got: np.ndarray, want: np.ndarray, plane: O.Plane, dtype: 
         return
     g = O.decode(got[..., rot], dtype)
     w = O.decode(want[..., rot], dtype)
+    src = w if inputs is None else O.decode(inputs[..., rot], dtype)
+    norms = pair_norms(src, plane, rot)
     if dtype == O.BF16:
         err = np.abs(g - w)
-        tol = O.ulp(w, O.BF16)
+        tol = np.maximum(O.ulp(w, O.BF16), F32_PAIR_RTOL * norms)
         if not np.all(err <= tol):
             bad = np.argwhere(err > tol)
-            raise AssertionError(f"{what}: bf16 rotary error beyond 1 ulp at {bad[:5].tolist()} "
-                                 f"({len(bad)} total, max err {err.max():.3g})")
+            raise AssertionError(f"{what}: bf16 rotary error beyond max(1 ulp, 2e-6 |pair|) at "
+                                 f"{bad[:5].tolist()} ({len(bad)} total, max err {err.max():.3g})")
+        global LAST_BF16_EXACT_FRACTION
+        LAST_BF16_EXACT_FRACTION = float(np.mean(got[..., rot] == want[..., rot]))
         return
-    src = w if inputs is None else O.decode(inputs[..., rot], dtype)
     for cols in plane.rotary_columns():
         # positions of this head's band inside the compressed rotary selection
         sel = np.searchsorted(np.flatnonzero(rot), cols)

@@ -10,6 +10,7 @@ import torch
 
 import workloads as W
 from oracle import splice_oracle as O
+from tests import parity_util as PU
 from tests.parity_util import assert_rows_match, host, oracle_plane
 
 pytestmark = pytest.mark.gpu
@@ -47,9 +48,9 @@ def _run_and_check(L, wl, planes_dev, stubs_dev, label):
     assert new_len == O.new_length(n, odirs)
     for pi, (desc, t) in enumerate(zip(wl.planes, planes_dev)):
         plane = oracle_plane(desc)
-        got = host(t).reshape(wl.n_layers, wl.capacity, -1)
-        src = before[pi].reshape(wl.n_layers, wl.capacity, -1)
-        stubs = [s[pi].reshape(wl.n_layers, s[pi].shape[1], -1) for s in stubs_h]
+        got = host(t).reshape(wl.n_layers, wl.capacity, plane.row_elems)
+        src = before[pi].reshape(wl.n_layers, wl.capacity, plane.row_elems)
+        stubs = [s[pi].reshape(wl.n_layers, s[pi].shape[1], plane.row_elems) for s in stubs_h]
         want, _ = O.splice_contig(src, n, odirs, stubs, plane, wl.dtype)
         assert_rows_match(got[:, :new_len], want[:, :new_len], plane, wl.dtype,
                           inputs=_inputs_for_new_rows(src, n, odirs, stubs),
@@ -149,6 +150,7 @@ def test_mla_dsv3_32k_full(L):
     planes_dev, stubs_dev = W.alloc_contig(wl, DEV)
     n_new = _run_and_check(L, wl, planes_dev, stubs_dev, "mla_dsv3_32k")
     assert n_new == 32768 - 4064
+    print(f"[info] bf16 rotary elements bit-identical to the oracle: {PU.LAST_BF16_EXACT_FRACTION:.6f}")
 
 
 def test_gqa_llama3_8b_16k_full(L):
@@ -156,6 +158,7 @@ def test_gqa_llama3_8b_16k_full(L):
     planes_dev, stubs_dev = W.alloc_contig(wl, DEV)
     n_new = _run_and_check(L, wl, planes_dev, stubs_dev, "gqa_llama3_8b_16k")
     assert n_new == 16384 - 2024
+    print(f"[info] bf16 rotary elements bit-identical to the oracle: {PU.LAST_BF16_EXACT_FRACTION:.6f}")
 
 
 @pytest.mark.parametrize("paged", [False, True])

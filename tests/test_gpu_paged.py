@@ -77,7 +77,8 @@ def test_small_random_paged_whole_pool(L, kind, dtype):
             pools, bt, free, stubs = W.alloc_paged(wl, DEV, spare_pages=3)
             before = [host(p) for p in pools]
             bt_h, free_h = host(bt), host(free)
-            stubs_h = [[host(s).reshape(wl.n_layers, s.shape[1], -1) for s in per] for per in stubs]
+            stubs_h = [[host(s).reshape(wl.n_layers, s.shape[1], p.row_elems) for s, p in zip(per, wl.planes)]
+                       for per in stubs]
             bt_out, freed, new_lens = _run_gpu(L, wl, pools, bt, free, stubs)
             planes = [oracle_plane(p) for p in wl.planes]
             flat = [b.reshape(b.shape[0], b.shape[1], b.shape[2], -1) for b in before]
