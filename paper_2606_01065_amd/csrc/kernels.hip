@@ -3,18 +3,26 @@
 //
 // The path is bandwidth-bound element movement with a little fp32 arithmetic on the rotary
 // band (about 0.1-0.4 flop per byte), so there is no matrix-core work here: rows are moved as
-// 16-byte vectors by 64-wide wavefronts, each wave touching whole 128-byte lines, and the
-// re-anchoring rotation (Eq. "rotate": each pair (a, b) becomes (a c - b s, a s + b c)) is
-// applied in registers between the load and the store of a moved row.  cos/sin of
-// (shift * theta_i) come from the host, evaluated in fp64 once per call and shift, and live in
-// registers for the whole of a thread's work.
+// 16-byte vectors, and the re-anchoring rotation (Eq. "rotate": each pair (a, b) becomes
+// (a c - b s, a s + b c)) is applied in registers between the load and the store of a moved
+// row, with the result rounded to bf16 by the hardware's round-to-nearest-even conversion.
+// cos/sin of (shift * theta_i) come from the host, evaluated in fp64 once per call and shift,
+// and are staged once per workgroup in LDS.
+//
+// Access shape.  One thread moves one 16-byte chunk, and the chunks of the moved rows are laid
+// end to end over the threads, so every load and store instruction of a 64-wide wavefront
+// covers 1 KiB of consecutive bytes of whole rows; that is the shape that streams at the copy
+// ceiling of the chip.  For a half-split (NEOX) band the partner half of a chunk lives in
+// another lane of the same wavefront and is exchanged with a lane shuffle instead of being
+// loaded twice.  Index arithmetic uses precomputed multiply-shift division.
 //
 // In-place contiguous compaction.  A segment moved left by m rows writes row x with the old
-// content of row x + m.  Rows are split into m "chains": chain c owns rows c, c+m, c+2m, ...
-// of the segment, and one thread walks its chain in ascending order (descending for a right
-// shift), so every row it overwrites is one it has already read itself; different chains and
-// different 16-byte columns never touch the same bytes.  Loads of up to WIN consecutive chain
-// steps are issued together before their stores, which keeps enough bytes in flight per thread.
+// content of row x + m.  The host splits the segment into equal rounds of at most m rows taken
+// in ascending order (descending for a right shift): inside a round sources and destinations
+// are disjoint, and every row a round overwrites was read by an earlier round, so consecutive
+// launches on one stream order the whole move.  Shifts so small that this would need many
+// rounds use ordered chains instead: chain c owns rows c, c+m, c+2m, ... and one thread walks it
+// in order, overwriting only rows it has already read itself.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -27,26 +35,54 @@
 
 namespace leyline {
 
-constexpr int TPB = 256;
-constexpr int WIN = 8;
+// Launch shape and streaming hints (compile-time constants; the defaults are the tuned ones).
+#ifndef LEYLINE_TPB
+#define LEYLINE_TPB 512
+#endif
+#ifndef LEYLINE_WIN
+#define LEYLINE_WIN 8
+#endif
+#ifndef LEYLINE_NT_LOAD
+#define LEYLINE_NT_LOAD 1
+#endif
+#ifndef LEYLINE_NT_STORE
+#define LEYLINE_NT_STORE 1
+#endif
+
+constexpr int TPB = LEYLINE_TPB;
+constexpr int WIN = LEYLINE_WIN;
 constexpr int MAX_PAGE = 256;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-__device__ __forceinline__ u32x4 ld16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
-__device__ __forceinline__ void st16(char* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+// 16-byte vector accesses.  Moved rows are touched exactly once per call, so the streaming
+// (nontemporal) forms keep them from displacing other data in the caches.
+__device__ __forceinline__ u32x4 ld16(const char* p) {
+#if LEYLINE_NT_LOAD
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+#else
+    return *reinterpret_cast<const u32x4*>(p);
+#endif
+}
+__device__ __forceinline__ void st16(char* p, u32x4 v) {
+#if LEYLINE_NT_STORE
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+#else
+    *reinterpret_cast<u32x4*>(p) = v;
+#endif
+}
 
 // ----------------------------------------------------------------------- element helpers ---
 
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// fp32 -> bf16, round to nearest, ties to even (NaN stays a quiet NaN).
-__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
+// Two fp32 values -> two bf16 in one word (low half = a), round to nearest even.
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+    const bf16x2 v = __builtin_convertvector(f32x2{a, b}, bf16x2);
+    return __builtin_bit_cast(uint32_t, v);
 }
 
 __device__ __forceinline__ void rot_pair(float& a, float& b, float c, float s) {
@@ -56,56 +92,66 @@ __device__ __forceinline__ void rot_pair(float& a, float& b, float c, float s) {
     b = b2;
 }
 
-// Elements per 16-byte chunk for an element size.
-template <int ESZ> struct Elt { static constexpr int EPC = 16 / ESZ; };
+template <int ESZ> struct Elt { static constexpr int EPC = 16 / ESZ; };   // elements per chunk
 
-// Rotate one interleaved chunk: EPC/2 pairs (2i, 2i+1).
-template <int ESZ> __device__ __forceinline__ void rot_interleaved(u32x4& v, const float* c, const float* s);
-template <> __device__ __forceinline__ void rot_interleaved<2>(u32x4& v, const float* c, const float* s) {
+// Interleaved chunk: EPC/2 pairs (2i, 2i+1), cos/sin from table[cs + i].
+template <int ESZ> __device__ __forceinline__ void rot_interleaved(u32x4& v, const KCosSin* t, int32_t cs);
+template <> __device__ __forceinline__ void rot_interleaved<2>(u32x4& v, const KCosSin* t, int32_t cs) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
+        const KCosSin k = t[cs + i];
         float a = bf_lo(v[i]), b = bf_hi(v[i]);
-        rot_pair(a, b, c[i], s[i]);
-        v[i] = f32_to_bf16(a) | (f32_to_bf16(b) << 16);
+        rot_pair(a, b, k.c, k.s);
+        v[i] = pack_bf16(a, b);
     }
 }
-template <> __device__ __forceinline__ void rot_interleaved<4>(u32x4& v, const float* c, const float* s) {
+template <> __device__ __forceinline__ void rot_interleaved<4>(u32x4& v, const KCosSin* t, int32_t cs) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
+        const KCosSin k = t[cs + i];
         float a = __uint_as_float(v[2 * i]), b = __uint_as_float(v[2 * i + 1]);
-        rot_pair(a, b, c[i], s[i]);
+        rot_pair(a, b, k.c, k.s);
         v[2 * i] = __float_as_uint(a);
         v[2 * i + 1] = __float_as_uint(b);
     }
 }
 
-// Rotate a half-split (NEOX) chunk pair: element e of the low-half chunk with element e of the
-// high-half chunk, EPC pairs.
-template <int ESZ> __device__ __forceinline__ void rot_neox(u32x4& va, u32x4& vb, const float* c, const float* s);
-template <> __device__ __forceinline__ void rot_neox<2>(u32x4& va, u32x4& vb, const float* c, const float* s) {
+// Half-split chunks: element e of the low-half chunk `x` pairs with element e of the high-half
+// chunk `y`; EPC pairs with cos/sin table[cs + e].  Both chunks are updated.
+template <int ESZ> __device__ __forceinline__ void rot_halves(u32x4& x, u32x4& y, const KCosSin* t, int32_t cs);
+template <> __device__ __forceinline__ void rot_halves<2>(u32x4& x, u32x4& y, const KCosSin* t, int32_t cs) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        float a0 = bf_lo(va[i]), a1 = bf_hi(va[i]);
-        float b0 = bf_lo(vb[i]), b1 = bf_hi(vb[i]);
-        rot_pair(a0, b0, c[2 * i], s[2 * i]);
-        rot_pair(a1, b1, c[2 * i + 1], s[2 * i + 1]);
-        va[i] = f32_to_bf16(a0) | (f32_to_bf16(a1) << 16);
-        vb[i] = f32_to_bf16(b0) | (f32_to_bf16(b1) << 16);
+        const KCosSin k0 = t[cs + 2 * i], k1 = t[cs + 2 * i + 1];
+        float a0 = bf_lo(x[i]), a1 = bf_hi(x[i]);
+        float b0 = bf_lo(y[i]), b1 = bf_hi(y[i]);
+        rot_pair(a0, b0, k0.c, k0.s);
+        rot_pair(a1, b1, k1.c, k1.s);
+        x[i] = pack_bf16(a0, a1);
+        y[i] = pack_bf16(b0, b1);
     }
 }
-template <> __device__ __forceinline__ void rot_neox<4>(u32x4& va, u32x4& vb, const float* c, const float* s) {
+template <> __device__ __forceinline__ void rot_halves<4>(u32x4& x, u32x4& y, const KCosSin* t, int32_t cs) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        float a = __uint_as_float(va[i]), b = __uint_as_float(vb[i]);
-        rot_pair(a, b, c[i], s[i]);
-        va[i] = __float_as_uint(a);
-        vb[i] = __float_as_uint(b);
+        const KCosSin k = t[cs + i];
+        float a = __uint_as_float(x[i]), b = __uint_as_float(y[i]);
+        rot_pair(a, b, k.c, k.s);
+        x[i] = __float_as_uint(a);
+        y[i] = __float_as_uint(b);
     }
 }
 
-// A work unit of a row: chunk a, partner chunk b (-1 if none), first rotary pair, kind.
+// ------------------------------------------------------------------------- row geometry ---
+
+__device__ __forceinline__ int32_t fdiv(int32_t n, KDiv d) {
+    return int32_t((__umulhi(uint32_t(n), d.mul) + uint32_t(n)) >> d.shift);
+}
+
+// Two-chunk units over all chunks of a row (half-split planes without lane exchange, and the
+// ordered-chain kernel): unit u is a chunk, or a low-half chunk together with its partner.
 struct Unit {
-    int32_t a, b, pair, kind;   // kind: KROT_NONE / KROT_INTERLEAVED / KROT_NEOX
+    int32_t a, b, pair, kind;
 };
 
 template <int ESZ>
@@ -113,7 +159,7 @@ __device__ __forceinline__ Unit map_unit(const KPlane& p, int32_t u) {
     constexpr int EPC = Elt<ESZ>::EPC;
     Unit r{u, -1, 0, KROT_NONE};
     if (p.rot == KROT_INTERLEAVED) {
-        const int32_t h = u / p.head_chunks, j = u - h * p.head_chunks;
+        const int32_t h = fdiv(u, p.head_div), j = u - h * p.head_chunks;
         if (h < p.n_heads && j >= p.rot_lo && j < p.rot_lo + p.rot_chunks) {
             r.kind = KROT_INTERLEAVED;
             r.pair = (j - p.rot_lo) * (EPC / 2);
@@ -124,7 +170,7 @@ __device__ __forceinline__ Unit map_unit(const KPlane& p, int32_t u) {
         if (u >= head_units) {
             r.a = p.n_heads * p.head_chunks + (u - head_units);
         } else {
-            const int32_t h = u / uh, j = u - h * uh;
+            const int32_t h = fdiv(u, p.uhead_div), j = u - h * uh;
             r.a = h * p.head_chunks + (j < p.rot_lo + half ? j : j + half);
             if (j >= p.rot_lo && j < p.rot_lo + half) {
                 r.kind = KROT_NEOX;
@@ -136,90 +182,164 @@ __device__ __forceinline__ Unit map_unit(const KPlane& p, int32_t u) {
     return r;
 }
 
-// A rotary-only unit (the u-th rotary work unit of a row).
+// Row kernels: move unit u of one row from src to dst, re-anchored with the cos/sin block
+// table[cs + pair] (cs < 0: copied unchanged).  In lane-exchange mode the partner lanes of a
+// half-split band belong to the same row and take the same path.
 template <int ESZ>
-__device__ __forceinline__ Unit map_rot_unit(const KPlane& p, int32_t u) {
+__device__ __forceinline__ void move_row_unit(const KPlane& pl, const char* src, char* dst, int32_t u,
+                                              const KCosSin* table, int32_t cs) {
     constexpr int EPC = Elt<ESZ>::EPC;
-    Unit r{0, -1, 0, p.rot};
-    if (p.rot == KROT_INTERLEAVED) {
-        const int32_t h = u / p.rot_chunks, j = u - h * p.rot_chunks;
-        r.a = h * p.head_chunks + p.rot_lo + j;
-        r.pair = j * (EPC / 2);
-    } else {
-        const int32_t half = p.rot_chunks >> 1;
-        const int32_t h = u / half, j = u - h * half;
-        r.a = h * p.head_chunks + p.rot_lo + j;
-        r.b = r.a + half;
-        r.pair = j * EPC;
+    if (pl.rot == KROT_NEOX && !pl.neox_lanes) {
+        const Unit un = map_unit<ESZ>(pl, u);
+        const int64_t a = int64_t(un.a) * 16, b = int64_t(un.b) * 16;
+        u32x4 x = ld16(src + a), y;
+        if (un.b >= 0) y = ld16(src + b);
+        if (cs >= 0 && un.kind == KROT_NEOX) rot_halves<ESZ>(x, y, table, cs + un.pair);
+        st16(dst + a, x);
+        if (un.b >= 0) st16(dst + b, y);
+        return;
     }
-    return r;
-}
-
-template <int ESZ>
-__device__ __forceinline__ void load_cs(const KCosSin* table, const Unit& un, float* c, float* s) {
-    constexpr int EPC = Elt<ESZ>::EPC;
-    const int n = un.kind == KROT_NEOX ? EPC : EPC / 2;
+    const int64_t off = int64_t(u) * 16;
+    u32x4 v = ld16(src + off);
+    if (cs >= 0 && pl.rot != KROT_NONE) {
+        const int32_t h = fdiv(u, pl.head_div);
+        const int32_t j = u - h * pl.head_chunks - pl.rot_lo;
+        if (h < pl.n_heads && j >= 0 && j < pl.rot_chunks) {
+            if (pl.rot == KROT_INTERLEAVED) {
+                rot_interleaved<ESZ>(v, table, cs + j * (EPC / 2));
+            } else {
+                const int32_t half = pl.rot_chunks >> 1;
+                const bool lo = j < half;
+                const int lane = int(threadIdx.x & 63);
+                const int partner = lo ? lane + half : lane - half;
+                u32x4 o;
 #pragma unroll
-    for (int i = 0; i < EPC; ++i) {
-        if (i < n) {
-            const KCosSin v = table[un.pair + i];
-            c[i] = v.c;
-            s[i] = v.s;
-        } else {
-            c[i] = 1.0f;
-            s[i] = 0.0f;
+                for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[i]), partner, 64));
+                if (lo) rot_halves<ESZ>(v, o, table, cs + j * EPC);
+                else rot_halves<ESZ>(o, v, table, cs + (j - half) * EPC);
+            }
         }
     }
+    st16(dst + off, v);
 }
 
+// Rotary-only kernels: band index q of one row (bands of consecutive heads back to back).
 template <int ESZ>
-__device__ __forceinline__ void apply_rot(const Unit& un, u32x4& va, u32x4& vb, const float* c, const float* s) {
-    if (un.kind == KROT_INTERLEAVED) rot_interleaved<ESZ>(va, c, s);
-    else if (un.kind == KROT_NEOX) rot_neox<ESZ>(va, vb, c, s);
+__device__ __forceinline__ void move_band(const KPlane& pl, const char* src, char* dst, int32_t q,
+                                          const KCosSin* table, int32_t cs) {
+    constexpr int EPC = Elt<ESZ>::EPC;
+    const int32_t h = fdiv(q, pl.band_div);
+    const int32_t j = q - h * pl.band_tpr;
+    const int64_t a = (int64_t(h) * pl.head_chunks + pl.rot_lo + j) * 16;
+    if (pl.rot == KROT_NEOX && pl.band_tpr != pl.rot_chunks) {
+        const int64_t b = a + int64_t(pl.rot_chunks / 2) * 16;
+        u32x4 x = ld16(src + a), y = ld16(src + b);
+        rot_halves<ESZ>(x, y, table, cs + j * EPC);
+        st16(dst + a, x);
+        st16(dst + b, y);
+        return;
+    }
+    u32x4 v = ld16(src + a);
+    if (pl.rot == KROT_INTERLEAVED) {
+        rot_interleaved<ESZ>(v, table, cs + j * (EPC / 2));
+    } else {
+        const int32_t half = pl.rot_chunks >> 1;
+        const bool lo = j < half;
+        const int lane = int(threadIdx.x & 63);
+        const int partner = lo ? lane + half : lane - half;
+        u32x4 o;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[i]), partner, 64));
+        if (lo) rot_halves<ESZ>(v, o, table, cs + j * EPC);
+        else rot_halves<ESZ>(o, v, table, cs + (j - half) * EPC);
+    }
+    st16(dst + a, v);
 }
 
 // --------------------------------------------------------------------- contiguous splice ---
 
+// Rounds and replacement copies: rows laid end to end, one unit per thread; blockIdx.z selects
+// the (job, plane) item.  A thread's data load is issued before the workgroup stages its
+// cos/sin block in LDS, so the two memory latencies overlap.
 template <int ESZ>
-__global__ __launch_bounds__(TPB) void contig_splice_kernel(const KContigParams P) {
+__global__ __launch_bounds__(TPB) void contig_move_kernel(const KContigParams P) {
+    constexpr int EPC = Elt<ESZ>::EPC;
+    __shared__ KCosSin lcs[KMAX_CS];
+    const KItem& I = P.items[blockIdx.z];
+    const KPlane& pl = I.pl;
+    if (int64_t(blockIdx.x) * TPB >= I.count * pl.tpr) return;    // block past this item's rows
     const int layer = blockIdx.y;
-    const int bx = blockIdx.x;
-    int item = 0;
-    while (item < P.n_items - 1 && bx >= P.item_block_end[item]) ++item;
-    const int first = item ? P.item_block_end[item - 1] : 0;
-    const int pid = P.item_plane[item];
-    const KPlane& pl = P.planes[pid];
-    const KContigJob& J = P.jobs[P.item_job[item]];
-    const int32_t t = (bx - first) * TPB + int32_t(threadIdx.x);
-    const int32_t U = pl.units;
-    const int32_t c = t / U, u = t - c * U;
-    if (c >= J.chains) return;
-    const Unit un = map_unit<ESZ>(pl, u);
-    const int64_t oa = int64_t(un.a) * 16, ob = int64_t(un.b) * 16;
+    const int32_t t = int32_t(blockIdx.x) * TPB + int32_t(threadIdx.x);
+    const int32_t r = fdiv(t, pl.tpr_div), u = t - r * pl.tpr;
+    const bool active = r < I.count;
     char* lbase = pl.base + int64_t(layer) * pl.layer_stride;
-    const int64_t ts = pl.token_stride;
-
-    if (J.is_stub) {
-        const char* src = J.stub[pid] + (int64_t(layer) * J.count + c) * pl.row_bytes;
-        char* dst = lbase + (J.dst0 + c) * ts;
-        const u32x4 va = ld16(src + oa);
-        u32x4 vb;
-        if (un.b >= 0) vb = ld16(src + ob);
-        st16(dst + oa, va);
-        if (un.b >= 0) st16(dst + ob, vb);
+    const char* src;
+    char* dst;
+    if (I.kind == KJOB_STUB) {
+        src = I.stub + (int64_t(layer) * I.count + r) * pl.row_bytes;
+        dst = lbase + (I.dst0 + r) * pl.token_stride;
+    } else {
+        src = lbase + (I.src0 + r) * pl.token_stride;
+        dst = const_cast<char*>(src) + I.delta * pl.token_stride;
+    }
+    const bool rot = I.cs >= 0;                                    // block-uniform
+    if (!rot || (pl.rot == KROT_NEOX && !pl.neox_lanes)) {
+        // plain copies, and half-split two-chunk units (rare layouts): no early data load
+        if (rot) {
+            for (int i = threadIdx.x; i < pl.n_pairs; i += TPB) lcs[i] = P.cs[I.cs + i];
+            __syncthreads();
+        }
+        if (active) move_row_unit<ESZ>(pl, src, dst, u, lcs, rot ? 0 : -1);
         return;
     }
+    const int64_t off = int64_t(u) * 16;
+    u32x4 v;
+    if (active) v = ld16(src + off);
+    for (int i = threadIdx.x; i < pl.n_pairs; i += TPB) lcs[i] = P.cs[I.cs + i];
+    __syncthreads();
+    if (!active) return;
+    const int32_t h = fdiv(u, pl.head_div);
+    const int32_t j = u - h * pl.head_chunks - pl.rot_lo;
+    if (h < pl.n_heads && j >= 0 && j < pl.rot_chunks) {
+        if (pl.rot == KROT_INTERLEAVED) {
+            rot_interleaved<ESZ>(v, lcs, j * (EPC / 2));
+        } else {
+            const int32_t half = pl.rot_chunks >> 1;
+            const bool lo = j < half;
+            const int lane = int(threadIdx.x & 63);
+            const int partner = lo ? lane + half : lane - half;
+            u32x4 o;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[i]), partner, 64));
+            if (lo) rot_halves<ESZ>(v, o, lcs, j * EPC);
+            else rot_halves<ESZ>(o, v, lcs, (j - half) * EPC);
+        }
+    }
+    st16(dst + off, v);
+}
 
-    float cs_c[Elt<ESZ>::EPC], cs_s[Elt<ESZ>::EPC];
-    const bool rot = J.cs >= 0 && un.kind != KROT_NONE;
-    if (rot) load_cs<ESZ>(P.cs + J.cs + pl.cs_off, un, cs_c, cs_s);
+// Ordered chains (shifts too small for rounds): thread (chain c, unit u) walks rows c, c+m, ...
+template <int ESZ>
+__global__ __launch_bounds__(TPB) void contig_chain_kernel(const KContigParams P) {
+    const KItem& I = P.items[blockIdx.z];
+    const KPlane& pl = I.pl;
+    const int layer = blockIdx.y;
+    const int32_t t = int32_t(blockIdx.x) * TPB + int32_t(threadIdx.x);
+    char* lbase = pl.base + int64_t(layer) * pl.layer_stride;
+    const int64_t ts = pl.token_stride;
+    const int32_t U = pl.units_all;
+    const int32_t c = t / U, u = t - c * U;
+    if (c >= I.chains) return;
+    const Unit un = map_unit<ESZ>(pl, u);
+    const int64_t oa = int64_t(un.a) * 16, ob = int64_t(un.b) * 16;
+    const int32_t cs = (I.cs >= 0 && un.kind != KROT_NONE) ? I.cs + un.pair : -1;
 
-    const int64_t m = J.delta < 0 ? -J.delta : J.delta;
-    const int64_t steps = (J.count - c + m - 1) / m;
-    const char* src_c = lbase + (J.src0 + c) * ts;   // step k reads src_c + k*m*ts
+    const int64_t m = I.delta < 0 ? -I.delta : I.delta;
+    const int64_t steps = (I.count - c + m - 1) / m;
+    const char* src_c = lbase + (I.src0 + c) * ts;   // step k reads src_c + k*m*ts
     const int64_t step_bytes = m * ts;
-    const int64_t dshift = J.delta * ts;             // destination = source + dshift
-    const bool down = J.delta < 0;                   // left shift: ascending chain walk
+    const int64_t dshift = I.delta * ts;             // destination = source + dshift
+    const bool down = I.delta < 0;                   // left shift: ascending chain walk
 
     u32x4 va[WIN], vb[WIN];
     for (int64_t k0 = 0; k0 < steps; k0 += WIN) {
@@ -236,7 +356,10 @@ __global__ __launch_bounds__(TPB) void contig_splice_kernel(const KContigParams 
         for (int w = 0; w < WIN; ++w) {
             const int64_t k = down ? k0 + w : steps - 1 - (k0 + w);
             if (k0 + w < steps) {
-                if (rot) apply_rot<ESZ>(un, va[w], vb[w], cs_c, cs_s);
+                if (cs >= 0) {
+                    if (un.kind == KROT_INTERLEAVED) rot_interleaved<ESZ>(va[w], P.cs, cs);
+                    else rot_halves<ESZ>(va[w], vb[w], P.cs, cs);
+                }
                 char* d = const_cast<char*>(src_c) + k * step_bytes + dshift;
                 st16(d + oa, va[w]);
                 if (un.b >= 0) st16(d + ob, vb[w]);
@@ -253,40 +376,35 @@ __global__ __launch_bounds__(TPB) void rotate_rows_kernel(const KRotateParams P)
     const int64_t t = int64_t(blockIdx.x) * TPB + threadIdx.x;
     const int64_t i = t / P.units_per_row;
     if (i >= P.n_rows) return;
-    int32_t u = int32_t(t - i * P.units_per_row);
+    int32_t q = int32_t(t - i * P.units_per_row);
     int p = 0;
-    while (p < P.n_planes - 1 && u >= P.planes[p].rot_units) {
-        u -= P.planes[p].rot_units;
+    while (p < P.n_planes - 1 && q >= P.planes[p].rot_tpr) {
+        q -= P.planes[p].rot_tpr;
         ++p;
     }
     const KPlane& pl = P.planes[p];
     const int64_t row = P.rows ? P.rows[i] : P.row0 + i;
     if (row < 0 || row >= P.total_rows) {
-        if (P.status && u == 0 && p == 0) atomicOr(P.status, int(LEYLINE_STATUS_BAD_ROW));
+        if (P.status && q == 0 && p == 0) atomicOr(P.status, int(LEYLINE_STATUS_BAD_ROW));
         return;
     }
-    const Unit un = map_rot_unit<ESZ>(pl, u);
     char* r = pl.base + int64_t(layer) * pl.layer_stride;
     if (P.page_size > 0)
         r += (row / P.page_size) * pl.page_stride + (row % P.page_size) * pl.token_stride;
     else
         r += row * pl.token_stride;
-    float cs_c[Elt<ESZ>::EPC], cs_s[Elt<ESZ>::EPC];
-    load_cs<ESZ>(P.cs + pl.cs_off, un, cs_c, cs_s);
-    u32x4 va = ld16(r + int64_t(un.a) * 16), vb;
-    if (un.b >= 0) vb = ld16(r + int64_t(un.b) * 16);
-    apply_rot<ESZ>(un, va, vb, cs_c, cs_s);
-    st16(r + int64_t(un.a) * 16, va);
-    if (un.b >= 0) st16(r + int64_t(un.b) * 16, vb);
+    move_band<ESZ>(pl, r, r, q, P.cs, pl.cs_off);
 }
 
 // ------------------------------------------------------------------------------ paged splice ---
 //
-// One block per (page task, layer, plane).  ASSEMBLE tasks gather the rows of one new page
-// (prefix remainder, replacement tokens and shifted downstream rows, possibly from two old
-// pages) into a fresh page, rotating downstream rows on the way.  REMAP tasks rotate the
-// rotary bands of a re-used page in place.  Nothing is written to an old page except the
-// rotary bands of REMAP pages, which no ASSEMBLE task reads.
+// Blocks over (page task slice, layer, plane).  An ASSEMBLE task gathers the rows of one new
+// page (prefix remainder, replacement tokens and shifted downstream rows, possibly from two old
+// pages) into a fresh page, rotating downstream rows on the way; each of its blocks moves TPB
+// consecutive chunks of the page's rows, one per thread, after resolving the sources of the
+// rows it covers into LDS.  A REMAP task rotates the rotary bands
+// of a re-used page in place.  Nothing is written to an old page except the rotary bands of
+// REMAP pages, which no ASSEMBLE task reads.
 
 template <int ESZ>
 __global__ __launch_bounds__(TPB) void paged_splice_kernel(const KPagedParams P) {
@@ -297,13 +415,21 @@ __global__ __launch_bounds__(TPB) void paged_splice_kernel(const KPagedParams P)
     const int plane = blockIdx.z;
     const KPlane& pl = P.planes[plane];
     const int64_t lbase_off = int64_t(layer) * pl.layer_stride;
-    const int task = blockIdx.x;
+    const int bx = blockIdx.x;
+    const int n_asm_blocks = P.n_asm * P.asm_slices;
 
-    if (task < P.n_asm) {
+    if (bx < n_asm_blocks) {
+        const int task = bx / P.asm_slices;
+        const int32_t slice = bx - task * P.asm_slices;
         const KAssembleTask T = P.asm_tasks[task];
         const KSeqEntry S = P.seqs[T.seq];
         const int64_t lo = int64_t(T.k) * P.page_size;
-        const int valid = int(min(int64_t(P.page_size), int64_t(S.new_len) - lo));
+        const int32_t valid = int32_t(min(int64_t(P.page_size), int64_t(S.new_len) - lo));
+        const int32_t total = valid * pl.tpr;
+        const int32_t f0 = slice * TPB;
+        if (f0 >= total) return;                                  // whole block idle
+        const int32_t r0 = fdiv(f0, pl.tpr_div);
+        const int32_t r1 = min(valid, fdiv(min(total, f0 + TPB) - 1, pl.tpr_div) + 1);
         if (threadIdx.x == 0) {
             const int32_t fp = T.fresh < P.n_free ? P.free_pages[T.fresh] : -1;
             if (fp < 0 || fp >= P.capacity) {
@@ -313,7 +439,7 @@ __global__ __launch_bounds__(TPB) void paged_splice_kernel(const KPagedParams P)
                 page_dst = pl.base + lbase_off + int64_t(fp) * pl.page_stride;
             }
         }
-        for (int r = threadIdx.x; r < valid; r += TPB) {
+        for (int32_t r = r0 + int32_t(threadIdx.x); r < r1; r += TPB) {
             const int64_t q = lo + r;
             // last directive of the sequence whose replacement starts at or before q
             int32_t jlo = 0, jhi = S.dir_count;
@@ -343,80 +469,42 @@ __global__ __launch_bounds__(TPB) void paged_splice_kernel(const KPagedParams P)
                     src = pl.base + lbase_off + int64_t(pg) * pl.page_stride + (old % P.page_size) * pl.token_stride;
                 }
             }
-            row_src[r] = src;
-            row_cs[r] = cs;
+            row_src[r - r0] = src;
+            row_cs[r - r0] = cs;
         }
         __syncthreads();
         char* dst_page = page_dst;
-        if (!dst_page) return;
-        const int32_t U = pl.units;
-        const int32_t total = valid * U;
-        for (int32_t f0 = 0; f0 < total; f0 += TPB * WIN) {
-            u32x4 va[WIN], vb[WIN];
-            Unit un[WIN];
-            int32_t rr[WIN];
-#pragma unroll
-            for (int w = 0; w < WIN; ++w) {
-                const int32_t f = f0 + w * TPB + int32_t(threadIdx.x);
-                rr[w] = -1;
-                if (f < total) {
-                    const int32_t r = f / U;
-                    un[w] = map_unit<ESZ>(pl, f - r * U);
-                    const char* s = row_src[r];
-                    if (s) {
-                        rr[w] = r;
-                        va[w] = ld16(s + int64_t(un[w].a) * 16);
-                        if (un[w].b >= 0) vb[w] = ld16(s + int64_t(un[w].b) * 16);
-                    }
-                }
-            }
-#pragma unroll
-            for (int w = 0; w < WIN; ++w) {
-                const int32_t r = rr[w];
-                if (r >= 0) {
-                    const int32_t cs = row_cs[r];
-                    if (cs >= 0 && un[w].kind != KROT_NONE) {
-                        float c[Elt<ESZ>::EPC], s[Elt<ESZ>::EPC];
-                        load_cs<ESZ>(P.cs + cs + pl.cs_off, un[w], c, s);
-                        apply_rot<ESZ>(un[w], va[w], vb[w], c, s);
-                    }
-                    char* d = dst_page + int64_t(r) * pl.token_stride;
-                    st16(d + int64_t(un[w].a) * 16, va[w]);
-                    if (un[w].b >= 0) st16(d + int64_t(un[w].b) * 16, vb[w]);
-                }
-            }
-        }
+        const int32_t f = f0 + int32_t(threadIdx.x);
+        if (!dst_page || f >= total) return;
+        const int32_t r = fdiv(f, pl.tpr_div);
+        const char* src = row_src[r - r0];
+        if (!src) return;
+        const int32_t cs = row_cs[r - r0];
+        move_row_unit<ESZ>(pl, src, dst_page + int64_t(r) * pl.token_stride, f - r * pl.tpr, P.cs,
+                           cs >= 0 ? cs + pl.cs_off : -1);
         return;
     }
 
     // REMAP: rotate the rotary bands of a re-used page in place.
-    if (pl.rot_units == 0) return;
-    const KRemapTask T = P.remap_tasks[task - P.n_asm];
+    if (pl.rot_tpr == 0) return;
+    const int rb = bx - n_asm_blocks;
+    const int task = rb / P.remap_slices, slice = rb - task * P.remap_slices;
+    const KRemapTask T = P.remap_tasks[task];
     const KSeqEntry S = P.seqs[T.seq];
     const KDirEntry& D = P.dirs[T.dir];
     if (D.cs < 0) return;
     const int64_t lo = int64_t(T.k) * P.page_size;
-    const int valid = int(min(int64_t(P.page_size), int64_t(S.new_len) - lo));
+    const int32_t valid = int32_t(min(int64_t(P.page_size), int64_t(S.new_len) - lo));
+    const int32_t f = slice * TPB + int32_t(threadIdx.x);
+    if (f >= valid * pl.rot_tpr) return;
     const int32_t pg = P.bt_in[int64_t(T.seq) * P.bt_stride + T.src_page];
     if (pg < 0 || pg >= P.capacity) {
-        if (P.status && threadIdx.x == 0) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
+        if (P.status) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
         return;
     }
-    char* page = pl.base + lbase_off + int64_t(pg) * pl.page_stride;
-    const int32_t RU = pl.rot_units;
-    const int32_t total = valid * RU;
-    for (int32_t f = threadIdx.x; f < total; f += TPB) {
-        const int32_t r = f / RU;
-        const Unit un = map_rot_unit<ESZ>(pl, f - r * RU);
-        char* row = page + int64_t(r) * pl.token_stride;
-        float c[Elt<ESZ>::EPC], s[Elt<ESZ>::EPC];
-        load_cs<ESZ>(P.cs + D.cs + pl.cs_off, un, c, s);
-        u32x4 va = ld16(row + int64_t(un.a) * 16), vb;
-        if (un.b >= 0) vb = ld16(row + int64_t(un.b) * 16);
-        apply_rot<ESZ>(un, va, vb, c, s);
-        st16(row + int64_t(un.a) * 16, va);
-        if (un.b >= 0) st16(row + int64_t(un.b) * 16, vb);
-    }
+    const int32_t r = f / pl.rot_tpr;
+    char* row = pl.base + lbase_off + int64_t(pg) * pl.page_stride + int64_t(r) * pl.token_stride;
+    move_band<ESZ>(pl, row, row, f - r * pl.rot_tpr, P.cs, D.cs + pl.cs_off);
 }
 
 // New block tables and the freed-page list, resolved from the symbolic plan.
@@ -458,6 +546,8 @@ int launch(K kernel, dim3 grid, hipStream_t stream, const A& args) {
     return hip_status(hipGetLastError());
 }
 
+int64_t abs64(int64_t v) { return v < 0 ? -v : v; }
+
 }  // namespace
 
 }  // namespace leyline
@@ -478,52 +568,69 @@ extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len
     int n_planes = 0;
     rc = describe_cache(cache, false, planes, &n_planes);
     if (rc) return rc;
-    // every (job, plane) item's thread count must fit a 32-bit index
+    // threads of one (job, plane) item; every count must fit a 31-bit index
+    auto item_threads = [&](const ContigJobHost& j, int p) -> int64_t {
+        if (j.kind == KJOB_CHAIN) return std::min<int64_t>(j.count, abs64(j.delta)) * planes[p].units_all;
+        return j.count * planes[p].tpr;
+    };
     for (const auto& jobs : sched.launches)
         for (const auto& j : jobs)
-            for (int p = 0; p < n_planes; ++p) {
-                const int64_t rows = j.is_stub ? j.count : std::min<int64_t>(j.count, j.delta < 0 ? -j.delta : j.delta);
-                if (rows * planes[p].units > INT32_MAX - TPB) return LEYLINE_E_INVAL;
-            }
+            for (int p = 0; p < n_planes; ++p)
+                if (item_threads(j, p) > INT32_MAX - TPB) return LEYLINE_E_INVAL;
+    const int32_t cs_need = cos_sin_per_shift(cache);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    for (const auto& jobs : sched.launches) {
-        KContigParams P;
-        std::memset(&P, 0, sizeof(P));
-        std::memcpy(P.planes, planes, sizeof(planes));
-        P.n_layers = cache->n_layers;
-        std::vector<KCosSin> cs;
-        int32_t blocks = 0;
-        int n_items = 0;
-        for (size_t ji = 0; ji < jobs.size(); ++ji) {
-            const ContigJobHost& j = jobs[ji];
-            KContigJob& k = P.jobs[ji];
-            k.src0 = j.src0;
-            k.dst0 = j.dst0;
-            k.count = j.count;
-            k.delta = j.delta;
-            k.is_stub = j.is_stub ? 1 : 0;
-            k.chains = int32_t(j.is_stub ? j.count : std::min<int64_t>(j.count, j.delta < 0 ? -j.delta : j.delta));
-            k.cs = -1;
-            if (!j.is_stub && cos_sin_per_shift(cache) > 0) k.cs = append_cos_sin(cache, j.delta, cs);
-            if (j.is_stub)
-                for (int p = 0; p < n_planes; ++p) k.stub[p] = static_cast<const char*>(dirs[j.dir].stub[p]);
-            for (int p = 0; p < n_planes; ++p) {
-                const int64_t threads = int64_t(k.chains) * planes[p].units;
-                blocks += int32_t((threads + TPB - 1) / TPB);
-                P.item_job[n_items] = int32_t(ji);
-                P.item_plane[n_items] = p;
-                P.item_block_end[n_items] = blocks;
-                ++n_items;
+    for (const auto& group : sched.launches) {
+        // the jobs of a group are independent; replacement copies, chains and rounds go to
+        // separate launches, each a list of (job, plane) items selected by blockIdx.z
+        for (int kind : {int(KJOB_STUB), int(KJOB_CHAIN), int(KJOB_ROUND)}) {
+            KContigParams P;
+            std::vector<KCosSin> cs;
+            int64_t max_blocks = 0;
+            auto flush = [&]() -> int {
+                if (P.n_items == 0) return LEYLINE_OK;
+                if (cs.size() > size_t(KMAX_CS) || max_blocks > INT32_MAX) return LEYLINE_E_INVAL;
+                std::copy(cs.begin(), cs.end(), P.cs);
+                const dim3 grid(unsigned(max_blocks), unsigned(cache->n_layers), unsigned(P.n_items));
+                int r;
+                if (kind == KJOB_CHAIN)
+                    r = cache->dtype == LEYLINE_BF16 ? launch(contig_chain_kernel<2>, grid, s, P)
+                                                     : launch(contig_chain_kernel<4>, grid, s, P);
+                else
+                    r = cache->dtype == LEYLINE_BF16 ? launch(contig_move_kernel<2>, grid, s, P)
+                                                     : launch(contig_move_kernel<4>, grid, s, P);
+                P.n_items = 0;
+                cs.clear();
+                max_blocks = 0;
+                return r;
+            };
+            std::memset(&P, 0, sizeof(P));
+            for (const ContigJobHost& j : group) {
+                if (j.kind != kind) continue;
+                if (P.n_items + n_planes > KMAX_LAUNCH_ITEMS || int32_t(cs.size()) + cs_need > KMAX_CS) {
+                    rc = flush();
+                    if (rc) return rc;
+                }
+                const int32_t cs0 = (kind != KJOB_STUB && cs_need > 0) ? append_cos_sin(cache, j.delta, cs) : -1;
+                for (int p = 0; p < n_planes; ++p) {
+                    const int64_t th = item_threads(j, p);
+                    if (th == 0) continue;
+                    KItem& it = P.items[P.n_items++];
+                    std::memset(&it, 0, sizeof(it));
+                    it.pl = planes[p];
+                    it.src0 = j.src0;
+                    it.dst0 = j.dst0;
+                    it.count = j.count;
+                    it.delta = j.delta;
+                    it.kind = j.kind;
+                    it.chains = int32_t(kind == KJOB_CHAIN ? std::min<int64_t>(j.count, abs64(j.delta)) : 0);
+                    it.cs = (cs0 >= 0 && planes[p].rot != KROT_NONE) ? cs0 + planes[p].cs_off : -1;
+                    if (kind == KJOB_STUB) it.stub = static_cast<const char*>(dirs[j.dir].stub[p]);
+                    max_blocks = std::max(max_blocks, (th + TPB - 1) / TPB);
+                }
             }
+            rc = flush();
+            if (rc) return rc;
         }
-        P.n_items = n_items;
-        if (cs.size() > size_t(KMAX_CS)) return LEYLINE_E_INVAL;
-        std::copy(cs.begin(), cs.end(), P.cs);
-        if (blocks == 0) continue;
-        const dim3 grid(unsigned(blocks), unsigned(cache->n_layers));
-        rc = cache->dtype == LEYLINE_BF16 ? launch(contig_splice_kernel<2>, grid, s, P)
-                                          : launch(contig_splice_kernel<4>, grid, s, P);
-        if (rc) return rc;
     }
     if (new_len_out) *new_len_out = sched.new_len;
     return LEYLINE_OK;
@@ -543,8 +650,19 @@ extern "C" int leyline_rotate_delta(const leyline_cache* cache, int64_t delta,
     if (!rows && (row0 < 0 || row0 > total_rows || n_rows > total_rows - row0)) return LEYLINE_E_RANGE;
     KRotateParams P;
     std::memset(&P, 0, sizeof(P));
+    // The rotary bands of all planes are laid end to end per row.  With more than one rotary
+    // plane a band may start off its alignment, so half-split bands then use two-chunk units.
+    int n_rot = 0;
+    for (int p = 0; p < n_planes; ++p) n_rot += planes[p].rot_tpr > 0;
+    if (n_rot > 1)
+        for (int p = 0; p < n_planes; ++p)
+            if (planes[p].rot == KROT_NEOX && planes[p].band_tpr == planes[p].rot_chunks) {
+                planes[p].band_tpr = planes[p].rot_chunks / 2;
+                planes[p].rot_tpr = planes[p].n_heads * planes[p].band_tpr;
+                planes[p].band_div = make_div(planes[p].band_tpr);
+            }
     int32_t upr = 0;
-    for (int p = 0; p < n_planes; ++p) upr += planes[p].rot_units;
+    for (int p = 0; p < n_planes; ++p) upr += planes[p].rot_tpr;
     if (n_rows == 0 || upr == 0 || delta == 0) return LEYLINE_OK;   // R(0) is the identity
     std::memcpy(P.planes, planes, sizeof(planes));
     P.n_planes = n_planes;
@@ -614,6 +732,13 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         P.bt_stride = bt_stride;
         P.n_asm = t.n_asm;
         P.n_remap = t.n_remap;
+        int32_t asm_slices = 1, remap_slices = 1;
+        for (int p = 0; p < n_planes; ++p) {
+            asm_slices = std::max(asm_slices, (cache->page_size * planes[p].tpr + TPB - 1) / TPB);
+            remap_slices = std::max(remap_slices, (cache->page_size * planes[p].rot_tpr + TPB - 1) / TPB);
+        }
+        P.asm_slices = asm_slices;
+        P.remap_slices = remap_slices;
         P.capacity = cache->capacity;
         P.seqs = reinterpret_cast<const KSeqEntry*>(ws + t.off_seq);
         P.dirs = reinterpret_cast<const KDirEntry*>(ws + t.off_dir);
@@ -624,7 +749,9 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         P.free_pages = free_pages;
         P.n_free = n_free;
         P.status = device_status;
-        const dim3 grid(unsigned(t.n_asm + t.n_remap), unsigned(cache->n_layers), unsigned(n_planes));
+        const int64_t blocks = int64_t(t.n_asm) * asm_slices + int64_t(t.n_remap) * remap_slices;
+        if (blocks > INT32_MAX) return LEYLINE_E_INVAL;
+        const dim3 grid(unsigned(blocks), unsigned(cache->n_layers), unsigned(n_planes));
         rc = cache->dtype == LEYLINE_BF16 ? launch(paged_splice_kernel<2>, grid, s, P)
                                           : launch(paged_splice_kernel<4>, grid, s, P);
         if (rc) return rc;

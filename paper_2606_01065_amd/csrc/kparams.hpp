@@ -9,9 +9,17 @@
 
 namespace leyline {
 
-// Rows are moved as 16-byte vectors ("chunks").  A work unit is one chunk, or for half-split
-// (NEOX) rotary bands a chunk of the low half together with its partner chunk half a band away.
+// Rows are moved as 16-byte vectors ("chunks").  In the row kernels one thread moves one chunk
+// of a row, except for half-split (NEOX) bands whose halves cannot be exchanged between lanes of
+// a wavefront (neox_lanes == 0): there a thread moves a low-half chunk and its partner (a
+// "two-chunk unit").  Rotary-only kernels (rotate in place) map threads over the bands alone.
 enum : int32_t { KROT_NONE = 0, KROT_INTERLEAVED = 1, KROT_NEOX = 2 };
+
+// Division by a fixed divisor d: n / d == (umulhi(n, mul) + n) >> shift for 0 <= n < 2^31.
+struct KDiv {
+    uint32_t mul;
+    int32_t shift;
+};
 
 struct KPlane {
     char* base;              // device
@@ -20,14 +28,23 @@ struct KPlane {
     int64_t page_stride;     // bytes (paged caches)
     int32_t row_bytes;
     int32_t row_chunks;      // row_bytes / 16
-    int32_t units;           // work units per row (all chunks)
-    int32_t rot_units;       // work units per row that touch a rotary band
     int32_t rot;             // KROT_*
     int32_t n_heads;
     int32_t head_chunks;     // head stride in chunks
     int32_t rot_lo;          // first rotary chunk within a head
     int32_t rot_chunks;      // rotary band length in chunks (whole band, both halves)
     int32_t cs_off;          // offset of this plane's pairs within one shift's cos/sin block
+    int32_t n_pairs;         // rotary pairs per head (rot_dim / 2)
+    int32_t neox_lanes;      // 1: half-split partners are exchanged between lanes of a wavefront
+    int32_t stage_cs;        // 1: most chunks of a row rotate; stage cos/sin in LDS per workgroup
+    int32_t tpr;             // row kernels: threads per row (row_chunks, or two-chunk units)
+    int32_t units_all;       // two-chunk units per row (ordered-chain kernel)
+    KDiv tpr_div;            // division by tpr
+    KDiv head_div;           // division by head_chunks
+    KDiv uhead_div;          // division by head_chunks - rot_chunks/2 (two-chunk units per head)
+    int32_t band_tpr;        // rotary-only kernels: threads per band (rot_chunks, or half of it)
+    int32_t rot_tpr;         // rotary-only kernels: threads per row (n_heads * band_tpr)
+    KDiv band_div;           // division by band_tpr
 };
 
 struct KCosSin {
@@ -36,29 +53,39 @@ struct KCosSin {
 
 // ------------------------------------------------------------------------------ contiguous --
 constexpr int KMAX_JOBS = 6;
-constexpr int KMAX_ITEMS = KMAX_JOBS * LEYLINE_MAX_PLANES;
 constexpr int KMAX_CS = 192;
 
-struct KContigJob {
+
+
+// Kinds of contiguous jobs.
+enum : int32_t {
+    KJOB_ROUND = 0,   // rows [src0, src0+count) move by delta with count <= |delta|: sources and
+                      // destinations are disjoint, one chunk per thread
+    KJOB_CHAIN = 1,   // rows [src0, src0+count) move by delta, count > |delta|: ordered chains
+    KJOB_STUB = 2     // count replacement rows copied to [dst0, dst0+count)
+};
+
+// One (job, plane) item of a contiguous launch, self-contained so that a workgroup reads its
+// parameters with one level of independent scalar loads (blockIdx.z selects the item).
+struct KItem {
+    KPlane pl;
+    const char* stub;        // KJOB_STUB: dense [layers][count][row] for this plane
     int64_t src0;            // move: first source row
     int64_t dst0;            // stub: first destination row
     int64_t count;           // rows
-    int64_t delta;           // move: nonzero shift; stub: 0
-    int32_t chains;          // move: min(|delta|, count); stub: count
-    int32_t cs;              // move: first cos/sin entry of this shift (-1: no rotation)
-    int32_t is_stub;
+    int64_t delta;           // move: nonzero shift
+    int32_t kind;            // KJOB_*
+    int32_t chains;          // chain: min(|delta|, count)
+    int32_t cs;              // first cos/sin entry of this plane's pairs (-1: no rotation)
     int32_t pad;
-    const char* stub[LEYLINE_MAX_PLANES];   // stub: per plane, dense [layers][count][row]
 };
 
+constexpr int KMAX_LAUNCH_ITEMS = 8;
+
 struct KContigParams {
-    KPlane planes[LEYLINE_MAX_PLANES];
-    KContigJob jobs[KMAX_JOBS];
-    int32_t item_job[KMAX_ITEMS];
-    int32_t item_plane[KMAX_ITEMS];
-    int32_t item_block_end[KMAX_ITEMS];   // inclusive prefix sum of blocks per layer
+    KItem items[KMAX_LAUNCH_ITEMS];
     int32_t n_items;
-    int32_t n_layers;
+    int32_t pad;
     KCosSin cs[KMAX_CS];
 };
 
@@ -74,7 +101,7 @@ struct KRotateParams {
     int64_t row0;
     int64_t n_rows;
     int32_t* status;         // device, nullable
-    int32_t units_per_row;   // sum of rot_units over planes
+    int32_t units_per_row;   // sum of rot_tpr over planes
     int32_t pad2;
     KCosSin cs[KMAX_CS];
 };
@@ -123,6 +150,8 @@ struct KPagedParams {
     int32_t bt_stride;
     int32_t n_asm;
     int32_t n_remap;
+    int32_t asm_slices;      // blocks per ASSEMBLE task
+    int32_t remap_slices;    // blocks per REMAP task
     int64_t capacity;                    // physical pages
     const KSeqEntry* seqs;
     const KDirEntry* dirs;

@@ -22,6 +22,13 @@ int elem_size(int32_t dtype) {
 
 }  // namespace
 
+KDiv make_div(int32_t d) {
+    int32_t l = 0;
+    while ((int64_t(1) << l) < d) ++l;
+    const uint64_t mul = ((uint64_t(1) << 32) * ((uint64_t(1) << l) - uint64_t(d))) / uint64_t(d) + 1;
+    return KDiv{uint32_t(mul), l};
+}
+
 int describe_cache(const leyline_cache* cache, bool paged, KPlane out[LEYLINE_MAX_PLANES],
                    int* n_planes) {
     if (!cache) return LEYLINE_E_INVAL;
@@ -53,8 +60,9 @@ int describe_cache(const leyline_cache* cache, bool paged, KPlane out[LEYLINE_MA
         k.page_stride = paged ? pl.page_stride * esz : 0;
         k.row_bytes = int32_t(row_bytes);
         k.row_chunks = int32_t(row_bytes / 16);
-        k.units = k.row_chunks;
         k.rot = KROT_NONE;
+        k.tpr = k.row_chunks;
+        k.head_chunks = k.row_chunks;
         if (pl.rot_dim != 0) {
             if (pl.rot_dim < 0 || (pl.rot_dim & 1) || pl.n_heads < 1 || pl.head_stride <= 0 ||
                 pl.rot_offset < 0 || pl.rot_offset + pl.rot_dim > pl.head_stride ||
@@ -72,15 +80,37 @@ int describe_cache(const leyline_cache* cache, bool paged, KPlane out[LEYLINE_MA
             k.head_chunks = int32_t(int64_t(pl.head_stride) * esz / 16);
             k.rot_lo = int32_t(int64_t(pl.rot_offset) * esz / 16);
             k.rot_chunks = int32_t(int64_t(pl.rot_dim) * esz / 16);
-            if (neox) {
-                k.units = k.row_chunks - k.n_heads * (k.rot_chunks / 2);
-                k.rot_units = k.n_heads * (k.rot_chunks / 2);
-            } else {
-                k.rot_units = k.n_heads * k.rot_chunks;
-            }
+            k.n_pairs = pl.rot_dim / 2;
             k.cs_off = cs_off;
             cs_off += pl.rot_dim / 2;
+            if (neox) {
+                // Lane exchange in the row kernels: a wavefront covers 64 consecutive chunks of
+                // the rows laid end to end, so every band must sit inside one 64-chunk window.
+                bool ok = false;
+                if (k.row_chunks % 64 == 0) {
+                    ok = true;
+                    for (int h = 0; h < k.n_heads; ++h) {
+                        const int32_t lo = h * k.head_chunks + k.rot_lo, hi = lo + k.rot_chunks - 1;
+                        if (lo / 64 != hi / 64) ok = false;
+                    }
+                } else if (64 % k.row_chunks == 0) {
+                    ok = true;
+                }
+                k.neox_lanes = ok ? 1 : 0;
+                if (!ok) k.tpr = k.row_chunks - k.n_heads * (k.rot_chunks / 2);
+            }
+            // coefficients are staged per workgroup when rotating chunks are not a small minority
+            k.stage_cs = (4 * k.n_heads * k.rot_chunks >= k.row_chunks) ? 1 : 0;
+            // rotary-only kernels pack the bands of consecutive heads and rows back to back
+            k.band_tpr = (neox && !(k.rot_chunks <= 64 && !(k.rot_chunks & (k.rot_chunks - 1))))
+                             ? k.rot_chunks / 2 : k.rot_chunks;
+            k.rot_tpr = k.n_heads * k.band_tpr;
         }
+        k.units_all = k.rot == KROT_NEOX ? k.row_chunks - k.n_heads * (k.rot_chunks / 2) : k.row_chunks;
+        k.tpr_div = make_div(k.tpr);
+        k.head_div = make_div(k.head_chunks);
+        k.uhead_div = make_div(std::max(1, k.head_chunks - k.rot_chunks / 2));
+        k.band_div = make_div(std::max(1, k.band_tpr));
     }
     if (cs_off > KMAX_CS) return LEYLINE_E_INVAL;
     *n_planes = cache->n_planes;
@@ -160,28 +190,27 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
     for (int32_t j = 0; j < n_dirs; ++j) {
         const leyline_directive& d = dirs[j];
         if (d.stub_len > 0)
-            jobs.push_back(ContigJobHost{true, 0, d.span_start + shift, d.stub_len, 0, j});
+            jobs.push_back(ContigJobHost{KJOB_STUB, 0, d.span_start + shift, d.stub_len, 0, j});
         shift += d.stub_len - (d.span_end - d.span_start);
         const int64_t seg_end = (j + 1 < n_dirs) ? dirs[j + 1].span_start : seq_len;
         const int64_t count = seg_end - d.span_end;
         if (count > 0 && shift != 0)
-            jobs.push_back(ContigJobHost{false, d.span_end, 0, count, shift, j});
+            jobs.push_back(ContigJobHost{KJOB_CHAIN, d.span_end, 0, count, shift, j});
     }
     if (jobs.empty()) return LEYLINE_OK;
 
-    // Job a must finish before job b when b writes a row that a reads.  Within one job the
-    // overlap of its own source and destination is resolved by the kernel's chain order.  The
-    // resulting graph is acyclic: a left-moving segment can only wait for segments to its left,
-    // a right-moving one only for segments to its right, and a stub only for moves.
+    // Job a must finish before job b when b writes a row that a reads.  The resulting graph is
+    // acyclic: a left-moving segment can only wait for segments to its left, a right-moving one
+    // only for segments to its right, and a stub only for moves.
     const size_t n = jobs.size();
-    auto dst_lo = [&](const ContigJobHost& x) { return x.is_stub ? x.dst0 : x.src0 + x.delta; };
+    auto dst_lo = [&](const ContigJobHost& x) { return x.kind == KJOB_STUB ? x.dst0 : x.src0 + x.delta; };
     std::vector<int> level(n, 0);
     for (size_t iter = 0; iter < n; ++iter) {
         bool changed = false;
         for (size_t b = 0; b < n; ++b) {
             const int64_t blo = dst_lo(jobs[b]), bhi = blo + jobs[b].count;
             for (size_t a = 0; a < n; ++a) {
-                if (a == b || jobs[a].is_stub) continue;
+                if (a == b || jobs[a].kind == KJOB_STUB) continue;
                 const int64_t alo = jobs[a].src0, ahi = alo + jobs[a].count;
                 if (blo < ahi && alo < bhi && level[b] < level[a] + 1) {
                     level[b] = level[a] + 1;
@@ -191,23 +220,60 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
         }
         if (!changed) break;
     }
+
+    // Within a job, a left shift by m makes row x the destination of row x + m.  Splitting the
+    // source range into rounds of at most m rows, taken in ascending order (descending for a
+    // right shift), leaves each round with disjoint sources and destinations, and every row a
+    // round overwrites was read by an earlier round.  Rounds run as consecutive launches; a move
+    // needing more than MAX_ROUNDS rounds runs as ordered chains in a single launch instead.
     const int n_levels = *std::max_element(level.begin(), level.end()) + 1;
     const int32_t cs_need = cos_sin_per_shift(cache);
     for (int lv = 0; lv < n_levels; ++lv) {
-        std::vector<ContigJobHost> cur;
-        int32_t cs_used = 0;
+        std::vector<std::vector<ContigJobHost>> rounds(1);
         for (size_t a = 0; a < n; ++a) {
             if (level[a] != lv) continue;
-            const int32_t need = jobs[a].is_stub ? 0 : cs_need;
-            if (int(cur.size()) == KMAX_JOBS || cs_used + need > KMAX_CS) {
-                out->launches.push_back(cur);
-                cur.clear();
-                cs_used = 0;
+            const ContigJobHost& x = jobs[a];
+            if (x.kind == KJOB_STUB) {
+                rounds[0].push_back(x);
+                continue;
             }
-            cur.push_back(jobs[a]);
-            cs_used += need;
+            const int64_t m = x.delta < 0 ? -x.delta : x.delta;
+            const int64_t nr = (x.count + m - 1) / m;
+            if (nr > MAX_ROUNDS) {
+                rounds[0].push_back(x);       // KJOB_CHAIN
+                continue;
+            }
+            if (int64_t(rounds.size()) < nr) rounds.resize(size_t(nr));
+            // equal rounds of at most m rows (no small trailing launch)
+            const int64_t len = (x.count + nr - 1) / nr;
+            for (int64_t r = 0; r < nr; ++r) {
+                int64_t lo, hi;
+                if (x.delta < 0) {
+                    lo = x.src0 + r * len;
+                    hi = std::min(x.src0 + x.count, lo + len);
+                } else {
+                    hi = x.src0 + x.count - r * len;
+                    lo = std::max(x.src0, hi - len);
+                }
+                if (hi <= lo) continue;
+                rounds[size_t(r)].push_back(ContigJobHost{KJOB_ROUND, lo, 0, hi - lo, x.delta, x.dir});
+            }
         }
-        if (!cur.empty()) out->launches.push_back(cur);
+        for (const auto& rj : rounds) {
+            std::vector<ContigJobHost> cur;
+            int32_t cs_used = 0;
+            for (const ContigJobHost& x : rj) {
+                const int32_t need = x.kind == KJOB_STUB ? 0 : cs_need;
+                if (int(cur.size()) == KMAX_JOBS || cs_used + need > KMAX_CS) {
+                    out->launches.push_back(cur);
+                    cur.clear();
+                    cs_used = 0;
+                }
+                cur.push_back(x);
+                cs_used += need;
+            }
+            if (!cur.empty()) out->launches.push_back(cur);
+        }
     }
     return LEYLINE_OK;
 }

@@ -12,6 +12,9 @@
 
 namespace leyline {
 
+// Multiply-shift constants for division by d (1 <= d < 2^31), exact for numerators < 2^31.
+KDiv make_div(int32_t d);
+
 // A validated plane, reduced to what the kernels need (byte strides, 16-byte chunk geometry).
 int describe_cache(const leyline_cache* cache, bool paged, KPlane out[LEYLINE_MAX_PLANES],
                    int* n_planes);
@@ -32,10 +35,13 @@ int32_t cos_sin_per_shift(const leyline_cache* cache);
 // into launches so that no job of a launch overwrites a row another job of the same or a later
 // launch still has to read.
 struct ContigJobHost {
-    bool is_stub;
+    int32_t kind;       // KJOB_*
     int64_t src0, dst0, count, delta;
     int32_t dir;        // stub: directive index
 };
+
+// A move needing more rounds than this runs as ordered chains in one launch instead.
+constexpr int64_t MAX_ROUNDS = 16;
 
 struct ContigSchedule {
     int64_t new_len = 0;

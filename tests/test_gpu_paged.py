@@ -61,14 +61,20 @@ def _random_workload(rng, page, kind, dtype):
             r = rng.choice([0, 1, e - s, rng.randint(0, 2 * (e - s) + 3), max(0, e - s - page),
                             e - s + page])
             dirs.append(W.Dir(s, e, r, seq=b))
-    planes = [W.mla_plane()] if kind == "mla" else W.gqa_planes(heads=2, dim=128)
+    if kind == "mla":
+        planes = [W.mla_plane()]
+    elif kind == "mla_neox":      # half-split band that straddles wavefront windows: two-chunk units
+        planes = [W.PlaneDesc((576,), 1, 576, 512, 64, 1, 10000.0)]
+    else:
+        planes = W.gqa_planes(heads=2, dim=128)
     return W.Workload(f"paged_{kind}", 2, dtype, planes, dirs, lens, page_size=page,
                       seed=rng.randint(0, 10 ** 6))
 
 
-@pytest.mark.parametrize("kind,dtype", [("mla", "bf16"), ("gqa", "bf16"), ("mla", "f32")])
+@pytest.mark.parametrize("kind,dtype", [("mla", "bf16"), ("gqa", "bf16"), ("mla", "f32"),
+                                        ("gqa", "f32"), ("mla_neox", "bf16")])
 def test_small_random_paged_whole_pool(L, kind, dtype):
-    rng = random.Random(97 if kind == "mla" else 98)
+    rng = random.Random({"mla": 97, "gqa": 98, "mla_neox": 99}[kind] + (dtype == "f32"))
     for page in (1, 4, 16, 64):
         for ci in range(8):
             wl = _random_workload(rng, page, kind, dtype)
