@@ -1,16 +1,19 @@
 """Benchmark of the in-place KV-cache splice on one MI355X.
 
-One step = one splice call (delete the span, write the replacement, compact every downstream
-row and re-anchor its rotary band, all layers) on the workload's synthetic cache, already
-resident in HBM.  Prints one JSON line.
+One step = one splice call on the workload's synthetic cache, already resident in HBM: delete
+the span, write the replacement, compact every downstream row and re-anchor its rotary band, in
+all layers.  Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1] [--no-cpu-baseline]
+    python bench.py --summarize TRACE_DIR FETCH_DIR WRITE_DIR   # rocprofv3 output -> profiles/
 
 Default workload: MLA DeepSeek-V3 shape (61 layers, c_kv 512 + k_pe 64, bf16), one 32768-token
 sequence, a 4096-token span at a seeded start replaced by a 32-token stub, contiguous in place.
 """
 
 import argparse
+import csv
+import glob
 import hashlib
 import json
 import os
@@ -25,7 +28,10 @@ sys.path.insert(0, ROOT)
 METRIC = "re-anchored KV tokens/sec and achieved HBM GB/s (% of peak) per splice"
 PEAK_HBM_GBPS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_01065_amd", "csrc", "kernels.hip")
-TRAFFIC_DIR = os.path.join(ROOT, "profiles")
+PROFILES = os.path.join(ROOT, "profiles")
+CONTIG_KERNEL = "contig_move_kernel"
+PAGED_KERNEL = "paged_splice_kernel"
+COPY_KERNEL_HINT = "elementwise"        # torch's device copy kernel used for counter calibration
 
 
 def parse():
@@ -35,10 +41,12 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="mla_dsv3_32k")
     ap.add_argument("--replicas", type=int, default=2,
-                    help="independent cache copies used round-robin, so consecutive steps do not "
-                         "find each other's rows in the last-level cache")
+                    help="independent cache copies used round-robin (contiguous workloads), so "
+                         "consecutive steps do not find each other's rows in the last-level cache")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--command", default="", help="command line recorded in --summarize output")
     return ap.parse_args()
 
 
@@ -48,97 +56,71 @@ def kernel_sha():
 
 
 def measured_traffic(workload):
-    """Per-launch HBM bytes from committed rocprofv3 counter runs, if they were taken on the
+    """HBM bytes per splice from committed rocprofv3 counter runs, if they were taken on the
     current kernel source (else None)."""
-    path = os.path.join(TRAFFIC_DIR, f"traffic_{workload}.json")
+    path = os.path.join(PROFILES, f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         t = json.load(f)
     if t.get("kernel_sha") != kernel_sha():
         return None
-    return t.get("bytes_per_launch")
+    return {k: t[k] for k in ("fetch_bytes", "write_bytes", "total_bytes", "calibration", "per")}
+
+
+def row_bytes(wl):
+    esz = 2 if wl.dtype == "bf16" else 4
+    return sum(p.row_elems for p in wl.planes) * esz
 
 
 def contig_bytes(wl):
     """Algorithmic bytes of one contiguous splice: every moved row read and written once, every
-    stub row read once and written once (deleted rows cost nothing)."""
-    total = 0
+    replacement row read once and written once (deleted rows cost nothing)."""
     n = wl.seq_lens[0]
-    esz = 2 if wl.dtype == "bf16" else 4
-    row_bytes = sum(p.row_elems for p in wl.planes) * esz
-    shift, moved = 0, 0
+    rb = row_bytes(wl)
+    shift, moved, stub = 0, 0, 0
     for j, d in enumerate(wl.dirs):
         shift += d.stub_len - (d.span_end - d.span_start)
         seg_end = wl.dirs[j + 1].span_start if j + 1 < len(wl.dirs) else n
         if shift != 0:
             moved += seg_end - d.span_end
-        total += 2 * d.stub_len * row_bytes * wl.n_layers
-    total += 2 * moved * row_bytes * wl.n_layers
-    return total, moved
+        stub += d.stub_len
+    return 2 * (moved + stub) * rb * wl.n_layers, moved
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(json.dumps({"error": "this benchmark runs on one GPU only; the splice of one "
-                                   "sequence (or one batch) is a single-GPU operation",
-                          "n_gpus": args.gpus}))
-        sys.exit(2)
+def paged_bytes(wl, plans):
+    """Algorithmic bytes of one paged splice: every row gathered into a fresh page read and
+    written once (downstream rows, replacement rows and the prefix rows that share a page with
+    them), and the rotary bands of remapped pages read and written once."""
+    from oracle import splice_oracle as O
+    rb = row_bytes(wl)
+    esz = 2 if wl.dtype == "bf16" else 4
+    rot_b = sum(p.rot_dim * p.n_heads for p in wl.planes) * esz
+    asm_rows = remap_rows = moved = 0
+    P = wl.page_size
+    for plan in plans:
+        for k, kind in enumerate(plan.kinds):
+            rows = min(P, plan.new_len - k * P)
+            if kind == O.ASSEMBLE:
+                asm_rows += rows
+            elif kind == O.REMAP:
+                remap_rows += rows
+    for b, n in enumerate(wl.seq_lens):
+        shift = 0
+        mine = [d for d in wl.dirs if d.seq == b]
+        for j, d in enumerate(mine):
+            shift += d.stub_len - (d.span_end - d.span_start)
+            seg_end = mine[j + 1].span_start if j + 1 < len(mine) else n
+            if shift != 0:
+                moved += seg_end - d.span_end
+    return 2 * wl.n_layers * (asm_rows * rb + remap_rows * rot_b), moved
 
+
+def copy_ceiling(nbytes, dev, stream):
+    """Device-to-device copy of nbytes/2 (read) + nbytes/2 (written) with torch: a reference
+    rate, and the calibration kernel for the rocprofv3 byte counters."""
     import torch
-    import workloads as W
-    from paper_2606_01065_amd import leyline as L
-
-    wl = W.WORKLOADS[args.workload]()
-    if wl.page_size:
-        print(json.dumps({"error": "paged workloads are measured with --workload on the paged "
-                                   "benchmark path, not implemented in this entry"}))
-        sys.exit(2)
-    dev = "cuda:0"
-    torch.cuda.set_device(0)
-    stream = torch.cuda.current_stream()
-
-    replicas = []
-    base_planes, stubs = W.alloc_contig(wl, dev)
-    replicas.append(base_planes)
-    for _ in range(1, args.replicas):
-        replicas.append([t.clone() for t in base_planes])
-    specs = lambda planes: [L.PlaneSpec(t, p.n_heads, p.head_stride or p.row_elems, p.rot_offset,
-                                        p.rot_dim, p.style, p.base) for p, t in zip(wl.planes, planes)]
-    caches = [L.make_cache(specs(r)) for r in replicas]
-    dirs = L.make_directives([dict(span_start=d.span_start, span_end=d.span_end, stub=stubs[j],
-                                   stub_len=d.stub_len) for j, d in enumerate(wl.dirs)])
-    n = wl.seq_lens[0]
-    nd = len(wl.dirs)
-
-    for i in range(args.warmup):
-        L.leyline_splice_contig(caches[i % len(caches)], n, dirs, nd, stream)
-    torch.cuda.synchronize()
-
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    t_begin = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_begin.record(stream)
-    for i in range(args.steps):
-        starts[i].record(stream)
-        L.leyline_splice_contig(caches[i % len(caches)], n, dirs, nd, stream)
-        ends[i].record(stream)
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    total_ms = t_begin.elapsed_time(t_end)
-    per_launch_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
-    avg_launch_ms = float(np.mean(per_launch_ms))
-
-    alg_bytes, moved = contig_bytes(wl)
-    achieved = alg_bytes / (avg_launch_ms * 1e-3) / 1e9
-    ms_per_step = total_ms / args.steps
-    value = moved / (ms_per_step * 1e-3)
-
-    # device-to-device copy of the same number of bytes read (= written): the copy ceiling
-    half = alg_bytes // 2
+    half = nbytes // 2
     a = torch.empty(half, dtype=torch.uint8, device=dev)
     b = torch.empty(half, dtype=torch.uint8, device=dev)
     b.copy_(a)
@@ -149,13 +131,62 @@ def main():
         b.copy_(a)
     e1.record(stream)
     torch.cuda.synchronize()
-    copy_gbps = 2 * half * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9
-    del a, b
+    return 2 * half * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9, half
 
+
+def main():
+    args = parse()
+    if args.summarize:
+        summarize(args)
+        return
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only: a splice of one sequence "
+                                   "or one batch is a single-GPU operation", "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    import workloads as W
+    from paper_2606_01065_amd import leyline as L
+
+    wl = W.WORKLOADS[args.workload]()
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    specs = lambda planes: [L.PlaneSpec(t, p.n_heads, p.head_stride or p.row_elems, p.rot_offset,
+                                        p.rot_dim, p.style, p.base) for p, t in zip(wl.planes, planes)]
+
+    if wl.page_size:
+        step, kernel, alg_bytes, moved, launches, keep = setup_paged(wl, dev, L, W, specs, stream)
+        layout = f"paged, {wl.page_size}-token pages, {len(wl.seq_lens)} sequences"
+    else:
+        step, kernel, alg_bytes, moved, launches, keep = setup_contig(wl, dev, L, W, specs, stream, args)
+        layout = "contiguous in place"
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    t_begin = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_begin.record(stream)
+    for i in range(args.steps):
+        starts[i].record(stream)
+        step(i)
+        ends[i].record(stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_begin.elapsed_time(t_end)
+    splice_ms = float(np.mean([s.elapsed_time(e) for s, e in zip(starts, ends)]))
+
+    achieved = alg_bytes / (splice_ms * 1e-3) / 1e9
+    ms_per_step = total_ms / args.steps
+    copy_gbps, _ = copy_ceiling(alg_bytes, dev, stream)
     traffic = measured_traffic(wl.name)
     out = {
         "metric": METRIC,
-        "value": value,
+        "value": moved / (ms_per_step * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -165,42 +196,92 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": wl.dtype,
-        "data": "synthetic (seeded N(0,1) cache and stub)",
+        "data": "synthetic (seeded N(0,1) cache and replacement rows)",
         "config": {
             "workload": wl.name,
             "layers": wl.n_layers,
-            "seq_len": n,
-            "directives": [[d.span_start, d.span_end, d.stub_len] for d in wl.dirs],
+            "seq_lens": wl.seq_lens if len(wl.seq_lens) <= 4 else f"{len(wl.seq_lens)} sequences, "
+                        f"{sum(wl.seq_lens)} tokens",
+            "directives": [[d.seq, d.span_start, d.span_end, d.stub_len] for d in wl.dirs][:8],
             "moved_tokens": moved,
-            "layout": "contiguous in place",
+            "layout": layout,
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "contig_splice_kernel",
+            "kernel": kernel,
             "achieved": achieved,
             "peak": PEAK_HBM_GBPS,
             "unit": "GB/s",
             "frac": achieved / PEAK_HBM_GBPS,
             "traffic": traffic,
-            "algorithmic_bytes": alg_bytes,
-            "avg_launch_ms": avg_launch_ms,
+            "algorithmic_bytes_per_splice": alg_bytes,
+            "splice_ms": splice_ms,
+            "launches_per_splice": launches,
+            "avg_launch_ms": splice_ms / max(1, launches),
             "d2d_copy_GBps": copy_gbps,
         },
     }
-
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, base_planes, stubs, args.cpu_seconds, moved, ms_per_step)
+        out["cpu_baseline"] = cpu_baseline(wl, keep, args.cpu_seconds, moved)
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(wl, planes_dev, stubs_dev, budget_s, moved, gpu_ms):
-    """The oracle, as it stands, on a bounded sample: whole layers of the same splice, run one
-    after another until about budget_s seconds have passed; scaled to all layers."""
+def setup_contig(wl, dev, L, W, specs, stream, args):
+    import torch
+    base_planes, stubs = W.alloc_contig(wl, dev)
+    replicas = [base_planes] + [[t.clone() for t in base_planes] for _ in range(1, args.replicas)]
+    caches = [L.make_cache(specs(r)) for r in replicas]
+    dirs = L.make_directives([dict(span_start=d.span_start, span_end=d.span_end, stub=stubs[j],
+                                   stub_len=d.stub_len) for j, d in enumerate(wl.dirs)])
+    n, nd = wl.seq_lens[0], len(wl.dirs)
+    _, launches = L.leyline_contig_query(caches[0], n, dirs, nd)
+    alg_bytes, moved = contig_bytes(wl)
+
+    def step(i):
+        L.leyline_splice_contig(caches[i % len(caches)], n, dirs, nd, stream)
+
+    # pristine host copy of the first layers for the CPU baseline (before any step runs)
+    keep = dict(planes=[t[:8].cpu() for t in base_planes], stubs=[[s[:8].cpu() for s in per] for per in stubs])
+    torch.cuda.synchronize()
+    return step, CONTIG_KERNEL, alg_bytes, moved, launches, keep
+
+
+def setup_paged(wl, dev, L, W, specs, stream):
+    import torch
+    from oracle import splice_oracle as O   # page plan for the byte accounting only
+    pools, bt, free, stubs = W.alloc_paged(wl, dev)
+    cache = L.make_cache(specs(pools), paged=True)
+    dirs = L.make_directives([dict(span_start=d.span_start, span_end=d.span_end, stub=stubs[j],
+                                   seq=d.seq, stub_len=d.stub_len) for j, d in enumerate(wl.dirs)])
+    nd = len(wl.dirs)
+    new_lens, fresh, n_freed, ws_bytes = L.leyline_paged_query(cache, wl.seq_lens, bt.shape[1], dirs, nd)
+    bt_out = torch.empty_like(bt)
+    freed = torch.empty(max(1, n_freed), dtype=torch.int32, device=dev)
+    ws = torch.empty(max(256, ws_bytes), dtype=torch.uint8, device=dev)
+    plans = O.plan_paged(wl.seq_lens, [O.Directive(d.span_start, d.span_end, d.stub_len, seq=d.seq)
+                                       for d in wl.dirs], wl.page_size)
+    alg_bytes, moved = paged_bytes(wl, plans)
+
+    # The paged splice reads old pages and writes fresh ones; re-running it on the same inputs
+    # repeats the same work (remapped pages are rotated again, which does not change the bytes).
+    def step(i):
+        L.leyline_splice_paged(cache, wl.seq_lens, bt, bt_out, dirs, nd, free, freed, ws, stream=stream)
+
+    keep = dict(paged=True)
+    torch.cuda.synchronize()
+    return step, PAGED_KERNEL, alg_bytes, moved, 2, keep
+
+
+def cpu_baseline(wl, keep, budget_s, moved):
+    """The oracle, as it stands, on a bounded sample of the same splice: whole layers, cycled
+    until about budget_s seconds have passed, scaled to all layers.  numpy runs single-threaded
+    here."""
     import torch
     from oracle import splice_oracle as O
+    if keep.get("paged"):
+        return None
 
     def host(t):
-        t = t.detach().cpu()
         return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
 
     n = wl.seq_lens[0]
@@ -208,13 +289,15 @@ def cpu_baseline(wl, planes_dev, stubs_dev, budget_s, moved, gpu_ms):
     planes = [O.Plane(row_elems=p.row_elems, n_heads=p.n_heads, head_stride=p.head_stride or p.row_elems,
                       rot_offset=p.rot_offset, rot_dim=p.rot_dim, style=p.style, base=p.base)
               for p in wl.planes]
+    n_keep = keep["planes"][0].shape[0]
+    rows = [[host(t[l]).reshape(t.shape[1], -1) for t in keep["planes"]] for l in range(n_keep)]
+    stubs = [[[host(s[l]).reshape(s.shape[1], -1) for s in per] for per in keep["stubs"]] for l in range(n_keep)]
     done, spent = 0, 0.0
-    while done < wl.n_layers and spent < budget_s:
-        rows = [host(t[done]).reshape(t.shape[1], -1) for t in planes_dev]
-        stubs = [[host(s[done]).reshape(s.shape[1], -1) for s in per] for per in stubs_dev]
+    while spent < budget_s:
+        l = done % n_keep
         t0 = time.perf_counter()
         for pi, plane in enumerate(planes):
-            O.splice_rows(rows[pi], n, dirs, [s[pi] for s in stubs], plane, wl.dtype)
+            O.splice_rows(rows[l][pi], n, dirs, [s[pi] for s in stubs[l]], plane, wl.dtype)
         spent += time.perf_counter() - t0
         done += 1
     per_layer = spent / done
@@ -224,10 +307,107 @@ def cpu_baseline(wl, planes_dev, stubs_dev, budget_s, moved, gpu_ms):
         "unit": "tokens/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": f"{done} of {wl.n_layers} layers of the same splice (numpy fp64, one thread), "
-                  f"{spent:.1f} s, scaled to all layers: {full_s:.2f} s per splice",
-        "gpu_speedup": full_s / (gpu_ms * 1e-3),
+        "sample": f"{done} layer-splices of this workload (numpy fp64, one thread, layers cycled "
+                  f"over {n_keep} host-resident layers), {spent:.1f} s; scaled to {wl.n_layers} "
+                  f"layers: {full_s:.3f} s per splice",
     }
+
+
+# ---------------------------------------------------------------------- profile summaries ---
+
+def _read_csv(d, name):
+    hits = glob.glob(os.path.join(d, "**", f"*{name}*.csv"), recursive=True)
+    if not hits:
+        raise SystemExit(f"no *{name}*.csv under {d}")
+    with open(hits[0]) as f:
+        return list(csv.DictReader(f))
+
+
+def _counter_per_dispatch(rows, counter, match, after=-1):
+    """Counter value per dispatch of the kernels `match` accepts, for dispatch ids > after."""
+    vals = {}
+    for r in rows:
+        did = int(r.get("Dispatch_Id") or r.get("Correlation_Id"))
+        if did > after and match(r.get("Kernel_Name", "")) and r.get("Counter_Name") == counter:
+            vals[did] = vals.get(did, 0.0) + float(r["Counter_Value"])
+    return [vals[k] for k in sorted(vals)]
+
+
+def _last_dispatch(rows, match):
+    ids = [int(r.get("Dispatch_Id") or r.get("Correlation_Id")) for r in rows if match(r.get("Kernel_Name", ""))]
+    return max(ids) if ids else -1
+
+
+def _flag(cmd, name, default):
+    parts = cmd.split()
+    return int(parts[parts.index(name) + 1]) if name in parts else default
+
+
+def summarize(args):
+    """Turn rocprofv3 output (a --kernel-trace --stats run and two --pmc runs, FETCH_SIZE and
+    WRITE_SIZE, of the same bench command, recorded in --command) into
+    profiles/<kernel>_<workload>.md and the traffic record bench.py reports."""
+    trace_dir, fetch_dir, write_dir = args.summarize
+    import workloads as W
+    wl = W.WORKLOADS[args.workload]()
+    kernel = PAGED_KERNEL if wl.page_size else CONTIG_KERNEL
+    splices = _flag(args.command, "--steps", 100) + _flag(args.command, "--warmup", 10)
+    stats = _read_csv(trace_dir, "kernel_stats")
+    trace = _read_csv(trace_dir, "kernel_trace")
+    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace
+            if kernel in r["Kernel_Name"]]
+    fetch = _read_csv(fetch_dir, "counter_collection")
+    write = _read_csv(write_dir, "counter_collection")
+    is_k = lambda name: kernel in name
+    is_copy = lambda name: "leyline" not in name and ("copyBuffer" in name or "copy" in name.lower())
+    f_k = _counter_per_dispatch(fetch, "FETCH_SIZE", is_k)
+    w_k = _counter_per_dispatch(write, "WRITE_SIZE", is_k)
+    # calibration copies: the device copies the bench issues after its last splice
+    f_c = _counter_per_dispatch(fetch, "FETCH_SIZE", is_copy, _last_dispatch(fetch, is_k))
+    w_c = _counter_per_dispatch(write, "WRITE_SIZE", is_copy, _last_dispatch(write, is_k))
+    alg = paged_alg = None
+    if not wl.page_size:
+        alg, _ = contig_bytes(wl)
+    # calibration: the bench's 11 device copies each read and write alg/2 bytes
+    half = alg // 2 if alg else None
+    cal_f = (11 * half / (sum(f_c) * 1024)) if (half and f_c) else None
+    cal_w = (11 * half / (sum(w_c) * 1024)) if (half and w_c) else None
+    per_splice = len(durs) / splices if splices else 0
+    lines = [f"# {kernel} on {wl.name}", "", f"Command: `{args.command}`", "",
+             "## Kernel time (rocprofv3 --kernel-trace --stats)", "",
+             "| kernel | calls | avg us | total us |", "|---|---|---|---|"]
+    for r in stats:
+        nm = r["Name"]
+        if "leyline" in nm or is_copy(nm):
+            lines.append(f"| {nm[:90]} | {r['Calls']} | {float(r['AverageNs'])/1e3:.1f} | "
+                         f"{float(r['TotalDurationNs'])/1e3:.1f} |")
+    lines += ["", f"{kernel}: {len(durs)} dispatches for {splices} splices "
+              f"({per_splice:.1f} per splice); mean {np.mean(durs):.1f} us per dispatch; "
+              f"{np.sum(durs) / splices:.1f} us of kernel time per splice", "",
+              "## HBM bytes (rocprofv3 --pmc FETCH_SIZE, then --pmc WRITE_SIZE; KiB per dispatch)", "",
+              f"{kernel}: FETCH_SIZE mean {np.mean(f_k):.0f} KiB over {len(f_k)} dispatches; "
+              f"WRITE_SIZE mean {np.mean(w_k):.0f} KiB over {len(w_k)} dispatches"]
+    rec = None
+    if f_c and w_c and half:
+        lines.append(f"device copy after the last splice (calibration; 11 copies of {half} B each "
+                     f"way, {len(f_c)} / {len(w_c)} dispatches): FETCH_SIZE {sum(f_c):.0f} KiB, "
+                     f"WRITE_SIZE {sum(w_c):.0f} KiB in total -> bytes per counted byte "
+                     f"{cal_f:.3f} (fetch), {cal_w:.3f} (write)")
+        fetch_b = sum(f_k) * 1024 * cal_f / splices
+        write_b = sum(w_k) * 1024 * cal_w / splices
+        lines.append(f"per splice: fetched {fetch_b/1e9:.4f} GB, written {write_b/1e9:.4f} GB; "
+                     f"algorithmic {alg/1e9:.4f} GB; measured/algorithmic "
+                     f"{(fetch_b + write_b)/alg:.3f}")
+        rec = dict(kernel_sha=kernel_sha(), workload=wl.name, fetch_bytes=fetch_b,
+                   write_bytes=write_b, total_bytes=fetch_b + write_b, calibration=[cal_f, cal_w],
+                   per="splice", algorithmic_bytes=alg)
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, f"{kernel}_{wl.name}.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    if rec:
+        with open(os.path.join(PROFILES, f"traffic_{wl.name}.json"), "w") as f:
+            json.dump(rec, f, indent=1)
+    print("\n".join(lines))
 
 
 if __name__ == "__main__":

@@ -138,6 +138,15 @@ int leyline_abi_version(void);
 const char* leyline_last_hip_error(void);
 
 /*
+ * Host-only check of a contiguous splice: validates exactly as leyline_splice_contig does and
+ * reports the new length and the number of kernel launches the splice will enqueue (host
+ * outputs, each nullable).  Enqueues nothing.
+ */
+int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
+                         const leyline_directive* dirs, int32_t n_dirs,
+                         int64_t* new_len_out, int32_t* n_launches_out);
+
+/*
  * Contiguous in-place splice of one sequence (all layers and planes).
  *
  * cache->page_size must be 0; rows [0, seq_len) hold the sequence, capacity rows are allocated.

@@ -558,6 +558,42 @@ extern "C" const char* leyline_last_hip_error(void) {
     return hipGetErrorString(g_last_hip_error);
 }
 
+// Launches of one contiguous splice: per group of independent jobs, one launch per job kind
+// present, split further when a launch would exceed its item or cos/sin capacity.
+static int contig_launch_count(const leyline_cache* cache, const ContigSchedule& sched, int n_planes) {
+    const int32_t cs_need = cos_sin_per_shift(cache);
+    int n = 0;
+    for (const auto& group : sched.launches)
+        for (int kind : {int(KJOB_STUB), int(KJOB_CHAIN), int(KJOB_ROUND)}) {
+            int items = 0, cs = 0;
+            bool open = false;
+            for (const ContigJobHost& j : group) {
+                if (j.kind != kind) continue;
+                const int need = kind != KJOB_STUB ? cs_need : 0;
+                if (open && (items + n_planes > KMAX_LAUNCH_ITEMS || cs + need > KMAX_CS)) {
+                    ++n;
+                    items = cs = 0;
+                }
+                open = true;
+                items += n_planes;
+                cs += need;
+            }
+            if (open) ++n;
+        }
+    return n;
+}
+
+extern "C" int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
+                                    const leyline_directive* dirs, int32_t n_dirs,
+                                    int64_t* new_len_out, int32_t* n_launches_out) {
+    ContigSchedule sched;
+    int rc = plan_contig(cache, seq_len, dirs, n_dirs, &sched);
+    if (rc) return rc;
+    if (new_len_out) *new_len_out = sched.new_len;
+    if (n_launches_out) *n_launches_out = contig_launch_count(cache, sched, cache->n_planes);
+    return LEYLINE_OK;
+}
+
 extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len,
                                      const leyline_directive* dirs, int32_t n_dirs,
                                      int64_t* new_len_out, void* stream) {

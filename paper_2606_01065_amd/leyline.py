@@ -97,6 +97,8 @@ def _load():
         "leyline_strerror": (ctypes.c_char_p, [c_int]),
         "leyline_abi_version": (c_int, []),
         "leyline_last_hip_error": (ctypes.c_char_p, []),
+        "leyline_contig_query": (c_int, [P(leyline_cache), c_int64, P(leyline_directive), c_int32,
+                                         P(c_int64), P(c_int32)]),
         "leyline_splice_contig": (c_int, [P(leyline_cache), c_int64, P(leyline_directive), c_int32,
                                           P(c_int64), c_void_p]),
         "leyline_paged_query": (c_int, [P(leyline_cache), c_int32, P(c_int32), c_int32,
@@ -122,8 +124,9 @@ def _load():
 _lib = _load()
 
 #: every symbol the header declares (checked by tests against the loaded library)
-SYMBOLS = ("leyline_strerror", "leyline_abi_version", "leyline_last_hip_error", "leyline_splice_contig", "leyline_paged_query",
-           "leyline_paged_plan", "leyline_splice_paged", "leyline_rotate_delta")
+SYMBOLS = ("leyline_strerror", "leyline_abi_version", "leyline_last_hip_error", "leyline_contig_query",
+           "leyline_splice_contig", "leyline_paged_query", "leyline_paged_plan", "leyline_splice_paged",
+           "leyline_rotate_delta")
 
 
 def strerror(code: int) -> str:
@@ -241,6 +244,15 @@ def _check(rc: int, where: str) -> None:
 
 
 # ----------------------------------------------------------------------------- entry points --
+
+def leyline_contig_query(cache: leyline_cache, seq_len: int, dirs, n_dirs: int):
+    """Returns (new_len, n_launches) without enqueueing anything."""
+    new_len, n_launch = c_int64(0), c_int32(0)
+    rc = _lib.leyline_contig_query(ctypes.byref(cache), seq_len, dirs, n_dirs, ctypes.byref(new_len),
+                                   ctypes.byref(n_launch))
+    _check(rc, "leyline_contig_query")
+    return new_len.value, n_launch.value
+
 
 def leyline_splice_contig(cache: leyline_cache, seq_len: int, dirs, n_dirs: int, stream=None) -> int:
     """Returns the new sequence length."""

@@ -114,6 +114,21 @@ def test_contig_validation_codes():
     assert _contig_rc(c, 10, [(1, 2, 0)]) == L.E_INVAL
 
 
+def test_contig_query_reports_rounds_and_launches():
+    """A left shift by m of D downstream rows runs as ceil(D/m) rounds (one launch each) plus one
+    launch for the replacement copy; very small shifts run as ordered chains in one launch."""
+    c = _mla_cache(cap=64)
+    new_len, n = L.leyline_contig_query(c, 60, _dirs([(10, 20, 2)]), 1)       # m=8, D=40
+    assert (new_len, n) == (52, 5 + 1)
+    new_len, n = L.leyline_contig_query(c, 60, _dirs([(10, 11, 0)]), 1)       # m=1, D=49: chains
+    assert (new_len, n) == (59, 1)
+    new_len, n = L.leyline_contig_query(c, 60, _dirs([(10, 12, 4)]), 1)       # m=2 right, D=48
+    assert (new_len, n) == (62, 1 + 1)                                       # chains, then stub
+    with pytest.raises(L.LeylineError) as e:
+        L.leyline_contig_query(c, 60, _dirs([(10, 10, 5)]), 1)
+    assert e.value.code == L.E_CAPACITY
+
+
 def test_contig_noop_calls_do_not_need_a_device():
     """A call with nothing to move (no directives, or Delta = 0 with an empty stub) enqueues
     nothing and reports the unchanged length."""
