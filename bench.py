@@ -30,7 +30,7 @@ PEAK_HBM_GBPS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_01065_amd", "csrc", "kernels.hip")
 PROFILES = os.path.join(ROOT, "profiles")
 CONTIG_KERNEL = "contig_move_kernel"
-PAGED_KERNEL = "paged_splice_kernel"
+PAGED_KERNEL = "paged_move_kernel"
 COPY_KERNEL_HINT = "elementwise"        # torch's device copy kernel used for counter calibration
 
 

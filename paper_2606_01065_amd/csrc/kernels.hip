@@ -51,7 +51,6 @@ namespace leyline {
 
 constexpr int TPB = LEYLINE_TPB;
 constexpr int WIN = LEYLINE_WIN;
-constexpr int MAX_PAGE = 256;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -398,49 +397,29 @@ __global__ __launch_bounds__(TPB) void rotate_rows_kernel(const KRotateParams P)
 
 // ------------------------------------------------------------------------------ paged splice ---
 //
-// Blocks over (page task slice, layer, plane).  An ASSEMBLE task gathers the rows of one new
-// page (prefix remainder, replacement tokens and shifted downstream rows, possibly from two old
-// pages) into a fresh page, rotating downstream rows on the way; each of its blocks moves TPB
-// consecutive chunks of the page's rows, one per thread, after resolving the sources of the
-// rows it covers into LDS.  A REMAP task rotates the rotary bands
-// of a re-used page in place.  Nothing is written to an old page except the rotary bands of
-// REMAP pages, which no ASSEMBLE task reads.
+// Three steps on the call's stream.  (1) paged_rows_kernel resolves every row of every ASSEMBLE
+// page once (shared by all layers and planes): which old physical page and row, or which
+// replacement token, it comes from, which fresh page it goes to, and which shift re-anchors it.
+// (2) paged_move_kernel moves those rows like the contiguous kernel: rows laid end to end, one
+// 16-byte chunk per thread, so each wavefront reads one row entry and moves whole lines.
+// (3) paged_remap_kernel rotates the rotary bands of REMAP pages (re-used whole pages) in place.
+// Nothing is written to an old page except the rotary bands of REMAP pages, which no ASSEMBLE
+// row reads.
 
-template <int ESZ>
-__global__ __launch_bounds__(TPB) void paged_splice_kernel(const KPagedParams P) {
-    __shared__ const char* row_src[MAX_PAGE];
-    __shared__ int32_t row_cs[MAX_PAGE];
-    __shared__ char* page_dst;
-    const int layer = blockIdx.y;
-    const int plane = blockIdx.z;
-    const KPlane& pl = P.planes[plane];
-    const int64_t lbase_off = int64_t(layer) * pl.layer_stride;
-    const int bx = blockIdx.x;
-    const int n_asm_blocks = P.n_asm * P.asm_slices;
-
-    if (bx < n_asm_blocks) {
-        const int task = bx / P.asm_slices;
-        const int32_t slice = bx - task * P.asm_slices;
-        const KAssembleTask T = P.asm_tasks[task];
-        const KSeqEntry S = P.seqs[T.seq];
-        const int64_t lo = int64_t(T.k) * P.page_size;
-        const int32_t valid = int32_t(min(int64_t(P.page_size), int64_t(S.new_len) - lo));
-        const int32_t total = valid * pl.tpr;
-        const int32_t f0 = slice * TPB;
-        if (f0 >= total) return;                                  // whole block idle
-        const int32_t r0 = fdiv(f0, pl.tpr_div);
-        const int32_t r1 = min(valid, fdiv(min(total, f0 + TPB) - 1, pl.tpr_div) + 1);
-        if (threadIdx.x == 0) {
-            const int32_t fp = T.fresh < P.n_free ? P.free_pages[T.fresh] : -1;
-            if (fp < 0 || fp >= P.capacity) {
-                if (P.status) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
-                page_dst = nullptr;
-            } else {
-                page_dst = pl.base + lbase_off + int64_t(fp) * pl.page_stride;
-            }
-        }
-        for (int32_t r = r0 + int32_t(threadIdx.x); r < r1; r += TPB) {
-            const int64_t q = lo + r;
+__global__ __launch_bounds__(TPB) void paged_rows_kernel(const KPagedParams P) {
+    const int32_t i = int32_t(blockIdx.x) * TPB + int32_t(threadIdx.x);
+    if (i >= P.n_rows) return;
+    const int32_t task = i / P.page_size, r = i - task * P.page_size;
+    const KAssembleTask T = P.asm_tasks[task];
+    const KSeqEntry S = P.seqs[T.seq];
+    const int64_t q = int64_t(T.k) * P.page_size + r;
+    KRowMove e{KROW_SKIP, 0, 0, r, -1, -1};
+    if (q < S.new_len) {
+        const int32_t fp = T.fresh < P.n_free ? P.free_pages[T.fresh] : -1;
+        if (fp < 0 || fp >= P.capacity) {
+            if (P.status) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
+        } else {
+            e.dst_page = fp;
             // last directive of the sequence whose replacement starts at or before q
             int32_t jlo = 0, jhi = S.dir_count;
             while (jlo < jhi) {
@@ -448,47 +427,64 @@ __global__ __launch_bounds__(TPB) void paged_splice_kernel(const KPagedParams P)
                 if (P.dirs[S.dir_begin + mid].stub_start <= q) jlo = mid + 1; else jhi = mid;
             }
             int64_t old = q;
-            int32_t cs = -1;
-            const char* src = nullptr;
             if (jlo > 0) {
-                const KDirEntry& D = P.dirs[S.dir_begin + jlo - 1];
+                const int32_t j = S.dir_begin + jlo - 1;
+                const KDirEntry& D = P.dirs[j];
                 if (q < D.stub_start + D.stub_len) {
-                    src = D.stub[plane] + (int64_t(layer) * D.stub_len + (q - D.stub_start)) * pl.row_bytes;
+                    e.src_page = KROW_STUB;
+                    e.src_row = int32_t(q - D.stub_start);
+                    e.dir = j;
                     old = -1;
                 } else {
                     old = q - D.delta;
-                    cs = D.cs;
+                    e.cs = D.cs;
                 }
             }
             if (old >= 0) {
                 const int32_t pg = P.bt_in[int64_t(T.seq) * P.bt_stride + old / P.page_size];
                 if (pg < 0 || pg >= P.capacity) {
                     if (P.status) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
-                    src = nullptr;
+                    e.src_page = KROW_SKIP;
                 } else {
-                    src = pl.base + lbase_off + int64_t(pg) * pl.page_stride + (old % P.page_size) * pl.token_stride;
+                    e.src_page = pg;
+                    e.src_row = int32_t(old % P.page_size);
                 }
             }
-            row_src[r - r0] = src;
-            row_cs[r - r0] = cs;
         }
-        __syncthreads();
-        char* dst_page = page_dst;
-        const int32_t f = f0 + int32_t(threadIdx.x);
-        if (!dst_page || f >= total) return;
-        const int32_t r = fdiv(f, pl.tpr_div);
-        const char* src = row_src[r - r0];
-        if (!src) return;
-        const int32_t cs = row_cs[r - r0];
-        move_row_unit<ESZ>(pl, src, dst_page + int64_t(r) * pl.token_stride, f - r * pl.tpr, P.cs,
-                           cs >= 0 ? cs + pl.cs_off : -1);
-        return;
     }
+    P.rows[i] = e;
+}
 
-    // REMAP: rotate the rotary bands of a re-used page in place.
+template <int ESZ>
+__global__ __launch_bounds__(TPB) void paged_move_kernel(const KPagedParams P) {
+    const int plane = blockIdx.z;
+    const KPlane& pl = P.planes[plane];
+    if (int64_t(blockIdx.x) * TPB >= int64_t(P.n_rows) * pl.tpr) return;   // past this plane
+    const int32_t t = int32_t(blockIdx.x) * TPB + int32_t(threadIdx.x);
+    const int32_t i = fdiv(t, pl.tpr_div), u = t - i * pl.tpr;
+    if (i >= P.n_rows) return;
+    const KRowMove e = P.rows[i];
+    if (e.src_page == KROW_SKIP) return;
+    const int layer = blockIdx.y;
+    char* lbase = pl.base + int64_t(layer) * pl.layer_stride;
+    const char* src;
+    if (e.src_page == KROW_STUB) {
+        const KDirEntry& D = P.dirs[e.dir];
+        src = D.stub[plane] + (int64_t(layer) * D.stub_len + e.src_row) * pl.row_bytes;
+    } else {
+        src = lbase + int64_t(e.src_page) * pl.page_stride + int64_t(e.src_row) * pl.token_stride;
+    }
+    char* dst = lbase + int64_t(e.dst_page) * pl.page_stride + int64_t(e.dst_row) * pl.token_stride;
+    move_row_unit<ESZ>(pl, src, dst, u, P.cs, e.cs >= 0 ? e.cs + pl.cs_off : -1);
+}
+
+template <int ESZ>
+__global__ __launch_bounds__(TPB) void paged_remap_kernel(const KPagedParams P) {
+    const int plane = blockIdx.z;
+    const KPlane& pl = P.planes[plane];
     if (pl.rot_tpr == 0) return;
-    const int rb = bx - n_asm_blocks;
-    const int task = rb / P.remap_slices, slice = rb - task * P.remap_slices;
+    const int layer = blockIdx.y;
+    const int task = blockIdx.x / P.remap_slices, slice = blockIdx.x - task * P.remap_slices;
     const KRemapTask T = P.remap_tasks[task];
     const KSeqEntry S = P.seqs[T.seq];
     const KDirEntry& D = P.dirs[T.dir];
@@ -503,7 +499,8 @@ __global__ __launch_bounds__(TPB) void paged_splice_kernel(const KPagedParams P)
         return;
     }
     const int32_t r = f / pl.rot_tpr;
-    char* row = pl.base + lbase_off + int64_t(pg) * pl.page_stride + int64_t(r) * pl.token_stride;
+    char* row = pl.base + int64_t(layer) * pl.layer_stride + int64_t(pg) * pl.page_stride +
+                int64_t(r) * pl.token_stride;
     move_band<ESZ>(pl, row, row, f - r * pl.rot_tpr, P.cs, D.cs + pl.cs_off);
 }
 
@@ -733,7 +730,7 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
     int n_planes = 0;
     int rc = describe_cache(cache, true, planes, &n_planes);
     if (rc) return rc;
-    if (cache->page_size > MAX_PAGE || bt_stride < 1 || n_free < 0 || freed_cap < 0) return LEYLINE_E_INVAL;
+    if (bt_stride < 1 || n_free < 0 || freed_cap < 0) return LEYLINE_E_INVAL;
     if (n_seqs > 0 && (!block_table_in || !block_table_out || block_table_in == block_table_out))
         return LEYLINE_E_INVAL;
     PagedPlan plan;
@@ -754,8 +751,10 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
     hipStream_t s = static_cast<hipStream_t>(stream);
     const KPagedTables& t = img.tables;
     char* ws = static_cast<char*>(workspace);
-    if (t.total > 0) {
-        rc = hip_status(hipMemcpyAsync(ws, img.bytes.data(), size_t(t.total), hipMemcpyHostToDevice, s));
+    for (int p = 0; p < n_planes; ++p)
+        if (int64_t(t.n_rows) * planes[p].tpr > INT32_MAX - TPB) return LEYLINE_E_INVAL;
+    if (t.upload > 0) {
+        rc = hip_status(hipMemcpyAsync(ws, img.bytes.data(), size_t(t.upload), hipMemcpyHostToDevice, s));
         if (rc) return rc;
     }
     if (t.n_asm + t.n_remap > 0) {
@@ -768,12 +767,12 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         P.bt_stride = bt_stride;
         P.n_asm = t.n_asm;
         P.n_remap = t.n_remap;
-        int32_t asm_slices = 1, remap_slices = 1;
+        P.n_rows = t.n_rows;
+        int32_t remap_slices = 1, max_tpr = 1;
         for (int p = 0; p < n_planes; ++p) {
-            asm_slices = std::max(asm_slices, (cache->page_size * planes[p].tpr + TPB - 1) / TPB);
             remap_slices = std::max(remap_slices, (cache->page_size * planes[p].rot_tpr + TPB - 1) / TPB);
+            max_tpr = std::max(max_tpr, planes[p].tpr);
         }
-        P.asm_slices = asm_slices;
         P.remap_slices = remap_slices;
         P.capacity = cache->capacity;
         P.seqs = reinterpret_cast<const KSeqEntry*>(ws + t.off_seq);
@@ -781,16 +780,27 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         P.cs = reinterpret_cast<const KCosSin*>(ws + t.off_cs);
         P.asm_tasks = reinterpret_cast<const KAssembleTask*>(ws + t.off_asm);
         P.remap_tasks = reinterpret_cast<const KRemapTask*>(ws + t.off_remap);
+        P.rows = reinterpret_cast<KRowMove*>(ws + t.off_rows);
         P.bt_in = block_table_in;
         P.free_pages = free_pages;
         P.n_free = n_free;
         P.status = device_status;
-        const int64_t blocks = int64_t(t.n_asm) * asm_slices + int64_t(t.n_remap) * remap_slices;
-        if (blocks > INT32_MAX) return LEYLINE_E_INVAL;
-        const dim3 grid(unsigned(blocks), unsigned(cache->n_layers), unsigned(n_planes));
-        rc = cache->dtype == LEYLINE_BF16 ? launch(paged_splice_kernel<2>, grid, s, P)
-                                          : launch(paged_splice_kernel<4>, grid, s, P);
-        if (rc) return rc;
+        const bool bf16 = cache->dtype == LEYLINE_BF16;
+        if (t.n_rows > 0) {
+            rc = launch(paged_rows_kernel, dim3(unsigned((t.n_rows + TPB - 1) / TPB)), s, P);
+            if (rc) return rc;
+            const int64_t blocks = (int64_t(t.n_rows) * max_tpr + TPB - 1) / TPB;
+            const dim3 grid(unsigned(blocks), unsigned(cache->n_layers), unsigned(n_planes));
+            rc = bf16 ? launch(paged_move_kernel<2>, grid, s, P) : launch(paged_move_kernel<4>, grid, s, P);
+            if (rc) return rc;
+        }
+        if (t.n_remap > 0) {
+            const int64_t blocks = int64_t(t.n_remap) * remap_slices;
+            if (blocks > INT32_MAX) return LEYLINE_E_INVAL;
+            const dim3 grid(unsigned(blocks), unsigned(cache->n_layers), unsigned(n_planes));
+            rc = bf16 ? launch(paged_remap_kernel<2>, grid, s, P) : launch(paged_remap_kernel<4>, grid, s, P);
+            if (rc) return rc;
+        }
     }
     if (t.n_pages + t.n_freed > 0) {
         KTableParams T;

@@ -128,6 +128,18 @@ struct KRemapTask {
     int32_t seq, k, src_page, dir;
 };
 
+// One row of an ASSEMBLE page, resolved on the device from the plan and the block tables.
+struct KRowMove {
+    int32_t src_page;        // physical page of the old row; KROW_STUB: replacement row; KROW_SKIP
+    int32_t src_row;         // row within that page, or token of the replacement
+    int32_t dst_page;        // fresh physical page
+    int32_t dst_row;         // row within the fresh page
+    int32_t cs;              // first cos/sin entry of the row's shift (-1: not rotated)
+    int32_t dir;             // replacement rows: directive index
+};
+constexpr int32_t KROW_STUB = -1;
+constexpr int32_t KROW_SKIP = -2;
+
 struct KPageEntry {
     int32_t kind, src;       // LEYLINE_PAGE_*, old logical page or fresh ordinal
 };
@@ -138,8 +150,12 @@ struct KFreedEntry {
 
 // Byte offsets of the tables inside the workspace (converted to pointers at launch).
 struct KPagedTables {
-    int64_t off_seq, off_dir, off_cs, off_asm, off_remap, off_pages, off_freed, total;
+    int64_t off_seq, off_dir, off_cs, off_asm, off_remap, off_pages, off_freed, off_rows;
+    int64_t upload;          // bytes uploaded from the host (the tables before the row table)
+    int64_t total;           // workspace bytes (the row table is written on the device)
     int32_t n_seqs, n_dirs, n_cs, n_asm, n_remap, n_pages, n_freed, bt_stride;
+    int32_t n_rows;          // n_asm * page_size
+    int32_t pad;
 };
 
 struct KPagedParams {
@@ -150,7 +166,7 @@ struct KPagedParams {
     int32_t bt_stride;
     int32_t n_asm;
     int32_t n_remap;
-    int32_t asm_slices;      // blocks per ASSEMBLE task
+    int32_t n_rows;          // ASSEMBLE rows (n_asm * page_size)
     int32_t remap_slices;    // blocks per REMAP task
     int64_t capacity;                    // physical pages
     const KSeqEntry* seqs;
@@ -163,6 +179,7 @@ struct KPagedParams {
     int32_t n_free;
     int32_t pad;
     int32_t* status;
+    KRowMove* rows;          // workspace, n_rows entries
 };
 
 struct KTableParams {

@@ -442,11 +442,16 @@ int build_paged_image(const leyline_cache* cache, const PagedPlan& plan, int32_t
     t.off_remap = place(remap_tasks.size() * sizeof(KRemapTask));
     t.off_pages = place(pages.size() * sizeof(KPageEntry));
     t.off_freed = place(freed.size() * sizeof(KFreedEntry));
+    t.upload = off;
+    const int64_t n_rows = int64_t(asm_tasks.size()) * plan.page_size;
+    if (n_rows > INT32_MAX) return LEYLINE_E_CAPACITY;
+    t.off_rows = place(size_t(n_rows) * sizeof(KRowMove));
     t.total = off;
     t.n_seqs = n_seqs; t.n_dirs = n_dirs; t.n_cs = int32_t(cs.size());
     t.n_asm = int32_t(asm_tasks.size()); t.n_remap = int32_t(remap_tasks.size());
     t.n_pages = int32_t(pages.size()); t.n_freed = int32_t(freed.size()); t.bt_stride = bt_stride;
-    img->bytes.assign(size_t(off), 0);
+    t.n_rows = int32_t(n_rows);
+    img->bytes.assign(size_t(t.upload), 0);
     auto put = [&](int64_t at, const void* src, size_t bytes) {
         if (bytes) std::memcpy(img->bytes.data() + at, src, bytes);
     };
