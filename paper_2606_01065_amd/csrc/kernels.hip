@@ -50,6 +50,14 @@ namespace leyline {
 #endif
 
 constexpr int TPB = LEYLINE_TPB;
+#ifndef LEYLINE_PAGED_TPB
+#define LEYLINE_PAGED_TPB 256
+#endif
+#ifndef LEYLINE_PAGED_LPT
+#define LEYLINE_PAGED_LPT 2
+#endif
+constexpr int PAGED_TPB = LEYLINE_PAGED_TPB;   // paged gather workgroup size
+constexpr int PAGED_LPT = LEYLINE_PAGED_LPT;   // layers per paged-gather thread
 constexpr int WIN = LEYLINE_WIN;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -181,13 +189,37 @@ __device__ __forceinline__ Unit map_unit(const KPlane& p, int32_t u) {
     return r;
 }
 
+// Re-anchor chunk u of one row in registers with the cos/sin block table[cs + pair] (single-chunk
+// mode: interleaved bands, or half-split bands whose partner chunks sit in the same wavefront and
+// are exchanged between lanes).  Partner lanes belong to the same row and take the same path.
+template <int ESZ>
+__device__ __forceinline__ void rotate_chunk(const KPlane& pl, u32x4& v, int32_t u, const KCosSin* table,
+                                             int32_t cs) {
+    constexpr int EPC = Elt<ESZ>::EPC;
+    const int32_t h = fdiv(u, pl.head_div);
+    const int32_t j = u - h * pl.head_chunks - pl.rot_lo;
+    if (h < pl.n_heads && j >= 0 && j < pl.rot_chunks) {
+        if (pl.rot == KROT_INTERLEAVED) {
+            rot_interleaved<ESZ>(v, table, cs + j * (EPC / 2));
+        } else {
+            const int32_t half = pl.rot_chunks >> 1;
+            const bool lo = j < half;
+            const int lane = int(threadIdx.x & 63);
+            const int partner = lo ? lane + half : lane - half;
+            u32x4 o;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[i]), partner, 64));
+            if (lo) rot_halves<ESZ>(v, o, table, cs + j * EPC);
+            else rot_halves<ESZ>(o, v, table, cs + (j - half) * EPC);
+        }
+    }
+}
+
 // Row kernels: move unit u of one row from src to dst, re-anchored with the cos/sin block
-// table[cs + pair] (cs < 0: copied unchanged).  In lane-exchange mode the partner lanes of a
-// half-split band belong to the same row and take the same path.
+// table[cs + pair] (cs < 0: copied unchanged).
 template <int ESZ>
 __device__ __forceinline__ void move_row_unit(const KPlane& pl, const char* src, char* dst, int32_t u,
                                               const KCosSin* table, int32_t cs) {
-    constexpr int EPC = Elt<ESZ>::EPC;
     if (pl.rot == KROT_NEOX && !pl.neox_lanes) {
         const Unit un = map_unit<ESZ>(pl, u);
         const int64_t a = int64_t(un.a) * 16, b = int64_t(un.b) * 16;
@@ -200,25 +232,7 @@ __device__ __forceinline__ void move_row_unit(const KPlane& pl, const char* src,
     }
     const int64_t off = int64_t(u) * 16;
     u32x4 v = ld16(src + off);
-    if (cs >= 0 && pl.rot != KROT_NONE) {
-        const int32_t h = fdiv(u, pl.head_div);
-        const int32_t j = u - h * pl.head_chunks - pl.rot_lo;
-        if (h < pl.n_heads && j >= 0 && j < pl.rot_chunks) {
-            if (pl.rot == KROT_INTERLEAVED) {
-                rot_interleaved<ESZ>(v, table, cs + j * (EPC / 2));
-            } else {
-                const int32_t half = pl.rot_chunks >> 1;
-                const bool lo = j < half;
-                const int lane = int(threadIdx.x & 63);
-                const int partner = lo ? lane + half : lane - half;
-                u32x4 o;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[i]), partner, 64));
-                if (lo) rot_halves<ESZ>(v, o, table, cs + j * EPC);
-                else rot_halves<ESZ>(o, v, table, cs + (j - half) * EPC);
-            }
-        }
-    }
+    if (cs >= 0 && pl.rot != KROT_NONE) rotate_chunk<ESZ>(pl, v, u, table, cs);
     st16(dst + off, v);
 }
 
@@ -456,26 +470,48 @@ __global__ __launch_bounds__(TPB) void paged_rows_kernel(const KPagedParams P) {
 }
 
 template <int ESZ>
-__global__ __launch_bounds__(TPB) void paged_move_kernel(const KPagedParams P) {
+__global__ __launch_bounds__(PAGED_TPB) void paged_move_kernel(const KPagedParams P) {
     const int plane = blockIdx.z;
     const KPlane& pl = P.planes[plane];
-    if (int64_t(blockIdx.x) * TPB >= int64_t(P.n_rows) * pl.tpr) return;   // past this plane
-    const int32_t t = int32_t(blockIdx.x) * TPB + int32_t(threadIdx.x);
+    if (int64_t(blockIdx.x) * PAGED_TPB >= int64_t(P.n_rows) * pl.tpr) return;   // past this plane
+    const int32_t t = int32_t(blockIdx.x) * PAGED_TPB + int32_t(threadIdx.x);
     const int32_t i = fdiv(t, pl.tpr_div), u = t - i * pl.tpr;
     if (i >= P.n_rows) return;
     const KRowMove e = P.rows[i];
     if (e.src_page == KROW_SKIP) return;
-    const int layer = blockIdx.y;
-    char* lbase = pl.base + int64_t(layer) * pl.layer_stride;
+    // PAGED_LPT consecutive layers per thread: one row entry, all loads in flight before any store.
+    const int layer0 = int(blockIdx.y) * PAGED_LPT;
+    const int nl = min(PAGED_LPT, P.n_layers - layer0);
     const char* src;
+    int64_t src_step;
     if (e.src_page == KROW_STUB) {
         const KDirEntry& D = P.dirs[e.dir];
-        src = D.stub[plane] + (int64_t(layer) * D.stub_len + e.src_row) * pl.row_bytes;
+        src_step = D.stub_len * pl.row_bytes;
+        src = D.stub[plane] + int64_t(layer0) * src_step + int64_t(e.src_row) * pl.row_bytes;
     } else {
-        src = lbase + int64_t(e.src_page) * pl.page_stride + int64_t(e.src_row) * pl.token_stride;
+        src_step = pl.layer_stride;
+        src = pl.base + int64_t(layer0) * pl.layer_stride + int64_t(e.src_page) * pl.page_stride +
+              int64_t(e.src_row) * pl.token_stride;
     }
-    char* dst = lbase + int64_t(e.dst_page) * pl.page_stride + int64_t(e.dst_row) * pl.token_stride;
-    move_row_unit<ESZ>(pl, src, dst, u, P.cs, e.cs >= 0 ? e.cs + pl.cs_off : -1);
+    char* dst = pl.base + int64_t(layer0) * pl.layer_stride + int64_t(e.dst_page) * pl.page_stride +
+                int64_t(e.dst_row) * pl.token_stride;
+    const int32_t cs = e.cs >= 0 ? e.cs + pl.cs_off : -1;
+    if (pl.rot == KROT_NEOX && !pl.neox_lanes) {
+        for (int l = 0; l < nl; ++l) move_row_unit<ESZ>(pl, src + l * src_step, dst + l * pl.layer_stride, u, P.cs, cs);
+        return;
+    }
+    const int64_t off = int64_t(u) * 16;
+    u32x4 v[PAGED_LPT];
+#pragma unroll
+    for (int l = 0; l < PAGED_LPT; ++l)
+        if (l < nl) v[l] = ld16(src + l * src_step + off);
+#pragma unroll
+    for (int l = 0; l < PAGED_LPT; ++l) {
+        if (l < nl) {
+            if (cs >= 0 && pl.rot != KROT_NONE) rotate_chunk<ESZ>(pl, v[l], u, P.cs, cs);
+            st16(dst + l * pl.layer_stride + off, v[l]);
+        }
+    }
 }
 
 template <int ESZ>
@@ -537,9 +573,9 @@ int hip_status(hipError_t e) {
 // Launch and report the launch's own status: an error left behind by an earlier, unrelated
 // runtime call on this thread is cleared first so it is not blamed on this launch.
 template <typename K, typename A>
-int launch(K kernel, dim3 grid, hipStream_t stream, const A& args) {
+int launch(K kernel, dim3 grid, hipStream_t stream, const A& args, int block = TPB) {
     (void)hipGetLastError();
-    hipLaunchKernelGGL(kernel, grid, dim3(TPB), 0, stream, args);
+    hipLaunchKernelGGL(kernel, grid, dim3(block), 0, stream, args);
     return hip_status(hipGetLastError());
 }
 
@@ -752,7 +788,7 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
     const KPagedTables& t = img.tables;
     char* ws = static_cast<char*>(workspace);
     for (int p = 0; p < n_planes; ++p)
-        if (int64_t(t.n_rows) * planes[p].tpr > INT32_MAX - TPB) return LEYLINE_E_INVAL;
+        if (int64_t(t.n_rows) * planes[p].tpr > INT32_MAX - 1024) return LEYLINE_E_INVAL;
     if (t.upload > 0) {
         rc = hip_status(hipMemcpyAsync(ws, img.bytes.data(), size_t(t.upload), hipMemcpyHostToDevice, s));
         if (rc) return rc;
@@ -789,9 +825,11 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         if (t.n_rows > 0) {
             rc = launch(paged_rows_kernel, dim3(unsigned((t.n_rows + TPB - 1) / TPB)), s, P);
             if (rc) return rc;
-            const int64_t blocks = (int64_t(t.n_rows) * max_tpr + TPB - 1) / TPB;
-            const dim3 grid(unsigned(blocks), unsigned(cache->n_layers), unsigned(n_planes));
-            rc = bf16 ? launch(paged_move_kernel<2>, grid, s, P) : launch(paged_move_kernel<4>, grid, s, P);
+            const int64_t blocks = (int64_t(t.n_rows) * max_tpr + PAGED_TPB - 1) / PAGED_TPB;
+            const dim3 grid(unsigned(blocks), unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT),
+                            unsigned(n_planes));
+            rc = bf16 ? launch(paged_move_kernel<2>, grid, s, P, PAGED_TPB)
+                      : launch(paged_move_kernel<4>, grid, s, P, PAGED_TPB);
             if (rc) return rc;
         }
         if (t.n_remap > 0) {

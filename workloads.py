@@ -183,6 +183,17 @@ def fresh_page_bound(w: Workload) -> int:
     return total
 
 
+def paged_new_lens(w: Workload) -> List[int]:
+    return [n + sum(d.stub_len - (d.span_end - d.span_start) for d in w.dirs if d.seq == b)
+            for b, n in enumerate(w.seq_lens)]
+
+
+def paged_bt_stride(w: Workload) -> int:
+    """Block-table width: pages of the longer of each sequence's old and new length."""
+    P = w.page_size
+    return max(-(-max(n, m) // P) for n, m in zip(w.seq_lens, paged_new_lens(w)))
+
+
 def alloc_paged(w: Workload, device, seed: int = None, fill: bool = True, spare_pages: int = 8):
     """Pool tensors [L, n_pool, P, *row] per plane; block table int32 [n_seqs, bt_stride] with the
     sequences' pages drawn from a seeded permutation of the pool; the rest is the free list.
@@ -191,10 +202,7 @@ def alloc_paged(w: Workload, device, seed: int = None, fill: bool = True, spare_
     P = w.page_size
     rng = np.random.default_rng(seed + 77)
     old_pages = [-(-n // P) for n in w.seq_lens]
-    new_lens = []
-    for b, n in enumerate(w.seq_lens):
-        new_lens.append(n + sum(d.stub_len - (d.span_end - d.span_start) for d in w.dirs if d.seq == b))
-    bt_stride = max(max(old_pages), max(-(-n // P) for n in new_lens))
+    bt_stride = paged_bt_stride(w)
     n_used = sum(old_pages)
     n_pool = n_used + fresh_page_bound(w) + spare_pages
     perm = rng.permutation(n_pool).astype(np.int32)
