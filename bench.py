@@ -31,6 +31,7 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2606_01065_amd", "csrc", "kernels.hip")
 PROFILES = os.path.join(ROOT, "profiles")
 CONTIG_KERNEL = "contig_move_kernel"
 PAGED_KERNEL = "paged_move_kernel"
+PAGED_REMAP_KERNEL = "paged_remap_kernel"
 COPY_KERNEL_HINT = "elementwise"        # torch's device copy kernel used for counter calibration
 
 
@@ -114,7 +115,9 @@ def paged_bytes(wl, kinds, new_lens, bt_stride, L):
             seg_end = mine[j + 1].span_start if j + 1 < len(mine) else n
             if shift != 0:
                 moved += seg_end - d.span_end
-    return 2 * wl.n_layers * (asm_rows * rb + remap_rows * rot_b), moved
+    asm_b, remap_b = 2 * wl.n_layers * asm_rows * rb, 2 * wl.n_layers * remap_rows * rot_b
+    kernel = PAGED_KERNEL if asm_b >= remap_b else PAGED_REMAP_KERNEL
+    return asm_b + remap_b, moved, kernel
 
 
 COPY_CAP = 1 << 31          # bytes per side of the reference / calibration copy
@@ -267,7 +270,7 @@ def setup_paged(wl, dev, L, W, specs, stream):
     freed = torch.empty(max(1, n_freed), dtype=torch.int32, device=dev)
     ws = torch.empty(max(256, ws_bytes), dtype=torch.uint8, device=dev)
     kinds, _, _, _ = L.leyline_paged_plan(wl.page_size, wl.seq_lens, dirs, nd, bt_stride, max(1, n_freed))
-    alg_bytes, moved = paged_bytes(wl, kinds, new_lens, bt_stride, L)
+    alg_bytes, moved, kernel = paged_bytes(wl, kinds, new_lens, bt_stride, L)
 
     # The paged splice reads old pages and writes fresh ones; re-running it on the same inputs
     # repeats the same work (remapped pages are rotated again, which does not change the bytes).
@@ -276,9 +279,9 @@ def setup_paged(wl, dev, L, W, specs, stream):
 
     keep = dict(paged=True)
     torch.cuda.synchronize()
-    # one gather launch per splice carries the bytes; the row-table and block-table kernels
-    # around it take about 10 us and are inside the timed splice
-    return step, PAGED_KERNEL, alg_bytes, moved, 1, keep
+    # one gather (or, on token-slot caches, one in-place rotation) launch per splice carries the
+    # bytes; the row-table and block-table kernels around it are inside the timed splice
+    return step, kernel, alg_bytes, moved, 1, keep
 
 
 def cpu_baseline(wl, keep, budget_s, moved):
@@ -359,7 +362,18 @@ def summarize(args):
     trace_dir, fetch_dir, write_dir = args.summarize
     import workloads as W
     wl = W.WORKLOADS[args.workload]()
-    kernel = PAGED_KERNEL if wl.page_size else CONTIG_KERNEL
+    if wl.page_size:
+        from paper_2606_01065_amd import leyline as L
+        bt_stride = W.paged_bt_stride(wl)
+        dirs = L.make_directives([dict(span_start=d.span_start, span_end=d.span_end, seq=d.seq,
+                                       stub_len=d.stub_len, stub=None) for d in wl.dirs])
+        new_lens = W.paged_new_lens(wl)
+        kinds, _, _, _ = L.leyline_paged_plan(wl.page_size, wl.seq_lens, dirs, len(wl.dirs), bt_stride,
+                                              sum(-(-n // wl.page_size) for n in wl.seq_lens))
+        alg, _, kernel = paged_bytes(wl, kinds, new_lens, bt_stride, L)
+    else:
+        alg, _ = contig_bytes(wl)
+        kernel = CONTIG_KERNEL
     splices = _flag(args.command, "--steps", 100) + _flag(args.command, "--warmup", 10)
     stats = _read_csv(trace_dir, "kernel_stats")
     trace = _read_csv(trace_dir, "kernel_trace")
@@ -374,17 +388,6 @@ def summarize(args):
     # calibration copies: the device copies the bench issues after its last splice
     f_c = _counter_per_dispatch(fetch, "FETCH_SIZE", is_copy, _last_dispatch(fetch, is_k))
     w_c = _counter_per_dispatch(write, "WRITE_SIZE", is_copy, _last_dispatch(write, is_k))
-    if wl.page_size:
-        from paper_2606_01065_amd import leyline as L
-        bt_stride = W.paged_bt_stride(wl)
-        dirs = L.make_directives([dict(span_start=d.span_start, span_end=d.span_end, seq=d.seq,
-                                       stub_len=d.stub_len, stub=None) for d in wl.dirs])
-        new_lens = W.paged_new_lens(wl)
-        kinds, _, _, _ = L.leyline_paged_plan(wl.page_size, wl.seq_lens, dirs, len(wl.dirs), bt_stride,
-                                              sum(-(-n // wl.page_size) for n in wl.seq_lens))
-        alg, _ = paged_bytes(wl, kinds, new_lens, bt_stride, L)
-    else:
-        alg, _ = contig_bytes(wl)
     # calibration: the bench's 11 device copies each read and write copy_half(alg) bytes
     half = copy_half(alg)
     cal_f = (11 * half / (sum(f_c) * 1024)) if (half and f_c) else None

@@ -241,7 +241,8 @@ int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, const int32
  * offset with page < capacity.  rows: device int64 [n_rows] (nullable: then rows row0 ..
  * row0+n_rows-1).  Listed rows must be distinct.  device_status as above (out-of-range listed
  * rows are skipped and flagged with LEYLINE_STATUS_BAD_ROW).
- * Errors: E_INVAL, E_RANGE (row0 range outside the cache), E_HIP.
+ * Errors: E_INVAL (also: a paged pool of 2^31 or more rows, or more than 2^31 band chunks in one
+ * plane's call), E_RANGE (row0 range outside the cache), E_HIP.
  */
 int leyline_rotate_delta(const leyline_cache* cache, int64_t delta,
                          const int64_t* rows, int64_t row0, int64_t n_rows,

@@ -236,7 +236,28 @@ __device__ __forceinline__ void move_row_unit(const KPlane& pl, const char* src,
     st16(dst + off, v);
 }
 
-// Rotary-only kernels: band index q of one row (bands of consecutive heads back to back).
+// Rotary-only kernels.  Band unit q of a row (bands of consecutive heads back to back) is chunk
+// j = q mod band_tpr of head h = q / band_tpr; in two-chunk mode (half-split bands without lane
+// exchange) it covers the low-half chunk j and its partner.
+template <int ESZ>
+__device__ __forceinline__ void rotate_band_chunk(const KPlane& pl, u32x4& v, int32_t j, const KCosSin* table,
+                                                  int32_t cs) {
+    constexpr int EPC = Elt<ESZ>::EPC;
+    if (pl.rot == KROT_INTERLEAVED) {
+        rot_interleaved<ESZ>(v, table, cs + j * (EPC / 2));
+    } else {
+        const int32_t half = pl.rot_chunks >> 1;
+        const bool lo = j < half;
+        const int lane = int(threadIdx.x & 63);
+        const int partner = lo ? lane + half : lane - half;
+        u32x4 o;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[i]), partner, 64));
+        if (lo) rot_halves<ESZ>(v, o, table, cs + j * EPC);
+        else rot_halves<ESZ>(o, v, table, cs + (j - half) * EPC);
+    }
+}
+
 template <int ESZ>
 __device__ __forceinline__ void move_band(const KPlane& pl, const char* src, char* dst, int32_t q,
                                           const KCosSin* table, int32_t cs) {
@@ -253,20 +274,63 @@ __device__ __forceinline__ void move_band(const KPlane& pl, const char* src, cha
         return;
     }
     u32x4 v = ld16(src + a);
-    if (pl.rot == KROT_INTERLEAVED) {
-        rot_interleaved<ESZ>(v, table, cs + j * (EPC / 2));
-    } else {
-        const int32_t half = pl.rot_chunks >> 1;
-        const bool lo = j < half;
-        const int lane = int(threadIdx.x & 63);
-        const int partner = lo ? lane + half : lane - half;
-        u32x4 o;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[i]), partner, 64));
-        if (lo) rot_halves<ESZ>(v, o, table, cs + j * EPC);
-        else rot_halves<ESZ>(o, v, table, cs + (j - half) * EPC);
-    }
+    rotate_band_chunk<ESZ>(pl, v, j, table, cs);
     st16(dst + a, v);
+}
+
+// Band unit q of one row in nl <= PAGED_LPT layers (row, row + lstride, ...), rotated in place:
+// every layer's loads are issued (band_load) before the cos/sin table is needed and before the
+// first store (band_rotate_store).
+struct BandPos {
+    int64_t a, b;    // byte offsets of the unit's chunk and (two-chunk mode) of its partner
+    int32_t j;       // chunk index within the head's band
+    bool two;
+};
+
+__device__ __forceinline__ BandPos band_pos(const KPlane& pl, int32_t q) {
+    BandPos p;
+    const int32_t h = fdiv(q, pl.band_div);
+    p.j = q - h * pl.band_tpr;
+    p.a = (int64_t(h) * pl.head_chunks + pl.rot_lo + p.j) * 16;
+    p.two = pl.rot == KROT_NEOX && pl.band_tpr != pl.rot_chunks;
+    p.b = p.a + int64_t(pl.rot_chunks / 2) * 16;
+    return p;
+}
+
+__device__ __forceinline__ void band_load(const BandPos& p, const char* row, int64_t lstride, int nl,
+                                          u32x4 (&x)[PAGED_LPT], u32x4 (&y)[PAGED_LPT]) {
+#pragma unroll
+    for (int l = 0; l < PAGED_LPT; ++l) {
+        if (l < nl) {
+            x[l] = ld16(row + l * lstride + p.a);
+            if (p.two) y[l] = ld16(row + l * lstride + p.b);
+        }
+    }
+}
+
+template <int ESZ>
+__device__ __forceinline__ void band_rotate_store(const KPlane& pl, const BandPos& p, char* row,
+                                                  int64_t lstride, int nl, u32x4 (&x)[PAGED_LPT],
+                                                  u32x4 (&y)[PAGED_LPT], const KCosSin* table, int32_t cs) {
+    constexpr int EPC = Elt<ESZ>::EPC;
+#pragma unroll
+    for (int l = 0; l < PAGED_LPT; ++l) {
+        if (l < nl) {
+            if (p.two) {
+                rot_halves<ESZ>(x[l], y[l], table, cs + p.j * EPC);
+                st16(row + l * lstride + p.b, y[l]);
+            } else {
+                rotate_band_chunk<ESZ>(pl, x[l], p.j, table, cs);
+            }
+            st16(row + l * lstride + p.a, x[l]);
+        }
+    }
+}
+
+// cos/sin block of one shift (n entries from table[c0]) staged in LDS by the whole workgroup.
+template <int NT>
+__device__ __forceinline__ void stage_cs(KCosSin* lcs, const KCosSin* table, int32_t c0, int32_t n) {
+    for (int i = threadIdx.x; i < n; i += NT) lcs[i] = table[c0 + i];
 }
 
 // --------------------------------------------------------------------- contiguous splice ---
@@ -383,30 +447,40 @@ __global__ __launch_bounds__(TPB) void contig_chain_kernel(const KContigParams P
 
 // ------------------------------------------------------------------------ rotate in place ---
 
+// In-place R(delta) on listed rows: band units of all rows laid end to end, one plane per
+// blockIdx.z, PAGED_LPT layers per thread, the shift's cos/sin staged in LDS.
 template <int ESZ>
-__global__ __launch_bounds__(TPB) void rotate_rows_kernel(const KRotateParams P) {
-    const int layer = blockIdx.y;
-    const int64_t t = int64_t(blockIdx.x) * TPB + threadIdx.x;
-    const int64_t i = t / P.units_per_row;
-    if (i >= P.n_rows) return;
-    int32_t q = int32_t(t - i * P.units_per_row);
-    int p = 0;
-    while (p < P.n_planes - 1 && q >= P.planes[p].rot_tpr) {
-        q -= P.planes[p].rot_tpr;
-        ++p;
+__global__ __launch_bounds__(PAGED_TPB) void rotate_rows_kernel(const KRotateParams P) {
+    __shared__ KCosSin lcs[KMAX_CS];
+    const int plane = blockIdx.z;
+    const KPlane& pl = P.planes[plane];
+    if (pl.rot_tpr == 0) return;
+    const int32_t tb = int32_t(blockIdx.x) * PAGED_TPB;
+    if (int64_t(tb) >= P.n_rows * pl.rot_tpr) return;                  // past this plane
+    const int32_t t = tb + int32_t(threadIdx.x);
+    const int32_t i = fdiv(t, P.rot_div[plane]), q = t - i * pl.rot_tpr;
+    bool active = i < P.n_rows;
+    int64_t row = active ? (P.rows ? P.rows[i] : P.row0 + i) : 0;
+    if (active && (row < 0 || row >= P.total_rows)) {
+        if (P.status && q == 0 && plane == 0 && blockIdx.y == 0) atomicOr(P.status, int(LEYLINE_STATUS_BAD_ROW));
+        active = false;
     }
-    const KPlane& pl = P.planes[p];
-    const int64_t row = P.rows ? P.rows[i] : P.row0 + i;
-    if (row < 0 || row >= P.total_rows) {
-        if (P.status && q == 0 && p == 0) atomicOr(P.status, int(LEYLINE_STATUS_BAD_ROW));
-        return;
-    }
-    char* r = pl.base + int64_t(layer) * pl.layer_stride;
-    if (P.page_size > 0)
-        r += (row / P.page_size) * pl.page_stride + (row % P.page_size) * pl.token_stride;
-    else
+    const int layer0 = int(blockIdx.y) * PAGED_LPT;
+    const int nl = min(PAGED_LPT, P.n_layers - layer0);
+    char* r = pl.base + int64_t(layer0) * pl.layer_stride;
+    if (P.page_size > 0) {
+        const int32_t pg = fdiv(int32_t(row), P.page_div);
+        r += int64_t(pg) * pl.page_stride + (row - int64_t(pg) * P.page_size) * pl.token_stride;
+    } else {
         r += row * pl.token_stride;
-    move_band<ESZ>(pl, r, r, q, P.cs, pl.cs_off);
+    }
+    const BandPos bp = band_pos(pl, q);
+    u32x4 x[PAGED_LPT], y[PAGED_LPT];
+    if (active) band_load(bp, r, pl.layer_stride, nl, x, y);
+    stage_cs<PAGED_TPB>(lcs, P.cs, pl.cs_off, pl.n_pairs);
+    __syncthreads();
+    if (!active) return;
+    band_rotate_store<ESZ>(pl, bp, r, pl.layer_stride, nl, x, y, lcs, 0);
 }
 
 // ------------------------------------------------------------------------------ paged splice ---
@@ -420,16 +494,47 @@ __global__ __launch_bounds__(TPB) void rotate_rows_kernel(const KRotateParams P)
 // Nothing is written to an old page except the rotary bands of REMAP pages, which no ASSEMBLE
 // row reads.
 
+// The run holding ordinal x among n runs sorted by ord0 (runs[0].ord0 <= x).
+__device__ __forceinline__ int32_t run_of(const KPageRun* runs, int32_t n, int32_t x) {
+    int32_t lo = 0, hi = n;
+    while (hi - lo > 1) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (runs[mid].ord0 <= x) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ void resolve_remap_page(const KPagedParams& P, int32_t m) {
+    const KPageRun R = P.remap_runs[run_of(P.remap_runs, P.n_remap_runs, m)];
+    const int32_t c = m - R.ord0;
+    const KSeqEntry S = P.seqs[R.seq];
+    const KDirEntry& D = P.dirs[R.dir];
+    KRemapPage e{0, D.cs, 0, 0};
+    const int32_t pg = P.bt_in[int64_t(R.seq) * P.bt_stride + R.src0 + c];
+    if (pg < 0 || pg >= P.capacity) {
+        if (P.status) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
+    } else if (D.cs >= 0) {
+        e.page = pg;
+        e.rows = int32_t(min(int64_t(P.page_size), int64_t(S.new_len) - int64_t(R.k0 + c) * P.page_size));
+    }
+    P.remap_pages[m] = e;
+}
+
+// Threads [0, n_rows) resolve ASSEMBLE rows, threads [n_rows, n_rows + n_remap) REMAP pages.
 __global__ __launch_bounds__(TPB) void paged_rows_kernel(const KPagedParams P) {
     const int32_t i = int32_t(blockIdx.x) * TPB + int32_t(threadIdx.x);
-    if (i >= P.n_rows) return;
-    const int32_t task = i / P.page_size, r = i - task * P.page_size;
-    const KAssembleTask T = P.asm_tasks[task];
-    const KSeqEntry S = P.seqs[T.seq];
-    const int64_t q = int64_t(T.k) * P.page_size + r;
+    if (i >= P.n_rows) {
+        if (i - P.n_rows < P.n_remap) resolve_remap_page(P, i - P.n_rows);
+        return;
+    }
+    const int32_t task = i / P.page_size, r = i - task * P.page_size;   // task = fresh ordinal
+    const KPageRun R = P.asm_runs[run_of(P.asm_runs, P.n_asm_runs, task)];
+    const int32_t seq = R.seq, k = R.k0 + (task - R.ord0);
+    const KSeqEntry S = P.seqs[seq];
+    const int64_t q = int64_t(k) * P.page_size + r;
     KRowMove e{KROW_SKIP, 0, 0, r, -1, -1};
     if (q < S.new_len) {
-        const int32_t fp = T.fresh < P.n_free ? P.free_pages[T.fresh] : -1;
+        const int32_t fp = task < P.n_free ? P.free_pages[task] : -1;
         if (fp < 0 || fp >= P.capacity) {
             if (P.status) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
         } else {
@@ -455,7 +560,7 @@ __global__ __launch_bounds__(TPB) void paged_rows_kernel(const KPagedParams P) {
                 }
             }
             if (old >= 0) {
-                const int32_t pg = P.bt_in[int64_t(T.seq) * P.bt_stride + old / P.page_size];
+                const int32_t pg = P.bt_in[int64_t(seq) * P.bt_stride + old / P.page_size];
                 if (pg < 0 || pg >= P.capacity) {
                     if (P.status) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
                     e.src_page = KROW_SKIP;
@@ -471,14 +576,16 @@ __global__ __launch_bounds__(TPB) void paged_rows_kernel(const KPagedParams P) {
 
 template <int ESZ>
 __global__ __launch_bounds__(PAGED_TPB) void paged_move_kernel(const KPagedParams P) {
+    __shared__ KCosSin lcs[KMAX_CS];
     const int plane = blockIdx.z;
     const KPlane& pl = P.planes[plane];
-    if (int64_t(blockIdx.x) * PAGED_TPB >= int64_t(P.n_rows) * pl.tpr) return;   // past this plane
-    const int32_t t = int32_t(blockIdx.x) * PAGED_TPB + int32_t(threadIdx.x);
+    const int32_t tb = int32_t(blockIdx.x) * PAGED_TPB;
+    if (int64_t(tb) >= int64_t(P.n_rows) * pl.tpr) return;            // past this plane
+    const int32_t t = tb + int32_t(threadIdx.x);
     const int32_t i = fdiv(t, pl.tpr_div), u = t - i * pl.tpr;
-    if (i >= P.n_rows) return;
-    const KRowMove e = P.rows[i];
-    if (e.src_page == KROW_SKIP) return;
+    KRowMove e{KROW_SKIP, 0, 0, 0, -1, -1};
+    if (i < P.n_rows) e = P.rows[i];
+    const bool active = e.src_page != KROW_SKIP;
     // PAGED_LPT consecutive layers per thread: one row entry, all loads in flight before any store.
     const int layer0 = int(blockIdx.y) * PAGED_LPT;
     const int nl = min(PAGED_LPT, P.n_layers - layer0);
@@ -496,65 +603,101 @@ __global__ __launch_bounds__(PAGED_TPB) void paged_move_kernel(const KPagedParam
     char* dst = pl.base + int64_t(layer0) * pl.layer_stride + int64_t(e.dst_page) * pl.page_stride +
                 int64_t(e.dst_row) * pl.token_stride;
     const int32_t cs = e.cs >= 0 ? e.cs + pl.cs_off : -1;
-    if (pl.rot == KROT_NEOX && !pl.neox_lanes) {
-        for (int l = 0; l < nl; ++l) move_row_unit<ESZ>(pl, src + l * src_step, dst + l * pl.layer_stride, u, P.cs, cs);
+    if (pl.rot == KROT_NEOX && !pl.neox_lanes) {        // two-chunk units (rare layouts)
+        if (active)
+            for (int l = 0; l < nl; ++l)
+                move_row_unit<ESZ>(pl, src + l * src_step, dst + l * pl.layer_stride, u, P.cs, cs);
         return;
     }
     const int64_t off = int64_t(u) * 16;
     u32x4 v[PAGED_LPT];
+    if (active) {
 #pragma unroll
-    for (int l = 0; l < PAGED_LPT; ++l)
-        if (l < nl) v[l] = ld16(src + l * src_step + off);
+        for (int l = 0; l < PAGED_LPT; ++l)
+            if (l < nl) v[l] = ld16(src + l * src_step + off);
+    }
+    // the cos/sin block of the workgroup's first row's shift, staged while the loads are in flight
+    const int32_t cs0 = pl.rot != KROT_NONE ? P.rows[fdiv(tb, pl.tpr_div)].cs : -1;
+    if (cs0 >= 0) stage_cs<PAGED_TPB>(lcs, P.cs, cs0 + pl.cs_off, pl.n_pairs);
+    __syncthreads();
+    if (!active) return;
+    const bool rot = cs >= 0 && pl.rot != KROT_NONE;
 #pragma unroll
     for (int l = 0; l < PAGED_LPT; ++l) {
         if (l < nl) {
-            if (cs >= 0 && pl.rot != KROT_NONE) rotate_chunk<ESZ>(pl, v[l], u, P.cs, cs);
+            if (rot) {
+                if (e.cs == cs0) rotate_chunk<ESZ>(pl, v[l], u, lcs, 0);
+                else rotate_chunk<ESZ>(pl, v[l], u, P.cs, cs);
+            }
             st16(dst + l * pl.layer_stride + off, v[l]);
         }
     }
 }
 
+// REMAP pages: band units of all valid rows of all REMAP pages laid end to end, PAGED_LPT layers
+// per thread, rotated in place.  The workgroup stages the cos/sin block of its first page's shift
+// in LDS; rows with another shift (where runs meet) read the table in the workspace.
 template <int ESZ>
-__global__ __launch_bounds__(TPB) void paged_remap_kernel(const KPagedParams P) {
+__global__ __launch_bounds__(PAGED_TPB) void paged_remap_kernel(const KPagedParams P) {
+    __shared__ KCosSin lcs[KMAX_CS];
     const int plane = blockIdx.z;
     const KPlane& pl = P.planes[plane];
     if (pl.rot_tpr == 0) return;
-    const int layer = blockIdx.y;
-    const int task = blockIdx.x / P.remap_slices, slice = blockIdx.x - task * P.remap_slices;
-    const KRemapTask T = P.remap_tasks[task];
-    const KSeqEntry S = P.seqs[T.seq];
-    const KDirEntry& D = P.dirs[T.dir];
-    if (D.cs < 0) return;
-    const int64_t lo = int64_t(T.k) * P.page_size;
-    const int32_t valid = int32_t(min(int64_t(P.page_size), int64_t(S.new_len) - lo));
-    const int32_t f = slice * TPB + int32_t(threadIdx.x);
-    if (f >= valid * pl.rot_tpr) return;
-    const int32_t pg = P.bt_in[int64_t(T.seq) * P.bt_stride + T.src_page];
-    if (pg < 0 || pg >= P.capacity) {
-        if (P.status) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
-        return;
-    }
-    const int32_t r = f / pl.rot_tpr;
-    char* row = pl.base + int64_t(layer) * pl.layer_stride + int64_t(pg) * pl.page_stride +
+    const int32_t upp = P.page_size * pl.rot_tpr;
+    const int32_t tb = int32_t(blockIdx.x) * PAGED_TPB;
+    if (int64_t(tb) >= int64_t(P.n_remap) * upp) return;               // past this plane
+    const int32_t t = tb + int32_t(threadIdx.x);
+    const int32_t m = fdiv(t, P.remap_div[plane]);
+    const int32_t cs0 = P.remap_pages[fdiv(tb, P.remap_div[plane])].cs;   // block's first page
+    bool active = m < P.n_remap;
+    KRemapPage e{0, -1, 0, 0};
+    if (active) e = P.remap_pages[m];
+    const int32_t f = t - m * upp;
+    const int32_t r = fdiv(f, P.rot_div[plane]);
+    active = active && r < e.rows;
+    const int layer0 = int(blockIdx.y) * PAGED_LPT;
+    const int nl = min(PAGED_LPT, P.n_layers - layer0);
+    char* row = pl.base + int64_t(layer0) * pl.layer_stride + int64_t(e.page) * pl.page_stride +
                 int64_t(r) * pl.token_stride;
-    move_band<ESZ>(pl, row, row, f - r * pl.rot_tpr, P.cs, D.cs + pl.cs_off);
+    const BandPos bp = band_pos(pl, f - r * pl.rot_tpr);
+    u32x4 x[PAGED_LPT], y[PAGED_LPT];
+    if (active) band_load(bp, row, pl.layer_stride, nl, x, y);
+    if (cs0 >= 0) stage_cs<PAGED_TPB>(lcs, P.cs, cs0 + pl.cs_off, pl.n_pairs);
+    __syncthreads();
+    if (!active) return;
+    if (e.cs == cs0) band_rotate_store<ESZ>(pl, bp, row, pl.layer_stride, nl, x, y, lcs, 0);
+    else band_rotate_store<ESZ>(pl, bp, row, pl.layer_stride, nl, x, y, P.cs, e.cs + pl.cs_off);
 }
 
-// New block tables and the freed-page list, resolved from the symbolic plan.
+// New block tables and the freed-page list, expanded from the page runs.
 __global__ __launch_bounds__(TPB) void paged_tables_kernel(const KTableParams P) {
     const int64_t i = int64_t(blockIdx.x) * TPB + threadIdx.x;
-    if (i < P.n_pages) {
-        const KPageEntry e = P.pages[i];
-        const int64_t row = i / P.bt_stride;
+    const int64_t n_pages = int64_t(P.n_seqs) * P.bt_stride;
+    if (i < n_pages) {
+        const int32_t b = int32_t(i / P.bt_stride), k = int32_t(i - int64_t(b) * P.bt_stride);
+        const KSeqEntry S = P.seqs[b];
         int32_t v = -1;
-        if (e.kind == LEYLINE_PAGE_IDENTITY || e.kind == LEYLINE_PAGE_REMAP)
-            v = P.bt_in[row * P.bt_stride + e.src];
-        else if (e.kind == LEYLINE_PAGE_ASSEMBLE)
-            v = e.src < P.n_free ? P.free_pages[e.src] : -1;
+        if (S.run_count > 0 && int64_t(k) * P.page_size < S.new_len) {
+            int32_t lo = S.run_begin, hi = S.run_begin + S.run_count;
+            while (hi - lo > 1) {
+                const int32_t mid = (lo + hi) >> 1;
+                if (P.runs[mid].k0 <= k) lo = mid; else hi = mid;
+            }
+            const KPageRun R = P.runs[lo];
+            const int32_t src = R.src0 + (k - R.k0);
+            if (R.kind == LEYLINE_PAGE_ASSEMBLE) v = src < P.n_free ? P.free_pages[src] : -1;
+            else v = P.bt_in[int64_t(b) * P.bt_stride + src];
+        }
         P.bt_out[i] = v;
-    } else if (i < int64_t(P.n_pages) + P.n_freed) {
-        const KFreedEntry f = P.freed[i - P.n_pages];
-        P.freed_out[i - P.n_pages] = P.bt_in[int64_t(f.seq) * P.bt_stride + f.page];
+    } else if (i < n_pages + P.n_freed) {
+        const int32_t f = int32_t(i - n_pages);
+        int32_t lo = 0, hi = P.n_freed_runs;
+        while (hi - lo > 1) {
+            const int32_t mid = (lo + hi) >> 1;
+            if (P.freed[mid].out0 <= f) lo = mid; else hi = mid;
+        }
+        const KFreedRun R = P.freed[lo];
+        P.freed_out[f] = P.bt_in[int64_t(R.seq) * P.bt_stride + R.page0 + (f - R.out0)];
     }
 }
 
@@ -717,41 +860,35 @@ extern "C" int leyline_rotate_delta(const leyline_cache* cache, int64_t delta,
     if (n_rows < 0) return LEYLINE_E_INVAL;
     const int64_t total_rows = paged ? cache->capacity * cache->page_size : cache->capacity;
     if (!rows && (row0 < 0 || row0 > total_rows || n_rows > total_rows - row0)) return LEYLINE_E_RANGE;
+    if (n_rows == 0 || delta == 0) return LEYLINE_OK;   // R(0) is the identity
+    if (paged && total_rows > INT32_MAX) return LEYLINE_E_INVAL;
     KRotateParams P;
     std::memset(&P, 0, sizeof(P));
-    // The rotary bands of all planes are laid end to end per row.  With more than one rotary
-    // plane a band may start off its alignment, so half-split bands then use two-chunk units.
-    int n_rot = 0;
-    for (int p = 0; p < n_planes; ++p) n_rot += planes[p].rot_tpr > 0;
-    if (n_rot > 1)
-        for (int p = 0; p < n_planes; ++p)
-            if (planes[p].rot == KROT_NEOX && planes[p].band_tpr == planes[p].rot_chunks) {
-                planes[p].band_tpr = planes[p].rot_chunks / 2;
-                planes[p].rot_tpr = planes[p].n_heads * planes[p].band_tpr;
-                planes[p].band_div = make_div(planes[p].band_tpr);
-            }
-    int32_t upr = 0;
-    for (int p = 0; p < n_planes; ++p) upr += planes[p].rot_tpr;
-    if (n_rows == 0 || upr == 0 || delta == 0) return LEYLINE_OK;   // R(0) is the identity
+    int32_t max_rot = 0;
+    for (int p = 0; p < n_planes; ++p) {
+        max_rot = std::max(max_rot, planes[p].rot_tpr);
+        P.rot_div[p] = make_div(std::max(1, planes[p].rot_tpr));
+        if (n_rows * planes[p].rot_tpr > INT32_MAX - 1024) return LEYLINE_E_INVAL;
+    }
+    if (max_rot == 0) return LEYLINE_OK;
     std::memcpy(P.planes, planes, sizeof(planes));
     P.n_planes = n_planes;
     P.n_layers = cache->n_layers;
     P.page_size = paged ? cache->page_size : 0;
+    P.page_div = make_div(paged ? cache->page_size : 1);
     P.total_rows = total_rows;
     P.rows = rows;
     P.row0 = row0;
     P.n_rows = n_rows;
     P.status = device_status;
-    P.units_per_row = upr;
     std::vector<KCosSin> cs;
     append_cos_sin(cache, delta, cs);
     std::copy(cs.begin(), cs.end(), P.cs);
-    const int64_t blocks = (n_rows * upr + TPB - 1) / TPB;
-    if (blocks > INT32_MAX) return LEYLINE_E_INVAL;
-    const dim3 grid(unsigned(blocks), unsigned(cache->n_layers));
+    const int64_t blocks = (n_rows * max_rot + PAGED_TPB - 1) / PAGED_TPB;
+    const dim3 grid(unsigned(blocks), unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT), unsigned(n_planes));
     hipStream_t s = static_cast<hipStream_t>(stream);
-    return cache->dtype == LEYLINE_BF16 ? launch(rotate_rows_kernel<2>, grid, s, P)
-                                        : launch(rotate_rows_kernel<4>, grid, s, P);
+    return cache->dtype == LEYLINE_BF16 ? launch(rotate_rows_kernel<2>, grid, s, P, PAGED_TPB)
+                                        : launch(rotate_rows_kernel<4>, grid, s, P, PAGED_TPB);
 }
 
 extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, const int32_t* seq_lens,
@@ -775,9 +912,9 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
     rc = check_table_width(plan, seq_lens, bt_stride);
     if (rc) return rc;
     if (plan.n_fresh > n_free) return LEYLINE_E_CAPACITY;
-    if (int64_t(plan.freed_page.size()) > freed_cap) return LEYLINE_E_CAPACITY;
+    if (plan.n_freed > freed_cap) return LEYLINE_E_CAPACITY;
     if (plan.n_fresh > 0 && !free_pages) return LEYLINE_E_INVAL;
-    if (!plan.freed_page.empty() && !freed_pages_out) return LEYLINE_E_INVAL;
+    if (plan.n_freed > 0 && !freed_pages_out) return LEYLINE_E_INVAL;
     PagedImage img;
     rc = build_paged_image(cache, plan, n_seqs, dirs, n_dirs, bt_stride, &img);
     if (rc) return rc;
@@ -787,8 +924,11 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
     hipStream_t s = static_cast<hipStream_t>(stream);
     const KPagedTables& t = img.tables;
     char* ws = static_cast<char*>(workspace);
-    for (int p = 0; p < n_planes; ++p)
+    if (int64_t(t.n_rows) + t.n_remap > INT32_MAX - 1024) return LEYLINE_E_INVAL;
+    for (int p = 0; p < n_planes; ++p) {
         if (int64_t(t.n_rows) * planes[p].tpr > INT32_MAX - 1024) return LEYLINE_E_INVAL;
+        if (int64_t(t.n_remap) * cache->page_size * planes[p].rot_tpr > INT32_MAX - 1024) return LEYLINE_E_INVAL;
+    }
     if (t.upload > 0) {
         rc = hip_status(hipMemcpyAsync(ws, img.bytes.data(), size_t(t.upload), hipMemcpyHostToDevice, s));
         if (rc) return rc;
@@ -804,27 +944,32 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         P.n_asm = t.n_asm;
         P.n_remap = t.n_remap;
         P.n_rows = t.n_rows;
-        int32_t remap_slices = 1, max_tpr = 1;
+        int32_t max_tpr = 1, max_upp = 1;
         for (int p = 0; p < n_planes; ++p) {
-            remap_slices = std::max(remap_slices, (cache->page_size * planes[p].rot_tpr + TPB - 1) / TPB);
+            const int32_t upp = cache->page_size * planes[p].rot_tpr;
             max_tpr = std::max(max_tpr, planes[p].tpr);
+            max_upp = std::max(max_upp, upp);
+            P.remap_div[p] = make_div(std::max(1, upp));
+            P.rot_div[p] = make_div(std::max(1, planes[p].rot_tpr));
         }
-        P.remap_slices = remap_slices;
         P.capacity = cache->capacity;
         P.seqs = reinterpret_cast<const KSeqEntry*>(ws + t.off_seq);
         P.dirs = reinterpret_cast<const KDirEntry*>(ws + t.off_dir);
         P.cs = reinterpret_cast<const KCosSin*>(ws + t.off_cs);
-        P.asm_tasks = reinterpret_cast<const KAssembleTask*>(ws + t.off_asm);
-        P.remap_tasks = reinterpret_cast<const KRemapTask*>(ws + t.off_remap);
+        P.asm_runs = reinterpret_cast<const KPageRun*>(ws + t.off_asm_runs);
+        P.remap_runs = reinterpret_cast<const KPageRun*>(ws + t.off_remap_runs);
+        P.n_asm_runs = t.n_asm_runs;
+        P.n_remap_runs = t.n_remap_runs;
         P.rows = reinterpret_cast<KRowMove*>(ws + t.off_rows);
+        P.remap_pages = reinterpret_cast<KRemapPage*>(ws + t.off_remap_pages);
         P.bt_in = block_table_in;
         P.free_pages = free_pages;
         P.n_free = n_free;
         P.status = device_status;
         const bool bf16 = cache->dtype == LEYLINE_BF16;
+        rc = launch(paged_rows_kernel, dim3(unsigned((int64_t(t.n_rows) + t.n_remap + TPB - 1) / TPB)), s, P);
+        if (rc) return rc;
         if (t.n_rows > 0) {
-            rc = launch(paged_rows_kernel, dim3(unsigned((t.n_rows + TPB - 1) / TPB)), s, P);
-            if (rc) return rc;
             const int64_t blocks = (int64_t(t.n_rows) * max_tpr + PAGED_TPB - 1) / PAGED_TPB;
             const dim3 grid(unsigned(blocks), unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT),
                             unsigned(n_planes));
@@ -833,35 +978,38 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
             if (rc) return rc;
         }
         if (t.n_remap > 0) {
-            const int64_t blocks = int64_t(t.n_remap) * remap_slices;
-            if (blocks > INT32_MAX) return LEYLINE_E_INVAL;
-            const dim3 grid(unsigned(blocks), unsigned(cache->n_layers), unsigned(n_planes));
-            rc = bf16 ? launch(paged_remap_kernel<2>, grid, s, P) : launch(paged_remap_kernel<4>, grid, s, P);
+            const int64_t blocks = (int64_t(t.n_remap) * max_upp + PAGED_TPB - 1) / PAGED_TPB;
+            const dim3 grid(unsigned(blocks), unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT),
+                            unsigned(n_planes));
+            rc = bf16 ? launch(paged_remap_kernel<2>, grid, s, P, PAGED_TPB)
+                      : launch(paged_remap_kernel<4>, grid, s, P, PAGED_TPB);
             if (rc) return rc;
         }
     }
-    if (t.n_pages + t.n_freed > 0) {
+    const int64_t n_pages = int64_t(n_seqs) * bt_stride;
+    if (n_pages + t.n_freed > 0) {
         KTableParams T;
         std::memset(&T, 0, sizeof(T));
-        T.pages = reinterpret_cast<const KPageEntry*>(ws + t.off_pages);
-        T.freed = reinterpret_cast<const KFreedEntry*>(ws + t.off_freed);
+        T.seqs = reinterpret_cast<const KSeqEntry*>(ws + t.off_seq);
+        T.runs = reinterpret_cast<const KPageRun*>(ws + t.off_runs);
+        T.freed = reinterpret_cast<const KFreedRun*>(ws + t.off_freed_runs);
         T.bt_in = block_table_in;
         T.bt_out = block_table_out;
         T.free_pages = free_pages;
         T.freed_out = freed_pages_out;
-        T.status = device_status;
-        T.capacity = cache->capacity;
-        T.n_pages = t.n_pages;
-        T.n_freed = t.n_freed;
+        T.n_seqs = n_seqs;
         T.bt_stride = bt_stride;
+        T.page_size = cache->page_size;
+        T.n_freed = t.n_freed;
+        T.n_freed_runs = t.n_freed_runs;
         T.n_free = n_free;
-        const int64_t blocks = (int64_t(t.n_pages) + t.n_freed + TPB - 1) / TPB;
+        const int64_t blocks = (n_pages + t.n_freed + TPB - 1) / TPB;
         rc = launch(paged_tables_kernel, dim3(unsigned(blocks)), s, T);
         if (rc) return rc;
     }
     if (new_seq_lens_out)
         for (int32_t b = 0; b < n_seqs; ++b) new_seq_lens_out[b] = plan.new_lens[size_t(b)];
     if (n_fresh_used_out) *n_fresh_used_out = plan.n_fresh;
-    if (n_freed_out) *n_freed_out = int32_t(plan.freed_page.size());
+    if (n_freed_out) *n_freed_out = plan.n_freed;
     return LEYLINE_OK;
 }

@@ -101,14 +101,17 @@ struct KRotateParams {
     int64_t row0;
     int64_t n_rows;
     int32_t* status;         // device, nullable
-    int32_t units_per_row;   // sum of rot_tpr over planes
-    int32_t pad2;
+    KDiv rot_div[LEYLINE_MAX_PLANES];   // by rot_tpr (band units per row)
+    KDiv page_div;           // by page_size (paged caches)
     KCosSin cs[KMAX_CS];
 };
 
 // ----------------------------------------------------------------------------------- paged --
 struct KSeqEntry {
-    int32_t dir_begin, dir_count, old_len, new_len;
+    int32_t dir_begin, dir_count;   // the sequence's directives
+    int32_t new_len;
+    int32_t run_begin, run_count;   // the sequence's page runs
+    int32_t pad0, pad1, pad2;
 };
 
 struct KDirEntry {
@@ -120,12 +123,18 @@ struct KDirEntry {
     const char* stub[LEYLINE_MAX_PLANES];
 };
 
-struct KAssembleTask {
-    int32_t seq, k, fresh, pad;
+// A run of consecutive new logical pages [k0, k0 + count) of one sequence that share a kind.
+// IDENTITY and REMAP: page k0 + c re-uses old logical page src0 + c; ASSEMBLE: it takes fresh
+// ordinal src0 + c.  ord0 is the ordinal of the run's first page among all pages of its kind in
+// the call (ASSEMBLE: equal to src0); dir is the directive whose shift a REMAP run applies.
+struct KPageRun {
+    int32_t seq, k0, count, kind, src0, ord0, dir, pad;
 };
 
-struct KRemapTask {
-    int32_t seq, k, src_page, dir;
+// Old logical pages [page0, page0 + count) of one sequence that the call drops, written to
+// freed-list positions [out0, out0 + count).
+struct KFreedRun {
+    int32_t seq, page0, count, out0;
 };
 
 // One row of an ASSEMBLE page, resolved on the device from the plan and the block tables.
@@ -140,22 +149,21 @@ struct KRowMove {
 constexpr int32_t KROW_STUB = -1;
 constexpr int32_t KROW_SKIP = -2;
 
-struct KPageEntry {
-    int32_t kind, src;       // LEYLINE_PAGE_*, old logical page or fresh ordinal
-};
-
-struct KFreedEntry {
-    int32_t seq, page;
+// One REMAP page, resolved on the device: its physical page, the cos/sin entry of its shift and
+// the number of valid rows (0: nothing to rotate).
+struct KRemapPage {
+    int32_t page, cs, rows, pad;
 };
 
 // Byte offsets of the tables inside the workspace (converted to pointers at launch).
 struct KPagedTables {
-    int64_t off_seq, off_dir, off_cs, off_asm, off_remap, off_pages, off_freed, off_rows;
-    int64_t upload;          // bytes uploaded from the host (the tables before the row table)
-    int64_t total;           // workspace bytes (the row table is written on the device)
-    int32_t n_seqs, n_dirs, n_cs, n_asm, n_remap, n_pages, n_freed, bt_stride;
+    int64_t off_seq, off_dir, off_cs, off_runs, off_asm_runs, off_remap_runs, off_freed_runs;
+    int64_t off_rows, off_remap_pages;
+    int64_t upload;          // bytes uploaded from the host (the tables before the row tables)
+    int64_t total;           // workspace bytes (the row tables are written on the device)
+    int32_t n_seqs, n_dirs, n_cs, n_runs, n_asm_runs, n_remap_runs, n_freed_runs;
+    int32_t n_asm, n_remap, n_freed, bt_stride;
     int32_t n_rows;          // n_asm * page_size
-    int32_t pad;
 };
 
 struct KPagedParams {
@@ -167,34 +175,34 @@ struct KPagedParams {
     int32_t n_asm;
     int32_t n_remap;
     int32_t n_rows;          // ASSEMBLE rows (n_asm * page_size)
-    int32_t remap_slices;    // blocks per REMAP task
+    int32_t pad0;
+    KDiv remap_div[LEYLINE_MAX_PLANES];  // by page_size * rot_tpr (band units per REMAP page)
+    KDiv rot_div[LEYLINE_MAX_PLANES];    // by rot_tpr (band units per row)
     int64_t capacity;                    // physical pages
     const KSeqEntry* seqs;
     const KDirEntry* dirs;
     const KCosSin* cs;
-    const KAssembleTask* asm_tasks;
-    const KRemapTask* remap_tasks;
+    const KPageRun* asm_runs;            // ASSEMBLE runs, ascending ord0
+    const KPageRun* remap_runs;          // REMAP runs, ascending ord0
+    int32_t n_asm_runs, n_remap_runs;
     const int32_t* bt_in;
     const int32_t* free_pages;
     int32_t n_free;
     int32_t pad;
     int32_t* status;
     KRowMove* rows;          // workspace, n_rows entries
+    KRemapPage* remap_pages; // workspace, n_remap entries
 };
 
 struct KTableParams {
-    const KPageEntry* pages;   // [n_seqs * bt_stride]
-    const KFreedEntry* freed;  // [n_freed]
+    const KSeqEntry* seqs;
+    const KPageRun* runs;      // all runs, ascending (seq, k0)
+    const KFreedRun* freed;    // ascending out0
     const int32_t* bt_in;
     int32_t* bt_out;
     const int32_t* free_pages;
     int32_t* freed_out;
-    int32_t* status;
-    int64_t capacity;
-    int32_t n_pages;           // n_seqs * bt_stride
-    int32_t n_freed;
-    int32_t bt_stride;
-    int32_t n_free;
+    int32_t n_seqs, bt_stride, page_size, n_freed, n_freed_runs, n_free;
 };
 
 }  // namespace leyline

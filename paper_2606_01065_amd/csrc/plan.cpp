@@ -302,34 +302,47 @@ int plan_paged(int32_t page_size, int32_t n_seqs, const int32_t* seq_lens,
         if (dirs[j].seq < 0 || dirs[j].seq >= n_seqs) return LEYLINE_E_RANGE;
         if (j > 0 && dirs[j].seq < dirs[j - 1].seq) return LEYLINE_E_ORDER;
     }
+    const int64_t P = page_size;
     out->page_size = page_size;
     out->n_seqs = n_seqs;
-    out->new_lens.assign(n_seqs, 0);
-    out->page_seq.clear(); out->page_k.clear(); out->page_kind.clear();
-    out->page_src.clear(); out->page_dir.clear();
-    out->freed_seq.clear(); out->freed_page.clear();
-    out->n_fresh = out->n_assemble = out->n_remap = 0;
+    out->new_lens.assign(size_t(n_seqs), 0);
+    out->run_begin.assign(size_t(n_seqs) + 1, 0);
+    out->runs.clear();
+    out->freed.clear();
+    int64_t n_fresh = 0, n_remap = 0, n_freed = 0;
 
     int32_t j0 = 0;
     std::vector<Piece> pieces;
-    std::vector<char> kept;
+    std::vector<std::pair<int64_t, int64_t>> kept;   // re-used old pages [lo, hi), ascending
     for (int32_t b = 0; b < n_seqs; ++b) {
         int32_t j1 = j0;
         while (j1 < n_dirs && dirs[j1].seq == b) ++j1;
         const int64_t n = seq_lens[b];
         int rc = check_sequence(n, dirs + j0, j1 - j0, n_planes);
         if (rc) return rc;
-        // pieces in new-position order
+        // Pieces in new-position order.  Adjacent old-row pieces with the same shift (around a
+        // directive that deletes and inserts nothing) are one piece: the page rule looks at rows.
         pieces.clear();
+        auto add = [&](const Piece& p) {
+            if (!p.stub && !pieces.empty()) {
+                Piece& q = pieces.back();
+                if (!q.stub && q.hi == p.lo && q.shift == p.shift) {
+                    q.hi = p.hi;
+                    q.dir = p.dir;
+                    return;
+                }
+            }
+            pieces.push_back(p);
+        };
         int64_t shift = 0, cursor = 0, pos = 0;
         for (int32_t j = j0; j < j1; ++j) {
             const leyline_directive& d = dirs[j];
             if (d.span_start > cursor) {
-                pieces.push_back(Piece{pos, pos + d.span_start - cursor, false, shift, j > j0 ? j - 1 : -1});
+                add(Piece{pos, pos + d.span_start - cursor, false, shift, j > j0 ? j - 1 : -1});
                 pos += d.span_start - cursor;
             }
             if (d.stub_len > 0) {
-                pieces.push_back(Piece{pos, pos + d.stub_len, true, 0, j});
+                add(Piece{pos, pos + d.stub_len, true, 0, j});
                 pos += d.stub_len;
             }
             shift += d.stub_len - (d.span_end - d.span_start);
@@ -337,51 +350,64 @@ int plan_paged(int32_t page_size, int32_t n_seqs, const int32_t* seq_lens,
             if (pos > INT32_MAX) return LEYLINE_E_CAPACITY;
         }
         if (n > cursor) {
-            pieces.push_back(Piece{pos, pos + n - cursor, false, shift, j1 > j0 ? j1 - 1 : -1});
+            add(Piece{pos, pos + n - cursor, false, shift, j1 > j0 ? j1 - 1 : -1});
             pos += n - cursor;
         }
         if (pos > INT32_MAX) return LEYLINE_E_CAPACITY;
         const int64_t n_new = pos;
-        out->new_lens[b] = int32_t(n_new);
-        const int64_t old_pages = (n + page_size - 1) / page_size;
-        const int64_t new_pages = (n_new + page_size - 1) / page_size;
-        kept.assign(size_t(old_pages), 0);
-        size_t pi = 0;
-        for (int64_t k = 0; k < new_pages; ++k) {
-            const int64_t lo = k * page_size, hi = std::min<int64_t>(lo + page_size, n_new);
-            while (pi < pieces.size() && pieces[pi].hi <= lo) ++pi;
-            // pieces[pi] is the first piece overlapping [lo, hi)
-            const Piece& p = pieces[pi];
-            const bool single = p.lo <= lo && p.hi >= hi;
-            int32_t kind = LEYLINE_PAGE_ASSEMBLE, src = -1, dir = -1;
-            if (single && !p.stub && p.shift == 0) {
-                kind = LEYLINE_PAGE_IDENTITY;
-                src = int32_t(k);
-            } else if (single && !p.stub && p.shift % page_size == 0) {
-                kind = LEYLINE_PAGE_REMAP;
-                src = int32_t(k - p.shift / page_size);
-                dir = p.dir;
-            }
-            if (kind == LEYLINE_PAGE_ASSEMBLE) {
-                src = out->n_fresh++;
-                ++out->n_assemble;
+        out->new_lens[size_t(b)] = int32_t(n_new);
+        const int64_t old_pages = (n + P - 1) / P;
+        const int64_t new_pages = (n_new + P - 1) / P;
+        out->run_begin[size_t(b)] = int32_t(out->runs.size());
+        // A new page is re-used (IDENTITY for shift 0, REMAP for another multiple of the page
+        // size) when all its valid rows lie in one old-row piece whose shift keeps in-page
+        // offsets; every other page is ASSEMBLE.
+        auto assemble = [&](int64_t k0, int64_t k1) {
+            if (k1 <= k0) return;
+            out->runs.push_back(KPageRun{b, int32_t(k0), int32_t(k1 - k0), LEYLINE_PAGE_ASSEMBLE,
+                                         int32_t(n_fresh), int32_t(n_fresh), -1, 0});
+            n_fresh += k1 - k0;
+        };
+        kept.clear();
+        int64_t kcur = 0;
+        for (const Piece& p : pieces) {
+            if (p.stub || p.shift % P != 0) continue;
+            const int64_t first = (p.lo + P - 1) / P;
+            const int64_t last = p.hi == n_new ? (p.hi + P - 1) / P : p.hi / P;
+            if (first >= last) continue;
+            assemble(kcur, first);
+            const int64_t src0 = first - p.shift / P;
+            if (p.shift == 0) {
+                out->runs.push_back(KPageRun{b, int32_t(first), int32_t(last - first), LEYLINE_PAGE_IDENTITY,
+                                             int32_t(src0), 0, -1, 0});
             } else {
-                kept[size_t(src)] = 1;
-                if (kind == LEYLINE_PAGE_REMAP) ++out->n_remap;
+                out->runs.push_back(KPageRun{b, int32_t(first), int32_t(last - first), LEYLINE_PAGE_REMAP,
+                                             int32_t(src0), int32_t(n_remap), p.dir, 0});
+                n_remap += last - first;
             }
-            out->page_seq.push_back(b);
-            out->page_k.push_back(int32_t(k));
-            out->page_kind.push_back(kind);
-            out->page_src.push_back(src);
-            out->page_dir.push_back(dir);
+            kept.emplace_back(src0, src0 + (last - first));
+            kcur = last;
         }
-        for (int64_t kp = 0; kp < old_pages; ++kp)
-            if (!kept[size_t(kp)]) {
-                out->freed_seq.push_back(b);
-                out->freed_page.push_back(int32_t(kp));
+        assemble(kcur, new_pages);
+        int64_t c = 0;
+        for (const auto& r : kept) {
+            if (r.first > c) {
+                out->freed.push_back(KFreedRun{b, int32_t(c), int32_t(r.first - c), int32_t(n_freed)});
+                n_freed += r.first - c;
             }
+            c = r.second;
+        }
+        if (old_pages > c) {
+            out->freed.push_back(KFreedRun{b, int32_t(c), int32_t(old_pages - c), int32_t(n_freed)});
+            n_freed += old_pages - c;
+        }
+        if (n_fresh > INT32_MAX || n_remap > INT32_MAX || n_freed > INT32_MAX) return LEYLINE_E_CAPACITY;
         j0 = j1;
     }
+    out->run_begin[size_t(n_seqs)] = int32_t(out->runs.size());
+    out->n_fresh = int32_t(n_fresh);
+    out->n_remap = int32_t(n_remap);
+    out->n_freed = int32_t(n_freed);
     return LEYLINE_OK;
 }
 
@@ -396,36 +422,34 @@ int build_paged_image(const leyline_cache* cache, const PagedPlan& plan, int32_t
     for (int32_t b = 0; b < n_seqs; ++b) {
         int32_t j1 = j0;
         while (j1 < n_dirs && dirs[j1].seq == b) ++j1;
-        seqs[size_t(b)] = KSeqEntry{j0, j1 - j0, 0, plan.new_lens[size_t(b)]};
+        KSeqEntry& e = seqs[size_t(b)];
+        std::memset(&e, 0, sizeof(e));
+        e.dir_begin = j0;
+        e.dir_count = j1 - j0;
+        e.new_len = plan.new_lens[size_t(b)];
+        e.run_begin = plan.run_begin[size_t(b)];
+        e.run_count = plan.run_begin[size_t(b) + 1] - plan.run_begin[size_t(b)];
         int64_t shift = 0;
         for (int32_t j = j0; j < j1; ++j) {
             const leyline_directive& d = dirs[j];
-            KDirEntry& e = dtab[size_t(j)];
-            std::memset(&e, 0, sizeof(e));
-            e.stub_start = d.span_start + shift;
-            e.stub_len = d.stub_len;
+            KDirEntry& de = dtab[size_t(j)];
+            std::memset(&de, 0, sizeof(de));
+            de.stub_start = d.span_start + shift;
+            de.stub_len = d.stub_len;
             shift += d.stub_len - (d.span_end - d.span_start);
-            e.delta = shift;
-            e.cs = (shift != 0 && any_rot) ? append_cos_sin(cache, shift, cs) : -1;
+            de.delta = shift;
+            de.cs = (shift != 0 && any_rot) ? append_cos_sin(cache, shift, cs) : -1;
             for (int p = 0; p < cache->n_planes; ++p)
-                e.stub[p] = static_cast<const char*>(d.stub[p]);
+                de.stub[p] = static_cast<const char*>(d.stub[p]);
         }
         j0 = j1;
     }
-    std::vector<KAssembleTask> asm_tasks;
-    std::vector<KRemapTask> remap_tasks;
-    std::vector<KPageEntry> pages(size_t(n_seqs) * size_t(bt_stride), KPageEntry{LEYLINE_PAGE_NONE, -1});
-    for (size_t i = 0; i < plan.page_kind.size(); ++i) {
-        const int32_t b = plan.page_seq[i], k = plan.page_k[i];
-        if (k >= bt_stride) return LEYLINE_E_CAPACITY;
-        pages[size_t(b) * bt_stride + k] = KPageEntry{plan.page_kind[i], plan.page_src[i]};
-        if (plan.page_kind[i] == LEYLINE_PAGE_ASSEMBLE)
-            asm_tasks.push_back(KAssembleTask{b, k, plan.page_src[i], 0});
-        else if (plan.page_kind[i] == LEYLINE_PAGE_REMAP)
-            remap_tasks.push_back(KRemapTask{b, k, plan.page_src[i], plan.page_dir[i]});
+    std::vector<KPageRun> asm_runs, remap_runs;
+    for (const KPageRun& r : plan.runs) {
+        if (r.k0 + r.count > bt_stride) return LEYLINE_E_CAPACITY;
+        if (r.kind == LEYLINE_PAGE_ASSEMBLE) asm_runs.push_back(r);
+        else if (r.kind == LEYLINE_PAGE_REMAP) remap_runs.push_back(r);
     }
-    std::vector<KFreedEntry> freed(plan.freed_seq.size());
-    for (size_t i = 0; i < freed.size(); ++i) freed[i] = KFreedEntry{plan.freed_seq[i], plan.freed_page[i]};
 
     KPagedTables& t = img->tables;
     std::memset(&t, 0, sizeof(t));
@@ -438,18 +462,23 @@ int build_paged_image(const leyline_cache* cache, const PagedPlan& plan, int32_t
     t.off_seq = place(seqs.size() * sizeof(KSeqEntry));
     t.off_dir = place(dtab.size() * sizeof(KDirEntry));
     t.off_cs = place(cs.size() * sizeof(KCosSin));
-    t.off_asm = place(asm_tasks.size() * sizeof(KAssembleTask));
-    t.off_remap = place(remap_tasks.size() * sizeof(KRemapTask));
-    t.off_pages = place(pages.size() * sizeof(KPageEntry));
-    t.off_freed = place(freed.size() * sizeof(KFreedEntry));
+    t.off_runs = place(plan.runs.size() * sizeof(KPageRun));
+    t.off_asm_runs = place(asm_runs.size() * sizeof(KPageRun));
+    t.off_remap_runs = place(remap_runs.size() * sizeof(KPageRun));
+    t.off_freed_runs = place(plan.freed.size() * sizeof(KFreedRun));
     t.upload = off;
-    const int64_t n_rows = int64_t(asm_tasks.size()) * plan.page_size;
+    const int64_t n_rows = int64_t(plan.n_fresh) * plan.page_size;
     if (n_rows > INT32_MAX) return LEYLINE_E_CAPACITY;
     t.off_rows = place(size_t(n_rows) * sizeof(KRowMove));
+    t.off_remap_pages = place(size_t(plan.n_remap) * sizeof(KRemapPage));
     t.total = off;
     t.n_seqs = n_seqs; t.n_dirs = n_dirs; t.n_cs = int32_t(cs.size());
-    t.n_asm = int32_t(asm_tasks.size()); t.n_remap = int32_t(remap_tasks.size());
-    t.n_pages = int32_t(pages.size()); t.n_freed = int32_t(freed.size()); t.bt_stride = bt_stride;
+    t.n_runs = int32_t(plan.runs.size());
+    t.n_asm_runs = int32_t(asm_runs.size());
+    t.n_remap_runs = int32_t(remap_runs.size());
+    t.n_freed_runs = int32_t(plan.freed.size());
+    t.n_asm = plan.n_fresh; t.n_remap = plan.n_remap; t.n_freed = plan.n_freed;
+    t.bt_stride = bt_stride;
     t.n_rows = int32_t(n_rows);
     img->bytes.assign(size_t(t.upload), 0);
     auto put = [&](int64_t at, const void* src, size_t bytes) {
@@ -458,10 +487,10 @@ int build_paged_image(const leyline_cache* cache, const PagedPlan& plan, int32_t
     put(t.off_seq, seqs.data(), seqs.size() * sizeof(KSeqEntry));
     put(t.off_dir, dtab.data(), dtab.size() * sizeof(KDirEntry));
     put(t.off_cs, cs.data(), cs.size() * sizeof(KCosSin));
-    put(t.off_asm, asm_tasks.data(), asm_tasks.size() * sizeof(KAssembleTask));
-    put(t.off_remap, remap_tasks.data(), remap_tasks.size() * sizeof(KRemapTask));
-    put(t.off_pages, pages.data(), pages.size() * sizeof(KPageEntry));
-    put(t.off_freed, freed.data(), freed.size() * sizeof(KFreedEntry));
+    put(t.off_runs, plan.runs.data(), plan.runs.size() * sizeof(KPageRun));
+    put(t.off_asm_runs, asm_runs.data(), asm_runs.size() * sizeof(KPageRun));
+    put(t.off_remap_runs, remap_runs.data(), remap_runs.size() * sizeof(KPageRun));
+    put(t.off_freed_runs, plan.freed.data(), plan.freed.size() * sizeof(KFreedRun));
     return LEYLINE_OK;
 }
 
@@ -517,7 +546,7 @@ extern "C" int leyline_paged_query(const leyline_cache* cache, int32_t n_seqs,
     if (new_seq_lens)
         for (int32_t b = 0; b < n_seqs; ++b) new_seq_lens[b] = plan.new_lens[size_t(b)];
     if (n_fresh_needed) *n_fresh_needed = plan.n_fresh;
-    if (n_freed) *n_freed = int32_t(plan.freed_page.size());
+    if (n_freed) *n_freed = plan.n_freed;
     if (workspace_bytes) *workspace_bytes = img.tables.total;
     return LEYLINE_OK;
 }
@@ -534,20 +563,22 @@ extern "C" int leyline_paged_plan(int32_t page_size, int32_t n_seqs, const int32
     if (rc) return rc;
     rc = check_table_width(plan, seq_lens, bt_stride);
     if (rc) return rc;
-    if (int64_t(plan.freed_page.size()) > freed_cap) return LEYLINE_E_CAPACITY;
-    if (plan.freed_page.size() && (!freed_seq_out || !freed_page_out)) return LEYLINE_E_INVAL;
+    if (plan.n_freed > freed_cap) return LEYLINE_E_CAPACITY;
+    if (plan.n_freed > 0 && (!freed_seq_out || !freed_page_out)) return LEYLINE_E_INVAL;
     for (int64_t i = 0; i < int64_t(n_seqs) * bt_stride; ++i) {
         kind_out[i] = LEYLINE_PAGE_NONE;
         src_out[i] = -1;
     }
-    for (size_t i = 0; i < plan.page_k.size(); ++i) {
-        const int64_t at = int64_t(plan.page_seq[i]) * bt_stride + plan.page_k[i];
-        kind_out[at] = plan.page_kind[i];
-        src_out[at] = plan.page_src[i];
-    }
-    for (size_t i = 0; i < plan.freed_page.size(); ++i) {
-        freed_seq_out[i] = plan.freed_seq[i];
-        freed_page_out[i] = plan.freed_page[i];
-    }
+    for (const KPageRun& r : plan.runs)
+        for (int32_t c = 0; c < r.count; ++c) {
+            const int64_t at = int64_t(r.seq) * bt_stride + r.k0 + c;
+            kind_out[at] = r.kind;
+            src_out[at] = r.src0 + c;
+        }
+    for (const KFreedRun& r : plan.freed)
+        for (int32_t c = 0; c < r.count; ++c) {
+            freed_seq_out[r.out0 + c] = r.seq;
+            freed_page_out[r.out0 + c] = r.page0 + c;
+        }
     return LEYLINE_OK;
 }

@@ -53,15 +53,18 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
 
 // ------------------------------------------------------------------------------------------
 // Paged splice.
+// The plan is kept as runs of pages: its size grows with the number of directives and sequences,
+// not with the number of pages.
 struct PagedPlan {
     int32_t page_size = 0;
     int32_t n_seqs = 0;
     std::vector<int32_t> new_lens;
-    // per (seq, new logical page), in ascending order
-    std::vector<int32_t> page_seq, page_k, page_kind, page_src, page_dir;   // page_dir: remap shift's directive (-1: none)
-    std::vector<int32_t> freed_seq, freed_page;
-    int32_t n_fresh = 0;
-    int32_t n_assemble = 0, n_remap = 0;
+    std::vector<int32_t> run_begin;    // [n_seqs + 1]: sequence b owns runs [run_begin[b], run_begin[b+1])
+    std::vector<KPageRun> runs;        // ascending (seq, k0); they cover every new page exactly once
+    std::vector<KFreedRun> freed;      // ascending (seq, page0)
+    int32_t n_fresh = 0;               // ASSEMBLE pages (fresh pages consumed)
+    int32_t n_remap = 0;
+    int32_t n_freed = 0;
 };
 
 int plan_paged(int32_t page_size, int32_t n_seqs, const int32_t* seq_lens,

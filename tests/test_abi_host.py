@@ -176,6 +176,51 @@ def test_paged_plan_matches_oracle_bit_exactly():
             assert fp[:n_freed] == [x for p in plans for x in p.freed]
 
 
+def _random_paged_degenerate(rng, n_seqs, page, max_len=300):
+    """Directives drawn with replacement: empty spans, empty stubs (together: a directive that
+    changes nothing), adjacent spans and equal starts all occur."""
+    lens = [rng.randint(0, max_len) for _ in range(n_seqs)]
+    spec = []
+    for b, n in enumerate(lens):
+        k = rng.randint(0, 4)
+        cuts = sorted(rng.randint(0, n) for _ in range(2 * k))
+        for i in range(0, len(cuts), 2):
+            s, e = cuts[i], cuts[i + 1]
+            r = rng.choice([0, 0, e - s, rng.randint(0, 2 * (e - s) + 3), (e - s) + page,
+                            max(0, e - s - 2 * page)])
+            spec.append((s, e, r, b))
+    return lens, spec
+
+
+def test_paged_plan_matches_oracle_on_degenerate_directives():
+    rng = random.Random(37)
+    for page in (1, 2, 16):
+        for _ in range(150):
+            lens, spec = _random_paged_degenerate(rng, rng.randint(1, 4), page)
+            dirs = [O.Directive(s, e, r, seq=b) for s, e, r, b in spec]
+            try:
+                plans = O.plan_paged(lens, dirs, page)
+                for b, n in enumerate(lens):
+                    O.check_directives(n, [d for d in dirs if d.seq == b])
+            except O.DirectiveError:
+                with pytest.raises(L.LeylineError):
+                    L.leyline_paged_plan(page, lens, _dirs(spec), len(spec), 64, 4096)
+                continue
+            bt_stride = max([1] + [O.pages_for(max(n, p.new_len), page) for n, p in zip(lens, plans)])
+            n_freed = sum(len(p.freed) for p in plans)
+            kinds, srcs, fs, fp = L.leyline_paged_plan(page, lens, _dirs(spec), len(spec), bt_stride,
+                                                       n_freed)
+            kinds = np.array(kinds).reshape(len(lens), bt_stride)
+            srcs = np.array(srcs).reshape(len(lens), bt_stride)
+            for b, p in enumerate(plans):
+                k = len(p.kinds)
+                assert list(kinds[b, :k]) == p.kinds, (lens, spec, b)
+                assert list(srcs[b, :k]) == p.sources, (lens, spec, b)
+                assert np.all(kinds[b, k:] == L.PAGE_NONE)
+            assert fs[:n_freed] == [b for b, p in enumerate(plans) for _ in p.freed]
+            assert fp[:n_freed] == [x for p in plans for x in p.freed]
+
+
 def test_paged_query_and_plan_errors():
     import torch
     pool = _FakeTensor((2, 32, 16, 576), torch.bfloat16)

@@ -48,11 +48,11 @@ def _odirs(wl):
     return [O.Directive(d.span_start, d.span_end, d.stub_len, seq=d.seq) for d in wl.dirs]
 
 
-def _random_workload(rng, page, kind, dtype):
+def _random_workload(rng, page, kind, dtype, max_len=None):
     n_seqs = rng.randint(1, 4)
     lens, dirs = [], []
     for b in range(n_seqs):
-        n = rng.randint(0, 5 * page + 3)
+        n = rng.randint(0, max_len if max_len is not None else 5 * page + 3)
         lens.append(n)
         k = rng.randint(0, 3)
         cuts = sorted(rng.sample(range(n + 1), min(2 * k, n + 1)))
@@ -79,6 +79,35 @@ def test_small_random_paged_whole_pool(L, kind, dtype):
         for ci in range(8):
             wl = _random_workload(rng, page, kind, dtype)
             print(f"[case] paged {kind}/{dtype} page={page} case={ci} lens={wl.seq_lens} dirs={wl.dirs}",
+                  flush=True)
+            pools, bt, free, stubs = W.alloc_paged(wl, DEV, spare_pages=3)
+            before = [host(p) for p in pools]
+            bt_h, free_h = host(bt), host(free)
+            stubs_h = [[host(s).reshape(wl.n_layers, s.shape[1], p.row_elems) for s, p in zip(per, wl.planes)]
+                       for per in stubs]
+            bt_out, freed, new_lens = _run_gpu(L, wl, pools, bt, free, stubs)
+            planes = [oracle_plane(p) for p in wl.planes]
+            flat = [b.reshape(b.shape[0], b.shape[1], b.shape[2], -1) for b in before]
+            want, want_bt, want_lens, want_freed = O.splice_paged(
+                flat, planes, dtype, bt_h, wl.seq_lens, _odirs(wl), stubs_h, list(free_h), page)
+            assert new_lens == want_lens
+            assert np.array_equal(host(bt_out), want_bt)
+            assert list(host(freed)) == want_freed
+            for pi, plane in enumerate(planes):
+                got = host(pools[pi]).reshape(want[pi].shape)
+                assert_rows_match(got, want[pi], plane, dtype, what=f"page={page} case={ci} plane={pi}")
+
+
+@pytest.mark.parametrize("kind,dtype", [("mla", "bf16"), ("gqa", "bf16"), ("mla", "f32"),
+                                        ("mla_neox", "bf16")])
+def test_token_slot_paged_whole_pool(L, kind, dtype):
+    """Page sizes 1 and 2 (token-slot caches) with sequences long enough that the in-place
+    rotation of remapped slots spans many workgroups and ends in a ragged one."""
+    rng = random.Random({"mla": 197, "gqa": 198, "mla_neox": 199}[kind] + (dtype == "f32"))
+    for page in (1, 2):
+        for ci in range(3):
+            wl = _random_workload(rng, page, kind, dtype, max_len=900)
+            print(f"[case] slots {kind}/{dtype} page={page} case={ci} lens={wl.seq_lens} dirs={wl.dirs}",
                   flush=True)
             pools, bt, free, stubs = W.alloc_paged(wl, DEV, spare_pages=3)
             before = [host(p) for p in pools]
@@ -204,3 +233,16 @@ def test_mla_dsv3_paged_131k_full_and_sequential(L):
     del pools
     torch.cuda.empty_cache()
     _check_sampled(L, wl, seed=13)
+
+
+@pytest.mark.parametrize("name", ["mla_dsv3_slots_32k", "gqa_llama3_8b_slots_16k"])
+def test_token_slot_splice_full(L, name):
+    """Full-size splices on token-slot caches: every downstream token keeps its slot (its
+    rotary band is rotated in place), only the replacement tokens take fresh slots."""
+    wl = W.WORKLOADS[name]()
+    pools, bt, bt_out, new_lens, plans = _check_sampled(L, wl, seed=17)
+    kinds = [k for p in plans for k in p.kinds]
+    d = wl.dirs[0]
+    assert kinds.count(O.ASSEMBLE) == d.stub_len
+    assert kinds.count(O.REMAP) == wl.seq_lens[0] - d.span_end
+    assert kinds.count(O.IDENTITY) == d.span_start

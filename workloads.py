@@ -126,12 +126,29 @@ def mla_dsv3_paged_131k(seed: int = 5, n_layers: int = 61) -> Workload:
                     page_size=64, seed=seed)
 
 
+def mla_dsv3_slots_32k() -> Workload:
+    """The 32K MLA splice on a token-slot cache (page size 1, slots scattered over the pool): the
+    downstream tokens keep their slots, only their K_pe bands are rotated in place."""
+    w = mla_dsv3_32k()
+    return Workload("mla_dsv3_slots_32k", w.n_layers, w.dtype, w.planes, w.dirs, w.seq_lens,
+                    page_size=1, seed=w.seed)
+
+
+def gqa_llama3_8b_slots_16k() -> Workload:
+    """The 16K GQA splice on a token-slot cache: downstream K heads rotated in place, V untouched."""
+    w = gqa_llama3_8b_16k()
+    return Workload("gqa_llama3_8b_slots_16k", w.n_layers, w.dtype, w.planes, w.dirs, w.seq_lens,
+                    page_size=1, seed=w.seed)
+
+
 WORKLOADS = {
     "mla_1l_4k_f32": mla_1l_4k_f32,
     "mla_dsv3_32k": mla_dsv3_32k,
     "mla_dsv3_paged_b64": mla_dsv3_paged_b64,
     "gqa_llama3_8b_16k": gqa_llama3_8b_16k,
     "mla_dsv3_paged_131k": mla_dsv3_paged_131k,
+    "mla_dsv3_slots_32k": mla_dsv3_slots_32k,
+    "gqa_llama3_8b_slots_16k": gqa_llama3_8b_slots_16k,
 }
 
 
