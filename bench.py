@@ -30,8 +30,7 @@ PEAK_HBM_GBPS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_01065_amd", "csrc", "kernels.hip")
 PROFILES = os.path.join(ROOT, "profiles")
 CONTIG_KERNEL = "contig_move_kernel"
-PAGED_KERNEL = "paged_move_kernel"
-PAGED_REMAP_KERNEL = "paged_remap_kernel"
+PAGED_KERNEL = "paged_data_kernel"
 COPY_KERNEL_HINT = "elementwise"        # torch's device copy kernel used for counter calibration
 
 
@@ -115,9 +114,7 @@ def paged_bytes(wl, kinds, new_lens, bt_stride, L):
             seg_end = mine[j + 1].span_start if j + 1 < len(mine) else n
             if shift != 0:
                 moved += seg_end - d.span_end
-    asm_b, remap_b = 2 * wl.n_layers * asm_rows * rb, 2 * wl.n_layers * remap_rows * rot_b
-    kernel = PAGED_KERNEL if asm_b >= remap_b else PAGED_REMAP_KERNEL
-    return asm_b + remap_b, moved, kernel
+    return 2 * wl.n_layers * (asm_rows * rb + remap_rows * rot_b), moved, PAGED_KERNEL
 
 
 COPY_CAP = 1 << 31          # bytes per side of the reference / calibration copy
@@ -279,8 +276,8 @@ def setup_paged(wl, dev, L, W, specs, stream):
 
     keep = dict(paged=True)
     torch.cuda.synchronize()
-    # one gather (or, on token-slot caches, one in-place rotation) launch per splice carries the
-    # bytes; the row-table and block-table kernels around it are inside the timed splice
+    # one data launch per splice (gather of assembled pages and in-place rotation of remapped
+    # ones) carries the bytes; the resolve launch before it is inside the timed splice
     return step, kernel, alg_bytes, moved, 1, keep
 
 

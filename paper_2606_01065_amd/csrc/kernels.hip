@@ -81,6 +81,18 @@ __device__ __forceinline__ void st16(char* p, u32x4 v) {
 #endif
 }
 
+// Band kernels rotate a slice of each row in place.  When the slice is narrow (MLA: 128 of 1152
+// bytes) the cached forms are faster; when it is most of the row, the streaming forms.  The
+// choice is a template parameter: kernels are launched once per class of planes.
+template <bool NT> __device__ __forceinline__ u32x4 ld16_band(const char* p) {
+    if constexpr (NT) return ld16(p);
+    else return *reinterpret_cast<const u32x4*>(p);
+}
+template <bool NT> __device__ __forceinline__ void st16_band(char* p, u32x4 v) {
+    if constexpr (NT) st16(p, v);
+    else *reinterpret_cast<u32x4*>(p) = v;
+}
+
 // ----------------------------------------------------------------------- element helpers ---
 
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
@@ -297,18 +309,19 @@ __device__ __forceinline__ BandPos band_pos(const KPlane& pl, int32_t q) {
     return p;
 }
 
+template <bool NT>
 __device__ __forceinline__ void band_load(const BandPos& p, const char* row, int64_t lstride, int nl,
                                           u32x4 (&x)[PAGED_LPT], u32x4 (&y)[PAGED_LPT]) {
 #pragma unroll
     for (int l = 0; l < PAGED_LPT; ++l) {
         if (l < nl) {
-            x[l] = ld16(row + l * lstride + p.a);
-            if (p.two) y[l] = ld16(row + l * lstride + p.b);
+            x[l] = ld16_band<NT>(row + l * lstride + p.a);
+            if (p.two) y[l] = ld16_band<NT>(row + l * lstride + p.b);
         }
     }
 }
 
-template <int ESZ>
+template <int ESZ, bool NT>
 __device__ __forceinline__ void band_rotate_store(const KPlane& pl, const BandPos& p, char* row,
                                                   int64_t lstride, int nl, u32x4 (&x)[PAGED_LPT],
                                                   u32x4 (&y)[PAGED_LPT], const KCosSin* table, int32_t cs) {
@@ -318,11 +331,11 @@ __device__ __forceinline__ void band_rotate_store(const KPlane& pl, const BandPo
         if (l < nl) {
             if (p.two) {
                 rot_halves<ESZ>(x[l], y[l], table, cs + p.j * EPC);
-                st16(row + l * lstride + p.b, y[l]);
+                st16_band<NT>(row + l * lstride + p.b, y[l]);
             } else {
                 rotate_band_chunk<ESZ>(pl, x[l], p.j, table, cs);
             }
-            st16(row + l * lstride + p.a, x[l]);
+            st16_band<NT>(row + l * lstride + p.a, x[l]);
         }
     }
 }
@@ -449,12 +462,12 @@ __global__ __launch_bounds__(TPB) void contig_chain_kernel(const KContigParams P
 
 // In-place R(delta) on listed rows: band units of all rows laid end to end, one plane per
 // blockIdx.z, PAGED_LPT layers per thread, the shift's cos/sin staged in LDS.
-template <int ESZ>
+template <int ESZ, bool NT>
 __global__ __launch_bounds__(PAGED_TPB) void rotate_rows_kernel(const KRotateParams P) {
     __shared__ KCosSin lcs[KMAX_CS];
     const int plane = blockIdx.z;
     const KPlane& pl = P.planes[plane];
-    if (pl.rot_tpr == 0) return;
+    if (pl.rot_tpr == 0 || pl.band_nt != int(NT)) return;               // not this launch's class
     const int32_t tb = int32_t(blockIdx.x) * PAGED_TPB;
     if (int64_t(tb) >= P.n_rows * pl.rot_tpr) return;                  // past this plane
     const int32_t t = tb + int32_t(threadIdx.x);
@@ -476,21 +489,24 @@ __global__ __launch_bounds__(PAGED_TPB) void rotate_rows_kernel(const KRotatePar
     }
     const BandPos bp = band_pos(pl, q);
     u32x4 x[PAGED_LPT], y[PAGED_LPT];
-    if (active) band_load(bp, r, pl.layer_stride, nl, x, y);
+    if (active) band_load<NT>(bp, r, pl.layer_stride, nl, x, y);
     stage_cs<PAGED_TPB>(lcs, P.cs, pl.cs_off, pl.n_pairs);
     __syncthreads();
     if (!active) return;
-    band_rotate_store<ESZ>(pl, bp, r, pl.layer_stride, nl, x, y, lcs, 0);
+    band_rotate_store<ESZ, NT>(pl, bp, r, pl.layer_stride, nl, x, y, lcs, 0);
 }
 
 // ------------------------------------------------------------------------------ paged splice ---
 //
-// Three steps on the call's stream.  (1) paged_rows_kernel resolves every row of every ASSEMBLE
-// page once (shared by all layers and planes): which old physical page and row, or which
-// replacement token, it comes from, which fresh page it goes to, and which shift re-anchors it.
-// (2) paged_move_kernel moves those rows like the contiguous kernel: rows laid end to end, one
-// 16-byte chunk per thread, so each wavefront reads one row entry and moves whole lines.
-// (3) paged_remap_kernel rotates the rotary bands of REMAP pages (re-used whole pages) in place.
+// Two launches on the call's stream, after the plan's runs are uploaded.
+// (1) paged_resolve_kernel expands the runs once for all layers and planes: for every row of
+//     every ASSEMBLE page, which old physical page and row (or which replacement token) it comes
+//     from, which fresh page it goes to and which shift re-anchors it; for every REMAP page, its
+//     physical page and shift; and the new block tables and the freed-page list.
+// (2) paged_data_kernel moves the data.  Its first blocks gather ASSEMBLE rows like the
+//     contiguous kernel (rows laid end to end, one 16-byte chunk per thread, so a wavefront
+//     reads one row entry and moves whole lines); the remaining blocks rotate the rotary bands of
+//     REMAP pages (re-used whole pages) in place.
 // Nothing is written to an old page except the rotary bands of REMAP pages, which no ASSEMBLE
 // row reads.
 
@@ -520,11 +536,47 @@ __device__ __forceinline__ void resolve_remap_page(const KPagedParams& P, int32_
     P.remap_pages[m] = e;
 }
 
-// Threads [0, n_rows) resolve ASSEMBLE rows, threads [n_rows, n_rows + n_remap) REMAP pages.
-__global__ __launch_bounds__(TPB) void paged_rows_kernel(const KPagedParams P) {
-    const int32_t i = int32_t(blockIdx.x) * TPB + int32_t(threadIdx.x);
+// New block-table entry i (sequence i / bt_stride, page i % bt_stride) from the page runs.
+__device__ __forceinline__ void resolve_table_entry(const KPagedParams& P, int32_t i) {
+    const int32_t b = i / P.bt_stride, k = i - b * P.bt_stride;
+    const KSeqEntry S = P.seqs[b];
+    int32_t v = -1;
+    if (S.run_count > 0 && int64_t(k) * P.page_size < S.new_len) {
+        int32_t lo = S.run_begin, hi = S.run_begin + S.run_count;
+        while (hi - lo > 1) {
+            const int32_t mid = (lo + hi) >> 1;
+            if (P.runs[mid].k0 <= k) lo = mid; else hi = mid;
+        }
+        const KPageRun R = P.runs[lo];
+        const int32_t src = R.src0 + (k - R.k0);
+        if (R.kind == LEYLINE_PAGE_ASSEMBLE) v = src < P.n_free ? P.free_pages[src] : -1;
+        else v = P.bt_in[int64_t(b) * P.bt_stride + src];
+    }
+    P.bt_out[i] = v;
+}
+
+// Freed-list entry f from the freed runs.
+__device__ __forceinline__ void resolve_freed_entry(const KPagedParams& P, int32_t f) {
+    int32_t lo = 0, hi = P.n_freed_runs;
+    while (hi - lo > 1) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (P.freed_runs[mid].out0 <= f) lo = mid; else hi = mid;
+    }
+    const KFreedRun R = P.freed_runs[lo];
+    P.freed_out[f] = P.bt_in[int64_t(R.seq) * P.bt_stride + R.page0 + (f - R.out0)];
+}
+
+// Threads [0, n_rows): ASSEMBLE rows; then n_remap REMAP pages; then n_seqs * bt_stride block-
+// table entries; then n_freed freed-list entries.
+__global__ __launch_bounds__(TPB) void paged_resolve_kernel(const KPagedParams P) {
+    int32_t i = int32_t(blockIdx.x) * TPB + int32_t(threadIdx.x);
     if (i >= P.n_rows) {
-        if (i - P.n_rows < P.n_remap) resolve_remap_page(P, i - P.n_rows);
+        i -= P.n_rows;
+        if (i < P.n_remap) { resolve_remap_page(P, i); return; }
+        i -= P.n_remap;
+        if (i < P.n_table) { resolve_table_entry(P, i); return; }
+        i -= P.n_table;
+        if (i < P.n_freed) resolve_freed_entry(P, i);
         return;
     }
     const int32_t task = i / P.page_size, r = i - task * P.page_size;   // task = fresh ordinal
@@ -574,12 +626,12 @@ __global__ __launch_bounds__(TPB) void paged_rows_kernel(const KPagedParams P) {
     P.rows[i] = e;
 }
 
+// One workgroup of the ASSEMBLE gather (bx: its index among the gather's workgroups).
 template <int ESZ>
-__global__ __launch_bounds__(PAGED_TPB) void paged_move_kernel(const KPagedParams P) {
-    __shared__ KCosSin lcs[KMAX_CS];
+__device__ __forceinline__ void paged_move_block(const KPagedParams& P, int32_t bx, KCosSin* lcs) {
     const int plane = blockIdx.z;
     const KPlane& pl = P.planes[plane];
-    const int32_t tb = int32_t(blockIdx.x) * PAGED_TPB;
+    const int32_t tb = bx * PAGED_TPB;
     if (int64_t(tb) >= int64_t(P.n_rows) * pl.tpr) return;            // past this plane
     const int32_t t = tb + int32_t(threadIdx.x);
     const int32_t i = fdiv(t, pl.tpr_div), u = t - i * pl.tpr;
@@ -634,17 +686,17 @@ __global__ __launch_bounds__(PAGED_TPB) void paged_move_kernel(const KPagedParam
     }
 }
 
-// REMAP pages: band units of all valid rows of all REMAP pages laid end to end, PAGED_LPT layers
-// per thread, rotated in place.  The workgroup stages the cos/sin block of its first page's shift
-// in LDS; rows with another shift (where runs meet) read the table in the workspace.
-template <int ESZ>
-__global__ __launch_bounds__(PAGED_TPB) void paged_remap_kernel(const KPagedParams P) {
-    __shared__ KCosSin lcs[KMAX_CS];
+// One workgroup of the REMAP rotation: band units of all valid rows of all REMAP pages laid end
+// to end, PAGED_LPT layers per thread, rotated in place.  The workgroup stages the cos/sin block
+// of its first page's shift in LDS; rows with another shift (where runs meet) read the table in
+// the workspace.
+template <int ESZ, bool NT>
+__device__ __forceinline__ void paged_remap_block(const KPagedParams& P, int32_t bx, KCosSin* lcs) {
     const int plane = blockIdx.z;
     const KPlane& pl = P.planes[plane];
-    if (pl.rot_tpr == 0) return;
+    if (pl.rot_tpr == 0 || pl.band_nt != int(NT)) return;               // not this launch's class
     const int32_t upp = P.page_size * pl.rot_tpr;
-    const int32_t tb = int32_t(blockIdx.x) * PAGED_TPB;
+    const int32_t tb = bx * PAGED_TPB;
     if (int64_t(tb) >= int64_t(P.n_remap) * upp) return;               // past this plane
     const int32_t t = tb + int32_t(threadIdx.x);
     const int32_t m = fdiv(t, P.remap_div[plane]);
@@ -661,44 +713,22 @@ __global__ __launch_bounds__(PAGED_TPB) void paged_remap_kernel(const KPagedPara
                 int64_t(r) * pl.token_stride;
     const BandPos bp = band_pos(pl, f - r * pl.rot_tpr);
     u32x4 x[PAGED_LPT], y[PAGED_LPT];
-    if (active) band_load(bp, row, pl.layer_stride, nl, x, y);
+    if (active) band_load<NT>(bp, row, pl.layer_stride, nl, x, y);
     if (cs0 >= 0) stage_cs<PAGED_TPB>(lcs, P.cs, cs0 + pl.cs_off, pl.n_pairs);
     __syncthreads();
     if (!active) return;
-    if (e.cs == cs0) band_rotate_store<ESZ>(pl, bp, row, pl.layer_stride, nl, x, y, lcs, 0);
-    else band_rotate_store<ESZ>(pl, bp, row, pl.layer_stride, nl, x, y, P.cs, e.cs + pl.cs_off);
+    if (e.cs == cs0) band_rotate_store<ESZ, NT>(pl, bp, row, pl.layer_stride, nl, x, y, lcs, 0);
+    else band_rotate_store<ESZ, NT>(pl, bp, row, pl.layer_stride, nl, x, y, P.cs, e.cs + pl.cs_off);
 }
 
-// New block tables and the freed-page list, expanded from the page runs.
-__global__ __launch_bounds__(TPB) void paged_tables_kernel(const KTableParams P) {
-    const int64_t i = int64_t(blockIdx.x) * TPB + threadIdx.x;
-    const int64_t n_pages = int64_t(P.n_seqs) * P.bt_stride;
-    if (i < n_pages) {
-        const int32_t b = int32_t(i / P.bt_stride), k = int32_t(i - int64_t(b) * P.bt_stride);
-        const KSeqEntry S = P.seqs[b];
-        int32_t v = -1;
-        if (S.run_count > 0 && int64_t(k) * P.page_size < S.new_len) {
-            int32_t lo = S.run_begin, hi = S.run_begin + S.run_count;
-            while (hi - lo > 1) {
-                const int32_t mid = (lo + hi) >> 1;
-                if (P.runs[mid].k0 <= k) lo = mid; else hi = mid;
-            }
-            const KPageRun R = P.runs[lo];
-            const int32_t src = R.src0 + (k - R.k0);
-            if (R.kind == LEYLINE_PAGE_ASSEMBLE) v = src < P.n_free ? P.free_pages[src] : -1;
-            else v = P.bt_in[int64_t(b) * P.bt_stride + src];
-        }
-        P.bt_out[i] = v;
-    } else if (i < n_pages + P.n_freed) {
-        const int32_t f = int32_t(i - n_pages);
-        int32_t lo = 0, hi = P.n_freed_runs;
-        while (hi - lo > 1) {
-            const int32_t mid = (lo + hi) >> 1;
-            if (P.freed[mid].out0 <= f) lo = mid; else hi = mid;
-        }
-        const KFreedRun R = P.freed[lo];
-        P.freed_out[f] = P.bt_in[int64_t(R.seq) * P.bt_stride + R.page0 + (f - R.out0)];
-    }
+// Workgroups [0, move_blocks) gather ASSEMBLE rows, the rest rotate REMAP pages whose planes
+// belong to access class NT.
+template <int ESZ, bool NT>
+__global__ __launch_bounds__(PAGED_TPB) void paged_data_kernel(const KPagedParams P) {
+    __shared__ KCosSin lcs[KMAX_CS];
+    const int32_t bx = int32_t(blockIdx.x);
+    if (bx < P.move_blocks) paged_move_block<ESZ>(P, bx, lcs);
+    else paged_remap_block<ESZ, NT>(P, bx - P.move_blocks, lcs);
 }
 
 // -------------------------------------------------------------------------- host launchers ---
@@ -887,8 +917,21 @@ extern "C" int leyline_rotate_delta(const leyline_cache* cache, int64_t delta,
     const int64_t blocks = (n_rows * max_rot + PAGED_TPB - 1) / PAGED_TPB;
     const dim3 grid(unsigned(blocks), unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT), unsigned(n_planes));
     hipStream_t s = static_cast<hipStream_t>(stream);
-    return cache->dtype == LEYLINE_BF16 ? launch(rotate_rows_kernel<2>, grid, s, P, PAGED_TPB)
-                                        : launch(rotate_rows_kernel<4>, grid, s, P, PAGED_TPB);
+    const bool bf16 = cache->dtype == LEYLINE_BF16;
+    // one launch per access class present among the rotary planes
+    for (int nt = 1; nt >= 0; --nt) {
+        bool any = false;
+        for (int p = 0; p < n_planes; ++p) any = any || (planes[p].rot_tpr > 0 && planes[p].band_nt == nt);
+        if (!any) continue;
+        if (nt)
+            rc = bf16 ? launch(rotate_rows_kernel<2, true>, grid, s, P, PAGED_TPB)
+                      : launch(rotate_rows_kernel<4, true>, grid, s, P, PAGED_TPB);
+        else
+            rc = bf16 ? launch(rotate_rows_kernel<2, false>, grid, s, P, PAGED_TPB)
+                      : launch(rotate_rows_kernel<4, false>, grid, s, P, PAGED_TPB);
+        if (rc) return rc;
+    }
+    return LEYLINE_OK;
 }
 
 extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, const int32_t* seq_lens,
@@ -933,7 +976,10 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         rc = hip_status(hipMemcpyAsync(ws, img.bytes.data(), size_t(t.upload), hipMemcpyHostToDevice, s));
         if (rc) return rc;
     }
-    if (t.n_asm + t.n_remap > 0) {
+    const int64_t n_table = int64_t(n_seqs) * bt_stride;
+    const int64_t n_resolve = int64_t(t.n_rows) + t.n_remap + n_table + t.n_freed;
+    if (n_resolve > INT32_MAX - 1024) return LEYLINE_E_INVAL;
+    if (n_resolve > 0) {
         KPagedParams P;
         std::memset(&P, 0, sizeof(P));
         std::memcpy(P.planes, planes, sizeof(planes));
@@ -945,12 +991,14 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         P.n_remap = t.n_remap;
         P.n_rows = t.n_rows;
         int32_t max_tpr = 1, max_upp = 1;
+        bool any_band[2] = {false, false};
         for (int p = 0; p < n_planes; ++p) {
             const int32_t upp = cache->page_size * planes[p].rot_tpr;
             max_tpr = std::max(max_tpr, planes[p].tpr);
             max_upp = std::max(max_upp, upp);
             P.remap_div[p] = make_div(std::max(1, upp));
             P.rot_div[p] = make_div(std::max(1, planes[p].rot_tpr));
+            if (planes[p].rot_tpr > 0) any_band[planes[p].band_nt ? 1 : 0] = true;
         }
         P.capacity = cache->capacity;
         P.seqs = reinterpret_cast<const KSeqEntry*>(ws + t.off_seq);
@@ -962,50 +1010,41 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         P.n_remap_runs = t.n_remap_runs;
         P.rows = reinterpret_cast<KRowMove*>(ws + t.off_rows);
         P.remap_pages = reinterpret_cast<KRemapPage*>(ws + t.off_remap_pages);
+        P.runs = reinterpret_cast<const KPageRun*>(ws + t.off_runs);
+        P.freed_runs = reinterpret_cast<const KFreedRun*>(ws + t.off_freed_runs);
+        P.bt_out = block_table_out;
+        P.freed_out = freed_pages_out;
+        P.n_table = int32_t(n_table);
+        P.n_freed = t.n_freed;
+        P.n_freed_runs = t.n_freed_runs;
         P.bt_in = block_table_in;
         P.free_pages = free_pages;
         P.n_free = n_free;
         P.status = device_status;
         const bool bf16 = cache->dtype == LEYLINE_BF16;
-        rc = launch(paged_rows_kernel, dim3(unsigned((int64_t(t.n_rows) + t.n_remap + TPB - 1) / TPB)), s, P);
+        rc = launch(paged_resolve_kernel, dim3(unsigned((n_resolve + TPB - 1) / TPB)), s, P);
         if (rc) return rc;
-        if (t.n_rows > 0) {
-            const int64_t blocks = (int64_t(t.n_rows) * max_tpr + PAGED_TPB - 1) / PAGED_TPB;
-            const dim3 grid(unsigned(blocks), unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT),
-                            unsigned(n_planes));
-            rc = bf16 ? launch(paged_move_kernel<2>, grid, s, P, PAGED_TPB)
-                      : launch(paged_move_kernel<4>, grid, s, P, PAGED_TPB);
+        // data kernel: gather workgroups, then REMAP workgroups, once per access class of the
+        // rotary planes (the gather runs with the first launch)
+        const int64_t move_blocks = t.n_rows > 0 ? (int64_t(t.n_rows) * max_tpr + PAGED_TPB - 1) / PAGED_TPB : 0;
+        const int64_t remap_blocks = t.n_remap > 0 ? (int64_t(t.n_remap) * max_upp + PAGED_TPB - 1) / PAGED_TPB : 0;
+        const dim3 layers_planes(1, unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT), unsigned(n_planes));
+        bool first = true;
+        for (int nt = 1; nt >= 0; --nt) {
+            const int64_t rb = any_band[nt] ? remap_blocks : 0;
+            const int64_t mb = first ? move_blocks : 0;
+            if (mb + rb == 0) continue;
+            P.move_blocks = int32_t(mb);
+            const dim3 grid(unsigned(mb + rb), layers_planes.y, layers_planes.z);
+            if (nt)
+                rc = bf16 ? launch(paged_data_kernel<2, true>, grid, s, P, PAGED_TPB)
+                          : launch(paged_data_kernel<4, true>, grid, s, P, PAGED_TPB);
+            else
+                rc = bf16 ? launch(paged_data_kernel<2, false>, grid, s, P, PAGED_TPB)
+                          : launch(paged_data_kernel<4, false>, grid, s, P, PAGED_TPB);
             if (rc) return rc;
+            first = false;
         }
-        if (t.n_remap > 0) {
-            const int64_t blocks = (int64_t(t.n_remap) * max_upp + PAGED_TPB - 1) / PAGED_TPB;
-            const dim3 grid(unsigned(blocks), unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT),
-                            unsigned(n_planes));
-            rc = bf16 ? launch(paged_remap_kernel<2>, grid, s, P, PAGED_TPB)
-                      : launch(paged_remap_kernel<4>, grid, s, P, PAGED_TPB);
-            if (rc) return rc;
-        }
-    }
-    const int64_t n_pages = int64_t(n_seqs) * bt_stride;
-    if (n_pages + t.n_freed > 0) {
-        KTableParams T;
-        std::memset(&T, 0, sizeof(T));
-        T.seqs = reinterpret_cast<const KSeqEntry*>(ws + t.off_seq);
-        T.runs = reinterpret_cast<const KPageRun*>(ws + t.off_runs);
-        T.freed = reinterpret_cast<const KFreedRun*>(ws + t.off_freed_runs);
-        T.bt_in = block_table_in;
-        T.bt_out = block_table_out;
-        T.free_pages = free_pages;
-        T.freed_out = freed_pages_out;
-        T.n_seqs = n_seqs;
-        T.bt_stride = bt_stride;
-        T.page_size = cache->page_size;
-        T.n_freed = t.n_freed;
-        T.n_freed_runs = t.n_freed_runs;
-        T.n_free = n_free;
-        const int64_t blocks = (n_pages + t.n_freed + TPB - 1) / TPB;
-        rc = launch(paged_tables_kernel, dim3(unsigned(blocks)), s, T);
-        if (rc) return rc;
     }
     if (new_seq_lens_out)
         for (int32_t b = 0; b < n_seqs; ++b) new_seq_lens_out[b] = plan.new_lens[size_t(b)];

@@ -36,7 +36,8 @@ struct KPlane {
     int32_t cs_off;          // offset of this plane's pairs within one shift's cos/sin block
     int32_t n_pairs;         // rotary pairs per head (rot_dim / 2)
     int32_t neox_lanes;      // 1: half-split partners are exchanged between lanes of a wavefront
-    int32_t stage_cs;        // 1: most chunks of a row rotate; stage cos/sin in LDS per workgroup
+    int32_t band_nt;         // rotary-only kernels: 1 = streaming accesses (band is most of the
+                             // row), 0 = cached accesses (a narrow slice of each row)
     int32_t tpr;             // row kernels: threads per row (row_chunks, or two-chunk units)
     int32_t units_all;       // two-chunk units per row (ordered-chain kernel)
     KDiv tpr_div;            // division by tpr
@@ -192,17 +193,16 @@ struct KPagedParams {
     int32_t* status;
     KRowMove* rows;          // workspace, n_rows entries
     KRemapPage* remap_pages; // workspace, n_remap entries
+    // block tables and freed list (resolve kernel)
+    const KPageRun* runs;    // all runs, ascending (seq, k0)
+    const KFreedRun* freed_runs;
+    int32_t* bt_out;
+    int32_t* freed_out;
+    int32_t n_table;         // n_seqs * bt_stride
+    int32_t n_freed;
+    int32_t n_freed_runs;
+    int32_t move_blocks;     // data kernel: workgroups of the ASSEMBLE gather (the rest rotate)
 };
 
-struct KTableParams {
-    const KSeqEntry* seqs;
-    const KPageRun* runs;      // all runs, ascending (seq, k0)
-    const KFreedRun* freed;    // ascending out0
-    const int32_t* bt_in;
-    int32_t* bt_out;
-    const int32_t* free_pages;
-    int32_t* freed_out;
-    int32_t n_seqs, bt_stride, page_size, n_freed, n_freed_runs, n_free;
-};
 
 }  // namespace leyline
