@@ -30,6 +30,7 @@ PEAK_HBM_GBPS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_01065_amd", "csrc", "kernels.hip")
 PROFILES = os.path.join(ROOT, "profiles")
 CONTIG_KERNEL = "contig_move_kernel"
+CONTIG_TILE_KERNEL = "contig_tile_kernel"
 PAGED_KERNEL = "paged_data_kernel"
 COPY_KERNEL_HINT = "elementwise"        # torch's device copy kernel used for counter calibration
 
@@ -242,16 +243,19 @@ def setup_contig(wl, dev, L, W, specs, stream, args):
     dirs = L.make_directives([dict(span_start=d.span_start, span_end=d.span_end, stub=stubs[j],
                                    stub_len=d.stub_len) for j, d in enumerate(wl.dirs)])
     n, nd = wl.seq_lens[0], len(wl.dirs)
-    _, launches = L.leyline_contig_query(caches[0], n, dirs, nd)
+    q = L.leyline_contig_query(caches[0], n, dirs, nd)
+    ws = torch.empty(q.workspace_bytes, dtype=torch.uint8, device=dev) if q.workspace_bytes else None
     alg_bytes, moved = contig_bytes(wl)
+    # the kernel that carries most of the bytes: ordered tiles when the plan has them
+    kernel, launches = (CONTIG_TILE_KERNEL, q.tile_launches) if q.tile_launches else (CONTIG_KERNEL, q.launches)
 
     def step(i):
-        L.leyline_splice_contig(caches[i % len(caches)], n, dirs, nd, stream)
+        L.leyline_splice_contig(caches[i % len(caches)], n, dirs, nd, stream, workspace=ws)
 
     # pristine host copy of the first layers for the CPU baseline (before any step runs)
     keep = dict(planes=[t[:8].cpu() for t in base_planes], stubs=[[s[:8].cpu() for s in per] for per in stubs])
     torch.cuda.synchronize()
-    return step, CONTIG_KERNEL, alg_bytes, moved, launches, keep
+    return step, kernel, alg_bytes, moved, launches, keep
 
 
 def setup_paged(wl, dev, L, W, specs, stream):
@@ -374,6 +378,12 @@ def summarize(args):
     splices = _flag(args.command, "--steps", 100) + _flag(args.command, "--warmup", 10)
     stats = _read_csv(trace_dir, "kernel_stats")
     trace = _read_csv(trace_dir, "kernel_trace")
+    if not wl.page_size:
+        # the contiguous kernel that took the most time (rounds, or ordered tiles)
+        best = max((r for r in stats if CONTIG_KERNEL in r["Name"] or CONTIG_TILE_KERNEL in r["Name"]),
+                   key=lambda r: float(r["TotalDurationNs"]), default=None)
+        if best is not None and CONTIG_TILE_KERNEL in best["Name"]:
+            kernel = CONTIG_TILE_KERNEL
     durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace
             if kernel in r["Kernel_Name"]]
     fetch = _read_csv(fetch_dir, "counter_collection")

@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define LEYLINE_ABI_VERSION 1
+#define LEYLINE_ABI_VERSION 2
 #define LEYLINE_MAX_PLANES 4
 
 enum {
@@ -139,12 +139,14 @@ const char* leyline_last_hip_error(void);
 
 /*
  * Host-only check of a contiguous splice: validates exactly as leyline_splice_contig does and
- * reports the new length and the number of kernel launches the splice will enqueue (host
- * outputs, each nullable).  Enqueues nothing.
+ * reports (host outputs, each nullable) the new length, the number of kernel launches the splice
+ * will enqueue, how many of them are ordered-tile moves, and the device workspace it needs in
+ * bytes (0 when no move is done in ordered tiles).  Enqueues nothing.
  */
 int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
                          const leyline_directive* dirs, int32_t n_dirs,
-                         int64_t* new_len_out, int32_t* n_launches_out);
+                         int64_t* new_len_out, int32_t* n_launches_out,
+                         int32_t* n_tile_launches_out, int64_t* workspace_bytes_out);
 
 /*
  * Contiguous in-place splice of one sequence (all layers and planes).
@@ -155,12 +157,20 @@ int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
  * prefix rows untouched, each stub at its new position, each downstream row at its old position
  * plus the running shift with its rotary bands rotated by that shift.  Rows [new_len, max(seq_len,
  * new_len)) are left unspecified.  Source and destination ranges overlap; the library orders the
- * moves so that every row is read before it is overwritten.
- * Errors: E_INVAL, E_RANGE, E_ORDER, E_OVERLAP, E_CAPACITY (new length > capacity), E_MODE, E_HIP.
+ * moves so that every row is read before it is overwritten.  A segment whose shift is small
+ * against its length is moved in ordered tiles that coordinate through the workspace.
+ *
+ * workspace: device memory, 256-byte aligned, at least the size leyline_contig_query reports
+ * (NULL allowed when that size is 0).  The call clears it on `stream` before use; reuse it only
+ * after the stream has passed this call, and do not share one workspace between calls that may
+ * run at the same time.
+ * Errors: E_INVAL, E_RANGE, E_ORDER, E_OVERLAP, E_CAPACITY (new length > capacity), E_MODE,
+ * E_WORKSPACE (missing, misaligned or too small), E_HIP.
  */
 int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len,
                           const leyline_directive* dirs, int32_t n_dirs,
-                          int64_t* new_len_out, void* stream);
+                          int64_t* new_len_out, void* workspace, int64_t workspace_bytes,
+                          void* stream);
 
 /*
  * Sizes of a paged splice, computed on the host from lengths and directives alone.

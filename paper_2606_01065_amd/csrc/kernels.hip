@@ -458,6 +458,83 @@ __global__ __launch_bounds__(TPB) void contig_chain_kernel(const KContigParams P
     }
 }
 
+// Ordered tiles: moves by a shift too small for rounds.  The moved range is cut into tiles of
+// KTILE_CHUNKS chunks (counted from the first source row), one workgroup and one layer each.
+// Workgroups take tickets in the order they start; ticket t is tile t / n_layers of the item's
+// processing order (ascending tiles for a left shift, descending for a right one) in layer
+// t mod n_layers.  A tile loads its whole source into registers, waits until those loads have
+// returned and publishes "source read"; it then waits until each earlier tile whose source its
+// destination overlaps (at most two: the shift is M chunks, so those are the tiles floor(M/C)
+// and ceil(M/C) places earlier) has published the same, and only then stores.  No tile reads a
+// chunk another tile has written.  A tile waits only for tickets taken before its own, so every
+// wait ends.
+template <int ESZ>
+__global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KContigParams P) {
+    __shared__ KCosSin lcs[KMAX_CS];
+    __shared__ int32_t s_ticket;
+    if (threadIdx.x == 0) s_ticket = atomicAdd(P.tile_counter, 1);
+    __syncthreads();
+    const int32_t ticket = s_ticket;
+    if (ticket >= P.n_tickets) return;                            // block-uniform
+    int it = 0;
+    while (it + 1 < P.n_items && ticket >= P.items[it + 1].ticket0) ++it;
+    const KItem& I = P.items[it];
+    const KPlane& pl = I.pl;
+    const int32_t local = ticket - I.ticket0;
+    const int32_t order = local / P.n_layers, layer = local - order * P.n_layers;
+    const bool down = I.delta < 0;
+    const int32_t q = down ? order : I.n_tiles - 1 - order;
+    const int32_t total = int32_t(I.count) * pl.tpr;
+    const char* src = pl.base + int64_t(layer) * pl.layer_stride + I.src0 * pl.token_stride;
+    const int64_t dshift = I.delta * pl.token_stride;
+    // Every slot loads (past the end of the range: the range's last chunk, which stays unused),
+    // so that all loads are issued back to back without branches between them.
+    u32x4 v[KTILE_CPT];
+    int64_t off[KTILE_CPT];
+    int32_t uu[KTILE_CPT];
+#pragma unroll
+    for (int i = 0; i < KTILE_CPT; ++i) {
+        const int32_t g = q * KTILE_CHUNKS + i * KTILE_TPB + int32_t(threadIdx.x);
+        const int32_t gc = min(g, total - 1);
+        const int32_t r = fdiv(gc, pl.tpr_div);
+        uu[i] = g < total ? gc - r * pl.tpr : -1;
+        off[i] = int64_t(r) * pl.token_stride + int64_t(gc - r * pl.tpr) * 16;
+        v[i] = ld16(src + off[i]);
+    }
+    if (I.cs >= 0) stage_cs<KTILE_TPB>(lcs, P.cs, I.cs, pl.n_pairs);
+    __builtin_amdgcn_s_waitcnt(0);          // this thread's loads have returned
+    __syncthreads();                        // ... and every thread's
+    if (threadIdx.x == 0) {
+        __hip_atomic_store(P.tile_flags + ticket, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int64_t M = (down ? -I.delta : I.delta) * pl.tpr;   // shift in chunks
+        for (int64_t d = M / KTILE_CHUNKS; d <= (M + KTILE_CHUNKS - 1) / KTILE_CHUNKS; ++d) {
+            const int64_t j = order - d;
+            if (d == 0 || j < 0) continue;
+            const int32_t* f = P.tile_flags + I.ticket0 + j * P.n_layers + layer;
+            while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0)
+                __builtin_amdgcn_s_sleep(1);
+        }
+    }
+    __syncthreads();
+    char* dst = const_cast<char*>(src) + dshift;
+#pragma unroll
+    for (int i = 0; i < KTILE_CPT; ++i) {
+        if (uu[i] >= 0) {
+            if (I.cs >= 0) rotate_chunk<ESZ>(pl, v[i], uu[i], lcs, 0);
+            st16(dst + off[i], v[i]);
+        }
+    }
+}
+
+// Zeroes n 32-bit words (ticket counters and flags of the call's ordered-tile moves).
+struct KZeroParams {
+    int32_t* p;
+    int64_t n;
+};
+__global__ __launch_bounds__(TPB) void zero_words_kernel(const KZeroParams Z) {
+    for (int64_t i = int64_t(blockIdx.x) * TPB + threadIdx.x; i < Z.n; i += int64_t(gridDim.x) * TPB) Z.p[i] = 0;
+}
+
 // ------------------------------------------------------------------------ rotate in place ---
 
 // In-place R(delta) on listed rows: band units of all rows laid end to end, one plane per
@@ -768,7 +845,9 @@ extern "C" const char* leyline_last_hip_error(void) {
 // present, split further when a launch would exceed its item or cos/sin capacity.
 static int contig_launch_count(const leyline_cache* cache, const ContigSchedule& sched, int n_planes) {
     const int32_t cs_need = cos_sin_per_shift(cache);
-    int n = 0;
+    int n = sched.ws_bytes > 0 ? 1 : 0;      // clearing the tile workspace
+    for (const auto& group : sched.launches)
+        for (const ContigJobHost& j : group) n += j.kind == KJOB_TILE;   // one launch per tile move
     for (const auto& group : sched.launches)
         for (int kind : {int(KJOB_STUB), int(KJOB_CHAIN), int(KJOB_ROUND)}) {
             int items = 0, cs = 0;
@@ -791,21 +870,33 @@ static int contig_launch_count(const leyline_cache* cache, const ContigSchedule&
 
 extern "C" int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
                                     const leyline_directive* dirs, int32_t n_dirs,
-                                    int64_t* new_len_out, int32_t* n_launches_out) {
+                                    int64_t* new_len_out, int32_t* n_launches_out,
+                                    int32_t* n_tile_launches_out, int64_t* workspace_bytes_out) {
     ContigSchedule sched;
     int rc = plan_contig(cache, seq_len, dirs, n_dirs, &sched);
     if (rc) return rc;
     if (new_len_out) *new_len_out = sched.new_len;
     if (n_launches_out) *n_launches_out = contig_launch_count(cache, sched, cache->n_planes);
+    if (n_tile_launches_out) {
+        int32_t nt = 0;
+        for (const auto& group : sched.launches)
+            for (const ContigJobHost& j : group) nt += j.kind == KJOB_TILE;
+        *n_tile_launches_out = nt;
+    }
+    if (workspace_bytes_out) *workspace_bytes_out = sched.ws_bytes;
     return LEYLINE_OK;
 }
 
 extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len,
                                      const leyline_directive* dirs, int32_t n_dirs,
-                                     int64_t* new_len_out, void* stream) {
+                                     int64_t* new_len_out, void* workspace, int64_t workspace_bytes,
+                                     void* stream) {
     ContigSchedule sched;
     int rc = plan_contig(cache, seq_len, dirs, n_dirs, &sched);
     if (rc) return rc;
+    if (sched.ws_bytes > 0 && (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) ||
+                               workspace_bytes < sched.ws_bytes))
+        return LEYLINE_E_WORKSPACE;
     KPlane planes[LEYLINE_MAX_PLANES];
     int n_planes = 0;
     rc = describe_cache(cache, false, planes, &n_planes);
@@ -818,10 +909,49 @@ extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len
     for (const auto& jobs : sched.launches)
         for (const auto& j : jobs)
             for (int p = 0; p < n_planes; ++p)
-                if (item_threads(j, p) > INT32_MAX - TPB) return LEYLINE_E_INVAL;
+                if (item_threads(j, p) > INT32_MAX - std::max(TPB, KTILE_CHUNKS)) return LEYLINE_E_INVAL;
     const int32_t cs_need = cos_sin_per_shift(cache);
     hipStream_t s = static_cast<hipStream_t>(stream);
+    char* ws = static_cast<char*>(workspace);
+    if (sched.ws_bytes > 0) {
+        const int64_t words = sched.ws_bytes / 4;
+        const int64_t blocks = std::min<int64_t>((words + TPB - 1) / TPB, 1024);
+        rc = launch(zero_words_kernel, dim3(unsigned(blocks)), s, KZeroParams{reinterpret_cast<int32_t*>(ws), words});
+        if (rc) return rc;
+    }
     for (const auto& group : sched.launches) {
+        // ordered-tile moves: one launch each, items = the job's planes, one ticket per
+        // (tile, layer) of each item
+        for (const ContigJobHost& j : group) {
+            if (j.kind != KJOB_TILE) continue;
+            KContigParams P;
+            std::memset(&P, 0, sizeof(P));
+            std::vector<KCosSin> cs;
+            const int32_t cs0 = cs_need > 0 ? append_cos_sin(cache, j.delta, cs) : -1;
+            std::copy(cs.begin(), cs.end(), P.cs);
+            int64_t tickets = 0;
+            for (int p = 0; p < n_planes; ++p) {
+                KItem& it = P.items[P.n_items++];
+                std::memset(&it, 0, sizeof(it));
+                it.pl = planes[p];
+                it.src0 = j.src0;
+                it.count = j.count;
+                it.delta = j.delta;
+                it.kind = KJOB_TILE;
+                it.cs = (cs0 >= 0 && planes[p].rot != KROT_NONE) ? cs0 + planes[p].cs_off : -1;
+                it.n_tiles = int32_t(tile_count(j.count, planes[p].tpr));
+                it.ticket0 = int32_t(tickets);
+                tickets += int64_t(cache->n_layers) * it.n_tiles;
+            }
+            if (tickets > INT32_MAX - 1024) return LEYLINE_E_INVAL;
+            P.n_layers = cache->n_layers;
+            P.n_tickets = int32_t(tickets);
+            P.tile_counter = reinterpret_cast<int32_t*>(ws + j.ws_off);
+            P.tile_flags = P.tile_counter + KTILE_FLAGS_OFF;
+            rc = cache->dtype == LEYLINE_BF16 ? launch(contig_tile_kernel<2>, dim3(unsigned(tickets)), s, P, KTILE_TPB)
+                                              : launch(contig_tile_kernel<4>, dim3(unsigned(tickets)), s, P, KTILE_TPB);
+            if (rc) return rc;
+        }
         // the jobs of a group are independent; replacement copies, chains and rounds go to
         // separate launches, each a list of (job, plane) items selected by blockIdx.z
         for (int kind : {int(KJOB_STUB), int(KJOB_CHAIN), int(KJOB_ROUND)}) {

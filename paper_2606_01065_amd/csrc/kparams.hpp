@@ -63,8 +63,22 @@ enum : int32_t {
     KJOB_ROUND = 0,   // rows [src0, src0+count) move by delta with count <= |delta|: sources and
                       // destinations are disjoint, one chunk per thread
     KJOB_CHAIN = 1,   // rows [src0, src0+count) move by delta, count > |delta|: ordered chains
-    KJOB_STUB = 2     // count replacement rows copied to [dst0, dst0+count)
+                      // (layouts whose half-split partners need two-chunk units)
+    KJOB_STUB = 2,    // count replacement rows copied to [dst0, dst0+count)
+    KJOB_TILE = 3     // rows [src0, src0+count) move by delta, count > |delta|: ordered tiles
 };
+
+// Ordered-tile moves: chunks per thread and per tile (one tile = one workgroup, one layer).
+#ifndef LEYLINE_TILE_CPT
+#define LEYLINE_TILE_CPT 4
+#endif
+#ifndef LEYLINE_TILE_TPB
+#define LEYLINE_TILE_TPB 512
+#endif
+constexpr int KTILE_CPT = LEYLINE_TILE_CPT;
+constexpr int KTILE_TPB = LEYLINE_TILE_TPB;
+constexpr int KTILE_CHUNKS = KTILE_TPB * KTILE_CPT;
+constexpr int KTILE_FLAGS_OFF = 64;   // int32 words: the ticket counter, then the flags
 
 // One (job, plane) item of a contiguous launch, self-contained so that a workgroup reads its
 // parameters with one level of independent scalar loads (blockIdx.z selects the item).
@@ -78,6 +92,8 @@ struct KItem {
     int32_t kind;            // KJOB_*
     int32_t chains;          // chain: min(|delta|, count)
     int32_t cs;              // first cos/sin entry of this plane's pairs (-1: no rotation)
+    int32_t n_tiles;         // tile: tiles of TILE_CHUNKS chunks over the moved range, per layer
+    int32_t ticket0;         // tile: first ticket of this item (tickets: tile order x layers)
     int32_t pad;
 };
 
@@ -86,6 +102,10 @@ constexpr int KMAX_LAUNCH_ITEMS = 8;
 struct KContigParams {
     KItem items[KMAX_LAUNCH_ITEMS];
     int32_t n_items;
+    int32_t n_layers;
+    int32_t* tile_counter;   // tile launches: ticket counter, zero before the launch
+    int32_t* tile_flags;     // tile launches: one "source read" flag per ticket, zero before
+    int32_t n_tickets;
     int32_t pad;
     KCosSin cs[KMAX_CS];
 };

@@ -164,6 +164,10 @@ int check_sequence(int64_t seq_len, const leyline_directive* dirs, int32_t n_dir
 
 // ------------------------------------------------------------------------------ contiguous --
 
+int64_t tile_count(int64_t rows, int32_t tpr) {
+    return (rows * tpr + KTILE_CHUNKS - 1) / KTILE_CHUNKS;
+}
+
 int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_directive* dirs,
                 int32_t n_dirs, ContigSchedule* out) {
     KPlane planes[LEYLINE_MAX_PLANES];
@@ -184,6 +188,7 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
     if (new_len > cache->capacity) return LEYLINE_E_CAPACITY;
     out->new_len = new_len;
     out->launches.clear();
+    out->ws_bytes = 0;
 
     // Jobs: each downstream segment [e_j, s_{j+1}) moved by its running shift, each stub copied.
     std::vector<ContigJobHost> jobs;
@@ -229,6 +234,11 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
     // needing more than MAX_ROUNDS rounds runs as ordered chains in a single launch instead.
     const int n_levels = *std::max_element(level.begin(), level.end()) + 1;
     const int32_t cs_need = cos_sin_per_shift(cache);
+    // Moves too long for rounds run as ordered tiles when every plane moves single chunks
+    // (half-split bands whose partners cannot be exchanged between lanes use ordered chains).
+    bool tiles_ok = true;
+    for (int p = 0; p < n_planes; ++p)
+        if (planes[p].rot == KROT_NEOX && !planes[p].neox_lanes) tiles_ok = false;
     for (int lv = 0; lv < n_levels; ++lv) {
         std::vector<std::vector<ContigJobHost>> rounds(1);
         for (size_t a = 0; a < n; ++a) {
@@ -241,7 +251,17 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
             const int64_t m = x.delta < 0 ? -x.delta : x.delta;
             const int64_t nr = (x.count + m - 1) / m;
             if (nr > MAX_ROUNDS) {
-                rounds[0].push_back(x);       // KJOB_CHAIN
+                ContigJobHost y = x;
+                if (tiles_ok) {
+                    // ordered tiles: a ticket counter and one flag per (tile, layer, plane)
+                    y.kind = KJOB_TILE;
+                    y.ws_off = out->ws_bytes;
+                    int64_t flags = 0;
+                    for (int p = 0; p < n_planes; ++p) flags += int64_t(cache->n_layers) * tile_count(x.count, planes[p].tpr);
+                    if (flags > INT32_MAX - 1024) return LEYLINE_E_INVAL;
+                    out->ws_bytes += ((int64_t(KTILE_FLAGS_OFF) + flags) * 4 + 255) & ~int64_t(255);
+                }
+                rounds[0].push_back(y);       // KJOB_TILE or KJOB_CHAIN
                 continue;
             }
             if (int64_t(rounds.size()) < nr) rounds.resize(size_t(nr));

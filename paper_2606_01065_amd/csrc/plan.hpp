@@ -38,6 +38,7 @@ struct ContigJobHost {
     int32_t kind;       // KJOB_*
     int64_t src0, dst0, count, delta;
     int32_t dir;        // stub: directive index
+    int64_t ws_off = 0; // tile: byte offset of its ticket counter and flags in the workspace
 };
 
 // A move needing more rounds than this runs as ordered chains in one launch instead.
@@ -46,7 +47,11 @@ constexpr int64_t MAX_ROUNDS = 16;
 struct ContigSchedule {
     int64_t new_len = 0;
     std::vector<std::vector<ContigJobHost>> launches;
+    int64_t ws_bytes = 0;   // workspace of the ordered-tile moves (cleared on the device per call)
 };
+
+// Tiles of one ordered-tile move on a plane with `tpr` chunks per row.
+int64_t tile_count(int64_t rows, int32_t tpr);
 
 int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_directive* dirs,
                 int32_t n_dirs, ContigSchedule* out);

@@ -10,6 +10,7 @@ from __future__ import annotations
 import ctypes
 import os
 from ctypes import POINTER, Structure, c_double, c_int, c_int32, c_int64, c_void_p
+from collections import namedtuple
 from dataclasses import dataclass
 from typing import List, Optional, Sequence
 
@@ -98,9 +99,9 @@ def _load():
         "leyline_abi_version": (c_int, []),
         "leyline_last_hip_error": (ctypes.c_char_p, []),
         "leyline_contig_query": (c_int, [P(leyline_cache), c_int64, P(leyline_directive), c_int32,
-                                         P(c_int64), P(c_int32)]),
+                                         P(c_int64), P(c_int32), P(c_int32), P(c_int64)]),
         "leyline_splice_contig": (c_int, [P(leyline_cache), c_int64, P(leyline_directive), c_int32,
-                                          P(c_int64), c_void_p]),
+                                          P(c_int64), c_void_p, c_int64, c_void_p]),
         "leyline_paged_query": (c_int, [P(leyline_cache), c_int32, P(c_int32), c_int32,
                                         P(leyline_directive), c_int32, P(c_int32), P(c_int32),
                                         P(c_int32), P(c_int64)]),
@@ -205,7 +206,12 @@ def make_cache(planes: Sequence[PlaneSpec], paged: bool = False) -> leyline_cach
             keep.append(arr)
             pl.inv_freq = ctypes.cast(arr, POINTER(c_double))
     c._keep = keep           # keep host tables alive with the descriptor
+    c._device = getattr(t0, "device", None)
     return c
+
+
+def _cache_device(cache: leyline_cache):
+    return getattr(cache, "_device", None) or "cuda"
 
 
 def make_directives(dirs: Sequence[dict]) -> ctypes.Array:
@@ -245,20 +251,39 @@ def _check(rc: int, where: str) -> None:
 
 # ----------------------------------------------------------------------------- entry points --
 
-def leyline_contig_query(cache: leyline_cache, seq_len: int, dirs, n_dirs: int):
-    """Returns (new_len, n_launches) without enqueueing anything."""
-    new_len, n_launch = c_int64(0), c_int32(0)
+ContigQuery = namedtuple("ContigQuery", "new_len launches tile_launches workspace_bytes")
+
+
+def leyline_contig_query(cache: leyline_cache, seq_len: int, dirs, n_dirs: int) -> ContigQuery:
+    """(new_len, launches, tile_launches, workspace_bytes), without enqueueing anything."""
+    new_len, n_launch, n_tile, ws = c_int64(0), c_int32(0), c_int32(0), c_int64(0)
     rc = _lib.leyline_contig_query(ctypes.byref(cache), seq_len, dirs, n_dirs, ctypes.byref(new_len),
-                                   ctypes.byref(n_launch))
+                                   ctypes.byref(n_launch), ctypes.byref(n_tile), ctypes.byref(ws))
     _check(rc, "leyline_contig_query")
-    return new_len.value, n_launch.value
+    return ContigQuery(new_len.value, n_launch.value, n_tile.value, ws.value)
 
 
-def leyline_splice_contig(cache: leyline_cache, seq_len: int, dirs, n_dirs: int, stream=None) -> int:
-    """Returns the new sequence length."""
+def contig_workspace(cache: leyline_cache, seq_len: int, dirs, n_dirs: int, device="cuda"):
+    """A device workspace tensor of the size the splice needs (None when it needs none)."""
+    import torch
+    need = leyline_contig_query(cache, seq_len, dirs, n_dirs).workspace_bytes
+    return torch.empty(need, dtype=torch.uint8, device=device) if need else None
+
+
+def leyline_splice_contig(cache: leyline_cache, seq_len: int, dirs, n_dirs: int, stream=None,
+                          workspace=None) -> int:
+    """Returns the new sequence length.  workspace: a device tensor of at least the queried size;
+    when None, one is allocated with torch on the cache's device if the splice needs it."""
+    if workspace is None:
+        need = leyline_contig_query(cache, seq_len, dirs, n_dirs).workspace_bytes
+        if need:
+            import torch
+            workspace = torch.empty(need, dtype=torch.uint8, device=_cache_device(cache))
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
     new_len = c_int64(0)
     rc = _lib.leyline_splice_contig(ctypes.byref(cache), seq_len, dirs, n_dirs,
-                                    ctypes.byref(new_len), _stream(stream))
+                                    ctypes.byref(new_len), ws_ptr, ws_len, _stream(stream))
     _check(rc, "leyline_splice_contig")
     return new_len.value
 

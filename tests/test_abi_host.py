@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
     for name in declared:
         assert hasattr(lib, name), name
     assert sorted(L.SYMBOLS) == declared
-    assert L.leyline_abi_version() == 1
+    assert L.leyline_abi_version() == 2
     assert "overlap" in L.strerror(L.E_OVERLAP)
 
 
@@ -84,7 +84,8 @@ def _dirs(spec, stub_ptr=0x20000):
 def _contig_rc(cache, n, spec):
     new_len = ctypes.c_int64(-1)
     d = _dirs(spec)
-    return L._lib.leyline_splice_contig(ctypes.byref(cache), n, d, len(spec), ctypes.byref(new_len), None)
+    return L._lib.leyline_splice_contig(ctypes.byref(cache), n, d, len(spec), ctypes.byref(new_len),
+                                        None, 0, None)
 
 
 def test_contig_validation_codes():
@@ -97,11 +98,11 @@ def test_contig_validation_codes():
     assert _contig_rc(c, 60, [(10, 10, 5)]) == L.E_CAPACITY               # 65 > 64 rows
     d = _dirs([(1, 2, 0)])
     d[0].mode = L.FORGET
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None) == L.E_MODE
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, 0, None) == L.E_MODE
     d = _dirs([(1, 2, 3)], stub_ptr=0)                                    # stub pointer missing
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None) == L.E_INVAL
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, 0, None) == L.E_INVAL
     d = _dirs([(1, 2, 3)], stub_ptr=0x20008)                              # stub misaligned
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None) == L.E_INVAL
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, 0, None) == L.E_INVAL
     bad = _mla_cache(ptr=0x10008)                                         # cache misaligned
     assert _contig_rc(bad, 10, [(1, 2, 0)]) == L.E_INVAL
     c.planes[0].rot_dim = 63                                              # odd rotary band
@@ -114,19 +115,35 @@ def test_contig_validation_codes():
     assert _contig_rc(c, 10, [(1, 2, 0)]) == L.E_INVAL
 
 
-def test_contig_query_reports_rounds_and_launches():
+def test_contig_query_reports_rounds_tiles_and_workspace():
     """A left shift by m of D downstream rows runs as ceil(D/m) rounds (one launch each) plus one
-    launch for the replacement copy; very small shifts run as ordered chains in one launch."""
-    c = _mla_cache(cap=64)
-    new_len, n = L.leyline_contig_query(c, 60, _dirs([(10, 20, 2)]), 1)       # m=8, D=40
-    assert (new_len, n) == (52, 5 + 1)
-    new_len, n = L.leyline_contig_query(c, 60, _dirs([(10, 11, 0)]), 1)       # m=1, D=49: chains
-    assert (new_len, n) == (59, 1)
-    new_len, n = L.leyline_contig_query(c, 60, _dirs([(10, 12, 4)]), 1)       # m=2 right, D=48
-    assert (new_len, n) == (62, 1 + 1)                                       # chains, then stub
+    launch for the replacement copy and needs no workspace; when that takes more than 16 rounds
+    the move runs as ordered tiles in one launch, after one launch that clears the tiles'
+    counter and flags in the workspace."""
+    c = _mla_cache(cap=64)                                                   # 2 layers, 72 chunks/row
+    q = L.leyline_contig_query(c, 60, _dirs([(10, 20, 2)]), 1)               # m=8, D=40
+    assert (q.new_len, q.launches, q.tile_launches, q.workspace_bytes) == (52, 5 + 1, 0, 0)
+    q = L.leyline_contig_query(c, 60, _dirs([(10, 11, 0)]), 1)               # m=1, D=49: tiles
+    tiles = -(-49 * 72 // 2048)                                              # per layer
+    assert (q.new_len, q.launches, q.tile_launches) == (59, 1 + 1, 1)
+    assert q.workspace_bytes == -(-(64 + 2 * tiles) * 4 // 256) * 256
+    q = L.leyline_contig_query(c, 60, _dirs([(10, 12, 4)]), 1)               # m=2 right, D=48
+    assert (q.new_len, q.launches, q.tile_launches) == (62, 1 + 1 + 1, 1)   # clear, tiles, stub
     with pytest.raises(L.LeylineError) as e:
         L.leyline_contig_query(c, 60, _dirs([(10, 10, 5)]), 1)
     assert e.value.code == L.E_CAPACITY
+
+
+def test_contig_tiles_need_a_workspace():
+    c = _mla_cache(cap=64)
+    new_len = ctypes.c_int64(-1)
+    d = _dirs([(10, 11, 0)])
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 60, d, 1, ctypes.byref(new_len),
+                                        None, 0, None) == L.E_WORKSPACE
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 60, d, 1, ctypes.byref(new_len),
+                                        0x10080, 4096, None) == L.E_WORKSPACE      # misaligned
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 60, d, 1, ctypes.byref(new_len),
+                                        0x10000, 16, None) == L.E_WORKSPACE        # too small
 
 
 def test_contig_noop_calls_do_not_need_a_device():
@@ -134,10 +151,10 @@ def test_contig_noop_calls_do_not_need_a_device():
     nothing and reports the unchanged length."""
     c = _mla_cache()
     new_len = ctypes.c_int64(-1)
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 40, None, 0, ctypes.byref(new_len), None) == 0
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 40, None, 0, ctypes.byref(new_len), None, 0, None) == 0
     assert new_len.value == 40
     d = _dirs([(10, 10, 0)])
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 40, d, 1, ctypes.byref(new_len), None) == 0
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 40, d, 1, ctypes.byref(new_len), None, 0, None) == 0
     assert new_len.value == 40
 
 

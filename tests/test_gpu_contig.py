@@ -34,11 +34,19 @@ def _dir_dicts(wl, stubs):
                  stub_len=d.stub_len) for j, d in enumerate(wl.dirs)]
 
 
-def _run_and_check(L, wl, planes_dev, stubs_dev, label):
-    """Snapshot inputs, splice on the GPU, splice in the oracle, compare rows [0, n')."""
+def _run_and_check(L, wl, planes_dev, stubs_dev, label, layers=None):
+    """Snapshot inputs, splice on the GPU, splice in the oracle, compare rows [0, n') (of the
+    listed layers only, when given)."""
     print(f"[case] {label}", flush=True)
-    before = [host(t) for t in planes_dev]
-    stubs_h = [[host(s) for s in per] for per in stubs_dev]
+    if layers is not None:
+        sel = torch.tensor(layers, device=DEV)
+        before = [host(t.index_select(0, sel)) for t in planes_dev]
+        stubs_h = [[host(s.index_select(0, sel)) for s in per] for per in stubs_dev]
+    else:
+        before = [host(t) for t in planes_dev]
+    if layers is None:
+        stubs_h = [[host(s) for s in per] for per in stubs_dev]
+    n_check = wl.n_layers if layers is None else len(layers)
     cache = L.make_cache(_specs(L, wl, planes_dev))
     dirs = L.make_directives(_dir_dicts(wl, stubs_dev))
     n = wl.seq_lens[0]
@@ -48,9 +56,10 @@ def _run_and_check(L, wl, planes_dev, stubs_dev, label):
     assert new_len == O.new_length(n, odirs)
     for pi, (desc, t) in enumerate(zip(wl.planes, planes_dev)):
         plane = oracle_plane(desc)
-        got = host(t).reshape(wl.n_layers, wl.capacity, plane.row_elems)
-        src = before[pi].reshape(wl.n_layers, wl.capacity, plane.row_elems)
-        stubs = [s[pi].reshape(wl.n_layers, s[pi].shape[1], plane.row_elems) for s in stubs_h]
+        got_t = t if layers is None else t.index_select(0, torch.tensor(layers, device=DEV))
+        got = host(got_t).reshape(n_check, wl.capacity, plane.row_elems)
+        src = before[pi].reshape(n_check, wl.capacity, plane.row_elems)
+        stubs = [s[pi].reshape(n_check, s[pi].shape[1], plane.row_elems) for s in stubs_h]
         want, _ = O.splice_contig(src, n, odirs, stubs, plane, wl.dtype)
         assert_rows_match(got[:, :new_len], want[:, :new_len], plane, wl.dtype,
                           inputs=_inputs_for_new_rows(src, n, odirs, stubs),
@@ -159,6 +168,34 @@ def test_gqa_llama3_8b_16k_full(L):
     n_new = _run_and_check(L, wl, planes_dev, stubs_dev, "gqa_llama3_8b_16k")
     assert n_new == 16384 - 2024
     print(f"[info] bf16 rotary elements bit-identical to the oracle: {PU.LAST_BF16_EXACT_FRACTION:.6f}")
+
+
+@pytest.mark.parametrize("name,dirs,extra", [
+    ("mla_dsv3_32k", [W.Dir(2048, 2049, 0)], 0),           # shift -1: ordered tiles, ascending
+    ("mla_dsv3_32k", [W.Dir(2048, 2048, 3)], 3),           # insertion, shift +3: descending
+    ("gqa_llama3_8b_16k", [W.Dir(4096, 4103, 0)], 0),      # shift -7, K and V planes in one launch
+])
+def test_small_shift_full_size(L, name, dirs, extra):
+    """Shifts far too small for rounds run as ordered tiles; first, middle and last layers are
+    compared whole against the oracle."""
+    base = W.WORKLOADS[name]()
+    wl = W.Workload(name, base.n_layers, base.dtype, base.planes, dirs, base.seq_lens,
+                    capacity=base.capacity + extra, seed=base.seed)
+    planes_dev, stubs_dev = W.alloc_contig(wl, DEV)
+    cache = L.make_cache(_specs(L, wl, planes_dev))
+    q = L.leyline_contig_query(cache, wl.seq_lens[0], L.make_directives(_dir_dicts(wl, stubs_dev)), len(dirs))
+    assert q.tile_launches == 1 and q.workspace_bytes > 0
+    layers = [0, wl.n_layers // 2, wl.n_layers - 1]
+    _run_and_check(L, wl, planes_dev, stubs_dev, f"{name} small shift {dirs}", layers=layers)
+
+
+def test_mla_dsv3_32k_edits8(L):
+    """Eight edits drawn like the paper's randomized edit suite, both signs, one call."""
+    wl = W.mla_dsv3_32k_edits8()
+    planes_dev, stubs_dev = W.alloc_contig(wl, DEV)
+    layers = [0, 30, 60]
+    n_new = _run_and_check(L, wl, planes_dev, stubs_dev, "mla_dsv3_32k_edits8", layers=layers)
+    assert n_new == 32768 + sum(d.stub_len - (d.span_end - d.span_start) for d in wl.dirs)
 
 
 @pytest.mark.parametrize("paged", [False, True])

@@ -126,6 +126,25 @@ def mla_dsv3_paged_131k(seed: int = 5, n_layers: int = 61) -> Workload:
                     page_size=64, seed=seed)
 
 
+def mla_dsv3_32k_edits8(seed: int = 6) -> Workload:
+    """The 32K MLA contiguous cache with 8 non-overlapping edits in one call, drawn like the
+    paper's randomized edit suite: span sizes uniform in [8, 200] tokens at uniform positions,
+    replacement lengths uniform in [0, 2 * span], so shifts take both signs and stay small."""
+    rng = np.random.default_rng(seed)
+    n = 32768
+    spans: List[Tuple[int, int]] = []
+    while len(spans) < 8:
+        ln = int(rng.integers(8, 201))
+        s = int(rng.integers(0, n - ln + 1))
+        if all(s + ln <= a or s >= b for a, b in spans):
+            spans.append((s, s + ln))
+    spans.sort()
+    dirs = [Dir(a, b, int(rng.integers(0, 2 * (b - a) + 1))) for a, b in spans]
+    grow = max(0, max(int(x) for x in np.cumsum([d.stub_len - (d.span_end - d.span_start) for d in dirs])))
+    return Workload("mla_dsv3_32k_edits8", 61, "bf16", [mla_plane()], dirs, [n], capacity=n + grow,
+                    seed=seed)
+
+
 def mla_dsv3_slots_32k() -> Workload:
     """The 32K MLA splice on a token-slot cache (page size 1, slots scattered over the pool): the
     downstream tokens keep their slots, only their K_pe bands are rotated in place."""
@@ -147,6 +166,7 @@ WORKLOADS = {
     "mla_dsv3_paged_b64": mla_dsv3_paged_b64,
     "gqa_llama3_8b_16k": gqa_llama3_8b_16k,
     "mla_dsv3_paged_131k": mla_dsv3_paged_131k,
+    "mla_dsv3_32k_edits8": mla_dsv3_32k_edits8,
     "mla_dsv3_slots_32k": mla_dsv3_slots_32k,
     "gqa_llama3_8b_slots_16k": gqa_llama3_8b_slots_16k,
 }
