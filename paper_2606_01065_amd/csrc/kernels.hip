@@ -488,29 +488,28 @@ __global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KContigPar
     const char* src = pl.base + int64_t(layer) * pl.layer_stride + I.src0 * pl.token_stride;
     const int64_t dshift = I.delta * pl.token_stride;
     // Every slot loads (past the end of the range: the range's last chunk, which stays unused),
-    // so that all loads are issued back to back without branches between them.
+    // so that all loads are issued back to back without branches between them.  Row and column
+    // are recomputed at store time rather than kept in registers.
+    const int32_t g0 = q * KTILE_CHUNKS + int32_t(threadIdx.x);
     u32x4 v[KTILE_CPT];
-    int64_t off[KTILE_CPT];
-    int32_t uu[KTILE_CPT];
 #pragma unroll
     for (int i = 0; i < KTILE_CPT; ++i) {
-        const int32_t g = q * KTILE_CHUNKS + i * KTILE_TPB + int32_t(threadIdx.x);
-        const int32_t gc = min(g, total - 1);
+        const int32_t gc = min(g0 + i * KTILE_TPB, total - 1);
         const int32_t r = fdiv(gc, pl.tpr_div);
-        uu[i] = g < total ? gc - r * pl.tpr : -1;
-        off[i] = int64_t(r) * pl.token_stride + int64_t(gc - r * pl.tpr) * 16;
-        v[i] = ld16(src + off[i]);
+        v[i] = ld16(src + int64_t(r) * pl.token_stride + int64_t(gc - r * pl.tpr) * 16);
     }
     if (I.cs >= 0) stage_cs<KTILE_TPB>(lcs, P.cs, I.cs, pl.n_pairs);
     __builtin_amdgcn_s_waitcnt(0);          // this thread's loads have returned
     __syncthreads();                        // ... and every thread's
     if (threadIdx.x == 0) {
-        __hip_atomic_store(P.tile_flags + ticket, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const int64_t M = (down ? -I.delta : I.delta) * pl.tpr;   // shift in chunks
+        int32_t* flags = P.tile_flags + I.flag0;                 // this item's flags, by local ticket
+        __hip_atomic_store(flags + local, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // earlier tiles whose source this tile's destination overlaps: processing order minus d
+        const int64_t M = (down ? -I.delta : I.delta) * pl.tpr;  // shift in chunks
         for (int64_t d = M / KTILE_CHUNKS; d <= (M + KTILE_CHUNKS - 1) / KTILE_CHUNKS; ++d) {
             const int64_t j = order - d;
             if (d == 0 || j < 0) continue;
-            const int32_t* f = P.tile_flags + I.ticket0 + j * P.n_layers + layer;
+            const int32_t* f = flags + j * P.n_layers + layer;
             while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0)
                 __builtin_amdgcn_s_sleep(1);
         }
@@ -519,9 +518,11 @@ __global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KContigPar
     char* dst = const_cast<char*>(src) + dshift;
 #pragma unroll
     for (int i = 0; i < KTILE_CPT; ++i) {
-        if (uu[i] >= 0) {
-            if (I.cs >= 0) rotate_chunk<ESZ>(pl, v[i], uu[i], lcs, 0);
-            st16(dst + off[i], v[i]);
+        const int32_t g = g0 + i * KTILE_TPB;
+        if (g < total) {
+            const int32_t r = fdiv(g, pl.tpr_div), u = g - r * pl.tpr;
+            if (I.cs >= 0) rotate_chunk<ESZ>(pl, v[i], u, lcs, 0);
+            st16(dst + int64_t(r) * pl.token_stride + int64_t(u) * 16, v[i]);
         }
     }
 }
@@ -843,13 +844,15 @@ extern "C" const char* leyline_last_hip_error(void) {
 
 // Launches of one contiguous splice: per group of independent jobs, one launch per job kind
 // present, split further when a launch would exceed its item or cos/sin capacity.
-static int contig_launch_count(const leyline_cache* cache, const ContigSchedule& sched, int n_planes) {
+// Kernel launches of a schedule (only those of one job kind when only_kind >= 0), grouped the way
+// leyline_splice_contig groups them.
+static int contig_launch_count(const leyline_cache* cache, const ContigSchedule& sched, int n_planes,
+                               int only_kind = -1) {
     const int32_t cs_need = cos_sin_per_shift(cache);
-    int n = sched.ws_bytes > 0 ? 1 : 0;      // clearing the tile workspace
+    int n = (sched.ws_bytes > 0 && only_kind < 0) ? 1 : 0;      // clearing the tile workspace
     for (const auto& group : sched.launches)
-        for (const ContigJobHost& j : group) n += j.kind == KJOB_TILE;   // one launch per tile move
-    for (const auto& group : sched.launches)
-        for (int kind : {int(KJOB_STUB), int(KJOB_CHAIN), int(KJOB_ROUND)}) {
+        for (int kind : {int(KJOB_TILE), int(KJOB_STUB), int(KJOB_CHAIN), int(KJOB_ROUND)}) {
+            if (only_kind >= 0 && kind != only_kind) continue;
             int items = 0, cs = 0;
             bool open = false;
             for (const ContigJobHost& j : group) {
@@ -877,12 +880,7 @@ extern "C" int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
     if (rc) return rc;
     if (new_len_out) *new_len_out = sched.new_len;
     if (n_launches_out) *n_launches_out = contig_launch_count(cache, sched, cache->n_planes);
-    if (n_tile_launches_out) {
-        int32_t nt = 0;
-        for (const auto& group : sched.launches)
-            for (const ContigJobHost& j : group) nt += j.kind == KJOB_TILE;
-        *n_tile_launches_out = nt;
-    }
+    if (n_tile_launches_out) *n_tile_launches_out = contig_launch_count(cache, sched, cache->n_planes, KJOB_TILE);
     if (workspace_bytes_out) *workspace_bytes_out = sched.ws_bytes;
     return LEYLINE_OK;
 }
@@ -920,36 +918,57 @@ extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len
         if (rc) return rc;
     }
     for (const auto& group : sched.launches) {
-        // ordered-tile moves: one launch each, items = the job's planes, one ticket per
-        // (tile, layer) of each item
-        for (const ContigJobHost& j : group) {
-            if (j.kind != KJOB_TILE) continue;
+        // Ordered-tile moves of this group (independent of each other): batched into launches of
+        // up to KMAX_LAUNCH_ITEMS (job, plane) items within the cos/sin table.  A launch counts
+        // tickets on the counter of its first job's workspace region; each item's flags sit in its
+        // own job's region.
+        {
             KContigParams P;
             std::memset(&P, 0, sizeof(P));
             std::vector<KCosSin> cs;
-            const int32_t cs0 = cs_need > 0 ? append_cos_sin(cache, j.delta, cs) : -1;
-            std::copy(cs.begin(), cs.end(), P.cs);
             int64_t tickets = 0;
-            for (int p = 0; p < n_planes; ++p) {
-                KItem& it = P.items[P.n_items++];
-                std::memset(&it, 0, sizeof(it));
-                it.pl = planes[p];
-                it.src0 = j.src0;
-                it.count = j.count;
-                it.delta = j.delta;
-                it.kind = KJOB_TILE;
-                it.cs = (cs0 >= 0 && planes[p].rot != KROT_NONE) ? cs0 + planes[p].cs_off : -1;
-                it.n_tiles = int32_t(tile_count(j.count, planes[p].tpr));
-                it.ticket0 = int32_t(tickets);
-                tickets += int64_t(cache->n_layers) * it.n_tiles;
+            auto flush_tiles = [&]() -> int {
+                if (P.n_items == 0) return LEYLINE_OK;
+                if (tickets > INT32_MAX - 1024 || cs.size() > size_t(KMAX_CS)) return LEYLINE_E_INVAL;
+                std::copy(cs.begin(), cs.end(), P.cs);
+                P.n_layers = cache->n_layers;
+                P.n_tickets = int32_t(tickets);
+                P.tile_flags = reinterpret_cast<int32_t*>(ws);
+                const dim3 grid(static_cast<unsigned>(tickets), 1, 1);
+                const int r = cache->dtype == LEYLINE_BF16 ? launch(contig_tile_kernel<2>, grid, s, P, KTILE_TPB)
+                                                           : launch(contig_tile_kernel<4>, grid, s, P, KTILE_TPB);
+                std::memset(&P, 0, sizeof(P));
+                cs.clear();
+                tickets = 0;
+                return r;
+            };
+            for (const ContigJobHost& j : group) {
+                if (j.kind != KJOB_TILE) continue;
+                if (P.n_items + n_planes > KMAX_LAUNCH_ITEMS || int32_t(cs.size()) + cs_need > KMAX_CS) {
+                    rc = flush_tiles();
+                    if (rc) return rc;
+                }
+                if (P.n_items == 0) P.tile_counter = reinterpret_cast<int32_t*>(ws + j.ws_off);
+                const int32_t cs0 = cs_need > 0 ? append_cos_sin(cache, j.delta, cs) : -1;
+                int64_t flag = j.ws_off / 4 + KTILE_FLAGS_OFF;
+                for (int p = 0; p < n_planes; ++p) {
+                    KItem& it = P.items[P.n_items++];
+                    std::memset(&it, 0, sizeof(it));
+                    it.pl = planes[p];
+                    it.src0 = j.src0;
+                    it.count = j.count;
+                    it.delta = j.delta;
+                    it.kind = KJOB_TILE;
+                    it.cs = (cs0 >= 0 && planes[p].rot != KROT_NONE) ? cs0 + planes[p].cs_off : -1;
+                    it.n_tiles = int32_t(tile_count(j.count, planes[p].tpr));
+                    it.ticket0 = int32_t(tickets);
+                    it.flag0 = int32_t(flag);
+                    const int64_t n = int64_t(cache->n_layers) * it.n_tiles;
+                    tickets += n;
+                    flag += n;
+                }
             }
-            if (tickets > INT32_MAX - 1024) return LEYLINE_E_INVAL;
-            P.n_layers = cache->n_layers;
-            P.n_tickets = int32_t(tickets);
-            P.tile_counter = reinterpret_cast<int32_t*>(ws + j.ws_off);
-            P.tile_flags = P.tile_counter + KTILE_FLAGS_OFF;
-            rc = cache->dtype == LEYLINE_BF16 ? launch(contig_tile_kernel<2>, dim3(unsigned(tickets)), s, P, KTILE_TPB)
-                                              : launch(contig_tile_kernel<4>, dim3(unsigned(tickets)), s, P, KTILE_TPB);
+            rc = flush_tiles();
             if (rc) return rc;
         }
         // the jobs of a group are independent; replacement copies, chains and rounds go to

@@ -70,10 +70,10 @@ enum : int32_t {
 
 // Ordered-tile moves: chunks per thread and per tile (one tile = one workgroup, one layer).
 #ifndef LEYLINE_TILE_CPT
-#define LEYLINE_TILE_CPT 4
+#define LEYLINE_TILE_CPT 8
 #endif
 #ifndef LEYLINE_TILE_TPB
-#define LEYLINE_TILE_TPB 512
+#define LEYLINE_TILE_TPB 1024
 #endif
 constexpr int KTILE_CPT = LEYLINE_TILE_CPT;
 constexpr int KTILE_TPB = LEYLINE_TILE_TPB;
@@ -92,8 +92,10 @@ struct KItem {
     int32_t kind;            // KJOB_*
     int32_t chains;          // chain: min(|delta|, count)
     int32_t cs;              // first cos/sin entry of this plane's pairs (-1: no rotation)
-    int32_t n_tiles;         // tile: tiles of TILE_CHUNKS chunks over the moved range, per layer
-    int32_t ticket0;         // tile: first ticket of this item (tickets: tile order x layers)
+    int32_t n_tiles;         // tile: tiles of KTILE_CHUNKS chunks over the moved range, per layer
+    int32_t ticket0;         // tile: first ticket of this item in the launch
+    int32_t flag0;           // tile: first of the item's flags (int32 words from tile_flags), one
+                             // per (tile in processing order, layer)
     int32_t pad;
 };
 
@@ -104,7 +106,7 @@ struct KContigParams {
     int32_t n_items;
     int32_t n_layers;
     int32_t* tile_counter;   // tile launches: ticket counter, zero before the launch
-    int32_t* tile_flags;     // tile launches: one "source read" flag per ticket, zero before
+    int32_t* tile_flags;     // tile launches: base of the items' "source read" flags, zero before
     int32_t n_tickets;
     int32_t pad;
     KCosSin cs[KMAX_CS];

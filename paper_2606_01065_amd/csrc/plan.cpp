@@ -237,8 +237,11 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
     // Moves too long for rounds run as ordered tiles when every plane moves single chunks
     // (half-split bands whose partners cannot be exchanged between lanes use ordered chains).
     bool tiles_ok = true;
-    for (int p = 0; p < n_planes; ++p)
+    int64_t row_bytes_all = 0;
+    for (int p = 0; p < n_planes; ++p) {
         if (planes[p].rot == KROT_NEOX && !planes[p].neox_lanes) tiles_ok = false;
+        row_bytes_all += planes[p].row_bytes;
+    }
     for (int lv = 0; lv < n_levels; ++lv) {
         std::vector<std::vector<ContigJobHost>> rounds(1);
         for (size_t a = 0; a < n; ++a) {
@@ -250,7 +253,11 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
             }
             const int64_t m = x.delta < 0 ? -x.delta : x.delta;
             const int64_t nr = (x.count + m - 1) / m;
-            if (nr > MAX_ROUNDS) {
+            // Rounds cost one launch each: they are used for a single round, or when every round
+            // moves enough bytes to fill the device; otherwise ordered tiles (one launch shared
+            // by the level's tile moves) are faster.
+            const bool big_rounds = nr == 1 || m * row_bytes_all * cache->n_layers >= ROUND_MIN_BYTES;
+            if (nr > MAX_ROUNDS || (tiles_ok && !big_rounds)) {
                 ContigJobHost y = x;
                 if (tiles_ok) {
                     // ordered tiles: a ticket counter and one flag per (tile, layer, plane)
@@ -280,6 +287,7 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
                 rounds[size_t(r)].push_back(ContigJobHost{KJOB_ROUND, lo, 0, hi - lo, x.delta, x.dir});
             }
         }
+        if (out->ws_bytes / 4 > INT32_MAX - 1024) return LEYLINE_E_INVAL;
         for (const auto& rj : rounds) {
             std::vector<ContigJobHost> cur;
             int32_t cs_used = 0;

@@ -43,6 +43,8 @@ struct ContigJobHost {
 
 // A move needing more rounds than this runs as ordered chains in one launch instead.
 constexpr int64_t MAX_ROUNDS = 16;
+// Rounds moving fewer bytes than this (all layers and planes) are not worth a launch each.
+constexpr int64_t ROUND_MIN_BYTES = int64_t(64) << 20;
 
 struct ContigSchedule {
     int64_t new_len = 0;
