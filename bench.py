@@ -66,7 +66,7 @@ def measured_traffic(workload):
         t = json.load(f)
     if t.get("kernel_sha") != kernel_sha():
         return None
-    return {k: t[k] for k in ("fetch_bytes", "write_bytes", "total_bytes", "calibration", "per")}
+    return t
 
 
 def row_bytes(wl):
@@ -192,7 +192,8 @@ def main():
     achieved = alg_bytes / (splice_ms * 1e-3) / 1e9
     ms_per_step = total_ms / args.steps
     copy_gbps, _ = copy_ceiling(alg_bytes, dev, stream)
-    traffic = measured_traffic(wl.name)
+    rec = measured_traffic(wl.name)
+    traffic = rec["dispatch_bytes"] if rec and rec.get("kernel") == kernel else None
     out = {
         "metric": METRIC,
         "value": moved / (ms_per_step * 1e-3),
@@ -223,11 +224,15 @@ def main():
             "unit": "GB/s",
             "frac": achieved / PEAK_HBM_GBPS,
             "traffic": traffic,
+            "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)",
+            "algorithmic_bytes_per_launch": alg_bytes / max(1, launches),
             "algorithmic_bytes_per_splice": alg_bytes,
+            "traffic_per_splice": None if rec is None else {k: rec[k] for k in ("fetch_bytes", "write_bytes", "total_bytes")},
             "splice_ms": splice_ms,
             "launches_per_splice": launches,
             "avg_launch_ms": splice_ms / max(1, launches),
             "d2d_copy_GBps": copy_gbps,
+            "kernel_sha": kernel_sha(),
         },
     }
     if not args.no_cpu_baseline:
@@ -351,6 +356,16 @@ def _last_dispatch(rows, match):
     return max(ids) if ids else -1
 
 
+def _profiled_sha(trace_dir):
+    """kernel_sha printed by the profiled bench run (its output sits in <trace_dir>.log)."""
+    log = trace_dir.rstrip("/") + ".log"
+    if os.path.exists(log):
+        for line in open(log):
+            if line.startswith("{") and '"kernel_sha"' in line:
+                return json.loads(line)["roofline"]["kernel_sha"]
+    raise SystemExit(f"no bench JSON line with kernel_sha in {log}")
+
+
 def _flag(cmd, name, default):
     parts = cmd.split()
     return int(parts[parts.index(name) + 1]) if name in parts else default
@@ -389,9 +404,12 @@ def summarize(args):
     fetch = _read_csv(fetch_dir, "counter_collection")
     write = _read_csv(write_dir, "counter_collection")
     is_k = lambda name: kernel in name
+    is_lib = lambda name: "leyline::" in name
     is_copy = lambda name: "leyline" not in name and ("copyBuffer" in name or "copy" in name.lower())
     f_k = _counter_per_dispatch(fetch, "FETCH_SIZE", is_k)
     w_k = _counter_per_dispatch(write, "WRITE_SIZE", is_k)
+    f_all = _counter_per_dispatch(fetch, "FETCH_SIZE", is_lib)      # every library kernel of the splice
+    w_all = _counter_per_dispatch(write, "WRITE_SIZE", is_lib)
     # calibration copies: the device copies the bench issues after its last splice
     f_c = _counter_per_dispatch(fetch, "FETCH_SIZE", is_copy, _last_dispatch(fetch, is_k))
     w_c = _counter_per_dispatch(write, "WRITE_SIZE", is_copy, _last_dispatch(write, is_k))
@@ -420,14 +438,18 @@ def summarize(args):
                      f"way, {len(f_c)} / {len(w_c)} dispatches): FETCH_SIZE {sum(f_c):.0f} KiB, "
                      f"WRITE_SIZE {sum(w_c):.0f} KiB in total -> bytes per counted byte "
                      f"{cal_f:.3f} (fetch), {cal_w:.3f} (write)")
-        fetch_b = sum(f_k) * 1024 * cal_f / splices
-        write_b = sum(w_k) * 1024 * cal_w / splices
-        lines.append(f"per splice: fetched {fetch_b/1e9:.4f} GB, written {write_b/1e9:.4f} GB; "
-                     f"algorithmic {alg/1e9:.4f} GB; measured/algorithmic "
-                     f"{(fetch_b + write_b)/alg:.3f}")
-        rec = dict(kernel_sha=kernel_sha(), workload=wl.name, fetch_bytes=fetch_b,
-                   write_bytes=write_b, total_bytes=fetch_b + write_b, calibration=[cal_f, cal_w],
-                   per="splice", algorithmic_bytes=alg)
+        fetch_b = sum(f_all) * 1024 * cal_f / splices
+        write_b = sum(w_all) * 1024 * cal_w / splices
+        dom_b = (sum(f_k) * cal_f + sum(w_k) * cal_w) * 1024 / splices
+        lines.append(f"per splice, all library kernels: fetched {fetch_b/1e9:.4f} GB, written "
+                     f"{write_b/1e9:.4f} GB; algorithmic {alg/1e9:.4f} GB; measured/algorithmic "
+                     f"{(fetch_b + write_b)/alg:.3f}; {kernel} alone {dom_b/1e9:.4f} GB "
+                     f"({100 * dom_b / (fetch_b + write_b):.1f}%)")
+        rec = dict(kernel_sha=_profiled_sha(trace_dir), workload=wl.name, kernel=kernel,
+                   dispatch_bytes=(np.mean(f_k) * cal_f + np.mean(w_k) * cal_w) * 1024,
+                   dispatches_per_splice=per_splice, fetch_bytes=fetch_b, write_bytes=write_b,
+                   total_bytes=fetch_b + write_b, calibration=[cal_f, cal_w], per="splice",
+                   algorithmic_bytes=alg)
     os.makedirs(PROFILES, exist_ok=True)
     with open(os.path.join(PROFILES, f"{kernel}_{wl.name}.md"), "w") as f:
         f.write("\n".join(lines) + "\n")

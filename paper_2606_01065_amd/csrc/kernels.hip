@@ -1178,10 +1178,12 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         const int64_t move_blocks = t.n_rows > 0 ? (int64_t(t.n_rows) * max_tpr + PAGED_TPB - 1) / PAGED_TPB : 0;
         const int64_t remap_blocks = t.n_remap > 0 ? (int64_t(t.n_remap) * max_upp + PAGED_TPB - 1) / PAGED_TPB : 0;
         const dim3 layers_planes(1, unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT), unsigned(n_planes));
-        bool first = true;
+        // the gather goes with the first class that has REMAP work (or alone)
+        int gather_class = 1;
+        if (remap_blocks > 0 && !any_band[1] && any_band[0]) gather_class = 0;
         for (int nt = 1; nt >= 0; --nt) {
             const int64_t rb = any_band[nt] ? remap_blocks : 0;
-            const int64_t mb = first ? move_blocks : 0;
+            const int64_t mb = nt == gather_class ? move_blocks : 0;
             if (mb + rb == 0) continue;
             P.move_blocks = int32_t(mb);
             const dim3 grid(unsigned(mb + rb), layers_planes.y, layers_planes.z);
@@ -1192,7 +1194,6 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
                 rc = bf16 ? launch(paged_data_kernel<2, false>, grid, s, P, PAGED_TPB)
                           : launch(paged_data_kernel<4, false>, grid, s, P, PAGED_TPB);
             if (rc) return rc;
-            first = false;
         }
     }
     if (new_seq_lens_out)
