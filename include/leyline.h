@@ -14,7 +14,7 @@
  * specification", multiple directives).  RoPE pairs are interleaved (dims 2i, 2i+1) or half-split
  * (dims i, i+d/2) per plane (Sec. 3.3 "RoPE pairing convention").  Rotation arithmetic is fp32
  * with cos/sin of the exact integer shift times theta_i evaluated in fp64 once per call and
- * directive; results are rounded to nearest-even into the storage dtype (Sec. 5.1 "bf16 K-storage
+ * directive; results are rounded to nearest-even into the storage dtype (Sec. 4.1 "bf16 K-storage
  * precision floor").
  *
  * Conventions shared by every entry point

@@ -20,7 +20,7 @@ What is computed, and where the paper defines it
 * RoPE pairs are either interleaved (dims 2i, 2i+1) or half-split / NEOX (dims i, i+d/2)
   (Sec. 3.3 "RoPE pairing convention"; App. "RoPE pairing convention").
 * Rotation arithmetic is carried out in higher precision than storage and rounded on the way
-  back to the bf16 pool (Sec. 5.1 "bf16 K-storage precision floor"; App. "bf16 K-storage
+  back to the bf16 pool (Sec. 4.1 "bf16 K-storage precision floor"; App. "bf16 K-storage
   precision floor").  Here: float64 angles, float64 trig, float64 pair products, one
   round-to-nearest-even to the storage dtype.
 
@@ -200,7 +200,7 @@ def mla_plane(base: float = 10000.0, kv_lora_rank: int = 512, rope_dim: int = 64
 
 def gqa_planes(n_kv_heads: int = 8, head_dim: int = 128, base: float = 500000.0,
                style: int = NEOX) -> List[Plane]:
-    """GQA: K rotated over the whole head, V moved only (Sec. 7, "Extension to GQA and MHA")."""
+    """GQA: K rotated over the whole head, V moved only (Sec. 6, "Extension to GQA and MHA")."""
     row = n_kv_heads * head_dim
     k = Plane(row_elems=row, n_heads=n_kv_heads, head_stride=head_dim, rot_offset=0,
               rot_dim=head_dim, style=style, base=base)
