@@ -224,12 +224,16 @@ def rotate_rows(rows: np.ndarray, shift, plane: Plane, dtype: str) -> np.ndarray
 # Directives (Sec. 3.1; App. "Kernel specification: tensors and composition")
 # ----------------------------------------------------------------------------------------------
 
+AMORTIZE, FORGET = 0, 1     # directive modes (Sec. 3.1)
+
+
 @dataclass
 class Directive:
     span_start: int
     span_end: int
     stub_len: int
     seq: int = 0
+    mode: int = AMORTIZE
 
     @property
     def delta(self) -> int:
@@ -239,6 +243,27 @@ class Directive:
 
 class DirectiveError(ValueError):
     pass
+
+
+def resolve_forget(n: int, dirs: Sequence[Directive]) -> List[Directive]:
+    """FORGET (Sec. 3.1, "The FORGET mode") hands the edit to a prefix-trimmed re-prefill: the
+    cache keeps what precedes the span and everything from the span start on is computed again
+    by the model.  On the cache this is the deletion of [span_start, n) with no replacement.
+    A FORGET directive must be the last of its sequence and carry no replacement KV (the
+    replacement is part of what is re-prefilled)."""
+    out = list(dirs)
+    for j, d in enumerate(out):
+        if d.mode == FORGET:
+            if j != len(out) - 1:
+                raise DirectiveError("a FORGET directive must be the last of its sequence")
+            if d.stub_len != 0:
+                raise DirectiveError("a FORGET directive carries no replacement")
+            if not (0 <= d.span_start <= d.span_end <= n):
+                raise DirectiveError(f"span [{d.span_start},{d.span_end}) outside [0,{n}]")
+            out[j] = Directive(d.span_start, n, 0, d.seq)
+        elif d.mode != AMORTIZE:
+            raise DirectiveError("unknown mode")
+    return out
 
 
 def check_directives(n: int, dirs: Sequence[Directive]) -> None:
@@ -261,6 +286,7 @@ def row_sources(n: int, dirs: Sequence[Directive]) -> List[tuple]:
     ('old', p, delta)  -> old row p, shifted by the cumulative delta of its segment
     ('stub', j, t)     -> token t of directive j's replacement
     """
+    dirs = resolve_forget(n, dirs)
     check_directives(n, dirs)
     out: List[tuple] = []
     shift = 0
@@ -278,7 +304,7 @@ def row_sources(n: int, dirs: Sequence[Directive]) -> List[tuple]:
 
 
 def new_length(n: int, dirs: Sequence[Directive]) -> int:
-    return n + sum(d.delta for d in dirs)
+    return n + sum(d.delta for d in resolve_forget(n, dirs))
 
 
 def splice_rows(rows: np.ndarray, n: int, dirs: Sequence[Directive],
@@ -289,6 +315,7 @@ def splice_rows(rows: np.ndarray, n: int, dirs: Sequence[Directive],
     with delta_j the running sum of the directives' Deltas.  Non-rotary elements are copied
     bit-for-bit; rotary bands are rotated in float64 and rounded once.
     """
+    dirs = resolve_forget(n, dirs)
     check_directives(n, dirs)
     pieces = []
     shift = 0
@@ -327,6 +354,7 @@ def splice_sequential(cache: np.ndarray, n: int, dirs: Sequence[Directive],
     """Multi-directive reference by sequential application (App. "Kernel specification"):
     directive j is applied alone to the result of directives < j, its span translated by the
     running shift.  Rows are carried in float64 between steps (one rounding at the end)."""
+    dirs = resolve_forget(n, dirs)
     check_directives(n, dirs)
     n_layers = cache.shape[0]
     freqs = plane.frequencies() if plane.rot_dim else None
@@ -364,7 +392,8 @@ def pages_for(n: int, page: int) -> int:
     return (n + page - 1) // page
 
 
-def plan_sequence(n: int, dirs: Sequence[Directive], page: int, fresh_base: int) -> SeqPlan:
+def plan_sequence(n: int, dirs: Sequence[Directive], page: int, fresh_base: int,
+                  remap: bool = True) -> SeqPlan:
     """Page plan of one sequence.
 
     New logical page k is
@@ -374,6 +403,11 @@ def plan_sequence(n: int, dirs: Sequence[Directive], page: int, fresh_base: int)
                its rotary bands are rotated in place;
       ASSEMBLE otherwise: its rows are gathered into the next fresh page.
     Old pages referenced by neither an identity nor a remap page are freed.
+
+    remap=False (copy-on-write, for pools whose pages other sequences share) never re-uses a page
+    whose rows shift: such pages are assembled into fresh pages and no old page is written, as
+    the paper's Role A/B integration writes the rotated downstream KV into fresh destination
+    slots and leaves the originals to their other owners (Sec. 3.3, "Role B").
     """
     src = row_sources(n, dirs)
     n_new = len(src)
@@ -389,7 +423,7 @@ def plan_sequence(n: int, dirs: Sequence[Directive], page: int, fresh_base: int)
             plan.deltas.append(0)
             kept.add(k)
             continue
-        if all(r[0] == "old" for r in rows):
+        if remap and all(r[0] == "old" for r in rows):
             shifts = {r[2] for r in rows}
             old_pages = {r[1] // page for r in rows}
             same_off = all(r[1] % page == q % page for r, q in zip(rows, offs))
@@ -408,7 +442,8 @@ def plan_sequence(n: int, dirs: Sequence[Directive], page: int, fresh_base: int)
     return plan
 
 
-def plan_paged(seq_lens: Sequence[int], dirs: Sequence[Directive], page: int) -> List[SeqPlan]:
+def plan_paged(seq_lens: Sequence[int], dirs: Sequence[Directive], page: int,
+               remap: bool = True) -> List[SeqPlan]:
     """Plans for all sequences; fresh ordinals run in ascending (sequence, new page) order.
     ``dirs`` is sorted by (seq, span_start)."""
     by_seq = [[d for d in dirs if d.seq == b] for b in range(len(seq_lens))]
@@ -418,7 +453,7 @@ def plan_paged(seq_lens: Sequence[int], dirs: Sequence[Directive], page: int) ->
     plans = []
     fresh = 0
     for b, n in enumerate(seq_lens):
-        p = plan_sequence(int(n), by_seq[b], page, fresh)
+        p = plan_sequence(int(n), by_seq[b], page, fresh, remap)
         fresh += sum(1 for k in p.kinds if k == ASSEMBLE)
         plans.append(p)
     return plans
@@ -431,10 +466,10 @@ def gather_logical(pool: np.ndarray, layer: int, bt_row: np.ndarray, n: int, pag
 
 
 def paged_tables(block_table: np.ndarray, seq_lens: Sequence[int], dirs: Sequence[Directive],
-                 free_pages: Sequence[int], page: int):
+                 free_pages: Sequence[int], page: int, remap: bool = True):
     """New block table (entries past a sequence's last page = -1), new lengths, the freed
     physical pages, and the plans, from the page plan and the old block table."""
-    plans = plan_paged(seq_lens, dirs, page)
+    plans = plan_paged(seq_lens, dirs, page, remap)
     bt_out = np.full_like(block_table, -1)
     freed: List[int] = []
     for b, plan in enumerate(plans):
@@ -453,8 +488,9 @@ def paged_tables(block_table: np.ndarray, seq_lens: Sequence[int], dirs: Sequenc
 
 def splice_paged(pools: Sequence[np.ndarray], planes: Sequence[Plane], dtype: str,
                  block_table: np.ndarray, seq_lens: Sequence[int], dirs: Sequence[Directive],
-                 stubs: Sequence[Sequence[np.ndarray]], free_pages: Sequence[int], page: int):
-    """Paged splice.
+                 stubs: Sequence[Sequence[np.ndarray]], free_pages: Sequence[int], page: int,
+                 remap: bool = True):
+    """Paged splice (remap=False: copy-on-write, see plan_sequence).
 
     pools[plane]:      storage [L, n_pool_pages, page, row_elems]
     block_table:       int32 [n_seqs, bt_stride] (old physical pages per logical page)
@@ -464,7 +500,7 @@ def splice_paged(pools: Sequence[np.ndarray], planes: Sequence[Plane], dtype: st
     Returns (new pools, new block table (unused entries = -1), new lengths, freed physical pages).
     Rows at or past the new length inside the last page of a sequence are unspecified.
     """
-    bt_out, new_lens, freed, plans = paged_tables(block_table, seq_lens, dirs, free_pages, page)
+    bt_out, new_lens, freed, plans = paged_tables(block_table, seq_lens, dirs, free_pages, page, remap)
     out = [np.array(p, copy=True) for p in pools]
     for b, plan in enumerate(plans):
         my_dirs = [d for d in dirs if d.seq == b]

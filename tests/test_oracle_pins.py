@@ -296,14 +296,14 @@ def test_one_call_equals_sequential_application():
 
 # ------------------------------------------------------------------------------------ paged --
 
-def _paged_case(rng, nrng, n_seqs, page, dtype, plane, max_len=300, dirs_per_seq=2):
+def _paged_case(rng, nrng, n_seqs, page, dtype, plane, max_len=300, dirs_per_seq=2, remap=True):
     seq_lens = [rng.randint(1, max_len) for _ in range(n_seqs)]
     dirs = []
     for b, n in enumerate(seq_lens):
         for d in _random_dirs(rng, n, k_max=dirs_per_seq):
             d.seq = b
             dirs.append(d)
-    plans = O.plan_paged(seq_lens, dirs, page)
+    plans = O.plan_paged(seq_lens, dirs, page, remap)
     bt_stride = max(max(O.pages_for(n, page), O.pages_for(p.new_len, page))
                     for n, p in zip(seq_lens, plans)) + 1
     used = sum(O.pages_for(n, page) for n in seq_lens)
@@ -369,3 +369,68 @@ def test_paged_remap_only_for_whole_page_shifts():
     (plan,) = O.plan_paged([64], [O.Directive(16, 20, 4)], page)
     assert plan.kinds == [O.IDENTITY, O.IDENTITY, O.ASSEMBLE] + [O.IDENTITY] * 5
     assert plan.freed == [2]
+
+
+# ---------------------------------------------------------------------------- FORGET, copy-on-write
+
+def test_forget_is_a_prefix_trim_after_the_earlier_edits():
+    """FORGET hands the edit to a prefix-trimmed re-prefill (Sec. 3.1, "The FORGET mode"): with
+    list surgery, the earlier directives are applied and the list is cut at the FORGET span's
+    start (in post-edit coordinates); nothing from the span on is kept."""
+    rng = random.Random(41)
+    plane = O.Plane(row_elems=4)
+    for _ in range(200):
+        n = rng.randint(1, 40)
+        dirs = _random_dirs(rng, n)
+        tail_lo = dirs[-1].span_end if dirs else 0
+        s = rng.randint(tail_lo, n)
+        e = rng.randint(s, n)
+        dirs = dirs + [O.Directive(s, e, 0, mode=O.FORGET)]
+        rows = np.arange(n * 4, dtype=np.float32).reshape(n, 4)
+        stubs = [np.full((d.stub_len, 4), -(j + 1), dtype=np.float32) for j, d in enumerate(dirs)]
+        lst = [tuple(r) for r in rows]
+        del lst[s:]                                   # the FORGET cut, in pre-call coordinates
+        for j in reversed(range(len(dirs) - 1)):
+            d = dirs[j]
+            del lst[d.span_start:d.span_end]
+            lst[d.span_start:d.span_start] = [tuple(r) for r in stubs[j]]
+        got = O.splice_rows(rows, n, dirs, stubs, plane, O.F32)
+        assert [tuple(r) for r in got] == lst
+        assert O.new_length(n, dirs) == len(lst)
+
+
+def test_forget_must_be_last_and_carry_no_replacement():
+    with pytest.raises(O.DirectiveError):
+        O.row_sources(20, [O.Directive(2, 4, 0, mode=O.FORGET), O.Directive(6, 8, 1)])
+    with pytest.raises(O.DirectiveError):
+        O.row_sources(20, [O.Directive(2, 4, 3, mode=O.FORGET)])
+    assert O.new_length(20, [O.Directive(5, 9, 0, mode=O.FORGET)]) == 5
+
+
+def test_copy_on_write_plan_writes_no_old_page():
+    """remap=False: no page is re-used with a shift, so every old page in the new tables keeps
+    its contents bit for bit, and the logical content equals the in-place plan's."""
+    rng = random.Random(43)
+    nrng = np.random.default_rng(43)
+    plane = O.Plane(row_elems=16, n_heads=1, head_stride=16, rot_offset=8, rot_dim=8,
+                    style=O.INTERLEAVED, base=10000.0)
+    for page in (1, 4, 8):
+        for _ in range(15):
+            seq_lens, dirs, bt, free, pool, stubs = _paged_case(rng, nrng, 3, page, O.BF16, plane,
+                                                                max_len=60, remap=False)
+            (cow,), bt_c, lens_c, freed_c = O.splice_paged([pool], [plane], O.BF16, bt, seq_lens, dirs,
+                                                           stubs, free, page, remap=False)
+            (inp,), bt_i, lens_i, _ = O.splice_paged([pool], [plane], O.BF16, bt, seq_lens, dirs,
+                                                     stubs, free, page)
+            plans = O.plan_paged(seq_lens, dirs, page, remap=False)
+            assert all(k != O.REMAP for p in plans for k in p.kinds)
+            assert any(k == O.REMAP for p in O.plan_paged(seq_lens, dirs, page) for k in p.kinds) or page > 1
+            old = {int(bt[b, k]) for b, n in enumerate(seq_lens) for k in range(O.pages_for(n, page))}
+            for pg in old:
+                assert np.array_equal(cow[:, pg], pool[:, pg])               # old pages untouched
+            assert lens_c == lens_i
+            for b in range(len(seq_lens)):
+                for layer in range(2):
+                    a = O.gather_logical(cow, layer, bt_c[b], lens_c[b], page)
+                    c = O.gather_logical(inp, layer, bt_i[b], lens_i[b], page)
+                    assert np.array_equal(a, c)
