@@ -53,7 +53,8 @@ enum {
     LEYLINE_E_ORDER = -3,     /* directives not sorted by (seq, span_start)                   */
     LEYLINE_E_OVERLAP = -4,   /* two spans of one sequence overlap                            */
     LEYLINE_E_CAPACITY = -5,  /* new length > capacity, too few free pages, output too small  */
-    LEYLINE_E_MODE = -6,      /* FORGET requested: not a splice, the caller re-prefills       */
+    LEYLINE_E_MODE = -6,      /* a FORGET directive that is not the last of its sequence, or  */
+                              /* that carries a replacement                                   */
     LEYLINE_E_WORKSPACE = -7, /* workspace missing or smaller than the query reported         */
     LEYLINE_E_HIP = -8        /* the HIP runtime reported an error while enqueueing           */
 };
@@ -65,9 +66,20 @@ enum { LEYLINE_BF16 = 0, LEYLINE_F32 = 1 };
  * band; NEOX (half-split) pairs dims (i, i + rot_dim/2). */
 enum { LEYLINE_ROPE_INTERLEAVED = 0, LEYLINE_ROPE_NEOX = 1 };
 
-/* Directive mode (Sec. 3.1): AMORTIZE is the in-place splice; FORGET asks for true forgetting,
- * which is a prefix-trimmed re-prefill and is refused here with LEYLINE_E_MODE. */
+/* Directive mode (Sec. 3.1, "The FORGET mode").  AMORTIZE is the splice: replacement written,
+ * downstream rows moved and re-anchored.  FORGET asks for true forgetting, which the serving stack
+ * implements as a prefix-trimmed re-prefill: on the cache, the sequence is cut at the FORGET
+ * span's start (after the effect of the earlier directives) and nothing is moved or rotated; the
+ * caller then re-prefills from there.  A FORGET directive must be the last directive of its
+ * sequence and carry no replacement (stub_len = 0), else LEYLINE_E_MODE. */
 enum { LEYLINE_AMORTIZE = 0, LEYLINE_FORGET = 1 };
+
+/* Flags of the paged calls.  COPY_ON_WRITE: no old page is written.  A page whose rows all come
+ * from one old page with a nonzero whole-page shift is assembled into a fresh page instead of
+ * being re-used with its rotary bands rotated in place, so pages shared with other sequences (a
+ * radix prefix cache) keep their contents; the rotated KV goes to fresh pages, as the Role A/B
+ * integration of Sec. 3.3 writes it to fresh destination slots. */
+enum { LEYLINE_PAGED_COPY_ON_WRITE = 1 };
 
 /* Device-side status bits a kernel may OR into the optional device_status word. */
 enum {
@@ -120,7 +132,7 @@ typedef struct leyline_cache {
  */
 typedef struct leyline_directive {
     int32_t seq;
-    int32_t mode;           /* LEYLINE_AMORTIZE (LEYLINE_FORGET -> LEYLINE_E_MODE) */
+    int32_t mode;           /* LEYLINE_AMORTIZE or LEYLINE_FORGET */
     int64_t span_start;
     int64_t span_end;
     int64_t stub_len;
@@ -176,7 +188,8 @@ int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len,
  * Sizes of a paged splice, computed on the host from lengths and directives alone.
  *
  * cache: the paged cache the splice will run on (its plane layout sizes the cos/sin tables).
- * seq_lens: host [n_seqs]; bt_stride: row length of the block tables; dirs: host, sorted by
+ * seq_lens: host [n_seqs]; bt_stride: row length of the block tables; flags: LEYLINE_PAGED_*
+ * (as for the splice); dirs: host, sorted by
  * (seq, span_start).  Outputs (host, each nullable): new_seq_lens[n_seqs]; *n_fresh_needed =
  * fresh pages the call will consume; *n_freed = pages the call will drop from block tables;
  * *workspace_bytes = device workspace the call needs.
@@ -184,8 +197,8 @@ int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len,
  */
 int leyline_paged_query(const leyline_cache* cache, int32_t n_seqs, const int32_t* seq_lens,
                         int32_t bt_stride, const leyline_directive* dirs, int32_t n_dirs,
-                        int32_t* new_seq_lens, int32_t* n_fresh_needed, int32_t* n_freed,
-                        int64_t* workspace_bytes);
+                        uint32_t flags, int32_t* new_seq_lens, int32_t* n_fresh_needed,
+                        int32_t* n_freed, int64_t* workspace_bytes);
 
 /* Page kinds of a paged plan. */
 enum { LEYLINE_PAGE_IDENTITY = 0, LEYLINE_PAGE_REMAP = 1, LEYLINE_PAGE_ASSEMBLE = 2, LEYLINE_PAGE_NONE = -1 };
@@ -208,7 +221,8 @@ enum { LEYLINE_PAGE_IDENTITY = 0, LEYLINE_PAGE_REMAP = 1, LEYLINE_PAGE_ASSEMBLE 
  * too small.
  */
 int leyline_paged_plan(int32_t page_size, int32_t n_seqs, const int32_t* seq_lens,
-                       const leyline_directive* dirs, int32_t n_dirs, int32_t bt_stride,
+                       const leyline_directive* dirs, int32_t n_dirs, uint32_t flags,
+                       int32_t bt_stride,
                        int32_t* kind_out, int32_t* src_out,
                        int32_t* freed_seq_out, int32_t* freed_page_out, int32_t freed_cap);
 
@@ -228,15 +242,17 @@ int leyline_paged_plan(int32_t page_size, int32_t n_seqs, const int32_t* seq_len
  * page that a kernel of this call writes and the gather reads; reuse it only after the stream
  * has passed this call.  Any page_size whose rows keep the 16-byte alignment is accepted.
  *
+ * flags: 0, or LEYLINE_PAGED_COPY_ON_WRITE (no REMAP pages: no old page is written).
  * Ownership: only ASSEMBLE pages (fresh) and REMAP pages (rotary bands, in place) are written.
- * Pages holding the rows of a REMAP page must not be shared with another sequence.  Freed pages
+ * Pages holding the rows of a REMAP page must not be shared with another sequence (pass
+ * LEYLINE_PAGED_COPY_ON_WRITE when they may be).  Freed pages
  * are not written; the caller may recycle them once the stream has passed this call.
  * Errors: as leyline_splice_contig, plus E_CAPACITY (too few free pages, freed_cap or bt_stride
  * too small) and E_WORKSPACE.
  */
 int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, const int32_t* seq_lens,
                          const int32_t* block_table_in, int32_t* block_table_out, int32_t bt_stride,
-                         const leyline_directive* dirs, int32_t n_dirs,
+                         const leyline_directive* dirs, int32_t n_dirs, uint32_t flags,
                          const int32_t* free_pages, int32_t n_free,
                          int32_t* freed_pages_out, int32_t freed_cap,
                          int32_t* new_seq_lens_out, int32_t* n_fresh_used_out, int32_t* n_freed_out,

@@ -1085,7 +1085,7 @@ extern "C" int leyline_rotate_delta(const leyline_cache* cache, int64_t delta,
 
 extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, const int32_t* seq_lens,
                                     const int32_t* block_table_in, int32_t* block_table_out, int32_t bt_stride,
-                                    const leyline_directive* dirs, int32_t n_dirs,
+                                    const leyline_directive* dirs, int32_t n_dirs, uint32_t flags,
                                     const int32_t* free_pages, int32_t n_free,
                                     int32_t* freed_pages_out, int32_t freed_cap,
                                     int32_t* new_seq_lens_out, int32_t* n_fresh_used_out, int32_t* n_freed_out,
@@ -1098,8 +1098,10 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
     if (bt_stride < 1 || n_free < 0 || freed_cap < 0) return LEYLINE_E_INVAL;
     if (n_seqs > 0 && (!block_table_in || !block_table_out || block_table_in == block_table_out))
         return LEYLINE_E_INVAL;
+    if (flags & ~uint32_t(LEYLINE_PAGED_COPY_ON_WRITE)) return LEYLINE_E_INVAL;
     PagedPlan plan;
-    rc = plan_paged(cache->page_size, n_seqs, seq_lens, dirs, n_dirs, n_planes, &plan);
+    rc = plan_paged(cache->page_size, n_seqs, seq_lens, dirs, n_dirs, n_planes,
+                    !(flags & LEYLINE_PAGED_COPY_ON_WRITE), &plan);
     if (rc) return rc;
     rc = check_table_width(plan, seq_lens, bt_stride);
     if (rc) return rc;
@@ -1108,7 +1110,7 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
     if (plan.n_fresh > 0 && !free_pages) return LEYLINE_E_INVAL;
     if (plan.n_freed > 0 && !freed_pages_out) return LEYLINE_E_INVAL;
     PagedImage img;
-    rc = build_paged_image(cache, plan, n_seqs, dirs, n_dirs, bt_stride, &img);
+    rc = build_paged_image(cache, plan, n_seqs, plan.dirs, n_dirs, bt_stride, &img);
     if (rc) return rc;
     if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) || workspace_bytes < img.tables.total)
         return LEYLINE_E_WORKSPACE;

@@ -147,7 +147,6 @@ int check_sequence(int64_t seq_len, const leyline_directive* dirs, int32_t n_dir
     int64_t prev_start = 0, prev_end = 0;
     for (int32_t j = 0; j < n_dirs; ++j) {
         const leyline_directive& d = dirs[j];
-        if (d.mode == LEYLINE_FORGET) return LEYLINE_E_MODE;
         if (d.mode != LEYLINE_AMORTIZE) return LEYLINE_E_INVAL;
         if (d.span_start < 0 || d.span_start > d.span_end || d.span_end > seq_len || d.stub_len < 0)
             return LEYLINE_E_RANGE;
@@ -159,6 +158,34 @@ int check_sequence(int64_t seq_len, const leyline_directive* dirs, int32_t n_dir
         prev_start = d.span_start;
         prev_end = d.span_end;
     }
+    return LEYLINE_OK;
+}
+
+int resolve_forget(const leyline_directive* dirs, int32_t n_dirs, int32_t n_seqs,
+                   const int32_t* seq_lens, int64_t seq_len, std::vector<leyline_directive>* buf,
+                   const leyline_directive** use) {
+    *use = dirs;
+    if (n_dirs <= 0 || !dirs) return LEYLINE_OK;
+    bool any = false;
+    for (int32_t j = 0; j < n_dirs; ++j) {
+        const leyline_directive& d = dirs[j];
+        if (d.mode == LEYLINE_AMORTIZE) continue;
+        if (d.mode != LEYLINE_FORGET) return LEYLINE_E_INVAL;
+        if (j + 1 < n_dirs && dirs[j + 1].seq == d.seq) return LEYLINE_E_MODE;   // not the last
+        if (d.stub_len != 0) return LEYLINE_E_MODE;
+        if (seq_lens && (d.seq < 0 || d.seq >= n_seqs)) return LEYLINE_E_RANGE;
+        const int64_t n = seq_lens ? seq_lens[d.seq] : seq_len;
+        if (d.span_start < 0 || d.span_start > d.span_end || d.span_end > n) return LEYLINE_E_RANGE;
+        any = true;
+    }
+    if (!any) return LEYLINE_OK;
+    buf->assign(dirs, dirs + n_dirs);
+    for (leyline_directive& d : *buf) {
+        if (d.mode != LEYLINE_FORGET) continue;
+        d.span_end = seq_lens ? seq_lens[d.seq] : seq_len;
+        d.mode = LEYLINE_AMORTIZE;
+    }
+    *use = buf->data();
     return LEYLINE_OK;
 }
 
@@ -177,6 +204,9 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
     if (seq_len < 0 || seq_len > cache->capacity) return LEYLINE_E_RANGE;
     for (int32_t j = 0; j < n_dirs; ++j)
         if (dirs && dirs[j].seq != 0) return LEYLINE_E_RANGE;
+    std::vector<leyline_directive> resolved;
+    rc = resolve_forget(dirs, n_dirs, 1, nullptr, seq_len, &resolved, &dirs);
+    if (rc) return rc;
     rc = check_sequence(seq_len, dirs, n_dirs, n_planes);
     if (rc) return rc;
 
@@ -321,7 +351,8 @@ struct Piece {                 // a run of new positions with one source
 }  // namespace
 
 int plan_paged(int32_t page_size, int32_t n_seqs, const int32_t* seq_lens,
-               const leyline_directive* dirs, int32_t n_dirs, int32_t n_planes, PagedPlan* out) {
+               const leyline_directive* dirs, int32_t n_dirs, int32_t n_planes, bool remap,
+               PagedPlan* out) {
     if (page_size < 1 || n_seqs < 0 || (n_seqs > 0 && !seq_lens) || n_dirs < 0 ||
         (n_dirs > 0 && !dirs))
         return LEYLINE_E_INVAL;
@@ -331,6 +362,11 @@ int plan_paged(int32_t page_size, int32_t n_seqs, const int32_t* seq_lens,
         if (dirs[j].seq < 0 || dirs[j].seq >= n_seqs) return LEYLINE_E_RANGE;
         if (j > 0 && dirs[j].seq < dirs[j - 1].seq) return LEYLINE_E_ORDER;
     }
+    {
+        const int rc = resolve_forget(dirs, n_dirs, n_seqs, seq_lens, 0, &out->resolved, &dirs);
+        if (rc) return rc;
+    }
+    out->dirs = dirs;
     const int64_t P = page_size;
     out->page_size = page_size;
     out->n_seqs = n_seqs;
@@ -400,7 +436,7 @@ int plan_paged(int32_t page_size, int32_t n_seqs, const int32_t* seq_lens,
         kept.clear();
         int64_t kcur = 0;
         for (const Piece& p : pieces) {
-            if (p.stub || p.shift % P != 0) continue;
+            if (p.stub || p.shift % P != 0 || (p.shift != 0 && !remap)) continue;
             const int64_t first = (p.lo + P - 1) / P;
             const int64_t last = p.hi == n_new ? (p.hi + P - 1) / P : p.hi / P;
             if (first >= last) continue;
@@ -544,7 +580,7 @@ extern "C" const char* leyline_strerror(int code) {
         case LEYLINE_E_ORDER: return "directives not sorted by (seq, span_start)";
         case LEYLINE_E_OVERLAP: return "directive spans overlap";
         case LEYLINE_E_CAPACITY: return "capacity exceeded (rows, pages, block table or freed list)";
-        case LEYLINE_E_MODE: return "FORGET mode is a re-prefill, not a splice";
+        case LEYLINE_E_MODE: return "a FORGET directive must be the last of its sequence and carry no replacement";
         case LEYLINE_E_WORKSPACE: return "workspace missing or too small";
         case LEYLINE_E_HIP: return "HIP runtime error";
         default: return "unknown leyline status";
@@ -555,7 +591,7 @@ extern "C" int leyline_abi_version(void) { return LEYLINE_ABI_VERSION; }
 
 extern "C" int leyline_paged_query(const leyline_cache* cache, int32_t n_seqs,
                                    const int32_t* seq_lens, int32_t bt_stride,
-                                   const leyline_directive* dirs, int32_t n_dirs,
+                                   const leyline_directive* dirs, int32_t n_dirs, uint32_t flags,
                                    int32_t* new_seq_lens, int32_t* n_fresh_needed, int32_t* n_freed,
                                    int64_t* workspace_bytes) {
     using namespace leyline;
@@ -564,13 +600,15 @@ extern "C" int leyline_paged_query(const leyline_cache* cache, int32_t n_seqs,
     int rc = describe_cache(cache, true, planes, &n_planes);
     if (rc) return rc;
     if (bt_stride < 0) return LEYLINE_E_INVAL;
+    if (flags & ~uint32_t(LEYLINE_PAGED_COPY_ON_WRITE)) return LEYLINE_E_INVAL;
     PagedPlan plan;
-    rc = plan_paged(cache->page_size, n_seqs, seq_lens, dirs, n_dirs, n_planes, &plan);
+    rc = plan_paged(cache->page_size, n_seqs, seq_lens, dirs, n_dirs, n_planes,
+                    !(flags & LEYLINE_PAGED_COPY_ON_WRITE), &plan);
     if (rc) return rc;
     rc = check_table_width(plan, seq_lens, bt_stride);
     if (rc) return rc;
     PagedImage img;
-    rc = build_paged_image(cache, plan, n_seqs, dirs, n_dirs, bt_stride, &img);
+    rc = build_paged_image(cache, plan, n_seqs, plan.dirs, n_dirs, bt_stride, &img);
     if (rc) return rc;
     if (new_seq_lens)
         for (int32_t b = 0; b < n_seqs; ++b) new_seq_lens[b] = plan.new_lens[size_t(b)];
@@ -581,14 +619,17 @@ extern "C" int leyline_paged_query(const leyline_cache* cache, int32_t n_seqs,
 }
 
 extern "C" int leyline_paged_plan(int32_t page_size, int32_t n_seqs, const int32_t* seq_lens,
-                                  const leyline_directive* dirs, int32_t n_dirs, int32_t bt_stride,
+                                  const leyline_directive* dirs, int32_t n_dirs, uint32_t flags,
+                                  int32_t bt_stride,
                                   int32_t* kind_out, int32_t* src_out,
                                   int32_t* freed_seq_out, int32_t* freed_page_out, int32_t freed_cap) {
     using namespace leyline;
     if (bt_stride < 0 || (n_seqs > 0 && (!kind_out || !src_out))) return LEYLINE_E_INVAL;
+    if (flags & ~uint32_t(LEYLINE_PAGED_COPY_ON_WRITE)) return LEYLINE_E_INVAL;
     PagedPlan plan;
     // stub pointers are not needed for a symbolic plan: validate them against zero planes
-    int rc = plan_paged(page_size, n_seqs, seq_lens, dirs, n_dirs, 0, &plan);
+    int rc = plan_paged(page_size, n_seqs, seq_lens, dirs, n_dirs, 0,
+                        !(flags & LEYLINE_PAGED_COPY_ON_WRITE), &plan);
     if (rc) return rc;
     rc = check_table_width(plan, seq_lens, bt_stride);
     if (rc) return rc;

@@ -19,9 +19,19 @@ KDiv make_div(int32_t d);
 int describe_cache(const leyline_cache* cache, bool paged, KPlane out[LEYLINE_MAX_PLANES],
                    int* n_planes);
 
-// Validation of one sequence's directives (already restricted to that sequence).
+// Validation of one sequence's directives (already restricted to that sequence, FORGET already
+// resolved).
 int check_sequence(int64_t seq_len, const leyline_directive* dirs, int32_t n_dirs,
                    int32_t n_planes);
+
+// FORGET hands an edit to a prefix-trimmed re-prefill: on the cache it is the deletion of
+// [span_start, seq_len) with no replacement.  Checks the FORGET rules (last directive of its
+// sequence, no replacement, span inside the sequence) and, when a FORGET directive is present,
+// copies the directives into *buf with each FORGET replaced by that deletion; *use points at the
+// directives to plan with.  seq_lens: per sequence (paged), or NULL with seq_len (contiguous).
+int resolve_forget(const leyline_directive* dirs, int32_t n_dirs, int32_t n_seqs,
+                   const int32_t* seq_lens, int64_t seq_len, std::vector<leyline_directive>* buf,
+                   const leyline_directive** use);
 
 // cos/sin of (shift * theta_i), evaluated in fp64 and rounded to fp32, for every rotary pair of
 // every rotary plane, appended to `table`.  Returns the offset of the first entry.
@@ -65,6 +75,8 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
 struct PagedPlan {
     int32_t page_size = 0;
     int32_t n_seqs = 0;
+    std::vector<leyline_directive> resolved;   // the directives with FORGET resolved (if any)
+    const leyline_directive* dirs = nullptr;   // the directives the plan was made from
     std::vector<int32_t> new_lens;
     std::vector<int32_t> run_begin;    // [n_seqs + 1]: sequence b owns runs [run_begin[b], run_begin[b+1])
     std::vector<KPageRun> runs;        // ascending (seq, k0); they cover every new page exactly once
@@ -74,8 +86,10 @@ struct PagedPlan {
     int32_t n_freed = 0;
 };
 
+// remap = false: copy-on-write (no page whose rows shift is re-used; such pages are assembled).
 int plan_paged(int32_t page_size, int32_t n_seqs, const int32_t* seq_lens,
-               const leyline_directive* dirs, int32_t n_dirs, int32_t n_planes, PagedPlan* out);
+               const leyline_directive* dirs, int32_t n_dirs, int32_t n_planes, bool remap,
+               PagedPlan* out);
 
 // E_CAPACITY unless every sequence's old and new page count fits a block-table row.
 int check_table_width(const PagedPlan& plan, const int32_t* seq_lens, int32_t bt_stride);

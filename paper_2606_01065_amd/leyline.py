@@ -9,7 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from ctypes import POINTER, Structure, c_double, c_int, c_int32, c_int64, c_void_p
+from ctypes import POINTER, Structure, c_double, c_int, c_int32, c_int64, c_uint32, c_void_p
 from collections import namedtuple
 from dataclasses import dataclass
 from typing import List, Optional, Sequence
@@ -24,6 +24,7 @@ ROPE_INTERLEAVED, ROPE_NEOX = 0, 1
 AMORTIZE, FORGET = 0, 1
 STATUS_BAD_PAGE, STATUS_BAD_ROW = 1, 2
 PAGE_IDENTITY, PAGE_REMAP, PAGE_ASSEMBLE, PAGE_NONE = 0, 1, 2, -1
+PAGED_COPY_ON_WRITE = 1
 
 
 class leyline_plane(Structure):
@@ -103,15 +104,15 @@ def _load():
         "leyline_splice_contig": (c_int, [P(leyline_cache), c_int64, P(leyline_directive), c_int32,
                                           P(c_int64), c_void_p, c_int64, c_void_p]),
         "leyline_paged_query": (c_int, [P(leyline_cache), c_int32, P(c_int32), c_int32,
-                                        P(leyline_directive), c_int32, P(c_int32), P(c_int32),
-                                        P(c_int32), P(c_int64)]),
+                                        P(leyline_directive), c_int32, c_uint32, P(c_int32),
+                                        P(c_int32), P(c_int32), P(c_int64)]),
         "leyline_paged_plan": (c_int, [c_int32, c_int32, P(c_int32), P(leyline_directive), c_int32,
-                                       c_int32, P(c_int32), P(c_int32), P(c_int32), P(c_int32),
-                                       c_int32]),
+                                       c_uint32, c_int32, P(c_int32), P(c_int32), P(c_int32),
+                                       P(c_int32), c_int32]),
         "leyline_splice_paged": (c_int, [P(leyline_cache), c_int32, P(c_int32), c_void_p, c_void_p,
-                                         c_int32, P(leyline_directive), c_int32, c_void_p, c_int32,
-                                         c_void_p, c_int32, P(c_int32), P(c_int32), P(c_int32),
-                                         c_void_p, c_void_p, c_int64, c_void_p]),
+                                         c_int32, P(leyline_directive), c_int32, c_uint32, c_void_p,
+                                         c_int32, c_void_p, c_int32, P(c_int32), P(c_int32),
+                                         P(c_int32), c_void_p, c_void_p, c_int64, c_void_p]),
         "leyline_rotate_delta": (c_int, [P(leyline_cache), c_int64, c_void_p, c_int64, c_int64,
                                          c_void_p, c_void_p]),
     }
@@ -288,20 +289,21 @@ def leyline_splice_contig(cache: leyline_cache, seq_len: int, dirs, n_dirs: int,
     return new_len.value
 
 
-def leyline_paged_query(cache: leyline_cache, seq_lens: Sequence[int], bt_stride: int, dirs, n_dirs: int):
+def leyline_paged_query(cache: leyline_cache, seq_lens: Sequence[int], bt_stride: int, dirs, n_dirs: int,
+                        flags: int = 0):
     """Returns (new_seq_lens, n_fresh_needed, n_freed, workspace_bytes)."""
     n = len(seq_lens)
     lens = (c_int32 * max(1, n))(*seq_lens)
     new = (c_int32 * max(1, n))()
     fresh, freed, ws = c_int32(0), c_int32(0), c_int64(0)
-    rc = _lib.leyline_paged_query(ctypes.byref(cache), n, lens, bt_stride, dirs, n_dirs, new,
+    rc = _lib.leyline_paged_query(ctypes.byref(cache), n, lens, bt_stride, dirs, n_dirs, flags, new,
                                   ctypes.byref(fresh), ctypes.byref(freed), ctypes.byref(ws))
     _check(rc, "leyline_paged_query")
     return list(new)[:n], fresh.value, freed.value, ws.value
 
 
 def leyline_paged_plan(page_size: int, seq_lens: Sequence[int], dirs, n_dirs: int, bt_stride: int,
-                       freed_cap: int):
+                       freed_cap: int, flags: int = 0):
     """Host-only symbolic plan: (kinds [n*bt_stride], srcs, freed_seq, freed_page)."""
     n = len(seq_lens)
     lens = (c_int32 * max(1, n))(*seq_lens)
@@ -309,7 +311,7 @@ def leyline_paged_plan(page_size: int, seq_lens: Sequence[int], dirs, n_dirs: in
     srcs = (c_int32 * max(1, n * bt_stride))()
     fs = (c_int32 * max(1, freed_cap))()
     fp = (c_int32 * max(1, freed_cap))()
-    rc = _lib.leyline_paged_plan(page_size, n, lens, dirs, n_dirs, bt_stride, kinds, srcs, fs, fp,
+    rc = _lib.leyline_paged_plan(page_size, n, lens, dirs, n_dirs, flags, bt_stride, kinds, srcs, fs, fp,
                                  freed_cap)
     _check(rc, "leyline_paged_plan")
     return list(kinds)[:n * bt_stride], list(srcs)[:n * bt_stride], list(fs), list(fp)
@@ -317,7 +319,7 @@ def leyline_paged_plan(page_size: int, seq_lens: Sequence[int], dirs, n_dirs: in
 
 def leyline_splice_paged(cache: leyline_cache, seq_lens: Sequence[int], block_table_in, block_table_out,
                          dirs, n_dirs: int, free_pages, freed_pages_out, workspace,
-                         device_status=None, stream=None):
+                         device_status=None, stream=None, flags: int = 0):
     """Returns (new_seq_lens, n_fresh_used, n_freed).  Tables are int32 device tensors."""
     n = len(seq_lens)
     lens = (c_int32 * max(1, n))(*seq_lens)
@@ -326,7 +328,7 @@ def leyline_splice_paged(cache: leyline_cache, seq_lens: Sequence[int], block_ta
     bt_stride = block_table_in.shape[1]
     rc = _lib.leyline_splice_paged(
         ctypes.byref(cache), n, lens, _ptr(block_table_in), _ptr(block_table_out), bt_stride,
-        dirs, n_dirs, _ptr(free_pages), 0 if free_pages is None else free_pages.numel(),
+        dirs, n_dirs, flags, _ptr(free_pages), 0 if free_pages is None else free_pages.numel(),
         _ptr(freed_pages_out), 0 if freed_pages_out is None else freed_pages_out.numel(),
         new, ctypes.byref(fresh), ctypes.byref(freed), _ptr(device_status),
         _ptr(workspace), 0 if workspace is None else workspace.numel() * workspace.element_size(),

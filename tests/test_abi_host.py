@@ -76,6 +76,7 @@ def _dirs(spec, stub_ptr=0x20000):
     arr = (L.leyline_directive * max(1, len(spec)))()
     for i, (s, e, r, *rest) in enumerate(spec):
         arr[i].seq = rest[0] if rest else 0
+        arr[i].mode = rest[1] if len(rest) > 1 else L.AMORTIZE
         arr[i].span_start, arr[i].span_end, arr[i].stub_len = s, e, r
         arr[i].stub[0] = stub_ptr if r else None
     return arr
@@ -96,9 +97,15 @@ def test_contig_validation_codes():
     assert _contig_rc(c, 60, [(10, 20, 1), (5, 8, 1)]) == L.E_ORDER
     assert _contig_rc(c, 60, [(10, 20, 1), (15, 30, 1)]) == L.E_OVERLAP
     assert _contig_rc(c, 60, [(10, 10, 5)]) == L.E_CAPACITY               # 65 > 64 rows
-    d = _dirs([(1, 2, 0)])
-    d[0].mode = L.FORGET
+    d = _dirs([(1, 2, 0), (5, 6, 0)])
+    d[0].mode = L.FORGET                                                  # FORGET not last
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 2, None, None, 0, None) == L.E_MODE
+    d = _dirs([(1, 2, 3)])
+    d[0].mode = L.FORGET                                                  # FORGET with a replacement
     assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, 0, None) == L.E_MODE
+    d = _dirs([(1, 2, 0)])
+    d[0].mode = 7
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, 0, None) == L.E_INVAL
     d = _dirs([(1, 2, 3)], stub_ptr=0)                                    # stub pointer missing
     assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, 0, None) == L.E_INVAL
     d = _dirs([(1, 2, 3)], stub_ptr=0x20008)                              # stub misaligned
@@ -149,6 +156,22 @@ def test_contig_tiles_need_a_workspace():
                                         0x10080, 4096, None) == L.E_WORKSPACE      # misaligned
     assert L._lib.leyline_splice_contig(ctypes.byref(c), 60, d, 1, ctypes.byref(new_len),
                                         0x10000, 16, None) == L.E_WORKSPACE        # too small
+
+
+def test_forget_trims_without_moving_anything():
+    """A FORGET directive (last of its sequence, no replacement) cuts the sequence at its span's
+    start after the earlier directives; the cut itself moves nothing."""
+    c = _mla_cache(cap=64)
+    d = _dirs([(30, 45, 0)])
+    d[0].mode = L.FORGET
+    q = L.leyline_contig_query(c, 60, d, 1)
+    assert (q.new_len, q.launches, q.workspace_bytes) == (30, 0, 0)
+    new_len = ctypes.c_int64(-1)
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 60, d, 1, ctypes.byref(new_len), None, 0, None) == 0
+    assert new_len.value == 30
+    d = _dirs([(10, 12, 0), (30, 30, 0)])                                # after a 2-row deletion
+    d[1].mode = L.FORGET
+    assert L.leyline_contig_query(c, 60, d, 2).new_len == 28
 
 
 def test_contig_noop_calls_do_not_need_a_device():
@@ -211,27 +234,35 @@ def _random_paged_degenerate(rng, n_seqs, page, max_len=300):
             r = rng.choice([0, 0, e - s, rng.randint(0, 2 * (e - s) + 3), (e - s) + page,
                             max(0, e - s - 2 * page)])
             spec.append((s, e, r, b))
+        if rng.random() < 0.3:                                           # a trailing FORGET
+            lo = spec[-1][1] if spec and spec[-1][3] == b else 0
+            s = rng.randint(lo, n)
+            spec.append((s, rng.randint(s, n), 0, b, O.FORGET))
     return lens, spec
 
 
 def test_paged_plan_matches_oracle_on_degenerate_directives():
+    """Degenerate directives, trailing FORGET directives, in-place and copy-on-write plans."""
     rng = random.Random(37)
     for page in (1, 2, 16):
         for _ in range(150):
             lens, spec = _random_paged_degenerate(rng, rng.randint(1, 4), page)
-            dirs = [O.Directive(s, e, r, seq=b) for s, e, r, b in spec]
+            cow = rng.random() < 0.5
+            flags = L.PAGED_COPY_ON_WRITE if cow else 0
+            dirs = [O.Directive(x[0], x[1], x[2], seq=x[3], mode=x[4] if len(x) > 4 else O.AMORTIZE)
+                    for x in spec]
             try:
-                plans = O.plan_paged(lens, dirs, page)
+                plans = O.plan_paged(lens, dirs, page, remap=not cow)
                 for b, n in enumerate(lens):
-                    O.check_directives(n, [d for d in dirs if d.seq == b])
+                    O.check_directives(n, O.resolve_forget(n, [d for d in dirs if d.seq == b]))
             except O.DirectiveError:
                 with pytest.raises(L.LeylineError):
-                    L.leyline_paged_plan(page, lens, _dirs(spec), len(spec), 64, 4096)
+                    L.leyline_paged_plan(page, lens, _dirs(spec), len(spec), 64, 4096, flags)
                 continue
             bt_stride = max([1] + [O.pages_for(max(n, p.new_len), page) for n, p in zip(lens, plans)])
             n_freed = sum(len(p.freed) for p in plans)
             kinds, srcs, fs, fp = L.leyline_paged_plan(page, lens, _dirs(spec), len(spec), bt_stride,
-                                                       n_freed)
+                                                       n_freed, flags)
             kinds = np.array(kinds).reshape(len(lens), bt_stride)
             srcs = np.array(srcs).reshape(len(lens), bt_stride)
             for b, p in enumerate(plans):

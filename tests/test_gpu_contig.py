@@ -31,7 +31,7 @@ def _specs(L, wl, tensors):
 
 def _dir_dicts(wl, stubs):
     return [dict(span_start=d.span_start, span_end=d.span_end, stub=stubs[j], seq=d.seq,
-                 stub_len=d.stub_len) for j, d in enumerate(wl.dirs)]
+                 stub_len=d.stub_len, mode=d.mode) for j, d in enumerate(wl.dirs)]
 
 
 def _run_and_check(L, wl, planes_dev, stubs_dev, label, layers=None):
@@ -52,7 +52,7 @@ def _run_and_check(L, wl, planes_dev, stubs_dev, label, layers=None):
     n = wl.seq_lens[0]
     new_len = L.leyline_splice_contig(cache, n, dirs, len(wl.dirs))
     torch.cuda.synchronize()
-    odirs = [O.Directive(d.span_start, d.span_end, d.stub_len) for d in wl.dirs]
+    odirs = [O.Directive(d.span_start, d.span_end, d.stub_len, mode=d.mode) for d in wl.dirs]
     assert new_len == O.new_length(n, odirs)
     for pi, (desc, t) in enumerate(zip(wl.planes, planes_dev)):
         plane = oracle_plane(desc)
@@ -69,6 +69,7 @@ def _run_and_check(L, wl, planes_dev, stubs_dev, label, layers=None):
 
 def _inputs_for_new_rows(src, n, dirs, stubs):
     """The pre-rotation rows in new-position order (prefix, stub, downstream), per layer."""
+    dirs = O.resolve_forget(n, dirs)
     pieces, cursor = [], 0
     for j, d in enumerate(dirs):
         pieces.append(src[:, cursor:d.span_start])
@@ -168,6 +169,23 @@ def test_gqa_llama3_8b_16k_full(L):
     n_new = _run_and_check(L, wl, planes_dev, stubs_dev, "gqa_llama3_8b_16k")
     assert n_new == 16384 - 2024
     print(f"[info] bf16 rotary elements bit-identical to the oracle: {PU.LAST_BF16_EXACT_FRACTION:.6f}")
+
+
+@pytest.mark.parametrize("kind", ["mla", "gqa"])
+def test_forget_prefix_trim(L, kind):
+    """A trailing FORGET directive cuts the sequence after the earlier edits; rows before the cut
+    match the oracle, nothing past it is compared (the caller re-prefills it)."""
+    rng = random.Random(71 if kind == "mla" else 72)
+    for ci in range(6):
+        n = rng.randint(50, 700)
+        dirs = _random_dirs(rng, n, rng.randint(0, 2))
+        lo = dirs[-1].span_end if dirs else 0
+        s = rng.randint(lo, n)
+        dirs.append(W.Dir(s, rng.randint(s, n), 0, mode=1))
+        grow = sum(max(0, d.stub_len - (d.span_end - d.span_start)) for d in dirs if d.mode == 0)
+        wl = _small_workload(rng, kind, "bf16", 3, n, dirs, extra=grow + 4)
+        planes_dev, stubs_dev = W.alloc_contig(wl, DEV, seed=500 + ci)
+        _run_and_check(L, wl, planes_dev, stubs_dev, f"forget {kind} case {ci} n={n} dirs={dirs}")
 
 
 @pytest.mark.parametrize("name,dirs,extra", [

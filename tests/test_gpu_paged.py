@@ -23,21 +23,22 @@ def L():
     return leyline
 
 
-def _run_gpu(L, wl, pools, bt, free, stubs):
+def _run_gpu(L, wl, pools, bt, free, stubs, flags=0):
     specs = [L.PlaneSpec(t, p.n_heads, p.head_stride or p.row_elems, p.rot_offset, p.rot_dim,
                          p.style, p.base) for p, t in zip(wl.planes, pools)]
     cache = L.make_cache(specs, paged=True)
     dirs = L.make_directives([dict(span_start=d.span_start, span_end=d.span_end, stub=stubs[j],
-                                   seq=d.seq, stub_len=d.stub_len) for j, d in enumerate(wl.dirs)])
+                                   seq=d.seq, stub_len=d.stub_len, mode=d.mode)
+                              for j, d in enumerate(wl.dirs)])
     new_lens, fresh, n_freed, ws_bytes = L.leyline_paged_query(cache, wl.seq_lens, bt.shape[1], dirs,
-                                                                len(wl.dirs))
+                                                                len(wl.dirs), flags)
     bt_out = torch.full_like(bt, -7)
     freed = torch.full((max(1, n_freed),), -7, dtype=torch.int32, device=DEV)
     ws = torch.empty(max(256, ws_bytes), dtype=torch.uint8, device=DEV)
     status = torch.zeros(1, dtype=torch.int32, device=DEV)
     got_lens, got_fresh, got_freed = L.leyline_splice_paged(cache, wl.seq_lens, bt, bt_out, dirs,
                                                             len(wl.dirs), free, freed, ws,
-                                                            device_status=status)
+                                                            device_status=status, flags=flags)
     torch.cuda.synchronize()
     assert (got_lens, got_fresh, got_freed) == (new_lens, fresh, n_freed)
     assert int(status.item()) == 0
@@ -45,7 +46,7 @@ def _run_gpu(L, wl, pools, bt, free, stubs):
 
 
 def _odirs(wl):
-    return [O.Directive(d.span_start, d.span_end, d.stub_len, seq=d.seq) for d in wl.dirs]
+    return [O.Directive(d.span_start, d.span_end, d.stub_len, seq=d.seq, mode=d.mode) for d in wl.dirs]
 
 
 def _random_workload(rng, page, kind, dtype, max_len=None):
@@ -96,6 +97,56 @@ def test_small_random_paged_whole_pool(L, kind, dtype):
             for pi, plane in enumerate(planes):
                 got = host(pools[pi]).reshape(want[pi].shape)
                 assert_rows_match(got, want[pi], plane, dtype, what=f"page={page} case={ci} plane={pi}")
+
+
+@pytest.mark.parametrize("kind", ["mla", "gqa"])
+def test_forget_and_copy_on_write_whole_pool(L, kind):
+    """Trailing FORGET directives (prefix trims) and copy-on-write plans (no old page written):
+    whole pools against the oracle, and under copy-on-write every old page byte-identical."""
+    rng = random.Random({"mla": 301, "gqa": 302}[kind])
+    for page in (1, 4, 16):
+        for ci in range(6):
+            wl = _random_workload(rng, page, kind, "bf16", max_len=300 if page == 1 else None)
+            if rng.random() < 0.6:                                   # a FORGET ends some sequences
+                dirs = list(wl.dirs)
+                for b, n in enumerate(wl.seq_lens):
+                    mine = [d for d in dirs if d.seq == b]
+                    lo = mine[-1].span_end if mine else 0
+                    if lo <= n and rng.random() < 0.6:
+                        s = rng.randint(lo, n)
+                        dirs.append(W.Dir(s, rng.randint(s, n), 0, seq=b, mode=1))
+                dirs.sort(key=lambda d: (d.seq, d.span_start, d.mode))
+                wl = W.Workload(wl.name, wl.n_layers, wl.dtype, wl.planes, dirs, wl.seq_lens,
+                                page_size=page, seed=wl.seed)
+            cow = ci % 2 == 0
+            print(f"[case] forget/cow {kind} page={page} case={ci} cow={cow} lens={wl.seq_lens} "
+                  f"dirs={wl.dirs}", flush=True)
+            # the pool must hold the fresh pages of the copy-on-write plan
+            plans = O.plan_paged(wl.seq_lens, _odirs(wl), page, remap=not cow)
+            extra = sum(k == O.ASSEMBLE for p in plans for k in p.kinds) + 3
+            pools, bt, free, stubs = W.alloc_paged(wl, DEV, spare_pages=extra)
+            before = [host(p) for p in pools]
+            bt_h, free_h = host(bt), host(free)
+            stubs_h = [[host(s).reshape(wl.n_layers, s.shape[1], p.row_elems) for s, p in zip(per, wl.planes)]
+                       for per in stubs]
+            bt_out, freed, new_lens = _run_gpu(L, wl, pools, bt, free, stubs,
+                                               flags=L.PAGED_COPY_ON_WRITE if cow else 0)
+            planes = [oracle_plane(p) for p in wl.planes]
+            flat = [b.reshape(b.shape[0], b.shape[1], b.shape[2], -1) for b in before]
+            want, want_bt, want_lens, want_freed = O.splice_paged(
+                flat, planes, "bf16", bt_h, wl.seq_lens, _odirs(wl), stubs_h, list(free_h), page,
+                remap=not cow)
+            assert new_lens == want_lens
+            assert np.array_equal(host(bt_out), want_bt)
+            assert list(host(freed)) == want_freed
+            old_pages = sorted({int(bt_h[b, k]) for b, n in enumerate(wl.seq_lens)
+                                for k in range(O.pages_for(n, page))})
+            for pi, plane in enumerate(planes):
+                got = host(pools[pi])
+                assert_rows_match(got.reshape(want[pi].shape), want[pi], plane, "bf16",
+                                  what=f"page={page} case={ci} plane={pi}")
+                if cow:
+                    assert np.array_equal(got[:, old_pages], before[pi][:, old_pages])
 
 
 @pytest.mark.parametrize("kind,dtype", [("mla", "bf16"), ("gqa", "bf16"), ("mla", "f32"),

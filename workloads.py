@@ -51,6 +51,7 @@ class Dir:
     span_end: int
     stub_len: int
     seq: int = 0
+    mode: int = 0                 # 0 AMORTIZE, 1 FORGET
 
 
 @dataclass
