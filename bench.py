@@ -187,7 +187,8 @@ def main():
     t_end.record(stream)
     torch.cuda.synchronize()
     total_ms = t_begin.elapsed_time(t_end)
-    splice_ms = float(np.mean([s.elapsed_time(e) for s, e in zip(starts, ends)]))
+    per_splice = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
+    splice_ms = float(np.mean(per_splice))
 
     achieved = alg_bytes / (splice_ms * 1e-3) / 1e9
     ms_per_step = total_ms / args.steps
@@ -229,6 +230,7 @@ def main():
             "algorithmic_bytes_per_splice": alg_bytes,
             "traffic_per_splice": None if rec is None else {k: rec[k] for k in ("fetch_bytes", "write_bytes", "total_bytes")},
             "splice_ms": splice_ms,
+            "splice_ms_p10_p50_p90": [float(x) for x in np.percentile(per_splice, [10, 50, 90])],
             "launches_per_splice": launches,
             "avg_launch_ms": splice_ms / max(1, launches),
             "d2d_copy_GBps": copy_gbps,
@@ -290,6 +292,17 @@ def setup_paged(wl, dev, L, W, specs, stream):
     return step, kernel, alg_bytes, moved, 1, keep
 
 
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(wl, keep, budget_s, moved):
     """The oracle, as it stands, on a bounded sample of the same splice: whole layers, cycled
     until about budget_s seconds have passed, scaled to all layers.  numpy runs single-threaded
@@ -324,6 +337,8 @@ def cpu_baseline(wl, keep, budget_s, moved):
         "value": moved / full_s,
         "unit": "tokens/s",
         "cores": 1,
+        "host_cpus": os.cpu_count(),
+        "host_cpu_model": _cpu_model(),
         "kind": "oracle",
         "sample": f"{done} layer-splices of this workload (numpy fp64, one thread, layers cycled "
                   f"over {n_keep} host-resident layers), {spent:.1f} s; scaled to {wl.n_layers} "
