@@ -50,6 +50,14 @@ namespace leyline {
 #endif
 
 constexpr int TPB = LEYLINE_TPB;
+#ifndef LEYLINE_CONTIG_RPT
+#define LEYLINE_CONTIG_RPT 2
+#endif
+#ifndef LEYLINE_MOVE_TPB
+#define LEYLINE_MOVE_TPB 256
+#endif
+constexpr int CRPT = LEYLINE_CONTIG_RPT;   // rows per thread of the round / stub kernel
+constexpr int MOVE_TPB = LEYLINE_MOVE_TPB; // its workgroup size
 #ifndef LEYLINE_PAGED_TPB
 #define LEYLINE_PAGED_TPB 256
 #endif
@@ -348,64 +356,86 @@ __device__ __forceinline__ void stage_cs(KCosSin* lcs, const KCosSin* table, int
 
 // --------------------------------------------------------------------- contiguous splice ---
 
-// Rounds and replacement copies: rows laid end to end, one unit per thread; blockIdx.z selects
-// the (job, plane) item.  A thread's data load is issued before the workgroup stages its
-// cos/sin block in LDS, so the two memory latencies overlap.
+// Rounds and replacement copies: rows laid end to end, one unit per thread for CRPT rows (the
+// same column of consecutive rows, so one cos/sin lookup serves them all); blockIdx.z selects the
+// (job, plane) item.  A thread's data loads are issued before the workgroup stages its cos/sin
+// block in LDS, so the two memory latencies overlap.  Past the item's last row a thread loads
+// that last row again (every load issued without branching) and stores nothing.
 template <int ESZ>
-__global__ __launch_bounds__(TPB) void contig_move_kernel(const KContigParams P) {
+__global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigParams P) {
     constexpr int EPC = Elt<ESZ>::EPC;
     __shared__ KCosSin lcs[KMAX_CS];
     const KItem& I = P.items[blockIdx.z];
     const KPlane& pl = I.pl;
-    if (int64_t(blockIdx.x) * TPB >= I.count * pl.tpr) return;    // block past this item's rows
+    const int64_t groups = (I.count + CRPT - 1) / CRPT;
+    if (int64_t(blockIdx.x) * MOVE_TPB >= groups * pl.tpr) return;      // block past this item's rows
     const int layer = blockIdx.y;
-    const int32_t t = int32_t(blockIdx.x) * TPB + int32_t(threadIdx.x);
-    const int32_t r = fdiv(t, pl.tpr_div), u = t - r * pl.tpr;
-    const bool active = r < I.count;
+    const int32_t t = int32_t(blockIdx.x) * MOVE_TPB + int32_t(threadIdx.x);
+    const int32_t g = fdiv(t, pl.tpr_div), u = t - g * pl.tpr;
+    const int64_t r0 = int64_t(g) * CRPT;
+    const bool active = r0 < I.count;
     char* lbase = pl.base + int64_t(layer) * pl.layer_stride;
     const char* src;
     char* dst;
+    int64_t src_step;
     if (I.kind == KJOB_STUB) {
-        src = I.stub + (int64_t(layer) * I.count + r) * pl.row_bytes;
-        dst = lbase + (I.dst0 + r) * pl.token_stride;
+        src = I.stub + int64_t(layer) * I.count * pl.row_bytes;
+        src_step = pl.row_bytes;
+        dst = lbase + I.dst0 * pl.token_stride;
     } else {
-        src = lbase + (I.src0 + r) * pl.token_stride;
+        src = lbase + I.src0 * pl.token_stride;
+        src_step = pl.token_stride;
         dst = const_cast<char*>(src) + I.delta * pl.token_stride;
     }
     const bool rot = I.cs >= 0;                                    // block-uniform
     if (!rot || (pl.rot == KROT_NEOX && !pl.neox_lanes)) {
         // plain copies, and half-split two-chunk units (rare layouts): no early data load
         if (rot) {
-            for (int i = threadIdx.x; i < pl.n_pairs; i += TPB) lcs[i] = P.cs[I.cs + i];
+            for (int i = threadIdx.x; i < pl.n_pairs; i += MOVE_TPB) lcs[i] = P.cs[I.cs + i];
             __syncthreads();
         }
-        if (active) move_row_unit<ESZ>(pl, src, dst, u, lcs, rot ? 0 : -1);
+        if (!active) return;
+        for (int k = 0; k < CRPT; ++k) {
+            const int64_t r = r0 + k;
+            if (r < I.count)
+                move_row_unit<ESZ>(pl, src + r * src_step, dst + r * pl.token_stride, u, lcs, rot ? 0 : -1);
+        }
         return;
     }
     const int64_t off = int64_t(u) * 16;
-    u32x4 v;
-    if (active) v = ld16(src + off);
-    for (int i = threadIdx.x; i < pl.n_pairs; i += TPB) lcs[i] = P.cs[I.cs + i];
+    u32x4 v[CRPT];
+#pragma unroll
+    for (int k = 0; k < CRPT; ++k) {
+        const int64_t r = min(r0 + k, I.count - 1);
+        v[k] = ld16(src + r * src_step + off);
+    }
+    for (int i = threadIdx.x; i < pl.n_pairs; i += MOVE_TPB) lcs[i] = P.cs[I.cs + i];
     __syncthreads();
     if (!active) return;
     const int32_t h = fdiv(u, pl.head_div);
     const int32_t j = u - h * pl.head_chunks - pl.rot_lo;
-    if (h < pl.n_heads && j >= 0 && j < pl.rot_chunks) {
-        if (pl.rot == KROT_INTERLEAVED) {
-            rot_interleaved<ESZ>(v, lcs, j * (EPC / 2));
-        } else {
-            const int32_t half = pl.rot_chunks >> 1;
-            const bool lo = j < half;
-            const int lane = int(threadIdx.x & 63);
-            const int partner = lo ? lane + half : lane - half;
-            u32x4 o;
+    const bool in_band = h < pl.n_heads && j >= 0 && j < pl.rot_chunks;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[i]), partner, 64));
-            if (lo) rot_halves<ESZ>(v, o, lcs, j * EPC);
-            else rot_halves<ESZ>(o, v, lcs, (j - half) * EPC);
+    for (int k = 0; k < CRPT; ++k) {
+        if (r0 + k < I.count) {
+            if (in_band) {
+                if (pl.rot == KROT_INTERLEAVED) {
+                    rot_interleaved<ESZ>(v[k], lcs, j * (EPC / 2));
+                } else {
+                    const int32_t half = pl.rot_chunks >> 1;
+                    const bool lo = j < half;
+                    const int lane = int(threadIdx.x & 63);
+                    const int partner = lo ? lane + half : lane - half;
+                    u32x4 o;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[k][i]), partner, 64));
+                    if (lo) rot_halves<ESZ>(v[k], o, lcs, j * EPC);
+                    else rot_halves<ESZ>(o, v[k], lcs, (j - half) * EPC);
+                }
+            }
+            st16(dst + (r0 + k) * pl.token_stride + off, v[k]);
         }
     }
-    st16(dst + off, v);
 }
 
 // Ordered chains (shifts too small for rounds): thread (chain c, unit u) walks rows c, c+m, ...
@@ -902,7 +932,8 @@ extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len
     // threads of one (job, plane) item; every count must fit a 31-bit index
     auto item_threads = [&](const ContigJobHost& j, int p) -> int64_t {
         if (j.kind == KJOB_CHAIN) return std::min<int64_t>(j.count, abs64(j.delta)) * planes[p].units_all;
-        return j.count * planes[p].tpr;
+        if (j.kind == KJOB_TILE) return j.count * planes[p].tpr;
+        return (j.count + CRPT - 1) / CRPT * planes[p].tpr;
     };
     for (const auto& jobs : sched.launches)
         for (const auto& j : jobs)
@@ -987,8 +1018,8 @@ extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len
                     r = cache->dtype == LEYLINE_BF16 ? launch(contig_chain_kernel<2>, grid, s, P)
                                                      : launch(contig_chain_kernel<4>, grid, s, P);
                 else
-                    r = cache->dtype == LEYLINE_BF16 ? launch(contig_move_kernel<2>, grid, s, P)
-                                                     : launch(contig_move_kernel<4>, grid, s, P);
+                    r = cache->dtype == LEYLINE_BF16 ? launch(contig_move_kernel<2>, grid, s, P, MOVE_TPB)
+                                                     : launch(contig_move_kernel<4>, grid, s, P, MOVE_TPB);
                 P.n_items = 0;
                 cs.clear();
                 max_blocks = 0;
@@ -1016,7 +1047,8 @@ extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len
                     it.chains = int32_t(kind == KJOB_CHAIN ? std::min<int64_t>(j.count, abs64(j.delta)) : 0);
                     it.cs = (cs0 >= 0 && planes[p].rot != KROT_NONE) ? cs0 + planes[p].cs_off : -1;
                     if (kind == KJOB_STUB) it.stub = static_cast<const char*>(dirs[j.dir].stub[p]);
-                    max_blocks = std::max(max_blocks, (th + TPB - 1) / TPB);
+                    const int block = kind == KJOB_CHAIN ? TPB : MOVE_TPB;
+                    max_blocks = std::max(max_blocks, (th + block - 1) / block);
                 }
             }
             rc = flush();
