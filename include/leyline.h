@@ -237,10 +237,11 @@ int leyline_paged_plan(int32_t page_size, int32_t n_seqs, const int32_t* seq_len
  * Host outputs (nullable): new_seq_lens_out[n_seqs], *n_fresh_used_out, *n_freed_out.
  * device_status: device int32, nullable; kernels OR LEYLINE_STATUS_* bits into it when a page
  * index read from device memory is outside [0, capacity) (that row is then skipped).
- * workspace: device, >= the size leyline_paged_query reports.  It receives the plan (uploaded with
- * an asynchronous copy on `stream`) and a table of one 24-byte entry per row of every ASSEMBLE
- * page that a kernel of this call writes and the gather reads; reuse it only after the stream
- * has passed this call.  Any page_size whose rows keep the 16-byte alignment is accepted.
+ * workspace: device, 256-byte aligned, >= the size leyline_paged_query reports.  It receives the
+ * plan (runs of pages, per-sequence and per-directive tables and cos/sin, a few KB, uploaded with
+ * an asynchronous copy on `stream`) and the tables a kernel of this call writes from it (24 bytes
+ * per row of every ASSEMBLE page, 16 bytes per REMAP page); reuse it only after the stream has
+ * passed this call.  Any page_size whose rows keep the 16-byte alignment is accepted.
  *
  * flags: 0, or LEYLINE_PAGED_COPY_ON_WRITE (no REMAP pages: no old page is written).
  * Ownership: only ASSEMBLE pages (fresh) and REMAP pages (rotary bands, in place) are written.
