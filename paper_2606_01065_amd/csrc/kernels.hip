@@ -674,8 +674,53 @@ __device__ __forceinline__ void resolve_freed_entry(const KPagedParams& P, int32
     P.freed_out[f] = P.bt_in[int64_t(R.seq) * P.bt_stride + R.page0 + (f - R.out0)];
 }
 
-// Threads [0, n_rows): ASSEMBLE rows; then n_remap REMAP pages; then n_seqs * bt_stride block-
-// table entries; then n_freed freed-list entries.
+// Orders the call's fresh pages by physical destination page, in buckets of 2^order_shift pages,
+// so that the gather writes neighbouring pages together (with a scattered free list this saves
+// address-translation misses: measured 3 points of peak).  One workgroup: a histogram of the
+// buckets in LDS, an exclusive scan, and a scatter of the fresh ordinals into P.order.  A page
+// outside the pool counts in bucket 0 (its rows are flagged and skipped when resolved).
+constexpr int ORDER_TPB = 1024;
+__global__ __launch_bounds__(ORDER_TPB) void paged_order_kernel(const KPagedParams P) {
+    __shared__ int32_t cnt[KORDER_BUCKETS];
+    __shared__ int32_t part[ORDER_TPB];
+    const int tid = int(threadIdx.x);
+    for (int i = tid; i < KORDER_BUCKETS; i += ORDER_TPB) cnt[i] = 0;
+    __syncthreads();
+    auto bucket = [&](int32_t t) {
+        const int32_t pg = t < P.n_free ? P.free_pages[t] : -1;
+        return (pg < 0 || pg >= P.capacity) ? 0 : (pg >> P.order_shift);
+    };
+    for (int32_t t = tid; t < P.n_asm; t += ORDER_TPB) atomicAdd(&cnt[bucket(t)], 1);
+    __syncthreads();
+    // exclusive scan: each thread owns KORDER_BUCKETS / ORDER_TPB consecutive buckets
+    constexpr int PER = KORDER_BUCKETS / ORDER_TPB;
+    int32_t own[PER], sum = 0;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        own[k] = cnt[tid * PER + k];
+        sum += own[k];
+    }
+    part[tid] = sum;
+    __syncthreads();
+    for (int off = 1; off < ORDER_TPB; off <<= 1) {
+        const int32_t v = tid >= off ? part[tid - off] : 0;
+        __syncthreads();
+        part[tid] += v;
+        __syncthreads();
+    }
+    int32_t run = part[tid] - sum;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        cnt[tid * PER + k] = run;
+        run += own[k];
+    }
+    __syncthreads();
+    for (int32_t t = tid; t < P.n_asm; t += ORDER_TPB) P.order[atomicAdd(&cnt[bucket(t)], 1)] = t;
+}
+
+// Threads [0, n_rows): ASSEMBLE rows, laid out in destination order when P.order is set; then
+// n_remap REMAP pages; then n_seqs * bt_stride block-table entries; then n_freed freed-list
+// entries.
 __global__ __launch_bounds__(TPB) void paged_resolve_kernel(const KPagedParams P) {
     int32_t i = int32_t(blockIdx.x) * TPB + int32_t(threadIdx.x);
     if (i >= P.n_rows) {
@@ -687,7 +732,8 @@ __global__ __launch_bounds__(TPB) void paged_resolve_kernel(const KPagedParams P
         if (i < P.n_freed) resolve_freed_entry(P, i);
         return;
     }
-    const int32_t task = i / P.page_size, r = i - task * P.page_size;   // task = fresh ordinal
+    const int32_t slot = i / P.page_size, r = i - slot * P.page_size;
+    const int32_t task = P.order ? P.order[slot] : slot;               // fresh ordinal
     const KPageRun R = P.asm_runs[run_of(P.asm_runs, P.n_asm_runs, task)];
     const int32_t seq = R.seq, k = R.k0 + (task - R.ord0);
     const KSeqEntry S = P.seqs[seq];
@@ -1205,6 +1251,14 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         P.n_free = n_free;
         P.status = device_status;
         const bool bf16 = cache->dtype == LEYLINE_BF16;
+        if (t.n_asm >= KORDER_MIN) {
+            int32_t shift = 0;
+            while (((cache->capacity - 1) >> shift) >= KORDER_BUCKETS) ++shift;
+            P.order_shift = shift;
+            P.order = reinterpret_cast<int32_t*>(ws + t.off_order);
+            rc = launch(paged_order_kernel, dim3(1), s, P, ORDER_TPB);
+            if (rc) return rc;
+        }
         rc = launch(paged_resolve_kernel, dim3(unsigned((n_resolve + TPB - 1) / TPB)), s, P);
         if (rc) return rc;
         // data kernel: gather workgroups, then REMAP workgroups, once per access class of the

@@ -181,7 +181,7 @@ struct KRemapPage {
 // Byte offsets of the tables inside the workspace (converted to pointers at launch).
 struct KPagedTables {
     int64_t off_seq, off_dir, off_cs, off_runs, off_asm_runs, off_remap_runs, off_freed_runs;
-    int64_t off_rows, off_remap_pages;
+    int64_t off_rows, off_remap_pages, off_order;
     int64_t upload;          // bytes uploaded from the host (the tables before the row tables)
     int64_t total;           // workspace bytes (the row tables are written on the device)
     int32_t n_seqs, n_dirs, n_cs, n_runs, n_asm_runs, n_remap_runs, n_freed_runs;
@@ -198,7 +198,7 @@ struct KPagedParams {
     int32_t n_asm;
     int32_t n_remap;
     int32_t n_rows;          // ASSEMBLE rows (n_asm * page_size)
-    int32_t pad0;
+    int32_t order_shift;     // destination-order bucket = physical page >> order_shift
     KDiv remap_div[LEYLINE_MAX_PLANES];  // by page_size * rot_tpr (band units per REMAP page)
     KDiv rot_div[LEYLINE_MAX_PLANES];    // by rot_tpr (band units per row)
     int64_t capacity;                    // physical pages
@@ -224,7 +224,14 @@ struct KPagedParams {
     int32_t n_freed;
     int32_t n_freed_runs;
     int32_t move_blocks;     // data kernel: workgroups of the ASSEMBLE gather (the rest rotate)
+    int32_t pad1;
+    int32_t* order;          // workspace, n_asm fresh ordinals in destination-page order (or null)
 };
+
+// The gather is ordered by destination page (neighbouring physical pages processed together)
+// when a call assembles at least this many pages; KORDER_BUCKETS buckets of pages, counted in LDS.
+constexpr int32_t KORDER_MIN = 64;
+constexpr int32_t KORDER_BUCKETS = 4096;
 
 
 }  // namespace leyline

@@ -536,6 +536,7 @@ int build_paged_image(const leyline_cache* cache, const PagedPlan& plan, int32_t
     if (n_rows > INT32_MAX) return LEYLINE_E_CAPACITY;
     t.off_rows = place(size_t(n_rows) * sizeof(KRowMove));
     t.off_remap_pages = place(size_t(plan.n_remap) * sizeof(KRemapPage));
+    t.off_order = place(plan.n_fresh >= KORDER_MIN ? size_t(plan.n_fresh) * sizeof(int32_t) : 0);
     t.total = off;
     t.n_seqs = n_seqs; t.n_dirs = n_dirs; t.n_cs = int32_t(cs.size());
     t.n_runs = int32_t(plan.runs.size());
