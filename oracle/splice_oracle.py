@@ -24,13 +24,18 @@ What is computed, and where the paper defines it
   precision floor").  Here: float64 angles, float64 trig, float64 pair products, one
   round-to-nearest-even to the storage dtype.
 
+* A FORGET directive hands the edit to a prefix-trimmed re-prefill (Sec. 3.1, "The FORGET
+  mode"): on the cache, the sequence is cut at the span's start after the earlier directives.
+
 The frequency schedule ``theta_i = base ** (-2 i / d_rot)`` is RoFormer's, which the paper cites
 for RoPE without restating (Sec. 3.2).
 
 Paged caches are not described by the paper at all.  The page-kind rule below (identity /
 remap / assemble, fresh pages drawn in ascending (sequence, page) order, freed pages listed in
-ascending (sequence, old page) order) is this project's reading.  It is pinned by invariants and
-by reconstruction against the contiguous definition, not by any value in the paper.
+ascending (sequence, old page) order) is this project's reading, and so is its copy-on-write
+variant (no page re-used with a shift), read from the Role A/B integration of Sec. 3.3 that writes
+rotated KV to fresh destination slots.  Both are pinned by invariants and by reconstruction
+against the contiguous definition, not by any value in the paper.
 
 Everything here is deliberately plain: no blocking, no fusion, no reordering beyond what the
 definition states.

@@ -234,6 +234,10 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
             jobs.push_back(ContigJobHost{KJOB_CHAIN, d.span_end, 0, count, shift, j});
     }
     if (jobs.empty()) return LEYLINE_OK;
+    // kernels index the chunks of one (job, plane) with 31-bit integers
+    for (const ContigJobHost& x : jobs)
+        for (int p = 0; p < n_planes; ++p)
+            if (x.count * planes[p].row_chunks > INT32_MAX - 2 * int64_t(KTILE_CHUNKS)) return LEYLINE_E_INVAL;
 
     // Job a must finish before job b when b writes a row that a reads.  The resulting graph is
     // acyclic: a left-moving segment can only wait for segments to its left, a right-moving one

@@ -328,3 +328,21 @@ def test_rotate_delta_validation():
         L.leyline_rotate_delta(c, 5, row0=60, n_rows=5, stream=0)
     assert e.value.code == L.E_RANGE
     L.leyline_rotate_delta(c, 0, row0=0, n_rows=64, stream=0)             # R(0): nothing enqueued
+
+
+def test_sizes_beyond_31_bit_indices_are_refused_before_any_enqueue():
+    """Kernels index chunks with 31-bit integers; descriptors whose moves or tables would not fit
+    are refused on the host (no device access: the pointers here are fake)."""
+    huge = _mla_cache(n_layers=2, cap=1 << 31)                # 72 chunks per row
+    n = (1 << 31) - 8
+    rc = _contig_rc(huge, n, [(10, 12, 0)])                    # ~2^31 rows moved: > 2^31 chunks
+    assert rc in (L.E_INVAL, L.E_WORKSPACE)
+    with pytest.raises(L.LeylineError) as e:
+        L.leyline_contig_query(huge, n, _dirs([(10, 12, 0)]), 1)
+    assert e.value.code == L.E_INVAL
+    import torch
+    pool = _FakeTensor((2, 1 << 26, 64, 576), torch.bfloat16)  # 2^32 rows in the pool
+    cache = L.make_cache([L.PlaneSpec(pool, 1, 576, 512, 64)], paged=True)
+    with pytest.raises(L.LeylineError) as e:                 # in-place rotation of paged rows
+        L.leyline_rotate_delta(cache, 5, row0=0, n_rows=10, stream=0)
+    assert e.value.code == L.E_INVAL
