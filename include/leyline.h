@@ -176,6 +176,8 @@ int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
  * (NULL allowed when that size is 0).  The call clears it on `stream` before use; reuse it only
  * after the stream has passed this call, and do not share one workspace between calls that may
  * run at the same time.
+ * Enqueues kernels only (all parameters travel as kernel arguments; the workspace is cleared by a
+ * kernel), so the call may be captured into a HIP graph; each replay repeats the same splice.
  * Errors: E_INVAL, E_RANGE, E_ORDER, E_OVERLAP, E_CAPACITY (new length > capacity), E_MODE,
  * E_WORKSPACE (missing, misaligned or too small), E_HIP.
  */
@@ -242,6 +244,8 @@ int leyline_paged_plan(int32_t page_size, int32_t n_seqs, const int32_t* seq_len
  * an asynchronous copy on `stream`) and the tables a kernel of this call writes from it (24 bytes
  * per row of every ASSEMBLE page, 16 bytes per REMAP page); reuse it only after the stream has
  * passed this call.  Any page_size whose rows keep the 16-byte alignment is accepted.
+ * The plan is uploaded from host memory the call owns only while it runs: do not capture this
+ * call into a HIP graph.
  *
  * flags: 0, or LEYLINE_PAGED_COPY_ON_WRITE (no REMAP pages: no old page is written).
  * Ownership: only ASSEMBLE pages (fresh) and REMAP pages (rotary bands, in place) are written.
