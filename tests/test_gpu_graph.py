@@ -1,0 +1,78 @@
+"""The contiguous splice and the in-place rotation enqueue kernels only, so a caller may capture
+them into a HIP graph.  Each test runs the call eagerly, captures it, then replays the graph
+several times, restoring the input eagerly between replays, and compares every replay with the
+eager result bit for bit (same kernels, same inputs)."""
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from tests.parity_util import host
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2606_01065_amd import leyline
+    return leyline
+
+
+def _mla_cache(L, n_layers, capacity, seed):
+    wl = W.Workload("graph", n_layers, "bf16", [W.mla_plane()], [], [capacity], capacity=capacity, seed=seed)
+    planes, _ = W.alloc_contig(wl, DEV)
+    t = planes[0]
+    return t, L.make_cache([L.PlaneSpec(t, 1, 576, 512, 64, L.ROPE_INTERLEAVED, 10000.0)])
+
+
+def _replay_and_compare(fn, t, pristine, eager):
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    t.copy_(pristine)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=stream):
+        fn()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        t.copy_(pristine)                      # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(host(t), eager), f"replay {rep} differs from the eager call"
+
+
+@pytest.mark.parametrize("layers,n,span,stub_len,tiles", [
+    (3, 3000, (500, 501), 0, 1),          # shift -1: ordered tiles (clear + tile launches)
+    (20, 12000, (1000, 5000), 16, 0),     # shift -3984, 92 MB rounds: round launches + stub copy
+])
+def test_contig_splice_in_a_graph(L, layers, n, span, stub_len, tiles):
+    cap = n
+    t, cache = _mla_cache(L, layers, cap, seed=31)
+    pristine = t.clone()
+    stub = torch.randn((layers, stub_len, 576), device=DEV).to(torch.bfloat16) if stub_len else None
+    dirs = L.make_directives([dict(span_start=span[0], span_end=span[1], stub=[stub] if stub is not None else None,
+                                   stub_len=stub_len)])
+    q = L.leyline_contig_query(cache, n, dirs, 1)
+    assert q.tile_launches == tiles
+    ws = torch.empty(max(256, q.workspace_bytes), dtype=torch.uint8, device=DEV)
+    print(f"[case] graph contig span={span} stub={stub_len} launches={q.launches} tiles={q.tile_launches}",
+          flush=True)
+    L.leyline_splice_contig(cache, n, dirs, 1, workspace=ws)
+    torch.cuda.synchronize()
+    eager = host(t)
+    assert not np.array_equal(eager, host(pristine))
+    _replay_and_compare(lambda: L.leyline_splice_contig(cache, n, dirs, 1, workspace=ws), t, pristine, eager)
+
+
+def test_rotate_delta_in_a_graph(L):
+    t, cache = _mla_cache(L, 2, 2048, seed=32)
+    pristine = t.clone()
+    print("[case] graph rotate", flush=True)
+    L.leyline_rotate_delta(cache, -4064, row0=100, n_rows=1500)
+    torch.cuda.synchronize()
+    eager = host(t)
+    _replay_and_compare(lambda: L.leyline_rotate_delta(cache, -4064, row0=100, n_rows=1500), t, pristine, eager)
