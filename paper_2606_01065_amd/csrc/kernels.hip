@@ -348,6 +348,14 @@ __device__ __forceinline__ void band_rotate_store(const KPlane& pl, const BandPo
     }
 }
 
+// The plane whose workgroup range [base[p], base[p+1]) holds workgroup bx (ranges of planes
+// without work are empty, so no workgroup is launched for them).
+__device__ __forceinline__ int plane_of(const int32_t* base, int n, int32_t bx) {
+    int p = 0;
+    while (p + 1 < n && bx >= base[p + 1]) ++p;
+    return p;
+}
+
 // cos/sin block of one shift (n entries from table[c0]) staged in LDS by the whole workgroup.
 template <int NT>
 __device__ __forceinline__ void stage_cs(KCosSin* lcs, const KCosSin* table, int32_t c0, int32_t n) {
@@ -568,22 +576,24 @@ __global__ __launch_bounds__(TPB) void zero_words_kernel(const KZeroParams Z) {
 
 // ------------------------------------------------------------------------ rotate in place ---
 
-// In-place R(delta) on listed rows: band units of all rows laid end to end, one plane per
-// blockIdx.z, PAGED_LPT layers per thread, the shift's cos/sin staged in LDS.
-template <int ESZ, bool NT>
+// In-place R(delta) on listed rows: band units of all rows laid end to end, the workgroups of
+// each rotary plane after those of the previous one, PAGED_LPT layers per thread, the shift's
+// cos/sin staged in LDS.
+// SOLO: only plane 0 has work in this launch, so no workgroup looks its plane up (one level of
+// dependent scalar loads less before the data loads).
+template <int ESZ, bool NT, bool SOLO>
 __global__ __launch_bounds__(PAGED_TPB) void rotate_rows_kernel(const KRotateParams P) {
     __shared__ KCosSin lcs[KMAX_CS];
-    const int plane = blockIdx.z;
+    const int plane = SOLO ? 0 : plane_of(P.rot_base, P.n_planes, int32_t(blockIdx.x));
     const KPlane& pl = P.planes[plane];
-    if (pl.rot_tpr == 0 || pl.band_nt != int(NT)) return;               // not this launch's class
-    const int32_t tb = int32_t(blockIdx.x) * PAGED_TPB;
+    const int32_t tb = (SOLO ? int32_t(blockIdx.x) : int32_t(blockIdx.x) - P.rot_base[plane]) * PAGED_TPB;
     if (int64_t(tb) >= P.n_rows * pl.rot_tpr) return;                  // past this plane
     const int32_t t = tb + int32_t(threadIdx.x);
     const int32_t i = fdiv(t, P.rot_div[plane]), q = t - i * pl.rot_tpr;
     bool active = i < P.n_rows;
     int64_t row = active ? (P.rows ? P.rows[i] : P.row0 + i) : 0;
     if (active && (row < 0 || row >= P.total_rows)) {
-        if (P.status && q == 0 && plane == 0 && blockIdx.y == 0) atomicOr(P.status, int(LEYLINE_STATUS_BAD_ROW));
+        if (P.status && q == 0 && blockIdx.y == 0) atomicOr(P.status, int(LEYLINE_STATUS_BAD_ROW));
         active = false;
     }
     const int layer0 = int(blockIdx.y) * PAGED_LPT;
@@ -782,8 +792,7 @@ __global__ __launch_bounds__(TPB) void paged_resolve_kernel(const KPagedParams P
 
 // One workgroup of the ASSEMBLE gather (bx: its index among the gather's workgroups).
 template <int ESZ>
-__device__ __forceinline__ void paged_move_block(const KPagedParams& P, int32_t bx, KCosSin* lcs) {
-    const int plane = blockIdx.z;
+__device__ __forceinline__ void paged_move_block(const KPagedParams& P, int plane, int32_t bx, KCosSin* lcs) {
     const KPlane& pl = P.planes[plane];
     const int32_t tb = bx * PAGED_TPB;
     if (int64_t(tb) >= int64_t(P.n_rows) * pl.tpr) return;            // past this plane
@@ -845,10 +854,8 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, int32_t 
 // of its first page's shift in LDS; rows with another shift (where runs meet) read the table in
 // the workspace.
 template <int ESZ, bool NT>
-__device__ __forceinline__ void paged_remap_block(const KPagedParams& P, int32_t bx, KCosSin* lcs) {
-    const int plane = blockIdx.z;
+__device__ __forceinline__ void paged_remap_block(const KPagedParams& P, int plane, int32_t bx, KCosSin* lcs) {
     const KPlane& pl = P.planes[plane];
-    if (pl.rot_tpr == 0 || pl.band_nt != int(NT)) return;               // not this launch's class
     const int32_t upp = P.page_size * pl.rot_tpr;
     const int32_t tb = bx * PAGED_TPB;
     if (int64_t(tb) >= int64_t(P.n_remap) * upp) return;               // past this plane
@@ -875,14 +882,22 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, int32_t
     else band_rotate_store<ESZ, NT>(pl, bp, row, pl.layer_stride, nl, x, y, P.cs, e.cs + pl.cs_off);
 }
 
-// Workgroups [0, move_blocks) gather ASSEMBLE rows, the rest rotate REMAP pages whose planes
-// belong to access class NT.
-template <int ESZ, bool NT>
+// The first workgroups gather ASSEMBLE rows (plane by plane), the rest rotate REMAP pages of the
+// planes in access class NT (plane by plane); planes without work get no workgroups.  SOLO: only
+// plane 0 has work in this launch, so no workgroup looks its plane up.
+template <int ESZ, bool NT, bool SOLO>
 __global__ __launch_bounds__(PAGED_TPB) void paged_data_kernel(const KPagedParams P) {
     __shared__ KCosSin lcs[KMAX_CS];
-    const int32_t bx = int32_t(blockIdx.x);
-    if (bx < P.move_blocks) paged_move_block<ESZ>(P, bx, lcs);
-    else paged_remap_block<ESZ, NT>(P, bx - P.move_blocks, lcs);
+    int32_t bx = int32_t(blockIdx.x);
+    const int32_t moves = SOLO ? P.move_base[1] : P.move_base[P.n_planes];
+    if (bx < moves) {
+        const int p = SOLO ? 0 : plane_of(P.move_base, P.n_planes, bx);
+        paged_move_block<ESZ>(P, p, bx - P.move_base[p], lcs);
+    } else {
+        bx -= moves;
+        const int p = SOLO ? 0 : plane_of(P.remap_base, P.n_planes, bx);
+        paged_remap_block<ESZ, NT>(P, p, bx - P.remap_base[p], lcs);
+    }
 }
 
 // -------------------------------------------------------------------------- host launchers ---
@@ -1141,21 +1156,32 @@ extern "C" int leyline_rotate_delta(const leyline_cache* cache, int64_t delta,
     std::vector<KCosSin> cs;
     append_cos_sin(cache, delta, cs);
     std::copy(cs.begin(), cs.end(), P.cs);
-    const int64_t blocks = (n_rows * max_rot + PAGED_TPB - 1) / PAGED_TPB;
-    const dim3 grid(unsigned(blocks), unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT), unsigned(n_planes));
     hipStream_t s = static_cast<hipStream_t>(stream);
     const bool bf16 = cache->dtype == LEYLINE_BF16;
-    // one launch per access class present among the rotary planes
+    // one launch per access class present among the rotary planes; each launch lays out the
+    // workgroups of its planes one plane after another
     for (int nt = 1; nt >= 0; --nt) {
-        bool any = false;
-        for (int p = 0; p < n_planes; ++p) any = any || (planes[p].rot_tpr > 0 && planes[p].band_nt == nt);
-        if (!any) continue;
+        int64_t total = 0;
+        P.rot_base[0] = 0;
+        for (int p = 0; p < n_planes; ++p) {
+            if (planes[p].rot_tpr > 0 && planes[p].band_nt == nt)
+                total += (n_rows * planes[p].rot_tpr + PAGED_TPB - 1) / PAGED_TPB;
+            if (total > INT32_MAX - 1024) return LEYLINE_E_INVAL;
+            P.rot_base[p + 1] = int32_t(total);
+        }
+        if (total == 0) continue;
+        const dim3 grid(unsigned(total), unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT), 1);
+        const bool solo = P.rot_base[1] == total;                        // plane 0 only
         if (nt)
-            rc = bf16 ? launch(rotate_rows_kernel<2, true>, grid, s, P, PAGED_TPB)
-                      : launch(rotate_rows_kernel<4, true>, grid, s, P, PAGED_TPB);
+            rc = solo ? (bf16 ? launch(rotate_rows_kernel<2, true, true>, grid, s, P, PAGED_TPB)
+                              : launch(rotate_rows_kernel<4, true, true>, grid, s, P, PAGED_TPB))
+                      : (bf16 ? launch(rotate_rows_kernel<2, true, false>, grid, s, P, PAGED_TPB)
+                              : launch(rotate_rows_kernel<4, true, false>, grid, s, P, PAGED_TPB));
         else
-            rc = bf16 ? launch(rotate_rows_kernel<2, false>, grid, s, P, PAGED_TPB)
-                      : launch(rotate_rows_kernel<4, false>, grid, s, P, PAGED_TPB);
+            rc = solo ? (bf16 ? launch(rotate_rows_kernel<2, false, true>, grid, s, P, PAGED_TPB)
+                              : launch(rotate_rows_kernel<4, false, true>, grid, s, P, PAGED_TPB))
+                      : (bf16 ? launch(rotate_rows_kernel<2, false, false>, grid, s, P, PAGED_TPB)
+                              : launch(rotate_rows_kernel<4, false, false>, grid, s, P, PAGED_TPB));
         if (rc) return rc;
     }
     return LEYLINE_OK;
@@ -1262,25 +1288,36 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         rc = launch(paged_resolve_kernel, dim3(unsigned((n_resolve + TPB - 1) / TPB)), s, P);
         if (rc) return rc;
         // data kernel: gather workgroups, then REMAP workgroups, once per access class of the
-        // rotary planes (the gather runs with the first launch)
-        const int64_t move_blocks = t.n_rows > 0 ? (int64_t(t.n_rows) * max_tpr + PAGED_TPB - 1) / PAGED_TPB : 0;
-        const int64_t remap_blocks = t.n_remap > 0 ? (int64_t(t.n_remap) * max_upp + PAGED_TPB - 1) / PAGED_TPB : 0;
-        const dim3 layers_planes(1, unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT), unsigned(n_planes));
-        // the gather goes with the first class that has REMAP work (or alone)
+        // rotary planes; the gather goes with the first class that has REMAP work (or alone)
         int gather_class = 1;
-        if (remap_blocks > 0 && !any_band[1] && any_band[0]) gather_class = 0;
+        if (t.n_remap > 0 && !any_band[1] && any_band[0]) gather_class = 0;
+        const dim3 layers(1, unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT), 1);
         for (int nt = 1; nt >= 0; --nt) {
-            const int64_t rb = any_band[nt] ? remap_blocks : 0;
-            const int64_t mb = nt == gather_class ? move_blocks : 0;
+            int64_t mb = 0, rb = 0;
+            P.move_base[0] = P.remap_base[0] = 0;
+            for (int p = 0; p < n_planes; ++p) {
+                if (nt == gather_class && t.n_rows > 0)
+                    mb += (int64_t(t.n_rows) * planes[p].tpr + PAGED_TPB - 1) / PAGED_TPB;
+                if (t.n_remap > 0 && planes[p].rot_tpr > 0 && planes[p].band_nt == nt)
+                    rb += (int64_t(t.n_remap) * cache->page_size * planes[p].rot_tpr + PAGED_TPB - 1) / PAGED_TPB;
+                if (mb > INT32_MAX - 1024 || rb > INT32_MAX - 1024 || mb + rb > INT32_MAX - 1024)
+                    return LEYLINE_E_INVAL;
+                P.move_base[p + 1] = int32_t(mb);
+                P.remap_base[p + 1] = int32_t(rb);
+            }
             if (mb + rb == 0) continue;
-            P.move_blocks = int32_t(mb);
-            const dim3 grid(unsigned(mb + rb), layers_planes.y, layers_planes.z);
+            const dim3 grid(unsigned(mb + rb), layers.y, 1);
+            const bool solo = P.move_base[1] == mb && P.remap_base[1] == rb;   // plane 0 only
             if (nt)
-                rc = bf16 ? launch(paged_data_kernel<2, true>, grid, s, P, PAGED_TPB)
-                          : launch(paged_data_kernel<4, true>, grid, s, P, PAGED_TPB);
+                rc = solo ? (bf16 ? launch(paged_data_kernel<2, true, true>, grid, s, P, PAGED_TPB)
+                                  : launch(paged_data_kernel<4, true, true>, grid, s, P, PAGED_TPB))
+                          : (bf16 ? launch(paged_data_kernel<2, true, false>, grid, s, P, PAGED_TPB)
+                                  : launch(paged_data_kernel<4, true, false>, grid, s, P, PAGED_TPB));
             else
-                rc = bf16 ? launch(paged_data_kernel<2, false>, grid, s, P, PAGED_TPB)
-                          : launch(paged_data_kernel<4, false>, grid, s, P, PAGED_TPB);
+                rc = solo ? (bf16 ? launch(paged_data_kernel<2, false, true>, grid, s, P, PAGED_TPB)
+                                  : launch(paged_data_kernel<4, false, true>, grid, s, P, PAGED_TPB))
+                          : (bf16 ? launch(paged_data_kernel<2, false, false>, grid, s, P, PAGED_TPB)
+                                  : launch(paged_data_kernel<4, false, false>, grid, s, P, PAGED_TPB));
             if (rc) return rc;
         }
     }

@@ -126,6 +126,8 @@ struct KRotateParams {
     int32_t* status;         // device, nullable
     KDiv rot_div[LEYLINE_MAX_PLANES];   // by rot_tpr (band units per row)
     KDiv page_div;           // by page_size (paged caches)
+    int32_t rot_base[LEYLINE_MAX_PLANES + 1];   // workgroups of plane p: [rot_base[p], rot_base[p+1])
+    int32_t pad3;
     KCosSin cs[KMAX_CS];
 };
 
@@ -223,7 +225,10 @@ struct KPagedParams {
     int32_t n_table;         // n_seqs * bt_stride
     int32_t n_freed;
     int32_t n_freed_runs;
-    int32_t move_blocks;     // data kernel: workgroups of the ASSEMBLE gather (the rest rotate)
+    int32_t move_base[LEYLINE_MAX_PLANES + 1];   // data kernel: gather workgroups of plane p are
+                                                 // [move_base[p], move_base[p+1])
+    int32_t remap_base[LEYLINE_MAX_PLANES + 1];  // then REMAP workgroups of plane p, numbered
+                                                 // from 0 after the gather's
     int32_t pad1;
     int32_t* order;          // workspace, n_asm fresh ordinals in destination-page order (or null)
 };
