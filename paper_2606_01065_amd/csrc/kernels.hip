@@ -628,6 +628,32 @@ __global__ __launch_bounds__(PAGED_TPB) void rotate_rows_kernel(const KRotatePar
 // Nothing is written to an old page except the rotary bands of REMAP pages, which no ASSEMBLE
 // row reads.
 
+// The plan's tables, in the workspace or in this launch's kernel arguments.
+struct PlanView {
+    const KSeqEntry* seqs;
+    const KDirEntry* dirs;
+    const KCosSin* cs;
+    const KPageRun* runs;
+    const KPageRun* asm_runs;
+    const KPageRun* remap_runs;
+    const KFreedRun* freed_runs;
+};
+
+// The kernel's only argument is a KPagedParams at the start of the kernel-argument segment, so an
+// inline plan sits at that segment's address plus the offset of `blob` (the address of the
+// argument itself is not taken, which would make the compiler copy it into private memory).
+__device__ __forceinline__ PlanView plan_view(const KPagedParams& P) {
+    const char* kernarg = (const char*)__builtin_amdgcn_kernarg_segment_ptr();
+    const char* b = P.plan ? P.plan : kernarg + offsetof(KPagedParams, blob);
+    return PlanView{reinterpret_cast<const KSeqEntry*>(b + P.off_seq),
+                    reinterpret_cast<const KDirEntry*>(b + P.off_dir),
+                    reinterpret_cast<const KCosSin*>(b + P.off_cs),
+                    reinterpret_cast<const KPageRun*>(b + P.off_runs),
+                    reinterpret_cast<const KPageRun*>(b + P.off_asm_runs),
+                    reinterpret_cast<const KPageRun*>(b + P.off_remap_runs),
+                    reinterpret_cast<const KFreedRun*>(b + P.off_freed_runs)};
+}
+
 // The run holding ordinal x among n runs sorted by ord0 (runs[0].ord0 <= x).
 __device__ __forceinline__ int32_t run_of(const KPageRun* runs, int32_t n, int32_t x) {
     int32_t lo = 0, hi = n;
@@ -638,11 +664,11 @@ __device__ __forceinline__ int32_t run_of(const KPageRun* runs, int32_t n, int32
     return lo;
 }
 
-__device__ __forceinline__ void resolve_remap_page(const KPagedParams& P, int32_t m) {
-    const KPageRun R = P.remap_runs[run_of(P.remap_runs, P.n_remap_runs, m)];
+__device__ __forceinline__ void resolve_remap_page(const KPagedParams& P, const PlanView& V, int32_t m) {
+    const KPageRun R = V.remap_runs[run_of(V.remap_runs, P.n_remap_runs, m)];
     const int32_t c = m - R.ord0;
-    const KSeqEntry S = P.seqs[R.seq];
-    const KDirEntry& D = P.dirs[R.dir];
+    const KSeqEntry S = V.seqs[R.seq];
+    const KDirEntry& D = V.dirs[R.dir];
     KRemapPage e{0, D.cs, 0, 0};
     const int32_t pg = P.bt_in[int64_t(R.seq) * P.bt_stride + R.src0 + c];
     if (pg < 0 || pg >= P.capacity) {
@@ -655,17 +681,17 @@ __device__ __forceinline__ void resolve_remap_page(const KPagedParams& P, int32_
 }
 
 // New block-table entry i (sequence i / bt_stride, page i % bt_stride) from the page runs.
-__device__ __forceinline__ void resolve_table_entry(const KPagedParams& P, int32_t i) {
+__device__ __forceinline__ void resolve_table_entry(const KPagedParams& P, const PlanView& V, int32_t i) {
     const int32_t b = i / P.bt_stride, k = i - b * P.bt_stride;
-    const KSeqEntry S = P.seqs[b];
+    const KSeqEntry S = V.seqs[b];
     int32_t v = -1;
     if (S.run_count > 0 && int64_t(k) * P.page_size < S.new_len) {
         int32_t lo = S.run_begin, hi = S.run_begin + S.run_count;
         while (hi - lo > 1) {
             const int32_t mid = (lo + hi) >> 1;
-            if (P.runs[mid].k0 <= k) lo = mid; else hi = mid;
+            if (V.runs[mid].k0 <= k) lo = mid; else hi = mid;
         }
-        const KPageRun R = P.runs[lo];
+        const KPageRun R = V.runs[lo];
         const int32_t src = R.src0 + (k - R.k0);
         if (R.kind == LEYLINE_PAGE_ASSEMBLE) v = src < P.n_free ? P.free_pages[src] : -1;
         else v = P.bt_in[int64_t(b) * P.bt_stride + src];
@@ -674,13 +700,13 @@ __device__ __forceinline__ void resolve_table_entry(const KPagedParams& P, int32
 }
 
 // Freed-list entry f from the freed runs.
-__device__ __forceinline__ void resolve_freed_entry(const KPagedParams& P, int32_t f) {
+__device__ __forceinline__ void resolve_freed_entry(const KPagedParams& P, const PlanView& V, int32_t f) {
     int32_t lo = 0, hi = P.n_freed_runs;
     while (hi - lo > 1) {
         const int32_t mid = (lo + hi) >> 1;
-        if (P.freed_runs[mid].out0 <= f) lo = mid; else hi = mid;
+        if (V.freed_runs[mid].out0 <= f) lo = mid; else hi = mid;
     }
-    const KFreedRun R = P.freed_runs[lo];
+    const KFreedRun R = V.freed_runs[lo];
     P.freed_out[f] = P.bt_in[int64_t(R.seq) * P.bt_stride + R.page0 + (f - R.out0)];
 }
 
@@ -732,21 +758,22 @@ __global__ __launch_bounds__(ORDER_TPB) void paged_order_kernel(const KPagedPara
 // n_remap REMAP pages; then n_seqs * bt_stride block-table entries; then n_freed freed-list
 // entries.
 __global__ __launch_bounds__(TPB) void paged_resolve_kernel(const KPagedParams P) {
+    const PlanView V = plan_view(P);
     int32_t i = int32_t(blockIdx.x) * TPB + int32_t(threadIdx.x);
     if (i >= P.n_rows) {
         i -= P.n_rows;
-        if (i < P.n_remap) { resolve_remap_page(P, i); return; }
+        if (i < P.n_remap) { resolve_remap_page(P, V, i); return; }
         i -= P.n_remap;
-        if (i < P.n_table) { resolve_table_entry(P, i); return; }
+        if (i < P.n_table) { resolve_table_entry(P, V, i); return; }
         i -= P.n_table;
-        if (i < P.n_freed) resolve_freed_entry(P, i);
+        if (i < P.n_freed) resolve_freed_entry(P, V, i);
         return;
     }
     const int32_t slot = i / P.page_size, r = i - slot * P.page_size;
     const int32_t task = P.order ? P.order[slot] : slot;               // fresh ordinal
-    const KPageRun R = P.asm_runs[run_of(P.asm_runs, P.n_asm_runs, task)];
+    const KPageRun R = V.asm_runs[run_of(V.asm_runs, P.n_asm_runs, task)];
     const int32_t seq = R.seq, k = R.k0 + (task - R.ord0);
-    const KSeqEntry S = P.seqs[seq];
+    const KSeqEntry S = V.seqs[seq];
     const int64_t q = int64_t(k) * P.page_size + r;
     KRowMove e{KROW_SKIP, 0, 0, r, -1, -1};
     if (q < S.new_len) {
@@ -759,12 +786,12 @@ __global__ __launch_bounds__(TPB) void paged_resolve_kernel(const KPagedParams P
             int32_t jlo = 0, jhi = S.dir_count;
             while (jlo < jhi) {
                 const int32_t mid = (jlo + jhi) >> 1;
-                if (P.dirs[S.dir_begin + mid].stub_start <= q) jlo = mid + 1; else jhi = mid;
+                if (V.dirs[S.dir_begin + mid].stub_start <= q) jlo = mid + 1; else jhi = mid;
             }
             int64_t old = q;
             if (jlo > 0) {
                 const int32_t j = S.dir_begin + jlo - 1;
-                const KDirEntry& D = P.dirs[j];
+                const KDirEntry& D = V.dirs[j];
                 if (q < D.stub_start + D.stub_len) {
                     e.src_page = KROW_STUB;
                     e.src_row = int32_t(q - D.stub_start);
@@ -792,7 +819,8 @@ __global__ __launch_bounds__(TPB) void paged_resolve_kernel(const KPagedParams P
 
 // One workgroup of the ASSEMBLE gather (bx: its index among the gather's workgroups).
 template <int ESZ>
-__device__ __forceinline__ void paged_move_block(const KPagedParams& P, int plane, int32_t bx, KCosSin* lcs) {
+__device__ __forceinline__ void paged_move_block(const KPagedParams& P, const PlanView& V, int plane, int32_t bx,
+                                                 KCosSin* lcs) {
     const KPlane& pl = P.planes[plane];
     const int32_t tb = bx * PAGED_TPB;
     if (int64_t(tb) >= int64_t(P.n_rows) * pl.tpr) return;            // past this plane
@@ -807,7 +835,7 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, int plan
     const char* src;
     int64_t src_step;
     if (e.src_page == KROW_STUB) {
-        const KDirEntry& D = P.dirs[e.dir];
+        const KDirEntry& D = V.dirs[e.dir];
         src_step = D.stub_len * pl.row_bytes;
         src = D.stub[plane] + int64_t(layer0) * src_step + int64_t(e.src_row) * pl.row_bytes;
     } else {
@@ -821,7 +849,7 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, int plan
     if (pl.rot == KROT_NEOX && !pl.neox_lanes) {        // two-chunk units (rare layouts)
         if (active)
             for (int l = 0; l < nl; ++l)
-                move_row_unit<ESZ>(pl, src + l * src_step, dst + l * pl.layer_stride, u, P.cs, cs);
+                move_row_unit<ESZ>(pl, src + l * src_step, dst + l * pl.layer_stride, u, V.cs, cs);
         return;
     }
     const int64_t off = int64_t(u) * 16;
@@ -833,7 +861,7 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, int plan
     }
     // the cos/sin block of the workgroup's first row's shift, staged while the loads are in flight
     const int32_t cs0 = pl.rot != KROT_NONE ? P.rows[fdiv(tb, pl.tpr_div)].cs : -1;
-    if (cs0 >= 0) stage_cs<PAGED_TPB>(lcs, P.cs, cs0 + pl.cs_off, pl.n_pairs);
+    if (cs0 >= 0) stage_cs<PAGED_TPB>(lcs, V.cs, cs0 + pl.cs_off, pl.n_pairs);
     __syncthreads();
     if (!active) return;
     const bool rot = cs >= 0 && pl.rot != KROT_NONE;
@@ -842,7 +870,7 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, int plan
         if (l < nl) {
             if (rot) {
                 if (e.cs == cs0) rotate_chunk<ESZ>(pl, v[l], u, lcs, 0);
-                else rotate_chunk<ESZ>(pl, v[l], u, P.cs, cs);
+                else rotate_chunk<ESZ>(pl, v[l], u, V.cs, cs);
             }
             st16(dst + l * pl.layer_stride + off, v[l]);
         }
@@ -854,7 +882,8 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, int plan
 // of its first page's shift in LDS; rows with another shift (where runs meet) read the table in
 // the workspace.
 template <int ESZ, bool NT>
-__device__ __forceinline__ void paged_remap_block(const KPagedParams& P, int plane, int32_t bx, KCosSin* lcs) {
+__device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const PlanView& V, int plane, int32_t bx,
+                                                  KCosSin* lcs) {
     const KPlane& pl = P.planes[plane];
     const int32_t upp = P.page_size * pl.rot_tpr;
     const int32_t tb = bx * PAGED_TPB;
@@ -875,11 +904,11 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, int pla
     const BandPos bp = band_pos(pl, f - r * pl.rot_tpr);
     u32x4 x[PAGED_LPT], y[PAGED_LPT];
     if (active) band_load<NT>(bp, row, pl.layer_stride, nl, x, y);
-    if (cs0 >= 0) stage_cs<PAGED_TPB>(lcs, P.cs, cs0 + pl.cs_off, pl.n_pairs);
+    if (cs0 >= 0) stage_cs<PAGED_TPB>(lcs, V.cs, cs0 + pl.cs_off, pl.n_pairs);
     __syncthreads();
     if (!active) return;
     if (e.cs == cs0) band_rotate_store<ESZ, NT>(pl, bp, row, pl.layer_stride, nl, x, y, lcs, 0);
-    else band_rotate_store<ESZ, NT>(pl, bp, row, pl.layer_stride, nl, x, y, P.cs, e.cs + pl.cs_off);
+    else band_rotate_store<ESZ, NT>(pl, bp, row, pl.layer_stride, nl, x, y, V.cs, e.cs + pl.cs_off);
 }
 
 // The first workgroups gather ASSEMBLE rows (plane by plane), the rest rotate REMAP pages of the
@@ -888,15 +917,16 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, int pla
 template <int ESZ, bool NT, bool SOLO>
 __global__ __launch_bounds__(PAGED_TPB) void paged_data_kernel(const KPagedParams P) {
     __shared__ KCosSin lcs[KMAX_CS];
+    const PlanView V = plan_view(P);
     int32_t bx = int32_t(blockIdx.x);
     const int32_t moves = SOLO ? P.move_base[1] : P.move_base[P.n_planes];
     if (bx < moves) {
         const int p = SOLO ? 0 : plane_of(P.move_base, P.n_planes, bx);
-        paged_move_block<ESZ>(P, p, bx - P.move_base[p], lcs);
+        paged_move_block<ESZ>(P, V, p, bx - P.move_base[p], lcs);
     } else {
         bx -= moves;
         const int p = SOLO ? 0 : plane_of(P.remap_base, P.n_planes, bx);
-        paged_remap_block<ESZ, NT>(P, p, bx - P.remap_base[p], lcs);
+        paged_remap_block<ESZ, NT>(P, V, p, bx - P.remap_base[p], lcs);
     }
 }
 
@@ -1227,7 +1257,9 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         if (int64_t(t.n_rows) * planes[p].tpr > INT32_MAX - 1024) return LEYLINE_E_INVAL;
         if (int64_t(t.n_remap) * cache->page_size * planes[p].rot_tpr > INT32_MAX - 1024) return LEYLINE_E_INVAL;
     }
-    if (t.upload > 0) {
+    if (t.upload > INT32_MAX) return LEYLINE_E_INVAL;
+    const bool inline_plan = t.upload <= KPLAN_INLINE;
+    if (!inline_plan) {
         rc = hip_status(hipMemcpyAsync(ws, img.bytes.data(), size_t(t.upload), hipMemcpyHostToDevice, s));
         if (rc) return rc;
     }
@@ -1256,17 +1288,20 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
             if (planes[p].rot_tpr > 0) any_band[planes[p].band_nt ? 1 : 0] = true;
         }
         P.capacity = cache->capacity;
-        P.seqs = reinterpret_cast<const KSeqEntry*>(ws + t.off_seq);
-        P.dirs = reinterpret_cast<const KDirEntry*>(ws + t.off_dir);
-        P.cs = reinterpret_cast<const KCosSin*>(ws + t.off_cs);
-        P.asm_runs = reinterpret_cast<const KPageRun*>(ws + t.off_asm_runs);
-        P.remap_runs = reinterpret_cast<const KPageRun*>(ws + t.off_remap_runs);
+        // a plan small enough travels in the kernel arguments; otherwise it was uploaded above
+        P.plan = inline_plan ? nullptr : ws;
+        if (inline_plan) std::memcpy(P.blob, img.bytes.data(), size_t(t.upload));
+        P.off_seq = int32_t(t.off_seq);
+        P.off_dir = int32_t(t.off_dir);
+        P.off_cs = int32_t(t.off_cs);
+        P.off_runs = int32_t(t.off_runs);
+        P.off_asm_runs = int32_t(t.off_asm_runs);
+        P.off_remap_runs = int32_t(t.off_remap_runs);
+        P.off_freed_runs = int32_t(t.off_freed_runs);
         P.n_asm_runs = t.n_asm_runs;
         P.n_remap_runs = t.n_remap_runs;
         P.rows = reinterpret_cast<KRowMove*>(ws + t.off_rows);
         P.remap_pages = reinterpret_cast<KRemapPage*>(ws + t.off_remap_pages);
-        P.runs = reinterpret_cast<const KPageRun*>(ws + t.off_runs);
-        P.freed_runs = reinterpret_cast<const KFreedRun*>(ws + t.off_freed_runs);
         P.bt_out = block_table_out;
         P.freed_out = freed_pages_out;
         P.n_table = int32_t(n_table);

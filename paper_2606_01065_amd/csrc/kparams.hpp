@@ -191,6 +191,9 @@ struct KPagedTables {
     int32_t n_rows;          // n_asm * page_size
 };
 
+// Plans of at most this many bytes travel in the kernel arguments instead of being uploaded.
+constexpr int32_t KPLAN_INLINE = 2560;
+
 struct KPagedParams {
     KPlane planes[LEYLINE_MAX_PLANES];
     int32_t n_planes;
@@ -204,11 +207,10 @@ struct KPagedParams {
     KDiv remap_div[LEYLINE_MAX_PLANES];  // by page_size * rot_tpr (band units per REMAP page)
     KDiv rot_div[LEYLINE_MAX_PLANES];    // by rot_tpr (band units per row)
     int64_t capacity;                    // physical pages
-    const KSeqEntry* seqs;
-    const KDirEntry* dirs;
-    const KCosSin* cs;
-    const KPageRun* asm_runs;            // ASSEMBLE runs, ascending ord0
-    const KPageRun* remap_runs;          // REMAP runs, ascending ord0
+    // plan tables: at `plan` (the workspace copy), or, when plan is null, in `blob` below (a plan
+    // small enough to travel in the kernel arguments); byte offsets within either
+    const char* plan;
+    int32_t off_seq, off_dir, off_cs, off_runs, off_asm_runs, off_remap_runs, off_freed_runs;
     int32_t n_asm_runs, n_remap_runs;
     const int32_t* bt_in;
     const int32_t* free_pages;
@@ -218,8 +220,6 @@ struct KPagedParams {
     KRowMove* rows;          // workspace, n_rows entries
     KRemapPage* remap_pages; // workspace, n_remap entries
     // block tables and freed list (resolve kernel)
-    const KPageRun* runs;    // all runs, ascending (seq, k0)
-    const KFreedRun* freed_runs;
     int32_t* bt_out;
     int32_t* freed_out;
     int32_t n_table;         // n_seqs * bt_stride
@@ -231,6 +231,7 @@ struct KPagedParams {
                                                  // from 0 after the gather's
     int32_t pad1;
     int32_t* order;          // workspace, n_asm fresh ordinals in destination-page order (or null)
+    alignas(16) unsigned char blob[KPLAN_INLINE];
 };
 
 // The gather is ordered by destination page (neighbouring physical pages processed together)

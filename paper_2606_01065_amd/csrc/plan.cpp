@@ -523,25 +523,28 @@ int build_paged_image(const leyline_cache* cache, const PagedPlan& plan, int32_t
     KPagedTables& t = img->tables;
     std::memset(&t, 0, sizeof(t));
     int64_t off = 0;
-    auto place = [&](size_t bytes) {
+    auto place = [&](size_t bytes, int64_t align) {
+        off = (off + align - 1) / align * align;
         const int64_t at = off;
-        off += int64_t((bytes + 255) / 256 * 256);
+        off += int64_t(bytes);
         return at;
     };
-    t.off_seq = place(seqs.size() * sizeof(KSeqEntry));
-    t.off_dir = place(dtab.size() * sizeof(KDirEntry));
-    t.off_cs = place(cs.size() * sizeof(KCosSin));
-    t.off_runs = place(plan.runs.size() * sizeof(KPageRun));
-    t.off_asm_runs = place(asm_runs.size() * sizeof(KPageRun));
-    t.off_remap_runs = place(remap_runs.size() * sizeof(KPageRun));
-    t.off_freed_runs = place(plan.freed.size() * sizeof(KFreedRun));
-    t.upload = off;
+    // the plan tables, packed (16-byte aligned) so that small plans fit in kernel arguments
+    t.off_seq = place(seqs.size() * sizeof(KSeqEntry), 16);
+    t.off_dir = place(dtab.size() * sizeof(KDirEntry), 16);
+    t.off_cs = place(cs.size() * sizeof(KCosSin), 16);
+    t.off_runs = place(plan.runs.size() * sizeof(KPageRun), 16);
+    t.off_asm_runs = place(asm_runs.size() * sizeof(KPageRun), 16);
+    t.off_remap_runs = place(remap_runs.size() * sizeof(KPageRun), 16);
+    t.off_freed_runs = place(plan.freed.size() * sizeof(KFreedRun), 16);
+    t.upload = (off + 15) / 16 * 16;
     const int64_t n_rows = int64_t(plan.n_fresh) * plan.page_size;
     if (n_rows > INT32_MAX) return LEYLINE_E_CAPACITY;
-    t.off_rows = place(size_t(n_rows) * sizeof(KRowMove));
-    t.off_remap_pages = place(size_t(plan.n_remap) * sizeof(KRemapPage));
-    t.off_order = place(plan.n_fresh >= KORDER_MIN ? size_t(plan.n_fresh) * sizeof(int32_t) : 0);
-    t.total = off;
+    // the tables the kernels write
+    t.off_rows = place(size_t(n_rows) * sizeof(KRowMove), 256);
+    t.off_remap_pages = place(size_t(plan.n_remap) * sizeof(KRemapPage), 256);
+    t.off_order = place(plan.n_fresh >= KORDER_MIN ? size_t(plan.n_fresh) * sizeof(int32_t) : 0, 256);
+    t.total = (off + 255) / 256 * 256;
     t.n_seqs = n_seqs; t.n_dirs = n_dirs; t.n_cs = int32_t(cs.size());
     t.n_runs = int32_t(plan.runs.size());
     t.n_asm_runs = int32_t(asm_runs.size());
