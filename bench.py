@@ -166,7 +166,8 @@ def main():
 
     if wl.page_size:
         step, kernel, alg_bytes, moved, launches, keep = setup_paged(wl, dev, L, W, specs, stream)
-        layout = f"paged, {wl.page_size}-token pages, {len(wl.seq_lens)} sequences"
+        layout = (f"paged, {wl.page_size}-token pages, {len(wl.seq_lens)} sequences"
+                  + (", copy-on-write" if wl.paged_flags else ""))
     else:
         step, kernel, alg_bytes, moved, launches, keep = setup_contig(wl, dev, L, W, specs, stream, args)
         layout = "contiguous in place"
@@ -273,17 +274,19 @@ def setup_paged(wl, dev, L, W, specs, stream):
                                    seq=d.seq, stub_len=d.stub_len) for j, d in enumerate(wl.dirs)])
     nd = len(wl.dirs)
     bt_stride = bt.shape[1]
-    new_lens, fresh, n_freed, ws_bytes = L.leyline_paged_query(cache, wl.seq_lens, bt_stride, dirs, nd)
+    fl = wl.paged_flags
+    new_lens, fresh, n_freed, ws_bytes = L.leyline_paged_query(cache, wl.seq_lens, bt_stride, dirs, nd, fl)
     bt_out = torch.empty_like(bt)
     freed = torch.empty(max(1, n_freed), dtype=torch.int32, device=dev)
     ws = torch.empty(max(256, ws_bytes), dtype=torch.uint8, device=dev)
-    kinds, _, _, _ = L.leyline_paged_plan(wl.page_size, wl.seq_lens, dirs, nd, bt_stride, max(1, n_freed))
+    kinds, _, _, _ = L.leyline_paged_plan(wl.page_size, wl.seq_lens, dirs, nd, bt_stride, max(1, n_freed), fl)
     alg_bytes, moved, kernel = paged_bytes(wl, kinds, new_lens, bt_stride, L)
 
     # The paged splice reads old pages and writes fresh ones; re-running it on the same inputs
     # repeats the same work (remapped pages are rotated again, which does not change the bytes).
     def step(i):
-        L.leyline_splice_paged(cache, wl.seq_lens, bt, bt_out, dirs, nd, free, freed, ws, stream=stream)
+        L.leyline_splice_paged(cache, wl.seq_lens, bt, bt_out, dirs, nd, free, freed, ws, stream=stream,
+                               flags=fl)
 
     keep = dict(paged=True)
     torch.cuda.synchronize()
@@ -400,7 +403,8 @@ def summarize(args):
                                        stub_len=d.stub_len, stub=None) for d in wl.dirs])
         new_lens = W.paged_new_lens(wl)
         kinds, _, _, _ = L.leyline_paged_plan(wl.page_size, wl.seq_lens, dirs, len(wl.dirs), bt_stride,
-                                              sum(-(-n // wl.page_size) for n in wl.seq_lens))
+                                              sum(-(-n // wl.page_size) for n in wl.seq_lens),
+                                              wl.paged_flags)
         alg, _, kernel = paged_bytes(wl, kinds, new_lens, bt_stride, L)
     else:
         alg, _ = contig_bytes(wl)

@@ -346,3 +346,26 @@ def test_sizes_beyond_31_bit_indices_are_refused_before_any_enqueue():
     with pytest.raises(L.LeylineError) as e:                 # in-place rotation of paged rows
         L.leyline_rotate_delta(cache, 5, row0=0, n_rows=10, stream=0)
     assert e.value.code == L.E_INVAL
+
+
+@pytest.mark.parametrize("name", ["mla_dsv3_paged_b64", "mla_dsv3_paged_131k", "mla_dsv3_slots_32k",
+                                  "gqa_llama3_8b_slots_16k", "mla_dsv3_slots_cow_32k"])
+def test_paged_plan_matches_oracle_on_benchmark_workloads(name):
+    """The page plans of the benchmarked paged splices (full size, host only) equal the oracle's."""
+    import workloads as W
+    wl = W.WORKLOADS[name]()
+    remap = not (wl.paged_flags & L.PAGED_COPY_ON_WRITE)
+    dirs = [O.Directive(d.span_start, d.span_end, d.stub_len, seq=d.seq) for d in wl.dirs]
+    plans = O.plan_paged(wl.seq_lens, dirs, wl.page_size, remap=remap)
+    bt_stride = W.paged_bt_stride(wl)
+    n_freed = sum(len(p.freed) for p in plans)
+    spec = [(d.span_start, d.span_end, d.stub_len, d.seq) for d in wl.dirs]
+    kinds, srcs, fs, fp = L.leyline_paged_plan(wl.page_size, wl.seq_lens, _dirs(spec), len(spec), bt_stride,
+                                               max(1, n_freed), wl.paged_flags)
+    kinds = np.array(kinds).reshape(len(wl.seq_lens), bt_stride)
+    srcs = np.array(srcs).reshape(len(wl.seq_lens), bt_stride)
+    for b, p in enumerate(plans):
+        k = len(p.kinds)
+        assert list(kinds[b, :k]) == p.kinds
+        assert list(srcs[b, :k]) == p.sources
+    assert fp[:n_freed] == [x for p in plans for x in p.freed]

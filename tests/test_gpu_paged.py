@@ -201,7 +201,9 @@ def _check_sampled(L, wl, seed):
     P = wl.page_size
     odirs = _odirs(wl)
     bt_h, free_h = host(bt), host(free)
-    want_bt, want_lens, want_freed, plans = O.paged_tables(bt_h, wl.seq_lens, odirs, list(free_h), P)
+    cow = bool(wl.paged_flags & L.PAGED_COPY_ON_WRITE)
+    want_bt, want_lens, want_freed, plans = O.paged_tables(bt_h, wl.seq_lens, odirs, list(free_h), P,
+                                                           remap=not cow)
     # sampled outputs and their sources (old rows read before the call)
     samples = []   # (seq, new position, kind, source index, shift)
     for b, n in enumerate(wl.seq_lens):
@@ -220,7 +222,7 @@ def _check_sampled(L, wl, seed):
     for j, d in enumerate(wl.dirs):
         dir_index.setdefault(d.seq, []).append(j)
     print(f"[case] {wl.name}: splicing on the GPU", flush=True)
-    bt_out, freed, new_lens = _run_gpu(L, wl, pools, bt, free, stubs)
+    bt_out, freed, new_lens = _run_gpu(L, wl, pools, bt, free, stubs, flags=wl.paged_flags)
     assert new_lens == want_lens
     assert np.array_equal(host(bt_out), want_bt)
     assert list(host(freed)) == want_freed
@@ -242,6 +244,10 @@ def _check_sampled(L, wl, seed):
                 j = dir_index[b][a]
                 want[:, i] = stubs_h[j][pi].reshape(wl.n_layers, -1, plane.row_elems)[:, c]
         assert_rows_match(got, want, plane, wl.dtype, what=f"{wl.name} plane {pi}")
+        if cow:   # the old rows the samples came from are untouched
+            old_now = host(pools[pi][:, pages_old, offs_old]).reshape(wl.n_layers, len(samples), -1)
+            from_old = [i for i, x in enumerate(samples) if x[2] == "old"]
+            assert np.array_equal(old_now[:, from_old], old[:, from_old])
     return pools, bt, bt_out, new_lens, plans
 
 
@@ -284,6 +290,18 @@ def test_mla_dsv3_paged_131k_full_and_sequential(L):
     del pools
     torch.cuda.empty_cache()
     _check_sampled(L, wl, seed=13)
+
+
+def test_token_slot_copy_on_write_full(L):
+    """The full-size MLA token-slot splice with copy-on-write: every downstream token is rotated
+    into a fresh slot, the prefix keeps its slots, and no old slot is written."""
+    wl = W.mla_dsv3_slots_cow_32k()
+    pools, bt, bt_out, new_lens, plans = _check_sampled(L, wl, seed=19)
+    kinds = [k for p in plans for k in p.kinds]
+    d = wl.dirs[0]
+    assert kinds.count(O.ASSEMBLE) == d.stub_len + wl.seq_lens[0] - d.span_end
+    assert kinds.count(O.REMAP) == 0
+    assert kinds.count(O.IDENTITY) == d.span_start
 
 
 @pytest.mark.parametrize("name", ["mla_dsv3_slots_32k", "gqa_llama3_8b_slots_16k"])

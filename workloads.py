@@ -17,6 +17,11 @@ Workloads (MLA rows: latent c_kv[512] + K_pe[64]; GQA rows: 8 KV heads x 128):
                       delete [4096,6144), 24-token stub
   mla_dsv3_paged_131k 61 layers, 64-token pages, one 131072-token sequence, 8 non-overlapping
                       directives (spans U[256,8192], stubs U[0,64])
+  mla_dsv3_32k_edits8 the 32K MLA cache with 8 seeded edits (spans U[8,200], stubs U[0,2*span])
+  mla_dsv3_slots_32k, gqa_llama3_8b_slots_16k
+                      the 32K MLA and 16K GQA splices on token-slot caches (page size 1)
+  mla_dsv3_slots_cow_32k
+                      the 32K MLA token-slot splice with copy-on-write (fresh slots downstream)
 """
 
 from __future__ import annotations
@@ -64,6 +69,7 @@ class Workload:
     seq_lens: List[int]
     page_size: int = 0            # 0: contiguous
     capacity: int = 0             # contiguous rows per layer
+    paged_flags: int = 0          # paged splice flags (1: copy-on-write, no old page written)
     seed: int = 0
     notes: dict = field(default_factory=dict)
 
@@ -161,6 +167,15 @@ def gqa_llama3_8b_slots_16k() -> Workload:
                     page_size=1, seed=w.seed)
 
 
+def mla_dsv3_slots_cow_32k() -> Workload:
+    """The 32K MLA splice on a token-slot cache with copy-on-write: every downstream token is
+    rotated into a fresh slot and its old slot is left as it was (other holders of those slots,
+    such as a prefix tree, keep reading the original keys)."""
+    w = mla_dsv3_slots_32k()
+    return Workload("mla_dsv3_slots_cow_32k", w.n_layers, w.dtype, w.planes, w.dirs, w.seq_lens,
+                    page_size=1, seed=w.seed, paged_flags=1)
+
+
 WORKLOADS = {
     "mla_1l_4k_f32": mla_1l_4k_f32,
     "mla_dsv3_32k": mla_dsv3_32k,
@@ -170,6 +185,7 @@ WORKLOADS = {
     "mla_dsv3_32k_edits8": mla_dsv3_32k_edits8,
     "mla_dsv3_slots_32k": mla_dsv3_slots_32k,
     "gqa_llama3_8b_slots_16k": gqa_llama3_8b_slots_16k,
+    "mla_dsv3_slots_cow_32k": mla_dsv3_slots_cow_32k,
 }
 
 
