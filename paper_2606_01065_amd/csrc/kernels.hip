@@ -212,14 +212,14 @@ __device__ __forceinline__ Unit map_unit(const KPlane& p, int32_t u) {
 // Re-anchor chunk u of one row in registers with the cos/sin block table[cs + pair] (single-chunk
 // mode: interleaved bands, or half-split bands whose partner chunks sit in the same wavefront and
 // are exchanged between lanes).  Partner lanes belong to the same row and take the same path.
-template <int ESZ>
+template <int ESZ, int ROT = KROT_NONE>
 __device__ __forceinline__ void rotate_chunk(const KPlane& pl, u32x4& v, int32_t u, const KCosSin* table,
                                              int32_t cs) {
     constexpr int EPC = Elt<ESZ>::EPC;
     const int32_t h = fdiv(u, pl.head_div);
     const int32_t j = u - h * pl.head_chunks - pl.rot_lo;
     if (h < pl.n_heads && j >= 0 && j < pl.rot_chunks) {
-        if (pl.rot == KROT_INTERLEAVED) {
+        if (ROT == KROT_INTERLEAVED || (ROT == KROT_NONE && pl.rot == KROT_INTERLEAVED)) {
             rot_interleaved<ESZ>(v, table, cs + j * (EPC / 2));
         } else {
             const int32_t half = pl.rot_chunks >> 1;
@@ -498,15 +498,18 @@ __global__ __launch_bounds__(TPB) void contig_chain_kernel(const KContigParams P
 
 // Ordered tiles: moves by a shift too small for rounds.  The moved range is cut into tiles of
 // KTILE_CHUNKS chunks (counted from the first source row), one workgroup and one layer each.
-// Workgroups take tickets in the order they start; ticket t is tile t / n_layers of the item's
+// Workgroups take tickets in the order they start; ticket t is tile t mod n_tiles of the item's
 // processing order (ascending tiles for a left shift, descending for a right one) in layer
-// t mod n_layers.  A tile loads its whole source into registers, waits until those loads have
+// t / n_tiles, so that workgroups running together cover one stretch of one layer (measured:
+// interleaving the layers instead costs several points of bandwidth).  A tile loads its whole source into registers, waits until those loads have
 // returned and publishes "source read"; it then waits until each earlier tile whose source its
 // destination overlaps (at most two: the shift is M chunks, so those are the tiles floor(M/C)
 // and ceil(M/C) places earlier) has published the same, and only then stores.  No tile reads a
 // chunk another tile has written.  A tile waits only for tickets taken before its own, so every
 // wait ends.
-template <int ESZ>
+// ROT: the rotary style of every re-anchored item of the launch (KROT_NONE: looked up per item),
+// so that the style this launch does not use costs no registers.
+template <int ESZ, int ROT>
 __global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KContigParams P) {
     __shared__ KCosSin lcs[KMAX_CS];
     __shared__ int32_t s_ticket;
@@ -519,7 +522,7 @@ __global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KContigPar
     const KItem& I = P.items[it];
     const KPlane& pl = I.pl;
     const int32_t local = ticket - I.ticket0;
-    const int32_t order = local / P.n_layers, layer = local - order * P.n_layers;
+    const int32_t layer = local / I.n_tiles, order = local - layer * I.n_tiles;
     const bool down = I.delta < 0;
     const int32_t q = down ? order : I.n_tiles - 1 - order;
     const int32_t total = int32_t(I.count) * pl.tpr;
@@ -547,7 +550,7 @@ __global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KContigPar
         for (int64_t d = M / KTILE_CHUNKS; d <= (M + KTILE_CHUNKS - 1) / KTILE_CHUNKS; ++d) {
             const int64_t j = order - d;
             if (d == 0 || j < 0) continue;
-            const int32_t* f = flags + j * P.n_layers + layer;
+            const int32_t* f = flags + int64_t(layer) * I.n_tiles + j;
             while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0)
                 __builtin_amdgcn_s_sleep(1);
         }
@@ -559,10 +562,22 @@ __global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KContigPar
         const int32_t g = g0 + i * KTILE_TPB;
         if (g < total) {
             const int32_t r = fdiv(g, pl.tpr_div), u = g - r * pl.tpr;
-            if (I.cs >= 0) rotate_chunk<ESZ>(pl, v[i], u, lcs, 0);
+            if (I.cs >= 0) rotate_chunk<ESZ, ROT>(pl, v[i], u, lcs, 0);
             st16(dst + int64_t(r) * pl.token_stride + int64_t(u) * 16, v[i]);
         }
     }
+}
+
+// The rotary style shared by every re-anchored item of a contiguous launch, or KROT_NONE when
+// items of both styles (or none) are re-anchored.
+static int32_t launch_rot_style(const KContigParams& P) {
+    int32_t style = KROT_NONE;
+    for (int32_t i = 0; i < P.n_items; ++i) {
+        if (P.items[i].cs < 0 || P.items[i].pl.rot == KROT_NONE) continue;
+        if (style != KROT_NONE && style != P.items[i].pl.rot) return KROT_NONE;
+        style = P.items[i].pl.rot;
+    }
+    return style;
 }
 
 // Zeroes n 32-bit words (ticket counters and flags of the call's ordered-tile moves).
@@ -1057,8 +1072,21 @@ extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len
                 P.n_tickets = int32_t(tickets);
                 P.tile_flags = reinterpret_cast<int32_t*>(ws);
                 const dim3 grid(static_cast<unsigned>(tickets), 1, 1);
-                const int r = cache->dtype == LEYLINE_BF16 ? launch(contig_tile_kernel<2>, grid, s, P, KTILE_TPB)
-                                                           : launch(contig_tile_kernel<4>, grid, s, P, KTILE_TPB);
+                const bool bf = cache->dtype == LEYLINE_BF16;
+                int r;
+                switch (launch_rot_style(P)) {
+                case KROT_INTERLEAVED:
+                    r = bf ? launch(contig_tile_kernel<2, KROT_INTERLEAVED>, grid, s, P, KTILE_TPB)
+                           : launch(contig_tile_kernel<4, KROT_INTERLEAVED>, grid, s, P, KTILE_TPB);
+                    break;
+                case KROT_NEOX:
+                    r = bf ? launch(contig_tile_kernel<2, KROT_NEOX>, grid, s, P, KTILE_TPB)
+                           : launch(contig_tile_kernel<4, KROT_NEOX>, grid, s, P, KTILE_TPB);
+                    break;
+                default:
+                    r = bf ? launch(contig_tile_kernel<2, KROT_NONE>, grid, s, P, KTILE_TPB)
+                           : launch(contig_tile_kernel<4, KROT_NONE>, grid, s, P, KTILE_TPB);
+                }
                 std::memset(&P, 0, sizeof(P));
                 cs.clear();
                 tickets = 0;

@@ -95,7 +95,7 @@ struct KItem {
     int32_t n_tiles;         // tile: tiles of KTILE_CHUNKS chunks over the moved range, per layer
     int32_t ticket0;         // tile: first ticket of this item in the launch
     int32_t flag0;           // tile: first of the item's flags (int32 words from tile_flags), one
-                             // per (tile in processing order, layer)
+                             // per (layer, tile in processing order), at layer * n_tiles + tile
     int32_t pad;
 };
 
