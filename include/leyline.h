@@ -152,8 +152,8 @@ const char* leyline_last_hip_error(void);
 /*
  * Host-only check of a contiguous splice: validates exactly as leyline_splice_contig does and
  * reports (host outputs, each nullable) the new length, the number of kernel launches the splice
- * will enqueue, how many of them are ordered-tile moves, and the device workspace it needs in
- * bytes (0 when no move is done in ordered tiles).  Enqueues nothing.
+ * will enqueue, how many of them are ordered-tile launches, and the device workspace it needs in
+ * bytes (0 when the splice runs without ordered tiles).  Enqueues nothing.
  */
 int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
                          const leyline_directive* dirs, int32_t n_dirs,
@@ -169,15 +169,19 @@ int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
  * prefix rows untouched, each stub at its new position, each downstream row at its old position
  * plus the running shift with its rotary bands rotated by that shift.  Rows [new_len, max(seq_len,
  * new_len)) are left unspecified.  Source and destination ranges overlap; the library orders the
- * moves so that every row is read before it is overwritten.  A segment whose shift is small
- * against its length is moved in ordered tiles that coordinate through the workspace.
+ * moves so that every row is read before it is overwritten.  When every shift is large against
+ * its segment the moves run as rounds (independent launches); otherwise the whole call (moves and
+ * stub copies of every directive) runs as ordered tiles, normally in a single launch, whose
+ * workgroups coordinate through counters and flags in the workspace.
  *
  * workspace: device memory, 256-byte aligned, at least the size leyline_contig_query reports
- * (NULL allowed when that size is 0).  The call clears it on `stream` before use; reuse it only
- * after the stream has passed this call, and do not share one workspace between calls that may
- * run at the same time.
- * Enqueues kernels only (all parameters travel as kernel arguments; the workspace is cleared by a
- * kernel), so the call may be captured into a HIP graph; each replay repeats the same splice.
+ * (NULL allowed when that size is 0); it holds the tiles' ticket counters and flags and the
+ * call's cos/sin table.  The call writes it on `stream` before use; reuse it only after the
+ * stream has passed this call, and do not share one workspace between calls that may run at the
+ * same time.
+ * Enqueues kernels only (all parameters travel as kernel arguments; the workspace is cleared and
+ * filled by a kernel), so the call may be captured into a HIP graph; each replay repeats the same
+ * splice.
  * Errors: E_INVAL, E_RANGE, E_ORDER, E_OVERLAP, E_CAPACITY (new length > capacity), E_MODE,
  * E_WORKSPACE (missing, misaligned or too small), E_HIP.
  */

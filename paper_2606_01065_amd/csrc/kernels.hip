@@ -496,38 +496,46 @@ __global__ __launch_bounds__(TPB) void contig_chain_kernel(const KContigParams P
     }
 }
 
-// Ordered tiles: moves by a shift too small for rounds.  The moved range is cut into tiles of
-// KTILE_CHUNKS chunks (counted from the first source row), one workgroup and one layer each.
-// Workgroups take tickets in the order they start; ticket t is tile t mod n_tiles of the item's
-// processing order (ascending tiles for a left shift, descending for a right one) in layer
-// t / n_tiles, so that workgroups running together cover one stretch of one layer (measured:
-// interleaving the layers instead costs several points of bandwidth).  A tile loads its whole source into registers, waits until those loads have
-// returned and publishes "source read"; it then waits until each earlier tile whose source its
-// destination overlaps (at most two: the shift is M chunks, so those are the tiles floor(M/C)
-// and ceil(M/C) places earlier) has published the same, and only then stores.  No tile reads a
-// chunk another tile has written.  A tile waits only for tickets taken before its own, so every
-// wait ends.
+// Ordered tiles: every job of a call whose moves are too short-shifted for rounds.  Each
+// (job, plane) item is cut into tiles of KTILE_CHUNKS chunks (counted from its first row), one
+// workgroup and one layer each.  Workgroups take tickets in the order they start; the items of a
+// launch own consecutive ticket ranges in dependency order, and within an item ticket t is tile
+// t mod n_tiles of its processing order (a left shift ascending, a right shift descending) in
+// layer t / n_tiles, so that workgroups running together cover one stretch of one layer
+// (interleaving the layers costs several points of bandwidth).
+//
+// A tile loads its whole source into registers, waits until those loads have returned and (a
+// move) publishes "source read".  Before storing it waits for every tile whose source rows its
+// destination overlaps (tile_wait_flags), so no tile reads a chunk another tile has written.  A tile waits only
+// for tickets taken before its own, by workgroups that publish before they wait, so every wait
+// ends.
+//
 // ROT: the rotary style of every re-anchored item of the launch (KROT_NONE: looked up per item),
 // so that the style this launch does not use costs no registers.
+__device__ __forceinline__ void wait_flag(const int32_t* f) {
+    while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) __builtin_amdgcn_s_sleep(1);
+}
+
 template <int ESZ, int ROT>
-__global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KContigParams P) {
+__global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KTileParams P) {
     __shared__ KCosSin lcs[KMAX_CS];
     __shared__ int32_t s_ticket;
-    if (threadIdx.x == 0) s_ticket = atomicAdd(P.tile_counter, 1);
+    if (threadIdx.x == 0) s_ticket = atomicAdd(P.counter, 1);
     __syncthreads();
     const int32_t ticket = s_ticket;
     if (ticket >= P.n_tickets) return;                            // block-uniform
     int it = 0;
     while (it + 1 < P.n_items && ticket >= P.items[it + 1].ticket0) ++it;
-    const KItem& I = P.items[it];
-    const KPlane& pl = I.pl;
+    const KTileItem& I = P.items[it];
+    const KPlane& pl = P.planes[I.plane];
+    const bool move = I.kind == KJOB_TILE;
     const int32_t local = ticket - I.ticket0;
     const int32_t layer = local / I.n_tiles, order = local - layer * I.n_tiles;
-    const bool down = I.delta < 0;
-    const int32_t q = down ? order : I.n_tiles - 1 - order;
+    const int32_t q = I.delta <= 0 ? order : I.n_tiles - 1 - order;
     const int32_t total = int32_t(I.count) * pl.tpr;
-    const char* src = pl.base + int64_t(layer) * pl.layer_stride + I.src0 * pl.token_stride;
-    const int64_t dshift = I.delta * pl.token_stride;
+    char* lbase = pl.base + int64_t(layer) * pl.layer_stride;
+    const char* src = move ? lbase + I.src0 * pl.token_stride : I.stub + int64_t(layer) * I.count * pl.row_bytes;
+    const int64_t src_step = move ? pl.token_stride : pl.row_bytes;
     // Every slot loads (past the end of the range: the range's last chunk, which stays unused),
     // so that all loads are issued back to back without branches between them.  Row and column
     // are recomputed at store time rather than kept in registers.
@@ -537,26 +545,18 @@ __global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KContigPar
     for (int i = 0; i < KTILE_CPT; ++i) {
         const int32_t gc = min(g0 + i * KTILE_TPB, total - 1);
         const int32_t r = fdiv(gc, pl.tpr_div);
-        v[i] = ld16(src + int64_t(r) * pl.token_stride + int64_t(gc - r * pl.tpr) * 16);
+        v[i] = ld16(src + int64_t(r) * src_step + int64_t(gc - r * pl.tpr) * 16);
     }
     if (I.cs >= 0) stage_cs<KTILE_TPB>(lcs, P.cs, I.cs, pl.n_pairs);
     __builtin_amdgcn_s_waitcnt(0);          // this thread's loads have returned
     __syncthreads();                        // ... and every thread's
     if (threadIdx.x == 0) {
-        int32_t* flags = P.tile_flags + I.flag0;                 // this item's flags, by local ticket
-        __hip_atomic_store(flags + local, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        // earlier tiles whose source this tile's destination overlaps: processing order minus d
-        const int64_t M = (down ? -I.delta : I.delta) * pl.tpr;  // shift in chunks
-        for (int64_t d = M / KTILE_CHUNKS; d <= (M + KTILE_CHUNKS - 1) / KTILE_CHUNKS; ++d) {
-            const int64_t j = order - d;
-            if (d == 0 || j < 0) continue;
-            const int32_t* f = flags + int64_t(layer) * I.n_tiles + j;
-            while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0)
-                __builtin_amdgcn_s_sleep(1);
-        }
+        if (move)
+            __hip_atomic_store(P.flags + I.flag0 + local, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        tile_wait_flags(P, it, layer, order, [&](int64_t f) { wait_flag(P.flags + f); });
     }
     __syncthreads();
-    char* dst = const_cast<char*>(src) + dshift;
+    char* dst = lbase + I.dst0 * pl.token_stride;
 #pragma unroll
     for (int i = 0; i < KTILE_CPT; ++i) {
         const int32_t g = g0 + i * KTILE_TPB;
@@ -568,25 +568,25 @@ __global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KContigPar
     }
 }
 
-// The rotary style shared by every re-anchored item of a contiguous launch, or KROT_NONE when
-// items of both styles (or none) are re-anchored.
-static int32_t launch_rot_style(const KContigParams& P) {
+// The rotary style shared by every re-anchored item of a tile launch, or KROT_NONE when items of
+// both styles (or none) are re-anchored.
+static int32_t launch_rot_style(const KTileParams& P) {
     int32_t style = KROT_NONE;
     for (int32_t i = 0; i < P.n_items; ++i) {
-        if (P.items[i].cs < 0 || P.items[i].pl.rot == KROT_NONE) continue;
-        if (style != KROT_NONE && style != P.items[i].pl.rot) return KROT_NONE;
-        style = P.items[i].pl.rot;
+        const int32_t rot = P.planes[P.items[i].plane].rot;
+        if (P.items[i].cs < 0 || rot == KROT_NONE) continue;
+        if (style != KROT_NONE && style != rot) return KROT_NONE;
+        style = rot;
     }
     return style;
 }
 
-// Zeroes n 32-bit words (ticket counters and flags of the call's ordered-tile moves).
-struct KZeroParams {
-    int32_t* p;
-    int64_t n;
-};
-__global__ __launch_bounds__(TPB) void zero_words_kernel(const KZeroParams Z) {
-    for (int64_t i = int64_t(blockIdx.x) * TPB + threadIdx.x; i < Z.n; i += int64_t(gridDim.x) * TPB) Z.p[i] = 0;
+// Clears n_zero 32-bit words (the tile launches' ticket counters and flags) and writes n_cs
+// entries of the call's cos/sin table from the kernel arguments into the workspace.
+__global__ __launch_bounds__(TPB) void tile_prep_kernel(const KPrepParams Q) {
+    const int64_t stride = int64_t(gridDim.x) * TPB;
+    for (int64_t i = int64_t(blockIdx.x) * TPB + threadIdx.x; i < Q.n_zero; i += stride) Q.zero[i] = 0;
+    for (int64_t i = int64_t(blockIdx.x) * TPB + threadIdx.x; i < Q.n_cs; i += stride) Q.cs_dst[i] = Q.cs[i];
 }
 
 // ------------------------------------------------------------------------ rotate in place ---
@@ -978,17 +978,22 @@ extern "C" const char* leyline_last_hip_error(void) {
     return hipGetErrorString(g_last_hip_error);
 }
 
-// Launches of one contiguous splice: per group of independent jobs, one launch per job kind
-// present, split further when a launch would exceed its item or cos/sin capacity.
-// Kernel launches of a schedule (only those of one job kind when only_kind >= 0), grouped the way
-// leyline_splice_contig groups them.
+// Kernel launches of a schedule (only the ordered-tile launches when tiles_only): with tiles, the
+// prep launches and the tile launches; otherwise, per group of independent jobs, one launch per
+// job kind present, split further when a launch would exceed its item or cos/sin capacity.
 static int contig_launch_count(const leyline_cache* cache, const ContigSchedule& sched, int n_planes,
-                               int only_kind = -1) {
+                               bool tiles_only = false) {
+    if (sched.tiles) {
+        const int tile = int(sched.tile_launches.size());
+        if (tiles_only) return tile;
+        const int prep = std::max<int>(1, int((sched.cs.size() + KPREP_CS - 1) / KPREP_CS));
+        return prep + tile;
+    }
+    if (tiles_only) return 0;
     const int32_t cs_need = cos_sin_per_shift(cache);
-    int n = (sched.ws_bytes > 0 && only_kind < 0) ? 1 : 0;      // clearing the tile workspace
+    int n = 0;
     for (const auto& group : sched.launches)
-        for (int kind : {int(KJOB_TILE), int(KJOB_STUB), int(KJOB_CHAIN), int(KJOB_ROUND)}) {
-            if (only_kind >= 0 && kind != only_kind) continue;
+        for (int kind : {int(KJOB_STUB), int(KJOB_CHAIN), int(KJOB_ROUND)}) {
             int items = 0, cs = 0;
             bool open = false;
             for (const ContigJobHost& j : group) {
@@ -1007,6 +1012,60 @@ static int contig_launch_count(const leyline_cache* cache, const ContigSchedule&
     return n;
 }
 
+// The prep launches and ordered-tile launches of a tile schedule.
+static int launch_tiles(const leyline_cache* cache, const ContigSchedule& sched, const KPlane* planes,
+                        int n_planes, char* ws, hipStream_t s) {
+    // prep: clear the counters and flags, then write the cos/sin table in pieces that fit the
+    // kernel arguments
+    const int64_t words = sched.ws_cs / 4;
+    size_t c = 0;
+    do {
+        KPrepParams Q;
+        std::memset(&Q, 0, sizeof(Q));
+        Q.zero = c == 0 ? reinterpret_cast<int32_t*>(ws) : nullptr;
+        Q.n_zero = c == 0 ? words : 0;
+        const size_t n = std::min<size_t>(sched.cs.size() - c, size_t(KPREP_CS));
+        Q.cs_dst = reinterpret_cast<KCosSin*>(ws + sched.ws_cs) + c;
+        Q.n_cs = int32_t(n);
+        std::copy(sched.cs.begin() + int64_t(c), sched.cs.begin() + int64_t(c + n), Q.cs);
+        const int64_t work = std::max<int64_t>(Q.n_zero, Q.n_cs);
+        const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((work + TPB - 1) / TPB, 1024));
+        const int rc = launch(tile_prep_kernel, dim3(unsigned(blocks)), s, Q);
+        if (rc) return rc;
+        c += n;
+    } while (c < sched.cs.size());
+    const bool bf = cache->dtype == LEYLINE_BF16;
+    for (size_t k = 0; k < sched.tile_launches.size(); ++k) {
+        const TileLaunchHost& tl = sched.tile_launches[k];
+        KTileParams P;
+        std::memset(&P, 0, sizeof(P));
+        std::memcpy(P.planes, planes, sizeof(KPlane) * size_t(n_planes));
+        std::copy(tl.items.begin(), tl.items.end(), P.items);
+        P.n_items = int32_t(tl.items.size());
+        P.n_tickets = int32_t(tl.tickets);
+        P.counter = reinterpret_cast<int32_t*>(ws + 256 * int64_t(k));
+        P.flags = reinterpret_cast<int32_t*>(ws + sched.ws_flags);
+        P.cs = reinterpret_cast<const KCosSin*>(ws + sched.ws_cs);
+        const dim3 grid(static_cast<unsigned>(tl.tickets), 1, 1);
+        int r;
+        switch (launch_rot_style(P)) {
+        case KROT_INTERLEAVED:
+            r = bf ? launch(contig_tile_kernel<2, KROT_INTERLEAVED>, grid, s, P, KTILE_TPB)
+                   : launch(contig_tile_kernel<4, KROT_INTERLEAVED>, grid, s, P, KTILE_TPB);
+            break;
+        case KROT_NEOX:
+            r = bf ? launch(contig_tile_kernel<2, KROT_NEOX>, grid, s, P, KTILE_TPB)
+                   : launch(contig_tile_kernel<4, KROT_NEOX>, grid, s, P, KTILE_TPB);
+            break;
+        default:
+            r = bf ? launch(contig_tile_kernel<2, KROT_NONE>, grid, s, P, KTILE_TPB)
+                   : launch(contig_tile_kernel<4, KROT_NONE>, grid, s, P, KTILE_TPB);
+        }
+        if (r) return r;
+    }
+    return LEYLINE_OK;
+}
+
 extern "C" int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
                                     const leyline_directive* dirs, int32_t n_dirs,
                                     int64_t* new_len_out, int32_t* n_launches_out,
@@ -1016,7 +1075,7 @@ extern "C" int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
     if (rc) return rc;
     if (new_len_out) *new_len_out = sched.new_len;
     if (n_launches_out) *n_launches_out = contig_launch_count(cache, sched, cache->n_planes);
-    if (n_tile_launches_out) *n_tile_launches_out = contig_launch_count(cache, sched, cache->n_planes, KJOB_TILE);
+    if (n_tile_launches_out) *n_tile_launches_out = contig_launch_count(cache, sched, cache->n_planes, true);
     if (workspace_bytes_out) *workspace_bytes_out = sched.ws_bytes;
     return LEYLINE_OK;
 }
@@ -1035,92 +1094,25 @@ extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len
     int n_planes = 0;
     rc = describe_cache(cache, false, planes, &n_planes);
     if (rc) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* ws = static_cast<char*>(workspace);
+    if (sched.tiles) {
+        rc = launch_tiles(cache, sched, planes, n_planes, ws, s);
+        if (rc) return rc;
+        if (new_len_out) *new_len_out = sched.new_len;
+        return LEYLINE_OK;
+    }
     // threads of one (job, plane) item; every count must fit a 31-bit index
     auto item_threads = [&](const ContigJobHost& j, int p) -> int64_t {
         if (j.kind == KJOB_CHAIN) return std::min<int64_t>(j.count, abs64(j.delta)) * planes[p].units_all;
-        if (j.kind == KJOB_TILE) return j.count * planes[p].tpr;
         return (j.count + CRPT - 1) / CRPT * planes[p].tpr;
     };
     for (const auto& jobs : sched.launches)
         for (const auto& j : jobs)
             for (int p = 0; p < n_planes; ++p)
-                if (item_threads(j, p) > INT32_MAX - std::max(TPB, KTILE_CHUNKS)) return LEYLINE_E_INVAL;
+                if (item_threads(j, p) > INT32_MAX - TPB) return LEYLINE_E_INVAL;
     const int32_t cs_need = cos_sin_per_shift(cache);
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    char* ws = static_cast<char*>(workspace);
-    if (sched.ws_bytes > 0) {
-        const int64_t words = sched.ws_bytes / 4;
-        const int64_t blocks = std::min<int64_t>((words + TPB - 1) / TPB, 1024);
-        rc = launch(zero_words_kernel, dim3(unsigned(blocks)), s, KZeroParams{reinterpret_cast<int32_t*>(ws), words});
-        if (rc) return rc;
-    }
     for (const auto& group : sched.launches) {
-        // Ordered-tile moves of this group (independent of each other): batched into launches of
-        // up to KMAX_LAUNCH_ITEMS (job, plane) items within the cos/sin table.  A launch counts
-        // tickets on the counter of its first job's workspace region; each item's flags sit in its
-        // own job's region.
-        {
-            KContigParams P;
-            std::memset(&P, 0, sizeof(P));
-            std::vector<KCosSin> cs;
-            int64_t tickets = 0;
-            auto flush_tiles = [&]() -> int {
-                if (P.n_items == 0) return LEYLINE_OK;
-                if (tickets > INT32_MAX - 1024 || cs.size() > size_t(KMAX_CS)) return LEYLINE_E_INVAL;
-                std::copy(cs.begin(), cs.end(), P.cs);
-                P.n_layers = cache->n_layers;
-                P.n_tickets = int32_t(tickets);
-                P.tile_flags = reinterpret_cast<int32_t*>(ws);
-                const dim3 grid(static_cast<unsigned>(tickets), 1, 1);
-                const bool bf = cache->dtype == LEYLINE_BF16;
-                int r;
-                switch (launch_rot_style(P)) {
-                case KROT_INTERLEAVED:
-                    r = bf ? launch(contig_tile_kernel<2, KROT_INTERLEAVED>, grid, s, P, KTILE_TPB)
-                           : launch(contig_tile_kernel<4, KROT_INTERLEAVED>, grid, s, P, KTILE_TPB);
-                    break;
-                case KROT_NEOX:
-                    r = bf ? launch(contig_tile_kernel<2, KROT_NEOX>, grid, s, P, KTILE_TPB)
-                           : launch(contig_tile_kernel<4, KROT_NEOX>, grid, s, P, KTILE_TPB);
-                    break;
-                default:
-                    r = bf ? launch(contig_tile_kernel<2, KROT_NONE>, grid, s, P, KTILE_TPB)
-                           : launch(contig_tile_kernel<4, KROT_NONE>, grid, s, P, KTILE_TPB);
-                }
-                std::memset(&P, 0, sizeof(P));
-                cs.clear();
-                tickets = 0;
-                return r;
-            };
-            for (const ContigJobHost& j : group) {
-                if (j.kind != KJOB_TILE) continue;
-                if (P.n_items + n_planes > KMAX_LAUNCH_ITEMS || int32_t(cs.size()) + cs_need > KMAX_CS) {
-                    rc = flush_tiles();
-                    if (rc) return rc;
-                }
-                if (P.n_items == 0) P.tile_counter = reinterpret_cast<int32_t*>(ws + j.ws_off);
-                const int32_t cs0 = cs_need > 0 ? append_cos_sin(cache, j.delta, cs) : -1;
-                int64_t flag = j.ws_off / 4 + KTILE_FLAGS_OFF;
-                for (int p = 0; p < n_planes; ++p) {
-                    KItem& it = P.items[P.n_items++];
-                    std::memset(&it, 0, sizeof(it));
-                    it.pl = planes[p];
-                    it.src0 = j.src0;
-                    it.count = j.count;
-                    it.delta = j.delta;
-                    it.kind = KJOB_TILE;
-                    it.cs = (cs0 >= 0 && planes[p].rot != KROT_NONE) ? cs0 + planes[p].cs_off : -1;
-                    it.n_tiles = int32_t(tile_count(j.count, planes[p].tpr));
-                    it.ticket0 = int32_t(tickets);
-                    it.flag0 = int32_t(flag);
-                    const int64_t n = int64_t(cache->n_layers) * it.n_tiles;
-                    tickets += n;
-                    flag += n;
-                }
-            }
-            rc = flush_tiles();
-            if (rc) return rc;
-        }
         // the jobs of a group are independent; replacement copies, chains and rounds go to
         // separate launches, each a list of (job, plane) items selected by blockIdx.z
         for (int kind : {int(KJOB_STUB), int(KJOB_CHAIN), int(KJOB_ROUND)}) {

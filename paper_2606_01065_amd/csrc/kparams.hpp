@@ -7,6 +7,13 @@
 
 #include "leyline.h"
 
+// Functions used by both the kernels and host-side checks of their schedules.
+#if defined(__HIPCC__)
+#define LEYLINE_HD __host__ __device__
+#else
+#define LEYLINE_HD
+#endif
+
 namespace leyline {
 
 // Rows are moved as 16-byte vectors ("chunks").  In the row kernels one thread moves one chunk
@@ -65,23 +72,12 @@ enum : int32_t {
     KJOB_CHAIN = 1,   // rows [src0, src0+count) move by delta, count > |delta|: ordered chains
                       // (layouts whose half-split partners need two-chunk units)
     KJOB_STUB = 2,    // count replacement rows copied to [dst0, dst0+count)
-    KJOB_TILE = 3     // rows [src0, src0+count) move by delta, count > |delta|: ordered tiles
+    KJOB_TILE = 3     // rows [src0, src0+count) move by delta as ordered tiles
 };
 
-// Ordered-tile moves: chunks per thread and per tile (one tile = one workgroup, one layer).
-#ifndef LEYLINE_TILE_CPT
-#define LEYLINE_TILE_CPT 8
-#endif
-#ifndef LEYLINE_TILE_TPB
-#define LEYLINE_TILE_TPB 1024
-#endif
-constexpr int KTILE_CPT = LEYLINE_TILE_CPT;
-constexpr int KTILE_TPB = LEYLINE_TILE_TPB;
-constexpr int KTILE_CHUNKS = KTILE_TPB * KTILE_CPT;
-constexpr int KTILE_FLAGS_OFF = 64;   // int32 words: the ticket counter, then the flags
-
-// One (job, plane) item of a contiguous launch, self-contained so that a workgroup reads its
-// parameters with one level of independent scalar loads (blockIdx.z selects the item).
+// One (job, plane) item of a round, chain or replacement launch, self-contained so that a
+// workgroup reads its parameters with one level of independent scalar loads (blockIdx.z selects
+// the item).
 struct KItem {
     KPlane pl;
     const char* stub;        // KJOB_STUB: dense [layers][count][row] for this plane
@@ -92,10 +88,6 @@ struct KItem {
     int32_t kind;            // KJOB_*
     int32_t chains;          // chain: min(|delta|, count)
     int32_t cs;              // first cos/sin entry of this plane's pairs (-1: no rotation)
-    int32_t n_tiles;         // tile: tiles of KTILE_CHUNKS chunks over the moved range, per layer
-    int32_t ticket0;         // tile: first ticket of this item in the launch
-    int32_t flag0;           // tile: first of the item's flags (int32 words from tile_flags), one
-                             // per (layer, tile in processing order), at layer * n_tiles + tile
     int32_t pad;
 };
 
@@ -105,11 +97,107 @@ struct KContigParams {
     KItem items[KMAX_LAUNCH_ITEMS];
     int32_t n_items;
     int32_t n_layers;
-    int32_t* tile_counter;   // tile launches: ticket counter, zero before the launch
-    int32_t* tile_flags;     // tile launches: base of the items' "source read" flags, zero before
-    int32_t n_tickets;
-    int32_t pad;
     KCosSin cs[KMAX_CS];
+};
+
+// Ordered tiles: chunks per thread and per tile (one tile = one workgroup, one layer).
+#ifndef LEYLINE_TILE_CPT
+#define LEYLINE_TILE_CPT 8
+#endif
+#ifndef LEYLINE_TILE_TPB
+#define LEYLINE_TILE_TPB 1024
+#endif
+constexpr int KTILE_CPT = LEYLINE_TILE_CPT;
+constexpr int KTILE_TPB = LEYLINE_TILE_TPB;
+constexpr int KTILE_CHUNKS = KTILE_TPB * KTILE_CPT;
+
+// One (job, plane) item of an ordered-tile launch: a move (rows [src0, src0 + count) to
+// [dst0, dst0 + count), dst0 = src0 + delta) or a replacement copy (rows of `stub` to
+// [dst0, dst0 + count)), cut into n_tiles tiles per layer.
+struct KTileItem {
+    int64_t src0;
+    int64_t dst0;
+    int64_t count;
+    int64_t delta;           // move: nonzero shift; replacement: 0
+    const char* stub;        // replacement: dense [layers][count][row] of this plane
+    int32_t kind;            // KJOB_TILE (move) or KJOB_STUB
+    int32_t plane;
+    int32_t cs;              // first entry of the call's cos/sin table for this plane (-1: none)
+    int32_t n_tiles;         // tiles per layer
+    int32_t ticket0;         // first ticket of the item in its launch
+    int32_t flag0;           // move: first "source read" flag, one per (layer, tile in
+                             // processing order) at layer * n_tiles + tile; replacement: -1
+    uint32_t waits;          // bit a: item a of the launch, an earlier move of the same plane,
+                             // reads rows this item writes
+    int32_t pad;
+};
+
+constexpr int KTILE_MAX_ITEMS = 24;
+
+struct KTileParams {
+    KPlane planes[LEYLINE_MAX_PLANES];
+    KTileItem items[KTILE_MAX_ITEMS];
+    int32_t n_items;
+    int32_t n_tickets;
+    int32_t* counter;        // ticket counter of this launch, zero before it
+    int32_t* flags;          // the call's flags, zero before the first tile launch
+    const KCosSin* cs;       // the call's cos/sin table
+};
+
+LEYLINE_HD inline int64_t kmin64(int64_t a, int64_t b) { return a < b ? a : b; }
+LEYLINE_HD inline int64_t kmax64(int64_t a, int64_t b) { return a > b ? a : b; }
+
+// The flags that tile `order` (processing order) of item `it` of a tile launch, in `layer`, waits
+// for before it stores: f(i) for the flag word i of the call's flags, once per overlapping tile
+// (possibly for one flag more than once).  A move's tile waits for the earlier tiles of its own
+// move whose source its destination overlaps: the shift is M chunks, so the tiles floor(M/C) and
+// ceil(M/C) places earlier in processing order.  Any tile then waits for the tiles of the earlier
+// moves listed in its item's `waits` whose source rows overlap its destination rows.
+template <class F>
+LEYLINE_HD inline void tile_wait_flags(const KTileParams& P, int32_t it, int32_t layer, int32_t order, F&& f) {
+    const KTileItem& I = P.items[it];
+    const int64_t tpr = P.planes[I.plane].tpr;
+    const bool down = I.delta <= 0;
+    const int64_t q = down ? order : I.n_tiles - 1 - order;
+    if (I.kind == KJOB_TILE) {
+        const int64_t M = (down ? -I.delta : I.delta) * tpr;
+        for (int64_t d = M / KTILE_CHUNKS; d <= (M + KTILE_CHUNKS - 1) / KTILE_CHUNKS; ++d) {
+            const int64_t j = order - d;
+            if (d == 0 || j < 0) continue;
+            f(I.flag0 + int64_t(layer) * I.n_tiles + j);
+        }
+    }
+    uint32_t w = I.waits;
+    if (!w) return;
+    const int64_t c_hi = kmin64((q + 1) * KTILE_CHUNKS, I.count * tpr);
+    const int64_t lo = I.dst0 + q * KTILE_CHUNKS / tpr;                 // destination rows [lo, hi)
+    const int64_t hi = I.dst0 + (c_hi - 1) / tpr + 1;
+    while (w) {
+        const int a = __builtin_ctz(w);
+        w &= w - 1;
+        const KTileItem& A = P.items[a];
+        const int64_t x0 = kmax64(lo, A.src0), x1 = kmin64(hi, A.src0 + A.count);
+        if (x0 >= x1) continue;
+        const int64_t t0 = (x0 - A.src0) * tpr / KTILE_CHUNKS;
+        const int64_t t1 = ((x1 - A.src0) * tpr - 1) / KTILE_CHUNKS;
+        for (int64_t t = t0; t <= t1; ++t) {
+            const int64_t o = A.delta < 0 ? t : A.n_tiles - 1 - t;     // A's processing order
+            f(A.flag0 + int64_t(layer) * A.n_tiles + o);
+        }
+    }
+}
+
+// Before the tile launches of a call: clear its counters and flags, and write entries of its
+// cos/sin table into the workspace (carried here, in the kernel arguments).
+constexpr int KPREP_CS = 320;
+
+struct KPrepParams {
+    int32_t* zero;
+    int64_t n_zero;          // 32-bit words from `zero`
+    KCosSin* cs_dst;
+    int32_t n_cs;            // entries of cs[] written to cs_dst
+    int32_t pad;
+    KCosSin cs[KPREP_CS];
 };
 
 // ------------------------------------------------------------------------------ rotate-only --

@@ -195,6 +195,85 @@ int64_t tile_count(int64_t rows, int32_t tpr) {
     return (rows * tpr + KTILE_CHUNKS - 1) / KTILE_CHUNKS;
 }
 
+namespace {
+
+int64_t align256(int64_t v) { return (v + 255) & ~int64_t(255); }
+
+// Every job of the call as ordered-tile items, in dependency-level order, packed into launches of
+// at most KTILE_MAX_ITEMS items.  An item waits (inside its launch) for the earlier moves of its
+// plane whose source rows it overwrites; items of earlier launches are finished by stream order.
+// One cos/sin block per distinct shift goes into the call's table.
+int plan_tiles(const leyline_cache* cache, const leyline_directive* dirs, const KPlane* planes,
+               int n_planes, const std::vector<ContigJobHost>& jobs, const std::vector<int>& level,
+               ContigSchedule* out) {
+    std::vector<size_t> order(jobs.size());
+    for (size_t k = 0; k < order.size(); ++k) order[k] = k;
+    std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return level[a] < level[b]; });
+    const bool any_rot = cos_sin_per_shift(cache) > 0;
+    std::vector<std::pair<int64_t, int32_t>> shift_cs;      // shift -> first entry of its block
+    int64_t n_flags = 0;
+    TileLaunchHost cur;
+    out->tiles = true;
+    for (size_t k : order) {
+        const ContigJobHost& x = jobs[k];
+        const bool move = x.kind != KJOB_STUB;
+        if (int(cur.items.size()) + n_planes > KTILE_MAX_ITEMS) {
+            out->tile_launches.push_back(std::move(cur));
+            cur = TileLaunchHost();
+        }
+        int32_t cs0 = -1;
+        if (move && any_rot) {
+            for (const auto& e : shift_cs)
+                if (e.first == x.delta) cs0 = e.second;
+            if (cs0 < 0) {
+                cs0 = append_cos_sin(cache, x.delta, out->cs);
+                shift_cs.emplace_back(x.delta, cs0);
+            }
+        }
+        for (int p = 0; p < n_planes; ++p) {
+            KTileItem it;
+            std::memset(&it, 0, sizeof(it));
+            it.kind = move ? KJOB_TILE : KJOB_STUB;
+            it.plane = p;
+            it.count = x.count;
+            if (move) {
+                it.src0 = x.src0;
+                it.dst0 = x.src0 + x.delta;
+                it.delta = x.delta;
+                it.cs = (cs0 >= 0 && planes[p].rot != KROT_NONE) ? cs0 + planes[p].cs_off : -1;
+            } else {
+                it.dst0 = x.dst0;
+                it.stub = static_cast<const char*>(dirs[x.dir].stub[p]);
+                it.cs = -1;
+            }
+            const int64_t tiles = tile_count(x.count, planes[p].tpr);
+            const int64_t tickets = int64_t(cache->n_layers) * tiles;
+            it.n_tiles = int32_t(tiles);
+            it.ticket0 = int32_t(cur.tickets);
+            it.flag0 = -1;
+            if (move) {
+                it.flag0 = int32_t(n_flags);
+                n_flags += tickets;
+            }
+            for (size_t a = 0; a < cur.items.size(); ++a) {
+                const KTileItem& A = cur.items[a];
+                if (A.kind == KJOB_TILE && A.plane == p && it.dst0 < A.src0 + A.count && A.src0 < it.dst0 + it.count)
+                    it.waits |= 1u << a;
+            }
+            cur.tickets += tickets;
+            if (cur.tickets > INT32_MAX - 1024 || n_flags > INT32_MAX - 1024) return LEYLINE_E_INVAL;
+            cur.items.push_back(it);
+        }
+    }
+    if (!cur.items.empty()) out->tile_launches.push_back(std::move(cur));
+    out->ws_flags = 256 * int64_t(out->tile_launches.size());
+    out->ws_cs = align256(out->ws_flags + 4 * n_flags);
+    out->ws_bytes = align256(out->ws_cs + int64_t(sizeof(KCosSin)) * int64_t(out->cs.size()));
+    return LEYLINE_OK;
+}
+
+}  // namespace
+
 int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_directive* dirs,
                 int32_t n_dirs, ContigSchedule* out) {
     KPlane planes[LEYLINE_MAX_PLANES];
@@ -218,7 +297,10 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
     if (new_len > cache->capacity) return LEYLINE_E_CAPACITY;
     out->new_len = new_len;
     out->launches.clear();
-    out->ws_bytes = 0;
+    out->tiles = false;
+    out->tile_launches.clear();
+    out->cs.clear();
+    out->ws_flags = out->ws_cs = out->ws_bytes = 0;
 
     // Jobs: each downstream segment [e_j, s_{j+1}) moved by its running shift, each stub copied.
     std::vector<ContigJobHost> jobs;
@@ -261,21 +343,32 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
         if (!changed) break;
     }
 
-    // Within a job, a left shift by m makes row x the destination of row x + m.  Splitting the
-    // source range into rounds of at most m rows, taken in ascending order (descending for a
-    // right shift), leaves each round with disjoint sources and destinations, and every row a
-    // round overwrites was read by an earlier round.  Rounds run as consecutive launches; a move
-    // needing more than MAX_ROUNDS rounds runs as ordered chains in a single launch instead.
     const int n_levels = *std::max_element(level.begin(), level.end()) + 1;
-    const int32_t cs_need = cos_sin_per_shift(cache);
-    // Moves too long for rounds run as ordered tiles when every plane moves single chunks
-    // (half-split bands whose partners cannot be exchanged between lanes use ordered chains).
+    // Ordered tiles need every plane to move single chunks (half-split bands whose partners
+    // cannot be exchanged between lanes use ordered chains).
     bool tiles_ok = true;
     int64_t row_bytes_all = 0;
     for (int p = 0; p < n_planes; ++p) {
         if (planes[p].rot == KROT_NEOX && !planes[p].neox_lanes) tiles_ok = false;
         row_bytes_all += planes[p].row_bytes;
     }
+    // Within a job, a left shift by m makes row x the destination of row x + m.  Splitting the
+    // source range into rounds of at most m rows, taken in ascending order (descending for a
+    // right shift), leaves each round with disjoint sources and destinations, and every row a
+    // round overwrites was read by an earlier round.  Rounds cost one launch each: they are used
+    // for a single round, or when every round moves enough bytes to fill the device.  Once some
+    // move would need rounds too small or too many, the whole call runs as ordered tiles.
+    bool need_tiles = false;
+    for (const ContigJobHost& x : jobs) {
+        if (x.kind == KJOB_STUB) continue;
+        const int64_t m = x.delta < 0 ? -x.delta : x.delta;
+        const int64_t nr = (x.count + m - 1) / m;
+        const bool big_rounds = nr == 1 || m * row_bytes_all * cache->n_layers >= ROUND_MIN_BYTES;
+        if (nr > MAX_ROUNDS || !big_rounds) need_tiles = true;
+    }
+    if (tiles_ok && need_tiles) return plan_tiles(cache, dirs, planes, n_planes, jobs, level, out);
+
+    const int32_t cs_need = cos_sin_per_shift(cache);
     for (int lv = 0; lv < n_levels; ++lv) {
         std::vector<std::vector<ContigJobHost>> rounds(1);
         for (size_t a = 0; a < n; ++a) {
@@ -287,22 +380,9 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
             }
             const int64_t m = x.delta < 0 ? -x.delta : x.delta;
             const int64_t nr = (x.count + m - 1) / m;
-            // Rounds cost one launch each: they are used for a single round, or when every round
-            // moves enough bytes to fill the device; otherwise ordered tiles (one launch shared
-            // by the level's tile moves) are faster.
-            const bool big_rounds = nr == 1 || m * row_bytes_all * cache->n_layers >= ROUND_MIN_BYTES;
-            if (nr > MAX_ROUNDS || (tiles_ok && !big_rounds)) {
-                ContigJobHost y = x;
-                if (tiles_ok) {
-                    // ordered tiles: a ticket counter and one flag per (tile, layer, plane)
-                    y.kind = KJOB_TILE;
-                    y.ws_off = out->ws_bytes;
-                    int64_t flags = 0;
-                    for (int p = 0; p < n_planes; ++p) flags += int64_t(cache->n_layers) * tile_count(x.count, planes[p].tpr);
-                    if (flags > INT32_MAX - 1024) return LEYLINE_E_INVAL;
-                    out->ws_bytes += ((int64_t(KTILE_FLAGS_OFF) + flags) * 4 + 255) & ~int64_t(255);
-                }
-                rounds[0].push_back(y);       // KJOB_TILE or KJOB_CHAIN
+            if (nr > MAX_ROUNDS) {              // only without tiles: ordered chains
+                rounds[0].push_back(x);
+                rounds[0].back().kind = KJOB_CHAIN;
                 continue;
             }
             if (int64_t(rounds.size()) < nr) rounds.resize(size_t(nr));
@@ -321,7 +401,6 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
                 rounds[size_t(r)].push_back(ContigJobHost{KJOB_ROUND, lo, 0, hi - lo, x.delta, x.dir});
             }
         }
-        if (out->ws_bytes / 4 > INT32_MAX - 1024) return LEYLINE_E_INVAL;
         for (const auto& rj : rounds) {
             std::vector<ContigJobHost> cur;
             int32_t cs_used = 0;

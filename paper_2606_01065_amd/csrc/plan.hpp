@@ -48,18 +48,31 @@ struct ContigJobHost {
     int32_t kind;       // KJOB_*
     int64_t src0, dst0, count, delta;
     int32_t dir;        // stub: directive index
-    int64_t ws_off = 0; // tile: byte offset of its ticket counter and flags in the workspace
 };
 
-// A move needing more rounds than this runs as ordered chains in one launch instead.
+// A move needing more rounds than this runs as ordered chains (or tiles) instead.
 constexpr int64_t MAX_ROUNDS = 16;
 // Rounds moving fewer bytes than this (all layers and planes) are not worth a launch each.
 constexpr int64_t ROUND_MIN_BYTES = int64_t(64) << 20;
 
+// One ordered-tile launch: its items (in dependency order) and its number of tickets.
+struct TileLaunchHost {
+    std::vector<KTileItem> items;
+    int64_t tickets = 0;
+};
+
 struct ContigSchedule {
     int64_t new_len = 0;
+    // Rounds, chains and replacement copies: groups of independent jobs, in order.
     std::vector<std::vector<ContigJobHost>> launches;
-    int64_t ws_bytes = 0;   // workspace of the ordered-tile moves (cleared on the device per call)
+    // Ordered tiles (used for every job of a call once any move needs them): launches in order,
+    // after prep launches that clear the workspace and write the cos/sin table into it.
+    bool tiles = false;
+    std::vector<TileLaunchHost> tile_launches;
+    std::vector<KCosSin> cs;    // the call's cos/sin table (tiles)
+    int64_t ws_flags = 0;       // workspace byte offsets: ticket counters (256 bytes per tile
+    int64_t ws_cs = 0;          // launch) from 0, flags from ws_flags, cos/sin table from ws_cs
+    int64_t ws_bytes = 0;       // workspace bytes (0 without tiles)
 };
 
 // Tiles of one ordered-tile move on a plane with `tpr` chunks per row.

@@ -125,22 +125,28 @@ def test_contig_validation_codes():
 def test_contig_query_reports_rounds_tiles_and_workspace():
     """A left shift by m of D downstream rows can run as ceil(D/m) rounds (one launch each, no
     workspace) when every round moves at least 64 MB; otherwise, and whenever it would take more
-    than 16 rounds, the move runs as ordered tiles in one launch, after one launch that clears
-    the tiles' counter and flags in the workspace.  A replacement copy is one more launch."""
+    than 16 rounds, the whole call (moves and replacement copies) runs as ordered tiles in one
+    launch, after one launch that clears the tiles' counter and flags in the workspace and writes
+    the cos/sin table there.  With rounds, a replacement copy is one more launch."""
     big = _mla_cache(n_layers=61, cap=32768)                                # 1152-byte rows
     q = L.leyline_contig_query(big, 32768, _dirs([(14055, 18151, 32)]), 1)   # m=4064: 285 MB rounds
     assert (q.new_len, q.launches, q.tile_launches, q.workspace_bytes) == (32768 - 4064, 4 + 1, 0, 0)
     c = _mla_cache(cap=64)                                                  # 2 layers, 72 chunks/row
     q = L.leyline_contig_query(c, 60, _dirs([(10, 20, 2)]), 1)               # m=8, D=40: small rounds
-    assert (q.new_len, q.launches, q.tile_launches) == (52, 1 + 1 + 1, 1)    # clear, tiles, stub
+    assert (q.new_len, q.launches, q.tile_launches) == (52, 1 + 1, 1)        # prep, tiles (+ stub)
     q = L.leyline_contig_query(c, 60, _dirs([(10, 11, 0)]), 1)               # m=1, D=49
     tiles = -(-49 * 72 // 8192)                      # per layer; a tile is 1024 threads x 8 chunks
     assert (q.new_len, q.launches, q.tile_launches) == (59, 1 + 1, 1)
-    assert q.workspace_bytes == -(-(64 + 2 * tiles) * 4 // 256) * 256
+    # one 256-byte counter, a flag per (layer, tile), then 32 cos/sin pairs of 8 bytes
+    flags_end = 256 + 4 * 2 * tiles
+    assert q.workspace_bytes == -(-(-(-flags_end // 256) * 256 + 32 * 8) // 256) * 256
     q = L.leyline_contig_query(c, 60, _dirs([(10, 12, 4)]), 1)               # m=2 right, D=48
-    assert (q.new_len, q.launches, q.tile_launches) == (62, 1 + 1 + 1, 1)
+    assert (q.new_len, q.launches, q.tile_launches) == (62, 1 + 1, 1)
     q = L.leyline_contig_query(c, 60, _dirs([(10, 40, 2)]), 1)               # m=28 > D=20: one round
     assert (q.new_len, q.launches, q.tile_launches, q.workspace_bytes) == (32, 1 + 1, 0, 0)
+    # several directives with small shifts: one prep and one tile launch for all of them
+    q = L.leyline_contig_query(c, 60, _dirs([(5, 7, 1), (20, 22, 3), (40, 41, 0)]), 3)
+    assert (q.new_len, q.launches, q.tile_launches) == (59, 1 + 1, 1)
     with pytest.raises(L.LeylineError) as e:
         L.leyline_contig_query(c, 60, _dirs([(10, 10, 5)]), 1)
     assert e.value.code == L.E_CAPACITY

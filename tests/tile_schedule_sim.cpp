@@ -1,0 +1,271 @@
+// Host-side check of the ordered-tile schedules of contiguous splices.
+//
+// Random multi-directive splices are planned with the library's planner; every tile launch of a
+// plan is then executed on the CPU the way the tile kernel runs it: workgroups take tickets in
+// order (at most W in flight), each loads its source chunks, publishes "source read" (moves),
+// waits for the flags that tile_wait_flags lists and stores.  The order in which in-flight
+// workgroups load and store is drawn at random.  The check fails if a load sees a row that was
+// already overwritten, if a wait names a flag outside the launch or of a later ticket, if a
+// schedule stalls, or if the rows [0, new_len) differ from the splice's definition (prefix
+// unchanged, replacements at s_j + delta_{j-1}, segment j shifted by delta_j).  Values are row
+// identities, not data: rotation is not simulated.
+//
+// Usage: tile_schedule_sim SEED CASES   (prints "ok <tile cases> <tiles>" on success)
+#include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <random>
+#include <vector>
+
+#include "plan.hpp"
+
+using namespace leyline;
+
+namespace {
+
+struct Shape {
+    const char* name;
+    int32_t dtype;
+    int n_planes;
+    int32_t row_elems[2];
+    int32_t n_heads[2], head_stride[2], rot_offset[2], rot_dim[2], style[2];
+    int64_t max_len;
+};
+
+const Shape kShapes[] = {
+    // 32-byte rows (2 chunks), an interleaved 8-element band
+    {"tiny_interleaved", LEYLINE_BF16, 1, {16, 0}, {1, 0}, {16, 0}, {8, 0}, {8, 0}, {LEYLINE_ROPE_INTERLEAVED, 0}, 30000},
+    // K (two heads, half-split bands exchanged between lanes) and V planes, 8 chunks per row
+    {"small_kv", LEYLINE_BF16, 2, {64, 64}, {2, 1}, {32, 64}, {0, 0}, {32, 0}, {LEYLINE_ROPE_NEOX, 0}, 8000},
+    // MLA rows: c_kv 512 + k_pe 64 bf16 (72 chunks)
+    {"mla", LEYLINE_BF16, 1, {576, 0}, {1, 0}, {576, 0}, {512, 0}, {64, 0}, {LEYLINE_ROPE_INTERLEAVED, 0}, 2500},
+    // fp32 rows of 4 chunks, no rotary band
+    {"f32_plain", LEYLINE_F32, 1, {16, 0}, {1, 0}, {16, 0}, {0, 0}, {0, 0}, {0, 0}, 15000},
+};
+
+int64_t orig_val(int p, int l, int64_t row, int64_t c) { return ((((int64_t(p) * 4 + l) << 24) | row) << 10 | c) + 1; }
+int64_t stub_val(int j, int p, int l, int64_t t, int64_t c) {
+    return -(((((int64_t(j) * 4 + p) * 4 + l) << 24 | t) << 10 | c) + 1);
+}
+
+int fail(const char* what, int case_id) {
+    std::printf("FAIL case %d: %s\n", case_id, what);
+    return 1;
+}
+
+}  // namespace
+
+int main(int argc, char** argv) {
+    const unsigned seed = argc > 1 ? unsigned(std::atoi(argv[1])) : 1u;
+    const int cases = argc > 2 ? std::atoi(argv[2]) : 100;
+    std::mt19937_64 rng(seed);
+    auto uni = [&](int64_t lo, int64_t hi) { return std::uniform_int_distribution<int64_t>(lo, hi)(rng); };
+    int tile_cases = 0;
+    int64_t tiles_run = 0;
+    for (int ci = 0; ci < cases; ++ci) {
+        const Shape& sh = kShapes[uni(0, 3)];
+        const int L = int(uni(1, 3));
+        const int64_t n = uni(1, sh.max_len);
+        // directives: sorted, non-overlapping (adjacent allowed) spans; short shifts are common
+        const int k = int(uni(1, 8));
+        std::vector<int64_t> cuts;
+        for (int i = 0; i < 2 * k; ++i) cuts.push_back(uni(0, n));
+        std::sort(cuts.begin(), cuts.end());
+        std::vector<leyline_directive> dirs(static_cast<size_t>(k));
+        int64_t shift = 0, grow = 0;
+        for (int j = 0; j < k; ++j) {
+            leyline_directive& d = dirs[size_t(j)];
+            std::memset(&d, 0, sizeof(d));
+            d.span_start = cuts[size_t(2 * j)];
+            d.span_end = std::min(cuts[size_t(2 * j + 1)], d.span_start + (uni(0, 3) == 0 ? n : uni(0, 64)));
+            const int64_t span = d.span_end - d.span_start;
+            const int pick = int(uni(0, 4));
+            d.stub_len = pick == 0 ? 0 : pick == 1 ? span + uni(-3, 3) : pick == 2 ? span : uni(0, 2 * span + 3);
+            if (d.stub_len < 0) d.stub_len = 0;
+            for (int p = 0; p < sh.n_planes; ++p)
+                d.stub[p] = d.stub_len ? reinterpret_cast<const void*>(uintptr_t(0x1000000) * (j + 1) + 0x10000 * p) : nullptr;
+            shift += d.stub_len - span;
+            grow = std::max(grow, shift);
+        }
+        const int64_t new_len = n + shift, cap = n + grow + uni(0, 3);
+        leyline_cache cache;
+        std::memset(&cache, 0, sizeof(cache));
+        cache.dtype = sh.dtype;
+        cache.n_layers = L;
+        cache.n_planes = sh.n_planes;
+        cache.capacity = cap;
+        for (int p = 0; p < sh.n_planes; ++p) {
+            leyline_plane& pl = cache.planes[p];
+            pl.base = reinterpret_cast<void*>(uintptr_t(0x100000000ull) * (p + 1));
+            pl.row_elems = sh.row_elems[p];
+            pl.token_stride = sh.row_elems[p];
+            pl.layer_stride = cap * sh.row_elems[p];
+            pl.n_heads = sh.n_heads[p];
+            pl.head_stride = sh.head_stride[p];
+            pl.rot_offset = sh.rot_offset[p];
+            pl.rot_dim = sh.rot_dim[p];
+            pl.rope_style = sh.style[p];
+            pl.rope_base = 10000.0;
+        }
+        ContigSchedule sched;
+        const int rc = plan_contig(&cache, n, dirs.data(), k, &sched);
+        if (rc) {
+            std::printf("FAIL case %d: plan_contig returned %d\n", ci, rc);
+            return 1;
+        }
+        if (sched.new_len != new_len) return fail("new length", ci);
+        if (!sched.tiles) continue;
+        ++tile_cases;
+        KPlane planes[LEYLINE_MAX_PLANES];
+        int n_planes = 0;
+        if (describe_cache(&cache, false, planes, &n_planes)) return fail("describe_cache", ci);
+        // memory: per plane and layer, cap rows of tpr chunks holding row identities
+        std::vector<std::vector<int64_t>> mem(static_cast<size_t>(n_planes * L));
+        for (int p = 0; p < n_planes; ++p)
+            for (int l = 0; l < L; ++l) {
+                auto& m = mem[size_t(p * L + l)];
+                const int64_t tpr = planes[p].tpr;
+                m.assign(size_t(cap * tpr), 0);
+                for (int64_t r = 0; r < cap; ++r)
+                    for (int64_t c = 0; c < tpr; ++c) m[size_t(r * tpr + c)] = orig_val(p, l, r, c);
+            }
+        int64_t n_flags = 0;
+        for (const auto& tl : sched.tile_launches)
+            for (const auto& it : tl.items)
+                if (it.kind == KJOB_TILE) n_flags = std::max<int64_t>(n_flags, it.flag0 + int64_t(L) * it.n_tiles);
+        std::vector<int> flags(static_cast<size_t>(n_flags), 0);
+        for (const auto& tl : sched.tile_launches) {
+            if (tl.items.empty() || tl.items.size() > size_t(KTILE_MAX_ITEMS)) return fail("item count", ci);
+            KTileParams P;
+            std::memset(&P, 0, sizeof(P));
+            std::memcpy(P.planes, planes, sizeof(KPlane) * size_t(n_planes));
+            std::copy(tl.items.begin(), tl.items.end(), P.items);
+            P.n_items = int32_t(tl.items.size());
+            P.n_tickets = int32_t(tl.tickets);
+            // ticket -> (item, layer, order); flag -> ticket, for flags of this launch
+            struct Tile { int item, layer, order; };
+            std::vector<Tile> tiles(static_cast<size_t>(tl.tickets));
+            std::vector<int64_t> flag_ticket(size_t(n_flags), -1);
+            for (int i = 0; i < P.n_items; ++i) {
+                const KTileItem& I = P.items[i];
+                if (i + 1 < P.n_items && P.items[i + 1].ticket0 != I.ticket0 + int64_t(L) * I.n_tiles)
+                    return fail("ticket ranges", ci);
+                if (I.waits >> i) return fail("an item waits for itself or a later item", ci);
+                for (int l = 0; l < L; ++l)
+                    for (int o = 0; o < I.n_tiles; ++o) {
+                        const int64_t t = I.ticket0 + int64_t(l) * I.n_tiles + o;
+                        tiles[size_t(t)] = Tile{i, l, o};
+                        if (I.kind == KJOB_TILE) flag_ticket[size_t(I.flag0 + int64_t(l) * I.n_tiles + o)] = t;
+                    }
+            }
+            // loads and stores of one tile
+            auto chunks = [&](const Tile& T, int64_t* g0, int64_t* g1) {
+                const KTileItem& I = P.items[T.item];
+                const int64_t tpr = planes[I.plane].tpr, total = I.count * tpr;
+                const int64_t q = I.delta <= 0 ? T.order : I.n_tiles - 1 - T.order;
+                *g0 = q * KTILE_CHUNKS;
+                *g1 = std::min(total, *g0 + KTILE_CHUNKS);
+            };
+            std::vector<std::vector<int64_t>> buf(size_t(tl.tickets));
+            std::vector<int> state(size_t(tl.tickets), 0);        // 0 taken, 1 loaded, 2 stored
+            const int64_t W = std::vector<int64_t>{1, 2, 3, 8, 64, int64_t(1) << 40}[size_t(uni(0, 5))];
+            int64_t next = 0;
+            std::vector<int64_t> live;
+            std::vector<int64_t> waits;
+            while (next < tl.tickets || !live.empty()) {
+                // possible actions: take the next ticket, load a taken tile, store a loaded one
+                std::vector<std::pair<int, int64_t>> acts;
+                if (next < tl.tickets && int64_t(live.size()) < W) acts.emplace_back(0, next);
+                for (int64_t t : live) {
+                    if (state[size_t(t)] == 0) {
+                        acts.emplace_back(1, t);
+                        continue;
+                    }
+                    const Tile& T = tiles[size_t(t)];
+                    bool ready = true;
+                    bool bad = false;
+                    tile_wait_flags(P, T.item, T.layer, T.order, [&](int64_t f) {
+                        if (f < 0 || f >= n_flags || flag_ticket[size_t(f)] < 0 || flag_ticket[size_t(f)] >= t) bad = true;
+                        else if (!flags[size_t(f)]) ready = false;
+                    });
+                    if (bad) return fail("a wait names a flag outside the launch or of a later ticket", ci);
+                    if (ready) acts.emplace_back(2, t);
+                }
+                if (acts.empty()) return fail("schedule stalled", ci);
+                const auto a = acts[size_t(uni(0, int64_t(acts.size()) - 1))];
+                const int64_t t = a.second;
+                if (a.first == 0) {
+                    live.push_back(t);
+                    ++next;
+                    continue;
+                }
+                const Tile& T = tiles[size_t(t)];
+                const KTileItem& I = P.items[T.item];
+                const int p = I.plane;
+                const int64_t tpr = planes[p].tpr;
+                auto& m = mem[size_t(p * L + T.layer)];
+                int64_t g0, g1;
+                chunks(T, &g0, &g1);
+                if (a.first == 1) {
+                    auto& b = buf[size_t(t)];
+                    b.resize(size_t(g1 - g0));
+                    for (int64_t g = g0; g < g1; ++g) {
+                        const int64_t r = g / tpr, c = g % tpr;
+                        if (I.kind == KJOB_TILE) {
+                            const int64_t v = m[size_t((I.src0 + r) * tpr + c)];
+                            if (v != orig_val(p, T.layer, I.src0 + r, c)) return fail("a load saw an overwritten row", ci);
+                            b[size_t(g - g0)] = v;
+                        } else {
+                            int j = -1;
+                            for (int jj = 0; jj < k; ++jj)
+                                if (dirs[size_t(jj)].stub[p] == I.stub) j = jj;
+                            if (j < 0) return fail("unknown replacement", ci);
+                            b[size_t(g - g0)] = stub_val(j, p, T.layer, r, c);
+                        }
+                    }
+                    if (I.kind == KJOB_TILE) flags[size_t(I.flag0 + int64_t(T.layer) * I.n_tiles + T.order)] = 1;
+                    state[size_t(t)] = 1;
+                } else {
+                    const auto& b = buf[size_t(t)];
+                    for (int64_t g = g0; g < g1; ++g) {
+                        const int64_t r = g / tpr, c = g % tpr;
+                        m[size_t((I.dst0 + r) * tpr + c)] = b[size_t(g - g0)];
+                    }
+                    state[size_t(t)] = 2;
+                    live.erase(std::find(live.begin(), live.end(), t));
+                    ++tiles_run;
+                }
+            }
+        }
+        // rows [0, new_len) against the definition
+        for (int p = 0; p < n_planes; ++p)
+            for (int l = 0; l < L; ++l) {
+                const auto& m = mem[size_t(p * L + l)];
+                const int64_t tpr = planes[p].tpr;
+                auto check_row = [&](int64_t pos, int j, int64_t src) -> bool {   // j >= 0: stub j row src
+                    for (int64_t c = 0; c < tpr; ++c) {
+                        const int64_t want = j >= 0 ? stub_val(j, p, l, src, c) : orig_val(p, l, src, c);
+                        if (m[size_t(pos * tpr + c)] != want) return false;
+                    }
+                    return true;
+                };
+                int64_t pos = 0, delta = 0;
+                for (int64_t r = 0; r < dirs[0].span_start; ++r, ++pos)
+                    if (!check_row(pos, -1, r)) return fail("prefix row", ci);
+                for (int j = 0; j < k; ++j) {
+                    const leyline_directive& d = dirs[size_t(j)];
+                    if (pos != d.span_start + delta) return fail("position bookkeeping", ci);
+                    for (int64_t t = 0; t < d.stub_len; ++t, ++pos)
+                        if (!check_row(pos, j, t)) return fail("replacement row", ci);
+                    delta += d.stub_len - (d.span_end - d.span_start);
+                    const int64_t seg_end = j + 1 < k ? dirs[size_t(j + 1)].span_start : n;
+                    for (int64_t r = d.span_end; r < seg_end; ++r, ++pos)
+                        if (!check_row(pos, -1, r)) return fail("moved row", ci);
+                }
+                if (pos != new_len) return fail("new length bookkeeping", ci);
+            }
+    }
+    std::printf("ok %d %lld\n", tile_cases, static_cast<long long>(tiles_run));
+    return 0;
+}
