@@ -152,6 +152,17 @@ def test_contig_query_reports_rounds_tiles_and_workspace():
     assert e.value.code == L.E_CAPACITY
 
 
+def test_contig_many_directives_split_tile_and_prep_launches():
+    """A tile launch holds at most 24 (job, plane) items and a prep launch writes at most 320
+    cos/sin pairs: 16 small-shift edits on the MLA cache (16 moves, 16 copies, 16 shifts of 32
+    pairs) need two of each; the workspace holds both counters, the flags and the table."""
+    c = _mla_cache(n_layers=3, cap=4000)
+    spec = [(100 + 200 * i, 110 + 200 * i, 10 + (i % 3) + 1) for i in range(16)]
+    q = L.leyline_contig_query(c, 3800, _dirs(spec), 16)
+    assert (q.tile_launches, q.launches) == (2, 2 + 2)
+    assert q.workspace_bytes >= 2 * 256 + 16 * 32 * 8
+
+
 def test_contig_tiles_need_a_workspace():
     c = _mla_cache(cap=64)
     new_len = ctypes.c_int64(-1)

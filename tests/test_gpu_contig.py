@@ -207,6 +207,28 @@ def test_small_shift_full_size(L, name, dirs, extra):
     _run_and_check(L, wl, planes_dev, stubs_dev, f"{name} small shift {dirs}", layers=layers)
 
 
+@pytest.mark.parametrize("kind,k", [("mla", 16), ("mla", 20), ("gqa", 8)])
+def test_many_directives_several_tile_launches(L, kind, k):
+    """More (job, plane) items than one tile launch holds: the call runs as consecutive tile
+    launches in dependency order; whole cache against the oracle."""
+    rng = random.Random(900 + k + (kind == "gqa"))
+    for ci in range(3):
+        n = rng.randint(2500, 4000)
+        cuts = sorted(rng.sample(range(n + 1), 2 * k))
+        dirs = []
+        for i in range(0, 2 * k, 2):
+            s = cuts[i]
+            e = min(cuts[i + 1], s + rng.randint(0, 40))
+            dirs.append(W.Dir(s, e, max(0, (e - s) + rng.choice([-3, -1, 1, 2, 5]))))
+        wl = _small_workload(rng, kind, "bf16", 3, n, dirs, extra=rng.randint(0, 5))
+        planes_dev, stubs_dev = W.alloc_contig(wl, DEV, seed=2000 + ci)
+        cache = L.make_cache(_specs(L, wl, planes_dev))
+        q = L.leyline_contig_query(cache, n, L.make_directives(_dir_dicts(wl, stubs_dev)), k)
+        assert q.tile_launches >= 2, q
+        _run_and_check(L, wl, planes_dev, stubs_dev,
+                       f"{kind} {k} directives case {ci} n={n} tile launches={q.tile_launches}")
+
+
 def test_mla_dsv3_32k_edits8(L):
     """Eight edits drawn like the paper's randomized edit suite, both signs, one call."""
     wl = W.mla_dsv3_32k_edits8()

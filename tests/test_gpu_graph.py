@@ -45,27 +45,28 @@ def _replay_and_compare(fn, t, pristine, eager):
         assert np.array_equal(host(t), eager), f"replay {rep} differs from the eager call"
 
 
-@pytest.mark.parametrize("layers,n,span,stub_len,tiles", [
-    (3, 3000, (500, 501), 0, 1),          # shift -1: ordered tiles (clear + tile launches)
-    (20, 12000, (1000, 5000), 16, 0),     # shift -3984, 92 MB rounds: round launches + stub copy
+@pytest.mark.parametrize("layers,n,edits,tiles", [
+    (3, 3000, [(500, 501, 0)], 1),                        # shift -1: prep + one tile launch
+    (20, 12000, [(1000, 5000, 16)], 0),                   # shift -3984, 92 MB rounds + stub copy
+    (3, 3000, [(100, 104, 1), (700, 700, 2), (1500, 1530, 25), (2900, 2950, 0)], 1),  # edits in one tile launch
 ])
-def test_contig_splice_in_a_graph(L, layers, n, span, stub_len, tiles):
-    cap = n
+def test_contig_splice_in_a_graph(L, layers, n, edits, tiles):
+    cap = n + 8
     t, cache = _mla_cache(L, layers, cap, seed=31)
     pristine = t.clone()
-    stub = torch.randn((layers, stub_len, 576), device=DEV).to(torch.bfloat16) if stub_len else None
-    dirs = L.make_directives([dict(span_start=span[0], span_end=span[1], stub=[stub] if stub is not None else None,
-                                   stub_len=stub_len)])
-    q = L.leyline_contig_query(cache, n, dirs, 1)
+    stubs = [torch.randn((layers, r, 576), device=DEV).to(torch.bfloat16) if r else None for _, _, r in edits]
+    dirs = L.make_directives([dict(span_start=s, span_end=e, stub=[stubs[j]] if stubs[j] is not None else None,
+                                   stub_len=r) for j, (s, e, r) in enumerate(edits)])
+    k = len(edits)
+    q = L.leyline_contig_query(cache, n, dirs, k)
     assert q.tile_launches == tiles
     ws = torch.empty(max(256, q.workspace_bytes), dtype=torch.uint8, device=DEV)
-    print(f"[case] graph contig span={span} stub={stub_len} launches={q.launches} tiles={q.tile_launches}",
-          flush=True)
-    L.leyline_splice_contig(cache, n, dirs, 1, workspace=ws)
+    print(f"[case] graph contig edits={edits} launches={q.launches} tiles={q.tile_launches}", flush=True)
+    L.leyline_splice_contig(cache, n, dirs, k, workspace=ws)
     torch.cuda.synchronize()
     eager = host(t)
     assert not np.array_equal(eager, host(pristine))
-    _replay_and_compare(lambda: L.leyline_splice_contig(cache, n, dirs, 1, workspace=ws), t, pristine, eager)
+    _replay_and_compare(lambda: L.leyline_splice_contig(cache, n, dirs, k, workspace=ws), t, pristine, eager)
 
 
 def test_rotate_delta_in_a_graph(L):
