@@ -246,11 +246,12 @@ int leyline_paged_plan(int32_t page_size, int32_t n_seqs, const int32_t* seq_len
  * workspace: device, 256-byte aligned, >= the size leyline_paged_query reports.  It receives the
  * plan (runs of pages, per-sequence and per-directive tables and cos/sin; plans of at most 2560
  * bytes travel in the kernel arguments instead, larger ones are uploaded with an asynchronous
- * copy on `stream`) and the tables a kernel of this call writes from it (24 bytes per row of every
- * ASSEMBLE page, 16 bytes per REMAP page, 4 bytes per fresh page); reuse it only after the stream
- * has passed this call.  Any page_size whose rows keep the 16-byte alignment is accepted.
- * An uploaded plan comes from host memory the call owns only while it runs: do not capture this
- * call into a HIP graph.
+ * copy on `stream`) and, when the call assembles more than 1024 rows, the row table a kernel of
+ * this call writes from it (24 bytes per row of every ASSEMBLE page, 4 bytes per fresh page);
+ * reuse it only after the stream has passed this call.  Any page_size whose rows keep the
+ * 16-byte alignment is accepted.  A call with a plan of at most 2560 bytes enqueues kernels only
+ * (and, assembling at most 1024 rows, a single one); an uploaded plan comes from host memory the
+ * call owns only while it runs: do not capture such a call into a HIP graph.
  *
  * flags: 0, or LEYLINE_PAGED_COPY_ON_WRITE (no REMAP pages: no old page is written).
  * Ownership: only ASSEMBLE pages (fresh) and REMAP pages (rotary bands, in place) are written.

@@ -631,15 +631,17 @@ __global__ __launch_bounds__(PAGED_TPB) void rotate_rows_kernel(const KRotatePar
 
 // ------------------------------------------------------------------------------ paged splice ---
 //
-// Two launches on the call's stream, after the plan's runs are uploaded.
-// (1) paged_resolve_kernel expands the runs once for all layers and planes: for every row of
-//     every ASSEMBLE page, which old physical page and row (or which replacement token) it comes
-//     from, which fresh page it goes to and which shift re-anchors it; for every REMAP page, its
-//     physical page and shift; and the new block tables and the freed-page list.
-// (2) paged_data_kernel moves the data.  Its first blocks gather ASSEMBLE rows like the
-//     contiguous kernel (rows laid end to end, one 16-byte chunk per thread, so a wavefront
-//     reads one row entry and moves whole lines); the remaining blocks rotate the rotary bands of
-//     REMAP pages (re-used whole pages) in place.
+// paged_data_kernel moves the data.  Its first blocks gather ASSEMBLE rows like the contiguous
+// kernel (rows laid end to end, one 16-byte chunk per thread, so a wavefront reads one row entry
+// and moves whole lines); the next blocks rotate the rotary bands of REMAP pages (re-used whole
+// pages) in place, each looking its pages up in the plan and the old block table.  The rows of a
+// small gather (token-slot splices: the replacement rows) are resolved by the gathering blocks
+// themselves and the new block tables and freed list are written by further blocks of the same
+// launch: one launch per call.  A large gather first runs paged_resolve_kernel, which expands the
+// page runs once for all layers and planes into a row table (for every row of every ASSEMBLE
+// page: which old physical page and row, or which replacement token, it comes from, which fresh
+// page it goes to, which shift re-anchors it) and writes the block tables and the freed list;
+// paged_order_kernel before it lays the row table out in destination-page order.
 // Nothing is written to an old page except the rotary bands of REMAP pages, which no ASSEMBLE
 // row reads.
 
@@ -679,20 +681,21 @@ __device__ __forceinline__ int32_t run_of(const KPageRun* runs, int32_t n, int32
     return lo;
 }
 
-__device__ __forceinline__ void resolve_remap_page(const KPagedParams& P, const PlanView& V, int32_t m) {
-    const KPageRun R = V.remap_runs[run_of(V.remap_runs, P.n_remap_runs, m)];
+// REMAP page m of run R (whose shift has cos/sin entry cs and whose sequence has new length
+// new_len): its physical page from the old block table and its valid rows (0 when the page is
+// out of the pool, which is flagged).
+__device__ __forceinline__ KRemapPage remap_entry(const KPagedParams& P, const KPageRun& R, int32_t cs,
+                                                  int32_t new_len, int32_t m) {
     const int32_t c = m - R.ord0;
-    const KSeqEntry S = V.seqs[R.seq];
-    const KDirEntry& D = V.dirs[R.dir];
-    KRemapPage e{0, D.cs, 0, 0};
+    KRemapPage e{0, cs, 0, 0};
     const int32_t pg = P.bt_in[int64_t(R.seq) * P.bt_stride + R.src0 + c];
     if (pg < 0 || pg >= P.capacity) {
         if (P.status) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
-    } else if (D.cs >= 0) {
+    } else if (cs >= 0) {
         e.page = pg;
-        e.rows = int32_t(min(int64_t(P.page_size), int64_t(S.new_len) - int64_t(R.k0 + c) * P.page_size));
+        e.rows = int32_t(min(int64_t(P.page_size), int64_t(new_len) - int64_t(R.k0 + c) * P.page_size));
     }
-    P.remap_pages[m] = e;
+    return e;
 }
 
 // New block-table entry i (sequence i / bt_stride, page i % bt_stride) from the page runs.
@@ -769,21 +772,9 @@ __global__ __launch_bounds__(ORDER_TPB) void paged_order_kernel(const KPagedPara
     for (int32_t t = tid; t < P.n_asm; t += ORDER_TPB) P.order[atomicAdd(&cnt[bucket(t)], 1)] = t;
 }
 
-// Threads [0, n_rows): ASSEMBLE rows, laid out in destination order when P.order is set; then
-// n_remap REMAP pages; then n_seqs * bt_stride block-table entries; then n_freed freed-list
-// entries.
-__global__ __launch_bounds__(TPB) void paged_resolve_kernel(const KPagedParams P) {
-    const PlanView V = plan_view(P);
-    int32_t i = int32_t(blockIdx.x) * TPB + int32_t(threadIdx.x);
-    if (i >= P.n_rows) {
-        i -= P.n_rows;
-        if (i < P.n_remap) { resolve_remap_page(P, V, i); return; }
-        i -= P.n_remap;
-        if (i < P.n_table) { resolve_table_entry(P, V, i); return; }
-        i -= P.n_table;
-        if (i < P.n_freed) resolve_freed_entry(P, V, i);
-        return;
-    }
+// ASSEMBLE row i (row i mod page_size of the (i / page_size)-th fresh page in destination order
+// when P.order is set, else in plan order): where it comes from, where it goes, its shift.
+__device__ __forceinline__ KRowMove row_entry(const KPagedParams& P, const PlanView& V, int32_t i) {
     const int32_t slot = i / P.page_size, r = i - slot * P.page_size;
     const int32_t task = P.order ? P.order[slot] : slot;               // fresh ordinal
     const KPageRun R = V.asm_runs[run_of(V.asm_runs, P.n_asm_runs, task)];
@@ -791,49 +782,62 @@ __global__ __launch_bounds__(TPB) void paged_resolve_kernel(const KPagedParams P
     const KSeqEntry S = V.seqs[seq];
     const int64_t q = int64_t(k) * P.page_size + r;
     KRowMove e{KROW_SKIP, 0, 0, r, -1, -1};
-    if (q < S.new_len) {
-        const int32_t fp = task < P.n_free ? P.free_pages[task] : -1;
-        if (fp < 0 || fp >= P.capacity) {
-            if (P.status) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
-        } else {
-            e.dst_page = fp;
-            // last directive of the sequence whose replacement starts at or before q
-            int32_t jlo = 0, jhi = S.dir_count;
-            while (jlo < jhi) {
-                const int32_t mid = (jlo + jhi) >> 1;
-                if (V.dirs[S.dir_begin + mid].stub_start <= q) jlo = mid + 1; else jhi = mid;
-            }
-            int64_t old = q;
-            if (jlo > 0) {
-                const int32_t j = S.dir_begin + jlo - 1;
-                const KDirEntry& D = V.dirs[j];
-                if (q < D.stub_start + D.stub_len) {
-                    e.src_page = KROW_STUB;
-                    e.src_row = int32_t(q - D.stub_start);
-                    e.dir = j;
-                    old = -1;
-                } else {
-                    old = q - D.delta;
-                    e.cs = D.cs;
-                }
-            }
-            if (old >= 0) {
-                const int32_t pg = P.bt_in[int64_t(seq) * P.bt_stride + old / P.page_size];
-                if (pg < 0 || pg >= P.capacity) {
-                    if (P.status) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
-                    e.src_page = KROW_SKIP;
-                } else {
-                    e.src_page = pg;
-                    e.src_row = int32_t(old % P.page_size);
-                }
-            }
-        }
+    if (q >= S.new_len) return e;
+    const int32_t fp = task < P.n_free ? P.free_pages[task] : -1;
+    if (fp < 0 || fp >= P.capacity) {
+        if (P.status) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
+        return e;
     }
-    P.rows[i] = e;
+    e.dst_page = fp;
+    // last directive of the sequence whose replacement starts at or before q
+    int32_t jlo = 0, jhi = S.dir_count;
+    while (jlo < jhi) {
+        const int32_t mid = (jlo + jhi) >> 1;
+        if (V.dirs[S.dir_begin + mid].stub_start <= q) jlo = mid + 1; else jhi = mid;
+    }
+    int64_t old = q;
+    if (jlo > 0) {
+        const int32_t j = S.dir_begin + jlo - 1;
+        const KDirEntry& D = V.dirs[j];
+        if (q < D.stub_start + D.stub_len) {
+            e.src_page = KROW_STUB;
+            e.src_row = int32_t(q - D.stub_start);
+            e.dir = j;
+            return e;
+        }
+        old = q - D.delta;
+        e.cs = D.cs;
+    }
+    const int32_t pg = P.bt_in[int64_t(seq) * P.bt_stride + old / P.page_size];
+    if (pg < 0 || pg >= P.capacity) {
+        if (P.status) atomicOr(P.status, int(LEYLINE_STATUS_BAD_PAGE));
+        e.src_page = KROW_SKIP;
+    } else {
+        e.src_page = pg;
+        e.src_row = int32_t(old % P.page_size);
+    }
+    return e;
 }
 
-// One workgroup of the ASSEMBLE gather (bx: its index among the gather's workgroups).
-template <int ESZ>
+// Entry w of the call's table work: the n_table new block-table entries, then the n_freed
+// freed-list entries.
+__device__ __forceinline__ void table_work(const KPagedParams& P, const PlanView& V, int64_t w) {
+    if (w < P.n_table) resolve_table_entry(P, V, int32_t(w));
+    else if (w - P.n_table < P.n_freed) resolve_freed_entry(P, V, int32_t(w - P.n_table));
+}
+
+// Large gathers: threads [0, n_rows) write the row table (in destination order when P.order is
+// set), the following ones the block tables and the freed list.
+__global__ __launch_bounds__(TPB) void paged_resolve_kernel(const KPagedParams P) {
+    const PlanView V = plan_view(P);
+    const int32_t i = int32_t(blockIdx.x) * TPB + int32_t(threadIdx.x);
+    if (i < P.n_rows) P.rows[i] = row_entry(P, V, i);
+    else table_work(P, V, int64_t(i) - P.n_rows);
+}
+
+// One workgroup of the ASSEMBLE gather (bx: its index among the gather's workgroups).  INLINE:
+// the rows are resolved here from the plan instead of read from the row table.
+template <int ESZ, bool INLINE>
 __device__ __forceinline__ void paged_move_block(const KPagedParams& P, const PlanView& V, int plane, int32_t bx,
                                                  KCosSin* lcs) {
     const KPlane& pl = P.planes[plane];
@@ -842,7 +846,7 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, const Pl
     const int32_t t = tb + int32_t(threadIdx.x);
     const int32_t i = fdiv(t, pl.tpr_div), u = t - i * pl.tpr;
     KRowMove e{KROW_SKIP, 0, 0, 0, -1, -1};
-    if (i < P.n_rows) e = P.rows[i];
+    if (i < P.n_rows) e = INLINE ? row_entry(P, V, i) : P.rows[i];
     const bool active = e.src_page != KROW_SKIP;
     // PAGED_LPT consecutive layers per thread: one row entry, all loads in flight before any store.
     const int layer0 = int(blockIdx.y) * PAGED_LPT;
@@ -875,7 +879,11 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, const Pl
             if (l < nl) v[l] = ld16(src + l * src_step + off);
     }
     // the cos/sin block of the workgroup's first row's shift, staged while the loads are in flight
-    const int32_t cs0 = pl.rot != KROT_NONE ? P.rows[fdiv(tb, pl.tpr_div)].cs : -1;
+    int32_t cs0 = -1;
+    if (pl.rot != KROT_NONE) {
+        const int32_t i0 = fdiv(tb, pl.tpr_div);
+        cs0 = INLINE ? row_entry(P, V, i0).cs : P.rows[i0].cs;
+    }
     if (cs0 >= 0) stage_cs<PAGED_TPB>(lcs, V.cs, cs0 + pl.cs_off, pl.n_pairs);
     __syncthreads();
     if (!active) return;
@@ -894,8 +902,8 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, const Pl
 
 // One workgroup of the REMAP rotation: band units of all valid rows of all REMAP pages laid end
 // to end, PAGED_LPT layers per thread, rotated in place.  The workgroup stages the cos/sin block
-// of its first page's shift in LDS; rows with another shift (where runs meet) read the table in
-// the workspace.
+// of its first page's shift in LDS; rows with another shift (where runs meet) read the plan's
+// table.
 template <int ESZ, bool NT>
 __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const PlanView& V, int plane, int32_t bx,
                                                   KCosSin* lcs) {
@@ -905,10 +913,27 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const P
     if (int64_t(tb) >= int64_t(P.n_remap) * upp) return;               // past this plane
     const int32_t t = tb + int32_t(threadIdx.x);
     const int32_t m = fdiv(t, P.remap_div[plane]);
-    const int32_t cs0 = P.remap_pages[fdiv(tb, P.remap_div[plane])].cs;   // block's first page
+    // the run of the block's first page (block-uniform; a single run comes with the parameters);
+    // a lane whose page lies past that run looks its own run up
+    KPageRun R0 = P.remap0;
+    int32_t next0 = INT32_MAX, cs0 = P.remap0_cs, len0 = P.remap0_len;
+    if (P.n_remap_runs > 1) {
+        const int32_t r0 = run_of(V.remap_runs, P.n_remap_runs, fdiv(tb, P.remap_div[plane]));
+        R0 = V.remap_runs[r0];
+        next0 = r0 + 1 < P.n_remap_runs ? V.remap_runs[r0 + 1].ord0 : INT32_MAX;
+        cs0 = V.dirs[R0.dir].cs;
+        len0 = V.seqs[R0.seq].new_len;
+    }
     bool active = m < P.n_remap;
     KRemapPage e{0, -1, 0, 0};
-    if (active) e = P.remap_pages[m];
+    if (active) {
+        if (m < next0) {
+            e = remap_entry(P, R0, cs0, len0, m);
+        } else {
+            const KPageRun R = V.remap_runs[run_of(V.remap_runs, P.n_remap_runs, m)];
+            e = remap_entry(P, R, V.dirs[R.dir].cs, V.seqs[R.seq].new_len, m);
+        }
+    }
     const int32_t f = t - m * upp;
     const int32_t r = fdiv(f, P.rot_div[plane]);
     active = active && r < e.rows;
@@ -926,10 +951,12 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const P
     else band_rotate_store<ESZ, NT>(pl, bp, row, pl.layer_stride, nl, x, y, V.cs, e.cs + pl.cs_off);
 }
 
-// The first workgroups gather ASSEMBLE rows (plane by plane), the rest rotate REMAP pages of the
-// planes in access class NT (plane by plane); planes without work get no workgroups.  SOLO: only
-// plane 0 has work in this launch, so no workgroup looks its plane up.
-template <int ESZ, bool NT, bool SOLO>
+// The first workgroups gather ASSEMBLE rows (plane by plane), the next rotate REMAP pages of the
+// planes in access class NT (plane by plane), the last P.table_x per layer group write the block
+// tables and the freed list; planes without work get no workgroups.  SOLO: only plane 0 has work
+// in this launch, so no workgroup looks its plane up.  INLINE: the gather resolves its rows (no
+// row table) and the launch may carry table work.
+template <int ESZ, bool NT, bool SOLO, bool INLINE>
 __global__ __launch_bounds__(PAGED_TPB) void paged_data_kernel(const KPagedParams P) {
     __shared__ KCosSin lcs[KMAX_CS];
     const PlanView V = plan_view(P);
@@ -937,11 +964,20 @@ __global__ __launch_bounds__(PAGED_TPB) void paged_data_kernel(const KPagedParam
     const int32_t moves = SOLO ? P.move_base[1] : P.move_base[P.n_planes];
     if (bx < moves) {
         const int p = SOLO ? 0 : plane_of(P.move_base, P.n_planes, bx);
-        paged_move_block<ESZ>(P, V, p, bx - P.move_base[p], lcs);
-    } else {
-        bx -= moves;
+        paged_move_block<ESZ, INLINE>(P, V, p, bx - P.move_base[p], lcs);
+        return;
+    }
+    bx -= moves;
+    const int32_t remaps = SOLO ? P.remap_base[1] : P.remap_base[P.n_planes];
+    if (bx < remaps) {
         const int p = SOLO ? 0 : plane_of(P.remap_base, P.n_planes, bx);
         paged_remap_block<ESZ, NT>(P, V, p, bx - P.remap_base[p], lcs);
+        return;
+    }
+    // table work, spread over the layer groups
+    if (INLINE) {
+        const int64_t b = int64_t(blockIdx.y) * P.table_x + (bx - remaps);
+        table_work(P, V, b * PAGED_TPB + threadIdx.x);
     }
 }
 
@@ -1237,6 +1273,22 @@ extern "C" int leyline_rotate_delta(const leyline_cache* cache, int64_t delta,
     return LEYLINE_OK;
 }
 
+// The paged data kernel variant for (dtype, access class, one plane only, inline rows).
+static int launch_paged_data(bool bf16, bool nt, bool solo, bool inl, dim3 grid, hipStream_t s,
+                             const KPagedParams& P) {
+    using K = void (*)(KPagedParams);
+    static const K table[2][2][2][2] = {
+        {{{paged_data_kernel<4, false, false, false>, paged_data_kernel<4, false, false, true>},
+          {paged_data_kernel<4, false, true, false>, paged_data_kernel<4, false, true, true>}},
+         {{paged_data_kernel<4, true, false, false>, paged_data_kernel<4, true, false, true>},
+          {paged_data_kernel<4, true, true, false>, paged_data_kernel<4, true, true, true>}}},
+        {{{paged_data_kernel<2, false, false, false>, paged_data_kernel<2, false, false, true>},
+          {paged_data_kernel<2, false, true, false>, paged_data_kernel<2, false, true, true>}},
+         {{paged_data_kernel<2, true, false, false>, paged_data_kernel<2, true, false, true>},
+          {paged_data_kernel<2, true, true, false>, paged_data_kernel<2, true, true, true>}}}};
+    return launch(table[bf16][nt][solo][inl], grid, s, P, PAGED_TPB);
+}
+
 extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, const int32_t* seq_lens,
                                     const int32_t* block_table_in, int32_t* block_table_out, int32_t bt_stride,
                                     const leyline_directive* dirs, int32_t n_dirs, uint32_t flags,
@@ -1273,6 +1325,7 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
     const KPagedTables& t = img.tables;
     char* ws = static_cast<char*>(workspace);
     if (int64_t(t.n_rows) + t.n_remap > INT32_MAX - 1024) return LEYLINE_E_INVAL;
+    const bool row_table = t.n_rows > KINLINE_ROWS;       // else the gather resolves its rows
     for (int p = 0; p < n_planes; ++p) {
         if (int64_t(t.n_rows) * planes[p].tpr > INT32_MAX - 1024) return LEYLINE_E_INVAL;
         if (int64_t(t.n_remap) * cache->page_size * planes[p].rot_tpr > INT32_MAX - 1024) return LEYLINE_E_INVAL;
@@ -1284,9 +1337,9 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         if (rc) return rc;
     }
     const int64_t n_table = int64_t(n_seqs) * bt_stride;
-    const int64_t n_resolve = int64_t(t.n_rows) + t.n_remap + n_table + t.n_freed;
-    if (n_resolve > INT32_MAX - 1024) return LEYLINE_E_INVAL;
-    if (n_resolve > 0) {
+    const int64_t n_tables = n_table + t.n_freed;          // block-table and freed-list entries
+    if (int64_t(t.n_rows) + n_tables > INT32_MAX - 1024) return LEYLINE_E_INVAL;
+    if (int64_t(t.n_rows) + t.n_remap + n_tables > 0) {
         KPagedParams P;
         std::memset(&P, 0, sizeof(P));
         std::memcpy(P.planes, planes, sizeof(planes));
@@ -1320,8 +1373,17 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         P.off_freed_runs = int32_t(t.off_freed_runs);
         P.n_asm_runs = t.n_asm_runs;
         P.n_remap_runs = t.n_remap_runs;
-        P.rows = reinterpret_cast<KRowMove*>(ws + t.off_rows);
-        P.remap_pages = reinterpret_cast<KRemapPage*>(ws + t.off_remap_pages);
+        P.rows = row_table ? reinterpret_cast<KRowMove*>(ws + t.off_rows) : nullptr;
+        if (t.n_remap_runs == 1) {
+            // the single REMAP run, its shift's cos/sin entry and its sequence's new length
+            std::memcpy(&P.remap0, img.bytes.data() + t.off_remap_runs, sizeof(KPageRun));
+            KDirEntry d;
+            std::memcpy(&d, img.bytes.data() + t.off_dir + int64_t(P.remap0.dir) * int64_t(sizeof(KDirEntry)), sizeof(d));
+            KSeqEntry q;
+            std::memcpy(&q, img.bytes.data() + t.off_seq + int64_t(P.remap0.seq) * int64_t(sizeof(KSeqEntry)), sizeof(q));
+            P.remap0_cs = d.cs;
+            P.remap0_len = q.new_len;
+        }
         P.bt_out = block_table_out;
         P.freed_out = freed_pages_out;
         P.n_table = int32_t(n_table);
@@ -1332,21 +1394,28 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         P.n_free = n_free;
         P.status = device_status;
         const bool bf16 = cache->dtype == LEYLINE_BF16;
-        if (t.n_asm >= KORDER_MIN) {
-            int32_t shift = 0;
-            while (((cache->capacity - 1) >> shift) >= KORDER_BUCKETS) ++shift;
-            P.order_shift = shift;
-            P.order = reinterpret_cast<int32_t*>(ws + t.off_order);
-            rc = launch(paged_order_kernel, dim3(1), s, P, ORDER_TPB);
+        const unsigned layer_groups = unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT);
+        if (row_table) {
+            if (t.n_asm >= KORDER_MIN) {
+                int32_t shift = 0;
+                while (((cache->capacity - 1) >> shift) >= KORDER_BUCKETS) ++shift;
+                P.order_shift = shift;
+                P.order = reinterpret_cast<int32_t*>(ws + t.off_order);
+                rc = launch(paged_order_kernel, dim3(1), s, P, ORDER_TPB);
+                if (rc) return rc;
+            }
+            rc = launch(paged_resolve_kernel, dim3(unsigned((int64_t(t.n_rows) + n_tables + TPB - 1) / TPB)), s, P);
             if (rc) return rc;
+        } else {
+            // the first data launch writes the tables, spread over its layer groups
+            P.table_x = int32_t(((n_tables + PAGED_TPB - 1) / PAGED_TPB + layer_groups - 1) / layer_groups);
         }
-        rc = launch(paged_resolve_kernel, dim3(unsigned((n_resolve + TPB - 1) / TPB)), s, P);
-        if (rc) return rc;
         // data kernel: gather workgroups, then REMAP workgroups, once per access class of the
         // rotary planes; the gather goes with the first class that has REMAP work (or alone)
         int gather_class = 1;
         if (t.n_remap > 0 && !any_band[1] && any_band[0]) gather_class = 0;
-        const dim3 layers(1, unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT), 1);
+        const dim3 layers(1, layer_groups, 1);
+        bool tables_pending = P.table_x > 0;
         for (int nt = 1; nt >= 0; --nt) {
             int64_t mb = 0, rb = 0;
             P.move_base[0] = P.remap_base[0] = 0;
@@ -1360,19 +1429,13 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
                 P.move_base[p + 1] = int32_t(mb);
                 P.remap_base[p + 1] = int32_t(rb);
             }
-            if (mb + rb == 0) continue;
-            const dim3 grid(unsigned(mb + rb), layers.y, 1);
+            // the table work goes with the first launch, or alone in the last pass
+            if (mb + rb == 0 && !(tables_pending && nt == 0)) continue;
+            if (!tables_pending) P.table_x = 0;
+            tables_pending = false;
+            const dim3 grid(unsigned(mb + rb + P.table_x), layers.y, 1);
             const bool solo = P.move_base[1] == mb && P.remap_base[1] == rb;   // plane 0 only
-            if (nt)
-                rc = solo ? (bf16 ? launch(paged_data_kernel<2, true, true>, grid, s, P, PAGED_TPB)
-                                  : launch(paged_data_kernel<4, true, true>, grid, s, P, PAGED_TPB))
-                          : (bf16 ? launch(paged_data_kernel<2, true, false>, grid, s, P, PAGED_TPB)
-                                  : launch(paged_data_kernel<4, true, false>, grid, s, P, PAGED_TPB));
-            else
-                rc = solo ? (bf16 ? launch(paged_data_kernel<2, false, true>, grid, s, P, PAGED_TPB)
-                                  : launch(paged_data_kernel<4, false, true>, grid, s, P, PAGED_TPB))
-                          : (bf16 ? launch(paged_data_kernel<2, false, false>, grid, s, P, PAGED_TPB)
-                                  : launch(paged_data_kernel<4, false, false>, grid, s, P, PAGED_TPB));
+            rc = launch_paged_data(bf16, nt != 0, solo, !row_table, grid, s, P);
             if (rc) return rc;
         }
     }

@@ -262,8 +262,8 @@ struct KRowMove {
 constexpr int32_t KROW_STUB = -1;
 constexpr int32_t KROW_SKIP = -2;
 
-// One REMAP page, resolved on the device: its physical page, the cos/sin entry of its shift and
-// the number of valid rows (0: nothing to rotate).
+// One REMAP page, resolved on the device by the workgroups that rotate it: its physical page, the
+// cos/sin entry of its shift and the number of valid rows (0: nothing to rotate).
 struct KRemapPage {
     int32_t page, cs, rows, pad;
 };
@@ -271,9 +271,9 @@ struct KRemapPage {
 // Byte offsets of the tables inside the workspace (converted to pointers at launch).
 struct KPagedTables {
     int64_t off_seq, off_dir, off_cs, off_runs, off_asm_runs, off_remap_runs, off_freed_runs;
-    int64_t off_rows, off_remap_pages, off_order;
+    int64_t off_rows, off_order;
     int64_t upload;          // bytes uploaded from the host (the tables before the row tables)
-    int64_t total;           // workspace bytes (the row tables are written on the device)
+    int64_t total;           // workspace bytes (the row table is written on the device)
     int32_t n_seqs, n_dirs, n_cs, n_runs, n_asm_runs, n_remap_runs, n_freed_runs;
     int32_t n_asm, n_remap, n_freed, bt_stride;
     int32_t n_rows;          // n_asm * page_size
@@ -303,11 +303,11 @@ struct KPagedParams {
     const int32_t* bt_in;
     const int32_t* free_pages;
     int32_t n_free;
-    int32_t pad;
+    int32_t table_x;         // data kernel: workgroups per layer group writing the block tables and
+                             // the freed list (0: the resolve kernel writes them)
     int32_t* status;
-    KRowMove* rows;          // workspace, n_rows entries
-    KRemapPage* remap_pages; // workspace, n_remap entries
-    // block tables and freed list (resolve kernel)
+    KRowMove* rows;          // workspace, n_rows entries (null: the gather resolves rows itself)
+    // block tables and freed list
     int32_t* bt_out;
     int32_t* freed_out;
     int32_t n_table;         // n_seqs * bt_stride
@@ -319,8 +319,16 @@ struct KPagedParams {
                                                  // from 0 after the gather's
     int32_t pad1;
     int32_t* order;          // workspace, n_asm fresh ordinals in destination-page order (or null)
+    // the only REMAP run when n_remap_runs == 1, with its shift's cos/sin entry and its sequence's
+    // new length (read with the other parameters, one level of loads before the block table)
+    KPageRun remap0;
+    int32_t remap0_cs, remap0_len;
     alignas(16) unsigned char blob[KPLAN_INLINE];
 };
+
+// A call assembling at most this many rows gathers them without a row table: each gathering
+// workgroup resolves its rows from the plan, and the whole call is one data launch.
+constexpr int32_t KINLINE_ROWS = 1024;
 
 // The gather is ordered by destination page (neighbouring physical pages processed together)
 // when a call assembles at least this many pages; KORDER_BUCKETS buckets of pages, counted in LDS.

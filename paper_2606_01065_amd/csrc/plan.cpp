@@ -619,10 +619,10 @@ int build_paged_image(const leyline_cache* cache, const PagedPlan& plan, int32_t
     t.upload = (off + 15) / 16 * 16;
     const int64_t n_rows = int64_t(plan.n_fresh) * plan.page_size;
     if (n_rows > INT32_MAX) return LEYLINE_E_CAPACITY;
-    // the tables the kernels write
-    t.off_rows = place(size_t(n_rows) * sizeof(KRowMove), 256);
-    t.off_remap_pages = place(size_t(plan.n_remap) * sizeof(KRemapPage), 256);
-    t.off_order = place(plan.n_fresh >= KORDER_MIN ? size_t(plan.n_fresh) * sizeof(int32_t) : 0, 256);
+    // the tables the kernels write: the row table (and its destination order) of a large gather
+    const bool row_table = n_rows > KINLINE_ROWS;
+    t.off_rows = place(row_table ? size_t(n_rows) * sizeof(KRowMove) : 0, 256);
+    t.off_order = place(row_table && plan.n_fresh >= KORDER_MIN ? size_t(plan.n_fresh) * sizeof(int32_t) : 0, 256);
     t.total = (off + 255) / 256 * 256;
     t.n_seqs = n_seqs; t.n_dirs = n_dirs; t.n_cs = int32_t(cs.size());
     t.n_runs = int32_t(plan.runs.size());
