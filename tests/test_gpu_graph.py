@@ -77,3 +77,30 @@ def test_rotate_delta_in_a_graph(L):
     torch.cuda.synchronize()
     eager = host(t)
     _replay_and_compare(lambda: L.leyline_rotate_delta(cache, -4064, row0=100, n_rows=1500), t, pristine, eager)
+
+
+def test_paged_slot_splice_in_a_graph(L):
+    """A paged splice whose plan fits the kernel arguments (one sequence, one directive) and whose
+    gather is small enqueues one kernel: token-slot cache, REMAP rotation in place plus the stub
+    rows; the block table and freed list are outputs of the same launch."""
+    wl = W.Workload("graph_slots", 2, "bf16", [W.mla_plane()], [W.Dir(300, 420, 24)], [1500], page_size=1, seed=33)
+    pools, bt, free, stubs = W.alloc_paged(wl, DEV)
+    t = pools[0]
+    pristine = t.clone()
+    cache = L.make_cache([L.PlaneSpec(t, 1, 576, 512, 64, L.ROPE_INTERLEAVED, 10000.0)], paged=True)
+    d = wl.dirs[0]
+    dirs = L.make_directives([dict(span_start=d.span_start, span_end=d.span_end, stub=stubs[0], stub_len=d.stub_len)])
+    new_lens, fresh, n_freed, ws_bytes = L.leyline_paged_query(cache, wl.seq_lens, bt.shape[1], dirs, 1)
+    bt_out = torch.full_like(bt, -7)
+    freed = torch.full((max(1, n_freed),), -7, dtype=torch.int32, device=DEV)
+    ws = torch.empty(max(256, ws_bytes), dtype=torch.uint8, device=DEV)
+    run = lambda: L.leyline_splice_paged(cache, wl.seq_lens, bt, bt_out, dirs, 1, free, freed, ws)
+    print(f"[case] graph paged slots ws={ws_bytes} freed={n_freed} fresh={fresh}", flush=True)
+    run()
+    torch.cuda.synchronize()
+    eager, eager_bt, eager_freed = host(t), host(bt_out), host(freed)
+    assert not np.array_equal(eager, host(pristine))
+    bt_out.fill_(-7)
+    freed.fill_(-7)
+    _replay_and_compare(run, t, pristine, eager)
+    assert np.array_equal(host(bt_out), eager_bt) and np.array_equal(host(freed), eager_freed)
