@@ -291,7 +291,8 @@ def setup_paged(wl, dev, L, W, specs, stream):
     keep = dict(paged=True)
     torch.cuda.synchronize()
     # one data launch per splice (gather of assembled pages and in-place rotation of remapped
-    # ones) carries the bytes; the resolve launch before it is inside the timed splice
+    # ones) carries the bytes; the order and resolve launches of large gathers are inside the
+    # timed splice
     return step, kernel, alg_bytes, moved, 1, keep
 
 
