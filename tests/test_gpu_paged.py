@@ -149,6 +149,36 @@ def test_forget_and_copy_on_write_whole_pool(L, kind):
                     assert np.array_equal(got[:, old_pages], before[pi][:, old_pages])
 
 
+@pytest.mark.parametrize("kind", ["mla", "gqa"])
+@pytest.mark.parametrize("last_stub", [256, 257])
+def test_inline_and_row_table_gathers(L, kind, last_stub):
+    """Token-slot cache, four directives: the downstream slots form four REMAP runs whose
+    boundaries fall inside workgroups, and the replacements total 1024 rows (gathered without a
+    row table, one launch) or 1025 (row table); whole pool against the oracle."""
+    dirs = [W.Dir(500, 600, 256), W.Dir(1500, 1510, 256), W.Dir(2500, 2700, 256), W.Dir(4000, 4001, last_stub)]
+    planes = [W.mla_plane()] if kind == "mla" else W.gqa_planes(heads=2, dim=128)
+    wl = W.Workload(f"slots_{kind}", 2, "bf16", planes, dirs, [5000], page_size=1, seed=61 + last_stub)
+    plans = O.plan_paged(wl.seq_lens, _odirs(wl), 1)
+    assert sum(k == O.ASSEMBLE for k in plans[0].kinds) == 768 + last_stub
+    print(f"[case] slots {kind} gather rows={768 + last_stub}", flush=True)
+    pools, bt, free, stubs = W.alloc_paged(wl, DEV, spare_pages=3)
+    before = [host(p) for p in pools]
+    bt_h, free_h = host(bt), host(free)
+    stubs_h = [[host(s).reshape(wl.n_layers, s.shape[1], p.row_elems) for s, p in zip(per, wl.planes)]
+               for per in stubs]
+    bt_out, freed, new_lens = _run_gpu(L, wl, pools, bt, free, stubs)
+    oplanes = [oracle_plane(p) for p in wl.planes]
+    flat = [b.reshape(b.shape[0], b.shape[1], b.shape[2], -1) for b in before]
+    want, want_bt, want_lens, want_freed = O.splice_paged(
+        flat, oplanes, "bf16", bt_h, wl.seq_lens, _odirs(wl), stubs_h, list(free_h), 1)
+    assert new_lens == want_lens
+    assert np.array_equal(host(bt_out), want_bt)
+    assert list(host(freed)) == want_freed
+    for pi, plane in enumerate(oplanes):
+        got = host(pools[pi]).reshape(want[pi].shape)
+        assert_rows_match(got, want[pi], plane, "bf16", what=f"slots {kind} plane {pi}")
+
+
 @pytest.mark.parametrize("kind,dtype", [("mla", "bf16"), ("gqa", "bf16"), ("mla", "f32"),
                                         ("mla_neox", "bf16")])
 def test_token_slot_paged_whole_pool(L, kind, dtype):
