@@ -149,6 +149,57 @@ def test_forget_and_copy_on_write_whole_pool(L, kind):
                     assert np.array_equal(got[:, old_pages], before[pi][:, old_pages])
 
 
+def test_out_of_pool_pages_are_flagged_and_skipped(L):
+    """A block-table entry of a REMAP page and the first free-list entry point outside the pool:
+    the kernels flag LEYLINE_STATUS_BAD_PAGE and skip that page's rows; every other page equals
+    the oracle's result on the uncorrupted inputs, and the two skipped destinations keep their
+    contents."""
+    P = 4
+    dirs = [W.Dir(8, 12, 0, seq=0), W.Dir(10, 13, 1, seq=1)]     # seq 0: shift -4 (REMAP); seq 1: -2
+    wl = W.Workload("bad_pages", 2, "bf16", [W.mla_plane()], dirs, [40, 40], page_size=P, seed=77)
+    pools, bt, free, stubs = W.alloc_paged(wl, DEV, spare_pages=3)
+    before = host(pools[0])
+    bt_h, free_h = host(bt), host(free)
+    plans = O.plan_paged(wl.seq_lens, _odirs(wl), P)
+    assert plans[0].kinds[4] == O.REMAP and plans[0].sources[4] == 5
+    assert O.ASSEMBLE in plans[1].kinds
+    cap = pools[0].shape[1]
+    remap_page, fresh_page = int(bt_h[0, 5]), int(free_h[0])
+    bad_bt, bad_free = bt.clone(), free.clone()
+    bad_bt[0, 5] = cap + 7
+    bad_free[0] = -5
+    print(f"[case] out-of-pool pages: remap page {remap_page} -> {cap + 7}, fresh page {fresh_page} -> -5",
+          flush=True)
+    specs = [L.PlaneSpec(pools[0], 1, 576, 512, 64, L.ROPE_INTERLEAVED, 10000.0)]
+    cache = L.make_cache(specs, paged=True)
+    ldirs = L.make_directives([dict(span_start=d.span_start, span_end=d.span_end, stub=stubs[j], seq=d.seq,
+                                    stub_len=d.stub_len) for j, d in enumerate(wl.dirs)])
+    new_lens, fresh, n_freed, ws_bytes = L.leyline_paged_query(cache, wl.seq_lens, bt.shape[1], ldirs, 2)
+    bt_out = torch.full_like(bt, -7)
+    freed = torch.full((max(1, n_freed),), -7, dtype=torch.int32, device=DEV)
+    ws = torch.empty(max(256, ws_bytes), dtype=torch.uint8, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    L.leyline_splice_paged(cache, wl.seq_lens, bad_bt, bt_out, ldirs, 2, bad_free, freed, ws, device_status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == L.STATUS_BAD_PAGE
+    stubs_h = [[host(s).reshape(wl.n_layers, s.shape[1], 576) for s in per] for per in stubs]
+    plane = oracle_plane(wl.planes[0])
+    want, want_bt, _, _ = O.splice_paged([before.reshape(before.shape[0], before.shape[1], P, -1)], [plane], "bf16",
+                                         bt_h, wl.seq_lens, _odirs(wl), stubs_h, list(free_h), P)
+    got = host(pools[0]).reshape(want[0].shape)
+    skipped = [remap_page, fresh_page]
+    keep = [pg for pg in range(cap) if pg not in skipped]
+    assert_rows_match(got[:, keep], want[0][:, keep], plane, "bf16", what="pages with valid indices")
+    b = before.reshape(got.shape)
+    assert np.array_equal(got[:, skipped], b[:, skipped])
+    got_bt = host(bt_out)
+    assert got_bt[0, 4] == cap + 7                 # tables carry the entries they were given
+    want_bt = want_bt.copy()
+    want_bt[0, 4] = cap + 7
+    want_bt[want_bt == fresh_page] = -5
+    assert np.array_equal(got_bt, want_bt)
+
+
 @pytest.mark.parametrize("kind", ["mla", "gqa"])
 @pytest.mark.parametrize("last_stub", [256, 257])
 def test_inline_and_row_table_gathers(L, kind, last_stub):
