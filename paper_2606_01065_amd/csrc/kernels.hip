@@ -362,6 +362,23 @@ __device__ __forceinline__ void stage_cs(KCosSin* lcs, const KCosSin* table, int
     for (int i = threadIdx.x; i < n; i += NT) lcs[i] = table[c0 + i];
 }
 
+// The same staging split around a thread's data loads (one entry per thread, n <= block size):
+// cs_fetch before the data loads are issued, cs_commit after.  Vector loads complete in order,
+// so the wait before the LDS write then covers the cos/sin load only, and the barrier that
+// follows does not wait for any wavefront's data.
+template <class Ptr>
+__device__ __forceinline__ uint64_t cs_fetch(Ptr table, int32_t c0, int32_t n) {
+    uint64_t c = 0;     // one 64-bit value: merges with the default without a copy
+    if (int(threadIdx.x) < n) {
+        const KCosSin e = table[c0 + threadIdx.x];
+        c = uint64_t(__float_as_uint(e.c)) | (uint64_t(__float_as_uint(e.s)) << 32);
+    }
+    return c;
+}
+__device__ __forceinline__ void cs_commit(KCosSin* lcs, uint64_t c, int32_t n) {
+    if (int(threadIdx.x) < n) *reinterpret_cast<uint64_t*>(lcs + threadIdx.x) = c;
+}
+
 // --------------------------------------------------------------------- contiguous splice ---
 
 // Rounds and replacement copies: rows laid end to end, one unit per thread for CRPT rows (the
@@ -417,6 +434,8 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
         const int64_t r = min(r0 + k, I.count - 1);
         v[k] = ld16(src + r * src_step + off);
     }
+    // staged after the data loads are issued (staging split around them, as the paged kernels
+    // do, measured 1 point slower on the GQA cache here)
     for (int i = threadIdx.x; i < pl.n_pairs; i += MOVE_TPB) lcs[i] = P.cs[I.cs + i];
     __syncthreads();
     if (!active) return;
@@ -621,9 +640,11 @@ __global__ __launch_bounds__(PAGED_TPB) void rotate_rows_kernel(const KRotatePar
         r += row * pl.token_stride;
     }
     const BandPos bp = band_pos(pl, q);
+    static_assert(KMAX_CS <= PAGED_TPB, "one cos/sin entry per thread");
+    const uint64_t c = cs_fetch(P.cs, pl.cs_off, pl.n_pairs);
     u32x4 x[PAGED_LPT], y[PAGED_LPT];
     if (active) band_load<NT>(bp, r, pl.layer_stride, nl, x, y);
-    stage_cs<PAGED_TPB>(lcs, P.cs, pl.cs_off, pl.n_pairs);
+    cs_commit(lcs, c, pl.n_pairs);
     __syncthreads();
     if (!active) return;
     band_rotate_store<ESZ, NT>(pl, bp, r, pl.layer_stride, nl, x, y, lcs, 0);
@@ -659,9 +680,13 @@ struct PlanView {
 // The kernel's only argument is a KPagedParams at the start of the kernel-argument segment, so an
 // inline plan sits at that segment's address plus the offset of `blob` (the address of the
 // argument itself is not taken, which would make the compiler copy it into private memory).
+// Both places are global device memory; saying so lets the compiler read the tables with
+// global loads instead of flat ones (a flat load can only be waited for together with every
+// earlier memory access).
 __device__ __forceinline__ PlanView plan_view(const KPagedParams& P) {
-    const char* kernarg = (const char*)__builtin_amdgcn_kernarg_segment_ptr();
-    const char* b = P.plan ? P.plan : kernarg + offsetof(KPagedParams, blob);
+    using G = const __attribute__((address_space(1))) char*;
+    const G kernarg = (G)(const char*)__builtin_amdgcn_kernarg_segment_ptr();
+    const char* b = (const char*)(P.plan ? (G)P.plan : kernarg + offsetof(KPagedParams, blob));
     return PlanView{reinterpret_cast<const KSeqEntry*>(b + P.off_seq),
                     reinterpret_cast<const KDirEntry*>(b + P.off_dir),
                     reinterpret_cast<const KCosSin*>(b + P.off_cs),
@@ -798,7 +823,7 @@ __device__ __forceinline__ KRowMove row_entry(const KPagedParams& P, const PlanV
     int64_t old = q;
     if (jlo > 0) {
         const int32_t j = S.dir_begin + jlo - 1;
-        const KDirEntry& D = V.dirs[j];
+        const KDirEntry D = V.dirs[j];
         if (q < D.stub_start + D.stub_len) {
             e.src_page = KROW_STUB;
             e.src_row = int32_t(q - D.stub_start);
@@ -848,13 +873,20 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, const Pl
     KRowMove e{KROW_SKIP, 0, 0, 0, -1, -1};
     if (i < P.n_rows) e = INLINE ? row_entry(P, V, i) : P.rows[i];
     const bool active = e.src_page != KROW_SKIP;
+    // the cos/sin block of the workgroup's first row's shift, fetched before the data loads
+    int32_t cs0 = -1;
+    if (pl.rot != KROT_NONE) {
+        const int32_t i0 = fdiv(tb, pl.tpr_div);
+        cs0 = INLINE ? row_entry(P, V, i0).cs : P.rows[i0].cs;
+    }
+    const uint64_t c = cs_fetch(V.cs, cs0 + pl.cs_off, cs0 >= 0 ? pl.n_pairs : 0);
     // PAGED_LPT consecutive layers per thread: one row entry, all loads in flight before any store.
     const int layer0 = int(blockIdx.y) * PAGED_LPT;
     const int nl = min(PAGED_LPT, P.n_layers - layer0);
     const char* src;
     int64_t src_step;
     if (e.src_page == KROW_STUB) {
-        const KDirEntry& D = V.dirs[e.dir];
+        const KDirEntry D = V.dirs[e.dir];
         src_step = D.stub_len * pl.row_bytes;
         src = D.stub[plane] + int64_t(layer0) * src_step + int64_t(e.src_row) * pl.row_bytes;
     } else {
@@ -878,13 +910,7 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, const Pl
         for (int l = 0; l < PAGED_LPT; ++l)
             if (l < nl) v[l] = ld16(src + l * src_step + off);
     }
-    // the cos/sin block of the workgroup's first row's shift, staged while the loads are in flight
-    int32_t cs0 = -1;
-    if (pl.rot != KROT_NONE) {
-        const int32_t i0 = fdiv(tb, pl.tpr_div);
-        cs0 = INLINE ? row_entry(P, V, i0).cs : P.rows[i0].cs;
-    }
-    if (cs0 >= 0) stage_cs<PAGED_TPB>(lcs, V.cs, cs0 + pl.cs_off, pl.n_pairs);
+    cs_commit(lcs, c, cs0 >= 0 ? pl.n_pairs : 0);
     __syncthreads();
     if (!active) return;
     const bool rot = cs >= 0 && pl.rot != KROT_NONE;
@@ -924,6 +950,7 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const P
         cs0 = V.dirs[R0.dir].cs;
         len0 = V.seqs[R0.seq].new_len;
     }
+    const uint64_t c = cs_fetch(V.cs, cs0 + pl.cs_off, cs0 >= 0 ? pl.n_pairs : 0);
     bool active = m < P.n_remap;
     KRemapPage e{0, -1, 0, 0};
     if (active) {
@@ -944,7 +971,7 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const P
     const BandPos bp = band_pos(pl, f - r * pl.rot_tpr);
     u32x4 x[PAGED_LPT], y[PAGED_LPT];
     if (active) band_load<NT>(bp, row, pl.layer_stride, nl, x, y);
-    if (cs0 >= 0) stage_cs<PAGED_TPB>(lcs, V.cs, cs0 + pl.cs_off, pl.n_pairs);
+    cs_commit(lcs, c, cs0 >= 0 ? pl.n_pairs : 0);
     __syncthreads();
     if (!active) return;
     if (e.cs == cs0) band_rotate_store<ESZ, NT>(pl, bp, row, pl.layer_stride, nl, x, y, lcs, 0);
