@@ -27,7 +27,9 @@ sys.path.insert(0, ROOT)
 
 METRIC = "re-anchored KV tokens/sec and achieved HBM GB/s (% of peak) per splice"
 PEAK_HBM_GBPS = 8000.0
-KERNEL_SRC = os.path.join(ROOT, "paper_2606_01065_amd", "csrc", "kernels.hip")
+# the sources of the device code and of the planning that shapes its launches
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_01065_amd", "csrc", f)
+                  for f in ("kernels.hip", "kparams.hpp", "plan.hpp", "plan.cpp")]
 PROFILES = os.path.join(ROOT, "profiles")
 CONTIG_KERNEL = "contig_move_kernel"
 CONTIG_TILE_KERNEL = "contig_tile_kernel"
@@ -52,8 +54,17 @@ def parse():
 
 
 def kernel_sha():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Identity of the code that the counter runs measured: sha256 of the kernel and planning
+    sources with comments and blank lines removed, so that comment edits keep them valid (the
+    sources use line comments only and no "//" inside string literals)."""
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, encoding="utf-8") as f:
+            for line in f:
+                code = line.split("//", 1)[0].strip()
+                if code:
+                    h.update(code.encode() + b"\n")
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(workload):

@@ -7,7 +7,8 @@
 // (a c - b s, a s + b c)) is applied in registers between the load and the store of a moved
 // row, with the result rounded to bf16 by the hardware's round-to-nearest-even conversion.
 // cos/sin of (shift * theta_i) come from the host, evaluated in fp64 once per call and shift,
-// and are staged once per workgroup in LDS.
+// travel in the kernel arguments (or the call's workspace) and are staged once per workgroup in
+// LDS.
 //
 // Access shape.  One thread moves one 16-byte chunk, and the chunks of the moved rows are laid
 // end to end over the threads, so every load and store instruction of a 64-wide wavefront
@@ -20,9 +21,13 @@
 // content of row x + m.  The host splits the segment into equal rounds of at most m rows taken
 // in ascending order (descending for a right shift): inside a round sources and destinations
 // are disjoint, and every row a round overwrites was read by an earlier round, so consecutive
-// launches on one stream order the whole move.  Shifts so small that this would need many
-// rounds use ordered chains instead: chain c owns rows c, c+m, c+2m, ... and one thread walks it
-// in order, overwriting only rows it has already read itself.
+// launches on one stream order the whole move.  When some shift of a call is too small for a
+// few large rounds, the whole call (every move and replacement copy) runs as ordered tiles:
+// workgroups take tickets in start order and wait on per-tile "source read" flags, so that no
+// tile overwrites rows another tile has still to read (contig_tile_kernel).  Layouts whose
+// half-split partners cannot be exchanged between lanes use ordered chains instead: chain c owns
+// rows c, c+m, c+2m, ... and one thread walks it in order, overwriting only rows it has already
+// read itself.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -465,7 +470,8 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
     }
 }
 
-// Ordered chains (shifts too small for rounds): thread (chain c, unit u) walks rows c, c+m, ...
+// Ordered chains (shifts too small for rounds, on layouts whose half-split partners cannot be
+// exchanged between lanes, so tiles are not used): thread (chain c, unit u) walks rows c, c+m, ...
 template <int ESZ>
 __global__ __launch_bounds__(TPB) void contig_chain_kernel(const KContigParams P) {
     const KItem& I = P.items[blockIdx.z];
@@ -525,9 +531,9 @@ __global__ __launch_bounds__(TPB) void contig_chain_kernel(const KContigParams P
 //
 // A tile loads its whole source into registers, waits until those loads have returned and (a
 // move) publishes "source read".  Before storing it waits for every tile whose source rows its
-// destination overlaps (tile_wait_flags), so no tile reads a chunk another tile has written.  A tile waits only
-// for tickets taken before its own, by workgroups that publish before they wait, so every wait
-// ends.
+// destination overlaps (tile_wait_flags), so no tile reads a chunk another tile has written.
+// A tile waits only for tickets taken before its own, by workgroups that publish before they
+// wait, so every wait ends.
 //
 // ROT: the rotary style of every re-anchored item of the launch (KROT_NONE: looked up per item),
 // so that the style this launch does not use costs no registers.
@@ -680,9 +686,9 @@ struct PlanView {
 // The kernel's only argument is a KPagedParams at the start of the kernel-argument segment, so an
 // inline plan sits at that segment's address plus the offset of `blob` (the address of the
 // argument itself is not taken, which would make the compiler copy it into private memory).
-// Both places are global device memory; saying so lets the compiler read the tables with
-// global loads instead of flat ones (a flat load can only be waited for together with every
-// earlier memory access).
+// Both places are global device memory: the pointer is formed in the global address space so
+// that the compiler reads the tables with global loads instead of flat ones (a flat load can
+// only be waited for together with every earlier memory access).
 __device__ __forceinline__ PlanView plan_view(const KPagedParams& P) {
     using G = const __attribute__((address_space(1))) char*;
     const G kernarg = (G)(const char*)__builtin_amdgcn_kernarg_segment_ptr();
