@@ -7,6 +7,7 @@
 #include <climits>
 #include <cmath>
 #include <cstring>
+#include <map>
 
 namespace leyline {
 
@@ -210,7 +211,7 @@ int plan_tiles(const leyline_cache* cache, const leyline_directive* dirs, const 
     for (size_t k = 0; k < order.size(); ++k) order[k] = k;
     std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return level[a] < level[b]; });
     const bool any_rot = cos_sin_per_shift(cache) > 0;
-    std::vector<std::pair<int64_t, int32_t>> shift_cs;      // shift -> first entry of its block
+    std::map<int64_t, int32_t> shift_cs;                     // shift -> first entry of its block
     int64_t n_flags = 0;
     TileLaunchHost cur;
     out->tiles = true;
@@ -223,11 +224,12 @@ int plan_tiles(const leyline_cache* cache, const leyline_directive* dirs, const 
         }
         int32_t cs0 = -1;
         if (move && any_rot) {
-            for (const auto& e : shift_cs)
-                if (e.first == x.delta) cs0 = e.second;
-            if (cs0 < 0) {
+            const auto found = shift_cs.find(x.delta);
+            if (found != shift_cs.end()) {
+                cs0 = found->second;
+            } else {
                 cs0 = append_cos_sin(cache, x.delta, out->cs);
-                shift_cs.emplace_back(x.delta, cs0);
+                shift_cs.emplace(x.delta, cs0);
             }
         }
         for (int p = 0; p < n_planes; ++p) {
@@ -323,25 +325,46 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
 
     // Job a must finish before job b when b writes a row that a reads.  The resulting graph is
     // acyclic: a left-moving segment can only wait for segments to its left, a right-moving one
-    // only for segments to its right, and a stub only for moves.
+    // only for segments to its right, and a stub only for moves.  The destinations of all jobs
+    // are disjoint intervals, and so are the sources of the moves: one sweep over both, sorted by
+    // start, meets every overlapping (source, destination) pair, at most one per interval of
+    // either list.  A job's level is the length of the longest chain of jobs before it.
     const size_t n = jobs.size();
     auto dst_lo = [&](const ContigJobHost& x) { return x.kind == KJOB_STUB ? x.dst0 : x.src0 + x.delta; };
-    std::vector<int> level(n, 0);
-    for (size_t iter = 0; iter < n; ++iter) {
-        bool changed = false;
-        for (size_t b = 0; b < n; ++b) {
-            const int64_t blo = dst_lo(jobs[b]), bhi = blo + jobs[b].count;
-            for (size_t a = 0; a < n; ++a) {
-                if (a == b || jobs[a].kind == KJOB_STUB) continue;
-                const int64_t alo = jobs[a].src0, ahi = alo + jobs[a].count;
-                if (blo < ahi && alo < bhi && level[b] < level[a] + 1) {
-                    level[b] = level[a] + 1;
-                    changed = true;
-                }
-            }
-        }
-        if (!changed) break;
+    std::vector<size_t> by_dst(n), by_src;
+    for (size_t k = 0; k < n; ++k) {
+        by_dst[k] = k;
+        if (jobs[k].kind != KJOB_STUB) by_src.push_back(k);
     }
+    std::sort(by_dst.begin(), by_dst.end(), [&](size_t a, size_t b) { return dst_lo(jobs[a]) < dst_lo(jobs[b]); });
+    std::sort(by_src.begin(), by_src.end(), [&](size_t a, size_t b) { return jobs[a].src0 < jobs[b].src0; });
+    std::vector<std::vector<size_t>> succ(n);
+    std::vector<int> indeg(n, 0);
+    for (size_t i = 0, j = 0; i < by_dst.size() && j < by_src.size();) {
+        const size_t b = by_dst[i], a = by_src[j];
+        const int64_t blo = dst_lo(jobs[b]), bhi = blo + jobs[b].count;
+        const int64_t alo = jobs[a].src0, ahi = alo + jobs[a].count;
+        if (a != b && blo < ahi && alo < bhi) {
+            succ[a].push_back(b);
+            ++indeg[b];
+        }
+        if (bhi < ahi) ++i; else ++j;
+    }
+    std::vector<int> level(n, 0);
+    std::vector<size_t> ready;
+    for (size_t k = 0; k < n; ++k)
+        if (indeg[k] == 0) ready.push_back(k);
+    size_t done = 0;
+    while (!ready.empty()) {
+        const size_t a = ready.back();
+        ready.pop_back();
+        ++done;
+        for (size_t b : succ[a]) {
+            level[b] = std::max(level[b], level[a] + 1);
+            if (--indeg[b] == 0) ready.push_back(b);
+        }
+    }
+    if (done != n) return LEYLINE_E_INVAL;     // not reached: the graph is acyclic
 
     const int n_levels = *std::max_element(level.begin(), level.end()) + 1;
     // Ordered tiles need every plane to move single chunks (half-split bands whose partners

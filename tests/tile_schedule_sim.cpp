@@ -68,7 +68,7 @@ int main(int argc, char** argv) {
         const int L = int(uni(1, 3));
         const int64_t n = uni(1, sh.max_len);
         // directives: sorted, non-overlapping (adjacent allowed) spans; short shifts are common
-        const int k = int(uni(1, 8));
+        const int k = int(uni(0, 3) == 0 ? uni(9, 48) : uni(1, 8));   // some calls with many directives
         std::vector<int64_t> cuts;
         for (int i = 0; i < 2 * k; ++i) cuts.push_back(uni(0, n));
         std::sort(cuts.begin(), cuts.end());
@@ -79,6 +79,7 @@ int main(int argc, char** argv) {
             std::memset(&d, 0, sizeof(d));
             d.span_start = cuts[size_t(2 * j)];
             d.span_end = std::min(cuts[size_t(2 * j + 1)], d.span_start + (uni(0, 3) == 0 ? n : uni(0, 64)));
+            if (d.span_end < d.span_start) d.span_end = d.span_start;
             const int64_t span = d.span_end - d.span_start;
             const int pick = int(uni(0, 4));
             d.stub_len = pick == 0 ? 0 : pick == 1 ? span + uni(-3, 3) : pick == 2 ? span : uni(0, 2 * span + 3);
