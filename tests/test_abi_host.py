@@ -402,4 +402,4 @@ def test_contig_planning_scales_to_thousands_of_directives():
     q = L.leyline_contig_query(c, n, _dirs(spec), k)
     assert time.perf_counter() - t0 < 1.0
     assert q.new_len == n + sum(r - (e - s) for s, e, r in spec)
-    assert q.tile_launches >= (2 * k) // 24
+    assert k // 24 <= q.tile_launches <= (2 * k) // 24 + 1
