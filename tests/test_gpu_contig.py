@@ -86,11 +86,19 @@ def _small_workload(rng, kind, dtype, n_layers, n, dirs, extra=0):
         planes = W.gqa_planes(heads=2, dim=128)
     elif kind == "mla_neox":
         planes = [W.PlaneDesc((576,), 1, 576, 512, 64, 1, 10000.0)]
+    elif kind == "four":      # the most planes a cache may have, both rotary styles and band widths
+        planes = FOUR_PLANES
     else:  # several interleaved heads with a partial rotary band, and a move-only plane
         planes = [W.PlaneDesc((4, 64), 4, 64, 32, 32, 0, 50000.0), W.PlaneDesc((128,))]
     cap = n + max(0, sum(d.stub_len - (d.span_end - d.span_start) for d in dirs)) + extra
     return W.Workload(f"small_{kind}", n_layers, dtype, planes, dirs, [n], capacity=max(cap, n),
                       seed=rng.randint(0, 10 ** 6))
+
+
+# MLA row (narrow interleaved band), two-head half-split K, V, and a small plane whose interleaved
+# band is half its row
+FOUR_PLANES = [W.mla_plane(), W.PlaneDesc((2, 128), 2, 128, 0, 128, 1, 500000.0), W.PlaneDesc((256,)),
+               W.PlaneDesc((64,), 1, 64, 32, 32, 0, 10000.0)]
 
 
 def _random_dirs(rng, n, k):
@@ -129,7 +137,8 @@ def test_mla_1l_4k_f32_exact_recipe(L):
 
 
 @pytest.mark.parametrize("kind,dtype", [("mla", "bf16"), ("mla", "f32"), ("gqa", "bf16"),
-                                        ("gqa", "f32"), ("mla_neox", "bf16"), ("heads", "bf16")])
+                                        ("gqa", "f32"), ("mla_neox", "bf16"), ("heads", "bf16"),
+                                        ("four", "bf16")])
 def test_small_random_splices(L, kind, dtype):
     rng = random.Random(zlib.crc32(f"{kind}/{dtype}".encode()))
     cases = []

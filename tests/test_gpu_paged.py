@@ -66,6 +66,9 @@ def _random_workload(rng, page, kind, dtype, max_len=None):
         planes = [W.mla_plane()]
     elif kind == "mla_neox":      # half-split band that straddles wavefront windows: two-chunk units
         planes = [W.PlaneDesc((576,), 1, 576, 512, 64, 1, 10000.0)]
+    elif kind == "four":          # four planes, rotary bands of both access classes
+        planes = [W.mla_plane(), W.PlaneDesc((2, 128), 2, 128, 0, 128, 1, 500000.0), W.PlaneDesc((256,)),
+                  W.PlaneDesc((64,), 1, 64, 32, 32, 0, 10000.0)]
     else:
         planes = W.gqa_planes(heads=2, dim=128)
     return W.Workload(f"paged_{kind}", 2, dtype, planes, dirs, lens, page_size=page,
@@ -73,9 +76,9 @@ def _random_workload(rng, page, kind, dtype, max_len=None):
 
 
 @pytest.mark.parametrize("kind,dtype", [("mla", "bf16"), ("gqa", "bf16"), ("mla", "f32"),
-                                        ("gqa", "f32"), ("mla_neox", "bf16")])
+                                        ("gqa", "f32"), ("mla_neox", "bf16"), ("four", "bf16")])
 def test_small_random_paged_whole_pool(L, kind, dtype):
-    rng = random.Random({"mla": 97, "gqa": 98, "mla_neox": 99}[kind] + (dtype == "f32"))
+    rng = random.Random({"mla": 97, "gqa": 98, "mla_neox": 99, "four": 100}[kind] + (dtype == "f32"))
     for page in (1, 4, 16, 64):
         for ci in range(8):
             wl = _random_workload(rng, page, kind, dtype)
@@ -97,6 +100,33 @@ def test_small_random_paged_whole_pool(L, kind, dtype):
             for pi, plane in enumerate(planes):
                 got = host(pools[pi]).reshape(want[pi].shape)
                 assert_rows_match(got, want[pi], plane, dtype, what=f"page={page} case={ci} plane={pi}")
+
+
+@pytest.mark.parametrize("kind", ["mla", "gqa"])
+def test_page_sizes_not_powers_of_two(L, kind):
+    """Pages of 3 and 48 rows: page and row index arithmetic without power-of-two shortcuts;
+    whole pools against the oracle."""
+    rng = random.Random({"mla": 401, "gqa": 402}[kind])
+    for page in (3, 48):
+        for ci in range(5):
+            wl = _random_workload(rng, page, kind, "bf16")
+            print(f"[case] page={page} {kind} case={ci} lens={wl.seq_lens} dirs={wl.dirs}", flush=True)
+            pools, bt, free, stubs = W.alloc_paged(wl, DEV, spare_pages=3)
+            before = [host(p) for p in pools]
+            bt_h, free_h = host(bt), host(free)
+            stubs_h = [[host(s).reshape(wl.n_layers, s.shape[1], p.row_elems) for s, p in zip(per, wl.planes)]
+                       for per in stubs]
+            bt_out, freed, new_lens = _run_gpu(L, wl, pools, bt, free, stubs)
+            planes = [oracle_plane(p) for p in wl.planes]
+            flat = [b.reshape(b.shape[0], b.shape[1], b.shape[2], -1) for b in before]
+            want, want_bt, want_lens, want_freed = O.splice_paged(
+                flat, planes, "bf16", bt_h, wl.seq_lens, _odirs(wl), stubs_h, list(free_h), page)
+            assert new_lens == want_lens
+            assert np.array_equal(host(bt_out), want_bt)
+            assert list(host(freed)) == want_freed
+            for pi, plane in enumerate(planes):
+                got = host(pools[pi]).reshape(want[pi].shape)
+                assert_rows_match(got, want[pi], plane, "bf16", what=f"page={page} case={ci} plane={pi}")
 
 
 @pytest.mark.parametrize("kind", ["mla", "gqa"])
@@ -231,11 +261,11 @@ def test_inline_and_row_table_gathers(L, kind, last_stub):
 
 
 @pytest.mark.parametrize("kind,dtype", [("mla", "bf16"), ("gqa", "bf16"), ("mla", "f32"),
-                                        ("mla_neox", "bf16")])
+                                        ("mla_neox", "bf16"), ("four", "bf16")])
 def test_token_slot_paged_whole_pool(L, kind, dtype):
     """Page sizes 1 and 2 (token-slot caches) with sequences long enough that the in-place
     rotation of remapped slots spans many workgroups and ends in a ragged one."""
-    rng = random.Random({"mla": 197, "gqa": 198, "mla_neox": 199}[kind] + (dtype == "f32"))
+    rng = random.Random({"mla": 197, "gqa": 198, "mla_neox": 199, "four": 200}[kind] + (dtype == "f32"))
     for page in (1, 2):
         for ci in range(3):
             wl = _random_workload(rng, page, kind, dtype, max_len=900)
