@@ -10,7 +10,9 @@ and frequency schedules:
   convention" mentions the interpolated regime) through the contiguous, paged and rotate calls;
 * chained in-place rotations (App. "Chained-rotation drift in bf16"): every step against the
   oracle applied to the GPU's previous state, and the end state against fresh RoPE at the final
-  position within the paper's Table "drift" magnitudes.
+  position within the paper's Table "drift" magnitudes;
+* the precision-floor sweep (App. "bf16 K-storage precision floor"): keys at the paper's source
+  positions re-anchored by shifts up to 6794 in fp32 and bf16 storage, against fresh RoPE.
 """
 
 import random
@@ -248,3 +250,53 @@ def test_chained_rotations_step_by_step(L, style):
         mean = float(np.mean(drift[n]))
         print(f"[info] style {style}: N={n} mean rel-L2 {mean:.2e} (paper {bound:.1e})")
         assert mean <= bound
+
+
+FLOOR_SOURCES = (10, 100, 1000, 4000, 8000, 8836)
+FLOOR_DELTAS = (1, -1, 48, -48, 512, 2000, 6794, -6794)
+
+
+@pytest.mark.parametrize("dtype", [O.F32, O.BF16])
+def test_precision_floor_sweep(L, dtype):
+    """App. "bf16 K-storage precision floor": MLA K_pe keys RoPE'd at sources {10, ..., 8836}
+    (theta 1e4, interleaved) and re-anchored in place by shifts up to |6794|, against a fresh fp64
+    RoPE at p + delta, per entry relative to its pair's norm.  fp32 storage stays at fp32
+    rounding at every (p, delta): angles are formed in fp64 (the paper's fp32 path, with fp32
+    angles, grew to 1.6e-3 at (8836, 6794)).  bf16 storage sits at the storage floor (the
+    stored key's rounding plus the result's, under 3 bf16 half-steps), the same for every
+    shift."""
+    plane = O.mla_plane()
+    f = plane.frequencies()
+    rng = np.random.default_rng(77)
+    per = 64
+    src = np.repeat(np.array(FLOOR_SOURCES), per)
+    n = len(src)
+    raw = rng.standard_normal((n, 64))
+    rows = np.zeros((n, 576))
+    rows[:, :512] = rng.standard_normal((n, 512))
+    rows[:, 512:] = O.rope(raw, src, f, O.INTERLEAVED)
+    stored = O.encode(rows, dtype)
+    t = device(stored, DEV).view(1, n, 576)
+    cache = L.make_cache([_spec(L, t, plane)])
+    worst = {}
+    for dl in FLOOR_DELTAS:
+        t.copy_(device(stored, DEV).view(1, n, 576))
+        print(f"[case] floor {dtype} delta={dl}", flush=True)
+        L.leyline_rotate_delta(cache, dl, row0=0, n_rows=n)
+        torch.cuda.synchronize()
+        out = host(t).reshape(n, 576)
+        assert np.array_equal(out[:, :512], stored[:, :512])                 # latent untouched
+        got = O.decode(out[:, 512:], dtype)
+        fresh = O.rope(raw, src + dl, f, O.INTERLEAVED)
+        pair = np.repeat(np.hypot(fresh[:, 0::2], fresh[:, 1::2]), 2, axis=1)
+        err = (np.abs(got - fresh) / pair).reshape(len(FLOOR_SOURCES), per, 64).max(axis=(1, 2))
+        for p, e in zip(FLOOR_SOURCES, err):
+            worst[(p, dl)] = float(e)
+    print("[info] worst per-entry error / pair norm:", {k: f"{v:.2e}" for k, v in worst.items()})
+    if dtype == O.F32:
+        assert max(worst.values()) < 1e-5
+    else:
+        assert max(worst.values()) < 3 * 2.0 ** -8
+        small = max(v for (p, dl), v in worst.items() if abs(dl) == 1)
+        large = max(v for (p, dl), v in worst.items() if abs(dl) == 6794)
+        assert large < 1.5 * small                                           # independent of delta
