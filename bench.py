@@ -211,6 +211,7 @@ def main():
         "metric": METRIC,
         "value": moved / (ms_per_step * 1e-3),
         "unit": "tokens/s",
+        "token_layer_rows_per_s": moved * wl.n_layers / (ms_per_step * 1e-3),
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
