@@ -241,6 +241,21 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream
 
 
+def _stream_workspace(nbytes: int, stream, device):
+    """A device buffer allocated on the stream the call runs on: torch's caching allocator hands a
+    freed block out again only in that stream's order, so dropping the buffer when the call
+    returns cannot let later work reuse it while the call's kernels still run."""
+    import torch
+    if stream is None:
+        s = torch.cuda.current_stream(device)
+    elif isinstance(stream, int):
+        s = torch.cuda.ExternalStream(stream, device=device)
+    else:
+        s = stream
+    with torch.cuda.stream(s):
+        return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
 def _ptr(t) -> Optional[int]:
     return None if t is None else t.data_ptr()
 
@@ -278,8 +293,7 @@ def leyline_splice_contig(cache: leyline_cache, seq_len: int, dirs, n_dirs: int,
     if workspace is None:
         need = leyline_contig_query(cache, seq_len, dirs, n_dirs).workspace_bytes
         if need:
-            import torch
-            workspace = torch.empty(need, dtype=torch.uint8, device=_cache_device(cache))
+            workspace = _stream_workspace(need, stream, _cache_device(cache))
     ws_ptr = workspace.data_ptr() if workspace is not None else None
     ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
     new_len = c_int64(0)

@@ -34,7 +34,7 @@ def _dir_dicts(wl, stubs):
                  stub_len=d.stub_len, mode=d.mode) for j, d in enumerate(wl.dirs)]
 
 
-def _run_and_check(L, wl, planes_dev, stubs_dev, label, layers=None):
+def _run_and_check(L, wl, planes_dev, stubs_dev, label, layers=None, stream=None):
     """Snapshot inputs, splice on the GPU, splice in the oracle, compare rows [0, n') (of the
     listed layers only, when given)."""
     print(f"[case] {label}", flush=True)
@@ -50,7 +50,7 @@ def _run_and_check(L, wl, planes_dev, stubs_dev, label, layers=None):
     cache = L.make_cache(_specs(L, wl, planes_dev))
     dirs = L.make_directives(_dir_dicts(wl, stubs_dev))
     n = wl.seq_lens[0]
-    new_len = L.leyline_splice_contig(cache, n, dirs, len(wl.dirs))
+    new_len = L.leyline_splice_contig(cache, n, dirs, len(wl.dirs), stream=stream)
     torch.cuda.synchronize()
     odirs = [O.Directive(d.span_start, d.span_end, d.stub_len, mode=d.mode) for d in wl.dirs]
     assert new_len == O.new_length(n, odirs)
@@ -236,6 +236,22 @@ def test_many_directives_several_tile_launches(L, kind, k):
         assert q.tile_launches >= 2, q
         _run_and_check(L, wl, planes_dev, stubs_dev,
                        f"{kind} {k} directives case {ci} n={n} tile launches={q.tile_launches}")
+
+
+def test_side_stream_without_caller_workspace(L):
+    """Ordered-tile splices enqueued on a side stream with no caller workspace: the binding
+    allocates the workspace on that stream; results match the oracle."""
+    rng = random.Random(77)
+    side = torch.cuda.Stream()
+    for ci, kind in enumerate(["mla", "gqa", "mla", "gqa"]):
+        n = rng.randint(1500, 3000)
+        s = rng.randint(0, n - 10)
+        dirs = [W.Dir(s, s + rng.randint(1, 9), rng.randint(0, 12))]
+        wl = _small_workload(rng, kind, "bf16", 3, n, dirs, extra=12)
+        planes_dev, stubs_dev = W.alloc_contig(wl, DEV, seed=3000 + ci)
+        torch.cuda.synchronize()
+        _run_and_check(L, wl, planes_dev, stubs_dev, f"side stream {kind} case {ci} n={n} dirs={dirs}",
+                       stream=side)
 
 
 def test_mla_dsv3_32k_edits8(L):
