@@ -186,24 +186,30 @@ def main():
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    # The timed region: K splices back to back on the stream the kernels run on, bracketed by
+    # two HIP events and nothing in between (an event between splices adds its own packet).
     t_begin = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_begin.record(stream)
     for i in range(args.steps):
-        starts[i].record(stream)
         step(i)
-        ends[i].record(stream)
     t_end.record(stream)
     torch.cuda.synchronize()
     total_ms = t_begin.elapsed_time(t_end)
-    per_splice = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
-    splice_ms = float(np.mean(per_splice))
-
-    achieved = alg_bytes / (splice_ms * 1e-3) / 1e9
     ms_per_step = total_ms / args.steps
+    splice_ms = ms_per_step
+    achieved = alg_bytes / (splice_ms * 1e-3) / 1e9
+    # Spread of single splices, from a separate untimed pass with an event pair around each.
+    n_spread = min(args.steps, 20)
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(n_spread)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(n_spread)]
+    for i in range(n_spread):
+        starts[i].record(stream)
+        step(args.steps + i)
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    per_splice = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
     copy_gbps, _ = copy_ceiling(alg_bytes, dev, stream)
     rec = measured_traffic(wl.name)
     traffic = rec["dispatch_bytes"] if rec and rec.get("kernel") == kernel else None
@@ -244,6 +250,7 @@ def main():
             "traffic_per_splice": None if rec is None else {k: rec[k] for k in ("fetch_bytes", "write_bytes", "total_bytes")},
             "splice_ms": splice_ms,
             "splice_ms_p10_p50_p90": [float(x) for x in np.percentile(per_splice, [10, 50, 90])],
+            "splice_spread_sample": f"{n_spread} splices after the timed region, an event pair around each",
             "launches_per_splice": launches,
             "avg_launch_ms": splice_ms / max(1, launches),
             "d2d_copy_GBps": copy_gbps,
@@ -422,7 +429,9 @@ def summarize(args):
     else:
         alg, _ = contig_bytes(wl)
         kernel = CONTIG_KERNEL
-    splices = _flag(args.command, "--steps", 100) + _flag(args.command, "--warmup", 10)
+    steps = _flag(args.command, "--steps", 100)
+    # warmup, timed steps, then the spread pass of up to 20 single splices
+    splices = steps + _flag(args.command, "--warmup", 10) + min(steps, 20)
     stats = _read_csv(trace_dir, "kernel_stats")
     trace = _read_csv(trace_dir, "kernel_trace")
     if not wl.page_size:

@@ -88,7 +88,8 @@ def assert_rows_match(got: np.ndarray, want: np.ndarray, plane: O.Plane, dtype: 
             raise AssertionError(f"{what}: bf16 rotary error beyond max(1 ulp, 2e-6 |pair|) at "
                                  f"{bad[:5].tolist()} ({len(bad)} total, max err {err.max():.3g})")
         global LAST_BF16_EXACT_FRACTION
-        LAST_BF16_EXACT_FRACTION = float(np.mean(got[..., rot] == want[..., rot]))
+        same = got[..., rot] == want[..., rot]
+        LAST_BF16_EXACT_FRACTION = float(np.mean(same)) if same.size else None
         return
     for cols in plane.rotary_columns():
         # positions of this head's band inside the compressed rotary selection
