@@ -90,6 +90,8 @@ def test_new_positions_are_a_bijection():
         assert sorted(olds) == [p for p in range(n) if p not in deleted]
         assert olds == sorted(olds)          # order preserved
         assert len(src) == O.new_length(n, dirs)
+        # the shift recorded with a row is where it lands: new position = old position + shift
+        assert all(q == r[1] + r[2] for q, r in enumerate(src) if r[0] == "old")
 
 
 def test_rejects_overlap_unsorted_and_out_of_range():
@@ -340,6 +342,12 @@ def test_paged_invariants_and_reconstruction():
             assert used_fresh == set(free[:len(used_fresh)])
             assert set(referenced) | set(freed) == old | used_fresh            # nothing lost
             assert not (set(referenced) & set(freed))
+            for plan in O.plan_paged(seq_lens, dirs, page):
+                for k, (kind, src, delta) in enumerate(zip(plan.kinds, plan.sources, plan.deltas)):
+                    if kind == O.IDENTITY:
+                        assert src == k and delta == 0
+                    elif kind == O.REMAP:                   # a whole page moved by whole pages
+                        assert delta == (k - src) * page and delta != 0
             for b, n in enumerate(seq_lens):
                 my = [d for d in dirs if d.seq == b]
                 my_st = [stubs[i][0] for i, d in enumerate(dirs) if d.seq == b]
@@ -402,6 +410,9 @@ def test_forget_is_a_prefix_trim_after_the_earlier_edits():
 def test_forget_must_be_last_and_carry_no_replacement():
     with pytest.raises(O.DirectiveError):
         O.row_sources(20, [O.Directive(2, 4, 0, mode=O.FORGET), O.Directive(6, 8, 1)])
+    # an insertion at the very end would not overlap the trimmed tail: refused all the same
+    with pytest.raises(O.DirectiveError):
+        O.row_sources(20, [O.Directive(2, 4, 0, mode=O.FORGET), O.Directive(20, 20, 1)])
     with pytest.raises(O.DirectiveError):
         O.row_sources(20, [O.Directive(2, 4, 3, mode=O.FORGET)])
     assert O.new_length(20, [O.Directive(5, 9, 0, mode=O.FORGET)]) == 5
