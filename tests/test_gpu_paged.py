@@ -10,7 +10,7 @@ import torch
 
 import workloads as W
 from oracle import splice_oracle as O
-from tests.parity_util import assert_rows_match, host, oracle_plane
+from tests.parity_util import assert_rows_match, host, oracle_plane, rotary_mask
 
 pytestmark = pytest.mark.gpu
 
@@ -305,6 +305,108 @@ def _sample_positions(rng, wl, b, new_len, extra=24):
     return sorted(q for q in pts if 0 <= q < new_len)
 
 
+def _bits(t):
+    return t.contiguous().view(torch.int16 if t.dtype == torch.bfloat16 else torch.int32)
+
+
+class _EveryRow:
+    """Checks every row of every sequence, plane and layer at full size by properties:
+    non-rotary elements equal their source row's bit for bit, replacement rows equal the
+    replacement bit for bit, rows with shift 0 are bit-identical, and every rotary pair p of a
+    moved row has turned by its angle phi (p.p' = |p|^2 cos phi, p x p' = |p|^2 sin phi, within
+    storage rounding), with cos phi and sin phi taken from the oracle once per distinct shift.
+    The rotary bands of all source rows are snapshotted on the device before the call; their
+    non-rotary elements are read after it, where they still are (fresh pages are disjoint from
+    old ones, a re-used page changes only its rotary bands, copy-on-write writes no old page)."""
+
+    def __init__(self, wl, pools, bt_h, stubs):
+        P = wl.page_size
+        odirs = _odirs(wl)
+        glob = {}
+        for j, d in enumerate(wl.dirs):
+            glob.setdefault(d.seq, []).append(j)
+        stub_base = np.cumsum([0] + [d.stub_len for d in wl.dirs])
+        q_old, q_stub, a_old, shift, stub_row, seq_old, seq_stub = ([] for _ in range(7))
+        for b, n in enumerate(wl.seq_lens):
+            src = O.row_sources(n, [d for d in odirs if d.seq == b])
+            kind = np.array([x[0] == "old" for x in src], dtype=bool)
+            a = np.array([x[1] for x in src], dtype=np.int64)
+            c = np.array([x[2] for x in src], dtype=np.int64)
+            q = np.arange(len(src), dtype=np.int64)
+            q_old.append(q[kind]); a_old.append(a[kind]); shift.append(c[kind])
+            seq_old.append(np.full(int(kind.sum()), b))
+            loc = a[~kind]
+            stub_row.append(np.array([stub_base[glob[b][j]] for j in loc], dtype=np.int64) + c[~kind])
+            q_stub.append(q[~kind]); seq_stub.append(np.full(int((~kind).sum()), b))
+        cat = lambda xs: np.concatenate(xs) if xs else np.zeros(0, dtype=np.int64)
+        self.q_old, self.a_old, self.shift, self.seq_old = map(cat, (q_old, a_old, shift, seq_old))
+        self.q_stub, self.stub_row, self.seq_stub = map(cat, (q_stub, stub_row, seq_stub))
+        self.P, self.wl = P, wl
+        dev = lambda x: torch.from_numpy(np.ascontiguousarray(x, dtype=np.int64)).to(DEV)
+        self.op, self.oo = dev(bt_h[self.seq_old, self.a_old // P]), dev(self.a_old % P)
+        self.planes = [oracle_plane(desc) for desc in wl.planes]
+        self.rot = [torch.from_numpy(rotary_mask(pl)).to(DEV) for pl in self.planes]
+        # rotary bands of every source row, before the call
+        self.before = [torch.stack([pools[pi][layer][self.op, self.oo].reshape(len(self.a_old), self.planes[pi].row_elems)[:, self.rot[pi]]
+                                    for layer in range(wl.n_layers)])
+                       if self.planes[pi].rot_dim else None for pi in range(len(pools))]
+        # cos and sin of every (moved row, pair), from the oracle's rotation of unit pairs: one
+        # evaluation per distinct shift
+        moved_shifts = self.shift[self.shift != 0]
+        shifts, which = np.unique(moved_shifts, return_inverse=True)
+        self.angles = []
+        for pl in self.planes:
+            if not pl.rot_dim:
+                self.angles.append(None)
+                continue
+            ia, ib = O.pair_dims(pl.rot_dim, pl.style)
+            unit = np.zeros((len(shifts), pl.rot_dim))
+            unit[:, ia] = 1.0
+            turned = O.rotate(unit, shifts, pl.frequencies(), pl.style)     # (cos, sin) per pair
+            heads = range(pl.n_heads)
+            cs = np.concatenate([turned[:, ia] for _ in heads], axis=1)[which]
+            sn = np.concatenate([turned[:, ib] for _ in heads], axis=1)[which]
+            cols = lambda x: torch.from_numpy(np.concatenate([x + h * pl.rot_dim for h in heads])).to(DEV)
+            self.angles.append((cols(ia), cols(ib), torch.from_numpy(cs).to(DEV), torch.from_numpy(sn).to(DEV)))
+        self.stubs = [torch.cat([s[pi].reshape(wl.n_layers, s[pi].shape[1], self.planes[pi].row_elems)
+                                 for s in stubs], dim=1)
+                      if len(stubs) else None for pi in range(len(pools))]
+
+    def check(self, pools, bt_out_h):
+        P, wl = self.P, self.wl
+        dev = lambda x: torch.from_numpy(np.ascontiguousarray(x, dtype=np.int64)).to(DEV)
+        np_, no = dev(bt_out_h[self.seq_old, self.q_old // P]), dev(self.q_old % P)
+        sp, so = dev(bt_out_h[self.seq_stub, self.q_stub // P]), dev(self.q_stub % P)
+        moved = dev(self.shift != 0).bool()
+        rows = 0
+        for pi, plane in enumerate(self.planes):
+            rot = self.rot[pi]
+            for layer in range(wl.n_layers):
+                pool = pools[pi][layer]
+                got = pool[np_, no].reshape(len(self.a_old), plane.row_elems)
+                src = pool[self.op, self.oo].reshape(len(self.a_old), plane.row_elems)
+                assert torch.equal(_bits(got[:, ~rot]), _bits(src[:, ~rot])), f"plane {pi} layer {layer}: non-rotary"
+                if self.stubs[pi] is not None:
+                    gs = pool[sp, so].reshape(len(self.q_stub), plane.row_elems)
+                    assert torch.equal(_bits(gs), _bits(self.stubs[pi][layer, dev(self.stub_row)])), \
+                        f"plane {pi} layer {layer}: replacement rows"
+                if not plane.rot_dim:
+                    continue
+                g, b0 = got[:, rot], self.before[pi][layer]
+                assert torch.equal(_bits(g[~moved]), _bits(b0[~moved])), f"plane {pi} layer {layer}: shift-0 rows"
+                # every pair of a moved row turned by phi = shift * theta_i: with p its pair before
+                # and p' after, p.p' = |p|^2 cos(phi) and p x p' = |p|^2 sin(phi)
+                ia, ib, cs, sn = self.angles[pi]
+                gm, bm = g[moved].double(), b0[moved].double()
+                a, b, a2, b2 = bm[:, ia], bm[:, ib], gm[:, ia], gm[:, ib]
+                n2 = a * a + b * b
+                tol = (2.0 ** -7 if wl.dtype == "bf16" else 1e-5) * n2 + 1e-30
+                assert bool(((a * a2 + b * b2 - n2 * cs).abs() <= tol).all()), f"plane {pi} layer {layer}: pair angles (cos)"
+                assert bool(((a * b2 - b * a2 - n2 * sn).abs() <= tol).all()), f"plane {pi} layer {layer}: pair angles (sin)"
+            rows += len(self.a_old) + len(self.q_stub)
+        print(f"[info] every row checked by properties: {rows} rows x {wl.n_layers} layers", flush=True)
+
+
 def _check_sampled(L, wl, seed):
     rng = random.Random(seed)
     print(f"[case] {wl.name}: allocating and filling the pool", flush=True)
@@ -332,6 +434,7 @@ def _check_sampled(L, wl, seed):
     dir_index = {}
     for j, d in enumerate(wl.dirs):
         dir_index.setdefault(d.seq, []).append(j)
+    every = _EveryRow(wl, pools, bt_h, stubs)
     print(f"[case] {wl.name}: splicing on the GPU", flush=True)
     bt_out, freed, new_lens = _run_gpu(L, wl, pools, bt, free, stubs, flags=wl.paged_flags)
     assert new_lens == want_lens
@@ -359,6 +462,8 @@ def _check_sampled(L, wl, seed):
             old_now = host(pools[pi][:, pages_old, offs_old]).reshape(wl.n_layers, len(samples), -1)
             from_old = [i for i, x in enumerate(samples) if x[2] == "old"]
             assert np.array_equal(old_now[:, from_old], old[:, from_old])
+    every.check(pools, bt_out_h)
+    del every
     return pools, bt, bt_out, new_lens, plans
 
 
