@@ -104,3 +104,39 @@ def assert_rows_match(got: np.ndarray, want: np.ndarray, plane: O.Plane, dtype: 
         if not np.all(ok):
             bad = np.argwhere(~ok)
             raise AssertionError(f"{what}: fp32 pair error above {F32_PAIR_RTOL} at {bad[:5].tolist()}")
+
+
+def angle_tables(plane: O.Plane, shifts: np.ndarray, dev):
+    """For rows moved by `shifts` (one per row, nonzero): the columns of every pair's two members
+    within the plane's rotary selection (all heads), and cos/sin of every (row, pair) angle
+    phi = shift * theta_i, taken from the oracle's rotation of unit pairs (one evaluation per
+    distinct shift)."""
+    uniq, which = np.unique(np.asarray(shifts, dtype=np.int64), return_inverse=True)
+    ia, ib = O.pair_dims(plane.rot_dim, plane.style)
+    unit = np.zeros((len(uniq), plane.rot_dim))
+    unit[:, ia] = 1.0
+    turned = O.rotate(unit, uniq, plane.frequencies(), plane.style)       # (cos, sin) per pair
+    heads = range(plane.n_heads)
+    cs = np.concatenate([turned[:, ia] for _ in heads], axis=1)[which]
+    sn = np.concatenate([turned[:, ib] for _ in heads], axis=1)[which]
+    cols = lambda x: torch.from_numpy(np.concatenate([x + h * plane.rot_dim for h in heads])).to(dev)
+    return cols(ia), cols(ib), torch.from_numpy(cs).to(dev), torch.from_numpy(sn).to(dev)
+
+
+def assert_pairs_turned(before: torch.Tensor, after: torch.Tensor, tables, dtype: str, what: str = "") -> None:
+    """before/after: rotary selections [rows, n_rot] of moved rows (device, storage dtype).  Every
+    pair p must have turned by its angle: p.p' = |p|^2 cos(phi) and p x p' = |p|^2 sin(phi),
+    within storage rounding (2^-7 |p|^2 for bf16, 1e-5 |p|^2 for fp32)."""
+    ia, ib, cs, sn = tables
+    bm, gm = before.double(), after.double()
+    a, b, a2, b2 = bm[:, ia], bm[:, ib], gm[:, ia], gm[:, ib]
+    n2 = a * a + b * b
+    tol = (2.0 ** -7 if dtype == O.BF16 else 1e-5) * n2 + 1e-30
+    assert bool(((a * a2 + b * b2 - n2 * cs).abs() <= tol).all()), f"{what}: pair angles (cos)"
+    assert bool(((a * b2 - b * a2 - n2 * sn).abs() <= tol).all()), f"{what}: pair angles (sin)"
+
+
+def bits(t: torch.Tensor) -> torch.Tensor:
+    """Bit patterns of a bf16 or fp32 device tensor, for exact comparison."""
+    return t.contiguous().view(torch.int16 if t.dtype == torch.bfloat16 else torch.int32)
+

@@ -42,6 +42,7 @@ def _run_and_check(L, wl, planes_dev, stubs_dev, label, layers=None, stream=None
         sel = torch.tensor(layers, device=DEV)
         before = [host(t.index_select(0, sel)) for t in planes_dev]
         stubs_h = [[host(s.index_select(0, sel)) for s in per] for per in stubs_dev]
+        before_dev = [t.clone() for t in planes_dev]      # every layer, for the property check
     else:
         before = [host(t) for t in planes_dev]
     if layers is None:
@@ -64,7 +65,49 @@ def _run_and_check(L, wl, planes_dev, stubs_dev, label, layers=None, stream=None
         assert_rows_match(got[:, :new_len], want[:, :new_len], plane, wl.dtype,
                           inputs=_inputs_for_new_rows(src, n, odirs, stubs),
                           what=f"{label} plane {pi}")
+    if layers is not None:
+        _check_every_layer(wl, before_dev, planes_dev, stubs_dev, n, odirs, new_len, label)
     return new_len
+
+
+def _check_every_layer(wl, before, after, stubs, n, odirs, new_len, label):
+    """Rows [0, n') of every layer by properties (the oracle compares whole layers on a subset):
+    non-rotary elements and replacement rows bit-exact against their sources, shift-0 rows
+    bit-identical, every rotary pair of a moved row turned by its angle (cos and sin from the
+    oracle once per distinct shift)."""
+    src = O.row_sources(n, odirs)
+    assert len(src) == new_len
+    kind = np.array([x[0] == "old" for x in src], dtype=bool)
+    a = np.array([x[1] for x in src], dtype=np.int64)
+    c = np.array([x[2] for x in src], dtype=np.int64)
+    q = np.arange(new_len, dtype=np.int64)
+    base = np.cumsum([0] + [d.stub_len for d in odirs])
+    stub_row = np.array([base[j] for j in a[~kind]], dtype=np.int64) + c[~kind]
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+    q_old, a_old, q_st, st = t(q[kind]), t(a[kind]), t(q[~kind]), t(stub_row)
+    shift = c[kind]
+    moved = t(shift != 0)
+    for pi, desc in enumerate(wl.planes):
+        plane = oracle_plane(desc)
+        row = plane.row_elems
+        rot = t(PU.rotary_mask(plane))
+        tables = PU.angle_tables(plane, shift[shift != 0], DEV) if plane.rot_dim else None
+        b4 = before[pi].reshape(wl.n_layers, -1, row)
+        af = after[pi].reshape(wl.n_layers, -1, row)
+        st_all = torch.cat([s[pi].reshape(wl.n_layers, s[pi].shape[1], row) for s in stubs], dim=1) \
+            if len(stubs) else None
+        for layer in range(wl.n_layers):
+            what = f"{label} plane {pi} layer {layer}"
+            g, s0 = af[layer, q_old], b4[layer, a_old]
+            assert torch.equal(PU.bits(g[:, ~rot]), PU.bits(s0[:, ~rot])), f"{what}: non-rotary"
+            if st_all is not None:
+                assert torch.equal(PU.bits(af[layer, q_st]), PU.bits(st_all[layer, st])), f"{what}: replacement"
+            if plane.rot_dim:
+                gr, sr = g[:, rot], s0[:, rot]
+                assert torch.equal(PU.bits(gr[~moved]), PU.bits(sr[~moved])), f"{what}: shift-0 rows"
+                PU.assert_pairs_turned(sr[moved], gr[moved], tables, wl.dtype, what)
+    print(f"[info] {label}: every layer checked by properties ({new_len} rows x {wl.n_layers} layers)",
+          flush=True)
 
 
 def _inputs_for_new_rows(src, n, dirs, stubs):

@@ -10,7 +10,8 @@ import torch
 
 import workloads as W
 from oracle import splice_oracle as O
-from tests.parity_util import assert_rows_match, host, oracle_plane, rotary_mask
+from tests.parity_util import (angle_tables, assert_pairs_turned, assert_rows_match, bits, host,
+                               oracle_plane, rotary_mask)
 
 pytestmark = pytest.mark.gpu
 
@@ -305,10 +306,6 @@ def _sample_positions(rng, wl, b, new_len, extra=24):
     return sorted(q for q in pts if 0 <= q < new_len)
 
 
-def _bits(t):
-    return t.contiguous().view(torch.int16 if t.dtype == torch.bfloat16 else torch.int32)
-
-
 class _EveryRow:
     """Checks every row of every sequence, plane and layer at full size by properties:
     non-rotary elements equal their source row's bit for bit, replacement rows equal the
@@ -350,24 +347,8 @@ class _EveryRow:
         self.before = [torch.stack([pools[pi][layer][self.op, self.oo].reshape(len(self.a_old), self.planes[pi].row_elems)[:, self.rot[pi]]
                                     for layer in range(wl.n_layers)])
                        if self.planes[pi].rot_dim else None for pi in range(len(pools))]
-        # cos and sin of every (moved row, pair), from the oracle's rotation of unit pairs: one
-        # evaluation per distinct shift
-        moved_shifts = self.shift[self.shift != 0]
-        shifts, which = np.unique(moved_shifts, return_inverse=True)
-        self.angles = []
-        for pl in self.planes:
-            if not pl.rot_dim:
-                self.angles.append(None)
-                continue
-            ia, ib = O.pair_dims(pl.rot_dim, pl.style)
-            unit = np.zeros((len(shifts), pl.rot_dim))
-            unit[:, ia] = 1.0
-            turned = O.rotate(unit, shifts, pl.frequencies(), pl.style)     # (cos, sin) per pair
-            heads = range(pl.n_heads)
-            cs = np.concatenate([turned[:, ia] for _ in heads], axis=1)[which]
-            sn = np.concatenate([turned[:, ib] for _ in heads], axis=1)[which]
-            cols = lambda x: torch.from_numpy(np.concatenate([x + h * pl.rot_dim for h in heads])).to(DEV)
-            self.angles.append((cols(ia), cols(ib), torch.from_numpy(cs).to(DEV), torch.from_numpy(sn).to(DEV)))
+        moved = self.shift != 0
+        self.angles = [angle_tables(pl, self.shift[moved], DEV) if pl.rot_dim else None for pl in self.planes]
         self.stubs = [torch.cat([s[pi].reshape(wl.n_layers, s[pi].shape[1], self.planes[pi].row_elems)
                                  for s in stubs], dim=1)
                       if len(stubs) else None for pi in range(len(pools))]
@@ -385,24 +366,16 @@ class _EveryRow:
                 pool = pools[pi][layer]
                 got = pool[np_, no].reshape(len(self.a_old), plane.row_elems)
                 src = pool[self.op, self.oo].reshape(len(self.a_old), plane.row_elems)
-                assert torch.equal(_bits(got[:, ~rot]), _bits(src[:, ~rot])), f"plane {pi} layer {layer}: non-rotary"
+                assert torch.equal(bits(got[:, ~rot]), bits(src[:, ~rot])), f"plane {pi} layer {layer}: non-rotary"
                 if self.stubs[pi] is not None:
                     gs = pool[sp, so].reshape(len(self.q_stub), plane.row_elems)
-                    assert torch.equal(_bits(gs), _bits(self.stubs[pi][layer, dev(self.stub_row)])), \
+                    assert torch.equal(bits(gs), bits(self.stubs[pi][layer, dev(self.stub_row)])), \
                         f"plane {pi} layer {layer}: replacement rows"
                 if not plane.rot_dim:
                     continue
                 g, b0 = got[:, rot], self.before[pi][layer]
-                assert torch.equal(_bits(g[~moved]), _bits(b0[~moved])), f"plane {pi} layer {layer}: shift-0 rows"
-                # every pair of a moved row turned by phi = shift * theta_i: with p its pair before
-                # and p' after, p.p' = |p|^2 cos(phi) and p x p' = |p|^2 sin(phi)
-                ia, ib, cs, sn = self.angles[pi]
-                gm, bm = g[moved].double(), b0[moved].double()
-                a, b, a2, b2 = bm[:, ia], bm[:, ib], gm[:, ia], gm[:, ib]
-                n2 = a * a + b * b
-                tol = (2.0 ** -7 if wl.dtype == "bf16" else 1e-5) * n2 + 1e-30
-                assert bool(((a * a2 + b * b2 - n2 * cs).abs() <= tol).all()), f"plane {pi} layer {layer}: pair angles (cos)"
-                assert bool(((a * b2 - b * a2 - n2 * sn).abs() <= tol).all()), f"plane {pi} layer {layer}: pair angles (sin)"
+                assert torch.equal(bits(g[~moved]), bits(b0[~moved])), f"plane {pi} layer {layer}: shift-0 rows"
+                assert_pairs_turned(b0[moved], g[moved], self.angles[pi], wl.dtype, f"plane {pi} layer {layer}")
             rows += len(self.a_old) + len(self.q_stub)
         print(f"[info] every row checked by properties: {rows} rows x {wl.n_layers} layers", flush=True)
 
