@@ -1,0 +1,46 @@
+"""The C header compiles as strict C99, its structs have the layout the Python binding's ctypes
+structures assume, and a C program linked against the library alone (no torch in the process)
+reaches every declared entry point (no GPU)."""
+
+import ctypes
+import os
+import shutil
+import subprocess
+
+import pytest
+
+from paper_2606_01065_amd import leyline as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def layout(tmp_path_factory):
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not available")
+    exe = str(tmp_path_factory.mktemp("abi") / "abi_layout")
+    libdir = os.path.dirname(L.LIB_PATH)
+    subprocess.run([gcc, "-std=c99", "-pedantic", "-Wall", "-Wextra", "-Werror", "-I" + os.path.join(ROOT, "include"),
+                    os.path.join(ROOT, "tests", "abi_layout.c"), "-L" + libdir, "-lleyline",
+                    "-Wl,-rpath," + libdir, "-o", exe], check=True)
+    # the library's own HIP dependency resolves from its RUNPATH or the ROCm install
+    env = dict(os.environ)
+    env["LD_LIBRARY_PATH"] = ":".join(p for p in (env.get("LD_LIBRARY_PATH", ""), "/opt/rocm/lib") if p)
+    out = subprocess.run([exe], capture_output=True, text=True, check=True, env=env, timeout=60).stdout
+    return dict(line.split(" ", 1) for line in out.strip().splitlines())
+
+
+@pytest.mark.parametrize("struct", [L.leyline_plane, L.leyline_cache, L.leyline_directive])
+def test_binding_structs_match_the_header(layout, struct):
+    name = struct.__name__
+    assert int(layout[name]) == ctypes.sizeof(struct), name
+    for field, _ in struct._fields_:
+        assert int(layout[f"{name}.{field}"]) == getattr(struct, field).offset, f"{name}.{field}"
+
+
+def test_c_program_reaches_every_entry_point(layout):
+    assert int(layout["entry_points"]) == len(L.SYMBOLS)
+    declared, loaded = layout["abi_version"].split()
+    assert int(declared) == int(loaded) == L.leyline_abi_version()
+    assert "overlap" in layout["strerror_overlap"]
