@@ -388,14 +388,19 @@ __device__ __forceinline__ void cs_commit(KCosSin* lcs, uint64_t c, int32_t n) {
 
 // Rounds and replacement copies: rows laid end to end, one unit per thread for CRPT rows (the
 // same column of consecutive rows, so one cos/sin lookup serves them all); blockIdx.z selects the
-// (job, plane) item.  A thread's data loads are issued before the workgroup stages its cos/sin
-// block in LDS, so the two memory latencies overlap.  Past the item's last row a thread loads
-// that last row again (every load issued without branching) and stores nothing.
+// (job, plane) item.  A rotating item's workgroup stages its cos/sin block in LDS after the
+// threads have issued their data loads, so that the two latencies overlap.  Past the item's last
+// row a thread loads that last row again (every load issued without branching) and stores
+// nothing.
 template <int ESZ>
 __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigParams P) {
     constexpr int EPC = Elt<ESZ>::EPC;
+    static_assert(KMAX_CS <= MOVE_TPB, "one cos/sin entry per thread");
     __shared__ KCosSin lcs[KMAX_CS];
-    const KItem& I = P.items[blockIdx.z];
+    // The item as a value: its fields come in one level of independent scalar loads (through a
+    // reference the compiler loaded them one by one between the branches below).
+    KItem I;
+    __builtin_memcpy(&I, &P.items[blockIdx.z], sizeof(KItem));
     const KPlane& pl = I.pl;
     const int64_t groups = (I.count + CRPT - 1) / CRPT;
     if (int64_t(blockIdx.x) * MOVE_TPB >= groups * pl.tpr) return;      // block past this item's rows
@@ -405,21 +410,13 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
     const int64_t r0 = int64_t(g) * CRPT;
     const bool active = r0 < I.count;
     char* lbase = pl.base + int64_t(layer) * pl.layer_stride;
-    const char* src;
-    char* dst;
-    int64_t src_step;
-    if (I.kind == KJOB_STUB) {
-        src = I.stub + int64_t(layer) * I.count * pl.row_bytes;
-        src_step = pl.row_bytes;
-        dst = lbase + I.dst0 * pl.token_stride;
-    } else {
-        src = lbase + I.src0 * pl.token_stride;
-        src_step = pl.token_stride;
-        dst = const_cast<char*>(src) + I.delta * pl.token_stride;
-    }
+    const bool stub = I.kind == KJOB_STUB;
+    const char* src = stub ? I.stub + int64_t(layer) * I.count * pl.row_bytes : lbase + I.src0 * pl.token_stride;
+    const int64_t src_step = stub ? int64_t(pl.row_bytes) : pl.token_stride;
+    char* dst = lbase + (stub ? I.dst0 : I.src0 + I.delta) * pl.token_stride;
     const bool rot = I.cs >= 0;                                    // block-uniform
-    if (!rot || (pl.rot == KROT_NEOX && !pl.neox_lanes)) {
-        // plain copies, and half-split two-chunk units (rare layouts): no early data load
+    if (pl.rot == KROT_NEOX && !pl.neox_lanes) {
+        // half-split two-chunk units (rare layouts; a thread's unit is not a single chunk)
         if (rot) {
             for (int i = threadIdx.x; i < pl.n_pairs; i += MOVE_TPB) lcs[i] = P.cs[I.cs + i];
             __syncthreads();
@@ -433,20 +430,26 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
         return;
     }
     const int64_t off = int64_t(u) * 16;
+    // narrow bands (a slice of each row): entry fetched before the data, barrier waits for no
+    // data; wide bands (most of the row rotates): staged after the data loads, so the barrier
+    // also lines up the workgroup's stores (measured faster there)
+    const bool early = rot && !pl.band_nt;
+    const uint64_t c = cs_fetch(P.cs, I.cs, early ? pl.n_pairs : 0);
     u32x4 v[CRPT];
 #pragma unroll
     for (int k = 0; k < CRPT; ++k) {
         const int64_t r = min(r0 + k, I.count - 1);
         v[k] = ld16(src + r * src_step + off);
     }
-    // staged after the data loads are issued (staging split around them, as the paged kernels
-    // do, measured 1 point slower on the GQA cache here)
-    for (int i = threadIdx.x; i < pl.n_pairs; i += MOVE_TPB) lcs[i] = P.cs[I.cs + i];
-    __syncthreads();
+    if (rot) {
+        if (early) cs_commit(lcs, c, pl.n_pairs);
+        else for (int i = threadIdx.x; i < pl.n_pairs; i += MOVE_TPB) lcs[i] = P.cs[I.cs + i];
+        __syncthreads();
+    }
     if (!active) return;
     const int32_t h = fdiv(u, pl.head_div);
     const int32_t j = u - h * pl.head_chunks - pl.rot_lo;
-    const bool in_band = h < pl.n_heads && j >= 0 && j < pl.rot_chunks;
+    const bool in_band = rot && h < pl.n_heads && j >= 0 && j < pl.rot_chunks;
 #pragma unroll
     for (int k = 0; k < CRPT; ++k) {
         if (r0 + k < I.count) {
