@@ -552,9 +552,14 @@ __global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KTileParam
     __syncthreads();
     const int32_t ticket = s_ticket;
     if (ticket >= P.n_tickets) return;                            // block-uniform
+    // The item owning the ticket: items hold ascending ticket ranges, so its index is the number
+    // of later items whose range starts at or before the ticket (one level of loads, no loop).
     int it = 0;
-    while (it + 1 < P.n_items && ticket >= P.items[it + 1].ticket0) ++it;
-    const KTileItem& I = P.items[it];
+#pragma unroll
+    for (int i = 1; i < KTILE_MAX_ITEMS; ++i) it += ticket >= P.ticket0[i] ? 1 : 0;
+    // the item as a value: its fields come in one level of independent scalar loads
+    KTileItem I;
+    __builtin_memcpy(&I, &P.items[it], sizeof(KTileItem));
     const KPlane& pl = P.planes[I.plane];
     const bool move = I.kind == KJOB_TILE;
     const int32_t local = ticket - I.ticket0;
@@ -1114,6 +1119,8 @@ static int launch_tiles(const leyline_cache* cache, const ContigSchedule& sched,
         std::memcpy(P.planes, planes, sizeof(KPlane) * size_t(n_planes));
         std::copy(tl.items.begin(), tl.items.end(), P.items);
         P.n_items = int32_t(tl.items.size());
+        for (int32_t i = 0; i < KTILE_MAX_ITEMS; ++i)
+            P.ticket0[i] = i < P.n_items ? P.items[i].ticket0 : INT32_MAX;
         P.n_tickets = int32_t(tl.tickets);
         P.counter = reinterpret_cast<int32_t*>(ws + 256 * int64_t(k));
         P.flags = reinterpret_cast<int32_t*>(ws + sched.ws_flags);

@@ -137,6 +137,7 @@ constexpr int KTILE_MAX_ITEMS = 24;
 struct KTileParams {
     KPlane planes[LEYLINE_MAX_PLANES];
     KTileItem items[KTILE_MAX_ITEMS];
+    int32_t ticket0[KTILE_MAX_ITEMS];   // items[i].ticket0, side by side; INT32_MAX past n_items
     int32_t n_items;
     int32_t n_tickets;
     int32_t* counter;        // ticket counter of this launch, zero before it
