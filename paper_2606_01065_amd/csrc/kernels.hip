@@ -10,10 +10,11 @@
 // travel in the kernel arguments (or the call's workspace) and are staged once per workgroup in
 // LDS.
 //
-// Access shape.  One thread moves one 16-byte chunk, and the chunks of the moved rows are laid
-// end to end over the threads, so every load and store instruction of a 64-wide wavefront
-// covers 1 KiB of consecutive bytes of whole rows; that is the shape that streams at the copy
-// ceiling of the chip.  For a half-split (NEOX) band the partner half of a chunk lives in
+// Access shape.  The 16-byte chunks of the moved rows are laid end to end over the threads, so
+// that every load and store instruction of a 64-wide wavefront covers about 1 KiB of whole rows
+// (a thread repeats its chunk position in a few rows or layers: two consecutive rows in the
+// round kernel, two layers in the paged kernels, eight strided chunks in a tile); that is the
+// shape that streams near the copy ceiling of the chip.  For a half-split (NEOX) band the partner half of a chunk lives in
 // another lane of the same wavefront and is exchanged with a lane shuffle instead of being
 // loaded twice.  Index arithmetic uses precomputed multiply-shift division.
 //
