@@ -1,7 +1,8 @@
 """The benchmark's byte accounting and its command-line contract (no GPU).
 
 Algorithmic bytes follow the KV size of a token: (kv_lora_rank + rope_dim) elements per layer for
-an MLA cache, K and V heads for GQA (the per-token byte formula of Sec. 4.1); a moved or
+an MLA cache (the per-token KV formula of the section "Deployment-cell evidence at the policy
+layer", paragraph on KV bytes attributable to the splice), K and V heads for GQA; a moved or
 assembled row is read once and written once, a re-used page only has its rotary bands rewritten.
 The paged accounting is checked against a count over the oracle's own page plan."""
 
