@@ -553,11 +553,7 @@ __global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KTileParam
     __syncthreads();
     const int32_t ticket = s_ticket;
     if (ticket >= P.n_tickets) return;                            // block-uniform
-    // The item owning the ticket: items hold ascending ticket ranges, so its index is the number
-    // of later items whose range starts at or before the ticket (one level of loads, no loop).
-    int it = 0;
-#pragma unroll
-    for (int i = 1; i < KTILE_MAX_ITEMS; ++i) it += ticket >= P.ticket0[i] ? 1 : 0;
+    const int32_t it = tile_item_of(P, ticket);
     // the item as a value: its fields come in one level of independent scalar loads
     KTileItem I;
     __builtin_memcpy(&I, &P.items[it], sizeof(KTileItem));
@@ -1120,8 +1116,7 @@ static int launch_tiles(const leyline_cache* cache, const ContigSchedule& sched,
         std::memcpy(P.planes, planes, sizeof(KPlane) * size_t(n_planes));
         std::copy(tl.items.begin(), tl.items.end(), P.items);
         P.n_items = int32_t(tl.items.size());
-        for (int32_t i = 0; i < KTILE_MAX_ITEMS; ++i)
-            P.ticket0[i] = i < P.n_items ? P.items[i].ticket0 : INT32_MAX;
+        tile_fill_ticket_table(P);
         P.n_tickets = int32_t(tl.tickets);
         P.counter = reinterpret_cast<int32_t*>(ws + 256 * int64_t(k));
         P.flags = reinterpret_cast<int32_t*>(ws + sched.ws_flags);

@@ -3,6 +3,7 @@
 // fixed-width integers, floats and raw pointers.
 #pragma once
 
+#include <climits>
 #include <cstdint>
 
 #include "leyline.h"
@@ -144,6 +145,21 @@ struct KTileParams {
     int32_t* flags;          // the call's flags, zero before the first tile launch
     const KCosSin* cs;       // the call's cos/sin table
 };
+
+// The side-by-side table of the items' first tickets (INT32_MAX past the last item), filled by
+// the host before a tile launch.
+inline void tile_fill_ticket_table(KTileParams& P) {
+    for (int32_t i = 0; i < KTILE_MAX_ITEMS; ++i) P.ticket0[i] = i < P.n_items ? P.items[i].ticket0 : INT32_MAX;
+}
+
+// The item of a tile launch that owns `ticket`: items hold ascending ticket ranges, so its index
+// is the number of later items whose range starts at or before the ticket (a fixed number of
+// independent reads, no loop-carried dependency).
+LEYLINE_HD inline int32_t tile_item_of(const KTileParams& P, int32_t ticket) {
+    int32_t it = 0;
+    for (int32_t i = 1; i < KTILE_MAX_ITEMS; ++i) it += ticket >= P.ticket0[i] ? 1 : 0;
+    return it;
+}
 
 LEYLINE_HD inline int64_t kmin64(int64_t a, int64_t b) { return a < b ? a : b; }
 LEYLINE_HD inline int64_t kmax64(int64_t a, int64_t b) { return a > b ? a : b; }

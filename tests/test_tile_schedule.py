@@ -2,8 +2,9 @@
 
 tests/tile_schedule_sim.cpp plans random multi-directive splices with the library's planner and
 runs every tile launch of each plan under randomly interleaved workgroups, using the kernel's own
-wait rule (tile_wait_flags): no load may see an overwritten row, no schedule may stall, and the
-rows must come out as the splice defines them.  Planted mistakes in the wait rule or the planner's
+ticket-to-item lookup (tile_item_of, checked for every ticket) and wait rule (tile_wait_flags): no
+load may see an overwritten row, no schedule may stall, and the rows must come out as the splice
+defines them.  Planted mistakes in the wait rule or the planner's
 wait lists (dropped cross-item waits, a missing tile of the shift, an off-by-one tile range) make
 it fail."""
 

@@ -144,6 +144,7 @@ int main(int argc, char** argv) {
             std::copy(tl.items.begin(), tl.items.end(), P.items);
             P.n_items = int32_t(tl.items.size());
             P.n_tickets = int32_t(tl.tickets);
+            tile_fill_ticket_table(P);
             // ticket -> (item, layer, order); flag -> ticket, for flags of this launch
             struct Tile { int item, layer, order; };
             std::vector<Tile> tiles(static_cast<size_t>(tl.tickets));
@@ -156,6 +157,7 @@ int main(int argc, char** argv) {
                 for (int l = 0; l < L; ++l)
                     for (int o = 0; o < I.n_tiles; ++o) {
                         const int64_t t = I.ticket0 + int64_t(l) * I.n_tiles + o;
+                        if (tile_item_of(P, int32_t(t)) != i) return fail("ticket to item lookup", ci);
                         tiles[size_t(t)] = Tile{i, l, o};
                         if (I.kind == KJOB_TILE) flag_ticket[size_t(I.flag0 + int64_t(l) * I.n_tiles + o)] = t;
                     }
