@@ -79,11 +79,16 @@ def test_rotate_delta_in_a_graph(L):
     _replay_and_compare(lambda: L.leyline_rotate_delta(cache, -4064, row0=100, n_rows=1500), t, pristine, eager)
 
 
-def test_paged_slot_splice_in_a_graph(L):
+@pytest.mark.parametrize("page,span,stub,n", [
+    (1, (300, 420), 24, 1500),      # token slots: REMAP rotation in place plus the stub rows
+    (16, (100, 137), 3, 600),       # 16-token pages: a gather of about 500 rows into fresh pages
+])
+def test_paged_small_splice_in_a_graph(L, page, span, stub, n):
     """A paged splice whose plan fits the kernel arguments (one sequence, one directive) and whose
-    gather is small enqueues one kernel: token-slot cache, REMAP rotation in place plus the stub
-    rows; the block table and freed list are outputs of the same launch."""
-    wl = W.Workload("graph_slots", 2, "bf16", [W.mla_plane()], [W.Dir(300, 420, 24)], [1500], page_size=1, seed=33)
+    gather is small enqueues one kernel; the block table and freed list are outputs of the same
+    launch."""
+    wl = W.Workload("graph_paged", 2, "bf16", [W.mla_plane()], [W.Dir(span[0], span[1], stub)], [n],
+                    page_size=page, seed=33)
     pools, bt, free, stubs = W.alloc_paged(wl, DEV)
     t = pools[0]
     pristine = t.clone()
@@ -95,7 +100,7 @@ def test_paged_slot_splice_in_a_graph(L):
     freed = torch.full((max(1, n_freed),), -7, dtype=torch.int32, device=DEV)
     ws = torch.empty(max(256, ws_bytes), dtype=torch.uint8, device=DEV)
     run = lambda: L.leyline_splice_paged(cache, wl.seq_lens, bt, bt_out, dirs, 1, free, freed, ws)
-    print(f"[case] graph paged slots ws={ws_bytes} freed={n_freed} fresh={fresh}", flush=True)
+    print(f"[case] graph paged page={page} ws={ws_bytes} freed={n_freed} fresh={fresh}", flush=True)
     run()
     torch.cuda.synchronize()
     eager, eager_bt, eager_freed = host(t), host(bt_out), host(freed)
