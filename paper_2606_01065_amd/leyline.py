@@ -289,7 +289,9 @@ def contig_workspace(cache: leyline_cache, seq_len: int, dirs, n_dirs: int, devi
 def leyline_splice_contig(cache: leyline_cache, seq_len: int, dirs, n_dirs: int, stream=None,
                           workspace=None) -> int:
     """Returns the new sequence length.  workspace: a device tensor of at least the queried size;
-    when None, one is allocated with torch on the cache's device if the splice needs it."""
+    when None, the call queries the size and allocates one with torch if the splice needs it
+    (a caller that splices repeatedly keeps one workspace instead and saves the extra planning
+    and allocation per call)."""
     if workspace is None:
         need = leyline_contig_query(cache, seq_len, dirs, n_dirs).workspace_bytes
         if need:
