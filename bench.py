@@ -34,6 +34,8 @@ PROFILES = os.path.join(ROOT, "profiles")
 CONTIG_KERNEL = "contig_move_kernel"
 CONTIG_TILE_KERNEL = "contig_tile_kernel"
 PAGED_KERNEL = "paged_data_kernel"
+ROTATE_KERNEL = "rotate_rows_kernel"
+ROTATE_REPLICAS = 4     # rotate-only: cache copies used round-robin (bands of two copies fit the last-level cache)
 COPY_KERNEL_HINT = "elementwise"        # torch's device copy kernel used for counter calibration
 
 
@@ -98,6 +100,15 @@ def contig_bytes(wl):
             moved += seg_end - d.span_end
         stub += d.stub_len
     return 2 * (moved + stub) * rb * wl.n_layers, moved
+
+
+def rotate_bytes(wl):
+    """Algorithmic bytes of one in-place re-anchoring: every rotary band of the listed rows read
+    and written once."""
+    esz = 2 if wl.dtype == "bf16" else 4
+    _, _, n = wl.rotate
+    band = sum(p.rot_dim * p.n_heads for p in wl.planes) * esz
+    return 2 * n * band * wl.n_layers, n
 
 
 def paged_bytes(wl, kinds, new_lens, bt_stride, L):
@@ -175,7 +186,11 @@ def main():
     specs = lambda planes: [L.PlaneSpec(t, p.n_heads, p.head_stride or p.row_elems, p.rot_offset,
                                         p.rot_dim, p.style, p.base) for p, t in zip(wl.planes, planes)]
 
-    if wl.page_size:
+    if wl.rotate:
+        step, kernel, alg_bytes, moved, launches, keep = setup_rotate(wl, dev, L, W, specs, stream)
+        layout = (f"contiguous, rotary bands re-anchored in place (no movement), {ROTATE_REPLICAS} cache "
+                  "copies round-robin")
+    elif wl.page_size:
         step, kernel, alg_bytes, moved, launches, keep = setup_paged(wl, dev, L, W, specs, stream)
         layout = (f"paged, {wl.page_size}-token pages, {len(wl.seq_lens)} sequences"
                   + (", copy-on-write" if wl.paged_flags else ""))
@@ -235,6 +250,7 @@ def main():
             "directives": [[d.seq, d.span_start, d.span_end, d.stub_len] for d in wl.dirs][:8],
             "moved_tokens": moved,
             "layout": layout,
+            **({"rotate_delta_row0_rows": list(wl.rotate)} if wl.rotate else {}),
         },
         "roofline": {
             "bound": "hbm",
@@ -285,6 +301,23 @@ def setup_contig(wl, dev, L, W, specs, stream, args):
     return step, kernel, alg_bytes, moved, launches, keep
 
 
+def setup_rotate(wl, dev, L, W, specs, stream):
+    import torch
+    base_planes, _ = W.alloc_contig(wl, dev)
+    replicas = [base_planes] + [[t.clone() for t in base_planes] for _ in range(1, ROTATE_REPLICAS)]
+    caches = [L.make_cache(specs(r)) for r in replicas]
+    delta, row0, n = wl.rotate
+    alg_bytes, moved = rotate_bytes(wl)
+    # one launch per access class of the rotary planes (narrow bands cached, wide ones streaming)
+    launches = len({2 * p.n_heads * p.rot_dim >= p.row_elems for p in wl.planes if p.rot_dim})
+
+    def step(i):
+        L.leyline_rotate_delta(caches[i % len(caches)], delta, row0=row0, n_rows=n, stream=stream)
+
+    torch.cuda.synchronize()
+    return step, ROTATE_KERNEL, alg_bytes, moved, launches, dict(rotate=True)
+
+
 def setup_paged(wl, dev, L, W, specs, stream):
     import torch
     pools, bt, free, stubs = W.alloc_paged(wl, dev)
@@ -332,7 +365,7 @@ def cpu_baseline(wl, keep, budget_s, moved):
     here."""
     import torch
     from oracle import splice_oracle as O
-    if keep.get("paged"):
+    if keep.get("paged") or keep.get("rotate"):
         return None
 
     def host(t):
@@ -426,6 +459,9 @@ def summarize(args):
                                               sum(-(-n // wl.page_size) for n in wl.seq_lens),
                                               wl.paged_flags)
         alg, _, kernel = paged_bytes(wl, kinds, new_lens, bt_stride, L)
+    elif wl.rotate:
+        alg, _ = rotate_bytes(wl)
+        kernel = ROTATE_KERNEL
     else:
         alg, _ = contig_bytes(wl)
         kernel = CONTIG_KERNEL
@@ -434,7 +470,7 @@ def summarize(args):
     splices = steps + _flag(args.command, "--warmup", 10) + min(steps, 20)
     stats = _read_csv(trace_dir, "kernel_stats")
     trace = _read_csv(trace_dir, "kernel_trace")
-    if not wl.page_size:
+    if not wl.page_size and not wl.rotate:
         # the contiguous kernel that took the most time (rounds, or ordered tiles)
         best = max((r for r in stats if CONTIG_KERNEL in r["Name"] or CONTIG_TILE_KERNEL in r["Name"]),
                    key=lambda r: float(r["TotalDurationNs"]), default=None)

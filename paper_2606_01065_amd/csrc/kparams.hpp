@@ -218,8 +218,8 @@ struct KPrepParams {
 };
 
 // ------------------------------------------------------------------------------ rotate-only --
-struct KRotateParams {
-    KPlane planes[LEYLINE_MAX_PLANES];
+// The rotation's scalars, side by side so that a workgroup reads them as one value.
+struct KRotateHead {
     int32_t n_planes;
     int32_t n_layers;
     int32_t page_size;       // 0: contiguous
@@ -229,6 +229,11 @@ struct KRotateParams {
     int64_t row0;
     int64_t n_rows;
     int32_t* status;         // device, nullable
+};
+
+struct KRotateParams {
+    KPlane planes[LEYLINE_MAX_PLANES];
+    KRotateHead h;
     KDiv rot_div[LEYLINE_MAX_PLANES];   // by rot_tpr (band units per row)
     KDiv page_div;           // by page_size (paged caches)
     int32_t rot_base[LEYLINE_MAX_PLANES + 1];   // workgroups of plane p: [rot_base[p], rot_base[p+1])

@@ -337,6 +337,44 @@ def test_rotate_delta(L, kind, dtype, paged):
             before[pi] = g.reshape(before[pi].shape)
 
 
+@pytest.mark.parametrize("name", ["mla_dsv3_rotate_32k", "gqa_llama3_8b_rotate_16k"])
+def test_rotate_delta_full_size(L, name):
+    """Re-anchoring in place at full size (the benchmark's rotate-only workloads): three whole
+    layers against the oracle; every layer by properties (listed rows' pairs turned by their
+    angle, every other element bit-identical)."""
+    wl = W.WORKLOADS[name]()
+    delta, row0, n = wl.rotate
+    planes_dev, _ = W.alloc_contig(wl, DEV)
+    before = [t.clone() for t in planes_dev]
+    layers = [0, wl.n_layers // 2, wl.n_layers - 1]
+    sel = torch.tensor(layers, device=DEV)
+    print(f"[case] {name}: rotate rows [{row0}, {row0 + n}) by {delta}", flush=True)
+    cache = L.make_cache(_specs(L, wl, planes_dev))
+    L.leyline_rotate_delta(cache, delta, row0=row0, n_rows=n)
+    torch.cuda.synchronize()
+    rows = torch.arange(row0, row0 + n, device=DEV)
+    for pi, desc in enumerate(wl.planes):
+        plane = oracle_plane(desc)
+        row = plane.row_elems
+        b = host(before[pi].index_select(0, sel)).reshape(len(layers), wl.capacity, row)
+        g = host(planes_dev[pi].index_select(0, sel)).reshape(len(layers), wl.capacity, row)
+        want = b.copy()
+        for i in range(len(layers)):
+            want[i, row0:row0 + n] = O.rotate_rows(b[i, row0:row0 + n], delta, plane, wl.dtype)
+        assert_rows_match(g, want, plane, wl.dtype, inputs=b, what=f"{name} plane {pi}")
+        rot = torch.from_numpy(PU.rotary_mask(plane)).to(DEV)
+        tables = PU.angle_tables(plane, np.full(n, delta), DEV) if plane.rot_dim else None
+        b4, af = before[pi].reshape(wl.n_layers, -1, row), planes_dev[pi].reshape(wl.n_layers, -1, row)
+        for layer in range(wl.n_layers):
+            what = f"{name} plane {pi} layer {layer}"
+            gl, bl = af[layer], b4[layer]
+            assert torch.equal(PU.bits(gl[:, ~rot]), PU.bits(bl[:, ~rot])), f"{what}: non-rotary"
+            assert torch.equal(PU.bits(gl[:row0]), PU.bits(bl[:row0])), f"{what}: rows before"
+            assert torch.equal(PU.bits(gl[row0 + n:]), PU.bits(bl[row0 + n:])), f"{what}: rows after"
+            if plane.rot_dim:
+                PU.assert_pairs_turned(bl[rows][:, rot], gl[rows][:, rot], tables, wl.dtype, what)
+
+
 def test_rotate_delta_flags_bad_rows(L):
     wl = _small_workload(random.Random(1), "mla", "bf16", 1, 64, [])
     planes_dev, _ = W.alloc_contig(wl, DEV, seed=4)

@@ -22,6 +22,9 @@ Workloads (MLA rows: latent c_kv[512] + K_pe[64]; GQA rows: 8 KV heads x 128):
                       the 32K MLA and 16K GQA splices on token-slot caches (page size 1)
   mla_dsv3_slots_cow_32k
                       the 32K MLA token-slot splice with copy-on-write (fresh slots downstream)
+  mla_dsv3_rotate_32k, gqa_llama3_8b_rotate_16k
+                      re-anchoring in place without movement: the downstream rows of the 32K MLA
+                      and 16K GQA splices rotated by their shifts
 """
 
 from __future__ import annotations
@@ -70,6 +73,7 @@ class Workload:
     page_size: int = 0            # 0: contiguous
     capacity: int = 0             # contiguous rows per layer
     paged_flags: int = 0          # paged splice flags (1: copy-on-write, no old page written)
+    rotate: Tuple[int, int, int] = None   # (delta, row0, n_rows): re-anchoring in place, no move
     seed: int = 0
     notes: dict = field(default_factory=dict)
 
@@ -176,6 +180,24 @@ def mla_dsv3_slots_cow_32k() -> Workload:
                     page_size=1, seed=w.seed, paged_flags=1)
 
 
+def mla_dsv3_rotate_32k() -> Workload:
+    """Re-anchoring without movement on the 32K MLA cache: the K_pe bands of the headline
+    splice's downstream rows rotated in place by its shift (rows and shift of mla_dsv3_32k)."""
+    w = mla_dsv3_32k()
+    d = w.dirs[0]
+    n = w.seq_lens[0]
+    return Workload("mla_dsv3_rotate_32k", w.n_layers, w.dtype, w.planes, [], w.seq_lens, capacity=n,
+                    rotate=(d.stub_len - (d.span_end - d.span_start), d.span_end, n - d.span_end), seed=w.seed)
+
+
+def gqa_llama3_8b_rotate_16k() -> Workload:
+    """Re-anchoring without movement on the 16K GQA cache: whole K rows of the downstream rows
+    [6144, 16384) rotated in place by -2024, V untouched."""
+    w = gqa_llama3_8b_16k()
+    return Workload("gqa_llama3_8b_rotate_16k", w.n_layers, w.dtype, w.planes, [], w.seq_lens,
+                    capacity=w.capacity, rotate=(-2024, 6144, 16384 - 6144), seed=w.seed)
+
+
 WORKLOADS = {
     "mla_1l_4k_f32": mla_1l_4k_f32,
     "mla_dsv3_32k": mla_dsv3_32k,
@@ -186,6 +208,8 @@ WORKLOADS = {
     "mla_dsv3_slots_32k": mla_dsv3_slots_32k,
     "gqa_llama3_8b_slots_16k": gqa_llama3_8b_slots_16k,
     "mla_dsv3_slots_cow_32k": mla_dsv3_slots_cow_32k,
+    "mla_dsv3_rotate_32k": mla_dsv3_rotate_32k,
+    "gqa_llama3_8b_rotate_16k": gqa_llama3_8b_rotate_16k,
 }
 
 
