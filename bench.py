@@ -36,6 +36,7 @@ CONTIG_TILE_KERNEL = "contig_tile_kernel"
 PAGED_KERNEL = "paged_data_kernel"
 ROTATE_KERNEL = "rotate_rows_kernel"
 ROTATE_REPLICAS = 4     # rotate-only: cache copies used round-robin (bands of two copies fit the last-level cache)
+PAGED_REPLICAS = 4      # paged: at most this many pool copies used round-robin
 COPY_KERNEL_HINT = "elementwise"        # torch's device copy kernel used for counter calibration
 
 
@@ -193,7 +194,8 @@ def main():
     elif wl.page_size:
         step, kernel, alg_bytes, moved, launches, keep = setup_paged(wl, dev, L, W, specs, stream)
         layout = (f"paged, {wl.page_size}-token pages, {len(wl.seq_lens)} sequences"
-                  + (", copy-on-write" if wl.paged_flags else ""))
+                  + (", copy-on-write" if wl.paged_flags else "")
+                  + (f", {keep['replicas']} pool copies round-robin" if keep["replicas"] > 1 else ""))
     else:
         step, kernel, alg_bytes, moved, launches, keep = setup_contig(wl, dev, L, W, specs, stream, args)
         layout = "contiguous in place"
@@ -321,7 +323,13 @@ def setup_rotate(wl, dev, L, W, specs, stream):
 def setup_paged(wl, dev, L, W, specs, stream):
     import torch
     pools, bt, free, stubs = W.alloc_paged(wl, dev)
-    cache = L.make_cache(specs(pools), paged=True)
+    # Copies of the pool used in turn (same tables), so that a splice whose data would fit the
+    # last-level cache does not find the previous step's rows there; as many as fit in 40 GB.
+    pool_bytes = sum(p.numel() * p.element_size() for p in pools)
+    n_rep = max(1, min(PAGED_REPLICAS, int(40e9 // pool_bytes)))
+    copies = [pools] + [[p.clone() for p in pools] for _ in range(1, n_rep)]
+    caches = [L.make_cache(specs(c), paged=True) for c in copies]
+    cache = caches[0]
     dirs = L.make_directives([dict(span_start=d.span_start, span_end=d.span_end, stub=stubs[j],
                                    seq=d.seq, stub_len=d.stub_len) for j, d in enumerate(wl.dirs)])
     nd = len(wl.dirs)
@@ -337,10 +345,10 @@ def setup_paged(wl, dev, L, W, specs, stream):
     # The paged splice reads old pages and writes fresh ones; re-running it on the same inputs
     # repeats the same work (remapped pages are rotated again, which does not change the bytes).
     def step(i):
-        L.leyline_splice_paged(cache, wl.seq_lens, bt, bt_out, dirs, nd, free, freed, ws, stream=stream,
-                               flags=fl)
+        L.leyline_splice_paged(caches[i % n_rep], wl.seq_lens, bt, bt_out, dirs, nd, free, freed, ws,
+                               stream=stream, flags=fl)
 
-    keep = dict(paged=True)
+    keep = dict(paged=True, replicas=n_rep)
     torch.cuda.synchronize()
     # one data launch per splice (gather of assembled pages and in-place rotation of remapped
     # ones) carries the bytes; the order and resolve launches of large gathers are inside the

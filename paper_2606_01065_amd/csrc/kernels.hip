@@ -95,17 +95,6 @@ __device__ __forceinline__ void st16(char* p, u32x4 v) {
 #endif
 }
 
-// Band kernels rotate a slice of each row in place.  When the slice is narrow (MLA: 128 of 1152
-// bytes) the cached forms are faster; when it is most of the row, the streaming forms.  The
-// choice is a template parameter: kernels are launched once per class of planes.
-template <bool NT> __device__ __forceinline__ u32x4 ld16_band(const char* p) {
-    if constexpr (NT) return ld16(p);
-    else return *reinterpret_cast<const u32x4*>(p);
-}
-template <bool NT> __device__ __forceinline__ void st16_band(char* p, u32x4 v) {
-    if constexpr (NT) st16(p, v);
-    else *reinterpret_cast<u32x4*>(p) = v;
-}
 
 // ----------------------------------------------------------------------- element helpers ---
 
@@ -323,19 +312,18 @@ __device__ __forceinline__ BandPos band_pos(const KPlane& pl, int32_t q) {
     return p;
 }
 
-template <bool NT>
 __device__ __forceinline__ void band_load(const BandPos& p, const char* row, int64_t lstride, int nl,
                                           u32x4 (&x)[PAGED_LPT], u32x4 (&y)[PAGED_LPT]) {
 #pragma unroll
     for (int l = 0; l < PAGED_LPT; ++l) {
         if (l < nl) {
-            x[l] = ld16_band<NT>(row + l * lstride + p.a);
-            if (p.two) y[l] = ld16_band<NT>(row + l * lstride + p.b);
+            x[l] = ld16(row + l * lstride + p.a);
+            if (p.two) y[l] = ld16(row + l * lstride + p.b);
         }
     }
 }
 
-template <int ESZ, bool NT>
+template <int ESZ>
 __device__ __forceinline__ void band_rotate_store(const KPlane& pl, const BandPos& p, char* row,
                                                   int64_t lstride, int nl, u32x4 (&x)[PAGED_LPT],
                                                   u32x4 (&y)[PAGED_LPT], const KCosSin* table, int32_t cs) {
@@ -345,11 +333,11 @@ __device__ __forceinline__ void band_rotate_store(const KPlane& pl, const BandPo
         if (l < nl) {
             if (p.two) {
                 rot_halves<ESZ>(x[l], y[l], table, cs + p.j * EPC);
-                st16_band<NT>(row + l * lstride + p.b, y[l]);
+                st16(row + l * lstride + p.b, y[l]);
             } else {
                 rotate_band_chunk<ESZ>(pl, x[l], p.j, table, cs);
             }
-            st16_band<NT>(row + l * lstride + p.a, x[l]);
+            st16(row + l * lstride + p.a, x[l]);
         }
     }
 }
@@ -434,7 +422,7 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
     // narrow bands (a slice of each row): entry fetched before the data, barrier waits for no
     // data; wide bands (most of the row rotates): staged after the data loads, so the barrier
     // also lines up the workgroup's stores (measured faster there)
-    const bool early = rot && !pl.band_nt;
+    const bool early = rot && !pl.band_wide;
     const uint64_t c = cs_fetch(P.cs, I.cs, early ? pl.n_pairs : 0);
     u32x4 v[CRPT];
 #pragma unroll
@@ -626,7 +614,7 @@ __global__ __launch_bounds__(TPB) void tile_prep_kernel(const KPrepParams Q) {
 // cos/sin staged in LDS.
 // SOLO: only plane 0 has work in this launch, so no workgroup looks its plane up (one level of
 // dependent scalar loads less before the data loads).
-template <int ESZ, bool NT, bool SOLO, bool PAGED>
+template <int ESZ, bool SOLO, bool PAGED>
 __global__ __launch_bounds__(PAGED_TPB) void rotate_rows_kernel(const KRotateParams P) {
     __shared__ KCosSin lcs[KMAX_CS];
     // the call's scalars as one value: one level of independent scalar loads
@@ -657,11 +645,11 @@ __global__ __launch_bounds__(PAGED_TPB) void rotate_rows_kernel(const KRotatePar
     static_assert(KMAX_CS <= PAGED_TPB, "one cos/sin entry per thread");
     const uint64_t c = cs_fetch(P.cs, pl.cs_off, pl.n_pairs);
     u32x4 x[PAGED_LPT], y[PAGED_LPT];
-    if (active) band_load<NT>(bp, r, pl.layer_stride, nl, x, y);
+    if (active) band_load(bp, r, pl.layer_stride, nl, x, y);
     cs_commit(lcs, c, pl.n_pairs);
     __syncthreads();
     if (!active) return;
-    band_rotate_store<ESZ, NT>(pl, bp, r, pl.layer_stride, nl, x, y, lcs, 0);
+    band_rotate_store<ESZ>(pl, bp, r, pl.layer_stride, nl, x, y, lcs, 0);
 }
 
 // ------------------------------------------------------------------------------ paged splice ---
@@ -944,7 +932,7 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, const Pl
 // to end, PAGED_LPT layers per thread, rotated in place.  The workgroup stages the cos/sin block
 // of its first page's shift in LDS; rows with another shift (where runs meet) read the plan's
 // table.
-template <int ESZ, bool NT>
+template <int ESZ>
 __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const PlanView& V, int plane, int32_t bx,
                                                   KCosSin* lcs) {
     const KPlane& pl = P.planes[plane];
@@ -984,20 +972,20 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const P
                 int64_t(r) * pl.token_stride;
     const BandPos bp = band_pos(pl, f - r * pl.rot_tpr);
     u32x4 x[PAGED_LPT], y[PAGED_LPT];
-    if (active) band_load<NT>(bp, row, pl.layer_stride, nl, x, y);
+    if (active) band_load(bp, row, pl.layer_stride, nl, x, y);
     cs_commit(lcs, c, cs0 >= 0 ? pl.n_pairs : 0);
     __syncthreads();
     if (!active) return;
-    if (e.cs == cs0) band_rotate_store<ESZ, NT>(pl, bp, row, pl.layer_stride, nl, x, y, lcs, 0);
-    else band_rotate_store<ESZ, NT>(pl, bp, row, pl.layer_stride, nl, x, y, V.cs, e.cs + pl.cs_off);
+    if (e.cs == cs0) band_rotate_store<ESZ>(pl, bp, row, pl.layer_stride, nl, x, y, lcs, 0);
+    else band_rotate_store<ESZ>(pl, bp, row, pl.layer_stride, nl, x, y, V.cs, e.cs + pl.cs_off);
 }
 
-// The first workgroups gather ASSEMBLE rows (plane by plane), the next rotate REMAP pages of the
-// planes in access class NT (plane by plane), the last P.table_x per layer group write the block
-// tables and the freed list; planes without work get no workgroups.  SOLO: only plane 0 has work
+// The first workgroups gather ASSEMBLE rows (plane by plane), the next rotate REMAP pages' rotary
+// bands (plane by plane), the last P.table_x per layer group write the block tables and the
+// freed list; planes without work get no workgroups.  SOLO: only plane 0 has work
 // in this launch, so no workgroup looks its plane up.  INLINE: the gather resolves its rows (no
 // row table) and the launch may carry table work.
-template <int ESZ, bool NT, bool SOLO, bool INLINE>
+template <int ESZ, bool SOLO, bool INLINE>
 __global__ __launch_bounds__(PAGED_TPB) void paged_data_kernel(const KPagedParams P) {
     __shared__ KCosSin lcs[KMAX_CS];
     const PlanView V = plan_view(P);
@@ -1012,7 +1000,7 @@ __global__ __launch_bounds__(PAGED_TPB) void paged_data_kernel(const KPagedParam
     const int32_t remaps = SOLO ? P.remap_base[1] : P.remap_base[P.n_planes];
     if (bx < remaps) {
         const int p = SOLO ? 0 : plane_of(P.remap_base, P.n_planes, bx);
-        paged_remap_block<ESZ, NT>(P, V, p, bx - P.remap_base[p], lcs);
+        paged_remap_block<ESZ>(P, V, p, bx - P.remap_base[p], lcs);
         return;
     }
     // table work, spread over the layer groups
@@ -1248,20 +1236,15 @@ extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len
     return LEYLINE_OK;
 }
 
-// The rotation kernel variant for (dtype, access class, one plane only, paged cache).
-static int launch_rotate(bool bf16, bool nt, bool solo, bool paged, dim3 grid, hipStream_t s,
-                         const KRotateParams& P) {
+// The rotation kernel variant for (dtype, one plane only, paged cache).
+static int launch_rotate(bool bf16, bool solo, bool paged, dim3 grid, hipStream_t s, const KRotateParams& P) {
     using K = void (*)(KRotateParams);
-    static const K table[2][2][2][2] = {
-        {{{rotate_rows_kernel<4, false, false, false>, rotate_rows_kernel<4, false, false, true>},
-          {rotate_rows_kernel<4, false, true, false>, rotate_rows_kernel<4, false, true, true>}},
-         {{rotate_rows_kernel<4, true, false, false>, rotate_rows_kernel<4, true, false, true>},
-          {rotate_rows_kernel<4, true, true, false>, rotate_rows_kernel<4, true, true, true>}}},
-        {{{rotate_rows_kernel<2, false, false, false>, rotate_rows_kernel<2, false, false, true>},
-          {rotate_rows_kernel<2, false, true, false>, rotate_rows_kernel<2, false, true, true>}},
-         {{rotate_rows_kernel<2, true, false, false>, rotate_rows_kernel<2, true, false, true>},
-          {rotate_rows_kernel<2, true, true, false>, rotate_rows_kernel<2, true, true, true>}}}};
-    return launch(table[bf16][nt][solo][paged], grid, s, P, PAGED_TPB);
+    static const K table[2][2][2] = {
+        {{rotate_rows_kernel<4, false, false>, rotate_rows_kernel<4, false, true>},
+         {rotate_rows_kernel<4, true, false>, rotate_rows_kernel<4, true, true>}},
+        {{rotate_rows_kernel<2, false, false>, rotate_rows_kernel<2, false, true>},
+         {rotate_rows_kernel<2, true, false>, rotate_rows_kernel<2, true, true>}}};
+    return launch(table[bf16][solo][paged], grid, s, P, PAGED_TPB);
 }
 
 extern "C" int leyline_rotate_delta(const leyline_cache* cache, int64_t delta,
@@ -1302,42 +1285,30 @@ extern "C" int leyline_rotate_delta(const leyline_cache* cache, int64_t delta,
     std::copy(cs.begin(), cs.end(), P.cs);
     hipStream_t s = static_cast<hipStream_t>(stream);
     const bool bf16 = cache->dtype == LEYLINE_BF16;
-    // one launch per access class present among the rotary planes; each launch lays out the
-    // workgroups of its planes one plane after another
-    for (int nt = 1; nt >= 0; --nt) {
-        int64_t total = 0;
-        P.rot_base[0] = 0;
-        for (int p = 0; p < n_planes; ++p) {
-            if (planes[p].rot_tpr > 0 && planes[p].band_nt == nt)
-                total += (n_rows * planes[p].rot_tpr + PAGED_TPB - 1) / PAGED_TPB;
-            if (total > INT32_MAX - 1024) return LEYLINE_E_INVAL;
-            P.rot_base[p + 1] = int32_t(total);
-        }
-        if (total == 0) continue;
-        const dim3 grid(unsigned(total), unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT), 1);
-        const bool solo = P.rot_base[1] == total;                        // plane 0 only
-        // narrow bands: cached accesses on paged caches (scattered pages), streaming ones on
-        // contiguous caches (measured faster there: 56% -> 60% of peak on the 32K MLA cache)
-        rc = launch_rotate(bf16, nt != 0 || !paged, solo, paged, grid, s, P);
-        if (rc) return rc;
+    // one launch: the workgroups of each rotary plane after those of the previous one
+    int64_t total = 0;
+    P.rot_base[0] = 0;
+    for (int p = 0; p < n_planes; ++p) {
+        if (planes[p].rot_tpr > 0) total += (n_rows * planes[p].rot_tpr + PAGED_TPB - 1) / PAGED_TPB;
+        if (total > INT32_MAX - 1024) return LEYLINE_E_INVAL;
+        P.rot_base[p + 1] = int32_t(total);
     }
+    const dim3 grid(unsigned(total), unsigned((cache->n_layers + PAGED_LPT - 1) / PAGED_LPT), 1);
+    const bool solo = P.rot_base[1] == total;                            // plane 0 only
+    rc = launch_rotate(bf16, solo, paged, grid, s, P);
+    if (rc) return rc;
     return LEYLINE_OK;
 }
 
-// The paged data kernel variant for (dtype, access class, one plane only, inline rows).
-static int launch_paged_data(bool bf16, bool nt, bool solo, bool inl, dim3 grid, hipStream_t s,
-                             const KPagedParams& P) {
+// The paged data kernel variant for (dtype, one plane only, inline rows).
+static int launch_paged_data(bool bf16, bool solo, bool inl, dim3 grid, hipStream_t s, const KPagedParams& P) {
     using K = void (*)(KPagedParams);
-    static const K table[2][2][2][2] = {
-        {{{paged_data_kernel<4, false, false, false>, paged_data_kernel<4, false, false, true>},
-          {paged_data_kernel<4, false, true, false>, paged_data_kernel<4, false, true, true>}},
-         {{paged_data_kernel<4, true, false, false>, paged_data_kernel<4, true, false, true>},
-          {paged_data_kernel<4, true, true, false>, paged_data_kernel<4, true, true, true>}}},
-        {{{paged_data_kernel<2, false, false, false>, paged_data_kernel<2, false, false, true>},
-          {paged_data_kernel<2, false, true, false>, paged_data_kernel<2, false, true, true>}},
-         {{paged_data_kernel<2, true, false, false>, paged_data_kernel<2, true, false, true>},
-          {paged_data_kernel<2, true, true, false>, paged_data_kernel<2, true, true, true>}}}};
-    return launch(table[bf16][nt][solo][inl], grid, s, P, PAGED_TPB);
+    static const K table[2][2][2] = {
+        {{paged_data_kernel<4, false, false>, paged_data_kernel<4, false, true>},
+         {paged_data_kernel<4, true, false>, paged_data_kernel<4, true, true>}},
+        {{paged_data_kernel<2, false, false>, paged_data_kernel<2, false, true>},
+         {paged_data_kernel<2, true, false>, paged_data_kernel<2, true, true>}}};
+    return launch(table[bf16][solo][inl], grid, s, P, PAGED_TPB);
 }
 
 extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, const int32_t* seq_lens,
@@ -1402,14 +1373,12 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         P.n_remap = t.n_remap;
         P.n_rows = t.n_rows;
         int32_t max_tpr = 1, max_upp = 1;
-        bool any_band[2] = {false, false};
         for (int p = 0; p < n_planes; ++p) {
             const int32_t upp = cache->page_size * planes[p].rot_tpr;
             max_tpr = std::max(max_tpr, planes[p].tpr);
             max_upp = std::max(max_upp, upp);
             P.remap_div[p] = make_div(std::max(1, upp));
             P.rot_div[p] = make_div(std::max(1, planes[p].rot_tpr));
-            if (planes[p].rot_tpr > 0) any_band[planes[p].band_nt ? 1 : 0] = true;
         }
         P.capacity = cache->capacity;
         // a plan small enough travels in the kernel arguments; otherwise it was uploaded above
@@ -1461,32 +1430,23 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
             // the first data launch writes the tables, spread over its layer groups
             P.table_x = int32_t(((n_tables + PAGED_TPB - 1) / PAGED_TPB + layer_groups - 1) / layer_groups);
         }
-        // data kernel: gather workgroups, then REMAP workgroups, once per access class of the
-        // rotary planes; the gather goes with the first class that has REMAP work (or alone)
-        int gather_class = 1;
-        if (t.n_remap > 0 && !any_band[1] && any_band[0]) gather_class = 0;
-        const dim3 layers(1, layer_groups, 1);
-        bool tables_pending = P.table_x > 0;
-        for (int nt = 1; nt >= 0; --nt) {
-            int64_t mb = 0, rb = 0;
-            P.move_base[0] = P.remap_base[0] = 0;
-            for (int p = 0; p < n_planes; ++p) {
-                if (nt == gather_class && t.n_rows > 0)
-                    mb += (int64_t(t.n_rows) * planes[p].tpr + PAGED_TPB - 1) / PAGED_TPB;
-                if (t.n_remap > 0 && planes[p].rot_tpr > 0 && planes[p].band_nt == nt)
-                    rb += (int64_t(t.n_remap) * cache->page_size * planes[p].rot_tpr + PAGED_TPB - 1) / PAGED_TPB;
-                if (mb > INT32_MAX - 1024 || rb > INT32_MAX - 1024 || mb + rb > INT32_MAX - 1024)
-                    return LEYLINE_E_INVAL;
-                P.move_base[p + 1] = int32_t(mb);
-                P.remap_base[p + 1] = int32_t(rb);
-            }
-            // the table work goes with the first launch, or alone in the last pass
-            if (mb + rb == 0 && !(tables_pending && nt == 0)) continue;
-            if (!tables_pending) P.table_x = 0;
-            tables_pending = false;
-            const dim3 grid(unsigned(mb + rb + P.table_x), layers.y, 1);
+        // data kernel, one launch: gather workgroups, then the REMAP workgroups of every rotary
+        // plane, then (small gathers) the table work
+        int64_t mb = 0, rb = 0;
+        P.move_base[0] = P.remap_base[0] = 0;
+        for (int p = 0; p < n_planes; ++p) {
+            if (t.n_rows > 0) mb += (int64_t(t.n_rows) * planes[p].tpr + PAGED_TPB - 1) / PAGED_TPB;
+            if (t.n_remap > 0 && planes[p].rot_tpr > 0)
+                rb += (int64_t(t.n_remap) * cache->page_size * planes[p].rot_tpr + PAGED_TPB - 1) / PAGED_TPB;
+            if (mb > INT32_MAX - 1024 || rb > INT32_MAX - 1024 || mb + rb > INT32_MAX - 1024)
+                return LEYLINE_E_INVAL;
+            P.move_base[p + 1] = int32_t(mb);
+            P.remap_base[p + 1] = int32_t(rb);
+        }
+        if (mb + rb + P.table_x > 0) {
+            const dim3 grid(unsigned(mb + rb + P.table_x), layer_groups, 1);
             const bool solo = P.move_base[1] == mb && P.remap_base[1] == rb;   // plane 0 only
-            rc = launch_paged_data(bf16, nt != 0, solo, !row_table, grid, s, P);
+            rc = launch_paged_data(bf16, solo, !row_table, grid, s, P);
             if (rc) return rc;
         }
     }

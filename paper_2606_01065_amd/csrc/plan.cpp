@@ -100,9 +100,7 @@ int describe_cache(const leyline_cache* cache, bool paged, KPlane out[LEYLINE_MA
                 k.neox_lanes = ok ? 1 : 0;
                 if (!ok) k.tpr = k.row_chunks - k.n_heads * (k.rot_chunks / 2);
             }
-            // in-place band rotation streams when the bands make up at least half of the row;
-            // narrower slices (MLA: 128 of 1152 bytes) run faster through the caches
-            k.band_nt = (2 * k.n_heads * k.rot_chunks >= k.row_chunks) ? 1 : 0;
+            k.band_wide = (2 * k.n_heads * k.rot_chunks >= k.row_chunks) ? 1 : 0;
             // rotary-only kernels pack the bands of consecutive heads and rows back to back
             k.band_tpr = (neox && !(k.rot_chunks <= 64 && !(k.rot_chunks & (k.rot_chunks - 1))))
                              ? k.rot_chunks / 2 : k.rot_chunks;
