@@ -310,8 +310,7 @@ def setup_rotate(wl, dev, L, W, specs, stream):
     caches = [L.make_cache(specs(r)) for r in replicas]
     delta, row0, n = wl.rotate
     alg_bytes, moved = rotate_bytes(wl)
-    # one launch per access class of the rotary planes (narrow bands cached, wide ones streaming)
-    launches = len({2 * p.n_heads * p.rot_dim >= p.row_elems for p in wl.planes if p.rot_dim})
+    launches = 1                                  # every rotary plane in one launch
 
     def step(i):
         L.leyline_rotate_delta(caches[i % len(caches)], delta, row0=row0, n_rows=n, stream=stream)
