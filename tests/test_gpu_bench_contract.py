@@ -1,0 +1,53 @@
+"""The benchmark's output contract: one JSON line with the fields the round driver reads, a
+roofline object for the dominant kernel and, for the default workload, the oracle's CPU baseline."""
+
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _bench(*args):
+    print(f"[case] bench.py {' '.join(args)}", flush=True)
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args], capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode == 0, r.stderr[-3000:]
+    return json.loads(r.stdout.strip().splitlines()[-1])
+
+
+def _check_common(d, steps, warmup):
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
+                "scaling", "vs_baseline", "dtype", "data", "config", "roofline"):
+        assert key in d, key
+    assert d["n_gpus"] == 1 and d["steps"] == steps and d["warmup"] == warmup
+    assert d["unit"] == "tokens/s" and d["higher_is_better"] is True and d["scaling"] == "weak"
+    assert d["value"] > 0 and d["ms_per_step"] > 0
+    assert abs(d["value"] - d["config"]["moved_tokens"] / (d["ms_per_step"] * 1e-3)) <= 1e-6 * d["value"]
+    r = d["roofline"]
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    assert abs(r["frac"] - r["achieved"] / r["peak"]) < 1e-12
+    assert abs(r["achieved"] - r["algorithmic_bytes_per_splice"] / (r["splice_ms"] * 1e-3) / 1e9) <= 1e-6 * r["achieved"]
+    assert r["traffic"] is None or r["traffic"] > 0
+    assert isinstance(d["config"]["workload"], str)
+
+
+def test_default_run_reports_roofline_and_cpu_baseline():
+    d = _bench("--steps", "3", "--warmup", "1", "--cpu-seconds", "1")
+    _check_common(d, 3, 1)
+    assert d["config"]["workload"] == "mla_dsv3_32k" and d["dtype"] == "bf16"
+    c = d["cpu_baseline"]
+    assert c["kind"] == "oracle" and c["unit"] == "tokens/s" and c["value"] > 0
+    assert isinstance(c["cores"], int) and c["cores"] >= 1 and c["sample"]
+
+
+@pytest.mark.parametrize("workload", ["mla_dsv3_slots_32k", "gqa_llama3_8b_rotate_16k", "mla_dsv3_32k_edits8"])
+def test_other_workloads_keep_the_contract(workload):
+    d = _bench("--workload", workload, "--steps", "3", "--warmup", "1", "--no-cpu-baseline")
+    _check_common(d, 3, 1)
+    assert d["config"]["workload"] == workload and "cpu_baseline" not in d
