@@ -78,8 +78,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-// 16-byte vector accesses.  Moved rows and rotated bands are touched exactly once per call, so the streaming
-// (nontemporal) forms keep them from displacing other data in the caches.
+// 16-byte vector accesses.  Moved rows and rotated bands are touched exactly once per call, so
+// the streaming (nontemporal) forms keep them from displacing other data in the caches.
 __device__ __forceinline__ u32x4 ld16(const char* p) {
 #if LEYLINE_NT_LOAD
     return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
