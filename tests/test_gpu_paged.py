@@ -493,18 +493,29 @@ def test_token_slot_copy_on_write_full(L):
     assert kinds.count(O.IDENTITY) == d.span_start
 
 
-def test_paged_131k_copy_on_write_full(L):
-    """The 8-directive 131K-token splice on 64-token pages with copy-on-write: no page is re-used
-    with a shift (whole-page shifts are assembled too) and no old page is written."""
+def _whole_page_shift_131k(flags):
     base = W.mla_dsv3_paged_131k()
-    # replacements sized so that every shift is a whole number of pages: in place, the downstream
-    # pages would be re-used (REMAP); copy-on-write assembles them into fresh pages instead
+    # replacements sized so that every shift is a whole number of pages: downstream pages are
+    # re-used in place (REMAP) unless copy-on-write asks for fresh ones
     dirs = [W.Dir(d.span_start, d.span_end, (d.span_end - d.span_start) % 64) for d in base.dirs]
     odirs = [O.Directive(d.span_start, d.span_end, d.stub_len) for d in dirs]
     assert any(k == O.REMAP for k in O.plan_paged(base.seq_lens, odirs, 64)[0].kinds)
-    wl = W.Workload("mla_dsv3_paged_131k_cow", base.n_layers, base.dtype, base.planes, dirs, base.seq_lens,
-                    page_size=base.page_size, paged_flags=L.PAGED_COPY_ON_WRITE, seed=base.seed)
-    pools, bt, bt_out, new_lens, plans = _check_sampled(L, wl, seed=23)
+    return W.Workload("mla_dsv3_paged_131k_page_shifts", base.n_layers, base.dtype, base.planes, dirs,
+                      base.seq_lens, page_size=base.page_size, paged_flags=flags, seed=base.seed)
+
+
+def test_paged_131k_whole_page_shifts_full(L):
+    """The 8-directive 131K-token splice with whole-page shifts: about 1400 downstream pages keep
+    their physical page and have their K_pe bands rotated in place."""
+    pools, bt, bt_out, new_lens, plans = _check_sampled(L, _whole_page_shift_131k(0), seed=29)
+    kinds = [k for p in plans for k in p.kinds]
+    assert kinds.count(O.REMAP) > 1000
+
+
+def test_paged_131k_copy_on_write_full(L):
+    """The 8-directive 131K-token splice on 64-token pages with copy-on-write: no page is re-used
+    with a shift (whole-page shifts are assembled too) and no old page is written."""
+    pools, bt, bt_out, new_lens, plans = _check_sampled(L, _whole_page_shift_131k(L.PAGED_COPY_ON_WRITE), seed=23)
     kinds = [k for p in plans for k in p.kinds]
     assert kinds.count(O.REMAP) == 0 and kinds.count(O.ASSEMBLE) > 0
 
