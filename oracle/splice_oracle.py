@@ -107,13 +107,20 @@ def encode(x: np.ndarray, dtype: str) -> np.ndarray:
 
 
 def ulp(x64: np.ndarray, dtype: str) -> np.ndarray:
-    """Spacing of the storage format at |x| (used by tests to express tolerances)."""
+    """Spacing of the storage format at |x|: for a storage value x, the gap between |x| and the
+    next storage value away from zero (used by tests to express tolerances).
+
+    A binade [2**(e-1), 2**e) of bf16 holds 2**7 values (8 significant bits), so its spacing is
+    2**(e-8); float32 (24 significant bits) has 2**(e-24).  Zero and the subnormals share the
+    spacing of the smallest normal binade (bf16 2**-133, float32 2**-149).
+    """
     mag = np.abs(np.asarray(x64, dtype=np.float64))
-    _, e = np.frexp(mag)
+    _, e = np.frexp(mag)                          # mag = m * 2**e, m in [0.5, 1); frexp(0) -> e = 0
+    e = np.where(mag == 0, -125, np.maximum(e, -125))
     if dtype == BF16:
-        return np.ldexp(1.0, np.maximum(e, -125) - 8)
+        return np.ldexp(1.0, e - 8)
     if dtype == F32:
-        return np.ldexp(1.0, np.maximum(e, -125) - 24)
+        return np.ldexp(1.0, e - 24)
     raise ValueError(dtype)
 
 

@@ -58,6 +58,11 @@ MUTANTS = [
      "bf16 ties away from zero"),
     ("encode", "quantum = np.ldexp(1.0, e - 8)", "quantum = np.ldexp(1.0, e - 7)", "bf16 with 7 significant bits"),
     ("encode", "e = np.maximum(e, -125)", "e = np.maximum(e, -100)", "bf16 subnormal range"),
+    # the spacing that sets every bf16 / f32 parity tolerance
+    ("ulp", "return np.ldexp(1.0, e - 8)", "return np.ldexp(1.0, e - 7)", "bf16 ulp twice the spacing"),
+    ("ulp", "np.maximum(e, -125))", "np.maximum(e, -126))", "bf16 / f32 subnormal spacing halved"),
+    ("ulp", "np.where(mag == 0, -125,", "np.where(mag == 0, 0,", "spacing at zero taken from binade 0"),
+    ("ulp", "return np.ldexp(1.0, e - 24)", "return np.ldexp(1.0, e - 23)", "f32 ulp twice the spacing"),
     # directive checks
     ("check_directives", "if d.span_start < prev_end:", "if d.span_start < prev_end - 1:", "overlap by one accepted"),
     ("check_directives", "if not (0 <= d.span_start <= d.span_end <= n):",

@@ -240,6 +240,38 @@ def test_bf16_ties_round_to_even():
                           [-2.5, 0.15625])
 
 
+def _bf16_values(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns -> float64 through torch's own bf16 type (not the oracle's decode)."""
+    t = torch.from_numpy(np.asarray(bits, dtype=np.uint16).view(np.int16)).view(torch.bfloat16)
+    return t.to(torch.float64).numpy()
+
+
+def test_bf16_ulp_is_the_gap_to_the_next_value():
+    """ulp() sets every bf16 parity tolerance (the one-ulp bar of App. "bf16 K-storage precision
+    floor").  For every finite non-negative bf16 pattern b (zero and subnormals included),
+    ulp(value(b)) must equal value(b + 1) - value(b), and ulp(-x) must equal ulp(x)."""
+    b = np.arange(0, 0x7F7F, dtype=np.uint16)            # 0 .. one below the largest finite
+    x = _bf16_values(b)
+    gap = _bf16_values(b + 1) - x
+    assert np.array_equal(O.ulp(x, O.BF16), gap)
+    assert np.array_equal(O.ulp(-x, O.BF16), gap)
+    assert O.ulp(np.array([0.0]), O.BF16)[0] == 2.0 ** -133
+    assert O.ulp(np.array([1.0]), O.BF16)[0] == 2.0 ** -7
+
+
+def test_f32_ulp_is_the_gap_to_the_next_value():
+    """The same for float32 storage, against numpy's nextafter: random finite patterns, every
+    binade edge (2**k and its predecessor), subnormals and zero."""
+    rng = np.random.default_rng(21)
+    bits = rng.integers(0, 0x7F7FFFFF, size=200000, dtype=np.uint32)
+    edges = np.ldexp(np.float32(1.0), np.arange(-149, 128)).astype(np.float32)
+    below = np.nextafter(edges, np.float32(0.0))
+    x = np.concatenate([bits.view(np.float32), edges, below, np.float32([0.0, 1e-45, 1e-40, 1.0, 3.0])])
+    gap = np.nextafter(x, np.float32(np.inf)).astype(np.float64) - x.astype(np.float64)
+    assert np.array_equal(O.ulp(x.astype(np.float64), O.F32), gap)
+    assert np.array_equal(O.ulp(-x.astype(np.float64), O.F32), gap)
+
+
 def test_delta_zero_segment_is_bit_identical():
     rng = np.random.default_rng(8)
     plane = O.mla_plane()
