@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define LEYLINE_ABI_VERSION 2
+#define LEYLINE_ABI_VERSION 3
 #define LEYLINE_MAX_PLANES 4
 
 enum {
@@ -83,8 +83,10 @@ enum { LEYLINE_PAGED_COPY_ON_WRITE = 1 };
 
 /* Device-side status bits a kernel may OR into the optional device_status word. */
 enum {
-    LEYLINE_STATUS_BAD_PAGE = 1,  /* a block-table or free-list entry was outside [0, capacity) */
-    LEYLINE_STATUS_BAD_ROW = 2    /* a row index given to leyline_rotate_delta was out of range  */
+    LEYLINE_STATUS_BAD_PAGE = 1,     /* a block-table or free-list entry was outside [0, capacity) */
+    LEYLINE_STATUS_BAD_ROW = 2,      /* a row index given to leyline_rotate_delta was out of range  */
+    LEYLINE_STATUS_TILE_TIMEOUT = 4  /* an ordered tile of a contiguous splice gave up waiting for  */
+                                     /* a tile it depends on (see leyline_splice_contig)           */
 };
 
 /*
@@ -179,6 +181,12 @@ int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
  * call's cos/sin table.  The call writes it on `stream` before use; reuse it only after the
  * stream has passed this call, and do not share one workspace between calls that may run at the
  * same time.
+ * device_status: device int32, nullable.  A tile waits for the tiles whose source rows its
+ * destination overlaps; each wait is bounded (a few hundred milliseconds at least, where a
+ * correct schedule waits microseconds).  A tile that gives up ORs LEYLINE_STATUS_TILE_TIMEOUT
+ * into *device_status and stores nothing, so every workgroup still exits; the cache content is
+ * then unspecified.  This can only follow from a schedule fault or from two calls running at the
+ * same time on one workspace.
  * Enqueues kernels only (all parameters travel as kernel arguments; the workspace is cleared and
  * filled by a kernel), so the call may be captured into a HIP graph; each replay repeats the same
  * splice.
@@ -187,8 +195,8 @@ int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
  */
 int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len,
                           const leyline_directive* dirs, int32_t n_dirs,
-                          int64_t* new_len_out, void* workspace, int64_t workspace_bytes,
-                          void* stream);
+                          int64_t* new_len_out, int32_t* device_status,
+                          void* workspace, int64_t workspace_bytes, void* stream);
 
 /*
  * Sizes of a paged splice, computed on the host from lengths and directives alone.
@@ -236,9 +244,11 @@ int leyline_paged_plan(int32_t page_size, int32_t n_seqs, const int32_t* seq_len
  * Paged splice of a batch of sequences (all layers and planes), following the page plan above.
  *
  * cache->page_size > 0, cache->capacity = physical pages in the pool.
- * seq_lens: host [n_seqs].  block_table_in / block_table_out: device int32 [n_seqs][bt_stride],
- * must not alias; on completion block_table_out holds every sequence's new table and -1 past
- * its last page.  free_pages: device int32 [n_free], consumed from index 0 by ASSEMBLE pages.
+ * seq_lens: host [n_seqs].  block_table_in / block_table_out: device int32 [n_seqs][bt_stride];
+ * on completion block_table_out holds every sequence's new table and -1 past its last page.
+ * The old and new block tables, free_pages [n_free], freed_pages_out [freed_cap], the workspace
+ * [workspace_bytes] and device_status [1] are read and written by the same launch: no two of
+ * them may share a byte (E_INVAL).  free_pages: device int32 [n_free], consumed from index 0 by ASSEMBLE pages.
  * freed_pages_out: device int32 [freed_cap], receives the dropped physical pages.
  * Host outputs (nullable): new_seq_lens_out[n_seqs], *n_fresh_used_out, *n_freed_out.
  * device_status: device int32, nullable; kernels OR LEYLINE_STATUS_* bits into it when a page

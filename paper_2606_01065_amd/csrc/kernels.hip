@@ -525,12 +525,15 @@ __global__ __launch_bounds__(TPB) void contig_chain_kernel(const KContigParams P
 // move) publishes "source read".  Before storing it waits for every tile whose source rows its
 // destination overlaps (tile_wait_flags), so no tile reads a chunk another tile has written.
 // A tile waits only for tickets taken before its own, by workgroups that publish before they
-// wait, so every wait ends.
+// wait, so every wait ends.  The wait is still bounded (KTILE_SPIN_LIMIT polls per flag): a tile
+// that gives up flags LEYLINE_STATUS_TILE_TIMEOUT and stores nothing, and the launch drains.
 //
 // ROT: the rotary style of every re-anchored item of the launch (KROT_NONE: looked up per item),
 // so that the style this launch does not use costs no registers.
-__device__ __forceinline__ void wait_flag(const int32_t* f) {
-    while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) __builtin_amdgcn_s_sleep(1);
+__device__ __forceinline__ bool wait_flag(const int32_t* f) {
+    return tile_wait_bounded(
+        [f] { return __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0; },
+        [] { __builtin_amdgcn_s_sleep(1); }, KTILE_SPIN_LIMIT);
 }
 
 template <int ESZ, int ROT>
@@ -571,9 +574,13 @@ __global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KTileParam
     if (threadIdx.x == 0) {
         if (move)
             __hip_atomic_store(P.flags + I.flag0 + local, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        tile_wait_flags(P, it, layer, order, [&](int64_t f) { wait_flag(P.flags + f); });
+        bool ok = true;
+        tile_wait_flags(P, it, layer, order, [&](int64_t f) { ok = ok && wait_flag(P.flags + f); });
+        if (!ok && P.status) atomicOr(P.status, int(LEYLINE_STATUS_TILE_TIMEOUT));
+        s_ticket = ok ? 1 : 0;              // the ticket was read above; the word now says "store"
     }
     __syncthreads();
+    if (!s_ticket) return;                  // a wait was given up: store nothing (block-uniform)
     char* dst = lbase + I.dst0 * pl.token_stride;
 #pragma unroll
     for (int i = 0; i < KTILE_CPT; ++i) {
@@ -1033,6 +1040,23 @@ int launch(K kernel, dim3 grid, hipStream_t stream, const A& args, int block = T
 
 int64_t abs64(int64_t v) { return v < 0 ? -v : v; }
 
+// A device buffer given to a call: start and length in bytes (null or empty: no buffer).
+struct Span {
+    const void* p;
+    int64_t bytes;
+};
+
+// Whether two of the buffers share a byte.
+bool any_overlap(const Span* b, size_t n) {
+    for (size_t i = 0; i < n; ++i)
+        for (size_t j = i + 1; j < n; ++j) {
+            if (!b[i].p || !b[j].p || b[i].bytes <= 0 || b[j].bytes <= 0) continue;
+            const uintptr_t a0 = reinterpret_cast<uintptr_t>(b[i].p), c0 = reinterpret_cast<uintptr_t>(b[j].p);
+            if (a0 < c0 + uintptr_t(b[j].bytes) && c0 < a0 + uintptr_t(b[i].bytes)) return true;
+        }
+    return false;
+}
+
 }  // namespace
 
 }  // namespace leyline
@@ -1079,7 +1103,7 @@ static int contig_launch_count(const leyline_cache* cache, const ContigSchedule&
 
 // The prep launches and ordered-tile launches of a tile schedule.
 static int launch_tiles(const leyline_cache* cache, const ContigSchedule& sched, const KPlane* planes,
-                        int n_planes, char* ws, hipStream_t s) {
+                        int n_planes, char* ws, int32_t* status, hipStream_t s) {
     // prep: clear the counters and flags, then write the cos/sin table in pieces that fit the
     // kernel arguments
     const int64_t words = sched.ws_cs / 4;
@@ -1112,6 +1136,7 @@ static int launch_tiles(const leyline_cache* cache, const ContigSchedule& sched,
         P.counter = reinterpret_cast<int32_t*>(ws + 256 * int64_t(k));
         P.flags = reinterpret_cast<int32_t*>(ws + sched.ws_flags);
         P.cs = reinterpret_cast<const KCosSin*>(ws + sched.ws_cs);
+        P.status = status;
         const dim3 grid(static_cast<unsigned>(tl.tickets), 1, 1);
         int r;
         switch (launch_rot_style(P)) {
@@ -1148,8 +1173,8 @@ extern "C" int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
 
 extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len,
                                      const leyline_directive* dirs, int32_t n_dirs,
-                                     int64_t* new_len_out, void* workspace, int64_t workspace_bytes,
-                                     void* stream) {
+                                     int64_t* new_len_out, int32_t* device_status,
+                                     void* workspace, int64_t workspace_bytes, void* stream) {
     ContigSchedule sched;
     int rc = plan_contig(cache, seq_len, dirs, n_dirs, &sched);
     if (rc) return rc;
@@ -1163,7 +1188,7 @@ extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len
     hipStream_t s = static_cast<hipStream_t>(stream);
     char* ws = static_cast<char*>(workspace);
     if (sched.tiles) {
-        rc = launch_tiles(cache, sched, planes, n_planes, ws, s);
+        rc = launch_tiles(cache, sched, planes, n_planes, ws, device_status, s);
         if (rc) return rc;
         if (new_len_out) *new_len_out = sched.new_len;
         return LEYLINE_OK;
@@ -1323,10 +1348,19 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
     int n_planes = 0;
     int rc = describe_cache(cache, true, planes, &n_planes);
     if (rc) return rc;
-    if (bt_stride < 1 || n_free < 0 || freed_cap < 0) return LEYLINE_E_INVAL;
+    if (bt_stride < 1 || n_free < 0 || freed_cap < 0 || workspace_bytes < 0) return LEYLINE_E_INVAL;
     if (n_seqs > 0 && (!block_table_in || !block_table_out || block_table_in == block_table_out))
         return LEYLINE_E_INVAL;
     if (flags & ~uint32_t(LEYLINE_PAGED_COPY_ON_WRITE)) return LEYLINE_E_INVAL;
+    {
+        // One launch reads the old tables and the free list while it writes the new tables, the
+        // freed list, the workspace and the status word: no two of these may share a byte.
+        const int64_t bt_bytes = int64_t(n_seqs > 0 ? n_seqs : 0) * bt_stride * 4;
+        const Span bufs[] = {{block_table_in, bt_bytes},    {block_table_out, bt_bytes},
+                             {free_pages, int64_t(n_free) * 4}, {freed_pages_out, int64_t(freed_cap) * 4},
+                             {workspace, workspace_bytes},  {device_status, 4}};
+        if (any_overlap(bufs, sizeof(bufs) / sizeof(bufs[0]))) return LEYLINE_E_INVAL;
+    }
     PagedPlan plan;
     rc = plan_paged(cache->page_size, n_seqs, seq_lens, dirs, n_dirs, n_planes,
                     !(flags & LEYLINE_PAGED_COPY_ON_WRITE), &plan);

@@ -135,6 +135,25 @@ struct KTileItem {
 
 constexpr int KTILE_MAX_ITEMS = 24;
 
+// A tile's wait for one flag gives up after this many unsuccessful polls, each followed by a
+// short sleep (at least a few hundred milliseconds in all).  In a correct schedule the awaited
+// tile has already taken its ticket and only has its own loads to finish, which takes
+// microseconds; the bound turns a schedule fault (or a workspace shared by calls that overlap)
+// into a status bit and skipped stores instead of a workgroup that never exits.
+constexpr int32_t KTILE_SPIN_LIMIT = 1 << 22;
+
+// Polls ready() until it returns true, with pause() between polls, at most `limit` failed polls:
+// whether the wait succeeded.  The tile kernel waits this way; the CPU schedule simulator models
+// its give-up path with it.
+template <class R, class S>
+LEYLINE_HD inline bool tile_wait_bounded(R&& ready, S&& pause, int32_t limit) {
+    for (int32_t i = 0; i < limit; ++i) {
+        if (ready()) return true;
+        pause();
+    }
+    return ready();
+}
+
 struct KTileParams {
     KPlane planes[LEYLINE_MAX_PLANES];
     KTileItem items[KTILE_MAX_ITEMS];
@@ -144,6 +163,7 @@ struct KTileParams {
     int32_t* counter;        // ticket counter of this launch, zero before it
     int32_t* flags;          // the call's flags, zero before the first tile launch
     const KCosSin* cs;       // the call's cos/sin table
+    int32_t* status;         // device, nullable: LEYLINE_STATUS_TILE_TIMEOUT on a wait given up
 };
 
 // The side-by-side table of the items' first tickets (INT32_MAX past the last item), filled by

@@ -22,7 +22,7 @@ OK, E_INVAL, E_RANGE, E_ORDER, E_OVERLAP, E_CAPACITY, E_MODE, E_WORKSPACE, E_HIP
 BF16, F32 = 0, 1
 ROPE_INTERLEAVED, ROPE_NEOX = 0, 1
 AMORTIZE, FORGET = 0, 1
-STATUS_BAD_PAGE, STATUS_BAD_ROW = 1, 2
+STATUS_BAD_PAGE, STATUS_BAD_ROW, STATUS_TILE_TIMEOUT = 1, 2, 4
 PAGE_IDENTITY, PAGE_REMAP, PAGE_ASSEMBLE, PAGE_NONE = 0, 1, 2, -1
 PAGED_COPY_ON_WRITE = 1
 
@@ -102,7 +102,7 @@ def _load():
         "leyline_contig_query": (c_int, [P(leyline_cache), c_int64, P(leyline_directive), c_int32,
                                          P(c_int64), P(c_int32), P(c_int32), P(c_int64)]),
         "leyline_splice_contig": (c_int, [P(leyline_cache), c_int64, P(leyline_directive), c_int32,
-                                          P(c_int64), c_void_p, c_int64, c_void_p]),
+                                          P(c_int64), c_void_p, c_void_p, c_int64, c_void_p]),
         "leyline_paged_query": (c_int, [P(leyline_cache), c_int32, P(c_int32), c_int32,
                                         P(leyline_directive), c_int32, c_uint32, P(c_int32),
                                         P(c_int32), P(c_int32), P(c_int64)]),
@@ -287,11 +287,11 @@ def contig_workspace(cache: leyline_cache, seq_len: int, dirs, n_dirs: int, devi
 
 
 def leyline_splice_contig(cache: leyline_cache, seq_len: int, dirs, n_dirs: int, stream=None,
-                          workspace=None) -> int:
+                          workspace=None, device_status=None) -> int:
     """Returns the new sequence length.  workspace: a device tensor of at least the queried size;
     when None, the call queries the size and allocates one with torch if the splice needs it
     (a caller that splices repeatedly keeps one workspace instead and saves the extra planning
-    and allocation per call)."""
+    and allocation per call).  device_status: optional int32 device tensor (status bits)."""
     if workspace is None:
         need = leyline_contig_query(cache, seq_len, dirs, n_dirs).workspace_bytes
         if need:
@@ -300,7 +300,8 @@ def leyline_splice_contig(cache: leyline_cache, seq_len: int, dirs, n_dirs: int,
     ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
     new_len = c_int64(0)
     rc = _lib.leyline_splice_contig(ctypes.byref(cache), seq_len, dirs, n_dirs,
-                                    ctypes.byref(new_len), ws_ptr, ws_len, _stream(stream))
+                                    ctypes.byref(new_len), _ptr(device_status), ws_ptr, ws_len,
+                                    _stream(stream))
     _check(rc, "leyline_splice_contig")
     return new_len.value
 

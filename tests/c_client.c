@@ -110,7 +110,7 @@ int main(int argc, char** argv) {
 
     rc = leyline_contig_query(&cache, hdr[4], dirs, hdr[5], &new_len, &n_launch, &n_tile, &ws_bytes);
     if (rc == LEYLINE_OK && ws_bytes > 0) CHECK_HIP(hipMalloc(&ws, (size_t)ws_bytes));
-    if (rc == LEYLINE_OK) rc = leyline_splice_contig(&cache, hdr[4], dirs, hdr[5], &new_len, ws, ws_bytes, NULL);
+    if (rc == LEYLINE_OK) rc = leyline_splice_contig(&cache, hdr[4], dirs, hdr[5], &new_len, NULL, ws, ws_bytes, NULL);
     CHECK_HIP(hipDeviceSynchronize());
     printf("rc %d (%s) new_len %ld launches %d tile_launches %d workspace %ld\n", (int)rc,
            leyline_strerror((int)rc), (long)new_len, n_launch, n_tile, (long)ws_bytes);

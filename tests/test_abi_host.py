@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
     for name in declared:
         assert hasattr(lib, name), name
     assert sorted(L.SYMBOLS) == declared
-    assert L.leyline_abi_version() == 2
+    assert L.leyline_abi_version() == 3
     assert "overlap" in L.strerror(L.E_OVERLAP)
 
 
@@ -85,7 +85,7 @@ def _dirs(spec, stub_ptr=0x20000):
 def _contig_rc(cache, n, spec):
     new_len = ctypes.c_int64(-1)
     d = _dirs(spec)
-    return L._lib.leyline_splice_contig(ctypes.byref(cache), n, d, len(spec), ctypes.byref(new_len),
+    return L._lib.leyline_splice_contig(ctypes.byref(cache), n, d, len(spec), ctypes.byref(new_len), None,
                                         None, 0, None)
 
 
@@ -99,17 +99,17 @@ def test_contig_validation_codes():
     assert _contig_rc(c, 60, [(10, 10, 5)]) == L.E_CAPACITY               # 65 > 64 rows
     d = _dirs([(1, 2, 0), (5, 6, 0)])
     d[0].mode = L.FORGET                                                  # FORGET not last
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 2, None, None, 0, None) == L.E_MODE
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 2, None, None, None, 0, None) == L.E_MODE
     d = _dirs([(1, 2, 3)])
     d[0].mode = L.FORGET                                                  # FORGET with a replacement
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, 0, None) == L.E_MODE
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, None, 0, None) == L.E_MODE
     d = _dirs([(1, 2, 0)])
     d[0].mode = 7
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, 0, None) == L.E_INVAL
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, None, 0, None) == L.E_INVAL
     d = _dirs([(1, 2, 3)], stub_ptr=0)                                    # stub pointer missing
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, 0, None) == L.E_INVAL
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, None, 0, None) == L.E_INVAL
     d = _dirs([(1, 2, 3)], stub_ptr=0x20008)                              # stub misaligned
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, 0, None) == L.E_INVAL
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 10, d, 1, None, None, None, 0, None) == L.E_INVAL
     bad = _mla_cache(ptr=0x10008)                                         # cache misaligned
     assert _contig_rc(bad, 10, [(1, 2, 0)]) == L.E_INVAL
     c.planes[0].rot_dim = 63                                              # odd rotary band
@@ -172,11 +172,11 @@ def test_contig_tiles_need_a_workspace():
     c = _mla_cache(cap=64)
     new_len = ctypes.c_int64(-1)
     d = _dirs([(10, 11, 0)])
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 60, d, 1, ctypes.byref(new_len),
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 60, d, 1, ctypes.byref(new_len), None,
                                         None, 0, None) == L.E_WORKSPACE
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 60, d, 1, ctypes.byref(new_len),
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 60, d, 1, ctypes.byref(new_len), None,
                                         0x10080, 4096, None) == L.E_WORKSPACE      # misaligned
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 60, d, 1, ctypes.byref(new_len),
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 60, d, 1, ctypes.byref(new_len), None,
                                         0x10000, 16, None) == L.E_WORKSPACE        # too small
 
 
@@ -189,7 +189,7 @@ def test_forget_trims_without_moving_anything():
     q = L.leyline_contig_query(c, 60, d, 1)
     assert (q.new_len, q.launches, q.workspace_bytes) == (30, 0, 0)
     new_len = ctypes.c_int64(-1)
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 60, d, 1, ctypes.byref(new_len), None, 0, None) == 0
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 60, d, 1, ctypes.byref(new_len), None, None, 0, None) == 0
     assert new_len.value == 30
     d = _dirs([(10, 12, 0), (30, 30, 0)])                                # after a 2-row deletion
     d[1].mode = L.FORGET
@@ -201,10 +201,10 @@ def test_contig_noop_calls_do_not_need_a_device():
     nothing and reports the unchanged length."""
     c = _mla_cache()
     new_len = ctypes.c_int64(-1)
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 40, None, 0, ctypes.byref(new_len), None, 0, None) == 0
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 40, None, 0, ctypes.byref(new_len), None, None, 0, None) == 0
     assert new_len.value == 40
     d = _dirs([(10, 10, 0)])
-    assert L._lib.leyline_splice_contig(ctypes.byref(c), 40, d, 1, ctypes.byref(new_len), None, 0, None) == 0
+    assert L._lib.leyline_splice_contig(ctypes.byref(c), 40, d, 1, ctypes.byref(new_len), None, None, 0, None) == 0
     assert new_len.value == 40
 
 
@@ -342,6 +342,22 @@ def test_paged_splice_validates_before_any_enqueue():
     with pytest.raises(L.LeylineError) as e:                                # tables alias
         L.leyline_splice_paged(cache, lens, bt_in, bt_in, d, 1, free, freed, ws, stream=0)
     assert e.value.code == L.E_INVAL
+    # buffers that the same launch reads and writes may not share a byte: each overlapping pair
+    # is refused before anything is enqueued (a mere neighbour is fine, as above)
+    overlapping = [
+        dict(bt_out=_FakeTensor((1, 8), torch.int32, ptr=0x30000 + 16)),    # old / new table
+        dict(freed=_FakeTensor((8,), torch.int32, ptr=0x50000 + 60)),       # free list / freed list
+        dict(freed=_FakeTensor((8,), torch.int32, ptr=0x40000 + 28)),       # new table / freed list
+        dict(ws=_FakeTensor((4096,), torch.uint8, ptr=0x50000 - 256)),      # workspace / free list
+        dict(status=_FakeTensor((1,), torch.int32, ptr=0x30000 + 4)),       # status / old table
+    ]
+    for o in overlapping:
+        args = dict(bt_out=bt_out, freed=freed, ws=ws, status=None)
+        args.update(o)
+        with pytest.raises(L.LeylineError) as e:
+            L.leyline_splice_paged(cache, lens, bt_in, args["bt_out"], d, 1, free, args["freed"], args["ws"],
+                                   device_status=args["status"], stream=0)
+        assert e.value.code == L.E_INVAL, o
 
 
 def test_rotate_delta_validation():

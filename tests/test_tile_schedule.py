@@ -35,5 +35,16 @@ def sim(tmp_path_factory):
 def test_tile_schedules_are_race_free_and_complete(sim, seed):
     r = subprocess.run([sim, str(seed), "3000"], capture_output=True, text=True, timeout=300)
     assert r.returncode == 0, r.stdout + r.stderr
-    ok, cases, tiles = r.stdout.split()
-    assert ok == "ok" and int(cases) > 2000 and int(tiles) > 50000
+    ok, cases, tiles, gave_up = r.stdout.split()
+    assert ok == "ok" and int(cases) > 2000 and int(tiles) > 50000 and int(gave_up) == 0
+
+
+def test_a_wait_that_cannot_end_gives_up_and_every_tile_exits(sim):
+    """A planted schedule fault (the first tile of every launch also waits for the launch's last
+    tile, a later ticket) blocks launches whenever too few workgroups are in flight.  The kernel's
+    bounded wait must then give up (the timeout status bit, no stores) so that every workgroup
+    exits instead of hanging."""
+    r = subprocess.run([sim, "21", "300", "1"], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stdout + r.stderr
+    ok, cases, tiles, gave_up = r.stdout.split()
+    assert ok == "ok" and int(cases) > 150 and int(gave_up) > 0

@@ -10,7 +10,15 @@
 // unchanged, replacements at s_j + delta_{j-1}, segment j shifted by delta_j).  Values are row
 // identities, not data: rotation is not simulated.
 //
-// Usage: tile_schedule_sim SEED CASES   (prints "ok <tile cases> <tiles>" on success)
+// The kernel's wait is bounded (tile_wait_bounded, KTILE_SPIN_LIMIT polls): when every in-flight
+// tile is blocked, each waiting tile polls until the bound, gives up, flags the timeout status
+// and exits without storing.  A correct schedule never gets there.  With PLANT = 1 the first
+// move tile of every launch also waits for the flag of the launch's last move tile (a later
+// ticket: a planted schedule fault); then the give-up path must let every workgroup exit and
+// raise the status bit whenever the fault blocked the launch.
+//
+// Usage: tile_schedule_sim SEED CASES [PLANT]
+//        (prints "ok <tile cases> <tiles stored> <waits given up>" on success)
 #include <algorithm>
 #include <cstdio>
 #include <cstdlib>
@@ -59,6 +67,8 @@ int fail(const char* what, int case_id) {
 int main(int argc, char** argv) {
     const unsigned seed = argc > 1 ? unsigned(std::atoi(argv[1])) : 1u;
     const int cases = argc > 2 ? std::atoi(argv[2]) : 100;
+    const bool plant = argc > 3 && std::atoi(argv[3]) != 0;
+    int64_t gave_up = 0;
     std::mt19937_64 rng(seed);
     auto uni = [&](int64_t lo, int64_t hi) { return std::uniform_int_distribution<int64_t>(lo, hi)(rng); };
     int tile_cases = 0;
@@ -136,6 +146,7 @@ int main(int argc, char** argv) {
             for (const auto& it : tl.items)
                 if (it.kind == KJOB_TILE) n_flags = std::max<int64_t>(n_flags, it.flag0 + int64_t(L) * it.n_tiles);
         std::vector<int> flags(static_cast<size_t>(n_flags), 0);
+        int32_t status = 0;
         for (const auto& tl : sched.tile_launches) {
             if (tl.items.empty() || tl.items.size() > size_t(KTILE_MAX_ITEMS)) return fail("item count", ci);
             KTileParams P;
@@ -176,6 +187,31 @@ int main(int argc, char** argv) {
             int64_t next = 0;
             std::vector<int64_t> live;
             std::vector<int64_t> waits;
+            // planted fault: the first move tile also waits for the last move tile's flag
+            int64_t victim = -1, planted = -1;
+            if (plant) {
+                for (int64_t t = 0; t < tl.tickets; ++t)
+                    if (P.items[tiles[size_t(t)].item].kind == KJOB_TILE) {
+                        const Tile& T = tiles[size_t(t)];
+                        const KTileItem& I = P.items[T.item];
+                        const int64_t f = I.flag0 + int64_t(T.layer) * I.n_tiles + T.order;
+                        if (victim < 0) victim = t;
+                        else planted = f;
+                    }
+                if (planted < 0) victim = -1;
+            }
+            // whether loaded tile t may store (every flag it waits for set); bad: a wait names a
+            // flag outside the launch or of a later ticket
+            auto ready_to_store = [&](int64_t t, bool* bad) {
+                const Tile& T = tiles[size_t(t)];
+                bool ready = true;
+                tile_wait_flags(P, T.item, T.layer, T.order, [&](int64_t f) {
+                    if (f < 0 || f >= n_flags || flag_ticket[size_t(f)] < 0 || flag_ticket[size_t(f)] >= t) *bad = true;
+                    else if (!flags[size_t(f)]) ready = false;
+                });
+                if (t == victim && !flags[size_t(planted)]) ready = false;
+                return ready;
+            };
             while (next < tl.tickets || !live.empty()) {
                 // possible actions: take the next ticket, load a taken tile, store a loaded one
                 std::vector<std::pair<int, int64_t>> acts;
@@ -185,17 +221,29 @@ int main(int argc, char** argv) {
                         acts.emplace_back(1, t);
                         continue;
                     }
-                    const Tile& T = tiles[size_t(t)];
-                    bool ready = true;
                     bool bad = false;
-                    tile_wait_flags(P, T.item, T.layer, T.order, [&](int64_t f) {
-                        if (f < 0 || f >= n_flags || flag_ticket[size_t(f)] < 0 || flag_ticket[size_t(f)] >= t) bad = true;
-                        else if (!flags[size_t(f)]) ready = false;
-                    });
+                    const bool ready = ready_to_store(t, &bad);
                     if (bad) return fail("a wait names a flag outside the launch or of a later ticket", ci);
                     if (ready) acts.emplace_back(2, t);
                 }
-                if (acts.empty()) return fail("schedule stalled", ci);
+                if (acts.empty()) {
+                    // every in-flight tile is blocked: nothing changes while they poll, so each
+                    // waits out its bound, flags the timeout and exits without storing
+                    if (!plant) return fail("schedule stalled", ci);
+                    std::vector<int64_t> blocked = live;
+                    for (int64_t t : blocked) {
+                        bool bad = false;
+                        int64_t polls = 0;
+                        const bool ok = tile_wait_bounded([&] { return ready_to_store(t, &bad); },
+                                                          [&] { ++polls; }, KTILE_SPIN_LIMIT);
+                        if (ok || polls != KTILE_SPIN_LIMIT) return fail("bounded wait", ci);
+                        status |= LEYLINE_STATUS_TILE_TIMEOUT;
+                        state[size_t(t)] = 2;
+                        live.erase(std::find(live.begin(), live.end(), t));
+                        ++gave_up;
+                    }
+                    continue;
+                }
                 const auto a = acts[size_t(uni(0, int64_t(acts.size()) - 1))];
                 const int64_t t = a.second;
                 if (a.first == 0) {
@@ -241,6 +289,8 @@ int main(int argc, char** argv) {
                 }
             }
         }
+        // every workgroup has exited; a launch that gave up leaves its rows unspecified
+        if (status) continue;
         // rows [0, new_len) against the definition
         for (int p = 0; p < n_planes; ++p)
             for (int l = 0; l < L; ++l) {
@@ -269,6 +319,6 @@ int main(int argc, char** argv) {
                 if (pos != new_len) return fail("new length bookkeeping", ci);
             }
     }
-    std::printf("ok %d %lld\n", tile_cases, static_cast<long long>(tiles_run));
+    std::printf("ok %d %lld %lld\n", tile_cases, static_cast<long long>(tiles_run), static_cast<long long>(gave_up));
     return 0;
 }
