@@ -198,6 +198,29 @@ int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len,
                           int64_t* new_len_out, int32_t* device_status,
                           void* workspace, int64_t workspace_bytes, void* stream);
 
+/* Bytes of the library's fixed per-GPU scratch array used by leyline_splice_contig_noalloc. */
+#define LEYLINE_SCRATCH_BYTES (1 << 20)
+
+/*
+ * leyline_splice_contig without any device allocation, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ *
+ * Same splice, arguments, validation, kernels and results as leyline_splice_contig, but the
+ * workspace is a fixed array of LEYLINE_SCRATCH_BYTES bytes in device memory that the library
+ * holds on each GPU it runs on until the process ends (located on the first call on a device).
+ * The call uses the calling thread's current device; a non-NULL stream must belong to it
+ * (E_INVAL otherwise).  A splice whose ordered tiles need more workspace than
+ * LEYLINE_SCRATCH_BYTES returns LEYLINE_E_WORKSPACE before anything is enqueued (1 MiB holds
+ * the counters and flags of, e.g., a small-shift splice of a 61-layer MLA cache of about 480K
+ * tokens); use leyline_splice_contig with a caller workspace for those.  The call makes no
+ * device allocation or free (no hipMalloc / hipFree, no allocating library routine) and clears
+ * the counters and flags it needs with a kernel at its start.  Every call on one GPU shares that GPU's array: calls that may overlap
+ * in time on one GPU (other streams, other threads) race and must be ordered by the caller.
+ */
+int leyline_splice_contig_noalloc(const leyline_cache* cache, int64_t seq_len,
+                                  const leyline_directive* dirs, int32_t n_dirs,
+                                  int64_t* new_len_out, int32_t* device_status, void* stream);
+
 /*
  * Sizes of a paged splice, computed on the host from lengths and directives alone.
  *

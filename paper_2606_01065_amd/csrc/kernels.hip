@@ -33,6 +33,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "kparams.hpp"
@@ -1171,22 +1172,14 @@ extern "C" int leyline_contig_query(const leyline_cache* cache, int64_t seq_len,
     return LEYLINE_OK;
 }
 
-extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len,
-                                     const leyline_directive* dirs, int32_t n_dirs,
-                                     int64_t* new_len_out, int32_t* device_status,
-                                     void* workspace, int64_t workspace_bytes, void* stream) {
-    ContigSchedule sched;
-    int rc = plan_contig(cache, seq_len, dirs, n_dirs, &sched);
-    if (rc) return rc;
-    if (sched.ws_bytes > 0 && (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) ||
-                               workspace_bytes < sched.ws_bytes))
-        return LEYLINE_E_WORKSPACE;
+// The launches of a planned contiguous splice, on a workspace already checked against the plan.
+static int splice_contig_planned(const leyline_cache* cache, const ContigSchedule& sched,
+                                 const leyline_directive* dirs, int64_t* new_len_out,
+                                 int32_t* device_status, char* ws, hipStream_t s) {
     KPlane planes[LEYLINE_MAX_PLANES];
     int n_planes = 0;
-    rc = describe_cache(cache, false, planes, &n_planes);
+    int rc = describe_cache(cache, false, planes, &n_planes);
     if (rc) return rc;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    char* ws = static_cast<char*>(workspace);
     if (sched.tiles) {
         rc = launch_tiles(cache, sched, planes, n_planes, ws, device_status, s);
         if (rc) return rc;
@@ -1259,6 +1252,78 @@ extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len
     }
     if (new_len_out) *new_len_out = sched.new_len;
     return LEYLINE_OK;
+}
+
+extern "C" int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len,
+                                     const leyline_directive* dirs, int32_t n_dirs,
+                                     int64_t* new_len_out, int32_t* device_status,
+                                     void* workspace, int64_t workspace_bytes, void* stream) {
+    ContigSchedule sched;
+    int rc = plan_contig(cache, seq_len, dirs, n_dirs, &sched);
+    if (rc) return rc;
+    if (sched.ws_bytes > 0 && (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) ||
+                               workspace_bytes < sched.ws_bytes))
+        return LEYLINE_E_WORKSPACE;
+    return splice_contig_planned(cache, sched, dirs, new_len_out, device_status, static_cast<char*>(workspace),
+                                 static_cast<hipStream_t>(stream));
+}
+
+// ------------------------------------------------------------- splice without allocation ---
+//
+// The contiguous splice's workspace for callers that cannot allocate device memory (graph
+// capture, serving loops, harnesses that forbid hipMalloc): a fixed array in device memory, one
+// copy per GPU, held until the process ends.  Host code never passes the array's name (a host
+// stand-in, not a device address): its device address is looked up once per device, with that
+// device current, and only that address is handed to kernels.
+static __device__ __align__(256) char scratch[LEYLINE_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices];
+
+// The scratch array's address on the calling thread's current device; the stream must run on
+// that device.
+int scratch_on_current_device(hipStream_t stream, char** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(e);
+    if (dev < 0 || dev >= kScratchDevices) return LEYLINE_E_INVAL;
+    if (stream) {
+        hipDevice_t sd = -1;
+        e = hipStreamGetDevice(stream, &sd);
+        if (e != hipSuccess) return hip_status(e);
+        if (sd != dev) return LEYLINE_E_INVAL;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_status(e);
+        if (!p) return LEYLINE_E_HIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = static_cast<char*>(g_scratch_ptr[dev]);
+    return LEYLINE_OK;
+}
+
+}  // namespace
+
+extern "C" int leyline_splice_contig_noalloc(const leyline_cache* cache, int64_t seq_len,
+                                             const leyline_directive* dirs, int32_t n_dirs,
+                                             int64_t* new_len_out, int32_t* device_status, void* stream) {
+    ContigSchedule sched;
+    int rc = plan_contig(cache, seq_len, dirs, n_dirs, &sched);
+    if (rc) return rc;
+    if (sched.ws_bytes > LEYLINE_SCRATCH_BYTES) return LEYLINE_E_WORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* ws = nullptr;
+    if (sched.ws_bytes > 0) {
+        rc = scratch_on_current_device(s, &ws);
+        if (rc) return rc;
+    }
+    return splice_contig_planned(cache, sched, dirs, new_len_out, device_status, ws, s);
 }
 
 // The rotation kernel variant for (dtype, one plane only, paged cache).

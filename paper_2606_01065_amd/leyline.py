@@ -103,6 +103,8 @@ def _load():
                                          P(c_int64), P(c_int32), P(c_int32), P(c_int64)]),
         "leyline_splice_contig": (c_int, [P(leyline_cache), c_int64, P(leyline_directive), c_int32,
                                           P(c_int64), c_void_p, c_void_p, c_int64, c_void_p]),
+        "leyline_splice_contig_noalloc": (c_int, [P(leyline_cache), c_int64, P(leyline_directive), c_int32,
+                                                  P(c_int64), c_void_p, c_void_p]),
         "leyline_paged_query": (c_int, [P(leyline_cache), c_int32, P(c_int32), c_int32,
                                         P(leyline_directive), c_int32, c_uint32, P(c_int32),
                                         P(c_int32), P(c_int32), P(c_int64)]),
@@ -127,8 +129,11 @@ _lib = _load()
 
 #: every symbol the header declares (checked by tests against the loaded library)
 SYMBOLS = ("leyline_strerror", "leyline_abi_version", "leyline_last_hip_error", "leyline_contig_query",
-           "leyline_splice_contig", "leyline_paged_query", "leyline_paged_plan", "leyline_splice_paged",
-           "leyline_rotate_delta")
+           "leyline_splice_contig", "leyline_splice_contig_noalloc", "leyline_paged_query",
+           "leyline_paged_plan", "leyline_splice_paged", "leyline_rotate_delta")
+
+#: bytes of the library's fixed per-GPU scratch array (leyline_splice_contig_noalloc)
+SCRATCH_BYTES = 1 << 20
 
 
 def strerror(code: int) -> str:
@@ -303,6 +308,17 @@ def leyline_splice_contig(cache: leyline_cache, seq_len: int, dirs, n_dirs: int,
                                     ctypes.byref(new_len), _ptr(device_status), ws_ptr, ws_len,
                                     _stream(stream))
     _check(rc, "leyline_splice_contig")
+    return new_len.value
+
+
+def leyline_splice_contig_noalloc(cache: leyline_cache, seq_len: int, dirs, n_dirs: int, stream=None,
+                                  device_status=None) -> int:
+    """leyline_splice_contig on the library's fixed per-GPU scratch array (no workspace argument,
+    no device allocation).  Returns the new sequence length."""
+    new_len = c_int64(0)
+    rc = _lib.leyline_splice_contig_noalloc(ctypes.byref(cache), seq_len, dirs, n_dirs, ctypes.byref(new_len),
+                                            _ptr(device_status), _stream(stream))
+    _check(rc, "leyline_splice_contig_noalloc")
     return new_len.value
 
 

@@ -26,7 +26,8 @@ int main(void) {
         typedef void (*fn_t)(void);
         const fn_t fns[] = {
             (fn_t)leyline_strerror, (fn_t)leyline_abi_version, (fn_t)leyline_last_hip_error,
-            (fn_t)leyline_contig_query, (fn_t)leyline_splice_contig, (fn_t)leyline_paged_query,
+            (fn_t)leyline_contig_query, (fn_t)leyline_splice_contig, (fn_t)leyline_splice_contig_noalloc,
+            (fn_t)leyline_paged_query,
             (fn_t)leyline_paged_plan, (fn_t)leyline_splice_paged, (fn_t)leyline_rotate_delta,
         };
         size_t i, n = sizeof(fns) / sizeof(fns[0]);
@@ -36,5 +37,6 @@ int main(void) {
     }
     printf("abi_version %d %d\n", LEYLINE_ABI_VERSION, leyline_abi_version());
     printf("strerror_overlap %s\n", leyline_strerror(LEYLINE_E_OVERLAP));
+    printf("scratch_bytes %d\n", LEYLINE_SCRATCH_BYTES);
     return 0;
 }

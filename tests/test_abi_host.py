@@ -180,6 +180,25 @@ def test_contig_tiles_need_a_workspace():
                                         0x10000, 16, None) == L.E_WORKSPACE        # too small
 
 
+def test_noalloc_splice_refuses_more_than_its_scratch_before_any_enqueue():
+    """leyline_splice_contig_noalloc takes its workspace from a fixed 1 MiB array: a small-shift
+    splice whose ordered tiles need more (here 61 layers of a 600K-token MLA cache: one 4-byte
+    flag per tile of 8192 chunks and layer) is refused with E_WORKSPACE before any device call;
+    a call that moves nothing needs no scratch and no device."""
+    big = _mla_cache(n_layers=61, cap=600000)
+    d = _dirs([(10, 11, 0)])
+    assert L.leyline_contig_query(big, 600000, d, 1).workspace_bytes > L.SCRATCH_BYTES
+    new_len = ctypes.c_int64(-1)
+    assert L._lib.leyline_splice_contig_noalloc(ctypes.byref(big), 600000, d, 1, ctypes.byref(new_len),
+                                                None, None) == L.E_WORKSPACE
+    c = _mla_cache()
+    assert L._lib.leyline_splice_contig_noalloc(ctypes.byref(c), 40, None, 0, ctypes.byref(new_len),
+                                                None, None) == 0
+    assert new_len.value == 40
+    assert L._lib.leyline_splice_contig_noalloc(ctypes.byref(c), 70, None, 0, ctypes.byref(new_len),
+                                                None, None) == L.E_RANGE
+
+
 def test_forget_trims_without_moving_anything():
     """A FORGET directive (last of its sequence, no replacement) cuts the sequence at its span's
     start after the earlier directives; the cut itself moves nothing."""

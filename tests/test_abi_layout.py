@@ -44,3 +44,4 @@ def test_c_program_reaches_every_entry_point(layout):
     declared, loaded = layout["abi_version"].split()
     assert int(declared) == int(loaded) == L.leyline_abi_version()
     assert "overlap" in layout["strerror_overlap"]
+    assert int(layout["scratch_bytes"]) == L.SCRATCH_BYTES
