@@ -312,6 +312,9 @@ class _EveryRow:
     replacement bit for bit, rows with shift 0 are bit-identical, and every rotary pair p of a
     moved row has turned by its angle phi (p.p' = |p|^2 cos phi, p x p' = |p|^2 sin phi, within
     storage rounding), with cos phi and sin phi taken from the oracle once per distinct shift.
+    In three whole layers (first, middle, last) every row's rotary bands are also compared
+    element by element with the oracle's rotation of its source bands (Eq. "rotate"), at the
+    parity bar of assert_rows_match.
     The rotary bands of all source rows are snapshotted on the device before the call; their
     non-rotary elements are read after it, where they still are (fresh pages are disjoint from
     old ones, a re-used page changes only its rotary bands, copy-on-write writes no old page)."""
@@ -359,6 +362,7 @@ class _EveryRow:
         np_, no = dev(bt_out_h[self.seq_old, self.q_old // P]), dev(self.q_old % P)
         sp, so = dev(bt_out_h[self.seq_stub, self.q_stub // P]), dev(self.q_stub % P)
         moved = dev(self.shift != 0).bool()
+        oracle_layers = {0, wl.n_layers // 2, wl.n_layers - 1}
         rows = 0
         for pi, plane in enumerate(self.planes):
             rot = self.rot[pi]
@@ -376,8 +380,24 @@ class _EveryRow:
                 g, b0 = got[:, rot], self.before[pi][layer]
                 assert torch.equal(bits(g[~moved]), bits(b0[~moved])), f"plane {pi} layer {layer}: shift-0 rows"
                 assert_pairs_turned(b0[moved], g[moved], self.angles[pi], wl.dtype, f"plane {pi} layer {layer}")
+                if layer in oracle_layers:
+                    self._against_oracle(plane, host(b0), host(g), f"plane {pi} layer {layer}")
             rows += len(self.a_old) + len(self.q_stub)
-        print(f"[info] every row checked by properties: {rows} rows x {wl.n_layers} layers", flush=True)
+        print(f"[info] every row checked by properties: {rows} rows x {wl.n_layers} layers; rotary bands "
+              f"of layers {sorted(oracle_layers)} against the oracle", flush=True)
+
+    def _against_oracle(self, plane, before, got, what):
+        """Every row's rotary bands (the plane's rotary selection: each head's band back to back,
+        i.e. a plane of n_heads bands of rot_dim elements) against the oracle's R(shift) of the
+        bands the row had before the call, one oracle call per distinct shift."""
+        bands = O.Plane(row_elems=plane.n_heads * plane.rot_dim, n_heads=plane.n_heads,
+                        head_stride=plane.rot_dim, rot_offset=0, rot_dim=plane.rot_dim,
+                        style=plane.style, base=plane.base, freqs=plane.freqs)
+        want = np.empty_like(before)
+        for c in np.unique(self.shift):
+            sel = self.shift == c
+            want[sel] = O.rotate_rows(before[sel], int(c), bands, self.wl.dtype)
+        assert_rows_match(got, want, bands, self.wl.dtype, inputs=before, what=f"{what}: rotary bands vs oracle")
 
 
 def _check_sampled(L, wl, seed):
