@@ -53,6 +53,13 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"))
     ap.add_argument("--command", default="", help="command line recorded in --summarize output")
+    ap.add_argument("--also", default="gqa_llama3_8b_16k,mla_dsv3_paged_131k",
+                    help="further workloads timed in the same run and reported under \"also\" "
+                         "(comma-separated; empty: none)")
+    ap.add_argument("--cpu-procs", type=int, default=0,
+                    help="processes of the all-cores oracle leg (0: every CPU this process may use, at most 16)")
+    ap.add_argument("--cpu-leg", nargs=4, metavar=("DATA", "SECONDS", "PROCS", "OUT"),
+                    help=argparse.SUPPRESS)
     return ap.parse_args()
 
 
@@ -166,10 +173,89 @@ def copy_ceiling(nbytes, dev, stream):
     return 2 * half * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9, half
 
 
+def setup_workload(wl, dev, L, W, args, stream):
+    """(step, kernel, algorithmic bytes, moved tokens, dominant-kernel launches, keep, layout)."""
+    specs = lambda planes: [L.PlaneSpec(t, p.n_heads, p.head_stride or p.row_elems, p.rot_offset,
+                                        p.rot_dim, p.style, p.base) for p, t in zip(wl.planes, planes)]
+    if wl.rotate:
+        step, kernel, alg_bytes, moved, launches, keep = setup_rotate(wl, dev, L, W, specs, stream)
+        layout = (f"contiguous, rotary bands re-anchored in place (no movement), {ROTATE_REPLICAS} cache "
+                  "copies round-robin")
+    elif wl.page_size:
+        step, kernel, alg_bytes, moved, launches, keep = setup_paged(wl, dev, L, W, specs, stream)
+        layout = (f"paged, {wl.page_size}-token pages, {len(wl.seq_lens)} sequences"
+                  + (", copy-on-write" if wl.paged_flags else "")
+                  + (f", {keep['replicas']} pool copies round-robin" if keep["replicas"] > 1 else ""))
+    else:
+        step, kernel, alg_bytes, moved, launches, keep = setup_contig(wl, dev, L, W, specs, stream, args)
+        layout = "contiguous in place"
+    return step, kernel, alg_bytes, moved, launches, keep, layout
+
+
+def timed(step, steps, warmup, stream):
+    """Milliseconds per step: `warmup` untimed steps, then `steps` steps back to back on the
+    stream the kernels run on, bracketed by two HIP events and nothing in between (an event
+    between splices adds its own packet)."""
+    import torch
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t_begin = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_begin.record(stream)
+    for i in range(steps):
+        step(i)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    return t_begin.elapsed_time(t_end) / steps
+
+
+def roofline_of(wl, kernel, alg_bytes, launches, splice_ms):
+    """The dominant kernel against the HBM peak: algorithmic bytes per launch over the average
+    launch duration (the event-timed splice divided by its launches of that kernel), with the
+    committed counter traffic when it was taken on the current kernel sources."""
+    achieved = alg_bytes / (splice_ms * 1e-3) / 1e9
+    rec = measured_traffic(wl.name)
+    traffic = rec["dispatch_bytes"] if rec and rec.get("kernel") == kernel else None
+    return achieved, traffic, rec
+
+
+def measure_also(name, args, dev, L, W, stream):
+    """A second configuration timed in the same run (same protocol as the headline), reported as
+    a compact record."""
+    import torch
+    wl = W.WORKLOADS[name]()
+    step, kernel, alg_bytes, moved, launches, keep, layout = setup_workload(wl, dev, L, W, args, stream)
+    ms = timed(step, args.steps, args.warmup, stream)
+    achieved, traffic, _ = roofline_of(wl, kernel, alg_bytes, launches, ms)
+    del step, keep
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return {
+        "workload": wl.name,
+        "layout": layout,
+        "ms_per_step": ms,
+        "value": moved / (ms * 1e-3),
+        "unit": "tokens/s",
+        "kernel": kernel,
+        "launches_per_splice": launches,
+        "avg_launch_ms": ms / max(1, launches),
+        "achieved_GBps": achieved,
+        "frac": achieved / PEAK_HBM_GBPS,
+        "traffic": traffic,
+        "algorithmic_bytes_per_splice": alg_bytes,
+        "steps": args.steps,
+        "warmup": args.warmup,
+    }
+
+
 def main():
     args = parse()
     if args.summarize:
         summarize(args)
+        return
+    if args.cpu_leg:
+        cpu_leg(*args.cpu_leg)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only: a splice of one sequence "
@@ -184,39 +270,11 @@ def main():
     dev = "cuda:0"
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    specs = lambda planes: [L.PlaneSpec(t, p.n_heads, p.head_stride or p.row_elems, p.rot_offset,
-                                        p.rot_dim, p.style, p.base) for p, t in zip(wl.planes, planes)]
+    step, kernel, alg_bytes, moved, launches, keep, layout = setup_workload(wl, dev, L, W, args, stream)
 
-    if wl.rotate:
-        step, kernel, alg_bytes, moved, launches, keep = setup_rotate(wl, dev, L, W, specs, stream)
-        layout = (f"contiguous, rotary bands re-anchored in place (no movement), {ROTATE_REPLICAS} cache "
-                  "copies round-robin")
-    elif wl.page_size:
-        step, kernel, alg_bytes, moved, launches, keep = setup_paged(wl, dev, L, W, specs, stream)
-        layout = (f"paged, {wl.page_size}-token pages, {len(wl.seq_lens)} sequences"
-                  + (", copy-on-write" if wl.paged_flags else "")
-                  + (f", {keep['replicas']} pool copies round-robin" if keep["replicas"] > 1 else ""))
-    else:
-        step, kernel, alg_bytes, moved, launches, keep = setup_contig(wl, dev, L, W, specs, stream, args)
-        layout = "contiguous in place"
-
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    # The timed region: K splices back to back on the stream the kernels run on, bracketed by
-    # two HIP events and nothing in between (an event between splices adds its own packet).
-    t_begin = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_begin.record(stream)
-    for i in range(args.steps):
-        step(i)
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    total_ms = t_begin.elapsed_time(t_end)
-    ms_per_step = total_ms / args.steps
+    ms_per_step = timed(step, args.steps, args.warmup, stream)
     splice_ms = ms_per_step
-    achieved = alg_bytes / (splice_ms * 1e-3) / 1e9
+    achieved, traffic, rec = roofline_of(wl, kernel, alg_bytes, launches, splice_ms)
     # Spread of single splices, from a separate untimed pass with an event pair around each.
     n_spread = min(args.steps, 20)
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(n_spread)]
@@ -228,8 +286,6 @@ def main():
     torch.cuda.synchronize()
     per_splice = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
     copy_gbps, _ = copy_ceiling(alg_bytes, dev, stream)
-    rec = measured_traffic(wl.name)
-    traffic = rec["dispatch_bytes"] if rec and rec.get("kernel") == kernel else None
     out = {
         "metric": METRIC,
         "value": moved / (ms_per_step * 1e-3),
@@ -275,8 +331,14 @@ def main():
             "kernel_sha": kernel_sha(),
         },
     }
+    del step
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    also = [a for a in args.also.split(",") if a and a != wl.name]
+    if also:
+        out["also"] = [measure_also(a, args, dev, L, W, stream) for a in also]
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, keep, args.cpu_seconds, moved)
+        out["cpu_baseline"] = cpu_baseline(wl, keep, args.cpu_seconds, moved, args.cpu_procs)
     print(json.dumps(out), flush=True)
 
 
@@ -366,10 +428,66 @@ def _cpu_model():
     return None
 
 
-def cpu_baseline(wl, keep, budget_s, moved):
-    """The oracle, as it stands, on a bounded sample of the same splice: whole layers, cycled
-    until about budget_s seconds have passed, scaled to all layers.  numpy runs single-threaded
-    here."""
+def _oracle_inputs(meta):
+    from oracle import splice_oracle as O
+    dirs = [O.Directive(*d) for d in meta["dirs"]]
+    planes = [O.Plane(**p) for p in meta["planes"]]
+    return O, dirs, planes
+
+
+def _leg_work(arg):
+    """One worker of the all-cores leg: splices the sample's layers (worker i takes layers i,
+    i + procs, ... cyclically) with the oracle until `seconds` have passed; returns the count."""
+    data, i, procs, seconds = arg
+    with open(os.path.join(data, "meta.json")) as f:
+        meta = json.load(f)
+    O, dirs, planes = _oracle_inputs(meta)
+    rows = [np.load(os.path.join(data, f"plane_{pi}.npy"), mmap_mode="r") for pi in range(len(planes))]
+    stubs = [[np.load(os.path.join(data, f"stub_{j}_{pi}.npy"), mmap_mode="r") for pi in range(len(planes))]
+             for j in range(len(dirs))]
+    n_keep, done = rows[0].shape[0], 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        l = (i + done * procs) % n_keep
+        for pi, plane in enumerate(planes):
+            O.splice_rows(np.asarray(rows[pi][l]), meta["n"], dirs, [np.asarray(st[pi][l]) for st in stubs],
+                          plane, meta["dtype"])
+        done += 1
+    return done
+
+
+def cpu_leg(data, seconds, procs, out):
+    """The all-cores leg, in a child process that touches no GPU: `procs` forked workers run
+    _leg_work at once; writes the layer-splices done and the wall time."""
+    import multiprocessing as mp
+    procs = int(procs)
+    with mp.get_context("fork").Pool(procs) as pool:
+        t0 = time.perf_counter()
+        done = pool.map(_leg_work, [(data, i, procs, float(seconds)) for i in range(procs)])
+        wall = time.perf_counter() - t0
+    with open(out, "w") as f:
+        json.dump({"layer_splices": int(sum(done)), "wall_s": wall, "procs": procs}, f)
+
+
+def _host_cpus():
+    """CPUs this process may run on (the machine's CPU share, at most 16 on a one-GPU machine)."""
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
+def cpu_baseline(wl, keep, budget_s, moved, procs=0):
+    """The oracle, as it stands, on a bounded sample of the same splice: whole layers of the
+    headline cache (host copies taken before the first step), scaled to all layers.  Two legs:
+    one thread (numpy, single-threaded here), cycling over the sample's layers for about
+    budget_s seconds; and all host cores, `procs` processes (default: every CPU this process may
+    use, at most 16) splicing different layers at once for about the same time, in a child
+    process started for it."""
+    import shutil
+    import subprocess
+    import tempfile
+
     import torch
     from oracle import splice_oracle as O
     if keep.get("paged") or keep.get("rotate"):
@@ -379,10 +497,12 @@ def cpu_baseline(wl, keep, budget_s, moved):
         return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
 
     n = wl.seq_lens[0]
-    dirs = [O.Directive(d.span_start, d.span_end, d.stub_len) for d in wl.dirs]
-    planes = [O.Plane(row_elems=p.row_elems, n_heads=p.n_heads, head_stride=p.head_stride or p.row_elems,
-                      rot_offset=p.rot_offset, rot_dim=p.rot_dim, style=p.style, base=p.base)
-              for p in wl.planes]
+    meta = {"n": n, "dtype": wl.dtype, "n_layers": wl.n_layers,
+            "dirs": [[d.span_start, d.span_end, d.stub_len] for d in wl.dirs],
+            "planes": [dict(row_elems=p.row_elems, n_heads=p.n_heads, head_stride=p.head_stride or p.row_elems,
+                            rot_offset=p.rot_offset, rot_dim=p.rot_dim, style=p.style, base=p.base)
+                       for p in wl.planes]}
+    _, dirs, planes = _oracle_inputs(meta)
     n_keep = keep["planes"][0].shape[0]
     rows = [[host(t[l]).reshape(t.shape[1], -1) for t in keep["planes"]] for l in range(n_keep)]
     stubs = [[[host(s[l]).reshape(s.shape[1], -1) for s in per] for per in keep["stubs"]] for l in range(n_keep)]
@@ -396,17 +516,45 @@ def cpu_baseline(wl, keep, budget_s, moved):
         done += 1
     per_layer = spent / done
     full_s = per_layer * wl.n_layers
-    return {
+    out = {
         "value": moved / full_s,
         "unit": "tokens/s",
         "cores": 1,
-        "host_cpus": os.cpu_count(),
+        "host_cpus": _host_cpus(),
         "host_cpu_model": _cpu_model(),
         "kind": "oracle",
         "sample": f"{done} layer-splices of this workload (numpy fp64, one thread, layers cycled "
                   f"over {n_keep} host-resident layers), {spent:.1f} s; scaled to {wl.n_layers} "
                   f"layers: {full_s:.3f} s per splice",
     }
+    # all host cores: the same oracle in `procs` processes at once, each on its own layers
+    procs = procs or min(16, _host_cpus())
+    tmp = tempfile.mkdtemp(prefix="leyline_cpu_leg_")
+    try:
+        for pi in range(len(planes)):
+            np.save(os.path.join(tmp, f"plane_{pi}.npy"), np.stack([rows[l][pi] for l in range(n_keep)]))
+            for j in range(len(dirs)):
+                np.save(os.path.join(tmp, f"stub_{j}_{pi}.npy"), np.stack([stubs[l][j][pi] for l in range(n_keep)]))
+        with open(os.path.join(tmp, "meta.json"), "w") as f:
+            json.dump(meta, f)
+        res = os.path.join(tmp, "leg.json")
+        env = dict(os.environ, OMP_NUM_THREADS="1", OPENBLAS_NUM_THREADS="1", MKL_NUM_THREADS="1")
+        subprocess.run([sys.executable, os.path.abspath(__file__), "--cpu-leg", tmp, str(budget_s), str(procs), res],
+                       check=True, env=env, timeout=budget_s * 4 + 120)
+        with open(res) as f:
+            leg = json.load(f)
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+    splices = leg["layer_splices"] / wl.n_layers
+    out["all_cores"] = {
+        "value": moved * splices / leg["wall_s"],
+        "unit": "tokens/s",
+        "cores": leg["procs"],
+        "sample": f"{leg['layer_splices']} layer-splices in {leg['procs']} processes at once (one numpy "
+                  f"thread each, every process cycling over its share of the same {n_keep} layers) in "
+                  f"{leg['wall_s']:.1f} s of wall time; {wl.n_layers} layer-splices make one splice",
+    }
+    return out
 
 
 # ---------------------------------------------------------------------- profile summaries ---

@@ -44,10 +44,21 @@ def test_default_run_reports_roofline_and_cpu_baseline():
     c = d["cpu_baseline"]
     assert c["kind"] == "oracle" and c["unit"] == "tokens/s" and c["value"] > 0
     assert isinstance(c["cores"], int) and c["cores"] >= 1 and c["sample"]
+    ac = c["all_cores"]        # the same oracle in one process per host core
+    assert ac["unit"] == "tokens/s" and ac["value"] > 0 and ac["cores"] >= 1 and ac["sample"]
+    # the GQA target configuration and the 8-directive paged splice, timed in the same run
+    also = {a["workload"]: a for a in d["also"]}
+    assert set(also) == {"gqa_llama3_8b_16k", "mla_dsv3_paged_131k"}
+    for a in also.values():
+        assert a["ms_per_step"] > 0 and a["kernel"] and a["steps"] == 3
+        assert a["value"] > 0 and a["unit"] == "tokens/s"
+        assert abs(a["frac"] - a["achieved_GBps"] / 8000.0) < 1e-12
+        assert abs(a["achieved_GBps"] - a["algorithmic_bytes_per_splice"] / (a["ms_per_step"] * 1e-3) / 1e9) \
+            <= 1e-6 * a["achieved_GBps"]
 
 
 @pytest.mark.parametrize("workload", ["mla_dsv3_slots_32k", "gqa_llama3_8b_rotate_16k", "mla_dsv3_32k_edits8"])
 def test_other_workloads_keep_the_contract(workload):
-    d = _bench("--workload", workload, "--steps", "3", "--warmup", "1", "--no-cpu-baseline")
+    d = _bench("--workload", workload, "--steps", "3", "--warmup", "1", "--no-cpu-baseline", "--also", "")
     _check_common(d, 3, 1)
-    assert d["config"]["workload"] == workload and "cpu_baseline" not in d
+    assert d["config"]["workload"] == workload and "cpu_baseline" not in d and "also" not in d
