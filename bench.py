@@ -53,9 +53,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"))
     ap.add_argument("--command", default="", help="command line recorded in --summarize output")
-    ap.add_argument("--also", default="gqa_llama3_8b_16k,mla_dsv3_paged_131k",
+    ap.add_argument("--also", default="gqa_llama3_8b_16k,mla_dsv3_paged_131k,mla_dsv3_32k:exact,gqa_llama3_8b_16k:exact",
                     help="further workloads timed in the same run and reported under \"also\" "
-                         "(comma-separated; empty: none)")
+                         "(comma-separated; NAME:exact runs libleyline_exact.so; empty: none)")
     ap.add_argument("--cpu-procs", type=int, default=0,
                     help="processes of the all-cores oracle leg (0: every CPU this process may use, at most 16)")
     ap.add_argument("--cpu-leg", nargs=4, metavar=("DATA", "SECONDS", "PROCS", "OUT"),
@@ -220,19 +220,28 @@ def roofline_of(wl, kernel, alg_bytes, launches, splice_ms):
     return achieved, traffic, rec
 
 
-def measure_also(name, args, dev, L, W, stream):
-    """A second configuration timed in the same run (same protocol as the headline), reported as
-    a compact record."""
+def measure_also(spec, args, dev, L, W, stream):
+    """A further configuration timed in the same run (same protocol as the headline), reported as
+    a compact record.  spec: a workload name, with ":exact" for libleyline_exact.so (fp64 pair
+    arithmetic, results bit-identical to the oracle) instead of libleyline.so."""
     import torch
+    name, _, variant = spec.partition(":")
+    exact = variant == "exact"
     wl = W.WORKLOADS[name]()
-    step, kernel, alg_bytes, moved, launches, keep, layout = setup_workload(wl, dev, L, W, args, stream)
-    ms = timed(step, args.steps, args.warmup, stream)
-    achieved, traffic, _ = roofline_of(wl, kernel, alg_bytes, launches, ms)
-    del step, keep
-    torch.cuda.synchronize()
+    L.use_library(exact)
+    try:
+        step, kernel, alg_bytes, moved, launches, keep, layout = setup_workload(wl, dev, L, W, args, stream)
+        ms = timed(step, args.steps, args.warmup, stream)
+        pair_bits = L.leyline_pair_bits()
+        del step, keep
+        torch.cuda.synchronize()
+    finally:
+        L.use_library(False)
     torch.cuda.empty_cache()
+    achieved, traffic, _ = roofline_of(wl, kernel, alg_bytes, launches, ms)
     return {
         "workload": wl.name,
+        "pair_bits": pair_bits,
         "layout": layout,
         "ms_per_step": ms,
         "value": moved / (ms * 1e-3),
@@ -242,7 +251,7 @@ def measure_also(name, args, dev, L, W, stream):
         "avg_launch_ms": ms / max(1, launches),
         "achieved_GBps": achieved,
         "frac": achieved / PEAK_HBM_GBPS,
-        "traffic": traffic,
+        "traffic": None if exact else traffic,
         "algorithmic_bytes_per_splice": alg_bytes,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -308,6 +317,7 @@ def main():
             "directives": [[d.seq, d.span_start, d.span_end, d.stub_len] for d in wl.dirs][:8],
             "moved_tokens": moved,
             "layout": layout,
+            "pair_bits": L.leyline_pair_bits(),
             **({"rotate_delta_row0_rows": list(wl.rotate)} if wl.rotate else {}),
         },
         "roofline": {
@@ -334,7 +344,7 @@ def main():
     del step
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
-    also = [a for a in args.also.split(",") if a and a != wl.name]
+    also = [a for a in args.also.split(",") if a and a != wl.name]      # NAME:exact is kept
     if also:
         out["also"] = [measure_also(a, args, dev, L, W, stream) for a in also]
     if not args.no_cpu_baseline:

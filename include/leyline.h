@@ -147,6 +147,14 @@ const char* leyline_strerror(int code);
 /* LEYLINE_ABI_VERSION of the loaded library. */
 int leyline_abi_version(void);
 
+/* Precision of the loaded library's rotation arithmetic: 32 or 64.  libleyline.so (32) takes
+ * cos/sin rounded to fp32 and computes each rotated pair in fp32 (the paper's policy, Sec. 4.1
+ * "bf16 K-storage precision floor"), then rounds once to the storage dtype.  libleyline_exact.so
+ * (64) takes fp64 cos/sin and computes in fp64, then rounds once to the storage dtype, so stored
+ * values are the correctly rounded exact rotation (bit-identical to a float64 reference up to
+ * fp64 rounding).  Both export the same entry points. */
+int leyline_pair_bits(void);
+
 /* The HIP runtime's description of the error behind the last LEYLINE_E_HIP returned on the
  * calling thread ("no error" if there was none).  Static storage. */
 const char* leyline_last_hip_error(void);

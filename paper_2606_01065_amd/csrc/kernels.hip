@@ -108,11 +108,35 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
     return __builtin_bit_cast(uint32_t, v);
 }
 
-__device__ __forceinline__ void rot_pair(float& a, float& b, float c, float s) {
-    const float a2 = a * c - b * s;
-    const float b2 = a * s + b * c;
+// (a, b) -> (a c - b s, a s + b c) (Eq. "rotate").  BF16: the results are bf16-bound, and come back
+// as floats whose nearest-even bf16 is the stored value.  With fp64 pairs the products are fp64
+// and each result is rounded once (to odd for bf16, see f32_round_odd; to nearest-even for fp32).
+template <bool BF16>
+__device__ __forceinline__ void rot_pair(float& a, float& b, const KCosSin& k) {
+#if LEYLINE_PAIR_F64
+    const double x = a, y = b;
+    const double a2 = x * k.c - y * k.s;
+    const double b2 = x * k.s + y * k.c;
+    a = BF16 ? f32_round_odd(a2) : float(a2);
+    b = BF16 ? f32_round_odd(b2) : float(b2);
+#else
+    const float a2 = a * k.c - b * k.s;
+    const float b2 = a * k.s + b * k.c;
     a = a2;
     b = b2;
+#endif
+}
+
+// One member of a half-split pair, on the lane that holds it: the low member a becomes
+// a c - b s, the high member b becomes b c + a s, i.e. mine * c + partner * (lo ? -s : s).
+template <bool BF16>
+__device__ __forceinline__ float rot_own(float mine, float partner, const KCosSin& k, bool lo) {
+#if LEYLINE_PAIR_F64
+    const double r = double(mine) * k.c + double(partner) * (lo ? -k.s : k.s);
+    return BF16 ? f32_round_odd(r) : float(r);
+#else
+    return mine * k.c + partner * (lo ? -k.s : k.s);
+#endif
 }
 
 template <int ESZ> struct Elt { static constexpr int EPC = 16 / ESZ; };   // elements per chunk
@@ -124,7 +148,7 @@ template <> __device__ __forceinline__ void rot_interleaved<2>(u32x4& v, const K
     for (int i = 0; i < 4; ++i) {
         const KCosSin k = t[cs + i];
         float a = bf_lo(v[i]), b = bf_hi(v[i]);
-        rot_pair(a, b, k.c, k.s);
+        rot_pair<true>(a, b, k);
         v[i] = pack_bf16(a, b);
     }
 }
@@ -133,7 +157,7 @@ template <> __device__ __forceinline__ void rot_interleaved<4>(u32x4& v, const K
     for (int i = 0; i < 2; ++i) {
         const KCosSin k = t[cs + i];
         float a = __uint_as_float(v[2 * i]), b = __uint_as_float(v[2 * i + 1]);
-        rot_pair(a, b, k.c, k.s);
+        rot_pair<false>(a, b, k);
         v[2 * i] = __float_as_uint(a);
         v[2 * i + 1] = __float_as_uint(b);
     }
@@ -148,8 +172,8 @@ template <> __device__ __forceinline__ void rot_halves<2>(u32x4& x, u32x4& y, co
         const KCosSin k0 = t[cs + 2 * i], k1 = t[cs + 2 * i + 1];
         float a0 = bf_lo(x[i]), a1 = bf_hi(x[i]);
         float b0 = bf_lo(y[i]), b1 = bf_hi(y[i]);
-        rot_pair(a0, b0, k0.c, k0.s);
-        rot_pair(a1, b1, k1.c, k1.s);
+        rot_pair<true>(a0, b0, k0);
+        rot_pair<true>(a1, b1, k1);
         x[i] = pack_bf16(a0, a1);
         y[i] = pack_bf16(b0, b1);
     }
@@ -159,10 +183,45 @@ template <> __device__ __forceinline__ void rot_halves<4>(u32x4& x, u32x4& y, co
     for (int i = 0; i < 4; ++i) {
         const KCosSin k = t[cs + i];
         float a = __uint_as_float(x[i]), b = __uint_as_float(y[i]);
-        rot_pair(a, b, k.c, k.s);
+        rot_pair<false>(a, b, k);
         x[i] = __float_as_uint(a);
         y[i] = __float_as_uint(b);
     }
+}
+
+// Lane-exchanged half-split chunk: `v` is this lane's chunk of the band, `o` the partner lane's
+// (the other half); only this lane's elements are computed.  Element e pairs with element e of
+// the partner chunk, cos/sin table[cs + e].
+template <int ESZ> __device__ __forceinline__ void rot_halves_own(u32x4& v, const u32x4& o, const KCosSin* t,
+                                                                  int32_t cs, bool lo);
+template <> __device__ __forceinline__ void rot_halves_own<2>(u32x4& v, const u32x4& o, const KCosSin* t,
+                                                              int32_t cs, bool lo) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float m0 = rot_own<true>(bf_lo(v[i]), bf_lo(o[i]), t[cs + 2 * i], lo);
+        const float m1 = rot_own<true>(bf_hi(v[i]), bf_hi(o[i]), t[cs + 2 * i + 1], lo);
+        v[i] = pack_bf16(m0, m1);
+    }
+}
+template <> __device__ __forceinline__ void rot_halves_own<4>(u32x4& v, const u32x4& o, const KCosSin* t,
+                                                              int32_t cs, bool lo) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        v[i] = __float_as_uint(rot_own<false>(__uint_as_float(v[i]), __uint_as_float(o[i]), t[cs + i], lo));
+}
+
+// A lane-exchanged half-split chunk, rotated: `v` is this lane's chunk, `o` its partner lane's,
+// `cs` the cos/sin entry of the chunk's first pair, `lo` whether this lane holds low members.
+// With fp64 pairs only this lane's members are computed (halves the fp64 work); with fp32 pairs
+// both members of every pair are computed and the partner's discarded, which measured faster.
+template <int ESZ>
+__device__ __forceinline__ void rot_exchanged(u32x4& v, u32x4& o, const KCosSin* t, int32_t cs, bool lo) {
+#if LEYLINE_PAIR_F64
+    rot_halves_own<ESZ>(v, o, t, cs, lo);
+#else
+    if (lo) rot_halves<ESZ>(v, o, t, cs);
+    else rot_halves<ESZ>(o, v, t, cs);
+#endif
 }
 
 // ------------------------------------------------------------------------- row geometry ---
@@ -225,8 +284,7 @@ __device__ __forceinline__ void rotate_chunk(const KPlane& pl, u32x4& v, int32_t
             u32x4 o;
 #pragma unroll
             for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[i]), partner, 64));
-            if (lo) rot_halves<ESZ>(v, o, table, cs + j * EPC);
-            else rot_halves<ESZ>(o, v, table, cs + (j - half) * EPC);
+            rot_exchanged<ESZ>(v, o, table, cs + (lo ? j : j - half) * EPC, lo);
         }
     }
 }
@@ -269,8 +327,7 @@ __device__ __forceinline__ void rotate_band_chunk(const KPlane& pl, u32x4& v, in
         u32x4 o;
 #pragma unroll
         for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[i]), partner, 64));
-        if (lo) rot_halves<ESZ>(v, o, table, cs + j * EPC);
-        else rot_halves<ESZ>(o, v, table, cs + (j - half) * EPC);
+        rot_exchanged<ESZ>(v, o, table, cs + (lo ? j : j - half) * EPC, lo);
     }
 }
 
@@ -361,17 +418,26 @@ __device__ __forceinline__ void stage_cs(KCosSin* lcs, const KCosSin* table, int
 // cs_fetch before the data loads are issued, cs_commit after.  Vector loads complete in order,
 // so the wait before the LDS write then covers the cos/sin load only, and the barrier that
 // follows does not wait for any wavefront's data.
+#if LEYLINE_PAIR_F64
+typedef KCosSin CsReg;
+#else
+typedef uint64_t CsReg;   // one 64-bit value: merges with the default without a copy
+#endif
 template <class Ptr>
-__device__ __forceinline__ uint64_t cs_fetch(Ptr table, int32_t c0, int32_t n) {
-    uint64_t c = 0;     // one 64-bit value: merges with the default without a copy
+__device__ __forceinline__ CsReg cs_fetch(Ptr table, int32_t c0, int32_t n) {
+    CsReg c{};
     if (int(threadIdx.x) < n) {
         const KCosSin e = table[c0 + threadIdx.x];
+#if LEYLINE_PAIR_F64
+        c = e;
+#else
         c = uint64_t(__float_as_uint(e.c)) | (uint64_t(__float_as_uint(e.s)) << 32);
+#endif
     }
     return c;
 }
-__device__ __forceinline__ void cs_commit(KCosSin* lcs, uint64_t c, int32_t n) {
-    if (int(threadIdx.x) < n) *reinterpret_cast<uint64_t*>(lcs + threadIdx.x) = c;
+__device__ __forceinline__ void cs_commit(KCosSin* lcs, const CsReg& c, int32_t n) {
+    if (int(threadIdx.x) < n) *reinterpret_cast<CsReg*>(lcs + threadIdx.x) = c;
 }
 
 // --------------------------------------------------------------------- contiguous splice ---
@@ -424,7 +490,7 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
     // data; wide bands (most of the row rotates): staged after the data loads, so the barrier
     // also lines up the workgroup's stores (measured faster there)
     const bool early = rot && !pl.band_wide;
-    const uint64_t c = cs_fetch(P.cs, I.cs, early ? pl.n_pairs : 0);
+    const CsReg c = cs_fetch(P.cs, I.cs, early ? pl.n_pairs : 0);
     u32x4 v[CRPT];
 #pragma unroll
     for (int k = 0; k < CRPT; ++k) {
@@ -454,8 +520,7 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
                     u32x4 o;
 #pragma unroll
                     for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[k][i]), partner, 64));
-                    if (lo) rot_halves<ESZ>(v[k], o, lcs, j * EPC);
-                    else rot_halves<ESZ>(o, v[k], lcs, (j - half) * EPC);
+                    rot_exchanged<ESZ>(v[k], o, lcs, (lo ? j : j - half) * EPC, lo);
                 }
             }
             st16(dst + (r0 + k) * pl.token_stride + off, v[k]);
@@ -651,7 +716,7 @@ __global__ __launch_bounds__(PAGED_TPB) void rotate_rows_kernel(const KRotatePar
     }
     const BandPos bp = band_pos(pl, q);
     static_assert(KMAX_CS <= PAGED_TPB, "one cos/sin entry per thread");
-    const uint64_t c = cs_fetch(P.cs, pl.cs_off, pl.n_pairs);
+    const CsReg c = cs_fetch(P.cs, pl.cs_off, pl.n_pairs);
     u32x4 x[PAGED_LPT], y[PAGED_LPT];
     if (active) band_load(bp, r, pl.layer_stride, nl, x, y);
     cs_commit(lcs, c, pl.n_pairs);
@@ -889,7 +954,7 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, const Pl
         const int32_t i0 = fdiv(tb, pl.tpr_div);
         cs0 = INLINE ? row_entry(P, V, i0).cs : P.rows[i0].cs;
     }
-    const uint64_t c = cs_fetch(V.cs, cs0 + pl.cs_off, cs0 >= 0 ? pl.n_pairs : 0);
+    const CsReg c = cs_fetch(V.cs, cs0 + pl.cs_off, cs0 >= 0 ? pl.n_pairs : 0);
     // PAGED_LPT consecutive layers per thread: one row entry, all loads in flight before any store.
     const int layer0 = int(blockIdx.y) * PAGED_LPT;
     const int nl = min(PAGED_LPT, P.n_layers - layer0);
@@ -960,7 +1025,7 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const P
         cs0 = V.dirs[R0.dir].cs;
         len0 = V.seqs[R0.seq].new_len;
     }
-    const uint64_t c = cs_fetch(V.cs, cs0 + pl.cs_off, cs0 >= 0 ? pl.n_pairs : 0);
+    const CsReg c = cs_fetch(V.cs, cs0 + pl.cs_off, cs0 >= 0 ? pl.n_pairs : 0);
     bool active = m < P.n_remap;
     KRemapPage e{0, -1, 0, 0};
     if (active) {
@@ -1063,6 +1128,8 @@ bool any_overlap(const Span* b, size_t n) {
 }  // namespace leyline
 
 using namespace leyline;
+
+extern "C" int leyline_pair_bits(void) { return int(sizeof(kcs_t) * 8); }
 
 extern "C" const char* leyline_last_hip_error(void) {
     return hipGetErrorString(g_last_hip_error);

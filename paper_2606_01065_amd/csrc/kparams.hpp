@@ -56,13 +56,41 @@ struct KPlane {
     KDiv band_div;           // division by band_tpr
 };
 
+// Precision of the pair arithmetic.  0: fp32 cos/sin and fp32 products (the paper's policy);
+// 1: fp64 cos/sin and fp64 products, each result rounded once to the storage dtype, which makes
+// the stored values the correctly rounded ones of the exact rotation (up to fp64 rounding).
+#ifndef LEYLINE_PAIR_F64
+#define LEYLINE_PAIR_F64 0
+#endif
+#if LEYLINE_PAIR_F64
+typedef double kcs_t;
+#else
+typedef float kcs_t;
+#endif
+
 struct KCosSin {
-    float c, s;
+    kcs_t c, s;
 };
+
+// fp64 -> fp32 rounded to odd: the value truncated toward zero, with the last bit set when the
+// conversion was inexact.  Rounding this float to nearest-even bf16 (16 bits fewer) gives the
+// nearest-even bf16 of the fp64 value itself: rounding to odd with at least two extra bits and
+// then to nearest is one correct rounding (Boldo and Melquiond, "Emulation of FMA and correctly
+// rounded sums: proved algorithms using rounding to odd", 2008).  Built from the nearest-even
+// conversion: an inexact result whose last bit is even is replaced by its neighbour on the side
+// of the fp64 value, which is then the odd one of the two floats around it.
+LEYLINE_HD inline float f32_round_odd(double d) {
+    const float f = float(d);
+    uint32_t u = __builtin_bit_cast(uint32_t, f);
+    if (double(f) != d && !(u & 1u)) u += __builtin_fabs(d) > __builtin_fabs(double(f)) ? 1u : 0xffffffffu;
+    return __builtin_bit_cast(float, u);
+}
 
 // ------------------------------------------------------------------------------ contiguous --
 constexpr int KMAX_JOBS = 6;
-constexpr int KMAX_CS = 192;
+// cos/sin pairs one launch carries in its kernel arguments (and stages in LDS); sized so that the
+// argument blocks stay within 3.4 KB whatever the pair precision
+constexpr int KMAX_CS = LEYLINE_PAIR_F64 ? 120 : 192;
 
 
 
@@ -226,7 +254,7 @@ LEYLINE_HD inline void tile_wait_flags(const KTileParams& P, int32_t it, int32_t
 
 // Before the tile launches of a call: clear its counters and flags, and write entries of its
 // cos/sin table into the workspace (carried here, in the kernel arguments).
-constexpr int KPREP_CS = 320;
+constexpr int KPREP_CS = LEYLINE_PAIR_F64 ? 208 : 320;
 
 struct KPrepParams {
     int32_t* zero;

@@ -134,7 +134,7 @@ int32_t append_cos_sin(const leyline_cache* cache, int64_t shift, std::vector<KC
             const double theta = pl.inv_freq ? pl.inv_freq[i]
                                              : std::pow(pl.rope_base, -2.0 * i / pl.rot_dim);
             const double phi = d * theta;
-            table.push_back(KCosSin{float(std::cos(phi)), float(std::sin(phi))});
+            table.push_back(KCosSin{kcs_t(std::cos(phi)), kcs_t(std::sin(phi))});
         }
     }
     return first;

@@ -16,6 +16,8 @@ from typing import List, Optional, Sequence
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libleyline.so")
+#: the same entry points with fp64 pair arithmetic (results bit-identical to a float64 reference)
+EXACT_LIB_PATH = os.path.join(HERE, "libleyline_exact.so")
 
 MAX_PLANES = 4
 OK, E_INVAL, E_RANGE, E_ORDER, E_OVERLAP, E_CAPACITY, E_MODE, E_WORKSPACE, E_HIP = 0, -1, -2, -3, -4, -5, -6, -7, -8
@@ -81,14 +83,15 @@ def _hip_runtimes_mapped():
         return []
 
 
-def _load():
-    if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_01065_amd.build`")
+def _load(path=None):
+    path = path or LIB_PATH
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run `python -m paper_2606_01065_amd.build`")
     # torch ships its own HIP runtime.  It must be loaded before the library so that the
     # library's HIP dependency resolves to that same copy: two HIP/HSA runtimes in one process
     # cannot both open the GPU.
     import torch  # noqa: F401
-    lib = ctypes.CDLL(LIB_PATH)
+    lib = ctypes.CDLL(path)
     runtimes = _hip_runtimes_mapped()
     if len(runtimes) > 1:
         raise ImportError("more than one HIP runtime is loaded in this process "
@@ -98,6 +101,7 @@ def _load():
     sig = {
         "leyline_strerror": (ctypes.c_char_p, [c_int]),
         "leyline_abi_version": (c_int, []),
+        "leyline_pair_bits": (c_int, []),
         "leyline_last_hip_error": (ctypes.c_char_p, []),
         "leyline_contig_query": (c_int, [P(leyline_cache), c_int64, P(leyline_directive), c_int32,
                                          P(c_int64), P(c_int32), P(c_int32), P(c_int64)]),
@@ -127,8 +131,16 @@ def _load():
 
 _lib = _load()
 
+
+def use_library(exact: bool) -> None:
+    """Route every call of this module to libleyline_exact.so (fp64 pair arithmetic) or back to
+    libleyline.so (fp32 pair arithmetic)."""
+    global _lib
+    _lib = _load(EXACT_LIB_PATH if exact else LIB_PATH)
+
 #: every symbol the header declares (checked by tests against the loaded library)
-SYMBOLS = ("leyline_strerror", "leyline_abi_version", "leyline_last_hip_error", "leyline_contig_query",
+SYMBOLS = ("leyline_strerror", "leyline_abi_version", "leyline_pair_bits", "leyline_last_hip_error",
+           "leyline_contig_query",
            "leyline_splice_contig", "leyline_splice_contig_noalloc", "leyline_paged_query",
            "leyline_paged_plan", "leyline_splice_paged", "leyline_rotate_delta")
 
@@ -142,6 +154,10 @@ def strerror(code: int) -> str:
 
 def leyline_abi_version() -> int:
     return _lib.leyline_abi_version()
+
+
+def leyline_pair_bits() -> int:
+    return _lib.leyline_pair_bits()
 
 
 # ----------------------------------------------------------------------------- descriptors --

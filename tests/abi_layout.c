@@ -25,7 +25,8 @@ int main(void) {
     {
         typedef void (*fn_t)(void);
         const fn_t fns[] = {
-            (fn_t)leyline_strerror, (fn_t)leyline_abi_version, (fn_t)leyline_last_hip_error,
+            (fn_t)leyline_strerror, (fn_t)leyline_abi_version, (fn_t)leyline_pair_bits,
+            (fn_t)leyline_last_hip_error,
             (fn_t)leyline_contig_query, (fn_t)leyline_splice_contig, (fn_t)leyline_splice_contig_noalloc,
             (fn_t)leyline_paged_query,
             (fn_t)leyline_paged_plan, (fn_t)leyline_splice_paged, (fn_t)leyline_rotate_delta,

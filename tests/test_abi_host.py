@@ -199,6 +199,27 @@ def test_noalloc_splice_refuses_more_than_its_scratch_before_any_enqueue():
                                                 None, None) == L.E_RANGE
 
 
+def test_exact_library_sizes_its_tables_for_fp64_pairs():
+    """libleyline_exact.so keeps 16-byte fp64 cos/sin entries: a one-token shift of the 2-layer
+    MLA cache needs the same counter and flags and 32 pairs of 16 bytes; the small-shift edits
+    that need two prep launches of 320 fp32 pairs need three of 208 fp64 pairs."""
+    L.use_library(True)
+    try:
+        assert L.leyline_pair_bits() == 64
+        c = _mla_cache(cap=64)
+        q = L.leyline_contig_query(c, 60, _dirs([(10, 11, 0)]), 1)
+        tiles = -(-49 * 72 // 8192)
+        flags_end = 256 + 4 * 2 * tiles
+        assert q.workspace_bytes == -(-(-(-flags_end // 256) * 256 + 32 * 16) // 256) * 256
+        c = _mla_cache(n_layers=3, cap=4000)
+        spec = [(100 + 200 * i, 110 + 200 * i, 10 + (i % 3) + 1) for i in range(16)]
+        q = L.leyline_contig_query(c, 3800, _dirs(spec), 16)
+        assert (q.tile_launches, q.launches) == (2, 3 + 2)
+    finally:
+        L.use_library(False)
+    assert L.leyline_pair_bits() == 32
+
+
 def test_forget_trims_without_moving_anything():
     """A FORGET directive (last of its sequence, no replacement) cuts the sequence at its span's
     start after the earlier directives; the cut itself moves nothing."""
