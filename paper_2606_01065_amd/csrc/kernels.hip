@@ -580,19 +580,19 @@ __global__ __launch_bounds__(TPB) void contig_chain_kernel(const KContigParams P
 }
 
 // Ordered tiles: every job of a call whose moves are too short-shifted for rounds.  Each
-// (job, plane) item is cut into tiles of KTILE_CHUNKS chunks (counted from its first row), one
-// workgroup and one layer each.  Workgroups take tickets in the order they start; the items of a
-// launch own consecutive ticket ranges in dependency order, and within an item ticket t is tile
+// (job, plane) item is cut into tiles of KTILE_CHUNKS chunks (counted from its first row) in
+// each layer.  Workgroups take tile tickets from a counter, in order; the items of a launch own
+// consecutive ticket ranges in dependency order, and within an item ticket t is tile
 // t mod n_tiles of its processing order (a left shift ascending, a right shift descending) in
-// layer t / n_tiles, so that workgroups running together cover one stretch of one layer
-// (interleaving the layers costs several points of bandwidth).
+// layer t / n_tiles, so that the tiles in flight cover one stretch of one layer (interleaving
+// the layers costs several points of bandwidth).
 //
-// A tile loads its whole source into registers, waits until those loads have returned and (a
-// move) publishes "source read".  Before storing it waits for every tile whose source rows its
+// A tile's chunks are loaded into registers; once those loads have returned, a move tile
+// publishes "source read".  Before storing, a tile waits for every tile whose source rows its
 // destination overlaps (tile_wait_flags), so no tile reads a chunk another tile has written.
-// A tile waits only for tickets taken before its own, by workgroups that publish before they
-// wait, so every wait ends.  The wait is still bounded (KTILE_SPIN_LIMIT polls per flag): a tile
-// that gives up flags LEYLINE_STATUS_TILE_TIMEOUT and stores nothing, and the launch drains.
+// A tile waits only for tickets taken before its own, which publish without waiting, so every
+// wait ends.  The wait is still bounded (KTILE_SPIN_LIMIT polls per flag): a tile that gives up
+// flags LEYLINE_STATUS_TILE_TIMEOUT and stores nothing, and the launch drains.
 //
 // ROT: the rotary style of every re-anchored item of the launch (KROT_NONE: looked up per item),
 // so that the style this launch does not use costs no registers.
@@ -602,60 +602,142 @@ __device__ __forceinline__ bool wait_flag(const int32_t* f) {
         [] { __builtin_amdgcn_s_sleep(1); }, KTILE_SPIN_LIMIT);
 }
 
+// Persistent tile workgroups.  A workgroup keeps taking tickets until they run out, and holds at
+// most two tiles: the current one, whose chunks are in registers and whose "source read" flag is
+// published, and the next one, whose loads it issues before it waits for the current tile's
+// dependencies and stores it, so that the next tile's loads are in flight during that wait and
+// those stores.  Every wait still ends: the lowest unpublished ticket is either a workgroup's
+// current tile, published as soon as its loads return, or a workgroup's next tile, whose current
+// tile is lower, so all of that tile's dependencies are published and the workgroup goes on to
+// publish the next one.  A prefetched tile never reads a row that a lower ticket writes (a writer
+// always waits for the readers of its rows, which hold lower tickets).
+
+// One tile (ticket) of a tile launch, from the workgroup's point of view.
+struct TileCtx {
+    const char* src;
+    char* dst;
+    int64_t src_step;        // bytes between consecutive source rows
+    int32_t it, layer, order, local;
+    int32_t g0;              // this thread's first chunk of the tile
+    int32_t total;           // chunks of the item in one layer
+    int32_t cs;              // first cos/sin entry (-1: copied unchanged)
+    int32_t plane, flag0;
+    bool move;
+};
+
+__device__ __forceinline__ TileCtx tile_ctx(const KTileParams& P, int32_t ticket) {
+    TileCtx c;
+    c.it = tile_item_of(P, ticket);
+    KTileItem I;                // the item as a value: one level of independent scalar loads
+    __builtin_memcpy(&I, &P.items[c.it], sizeof(KTileItem));
+    const KPlane& pl = P.planes[I.plane];
+    c.move = I.kind == KJOB_TILE;
+    c.local = ticket - I.ticket0;
+    c.layer = c.local / I.n_tiles;
+    c.order = c.local - c.layer * I.n_tiles;
+    const int32_t q = I.delta <= 0 ? c.order : I.n_tiles - 1 - c.order;
+    c.total = int32_t(I.count) * pl.tpr;
+    char* lbase = pl.base + int64_t(c.layer) * pl.layer_stride;
+    c.src = c.move ? lbase + I.src0 * pl.token_stride : I.stub + int64_t(c.layer) * I.count * pl.row_bytes;
+    c.src_step = c.move ? pl.token_stride : pl.row_bytes;
+    c.dst = lbase + I.dst0 * pl.token_stride;
+    c.g0 = q * KTILE_CHUNKS + int32_t(threadIdx.x);
+    c.cs = I.cs;
+    c.plane = I.plane;
+    c.flag0 = I.flag0;
+    return c;
+}
+
+// Every slot loads (past the end of the range: the range's last chunk, which stays unused), so
+// that the loads are issued back to back without branches between them.
+__device__ __forceinline__ void tile_load(const KTileParams& P, const TileCtx& c, u32x4 (&v)[KTILE_CPT]) {
+    const KPlane& pl = P.planes[c.plane];
+#pragma unroll
+    for (int i = 0; i < KTILE_CPT; ++i) {
+        const int32_t gc = min(c.g0 + i * KTILE_TPB, c.total - 1);
+        const int32_t r = fdiv(gc, pl.tpr_div);
+        v[i] = ld16(c.src + int64_t(r) * c.src_step + int64_t(gc - r * pl.tpr) * 16);
+    }
+}
+
+template <int ESZ, int ROT>
+__device__ __forceinline__ void tile_store(const KTileParams& P, const TileCtx& c, u32x4 (&v)[KTILE_CPT],
+                                           const KCosSin* lcs) {
+    const KPlane& pl = P.planes[c.plane];
+#pragma unroll
+    for (int i = 0; i < KTILE_CPT; ++i) {
+        const int32_t g = c.g0 + i * KTILE_TPB;
+        if (g < c.total) {
+            const int32_t r = fdiv(g, pl.tpr_div), u = g - r * pl.tpr;
+            if (c.cs >= 0) rotate_chunk<ESZ, ROT>(pl, v[i], u, lcs, 0);
+            st16(c.dst + int64_t(r) * pl.token_stride + int64_t(u) * 16, v[i]);
+        }
+    }
+}
+
+// One step of a persistent workgroup: `cur` is loaded into `v` (loads issued) with its cos/sin
+// in `lcs`; the next ticket's tile goes to `nxt`, `nv` and `nlcs`.  Returns the next ticket
+// (>= n_tickets: none).  words[0] carries the next ticket, words[1] the store decision.
+template <int ESZ, int ROT>
+__device__ __forceinline__ int32_t tile_step(const KTileParams& P, const TileCtx& cur, u32x4 (&v)[KTILE_CPT],
+                                             const KCosSin* lcs, TileCtx& nxt, u32x4 (&nv)[KTILE_CPT],
+                                             KCosSin* nlcs, int32_t* words) {
+    __builtin_amdgcn_s_waitcnt(0);          // this thread's loads of the tile have returned
+    __syncthreads();                        // ... and every thread's; the tile's cos/sin are staged
+    if (threadIdx.x == 0) {
+        if (cur.move)
+            __hip_atomic_store(P.flags + cur.flag0 + cur.local, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        words[0] = atomicAdd(P.counter, 1);
+    }
+    __syncthreads();
+    const int32_t next = words[0];          // block-uniform
+    const bool more = next < P.n_tickets;
+    // Loads return in order, so a flag read issued after the next tile's loads would wait for
+    // them: the first wavefront waits for the current tile's dependencies before it issues its
+    // share of the next tile's loads; the other wavefronts issue theirs at once.
+    const bool waiter = threadIdx.x < 64;
+    if (more) nxt = tile_ctx(P, next);
+    if (more && !waiter) tile_load(P, nxt, nv);
+    if (threadIdx.x == 0) {
+        bool ok = true;
+        tile_wait_flags(P, cur.it, cur.layer, cur.order, [&](int64_t f) { ok = ok && wait_flag(P.flags + f); });
+        if (!ok && P.status) atomicOr(P.status, int(LEYLINE_STATUS_TILE_TIMEOUT));
+        words[1] = ok ? 1 : 0;
+    }
+    // the next tile's cos/sin (at most 64 pairs per plane, so the first wavefront fetches them)
+    const int32_t n_cs = more && nxt.cs >= 0 ? P.planes[nxt.plane].n_pairs : 0;
+    CsReg c{};
+    if (waiter) {
+        c = cs_fetch(P.cs, nxt.cs, n_cs);
+        if (more) tile_load(P, nxt, nv);
+    }
+    __syncthreads();
+    if (words[1]) tile_store<ESZ, ROT>(P, cur, v, lcs);   // a wait given up: store nothing
+    if (n_cs > 64) {                        // wider bands: the rest of the entries, plainly
+        if (!waiter) c = cs_fetch(P.cs, nxt.cs, n_cs);
+    }
+    cs_commit(nlcs, c, n_cs);
+    return more ? next : P.n_tickets;
+}
+
 template <int ESZ, int ROT>
 __global__ __launch_bounds__(KTILE_TPB) void contig_tile_kernel(const KTileParams P) {
-    __shared__ KCosSin lcs[KMAX_CS];
-    __shared__ int32_t s_ticket;
-    if (threadIdx.x == 0) s_ticket = atomicAdd(P.counter, 1);
+    __shared__ KCosSin lcs[2][KMAX_CS];
+    __shared__ int32_t words[2];
+    if (threadIdx.x == 0) words[0] = atomicAdd(P.counter, 1);
     __syncthreads();
-    const int32_t ticket = s_ticket;
+    int32_t ticket = words[0];
     if (ticket >= P.n_tickets) return;                            // block-uniform
-    const int32_t it = tile_item_of(P, ticket);
-    // the item as a value: its fields come in one level of independent scalar loads
-    KTileItem I;
-    __builtin_memcpy(&I, &P.items[it], sizeof(KTileItem));
-    const KPlane& pl = P.planes[I.plane];
-    const bool move = I.kind == KJOB_TILE;
-    const int32_t local = ticket - I.ticket0;
-    const int32_t layer = local / I.n_tiles, order = local - layer * I.n_tiles;
-    const int32_t q = I.delta <= 0 ? order : I.n_tiles - 1 - order;
-    const int32_t total = int32_t(I.count) * pl.tpr;
-    char* lbase = pl.base + int64_t(layer) * pl.layer_stride;
-    const char* src = move ? lbase + I.src0 * pl.token_stride : I.stub + int64_t(layer) * I.count * pl.row_bytes;
-    const int64_t src_step = move ? pl.token_stride : pl.row_bytes;
-    // Every slot loads (past the end of the range: the range's last chunk, which stays unused),
-    // so that all loads are issued back to back without branches between them.  Row and column
-    // are recomputed at store time rather than kept in registers.
-    const int32_t g0 = q * KTILE_CHUNKS + int32_t(threadIdx.x);
-    u32x4 v[KTILE_CPT];
-#pragma unroll
-    for (int i = 0; i < KTILE_CPT; ++i) {
-        const int32_t gc = min(g0 + i * KTILE_TPB, total - 1);
-        const int32_t r = fdiv(gc, pl.tpr_div);
-        v[i] = ld16(src + int64_t(r) * src_step + int64_t(gc - r * pl.tpr) * 16);
-    }
-    if (I.cs >= 0) stage_cs<KTILE_TPB>(lcs, P.cs, I.cs, pl.n_pairs);
-    __builtin_amdgcn_s_waitcnt(0);          // this thread's loads have returned
-    __syncthreads();                        // ... and every thread's
-    if (threadIdx.x == 0) {
-        if (move)
-            __hip_atomic_store(P.flags + I.flag0 + local, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        bool ok = true;
-        tile_wait_flags(P, it, layer, order, [&](int64_t f) { ok = ok && wait_flag(P.flags + f); });
-        if (!ok && P.status) atomicOr(P.status, int(LEYLINE_STATUS_TILE_TIMEOUT));
-        s_ticket = ok ? 1 : 0;              // the ticket was read above; the word now says "store"
-    }
-    __syncthreads();
-    if (!s_ticket) return;                  // a wait was given up: store nothing (block-uniform)
-    char* dst = lbase + I.dst0 * pl.token_stride;
-#pragma unroll
-    for (int i = 0; i < KTILE_CPT; ++i) {
-        const int32_t g = g0 + i * KTILE_TPB;
-        if (g < total) {
-            const int32_t r = fdiv(g, pl.tpr_div), u = g - r * pl.tpr;
-            if (I.cs >= 0) rotate_chunk<ESZ, ROT>(pl, v[i], u, lcs, 0);
-            st16(dst + int64_t(r) * pl.token_stride + int64_t(u) * 16, v[i]);
-        }
+    TileCtx a = tile_ctx(P, ticket), b = a;
+    u32x4 va[KTILE_CPT], vb[KTILE_CPT];
+    tile_load(P, a, va);
+    if (a.cs >= 0) stage_cs<KTILE_TPB>(lcs[0], P.cs, a.cs, P.planes[a.plane].n_pairs);
+    // two steps per iteration, so that the register buffers alternate without copies
+    for (;;) {
+        ticket = tile_step<ESZ, ROT>(P, a, va, lcs[0], b, vb, lcs[1], words);
+        if (ticket >= P.n_tickets) return;
+        ticket = tile_step<ESZ, ROT>(P, b, vb, lcs[1], a, va, lcs[0], words);
+        if (ticket >= P.n_tickets) return;
     }
 }
 
@@ -1169,6 +1251,27 @@ static int contig_launch_count(const leyline_cache* cache, const ContigSchedule&
     return n;
 }
 
+// Workgroups of a tile launch: persistent workgroups take tickets until they run out, so the grid
+// is the number that can be resident on the device at once (queried once per kernel variant and
+// device); more would only start once the tickets are gone.
+static int64_t tile_grid_cap(void (*kernel)(KTileParams)) {
+    static std::mutex mu;
+    static std::vector<std::pair<std::pair<void*, int>, int64_t>> known;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return INT32_MAX;
+    std::lock_guard<std::mutex> lock(mu);
+    for (const auto& k : known)
+        if (k.first.first == reinterpret_cast<void*>(kernel) && k.first.second == dev) return k.second;
+    int cus = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, KTILE_TPB, 0) != hipSuccess ||
+        cus <= 0 || per_cu <= 0)
+        return INT32_MAX;
+    const int64_t cap = int64_t(cus) * per_cu;
+    known.push_back({{reinterpret_cast<void*>(kernel), dev}, cap});
+    return cap;
+}
+
 // The prep launches and ordered-tile launches of a tile schedule.
 static int launch_tiles(const leyline_cache* cache, const ContigSchedule& sched, const KPlane* planes,
                         int n_planes, char* ws, int32_t* status, hipStream_t s) {
@@ -1205,21 +1308,13 @@ static int launch_tiles(const leyline_cache* cache, const ContigSchedule& sched,
         P.flags = reinterpret_cast<int32_t*>(ws + sched.ws_flags);
         P.cs = reinterpret_cast<const KCosSin*>(ws + sched.ws_cs);
         P.status = status;
-        const dim3 grid(static_cast<unsigned>(tl.tickets), 1, 1);
-        int r;
-        switch (launch_rot_style(P)) {
-        case KROT_INTERLEAVED:
-            r = bf ? launch(contig_tile_kernel<2, KROT_INTERLEAVED>, grid, s, P, KTILE_TPB)
-                   : launch(contig_tile_kernel<4, KROT_INTERLEAVED>, grid, s, P, KTILE_TPB);
-            break;
-        case KROT_NEOX:
-            r = bf ? launch(contig_tile_kernel<2, KROT_NEOX>, grid, s, P, KTILE_TPB)
-                   : launch(contig_tile_kernel<4, KROT_NEOX>, grid, s, P, KTILE_TPB);
-            break;
-        default:
-            r = bf ? launch(contig_tile_kernel<2, KROT_NONE>, grid, s, P, KTILE_TPB)
-                   : launch(contig_tile_kernel<4, KROT_NONE>, grid, s, P, KTILE_TPB);
-        }
+        using K = void (*)(KTileParams);
+        static const K kernels[2][3] = {
+            {contig_tile_kernel<4, KROT_NONE>, contig_tile_kernel<4, KROT_INTERLEAVED>, contig_tile_kernel<4, KROT_NEOX>},
+            {contig_tile_kernel<2, KROT_NONE>, contig_tile_kernel<2, KROT_INTERLEAVED>, contig_tile_kernel<2, KROT_NEOX>}};
+        const K kernel = kernels[bf][launch_rot_style(P)];
+        const dim3 grid(static_cast<unsigned>(std::min<int64_t>(tl.tickets, tile_grid_cap(kernel))), 1, 1);
+        const int r = launch(kernel, grid, s, P, KTILE_TPB);
         if (r) return r;
     }
     return LEYLINE_OK;

@@ -17,7 +17,7 @@
 // ticket: a planted schedule fault); then the give-up path must let every workgroup exit and
 // raise the status bit whenever the fault blocked the launch.
 //
-// Usage: tile_schedule_sim SEED CASES [PLANT]
+// Usage: tile_schedule_sim SEED CASES [PLANT [PERSIST]]
 //        (prints "ok <tile cases> <tiles stored> <waits given up>" on success)
 #include <algorithm>
 #include <cstdio>
@@ -68,6 +68,8 @@ int main(int argc, char** argv) {
     const unsigned seed = argc > 1 ? unsigned(std::atoi(argv[1])) : 1u;
     const int cases = argc > 2 ? std::atoi(argv[2]) : 100;
     const bool plant = argc > 3 && std::atoi(argv[3]) != 0;
+    // PERSIST: 0 one tile per workgroup, 1 persistent workgroups, 2 either, drawn per launch
+    const int persist_mode = argc > 4 ? std::atoi(argv[4]) : 2;
     int64_t gave_up = 0;
     std::mt19937_64 rng(seed);
     auto uni = [&](int64_t lo, int64_t hi) { return std::uniform_int_distribution<int64_t>(lo, hi)(rng); };
@@ -181,6 +183,7 @@ int main(int argc, char** argv) {
                 *g0 = q * KTILE_CHUNKS;
                 *g1 = std::min(total, *g0 + KTILE_CHUNKS);
             };
+            const bool persist = persist_mode == 1 || (persist_mode == 2 && uni(0, 1) == 1);
             std::vector<std::vector<int64_t>> buf(size_t(tl.tickets));
             std::vector<int> state(size_t(tl.tickets), 0);        // 0 taken, 1 loaded, 2 stored
             const int64_t W = std::vector<int64_t>{1, 2, 3, 8, 64, int64_t(1) << 40}[size_t(uni(0, 5))];
@@ -212,6 +215,145 @@ int main(int argc, char** argv) {
                 if (t == victim && !flags[size_t(planted)]) ready = false;
                 return ready;
             };
+            // reads tile t's chunks into buf[t] (0, or 1: a load saw an overwritten row, 2: unknown
+            // replacement); publish(t) sets a move tile's "source read" flag; store_tile writes
+            auto load_tile = [&](int64_t t) -> int {
+                const Tile& T = tiles[size_t(t)];
+                const KTileItem& I = P.items[T.item];
+                const int p = I.plane;
+                const int64_t tpr = planes[p].tpr;
+                auto& m = mem[size_t(p * L + T.layer)];
+                int64_t g0, g1;
+                chunks(T, &g0, &g1);
+                auto& b = buf[size_t(t)];
+                b.resize(size_t(g1 - g0));
+                for (int64_t g = g0; g < g1; ++g) {
+                    const int64_t r = g / tpr, c = g % tpr;
+                    if (I.kind == KJOB_TILE) {
+                        const int64_t v = m[size_t((I.src0 + r) * tpr + c)];
+                        if (v != orig_val(p, T.layer, I.src0 + r, c)) return 1;
+                        b[size_t(g - g0)] = v;
+                    } else {
+                        int j = -1;
+                        for (int jj = 0; jj < k; ++jj)
+                            if (dirs[size_t(jj)].stub[p] == I.stub) j = jj;
+                        if (j < 0) return 2;
+                        b[size_t(g - g0)] = stub_val(j, p, T.layer, r, c);
+                    }
+                }
+                return 0;
+            };
+            auto publish = [&](int64_t t) {
+                const Tile& T = tiles[size_t(t)];
+                const KTileItem& I = P.items[T.item];
+                if (I.kind == KJOB_TILE) flags[size_t(I.flag0 + int64_t(T.layer) * I.n_tiles + T.order)] = 1;
+            };
+            auto store_tile = [&](int64_t t) {
+                const Tile& T = tiles[size_t(t)];
+                const KTileItem& I = P.items[T.item];
+                const int p = I.plane;
+                const int64_t tpr = planes[p].tpr;
+                auto& m = mem[size_t(p * L + T.layer)];
+                int64_t g0, g1;
+                chunks(T, &g0, &g1);
+                const auto& b = buf[size_t(t)];
+                for (int64_t g = g0; g < g1; ++g) {
+                    const int64_t r = g / tpr, c = g % tpr;
+                    m[size_t((I.dst0 + r) * tpr + c)] = b[size_t(g - g0)];
+                }
+                ++tiles_run;
+            };
+            auto load_fail = [&](int rc) {
+                return fail(rc == 1 ? "a load saw an overwritten row" : "unknown replacement", ci);
+            };
+            if (persist) {
+                // G persistent workgroups (the kernel's LEYLINE_TILE_PERSIST design): each takes a
+                // ticket, loads it, then repeatedly publishes its current tile and takes the next
+                // ticket, loads the next tile (the load may complete before or after the store
+                // below), waits for the current tile's flags and stores it
+                struct Wg { int phase; int64_t cur, nxt; bool nxt_loaded; };
+                const int64_t G = std::vector<int64_t>{1, 2, 3, 8, 64}[size_t(uni(0, 4))];
+                std::vector<Wg> wgs(size_t(G), Wg{0, -1, -1, false});
+                size_t done = 0;
+                while (done < wgs.size()) {
+                    // enabled actions: (workgroup, kind) with kind 0 take first ticket, 1 load the
+                    // current tile, 2 publish + take next, 3 load the next tile, 4 store current
+                    std::vector<std::pair<size_t, int>> acts;
+                    for (size_t w = 0; w < wgs.size(); ++w) {
+                        const Wg& g = wgs[w];
+                        if (g.phase == 0) acts.emplace_back(w, 0);
+                        else if (g.phase == 1) acts.emplace_back(w, 1);
+                        else if (g.phase == 2) acts.emplace_back(w, 2);
+                        else if (g.phase == 3 || g.phase == 4) {
+                            if (g.nxt >= 0 && !g.nxt_loaded) acts.emplace_back(w, 3);
+                            if (g.phase == 3) {
+                                bool bad = false;
+                                const bool ready = ready_to_store(g.cur, &bad);
+                                if (bad) return fail("a wait names a flag outside the launch or of a later ticket", ci);
+                                if (ready) acts.emplace_back(w, 4);
+                            }
+                        }
+                    }
+                    // a workgroup whose current tile is stored (or given up) moves on once its next
+                    // tile is loaded, or exits when there is none
+                    auto move_on = [&](Wg& g) {
+                        if (g.phase == 4 && (g.nxt < 0 || g.nxt_loaded)) {
+                            if (g.nxt < 0) { g.phase = 5; ++done; }
+                            else { g.cur = g.nxt; g.nxt = -1; g.phase = 2; }
+                        }
+                    };
+                    if (acts.empty()) {
+                        if (!plant) return fail("persistent schedule stalled", ci);
+                        // every workgroup is blocked in its wait: each gives up (bounded wait),
+                        // stores nothing and goes on
+                        int blocked = 0;
+                        for (Wg& g : wgs) {
+                            if (g.phase != 3) continue;
+                            ++blocked;
+                            bool bad = false;
+                            int64_t polls = 0;
+                            const bool ok = tile_wait_bounded([&] { return ready_to_store(g.cur, &bad); },
+                                                              [&] { ++polls; }, KTILE_SPIN_LIMIT);
+                            if (ok || polls != KTILE_SPIN_LIMIT) return fail("bounded wait", ci);
+                            status |= LEYLINE_STATUS_TILE_TIMEOUT;
+                            ++gave_up;
+                            g.phase = 4;
+                            move_on(g);
+                        }
+                        if (!blocked) return fail("persistent workgroups blocked outside their wait", ci);
+                        continue;
+                    }
+                    const auto a = acts[size_t(uni(0, int64_t(acts.size()) - 1))];
+                    Wg& g = wgs[a.first];
+                    switch (a.second) {
+                    case 0:
+                        if (next >= tl.tickets) { g.phase = 5; ++done; break; }
+                        g.cur = next++;
+                        g.phase = 1;
+                        break;
+                    case 1:
+                        if (int rc = load_tile(g.cur)) return load_fail(rc);
+                        g.phase = 2;
+                        break;
+                    case 2:
+                        publish(g.cur);
+                        g.nxt = next < tl.tickets ? next++ : -1;
+                        g.nxt_loaded = false;
+                        g.phase = 3;
+                        break;
+                    case 3:
+                        if (int rc = load_tile(g.nxt)) return load_fail(rc);
+                        g.nxt_loaded = true;
+                        break;
+                    case 4:
+                        store_tile(g.cur);
+                        g.phase = 4;
+                        break;
+                    }
+                    move_on(g);
+                }
+                continue;
+            }
             while (next < tl.tickets || !live.empty()) {
                 // possible actions: take the next ticket, load a taken tile, store a loaded one
                 std::vector<std::pair<int, int64_t>> acts;
@@ -251,41 +393,14 @@ int main(int argc, char** argv) {
                     ++next;
                     continue;
                 }
-                const Tile& T = tiles[size_t(t)];
-                const KTileItem& I = P.items[T.item];
-                const int p = I.plane;
-                const int64_t tpr = planes[p].tpr;
-                auto& m = mem[size_t(p * L + T.layer)];
-                int64_t g0, g1;
-                chunks(T, &g0, &g1);
                 if (a.first == 1) {
-                    auto& b = buf[size_t(t)];
-                    b.resize(size_t(g1 - g0));
-                    for (int64_t g = g0; g < g1; ++g) {
-                        const int64_t r = g / tpr, c = g % tpr;
-                        if (I.kind == KJOB_TILE) {
-                            const int64_t v = m[size_t((I.src0 + r) * tpr + c)];
-                            if (v != orig_val(p, T.layer, I.src0 + r, c)) return fail("a load saw an overwritten row", ci);
-                            b[size_t(g - g0)] = v;
-                        } else {
-                            int j = -1;
-                            for (int jj = 0; jj < k; ++jj)
-                                if (dirs[size_t(jj)].stub[p] == I.stub) j = jj;
-                            if (j < 0) return fail("unknown replacement", ci);
-                            b[size_t(g - g0)] = stub_val(j, p, T.layer, r, c);
-                        }
-                    }
-                    if (I.kind == KJOB_TILE) flags[size_t(I.flag0 + int64_t(T.layer) * I.n_tiles + T.order)] = 1;
+                    if (int rc = load_tile(t)) return load_fail(rc);
+                    publish(t);
                     state[size_t(t)] = 1;
                 } else {
-                    const auto& b = buf[size_t(t)];
-                    for (int64_t g = g0; g < g1; ++g) {
-                        const int64_t r = g / tpr, c = g % tpr;
-                        m[size_t((I.dst0 + r) * tpr + c)] = b[size_t(g - g0)];
-                    }
+                    store_tile(t);
                     state[size_t(t)] = 2;
                     live.erase(std::find(live.begin(), live.end(), t));
-                    ++tiles_run;
                 }
             }
         }

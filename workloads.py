@@ -18,6 +18,7 @@ Workloads (MLA rows: latent c_kv[512] + K_pe[64]; GQA rows: 8 KV heads x 128):
   mla_dsv3_paged_131k 61 layers, 64-token pages, one 131072-token sequence, 8 non-overlapping
                       directives (spans U[256,8192], stubs U[0,64])
   mla_dsv3_32k_edits8 the 32K MLA cache with 8 seeded edits (spans U[8,200], stubs U[0,2*span])
+  mla_dsv3_32k_shift1 the 32K MLA cache with one token deleted (every downstream row moves by one)
   mla_dsv3_slots_32k, gqa_llama3_8b_slots_16k
                       the 32K MLA and 16K GQA splices on token-slot caches (page size 1)
   mla_dsv3_slots_cow_32k
@@ -156,6 +157,15 @@ def mla_dsv3_32k_edits8(seed: int = 6) -> Workload:
                     seed=seed)
 
 
+def mla_dsv3_32k_shift1() -> Workload:
+    """The 32K MLA contiguous cache with one token deleted at the headline's seeded start and no
+    replacement: every downstream row moves by one row, the smallest shift (ordered tiles)."""
+    w = mla_dsv3_32k()
+    s = w.dirs[0].span_start
+    return Workload("mla_dsv3_32k_shift1", w.n_layers, w.dtype, w.planes, [Dir(s, s + 1, 0)], w.seq_lens,
+                    capacity=w.capacity, seed=w.seed)
+
+
 def mla_dsv3_slots_32k() -> Workload:
     """The 32K MLA splice on a token-slot cache (page size 1, slots scattered over the pool): the
     downstream tokens keep their slots, only their K_pe bands are rotated in place."""
@@ -205,6 +215,7 @@ WORKLOADS = {
     "gqa_llama3_8b_16k": gqa_llama3_8b_16k,
     "mla_dsv3_paged_131k": mla_dsv3_paged_131k,
     "mla_dsv3_32k_edits8": mla_dsv3_32k_edits8,
+    "mla_dsv3_32k_shift1": mla_dsv3_32k_shift1,
     "mla_dsv3_slots_32k": mla_dsv3_slots_32k,
     "gqa_llama3_8b_slots_16k": gqa_llama3_8b_slots_16k,
     "mla_dsv3_slots_cow_32k": mla_dsv3_slots_cow_32k,
