@@ -56,6 +56,8 @@ def parse():
     ap.add_argument("--also", default="gqa_llama3_8b_16k,mla_dsv3_paged_131k,mla_dsv3_32k:exact,gqa_llama3_8b_16k:exact",
                     help="further workloads timed in the same run and reported under \"also\" "
                          "(comma-separated; NAME:exact runs libleyline_exact.so; empty: none)")
+    ap.add_argument("--exact", action="store_true",
+                    help="run the workload on libleyline_exact.so (fp64 pair arithmetic) instead of libleyline.so")
     ap.add_argument("--cpu-procs", type=int, default=0,
                     help="processes of the all-cores oracle leg (0: every CPU this process may use, at most 16)")
     ap.add_argument("--cpu-leg", nargs=4, metavar=("DATA", "SECONDS", "PROCS", "OUT"),
@@ -77,10 +79,15 @@ def kernel_sha():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload):
+def profile_key(workload, exact=False):
+    """Name under which a workload's profiles are kept (the exact library's get a suffix)."""
+    return workload + ("_exact" if exact else "")
+
+
+def measured_traffic(workload, exact=False):
     """HBM bytes per splice from committed rocprofv3 counter runs, if they were taken on the
     current kernel source (else None)."""
-    path = os.path.join(PROFILES, f"traffic_{workload}.json")
+    path = os.path.join(PROFILES, f"traffic_{profile_key(workload, exact)}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -210,12 +217,12 @@ def timed(step, steps, warmup, stream):
     return t_begin.elapsed_time(t_end) / steps
 
 
-def roofline_of(wl, kernel, alg_bytes, launches, splice_ms):
+def roofline_of(wl, kernel, alg_bytes, launches, splice_ms, exact=False):
     """The dominant kernel against the HBM peak: algorithmic bytes per launch over the average
     launch duration (the event-timed splice divided by its launches of that kernel), with the
     committed counter traffic when it was taken on the current kernel sources."""
     achieved = alg_bytes / (splice_ms * 1e-3) / 1e9
-    rec = measured_traffic(wl.name)
+    rec = measured_traffic(wl.name, exact)
     traffic = rec["dispatch_bytes"] if rec and rec.get("kernel") == kernel else None
     return achieved, traffic, rec
 
@@ -238,7 +245,7 @@ def measure_also(spec, args, dev, L, W, stream):
     finally:
         L.use_library(False)
     torch.cuda.empty_cache()
-    achieved, traffic, _ = roofline_of(wl, kernel, alg_bytes, launches, ms)
+    achieved, traffic, _ = roofline_of(wl, kernel, alg_bytes, launches, ms, exact)
     return {
         "workload": wl.name,
         "pair_bits": pair_bits,
@@ -251,7 +258,7 @@ def measure_also(spec, args, dev, L, W, stream):
         "avg_launch_ms": ms / max(1, launches),
         "achieved_GBps": achieved,
         "frac": achieved / PEAK_HBM_GBPS,
-        "traffic": None if exact else traffic,
+        "traffic": traffic,
         "algorithmic_bytes_per_splice": alg_bytes,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -279,11 +286,12 @@ def main():
     dev = "cuda:0"
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
+    L.use_library(args.exact)
     step, kernel, alg_bytes, moved, launches, keep, layout = setup_workload(wl, dev, L, W, args, stream)
 
     ms_per_step = timed(step, args.steps, args.warmup, stream)
     splice_ms = ms_per_step
-    achieved, traffic, rec = roofline_of(wl, kernel, alg_bytes, launches, splice_ms)
+    achieved, traffic, rec = roofline_of(wl, kernel, alg_bytes, launches, splice_ms, args.exact)
     # Spread of single splices, from a separate untimed pass with an event pair around each.
     n_spread = min(args.steps, 20)
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(n_spread)]
@@ -344,7 +352,9 @@ def main():
     del step
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
-    also = [a for a in args.also.split(",") if a and a != wl.name]      # NAME:exact is kept
+    L.use_library(False)
+    this = profile_key(wl.name, args.exact).replace("_exact", ":exact")
+    also = [a for a in args.also.split(",") if a and a != this]
     if also:
         out["also"] = [measure_also(a, args, dev, L, W, stream) for a in also]
     if not args.no_cpu_baseline:
@@ -693,10 +703,11 @@ def summarize(args):
                    total_bytes=fetch_b + write_b, calibration=[cal_f, cal_w], per="splice",
                    algorithmic_bytes=alg)
     os.makedirs(PROFILES, exist_ok=True)
-    with open(os.path.join(PROFILES, f"{kernel}_{wl.name}.md"), "w") as f:
+    key = profile_key(wl.name, "--exact" in args.command.split())
+    with open(os.path.join(PROFILES, f"{kernel}_{key}.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     if rec:
-        with open(os.path.join(PROFILES, f"traffic_{wl.name}.json"), "w") as f:
+        with open(os.path.join(PROFILES, f"traffic_{key}.json"), "w") as f:
             json.dump(rec, f, indent=1)
     print("\n".join(lines))
 
