@@ -289,6 +289,8 @@ int leyline_paged_plan(int32_t page_size, int32_t n_seqs, const int32_t* seq_len
  * bytes travel in the kernel arguments instead, larger ones are uploaded with an asynchronous
  * copy on `stream`) and, when the call assembles more than 1024 rows, the row table a kernel of
  * this call writes from it (24 bytes per row of every ASSEMBLE page, 4 bytes per fresh page);
+ * when some plane rotates at least 1 KiB per row and at least 64 pages are re-used, the REMAP
+ * pages resolved and sorted by physical page (16 bytes per REMAP page);
  * reuse it only after the stream has passed this call.  Any page_size whose rows keep the
  * 16-byte alignment is accepted.  A call with a plan of at most 2560 bytes enqueues kernels only
  * (and, assembling at most 1024 rows, a single one); an uploaded plan comes from host memory the

@@ -954,6 +954,80 @@ __global__ __launch_bounds__(ORDER_TPB) void paged_order_kernel(const KPagedPara
     for (int32_t t = tid; t < P.n_asm; t += ORDER_TPB) P.order[atomicAdd(&cnt[bucket(t)], 1)] = t;
 }
 
+// REMAP page m of the call (in plan order), resolved: its physical page, shift and valid rows.
+__device__ __forceinline__ KRemapPage remap_resolve(const KPagedParams& P, const PlanView& V, int32_t m) {
+    if (P.n_remap_runs == 1) return remap_entry(P, P.remap0, P.remap0_cs, P.remap0_len, m);
+    const KPageRun R = V.remap_runs[run_of(V.remap_runs, P.n_remap_runs, m)];
+    return remap_entry(P, R, V.dirs[R.dir].cs, V.seqs[R.seq].new_len, m);
+}
+
+// Lays the call's REMAP pages out in physical-page order, resolved (buckets of 2^remap_shift
+// pages; one workgroup: a histogram in LDS, an exclusive scan, a scatter), so that the rotating
+// workgroups that run together touch neighbouring pages.  A page outside the pool (flagged, no
+// rows to rotate) counts in bucket 0.  Up to ORDER_TPB * REMAP_SORT_PER pages are resolved once,
+// all loads of a thread in flight together, and kept in registers for the scatter; larger calls
+// sweep twice.
+constexpr int REMAP_SORT_PER = 16;
+
+__global__ __launch_bounds__(ORDER_TPB) void paged_remap_order_kernel(const KPagedParams P) {
+    __shared__ int32_t cnt[KORDER_BUCKETS];
+    __shared__ int32_t part[ORDER_TPB];
+    const PlanView V = plan_view(P);
+    const int tid = int(threadIdx.x);
+    const bool held = P.n_remap <= ORDER_TPB * REMAP_SORT_PER;     // block-uniform
+    for (int i = tid; i < KORDER_BUCKETS; i += ORDER_TPB) cnt[i] = 0;
+    KRemapPage e[REMAP_SORT_PER];
+    if (held) {
+#pragma unroll
+        for (int k = 0; k < REMAP_SORT_PER; ++k) {
+            const int32_t m = tid + k * ORDER_TPB;
+            e[k] = m < P.n_remap ? remap_resolve(P, V, m) : KRemapPage{0, -1, 0, 0};
+        }
+    }
+    __syncthreads();
+    if (held) {
+#pragma unroll
+        for (int k = 0; k < REMAP_SORT_PER; ++k)
+            if (tid + k * ORDER_TPB < P.n_remap) atomicAdd(&cnt[e[k].page >> P.remap_shift], 1);
+    } else {
+        for (int32_t m = tid; m < P.n_remap; m += ORDER_TPB)
+            atomicAdd(&cnt[remap_resolve(P, V, m).page >> P.remap_shift], 1);
+    }
+    __syncthreads();
+    constexpr int PER = KORDER_BUCKETS / ORDER_TPB;
+    int32_t own[PER], sum = 0;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        own[k] = cnt[tid * PER + k];
+        sum += own[k];
+    }
+    part[tid] = sum;
+    __syncthreads();
+    for (int off = 1; off < ORDER_TPB; off <<= 1) {
+        const int32_t v = tid >= off ? part[tid - off] : 0;
+        __syncthreads();
+        part[tid] += v;
+        __syncthreads();
+    }
+    int32_t run = part[tid] - sum;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        cnt[tid * PER + k] = run;
+        run += own[k];
+    }
+    __syncthreads();
+    if (held) {
+#pragma unroll
+        for (int k = 0; k < REMAP_SORT_PER; ++k)
+            if (tid + k * ORDER_TPB < P.n_remap) P.remap_sorted[atomicAdd(&cnt[e[k].page >> P.remap_shift], 1)] = e[k];
+    } else {
+        for (int32_t m = tid; m < P.n_remap; m += ORDER_TPB) {
+            const KRemapPage x = remap_resolve(P, V, m);
+            P.remap_sorted[atomicAdd(&cnt[x.page >> P.remap_shift], 1)] = x;
+        }
+    }
+}
+
 // ASSEMBLE row i (row i mod page_size of the (i / page_size)-th fresh page in destination order
 // when P.order is set, else in plan order): where it comes from, where it goes, its shift.
 __device__ __forceinline__ KRowMove row_entry(const KPagedParams& P, const PlanView& V, int32_t i) {
@@ -1097,10 +1171,13 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const P
     const int32_t t = tb + int32_t(threadIdx.x);
     const int32_t m = fdiv(t, P.remap_div[plane]);
     // the run of the block's first page (block-uniform; a single run comes with the parameters);
-    // a lane whose page lies past that run looks its own run up
+    // a lane whose page lies past that run looks its own run up.  With the pages in physical
+    // order, each lane reads its resolved page instead.
     KPageRun R0 = P.remap0;
     int32_t next0 = INT32_MAX, cs0 = P.remap0_cs, len0 = P.remap0_len;
-    if (P.n_remap_runs > 1) {
+    if (P.remap_sorted) {
+        cs0 = P.remap_sorted[fdiv(tb, P.remap_div[plane])].cs;
+    } else if (P.n_remap_runs > 1) {
         const int32_t r0 = run_of(V.remap_runs, P.n_remap_runs, fdiv(tb, P.remap_div[plane]));
         R0 = V.remap_runs[r0];
         next0 = r0 + 1 < P.n_remap_runs ? V.remap_runs[r0 + 1].ord0 : INT32_MAX;
@@ -1111,7 +1188,9 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const P
     bool active = m < P.n_remap;
     KRemapPage e{0, -1, 0, 0};
     if (active) {
-        if (m < next0) {
+        if (P.remap_sorted) {
+            e = P.remap_sorted[m];
+        } else if (m < next0) {
             e = remap_entry(P, R0, cs0, len0, m);
         } else {
             const KPageRun R = V.remap_runs[run_of(V.remap_runs, P.n_remap_runs, m)];
@@ -1690,6 +1769,15 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
         } else {
             // the first data launch writes the tables, spread over its layer groups
             P.table_x = int32_t(((n_tables + PAGED_TPB - 1) / PAGED_TPB + layer_groups - 1) / layer_groups);
+        }
+        if (t.remap_sorted) {
+            // wide rotary bands: the REMAP pages in physical order
+            int32_t shift = 0;
+            while (((cache->capacity - 1) >> shift) >= KORDER_BUCKETS) ++shift;
+            P.remap_shift = shift;
+            P.remap_sorted = reinterpret_cast<KRemapPage*>(ws + t.off_remap_sorted);
+            rc = launch(paged_remap_order_kernel, dim3(1), s, P, ORDER_TPB);
+            if (rc) return rc;
         }
         // data kernel, one launch: gather workgroups, then the REMAP workgroups of every rotary
         // plane, then (small gathers) the table work

@@ -341,12 +341,13 @@ struct KRemapPage {
 // Byte offsets of the tables inside the workspace (converted to pointers at launch).
 struct KPagedTables {
     int64_t off_seq, off_dir, off_cs, off_runs, off_asm_runs, off_remap_runs, off_freed_runs;
-    int64_t off_rows, off_order;
+    int64_t off_rows, off_order, off_remap_sorted;
     int64_t upload;          // bytes uploaded from the host (the tables before the row tables)
     int64_t total;           // workspace bytes (the row table is written on the device)
     int32_t n_seqs, n_dirs, n_cs, n_runs, n_asm_runs, n_remap_runs, n_freed_runs;
     int32_t n_asm, n_remap, n_freed, bt_stride;
     int32_t n_rows;          // n_asm * page_size
+    int32_t remap_sorted;    // 1: the REMAP pages are laid out in physical order at off_remap_sorted
 };
 
 // Plans of at most this many bytes travel in the kernel arguments instead of being uploaded.
@@ -389,6 +390,10 @@ struct KPagedParams {
                                                  // from 0 after the gather's
     int32_t pad1;
     int32_t* order;          // workspace, n_asm fresh ordinals in destination-page order (or null)
+    KRemapPage* remap_sorted;   // workspace, the REMAP pages resolved and in physical-page order
+                                // (or null: the rotating workgroups resolve them in plan order)
+    int32_t remap_shift;     // its bucket = physical page >> remap_shift
+    int32_t pad2;
     // the only REMAP run when n_remap_runs == 1, with its shift's cos/sin entry and its sequence's
     // new length (read with the other parameters, one level of loads before the block table)
     KPageRun remap0;
@@ -404,6 +409,12 @@ constexpr int32_t KINLINE_ROWS = 1024;
 // when a call assembles at least this many pages; KORDER_BUCKETS buckets of pages, counted in LDS.
 constexpr int32_t KORDER_MIN = 64;
 constexpr int32_t KORDER_BUCKETS = 4096;
+
+// The REMAP rotation runs in physical-page order (resolved and bucket-sorted by a first kernel)
+// when a call re-uses at least KORDER_MIN pages and some plane rotates at least this many bytes
+// per row (whole GQA K heads: neighbouring rows then share DRAM pages; narrow MLA bands gain
+// nothing from it).
+constexpr int32_t KREMAP_SORT_BYTES = 1024;
 
 
 }  // namespace leyline

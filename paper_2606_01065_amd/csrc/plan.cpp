@@ -644,6 +644,13 @@ int build_paged_image(const leyline_cache* cache, const PagedPlan& plan, int32_t
     const bool row_table = n_rows > KINLINE_ROWS;
     t.off_rows = place(row_table ? size_t(n_rows) * sizeof(KRowMove) : 0, 256);
     t.off_order = place(row_table && plan.n_fresh >= KORDER_MIN ? size_t(plan.n_fresh) * sizeof(int32_t) : 0, 256);
+    // the REMAP pages in physical order, when some plane rotates wide bands
+    int64_t rot_row_bytes = 0;
+    for (int p = 0; p < cache->n_planes; ++p)
+        rot_row_bytes = std::max<int64_t>(rot_row_bytes, int64_t(cache->planes[p].n_heads) *
+                                                             cache->planes[p].rot_dim * elem_size(cache->dtype));
+    const bool remap_sorted = plan.n_remap >= KORDER_MIN && rot_row_bytes >= KREMAP_SORT_BYTES;
+    t.off_remap_sorted = place(remap_sorted ? size_t(plan.n_remap) * sizeof(KRemapPage) : 0, 256);
     t.total = (off + 255) / 256 * 256;
     t.n_seqs = n_seqs; t.n_dirs = n_dirs; t.n_cs = int32_t(cs.size());
     t.n_runs = int32_t(plan.runs.size());
@@ -653,6 +660,7 @@ int build_paged_image(const leyline_cache* cache, const PagedPlan& plan, int32_t
     t.n_asm = plan.n_fresh; t.n_remap = plan.n_remap; t.n_freed = plan.n_freed;
     t.bt_stride = bt_stride;
     t.n_rows = int32_t(n_rows);
+    t.remap_sorted = remap_sorted ? 1 : 0;
     img->bytes.assign(size_t(t.upload), 0);
     auto put = [&](int64_t at, const void* src, size_t bytes) {
         if (bytes) std::memcpy(img->bytes.data() + at, src, bytes);

@@ -66,9 +66,9 @@ def test_contiguous_splice_is_bit_identical_to_the_oracle(L, name):
 
 
 @pytest.mark.parametrize("kind,dtype", [("mla", "bf16"), ("gqa", "bf16"), ("mla", "f32"), ("mla_neox", "bf16"),
-                                        ("four", "bf16")])
+                                        ("four", "bf16"), ("gqa8", "bf16")])
 def test_small_paged_pools_are_bit_identical_to_the_oracle(L, kind, dtype):
-    rng = random.Random({"mla": 801, "gqa": 802, "mla_neox": 803, "four": 804}[kind] + (dtype == "f32"))
+    rng = random.Random({"mla": 801, "gqa": 802, "mla_neox": 803, "four": 804, "gqa8": 805}[kind] + (dtype == "f32"))
     for page in (1, 16, 64):
         for ci in range(4):
             wl = _random_workload(rng, page, kind, dtype, max_len=900 if page == 1 else None)

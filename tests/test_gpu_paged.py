@@ -67,6 +67,8 @@ def _random_workload(rng, page, kind, dtype, max_len=None):
         planes = [W.mla_plane()]
     elif kind == "mla_neox":      # half-split band that straddles wavefront windows: two-chunk units
         planes = [W.PlaneDesc((576,), 1, 576, 512, 64, 1, 10000.0)]
+    elif kind == "gqa8":          # 2 KB rotated per row: re-used pages rotate in physical order
+        planes = W.gqa_planes(heads=8, dim=128)
     elif kind == "four":          # four planes, rotary bands of both access classes
         planes = [W.mla_plane(), W.PlaneDesc((2, 128), 2, 128, 0, 128, 1, 500000.0), W.PlaneDesc((256,)),
                   W.PlaneDesc((64,), 1, 64, 32, 32, 0, 10000.0)]
@@ -262,11 +264,13 @@ def test_inline_and_row_table_gathers(L, kind, last_stub):
 
 
 @pytest.mark.parametrize("kind,dtype", [("mla", "bf16"), ("gqa", "bf16"), ("mla", "f32"),
-                                        ("mla_neox", "bf16"), ("four", "bf16")])
+                                        ("mla_neox", "bf16"), ("four", "bf16"), ("gqa8", "bf16"),
+                                        ("gqa8", "f32")])
 def test_token_slot_paged_whole_pool(L, kind, dtype):
     """Page sizes 1 and 2 (token-slot caches) with sequences long enough that the in-place
-    rotation of remapped slots spans many workgroups and ends in a ragged one."""
-    rng = random.Random({"mla": 197, "gqa": 198, "mla_neox": 199, "four": 200}[kind] + (dtype == "f32"))
+    rotation of remapped slots spans many workgroups and ends in a ragged one.  With 8 GQA heads
+    (2 KB or more rotated per row) the re-used slots are first sorted by physical slot."""
+    rng = random.Random({"mla": 197, "gqa": 198, "mla_neox": 199, "four": 200, "gqa8": 201}[kind] + (dtype == "f32"))
     for page in (1, 2):
         for ci in range(3):
             wl = _random_workload(rng, page, kind, dtype, max_len=900)
