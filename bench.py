@@ -186,8 +186,8 @@ def setup_workload(wl, dev, L, W, args, stream):
                                         p.rot_dim, p.style, p.base) for p, t in zip(wl.planes, planes)]
     if wl.rotate:
         step, kernel, alg_bytes, moved, launches, keep = setup_rotate(wl, dev, L, W, specs, stream)
-        layout = (f"contiguous, rotary bands re-anchored in place (no movement), {ROTATE_REPLICAS} cache "
-                  "copies round-robin")
+        layout = (("token slots listed by physical slot" if wl.page_size else "contiguous")
+                  + f", rotary bands re-anchored in place (no movement), {ROTATE_REPLICAS} cache copies round-robin")
     elif wl.page_size:
         step, kernel, alg_bytes, moved, launches, keep = setup_paged(wl, dev, L, W, specs, stream)
         layout = (f"paged, {wl.page_size}-token pages, {len(wl.seq_lens)} sequences"
@@ -387,15 +387,28 @@ def setup_contig(wl, dev, L, W, specs, stream, args):
 
 def setup_rotate(wl, dev, L, W, specs, stream):
     import torch
-    base_planes, _ = W.alloc_contig(wl, dev)
-    replicas = [base_planes] + [[t.clone() for t in base_planes] for _ in range(1, ROTATE_REPLICAS)]
-    caches = [L.make_cache(specs(r)) for r in replicas]
     delta, row0, n = wl.rotate
+    if wl.page_size:
+        # a token-slot (paged) cache: the rows are the physical slots of logical rows
+        # [row0, row0 + n) of the sequence, listed
+        pools, bt, _, _ = W.alloc_paged(wl, dev)
+        replicas = [pools] + [[t.clone() for t in pools] for _ in range(1, ROTATE_REPLICAS)]
+        caches = [L.make_cache(specs(r), paged=True) for r in replicas]
+        idx = torch.arange(row0, row0 + n, device=dev)
+        rows = (bt[0].long()[idx // wl.page_size] * wl.page_size + idx % wl.page_size).contiguous()
+    else:
+        base_planes, _ = W.alloc_contig(wl, dev)
+        replicas = [base_planes] + [[t.clone() for t in base_planes] for _ in range(1, ROTATE_REPLICAS)]
+        caches = [L.make_cache(specs(r)) for r in replicas]
+        rows = None
     alg_bytes, moved = rotate_bytes(wl)
     launches = 1                                  # every rotary plane in one launch
 
     def step(i):
-        L.leyline_rotate_delta(caches[i % len(caches)], delta, row0=row0, n_rows=n, stream=stream)
+        if rows is None:
+            L.leyline_rotate_delta(caches[i % len(caches)], delta, row0=row0, n_rows=n, stream=stream)
+        else:
+            L.leyline_rotate_delta(caches[i % len(caches)], delta, rows=rows, stream=stream)
 
     torch.cuda.synchronize()
     return step, ROTATE_KERNEL, alg_bytes, moved, launches, dict(rotate=True)
@@ -624,7 +637,10 @@ def summarize(args):
     trace_dir, fetch_dir, write_dir = args.summarize
     import workloads as W
     wl = W.WORKLOADS[args.workload]()
-    if wl.page_size:
+    if wl.rotate:
+        alg, _ = rotate_bytes(wl)
+        kernel = ROTATE_KERNEL
+    elif wl.page_size:
         from paper_2606_01065_amd import leyline as L
         bt_stride = W.paged_bt_stride(wl)
         dirs = L.make_directives([dict(span_start=d.span_start, span_end=d.span_end, seq=d.seq,
@@ -634,9 +650,6 @@ def summarize(args):
                                               sum(-(-n // wl.page_size) for n in wl.seq_lens),
                                               wl.paged_flags)
         alg, _, kernel = paged_bytes(wl, kinds, new_lens, bt_stride, L)
-    elif wl.rotate:
-        alg, _ = rotate_bytes(wl)
-        kernel = ROTATE_KERNEL
     else:
         alg, _ = contig_bytes(wl)
         kernel = CONTIG_KERNEL

@@ -189,6 +189,21 @@ template <> __device__ __forceinline__ void rot_halves<4>(u32x4& x, u32x4& y, co
     }
 }
 
+// The partner lane's chunk of a lane-exchanged half-split band (partner: its lane index).  With
+// 16-chunk bands on 16-chunk boundaries the partner is lane ^ 8 of the same 16-lane DPP row, read
+// with a row rotation by 8 (no LDS traffic); otherwise a cross-lane permute.
+__device__ __forceinline__ u32x4 partner_chunk(const KPlane& pl, const u32x4& v, int partner) {
+    u32x4 o;
+    if (pl.neox_dpp) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = uint32_t(__builtin_amdgcn_update_dpp(0, int(v[i]), 0x128, 0xf, 0xf, false));
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[i]), partner, 64));
+    }
+    return o;
+}
+
 // Lane-exchanged half-split chunk: `v` is this lane's chunk of the band, `o` the partner lane's
 // (the other half); only this lane's elements are computed.  Element e pairs with element e of
 // the partner chunk, cos/sin table[cs + e].
@@ -281,9 +296,7 @@ __device__ __forceinline__ void rotate_chunk(const KPlane& pl, u32x4& v, int32_t
             const bool lo = j < half;
             const int lane = int(threadIdx.x & 63);
             const int partner = lo ? lane + half : lane - half;
-            u32x4 o;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[i]), partner, 64));
+            u32x4 o = partner_chunk(pl, v, partner);
             rot_exchanged<ESZ>(v, o, table, cs + (lo ? j : j - half) * EPC, lo);
         }
     }
@@ -324,9 +337,7 @@ __device__ __forceinline__ void rotate_band_chunk(const KPlane& pl, u32x4& v, in
         const bool lo = j < half;
         const int lane = int(threadIdx.x & 63);
         const int partner = lo ? lane + half : lane - half;
-        u32x4 o;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[i]), partner, 64));
+        u32x4 o = partner_chunk(pl, v, partner);
         rot_exchanged<ESZ>(v, o, table, cs + (lo ? j : j - half) * EPC, lo);
     }
 }
@@ -517,9 +528,7 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
                     const bool lo = j < half;
                     const int lane = int(threadIdx.x & 63);
                     const int partner = lo ? lane + half : lane - half;
-                    u32x4 o;
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) o[i] = uint32_t(__shfl(int(v[k][i]), partner, 64));
+                    u32x4 o = partner_chunk(pl, v[k], partner);
                     rot_exchanged<ESZ>(v[k], o, lcs, (lo ? j : j - half) * EPC, lo);
                 }
             }

@@ -44,6 +44,8 @@ struct KPlane {
     int32_t cs_off;          // offset of this plane's pairs within one shift's cos/sin block
     int32_t n_pairs;         // rotary pairs per head (rot_dim / 2)
     int32_t neox_lanes;      // 1: half-split partners are exchanged between lanes of a wavefront
+    int32_t neox_dpp;        // 1: ... and every band is 16 chunks on 16-chunk boundaries, so a
+                             // lane's partner is lane ^ 8 within its row of 16 lanes (DPP)
     int32_t band_wide;       // 1: the rotary bands make up at least half of the row (GQA K),
                              // 0: a narrow slice of each row (MLA K_pe)
     int32_t tpr;             // row kernels: threads per row (row_chunks, or two-chunk units)

@@ -99,6 +99,10 @@ int describe_cache(const leyline_cache* cache, bool paged, KPlane out[LEYLINE_MA
                 }
                 k.neox_lanes = ok ? 1 : 0;
                 if (!ok) k.tpr = k.row_chunks - k.n_heads * (k.rot_chunks / 2);
+                // every kernel lays a lane's chunk at lane mod 16 of its 16-chunk group when rows
+                // (row kernels) or bands (rotary-only kernels) are multiples of 16 chunks
+                k.neox_dpp = (ok && k.rot_chunks == 16 && k.head_chunks % 16 == 0 && k.rot_lo % 16 == 0 &&
+                              k.tpr % 16 == 0) ? 1 : 0;
             }
             k.band_wide = (2 * k.n_heads * k.rot_chunks >= k.row_chunks) ? 1 : 0;
             // rotary-only kernels pack the bands of consecutive heads and rows back to back

@@ -375,6 +375,45 @@ def test_rotate_delta_full_size(L, name):
                 PU.assert_pairs_turned(bl[rows][:, rot], gl[rows][:, rot], tables, wl.dtype, what)
 
 
+def test_rotate_delta_token_slots_full_size(L):
+    """Re-anchoring in place on a token-slot cache at full size (the paper's own kernel operation:
+    the K_pe bands of the 32K MLA splice's downstream slots, listed by physical slot, rotated
+    where they are): three whole layers of the pool against the oracle; every layer by
+    properties (listed slots' pairs turned by their angle, every other element bit-identical)."""
+    wl = W.WORKLOADS["mla_dsv3_slots_rotate_32k"]()
+    delta, row0, n = wl.rotate
+    pools, bt, _, _ = W.alloc_paged(wl, DEV)
+    before = [t.clone() for t in pools]
+    slots = bt[0, row0:row0 + n].long().contiguous()
+    print(f"[case] {wl.name}: rotate {n} listed slots by {delta}", flush=True)
+    specs = [L.PlaneSpec(t, p.n_heads, p.head_stride or p.row_elems, p.rot_offset, p.rot_dim, p.style, p.base)
+             for p, t in zip(wl.planes, pools)]
+    L.leyline_rotate_delta(L.make_cache(specs, paged=True), delta, rows=slots)
+    torch.cuda.synchronize()
+    plane = oracle_plane(wl.planes[0])
+    row = plane.row_elems
+    layers = [0, wl.n_layers // 2, wl.n_layers - 1]
+    sel = torch.tensor(layers, device=DEV)
+    b = host(before[0].index_select(0, sel)).reshape(len(layers), -1, row)
+    g = host(pools[0].index_select(0, sel)).reshape(len(layers), -1, row)
+    s_h = slots.cpu().numpy()
+    want = b.copy()
+    for i in range(len(layers)):
+        want[i, s_h] = O.rotate_rows(b[i, s_h], delta, plane, wl.dtype)
+    assert_rows_match(g, want, plane, wl.dtype, inputs=b, what=wl.name)
+    rot = torch.from_numpy(PU.rotary_mask(plane)).to(DEV)
+    tables = PU.angle_tables(plane, np.full(n, delta), DEV)
+    listed = torch.zeros(pools[0].shape[1], dtype=torch.bool, device=DEV)
+    listed[slots] = True
+    b4, af = before[0].reshape(wl.n_layers, -1, row), pools[0].reshape(wl.n_layers, -1, row)
+    for layer in range(wl.n_layers):
+        what = f"{wl.name} layer {layer}"
+        gl, bl = af[layer], b4[layer]
+        assert torch.equal(PU.bits(gl[:, ~rot]), PU.bits(bl[:, ~rot])), f"{what}: non-rotary"
+        assert torch.equal(PU.bits(gl[~listed]), PU.bits(bl[~listed])), f"{what}: slots not listed"
+        PU.assert_pairs_turned(bl[slots][:, rot], gl[slots][:, rot], tables, wl.dtype, what)
+
+
 def test_rotate_delta_flags_bad_rows(L):
     wl = _small_workload(random.Random(1), "mla", "bf16", 1, 64, [])
     planes_dev, _ = W.alloc_contig(wl, DEV, seed=4)

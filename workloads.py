@@ -26,6 +26,9 @@ Workloads (MLA rows: latent c_kv[512] + K_pe[64]; GQA rows: 8 KV heads x 128):
   mla_dsv3_rotate_32k, gqa_llama3_8b_rotate_16k
                       re-anchoring in place without movement: the downstream rows of the 32K MLA
                       and 16K GQA splices rotated by their shifts
+  mla_dsv3_slots_rotate_32k
+                      the same on a token-slot cache: the 32K MLA splice's downstream slots,
+                      listed by physical slot, rotated in place
 """
 
 from __future__ import annotations
@@ -200,6 +203,19 @@ def mla_dsv3_rotate_32k() -> Workload:
                     rotate=(d.stub_len - (d.span_end - d.span_start), d.span_end, n - d.span_end), seed=w.seed)
 
 
+def mla_dsv3_slots_rotate_32k() -> Workload:
+    """Re-anchoring in place on a token-slot cache, the operation of the paper's own kernel
+    (K_pe of re-keyed slots rotated where they are): the downstream slots of the 32K MLA
+    token-slot splice, listed by physical slot, rotated by its shift; no replacement, no tables.
+    The pool is the splice's own (same slots, same placement): its directive sizes the pool and
+    nothing else, so the two workloads differ only by the splice's own work."""
+    w = mla_dsv3_slots_32k()
+    d = w.dirs[0]
+    n = w.seq_lens[0]
+    return Workload("mla_dsv3_slots_rotate_32k", w.n_layers, w.dtype, w.planes, w.dirs, w.seq_lens, page_size=1,
+                    rotate=(d.stub_len - (d.span_end - d.span_start), d.span_end, n - d.span_end), seed=w.seed)
+
+
 def gqa_llama3_8b_rotate_16k() -> Workload:
     """Re-anchoring without movement on the 16K GQA cache: whole K rows of the downstream rows
     [6144, 16384) rotated in place by -2024, V untouched."""
@@ -221,6 +237,7 @@ WORKLOADS = {
     "mla_dsv3_slots_cow_32k": mla_dsv3_slots_cow_32k,
     "mla_dsv3_rotate_32k": mla_dsv3_rotate_32k,
     "gqa_llama3_8b_rotate_16k": gqa_llama3_8b_rotate_16k,
+    "mla_dsv3_slots_rotate_32k": mla_dsv3_slots_rotate_32k,
 }
 
 
