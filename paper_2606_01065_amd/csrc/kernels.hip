@@ -1104,7 +1104,7 @@ __global__ __launch_bounds__(TPB) void paged_resolve_kernel(const KPagedParams P
 // the rows are resolved here from the plan instead of read from the row table.
 template <int ESZ, bool INLINE>
 __device__ __forceinline__ void paged_move_block(const KPagedParams& P, const PlanView& V, int plane, int32_t bx,
-                                                 KCosSin* lcs) {
+                                                 int32_t lgroup, KCosSin* lcs) {
     const KPlane& pl = P.planes[plane];
     const int32_t tb = bx * PAGED_TPB;
     if (int64_t(tb) >= int64_t(P.n_rows) * pl.tpr) return;            // past this plane
@@ -1121,7 +1121,7 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, const Pl
     }
     const CsReg c = cs_fetch(V.cs, cs0 + pl.cs_off, cs0 >= 0 ? pl.n_pairs : 0);
     // PAGED_LPT consecutive layers per thread: one row entry, all loads in flight before any store.
-    const int layer0 = int(blockIdx.y) * PAGED_LPT;
+    const int layer0 = lgroup * PAGED_LPT;
     const int nl = min(PAGED_LPT, P.n_layers - layer0);
     const char* src;
     int64_t src_step;
@@ -1172,7 +1172,7 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, const Pl
 // table.
 template <int ESZ>
 __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const PlanView& V, int plane, int32_t bx,
-                                                  KCosSin* lcs) {
+                                                  int32_t lgroup, KCosSin* lcs) {
     const KPlane& pl = P.planes[plane];
     const int32_t upp = P.page_size * pl.rot_tpr;
     const int32_t tb = bx * PAGED_TPB;
@@ -1209,7 +1209,7 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const P
     const int32_t f = t - m * upp;
     const int32_t r = fdiv(f, P.rot_div[plane]);
     active = active && r < e.rows;
-    const int layer0 = int(blockIdx.y) * PAGED_LPT;
+    const int layer0 = lgroup * PAGED_LPT;
     const int nl = min(PAGED_LPT, P.n_layers - layer0);
     char* row = pl.base + int64_t(layer0) * pl.layer_stride + int64_t(e.page) * pl.page_stride +
                 int64_t(r) * pl.token_stride;
@@ -1223,34 +1223,39 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const P
     else band_rotate_store<ESZ>(pl, bp, row, pl.layer_stride, nl, x, y, V.cs, e.cs + pl.cs_off);
 }
 
-// The first workgroups gather ASSEMBLE rows (plane by plane), the next rotate REMAP pages' rotary
-// bands (plane by plane), the last P.table_x per layer group write the block tables and the
-// freed list; planes without work get no workgroups.  SOLO: only plane 0 has work
-// in this launch, so no workgroup looks its plane up.  INLINE: the gather resolves its rows (no
-// row table) and the launch may carry table work.
+// One dimension of workgroups: the gather workgroups of every layer group first (plane by plane
+// within a layer group), then (small gathers) the workgroups that write the block tables and the
+// freed list, then the REMAP workgroups of every layer group (plane by plane).  The gather's and
+// the tables' lookup chains are the longest, so they start first and the bulk of a token-slot
+// splice (the REMAP rotation) follows; planes without work get no workgroups.  SOLO: only plane 0
+// has work in this launch, so no workgroup looks its plane up.  INLINE: the gather resolves its
+// rows (no row table) and the launch may carry table work.
 template <int ESZ, bool SOLO, bool INLINE>
 __global__ __launch_bounds__(PAGED_TPB) void paged_data_kernel(const KPagedParams P) {
     __shared__ KCosSin lcs[KMAX_CS];
     const PlanView V = plan_view(P);
-    int32_t bx = int32_t(blockIdx.x);
+    int32_t b = int32_t(blockIdx.x);
     const int32_t moves = SOLO ? P.move_base[1] : P.move_base[P.n_planes];
-    if (bx < moves) {
+    if (b < moves * P.layer_groups) {
+        const int32_t y = fdiv(b, P.move_blk_div);
+        const int32_t bx = b - y * moves;
         const int p = SOLO ? 0 : plane_of(P.move_base, P.n_planes, bx);
-        paged_move_block<ESZ, INLINE>(P, V, p, bx - P.move_base[p], lcs);
+        paged_move_block<ESZ, INLINE>(P, V, p, bx - P.move_base[p], y, lcs);
         return;
     }
-    bx -= moves;
-    const int32_t remaps = SOLO ? P.remap_base[1] : P.remap_base[P.n_planes];
-    if (bx < remaps) {
-        const int p = SOLO ? 0 : plane_of(P.remap_base, P.n_planes, bx);
-        paged_remap_block<ESZ>(P, V, p, bx - P.remap_base[p], lcs);
-        return;
-    }
-    // table work, spread over the layer groups
+    b -= moves * P.layer_groups;
     if (INLINE) {
-        const int64_t b = int64_t(blockIdx.y) * P.table_x + (bx - remaps);
-        table_work(P, V, b * PAGED_TPB + threadIdx.x);
+        if (b < P.table_blocks) {
+            table_work(P, V, int64_t(b) * PAGED_TPB + threadIdx.x);
+            return;
+        }
+        b -= P.table_blocks;
     }
+    const int32_t remaps = SOLO ? P.remap_base[1] : P.remap_base[P.n_planes];
+    const int32_t y = fdiv(b, P.remap_blk_div);
+    const int32_t bx = b - y * remaps;
+    const int p = SOLO ? 0 : plane_of(P.remap_base, P.n_planes, bx);
+    paged_remap_block<ESZ>(P, V, p, bx - P.remap_base[p], y, lcs);
 }
 
 // -------------------------------------------------------------------------- host launchers ---
@@ -1777,7 +1782,7 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
             if (rc) return rc;
         } else {
             // the first data launch writes the tables, spread over its layer groups
-            P.table_x = int32_t(((n_tables + PAGED_TPB - 1) / PAGED_TPB + layer_groups - 1) / layer_groups);
+            P.table_blocks = int32_t((n_tables + PAGED_TPB - 1) / PAGED_TPB);
         }
         if (t.remap_sorted) {
             // wide rotary bands: the REMAP pages in physical order
@@ -1801,10 +1806,14 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
             P.move_base[p + 1] = int32_t(mb);
             P.remap_base[p + 1] = int32_t(rb);
         }
-        if (mb + rb + P.table_x > 0) {
-            const dim3 grid(unsigned(mb + rb + P.table_x), layer_groups, 1);
+        const int64_t blocks = (mb + rb) * int64_t(layer_groups) + P.table_blocks;
+        if (blocks > INT32_MAX - 1024) return LEYLINE_E_INVAL;
+        if (blocks > 0) {
+            P.layer_groups = int32_t(layer_groups);
+            P.move_blk_div = make_div(int32_t(std::max<int64_t>(1, mb)));
+            P.remap_blk_div = make_div(int32_t(std::max<int64_t>(1, rb)));
             const bool solo = P.move_base[1] == mb && P.remap_base[1] == rb;   // plane 0 only
-            rc = launch_paged_data(bf16, solo, !row_table, grid, s, P);
+            rc = launch_paged_data(bf16, solo, !row_table, dim3(unsigned(blocks)), s, P);
             if (rc) return rc;
         }
     }

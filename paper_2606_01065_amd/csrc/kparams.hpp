@@ -376,8 +376,11 @@ struct KPagedParams {
     const int32_t* bt_in;
     const int32_t* free_pages;
     int32_t n_free;
-    int32_t table_x;         // data kernel: workgroups per layer group writing the block tables and
-                             // the freed list (0: the resolve kernel writes them)
+    int32_t table_blocks;    // data kernel: workgroups writing the block tables and the freed list
+                             // (0: the resolve kernel writes them)
+    int32_t layer_groups;    // data kernel: groups of PAGED_LPT layers
+    KDiv move_blk_div;       // data kernel: division by the gather workgroups of one layer group
+    KDiv remap_blk_div;      // data kernel: division by the REMAP workgroups of one layer group
     int32_t* status;
     KRowMove* rows;          // workspace, n_rows entries (null: the gather resolves rows itself)
     // block tables and freed list
