@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--counters", nargs="+", metavar="PMC_DIR",
+                    help="rocprofv3 --pmc runs of the same bench command -> per-dispatch counter "
+                         "table of the dominant kernel in profiles/counters_<kernel>_<workload>.md")
     ap.add_argument("--command", default="", help="command line recorded in --summarize output")
     ap.add_argument("--also", default="gqa_llama3_8b_16k,mla_dsv3_paged_131k,mla_dsv3_32k:exact,gqa_llama3_8b_16k:exact",
                     help="further workloads timed in the same run and reported under \"also\" "
@@ -269,6 +272,9 @@ def main():
     args = parse()
     if args.summarize:
         summarize(args)
+        return
+    if args.counters:
+        summarize_counters(args)
         return
     if args.cpu_leg:
         cpu_leg(*args.cpu_leg)
@@ -722,6 +728,36 @@ def summarize(args):
     if rec:
         with open(os.path.join(PROFILES, f"traffic_{key}.json"), "w") as f:
             json.dump(rec, f, indent=1)
+    print("\n".join(lines))
+
+
+def summarize_counters(args):
+    """Mean value per dispatch of every counter in rocprofv3 --pmc runs (one directory per run) for
+    the workload's dominant library kernel, and per KiB of the splice's algorithmic bytes moved
+    by that kernel per dispatch."""
+    import workloads as W
+    wl = W.WORKLOADS[args.workload]()
+    kernel = ROTATE_KERNEL if wl.rotate else PAGED_KERNEL if wl.page_size else None
+    rows = []
+    for d in args.counters:
+        data = _read_csv(d, "counter_collection")
+        names = sorted({r["Counter_Name"] for r in data})
+        if kernel is None:     # contiguous: the library kernel with the most dispatches
+            counts = {}
+            for r in data:
+                if "leyline::" in r.get("Kernel_Name", ""):
+                    counts[r["Kernel_Name"]] = counts.get(r["Kernel_Name"], 0) + 1
+            top = max(counts, key=counts.get)
+            kernel = CONTIG_TILE_KERNEL if CONTIG_TILE_KERNEL in top else CONTIG_KERNEL
+        for n in names:
+            vals = _counter_per_dispatch(data, n, lambda k: kernel in k)
+            rows.append((n, len(vals), float(np.mean(vals)) if vals else float("nan")))
+    lines = [f"# {kernel} on {wl.name}: counters", "", f"Command: `{args.command}`", "",
+             "| counter | dispatches | mean per dispatch |", "|---|---|---|"]
+    lines += [f"| {n} | {k} | {v:.4g} |" for n, k, v in rows]
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, f"counters_{kernel}_{wl.name}.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
 

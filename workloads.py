@@ -17,6 +17,8 @@ Workloads (MLA rows: latent c_kv[512] + K_pe[64]; GQA rows: 8 KV heads x 128):
                       delete [4096,6144), 24-token stub
   mla_dsv3_paged_131k 61 layers, 64-token pages, one 131072-token sequence, 8 non-overlapping
                       directives (spans U[256,8192], stubs U[0,64])
+  mla_dsv3_paged_131k_inorder
+                      the same with the pool's pages handed out in order (placement study)
   mla_dsv3_32k_edits8 the 32K MLA cache with 8 seeded edits (spans U[8,200], stubs U[0,2*span])
   mla_dsv3_32k_shift1 the 32K MLA cache with one token deleted (every downstream row moves by one)
   mla_dsv3_slots_32k, gqa_llama3_8b_slots_16k
@@ -78,6 +80,8 @@ class Workload:
     capacity: int = 0             # contiguous rows per layer
     paged_flags: int = 0          # paged splice flags (1: copy-on-write, no old page written)
     rotate: Tuple[int, int, int] = None   # (delta, row0, n_rows): re-anchoring in place, no move
+    placement: str = "permuted"   # paged: pool pages handed to sequences and the free list in a
+                                  # seeded random order ("permuted") or in pool order ("in_order")
     seed: int = 0
     notes: dict = field(default_factory=dict)
 
@@ -139,6 +143,16 @@ def mla_dsv3_paged_131k(seed: int = 5, n_layers: int = 61) -> Workload:
     dirs = [Dir(a, b, int(rng.integers(0, 65))) for a, b in spans]
     return Workload("mla_dsv3_paged_131k", n_layers, "bf16", [mla_plane()], dirs, [n],
                     page_size=64, seed=seed)
+
+
+def mla_dsv3_paged_131k_inorder() -> Workload:
+    """The 131K-token 8-directive paged splice with the pool's pages handed out in pool order (the
+    sequence's pages and the free list each contiguous and ascending) instead of permuted: the
+    same bytes, without scattered pages to translate."""
+    w = mla_dsv3_paged_131k()
+    w.name = "mla_dsv3_paged_131k_inorder"
+    w.placement = "in_order"
+    return w
 
 
 def mla_dsv3_32k_edits8(seed: int = 6) -> Workload:
@@ -230,6 +244,7 @@ WORKLOADS = {
     "mla_dsv3_paged_b64": mla_dsv3_paged_b64,
     "gqa_llama3_8b_16k": gqa_llama3_8b_16k,
     "mla_dsv3_paged_131k": mla_dsv3_paged_131k,
+    "mla_dsv3_paged_131k_inorder": mla_dsv3_paged_131k_inorder,
     "mla_dsv3_32k_edits8": mla_dsv3_32k_edits8,
     "mla_dsv3_32k_shift1": mla_dsv3_32k_shift1,
     "mla_dsv3_slots_32k": mla_dsv3_slots_32k,
@@ -311,7 +326,7 @@ def alloc_paged(w: Workload, device, seed: int = None, fill: bool = True, spare_
     bt_stride = paged_bt_stride(w)
     n_used = sum(old_pages)
     n_pool = n_used + fresh_page_bound(w) + spare_pages
-    perm = rng.permutation(n_pool).astype(np.int32)
+    perm = (rng.permutation(n_pool) if w.placement == "permuted" else np.arange(n_pool)).astype(np.int32)
     bt = np.full((len(w.seq_lens), bt_stride), -1, dtype=np.int32)
     c = 0
     for b, k in enumerate(old_pages):
