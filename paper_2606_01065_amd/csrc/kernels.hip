@@ -454,8 +454,9 @@ __device__ __forceinline__ void cs_commit(KCosSin* lcs, const CsReg& c, int32_t 
 // --------------------------------------------------------------------- contiguous splice ---
 
 // Rounds and replacement copies: rows laid end to end, one unit per thread for CRPT rows (the
-// same column of consecutive rows, so one cos/sin lookup serves them all); blockIdx.z selects the
-// (job, plane) item.  A rotating item's workgroup stages its cos/sin block in LDS after the
+// same column of consecutive rows, so one cos/sin lookup serves them all); the (job, plane) items
+// of a launch own consecutive ranges of workgroups (blockIdx.x), so a small item (a replacement
+// copy) next to a round adds only its own workgroups.  A rotating item's workgroup stages its cos/sin block in LDS after the
 // threads have issued their data loads, so that the two latencies overlap.  Past the item's last
 // row a thread loads that last row again (every load issued without branching) and stores
 // nothing.
@@ -466,13 +467,19 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
     __shared__ KCosSin lcs[KMAX_CS];
     // The item as a value: its fields come in one level of independent scalar loads (through a
     // reference the compiler loaded them one by one between the branches below).
+    // the item whose range holds this workgroup: the number of later items starting at or before
+    // it (independent reads, no loop-carried dependency)
+    int32_t it = 0;
+#pragma unroll
+    for (int i = 1; i < KMAX_LAUNCH_ITEMS; ++i) it += int32_t(blockIdx.x) >= P.block0[i] ? 1 : 0;
     KItem I;
-    __builtin_memcpy(&I, &P.items[blockIdx.z], sizeof(KItem));
+    __builtin_memcpy(&I, &P.items[it], sizeof(KItem));
+    const int32_t bx = int32_t(blockIdx.x) - P.block0[it];
     const KPlane& pl = I.pl;
     const int64_t groups = (I.count + CRPT - 1) / CRPT;
-    if (int64_t(blockIdx.x) * MOVE_TPB >= groups * pl.tpr) return;      // block past this item's rows
+    if (int64_t(bx) * MOVE_TPB >= groups * pl.tpr) return;               // block past this item's rows
     const int layer = blockIdx.y;
-    const int32_t t = int32_t(blockIdx.x) * MOVE_TPB + int32_t(threadIdx.x);
+    const int32_t t = bx * MOVE_TPB + int32_t(threadIdx.x);
     const int32_t g = fdiv(t, pl.tpr_div), u = t - g * pl.tpr;
     const int64_t r0 = int64_t(g) * CRPT;
     const bool active = r0 < I.count;
@@ -1310,6 +1317,9 @@ extern "C" const char* leyline_last_hip_error(void) {
     return hipGetErrorString(g_last_hip_error);
 }
 
+// The launch a contiguous job goes to: replacement copies share the round kernel's launches.
+static int launch_kind(int kind) { return kind == KJOB_STUB ? int(KJOB_ROUND) : kind; }
+
 // Kernel launches of a schedule (only the ordered-tile launches when tiles_only): with tiles, the
 // prep launches and the tile launches; otherwise, per group of independent jobs, one launch per
 // job kind present, split further when a launch would exceed its item or cos/sin capacity.
@@ -1325,12 +1335,12 @@ static int contig_launch_count(const leyline_cache* cache, const ContigSchedule&
     const int32_t cs_need = cos_sin_per_shift(cache);
     int n = 0;
     for (const auto& group : sched.launches)
-        for (int kind : {int(KJOB_STUB), int(KJOB_CHAIN), int(KJOB_ROUND)}) {
+        for (int kind : {int(KJOB_CHAIN), int(KJOB_ROUND)}) {
             int items = 0, cs = 0;
             bool open = false;
             for (const ContigJobHost& j : group) {
-                if (j.kind != kind) continue;
-                const int need = kind != KJOB_STUB ? cs_need : 0;
+                if (launch_kind(j.kind) != kind) continue;
+                const int need = j.kind != KJOB_STUB ? cs_need : 0;
                 if (open && (items + n_planes > KMAX_LAUNCH_ITEMS || cs + need > KMAX_CS)) {
                     ++n;
                     items = cs = 0;
@@ -1454,39 +1464,46 @@ static int splice_contig_planned(const leyline_cache* cache, const ContigSchedul
     for (const auto& group : sched.launches) {
         // the jobs of a group are independent; replacement copies, chains and rounds go to
         // separate launches, each a list of (job, plane) items selected by blockIdx.z
-        for (int kind : {int(KJOB_STUB), int(KJOB_CHAIN), int(KJOB_ROUND)}) {
+        for (int kind : {int(KJOB_CHAIN), int(KJOB_ROUND)}) {
+            // ROUND launches carry the group's rounds and replacement copies, each (job, plane)
+            // item with its own range of workgroups; CHAIN launches select items by blockIdx.z
             KContigParams P;
             std::vector<KCosSin> cs;
-            int64_t max_blocks = 0;
+            int64_t max_blocks = 0, total_blocks = 0;
             auto flush = [&]() -> int {
                 if (P.n_items == 0) return LEYLINE_OK;
-                if (cs.size() > size_t(KMAX_CS) || max_blocks > INT32_MAX) return LEYLINE_E_INVAL;
+                if (cs.size() > size_t(KMAX_CS) || max_blocks > INT32_MAX || total_blocks > INT32_MAX)
+                    return LEYLINE_E_INVAL;
                 std::copy(cs.begin(), cs.end(), P.cs);
-                const dim3 grid(unsigned(max_blocks), unsigned(cache->n_layers), unsigned(P.n_items));
+                for (int32_t i = P.n_items; i < KMAX_LAUNCH_ITEMS; ++i) P.block0[i] = INT32_MAX;
                 int r;
-                if (kind == KJOB_CHAIN)
+                if (kind == KJOB_CHAIN) {
+                    const dim3 grid(unsigned(max_blocks), unsigned(cache->n_layers), unsigned(P.n_items));
                     r = cache->dtype == LEYLINE_BF16 ? launch(contig_chain_kernel<2>, grid, s, P)
                                                      : launch(contig_chain_kernel<4>, grid, s, P);
-                else
+                } else {
+                    const dim3 grid(unsigned(total_blocks), unsigned(cache->n_layers), 1);
                     r = cache->dtype == LEYLINE_BF16 ? launch(contig_move_kernel<2>, grid, s, P, MOVE_TPB)
                                                      : launch(contig_move_kernel<4>, grid, s, P, MOVE_TPB);
+                }
                 P.n_items = 0;
                 cs.clear();
-                max_blocks = 0;
+                max_blocks = total_blocks = 0;
                 return r;
             };
             std::memset(&P, 0, sizeof(P));
             for (const ContigJobHost& j : group) {
-                if (j.kind != kind) continue;
-                if (P.n_items + n_planes > KMAX_LAUNCH_ITEMS || int32_t(cs.size()) + cs_need > KMAX_CS) {
+                if (launch_kind(j.kind) != kind) continue;
+                const int32_t need = j.kind != KJOB_STUB ? cs_need : 0;
+                if (P.n_items + n_planes > KMAX_LAUNCH_ITEMS || int32_t(cs.size()) + need > KMAX_CS) {
                     rc = flush();
                     if (rc) return rc;
                 }
-                const int32_t cs0 = (kind != KJOB_STUB && cs_need > 0) ? append_cos_sin(cache, j.delta, cs) : -1;
+                const int32_t cs0 = (j.kind != KJOB_STUB && cs_need > 0) ? append_cos_sin(cache, j.delta, cs) : -1;
                 for (int p = 0; p < n_planes; ++p) {
                     const int64_t th = item_threads(j, p);
                     if (th == 0) continue;
-                    KItem& it = P.items[P.n_items++];
+                    KItem& it = P.items[P.n_items];
                     std::memset(&it, 0, sizeof(it));
                     it.pl = planes[p];
                     it.src0 = j.src0;
@@ -1496,9 +1513,13 @@ static int splice_contig_planned(const leyline_cache* cache, const ContigSchedul
                     it.kind = j.kind;
                     it.chains = int32_t(kind == KJOB_CHAIN ? std::min<int64_t>(j.count, abs64(j.delta)) : 0);
                     it.cs = (cs0 >= 0 && planes[p].rot != KROT_NONE) ? cs0 + planes[p].cs_off : -1;
-                    if (kind == KJOB_STUB) it.stub = static_cast<const char*>(dirs[j.dir].stub[p]);
+                    if (j.kind == KJOB_STUB) it.stub = static_cast<const char*>(dirs[j.dir].stub[p]);
                     const int block = kind == KJOB_CHAIN ? TPB : MOVE_TPB;
-                    max_blocks = std::max(max_blocks, (th + block - 1) / block);
+                    const int64_t blocks = (th + block - 1) / block;
+                    P.block0[P.n_items] = int32_t(std::min<int64_t>(total_blocks, INT32_MAX));
+                    max_blocks = std::max(max_blocks, blocks);
+                    total_blocks += blocks;
+                    ++P.n_items;
                 }
             }
             rc = flush();

@@ -126,6 +126,8 @@ constexpr int KMAX_LAUNCH_ITEMS = 8;
 
 struct KContigParams {
     KItem items[KMAX_LAUNCH_ITEMS];
+    int32_t block0[KMAX_LAUNCH_ITEMS];   // round and replacement launches: first workgroup (x) of
+                                         // each item, side by side; INT32_MAX past n_items
     int32_t n_items;
     int32_t n_layers;
     KCosSin cs[KMAX_CS];

@@ -127,12 +127,12 @@ def test_contig_query_reports_rounds_tiles_and_workspace():
     workspace) when every round moves at least 64 MB; otherwise, and whenever it would take more
     than 16 rounds, the whole call (moves and replacement copies) runs as ordered tiles in one
     launch, after one launch that clears the tiles' counter and flags in the workspace and writes
-    the cos/sin table there.  With rounds, a replacement copy is a launch of its own (in the first
-    round's launch it would add a workgroup grid of the round's size that mostly exits at once:
-    measured slower)."""
+    the cos/sin table there.  With rounds, a left shift's replacement copy rides in the first
+    round's launch with a workgroup range of its own; a right shift's copy overwrites downstream
+    rows and waits for the move in a launch of its own."""
     big = _mla_cache(n_layers=61, cap=32768)                                # 1152-byte rows
-    q = L.leyline_contig_query(big, 32768, _dirs([(14055, 18151, 32)]), 1)   # m=4064: 285 MB rounds
-    assert (q.new_len, q.launches, q.tile_launches, q.workspace_bytes) == (32768 - 4064, 4 + 1, 0, 0)
+    q = L.leyline_contig_query(big, 32768, _dirs([(14055, 18151, 32)]), 1)   # m=4064: 513 MB rounds
+    assert (q.new_len, q.launches, q.tile_launches, q.workspace_bytes) == (32768 - 4064, 4, 0, 0)
     c = _mla_cache(cap=64)                                                  # 2 layers, 72 chunks/row
     q = L.leyline_contig_query(c, 60, _dirs([(10, 20, 2)]), 1)               # m=8, D=40: small rounds
     assert (q.new_len, q.launches, q.tile_launches) == (52, 1 + 1, 1)        # prep, tiles (+ stub)
@@ -145,7 +145,7 @@ def test_contig_query_reports_rounds_tiles_and_workspace():
     q = L.leyline_contig_query(c, 60, _dirs([(10, 12, 4)]), 1)               # m=2 right, D=48
     assert (q.new_len, q.launches, q.tile_launches) == (62, 1 + 1, 1)
     q = L.leyline_contig_query(c, 60, _dirs([(10, 40, 2)]), 1)               # m=28 > D=20: one round
-    assert (q.new_len, q.launches, q.tile_launches, q.workspace_bytes) == (32, 1 + 1, 0, 0)
+    assert (q.new_len, q.launches, q.tile_launches, q.workspace_bytes) == (32, 1, 0, 0)
     # a right shift's replacement overwrites downstream rows: it waits for the move (two launches)
     q = L.leyline_contig_query(c, 30, _dirs([(10, 10, 20)]), 1)              # m=20 right, D=20
     assert (q.new_len, q.launches, q.tile_launches, q.workspace_bytes) == (50, 2, 0, 0)
