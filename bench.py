@@ -59,6 +59,9 @@ def parse():
     ap.add_argument("--also", default="gqa_llama3_8b_16k,mla_dsv3_paged_131k,mla_dsv3_32k:exact,gqa_llama3_8b_16k:exact",
                     help="further workloads timed in the same run and reported under \"also\" "
                          "(comma-separated; NAME:exact runs libleyline_exact.so; empty: none)")
+    ap.add_argument("--graph", action="store_true",
+                    help="contiguous and rotate-only workloads: capture GRAPH_SPLICES consecutive splices "
+                         "(cache copies in turn) into one HIP graph and time its replays")
     ap.add_argument("--exact", action="store_true",
                     help="run the workload on libleyline_exact.so (fp64 pair arithmetic) instead of libleyline.so")
     ap.add_argument("--cpu-procs", type=int, default=0,
@@ -202,6 +205,29 @@ def setup_workload(wl, dev, L, W, args, stream):
     return step, kernel, alg_bytes, moved, launches, keep, layout
 
 
+GRAPH_SPLICES = 4     # splices per captured graph (cycling the cache copies)
+
+
+def graph_step(step):
+    """A step function that replays a HIP graph holding GRAPH_SPLICES consecutive splices, one
+    splice per call: replay k runs on call k * GRAPH_SPLICES (the others enqueue nothing)."""
+    import torch
+    g = torch.cuda.CUDAGraph()
+    for i in range(GRAPH_SPLICES):      # eager warm-up: workspaces and plans allocated outside the capture
+        step(i)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=torch.cuda.Stream()):
+        for i in range(GRAPH_SPLICES):
+            step(i)
+    torch.cuda.synchronize()
+
+    def replayed(i):
+        if i % GRAPH_SPLICES == 0:
+            g.replay()
+    replayed.graph = g
+    return replayed
+
+
 def timed(step, steps, warmup, stream):
     """Milliseconds per step: `warmup` untimed steps, then `steps` steps back to back on the
     stream the kernels run on, bracketed by two HIP events and nothing in between (an event
@@ -293,7 +319,14 @@ def main():
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
     L.use_library(args.exact)
-    step, kernel, alg_bytes, moved, launches, keep, layout = setup_workload(wl, dev, L, W, args, stream)
+    if args.graph and wl.page_size and not wl.rotate:
+        raise SystemExit("--graph: paged splices with uploaded plans cannot be captured")
+    # graph mode: the calls take the stream that is current when they run (the capture stream)
+    step, kernel, alg_bytes, moved, launches, keep, layout = setup_workload(
+        wl, dev, L, W, args, None if args.graph else stream)
+    if args.graph:
+        step = graph_step(step)
+        layout += f", {GRAPH_SPLICES} splices captured in one HIP graph, replayed"
 
     ms_per_step = timed(step, args.steps, args.warmup, stream)
     splice_ms = ms_per_step
@@ -304,10 +337,13 @@ def main():
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(n_spread)]
     for i in range(n_spread):
         starts[i].record(stream)
-        step(args.steps + i)
+        if args.graph:
+            step.graph.replay()                 # GRAPH_SPLICES splices
+        else:
+            step(args.steps + i)
         ends[i].record(stream)
     torch.cuda.synchronize()
-    per_splice = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
+    per_splice = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)]) / (GRAPH_SPLICES if args.graph else 1)
     copy_gbps, _ = copy_ceiling(alg_bytes, dev, stream)
     out = {
         "metric": METRIC,
@@ -332,6 +368,7 @@ def main():
             "moved_tokens": moved,
             "layout": layout,
             "pair_bits": L.leyline_pair_bits(),
+            "graph": bool(args.graph),
             **({"rotate_delta_row0_rows": list(wl.rotate)} if wl.rotate else {}),
         },
         "roofline": {
@@ -348,7 +385,9 @@ def main():
             "traffic_per_splice": None if rec is None else {k: rec[k] for k in ("fetch_bytes", "write_bytes", "total_bytes")},
             "splice_ms": splice_ms,
             "splice_ms_p10_p50_p90": [float(x) for x in np.percentile(per_splice, [10, 50, 90])],
-            "splice_spread_sample": f"{n_spread} splices after the timed region, an event pair around each",
+            "splice_spread_sample": (f"{n_spread} graph replays of {GRAPH_SPLICES} splices after the timed region, "
+                                     "an event pair around each, per splice" if args.graph else
+                                     f"{n_spread} splices after the timed region, an event pair around each"),
             "launches_per_splice": launches,
             "avg_launch_ms": splice_ms / max(1, launches),
             "d2d_copy_GBps": copy_gbps,

@@ -227,7 +227,9 @@ def make_cache(planes: Sequence[PlaneSpec], paged: bool = False) -> leyline_cach
             arr = (c_double * len(p.inv_freq))(*p.inv_freq)
             keep.append(arr)
             pl.inv_freq = ctypes.cast(arr, POINTER(c_double))
-    c._keep = keep           # keep host tables alive with the descriptor
+        keep.append(t)
+    # the descriptor holds raw pointers: it keeps the plane tensors and its host tables alive
+    c._keep = keep
     c._device = getattr(t0, "device", None)
     return c
 
@@ -240,6 +242,7 @@ def make_directives(dirs: Sequence[dict]) -> ctypes.Array:
     """dirs: dicts with span_start, span_end, stub (list of per-plane tensors or None), optional
     seq and mode.  stub_len is taken from the stub tensors' token dim (dim 1) or 'stub_len'."""
     arr = (leyline_directive * max(1, len(dirs)))()
+    keep = []
     for i, d in enumerate(dirs):
         x = arr[i]
         x.seq = d.get("seq", 0)
@@ -250,6 +253,9 @@ def make_directives(dirs: Sequence[dict]) -> ctypes.Array:
         x.stub_len = d.get("stub_len", stubs[0].shape[1] if stubs else 0)
         for p, s in enumerate(stubs):
             x.stub[p] = s.data_ptr() if s is not None and s.numel() else None
+            if s is not None:
+                keep.append(s)
+    arr._keep = keep         # the array holds raw pointers: it keeps the replacement tensors alive
     return arr
 
 

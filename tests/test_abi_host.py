@@ -89,6 +89,28 @@ def _contig_rc(cache, n, spec):
                                         None, 0, None)
 
 
+def test_descriptors_keep_the_tensors_they_point_to_alive():
+    """make_cache and make_directives store raw device pointers; the descriptors must keep the
+    plane and replacement tensors alive, or a caller that keeps only the descriptors (a
+    benchmark's step closure, a captured graph) would splice freed memory."""
+    import gc
+    import weakref
+
+    import torch
+    plane = torch.zeros((2, 64, 576), dtype=torch.bfloat16)
+    stub = torch.zeros((2, 3, 576), dtype=torch.bfloat16)
+    wp, ws = weakref.ref(plane), weakref.ref(stub)
+    cache = L.make_cache([L.PlaneSpec(plane, 1, 576, 512, 64, L.ROPE_INTERLEAVED, 10000.0)])
+    dirs = L.make_directives([dict(span_start=1, span_end=2, stub=[stub])])
+    del plane, stub
+    gc.collect()
+    assert wp() is not None and ws() is not None
+    assert cache.planes[0].base == wp().data_ptr() and dirs[0].stub[0] == ws().data_ptr()
+    del cache, dirs
+    gc.collect()
+    assert wp() is None and ws() is None
+
+
 def test_contig_validation_codes():
     c = _mla_cache()
     assert _contig_rc(c, 65, [(0, 1, 0)]) == L.E_RANGE                    # seq_len > capacity

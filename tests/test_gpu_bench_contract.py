@@ -59,6 +59,15 @@ def test_default_run_reports_roofline_and_cpu_baseline():
             <= 1e-6 * a["achieved_GBps"]
 
 
+def test_graph_replay_keeps_the_contract():
+    """--graph: splices captured in a HIP graph and replayed (small-call latency without launch
+    overhead), on the one-layer workload and on the 8-edit tile splice."""
+    for workload in ("mla_1l_4k_f32", "mla_dsv3_32k_edits8"):
+        d = _bench("--workload", workload, "--steps", "8", "--warmup", "4", "--no-cpu-baseline", "--also=", "--graph")
+        _check_common(d, 8, 4)
+        assert d["config"]["graph"] is True and "HIP graph" in d["config"]["layout"]
+
+
 @pytest.mark.parametrize("workload", ["mla_dsv3_slots_32k", "gqa_llama3_8b_rotate_16k", "mla_dsv3_32k_edits8"])
 def test_other_workloads_keep_the_contract(workload):
     d = _bench("--workload", workload, "--steps", "3", "--warmup", "1", "--no-cpu-baseline", "--also", "")
