@@ -930,11 +930,15 @@ __device__ __forceinline__ void resolve_freed_entry(const KPagedParams& P, const
 // so that the gather writes neighbouring pages together (with a scattered free list this saves
 // address-translation misses: measured 3 points of peak).  One workgroup: a histogram of the
 // buckets in LDS, an exclusive scan, and a scatter of the fresh ordinals into P.order.  A page
-// outside the pool counts in bucket 0 (its rows are flagged and skipped when resolved).
+// outside the pool counts in bucket 0 (its rows are flagged and skipped when resolved).  Up to
+// ORDER_STAGE ordinals are scattered in LDS and written out in order: scattered 4-byte stores
+// from one compute unit cost about 5 us per 15,000.
 constexpr int ORDER_TPB = 1024;
+constexpr int ORDER_STAGE = 24576;
 __global__ __launch_bounds__(ORDER_TPB) void paged_order_kernel(const KPagedParams P) {
     __shared__ int32_t cnt[KORDER_BUCKETS];
     __shared__ int32_t part[ORDER_TPB];
+    __shared__ int32_t stage[ORDER_STAGE];
     const int tid = int(threadIdx.x);
     for (int i = tid; i < KORDER_BUCKETS; i += ORDER_TPB) cnt[i] = 0;
     __syncthreads();
@@ -967,7 +971,13 @@ __global__ __launch_bounds__(ORDER_TPB) void paged_order_kernel(const KPagedPara
         run += own[k];
     }
     __syncthreads();
-    for (int32_t t = tid; t < P.n_asm; t += ORDER_TPB) P.order[atomicAdd(&cnt[bucket(t)], 1)] = t;
+    if (P.n_asm <= ORDER_STAGE) {
+        for (int32_t t = tid; t < P.n_asm; t += ORDER_TPB) stage[atomicAdd(&cnt[bucket(t)], 1)] = t;
+        __syncthreads();
+        for (int32_t j = tid; j < P.n_asm; j += ORDER_TPB) P.order[j] = stage[j];
+    } else {
+        for (int32_t t = tid; t < P.n_asm; t += ORDER_TPB) P.order[atomicAdd(&cnt[bucket(t)], 1)] = t;
+    }
 }
 
 // REMAP page m of the call (in plan order), resolved: its physical page, shift and valid rows.
@@ -982,12 +992,14 @@ __device__ __forceinline__ KRemapPage remap_resolve(const KPagedParams& P, const
 // workgroups that run together touch neighbouring pages.  A page outside the pool (flagged, no
 // rows to rotate) counts in bucket 0.  Up to ORDER_TPB * REMAP_SORT_PER pages are resolved once,
 // all loads of a thread in flight together, and kept in registers for the scatter; larger calls
-// sweep twice.
+// sweep twice.  Held entries are scattered in LDS (packed into 8 bytes when P.remap_pack says
+// that the shift index and the row count fit 16 bits each) and written out in order.
 constexpr int REMAP_SORT_PER = 16;
 
 __global__ __launch_bounds__(ORDER_TPB) void paged_remap_order_kernel(const KPagedParams P) {
     __shared__ int32_t cnt[KORDER_BUCKETS];
     __shared__ int32_t part[ORDER_TPB];
+    __shared__ uint2 stage[ORDER_TPB * REMAP_SORT_PER];
     const PlanView V = plan_view(P);
     const int tid = int(threadIdx.x);
     const bool held = P.n_remap <= ORDER_TPB * REMAP_SORT_PER;     // block-uniform
@@ -1032,7 +1044,18 @@ __global__ __launch_bounds__(ORDER_TPB) void paged_remap_order_kernel(const KPag
         run += own[k];
     }
     __syncthreads();
-    if (held) {
+    if (held && P.remap_pack) {
+#pragma unroll
+        for (int k = 0; k < REMAP_SORT_PER; ++k)
+            if (tid + k * ORDER_TPB < P.n_remap)
+                stage[atomicAdd(&cnt[e[k].page >> P.remap_shift], 1)] =
+                    uint2{uint32_t(e[k].page), uint32_t(e[k].cs + 1) | (uint32_t(max(e[k].rows, 0)) << 16)};
+        __syncthreads();
+        for (int32_t j = tid; j < P.n_remap; j += ORDER_TPB) {
+            const uint2 w = stage[j];
+            P.remap_sorted[j] = KRemapPage{int32_t(w.x), int32_t(w.y & 0xffffu) - 1, int32_t(w.y >> 16), 0};
+        }
+    } else if (held) {
 #pragma unroll
         for (int k = 0; k < REMAP_SORT_PER; ++k)
             if (tid + k * ORDER_TPB < P.n_remap) P.remap_sorted[atomicAdd(&cnt[e[k].page >> P.remap_shift], 1)] = e[k];
@@ -1133,9 +1156,11 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, const Pl
     const char* src;
     int64_t src_step;
     if (e.src_page == KROW_STUB) {
-        const KDirEntry D = V.dirs[e.dir];
-        src_step = D.stub_len * pl.row_bytes;
-        src = D.stub[plane] + int64_t(layer0) * src_step + int64_t(e.src_row) * pl.row_bytes;
+        // fields read through the entry's address: a copy of the entry indexed by a run-time
+        // plane would be placed in LDS, 64 bytes per thread, by the compiler
+        const KDirEntry* D = V.dirs + e.dir;
+        src_step = D->stub_len * pl.row_bytes;
+        src = D->stub[plane] + int64_t(layer0) * src_step + int64_t(e.src_row) * pl.row_bytes;
     } else {
         src_step = pl.layer_stride;
         src = pl.base + int64_t(layer0) * pl.layer_stride + int64_t(e.src_page) * pl.page_stride +
@@ -1811,6 +1836,8 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
             while (((cache->capacity - 1) >> shift) >= KORDER_BUCKETS) ++shift;
             P.remap_shift = shift;
             P.remap_sorted = reinterpret_cast<KRemapPage*>(ws + t.off_remap_sorted);
+            // entries pack into 8 bytes: shift index + 1 and valid rows below 2^16
+            P.remap_pack = cache->page_size < 65536 && t.n_cs < 65535 ? 1 : 0;
             rc = launch(paged_remap_order_kernel, dim3(1), s, P, ORDER_TPB);
             if (rc) return rc;
         }

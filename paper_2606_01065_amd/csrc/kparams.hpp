@@ -400,7 +400,7 @@ struct KPagedParams {
     KRemapPage* remap_sorted;   // workspace, the REMAP pages resolved and in physical-page order
                                 // (or null: the rotating workgroups resolve them in plan order)
     int32_t remap_shift;     // its bucket = physical page >> remap_shift
-    int32_t pad2;
+    int32_t remap_pack;      // 1: a resolved REMAP page's shift index + 1 and rows fit 16 bits each
     // the only REMAP run when n_remap_runs == 1, with its shift's cos/sin entry and its sequence's
     // new length (read with the other parameters, one level of loads before the block table)
     KPageRun remap0;
