@@ -1217,7 +1217,9 @@ __device__ __forceinline__ void paged_remap_block(const KPagedParams& P, const P
     KPageRun R0 = P.remap0;
     int32_t next0 = INT32_MAX, cs0 = P.remap0_cs, len0 = P.remap0_len;
     if (P.remap_sorted) {
-        cs0 = P.remap_sorted[fdiv(tb, P.remap_div[plane])].cs;
+        // one run: its shift comes with the parameters, no load of the sorted table before the
+        // cos/sin fetch
+        cs0 = P.n_remap_runs == 1 ? P.remap0_cs : P.remap_sorted[fdiv(tb, P.remap_div[plane])].cs;
     } else if (P.n_remap_runs > 1) {
         const int32_t r0 = run_of(V.remap_runs, P.n_remap_runs, fdiv(tb, P.remap_div[plane]));
         R0 = V.remap_runs[r0];
