@@ -395,7 +395,7 @@ struct KPagedParams {
                                                  // [move_base[p], move_base[p+1])
     int32_t remap_base[LEYLINE_MAX_PLANES + 1];  // then REMAP workgroups of plane p, numbered
                                                  // from 0 after the gather's
-    int32_t pad1;
+    int32_t gather_split;    // data kernel: 1 = each XCD gathers its own eighth (see xcd_eighth)
     int32_t* order;          // workspace, n_asm fresh ordinals in destination-page order (or null)
     KRemapPage* remap_sorted;   // workspace, the REMAP pages resolved and in physical-page order
                                 // (or null: the rotating workgroups resolve them in plan order)
