@@ -56,7 +56,8 @@ def parse():
                     help="rocprofv3 --pmc runs of the same bench command -> per-dispatch counter "
                          "table of the dominant kernel in profiles/counters_<kernel>_<workload>.md")
     ap.add_argument("--command", default="", help="command line recorded in --summarize output")
-    ap.add_argument("--also", default="gqa_llama3_8b_16k,mla_dsv3_paged_131k,mla_dsv3_32k:exact,gqa_llama3_8b_16k:exact",
+    ap.add_argument("--also", default="gqa_llama3_8b_16k,mla_dsv3_paged_131k,mla_dsv3_paged_b64,mla_dsv3_32k:exact,"
+                                      "gqa_llama3_8b_16k:exact",
                     help="further workloads timed in the same run and reported under \"also\" "
                          "(comma-separated; NAME:exact runs libleyline_exact.so; empty: none)")
     ap.add_argument("--graph", action="store_true",

@@ -46,10 +46,11 @@ def test_default_run_reports_roofline_and_cpu_baseline():
     assert isinstance(c["cores"], int) and c["cores"] >= 1 and c["sample"]
     ac = c["all_cores"]        # the same oracle in one process per host core
     assert ac["unit"] == "tokens/s" and ac["value"] > 0 and ac["cores"] >= 1 and ac["sample"]
-    # the GQA target configuration and the 8-directive paged splice, timed in the same run
+    # the GQA target configuration, the 8-directive paged splice and the 64-sequence paged batch,
+    # timed in the same run
     also = {(a["workload"], a["pair_bits"]): a for a in d["also"]}
-    assert set(also) == {("gqa_llama3_8b_16k", 32), ("mla_dsv3_paged_131k", 32), ("mla_dsv3_32k", 64),
-                         ("gqa_llama3_8b_16k", 64)}
+    assert set(also) == {("gqa_llama3_8b_16k", 32), ("mla_dsv3_paged_131k", 32), ("mla_dsv3_paged_b64", 32),
+                         ("mla_dsv3_32k", 64), ("gqa_llama3_8b_16k", 64)}
     assert d["config"]["pair_bits"] == 32
     for a in also.values():
         assert a["ms_per_step"] > 0 and a["kernel"] and a["steps"] == 3
