@@ -56,6 +56,13 @@ struct KPlane {
     int32_t band_tpr;        // rotary-only kernels: threads per band (rot_chunks, or half of it)
     int32_t rot_tpr;         // rotary-only kernels: threads per row (n_heads * band_tpr)
     KDiv band_div;           // division by band_tpr
+    // Row kernels, narrow interleaved bands of one head: pack_groups = B > 0 lays the rows out in
+    // blocks of B row groups whose band chunks (B * rot_chunks = 64) come first, as one wavefront,
+    // and their other chunks after, so that only one wavefront in (B * tpr / 64) rotates.
+    int32_t pack_groups;
+    int32_t pack_nb_shift;   // log2(rot_chunks) when packing
+    KDiv pack_div;           // division by pack_groups * tpr
+    KDiv rest_div;           // division by tpr - rot_chunks
 };
 
 // Precision of the pair arithmetic.  0: fp32 cos/sin and fp32 products (the paper's policy);
@@ -64,6 +71,14 @@ struct KPlane {
 #ifndef LEYLINE_PAIR_F64
 #define LEYLINE_PAIR_F64 0
 #endif
+// The round and gather kernels lay the band chunks of narrow interleaved bands (MLA K_pe) out
+// in wavefronts of their own, so that the other wavefronts carry no pair arithmetic: with fp64
+// pairs the 32K MLA splice 74.3% -> 78.4% of peak; with fp32 pairs 79.2% -> 78.8%, so only the
+// fp64 build does it.
+#ifndef LEYLINE_BAND_PACK
+#define LEYLINE_BAND_PACK LEYLINE_PAIR_F64
+#endif
+
 #if LEYLINE_PAIR_F64
 typedef double kcs_t;
 #else
@@ -423,5 +438,39 @@ constexpr int32_t KORDER_BUCKETS = 4096;
 // nothing from it).
 constexpr int32_t KREMAP_SORT_BYTES = 1024;
 
+
+// n / d for 0 <= n < 2^31 with a KDiv (the kernels' multiply-shift division), on either side.
+LEYLINE_HD inline int32_t kdiv(int32_t n, KDiv d) {
+    const uint32_t hi = uint32_t((uint64_t(uint32_t(n)) * d.mul) >> 32);
+    return int32_t((hi + uint32_t(n)) >> d.shift);
+}
+
+// Unit t of a row kernel's item (row groups of a few rows laid end to end, one chunk per unit):
+// its row group g and chunk u (u < tpr for every t, also past the item's last group).  With
+// pack_groups = B, units come in blocks of B row groups: first the band chunks of the block's
+// groups (rot_chunks each), then each group's other chunks in order.
+LEYLINE_HD inline void row_unit(const KPlane& pl, int32_t t, int64_t groups, int32_t& g, int32_t& u) {
+    if (pl.pack_groups) {
+        const int32_t B = pl.pack_groups, nb = pl.rot_chunks;
+        const int32_t blk = kdiv(t, pl.pack_div);
+        const int32_t w = t - blk * B * pl.tpr;
+        const int32_t g0 = blk * B;
+        const int64_t left = groups - int64_t(g0);
+        const int32_t gb = int32_t(left <= 0 ? 0 : left < B ? left : B);   // groups of this block
+        if (w < gb * nb) {
+            g = g0 + (w >> pl.pack_nb_shift);
+            u = pl.rot_lo + (w & (nb - 1));
+        } else {
+            const int32_t w2 = w - gb * nb;
+            const int32_t gi = kdiv(w2, pl.rest_div);
+            const int32_t c = w2 - gi * (pl.tpr - nb);
+            g = g0 + gi;
+            u = c < pl.rot_lo ? c : c + nb;
+        }
+    } else {
+        g = kdiv(t, pl.tpr_div);
+        u = t - g * pl.tpr;
+    }
+}
 
 }  // namespace leyline

@@ -2,7 +2,8 @@
 against the oracle bit for bit: every element of the compared rows, rotary ones included, equals
 the oracle's float64 rotation rounded once (Eq. "rotate"; the rounding of App. "bf16 K-storage
 precision floor" taken exactly).  Full-size contiguous splices on three whole layers, the
-8-edit ordered-tile splice, one fp32 layer, small random paged pools of every kernel path, and
+8-edit ordered-tile splice, one fp32 layer, small random paged pools of every kernel path, the
+full-size 131K paged splice (sampled rows, and every row's rotary bands on three layers), and
 re-anchoring in place."""
 
 import random
@@ -14,7 +15,7 @@ import torch
 import workloads as W
 from oracle import splice_oracle as O
 from tests.parity_util import host, oracle_plane
-from tests.test_gpu_paged import _odirs, _random_workload, _run_gpu
+from tests.test_gpu_paged import _check_sampled, _odirs, _random_workload, _run_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -111,3 +112,9 @@ def test_rotation_in_place_is_bit_identical_to_the_oracle(L, kind):
                 flat[layer, r] = O.rotate_rows(flat[layer, r], delta, plane, wl.dtype)
             got = host(tensors[pi]).reshape(flat.shape)
             assert np.array_equal(got, flat), f"{kind} plane {pi} delta {delta}"
+
+
+def test_paged_131k_full_is_bit_identical(L):
+    """The 8-directive 131K-token paged splice at full size (gather through the row table, bands
+    packed into wavefronts of their own, each XCD gathering its own eighth)."""
+    _check_sampled(L, W.mla_dsv3_paged_131k(), seed=23, exact=True)
