@@ -499,7 +499,7 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
     const int layer = blockIdx.y;
     const int32_t t = bx * MOVE_TPB + int32_t(threadIdx.x);
     int32_t g, u;
-    row_unit(pl, t, groups, g, u);
+    row_unit(pl, LEYLINE_ROUND_PACK, t, groups, g, u);
     const int64_t r0 = int64_t(g) * CRPT;
     const bool active = r0 < I.count;
     char* lbase = pl.base + int64_t(layer) * pl.layer_stride;
@@ -1159,7 +1159,7 @@ __device__ __forceinline__ void paged_move_block(const KPagedParams& P, const Pl
     if (int64_t(tb) >= int64_t(P.n_rows) * pl.tpr) return;            // past this plane
     const int32_t t = tb + int32_t(threadIdx.x);
     int32_t i, u;
-    row_unit(pl, t, P.n_rows, i, u);
+    row_unit(pl, true, t, P.n_rows, i, u);
     KRowMove e{KROW_SKIP, 0, 0, 0, -1, -1};
     if (i < P.n_rows) e = INLINE ? row_entry(P, V, i) : P.rows[i];
     const bool active = e.src_page != KROW_SKIP;

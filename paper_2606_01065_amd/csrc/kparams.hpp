@@ -71,12 +71,13 @@ struct KPlane {
 #ifndef LEYLINE_PAIR_F64
 #define LEYLINE_PAIR_F64 0
 #endif
-// The round and gather kernels lay the band chunks of narrow interleaved bands (MLA K_pe) out
-// in wavefronts of their own, so that the other wavefronts carry no pair arithmetic: with fp64
-// pairs the 32K MLA splice 74.3% -> 78.4% of peak; with fp32 pairs 79.2% -> 78.8%, so only the
-// fp64 build does it.
-#ifndef LEYLINE_BAND_PACK
-#define LEYLINE_BAND_PACK LEYLINE_PAIR_F64
+// The gather kernel, and with fp64 pairs the round kernel too, lay the band chunks of narrow
+// interleaved bands (MLA K_pe) out in wavefronts of their own, so that the other wavefronts carry
+// no pair arithmetic (KPlane::pack_groups).  Round kernel, 32K MLA splice: fp64 pairs 74.3% ->
+// 78.4% of peak, fp32 pairs 79.2% -> 78.8%, so the fp32 build keeps its rows end to end there;
+// fp32 gathers gain 0.6-2.3 points.
+#ifndef LEYLINE_ROUND_PACK
+#define LEYLINE_ROUND_PACK LEYLINE_PAIR_F64
 #endif
 
 #if LEYLINE_PAIR_F64
@@ -446,11 +447,11 @@ LEYLINE_HD inline int32_t kdiv(int32_t n, KDiv d) {
 }
 
 // Unit t of a row kernel's item (row groups of a few rows laid end to end, one chunk per unit):
-// its row group g and chunk u (u < tpr for every t, also past the item's last group).  With
-// pack_groups = B, units come in blocks of B row groups: first the band chunks of the block's
+// its row group g and chunk u (u < tpr for every t, also past the item's last group).  With pack
+// and pack_groups = B, units come in blocks of B row groups: first the band chunks of the block's
 // groups (rot_chunks each), then each group's other chunks in order.
-LEYLINE_HD inline void row_unit(const KPlane& pl, int32_t t, int64_t groups, int32_t& g, int32_t& u) {
-    if (pl.pack_groups) {
+LEYLINE_HD inline void row_unit(const KPlane& pl, bool pack, int32_t t, int64_t groups, int32_t& g, int32_t& u) {
+    if (pack && pl.pack_groups) {
         const int32_t B = pl.pack_groups, nb = pl.rot_chunks;
         const int32_t blk = kdiv(t, pl.pack_div);
         const int32_t w = t - blk * B * pl.tpr;

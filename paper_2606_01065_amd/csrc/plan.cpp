@@ -109,7 +109,6 @@ int describe_cache(const leyline_cache* cache, bool paged, KPlane out[LEYLINE_MA
             k.band_tpr = (neox && !(k.rot_chunks <= 64 && !(k.rot_chunks & (k.rot_chunks - 1))))
                              ? k.rot_chunks / 2 : k.rot_chunks;
             k.rot_tpr = k.n_heads * k.band_tpr;
-#if LEYLINE_BAND_PACK
             // band chunks of 64 / rot_chunks row groups make one wavefront, the rest whole ones
             const int32_t nb = k.rot_chunks;
             if (k.rot == KROT_INTERLEAVED && k.n_heads == 1 && !k.band_wide && nb >= 1 && nb <= 64 &&
@@ -120,7 +119,6 @@ int describe_cache(const leyline_cache* cache, bool paged, KPlane out[LEYLINE_MA
                 k.pack_div = make_div(k.pack_groups * k.tpr);
                 k.rest_div = make_div(k.tpr - nb);
             }
-#endif
         }
         k.units_all = k.rot == KROT_NEOX ? k.row_chunks - k.n_heads * (k.rot_chunks / 2) : k.row_chunks;
         k.tpr_div = make_div(k.tpr);

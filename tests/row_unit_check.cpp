@@ -66,7 +66,7 @@ int main() {
             const int64_t valid = groups * p.tpr;
             for (int32_t t = 0; t < int32_t(valid + 1024); ++t) {
                 int32_t g, u;
-                row_unit(p, t, groups, g, u);
+                row_unit(p, true, t, groups, g, u);
                 if (u < 0 || u >= p.tpr) return fail("chunk outside the row", i, groups, t);
                 if (t < valid) {
                     if (g < 0 || g >= groups) return fail("valid unit names no group of the item", i, groups, t);
@@ -82,7 +82,7 @@ int main() {
                     int band = 0;
                     for (int32_t t = w0; t < w0 + 64; ++t) {
                         int32_t g, u;
-                        row_unit(p, t, groups, g, u);
+                        row_unit(p, true, t, groups, g, u);
                         band += (u >= p.rot_lo && u < p.rot_lo + p.rot_chunks) ? 1 : 0;
                     }
                     if (band != 0 && band != 64) return fail("wavefront mixes band and other chunks", i, groups, w0);
