@@ -615,7 +615,8 @@ __global__ __launch_bounds__(TPB) void contig_chain_kernel(const KContigParams P
 }
 
 // Ordered tiles: every job of a call whose moves are too short-shifted for rounds.  Each
-// (job, plane) item is cut into tiles of KTILE_CHUNKS chunks (counted from its first row) in
+// (job, plane) item is cut into tiles of tile_chunks chunks (KTILE_CHUNKS, or a whole number of
+// packed blocks for a packed item; counted from its first row) in
 // each layer.  Workgroups take tile tickets from a counter, in order; the items of a launch own
 // consecutive ticket ranges in dependency order, and within an item ticket t is tile
 // t mod n_tiles of its processing order (a left shift ascending, a right shift descending) in
@@ -655,9 +656,11 @@ struct TileCtx {
     int32_t it, layer, order, local;
     int32_t g0;              // this thread's first chunk of the tile
     int32_t total;           // chunks of the item in one layer
+    int32_t end;             // end of the tile's chunks
+    int32_t rows;            // rows of the item
     int32_t cs;              // first cos/sin entry (-1: copied unchanged)
     int32_t plane, flag0;
-    bool move;
+    bool move, pack;
 };
 
 __device__ __forceinline__ TileCtx tile_ctx(const KTileParams& P, int32_t ticket) {
@@ -676,22 +679,27 @@ __device__ __forceinline__ TileCtx tile_ctx(const KTileParams& P, int32_t ticket
     c.src = c.move ? lbase + I.src0 * pl.token_stride : I.stub + int64_t(c.layer) * I.count * pl.row_bytes;
     c.src_step = c.move ? pl.token_stride : pl.row_bytes;
     c.dst = lbase + I.dst0 * pl.token_stride;
-    c.g0 = q * KTILE_CHUNKS + int32_t(threadIdx.x);
+    c.g0 = q * I.tile_chunks + int32_t(threadIdx.x);
+    c.end = min(c.total, (q + 1) * I.tile_chunks);
+    c.rows = int32_t(I.count);
+    c.pack = LEYLINE_TILE_PACK && I.pack;
     c.cs = I.cs;
     c.plane = I.plane;
     c.flag0 = I.flag0;
     return c;
 }
 
-// Every slot loads (past the end of the range: the range's last chunk, which stays unused), so
-// that the loads are issued back to back without branches between them.
+// Every slot loads (past the end of the tile: the tile's last chunk, which stays unused), so
+// that the loads are issued back to back without branches between them.  A packed item's tiles
+// are whole packed blocks, so its units (row_unit) cover the same rows as in plain order.
 __device__ __forceinline__ void tile_load(const KTileParams& P, const TileCtx& c, u32x4 (&v)[KTILE_CPT]) {
     const KPlane& pl = P.planes[c.plane];
 #pragma unroll
     for (int i = 0; i < KTILE_CPT; ++i) {
-        const int32_t gc = min(c.g0 + i * KTILE_TPB, c.total - 1);
-        const int32_t r = fdiv(gc, pl.tpr_div);
-        v[i] = ld16(c.src + int64_t(r) * c.src_step + int64_t(gc - r * pl.tpr) * 16);
+        const int32_t gc = min(c.g0 + i * KTILE_TPB, c.end - 1);
+        int32_t r, u;
+        row_unit(pl, c.pack, gc, c.rows, r, u);
+        v[i] = ld16(c.src + int64_t(r) * c.src_step + int64_t(u) * 16);
     }
 }
 
@@ -702,8 +710,9 @@ __device__ __forceinline__ void tile_store(const KTileParams& P, const TileCtx& 
 #pragma unroll
     for (int i = 0; i < KTILE_CPT; ++i) {
         const int32_t g = c.g0 + i * KTILE_TPB;
-        if (g < c.total) {
-            const int32_t r = fdiv(g, pl.tpr_div), u = g - r * pl.tpr;
+        if (g < c.end) {
+            int32_t r, u;
+            row_unit(pl, c.pack, g, c.rows, r, u);
             if (c.cs >= 0) rotate_chunk<ESZ, ROT>(pl, v[i], u, lcs, 0);
             st16(c.dst + int64_t(r) * pl.token_stride + int64_t(u) * 16, v[i]);
         }

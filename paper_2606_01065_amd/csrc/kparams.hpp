@@ -79,6 +79,10 @@ struct KPlane {
 #ifndef LEYLINE_ROUND_PACK
 #define LEYLINE_ROUND_PACK LEYLINE_PAIR_F64
 #endif
+// The same in the ordered-tile kernel, whose packed items use tiles of whole packed blocks.
+#ifndef LEYLINE_TILE_PACK
+#define LEYLINE_TILE_PACK LEYLINE_PAIR_F64
+#endif
 
 #if LEYLINE_PAIR_F64
 typedef double kcs_t;
@@ -178,6 +182,8 @@ struct KTileItem {
                              // processing order) at layer * n_tiles + tile; replacement: -1
     uint32_t waits;          // bit a: item a of the launch, an earlier move of the same plane,
                              // reads rows this item writes
+    int32_t tile_chunks;     // chunks per tile: KTILE_CHUNKS, or a whole number of packed blocks
+    int32_t pack;            // 1: units laid out by row_unit with packed bands (tiles of whole rows)
     int32_t pad;
 };
 
@@ -246,7 +252,8 @@ LEYLINE_HD inline void tile_wait_flags(const KTileParams& P, int32_t it, int32_t
     const int64_t q = down ? order : I.n_tiles - 1 - order;
     if (I.kind == KJOB_TILE) {
         const int64_t M = (down ? -I.delta : I.delta) * tpr;
-        for (int64_t d = M / KTILE_CHUNKS; d <= (M + KTILE_CHUNKS - 1) / KTILE_CHUNKS; ++d) {
+        const int64_t T = I.tile_chunks;
+        for (int64_t d = M / T; d <= (M + T - 1) / T; ++d) {
             const int64_t j = order - d;
             if (d == 0 || j < 0) continue;
             f(I.flag0 + int64_t(layer) * I.n_tiles + j);
@@ -254,8 +261,8 @@ LEYLINE_HD inline void tile_wait_flags(const KTileParams& P, int32_t it, int32_t
     }
     uint32_t w = I.waits;
     if (!w) return;
-    const int64_t c_hi = kmin64((q + 1) * KTILE_CHUNKS, I.count * tpr);
-    const int64_t lo = I.dst0 + q * KTILE_CHUNKS / tpr;                 // destination rows [lo, hi)
+    const int64_t c_hi = kmin64((q + 1) * I.tile_chunks, I.count * tpr);
+    const int64_t lo = I.dst0 + q * I.tile_chunks / tpr;                // destination rows [lo, hi)
     const int64_t hi = I.dst0 + (c_hi - 1) / tpr + 1;
     while (w) {
         const int a = __builtin_ctz(w);
@@ -263,8 +270,8 @@ LEYLINE_HD inline void tile_wait_flags(const KTileParams& P, int32_t it, int32_t
         const KTileItem& A = P.items[a];
         const int64_t x0 = kmax64(lo, A.src0), x1 = kmin64(hi, A.src0 + A.count);
         if (x0 >= x1) continue;
-        const int64_t t0 = (x0 - A.src0) * tpr / KTILE_CHUNKS;
-        const int64_t t1 = ((x1 - A.src0) * tpr - 1) / KTILE_CHUNKS;
+        const int64_t t0 = (x0 - A.src0) * tpr / A.tile_chunks;
+        const int64_t t1 = ((x1 - A.src0) * tpr - 1) / A.tile_chunks;
         for (int64_t t = t0; t <= t1; ++t) {
             const int64_t o = A.delta < 0 ? t : A.n_tiles - 1 - t;     // A's processing order
             f(A.flag0 + int64_t(layer) * A.n_tiles + o);

@@ -204,8 +204,8 @@ int resolve_forget(const leyline_directive* dirs, int32_t n_dirs, int32_t n_seqs
 
 // ------------------------------------------------------------------------------ contiguous --
 
-int64_t tile_count(int64_t rows, int32_t tpr) {
-    return (rows * tpr + KTILE_CHUNKS - 1) / KTILE_CHUNKS;
+int64_t tile_count(int64_t rows, int32_t tpr, int32_t tile_chunks) {
+    return (rows * tpr + tile_chunks - 1) / tile_chunks;
 }
 
 namespace {
@@ -260,7 +260,14 @@ int plan_tiles(const leyline_cache* cache, const leyline_directive* dirs, const 
                 it.stub = static_cast<const char*>(dirs[x.dir].stub[p]);
                 it.cs = -1;
             }
-            const int64_t tiles = tile_count(x.count, planes[p].tpr);
+            // rotating narrow interleaved bands: tiles of whole packed blocks, units packed
+            it.tile_chunks = KTILE_CHUNKS;
+            const int32_t blk = planes[p].pack_groups * planes[p].tpr;
+            if (LEYLINE_TILE_PACK && move && it.cs >= 0 && planes[p].pack_groups && blk <= KTILE_CHUNKS) {
+                it.tile_chunks = (KTILE_CHUNKS / blk) * blk;
+                it.pack = 1;
+            }
+            const int64_t tiles = tile_count(x.count, planes[p].tpr, it.tile_chunks);
             const int64_t tickets = int64_t(cache->n_layers) * tiles;
             it.n_tiles = int32_t(tiles);
             it.ticket0 = int32_t(cur.tickets);

@@ -76,7 +76,7 @@ struct ContigSchedule {
 };
 
 // Tiles of one ordered-tile move on a plane with `tpr` chunks per row.
-int64_t tile_count(int64_t rows, int32_t tpr);
+int64_t tile_count(int64_t rows, int32_t tpr, int32_t tile_chunks);
 
 int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_directive* dirs,
                 int32_t n_dirs, ContigSchedule* out);

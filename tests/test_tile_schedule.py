@@ -19,17 +19,28 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2606_01065_amd", "csrc")
 
 
-@pytest.fixture(scope="module")
-def sim(tmp_path_factory):
+def _build(tmp_path_factory, name, defines):
     gxx = shutil.which("g++")
     if gxx is None:
         pytest.skip("g++ not available")
-    exe = str(tmp_path_factory.mktemp("tile_sim") / "tile_schedule_sim")
-    subprocess.run([gxx, "-O2", "-std=c++17", "-Wall", "-Wextra", "-Werror",
-                    "-I" + os.path.join(ROOT, "include"), "-I" + CSRC,
-                    os.path.join(ROOT, "tests", "tile_schedule_sim.cpp"), os.path.join(CSRC, "plan.cpp"),
-                    "-o", exe], check=True)
+    exe = str(tmp_path_factory.mktemp(name) / "tile_schedule_sim")
+    subprocess.run([gxx, "-O2", "-std=c++17", "-Wall", "-Wextra", "-Werror"] + defines
+                   + ["-I" + os.path.join(ROOT, "include"), "-I" + CSRC,
+                      os.path.join(ROOT, "tests", "tile_schedule_sim.cpp"), os.path.join(CSRC, "plan.cpp"),
+                      "-o", exe], check=True)
     return exe
+
+
+@pytest.fixture(scope="module")
+def sim(tmp_path_factory):
+    return _build(tmp_path_factory, "tile_sim", [])
+
+
+@pytest.fixture(scope="module")
+def sim_packed(tmp_path_factory):
+    """The planner and unit layout of the fp64-pair build, whose tile launches pack narrow
+    interleaved bands (MLA K_pe) and cut those items into tiles of whole packed blocks."""
+    return _build(tmp_path_factory, "tile_sim_packed", ["-DLEYLINE_PAIR_F64=1"])
 
 
 @pytest.mark.parametrize("seed", [11, 12, 13, 14])
@@ -62,3 +73,11 @@ def test_a_wait_that_cannot_end_gives_up_and_every_tile_exits(sim, persist):
     assert r.returncode == 0, r.stdout + r.stderr
     ok, cases, tiles, gave_up = r.stdout.split()
     assert ok == "ok" and int(cases) > 100 and int(gave_up) > 0
+
+
+@pytest.mark.parametrize("persist", [0, 1])
+def test_packed_tile_schedules_are_race_free_and_complete(sim_packed, persist):
+    r = subprocess.run([sim_packed, "17", "2500", "0", str(persist)], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stdout + r.stderr
+    ok, cases, tiles, gave_up = r.stdout.split()
+    assert ok == "ok" and int(cases) > 2000 and int(tiles) > 50000 and int(gave_up) == 0

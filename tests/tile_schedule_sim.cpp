@@ -180,8 +180,8 @@ int main(int argc, char** argv) {
                 const KTileItem& I = P.items[T.item];
                 const int64_t tpr = planes[I.plane].tpr, total = I.count * tpr;
                 const int64_t q = I.delta <= 0 ? T.order : I.n_tiles - 1 - T.order;
-                *g0 = q * KTILE_CHUNKS;
-                *g1 = std::min(total, *g0 + KTILE_CHUNKS);
+                *g0 = q * I.tile_chunks;
+                *g1 = std::min(total, *g0 + I.tile_chunks);
             };
             const bool persist = persist_mode == 1 || (persist_mode == 2 && uni(0, 1) == 1);
             std::vector<std::vector<int64_t>> buf(size_t(tl.tickets));
@@ -228,7 +228,9 @@ int main(int argc, char** argv) {
                 auto& b = buf[size_t(t)];
                 b.resize(size_t(g1 - g0));
                 for (int64_t g = g0; g < g1; ++g) {
-                    const int64_t r = g / tpr, c = g % tpr;
+                    int32_t r32, c32;             // the kernel's unit layout (packed or not)
+                    row_unit(planes[p], LEYLINE_TILE_PACK && I.pack, int32_t(g), I.count, r32, c32);
+                    const int64_t r = r32, c = c32;
                     if (I.kind == KJOB_TILE) {
                         const int64_t v = m[size_t((I.src0 + r) * tpr + c)];
                         if (v != orig_val(p, T.layer, I.src0 + r, c)) return 1;
@@ -258,7 +260,9 @@ int main(int argc, char** argv) {
                 chunks(T, &g0, &g1);
                 const auto& b = buf[size_t(t)];
                 for (int64_t g = g0; g < g1; ++g) {
-                    const int64_t r = g / tpr, c = g % tpr;
+                    int32_t r32, c32;             // the kernel's unit layout (packed or not)
+                    row_unit(planes[p], LEYLINE_TILE_PACK && I.pack, int32_t(g), I.count, r32, c32);
+                    const int64_t r = r32, c = c32;
                     m[size_t((I.dst0 + r) * tpr + c)] = b[size_t(g - g0)];
                 }
                 ++tiles_run;
