@@ -123,17 +123,35 @@ def angle_tables(plane: O.Plane, shifts: np.ndarray, dev):
     return cols(ia), cols(ib), torch.from_numpy(cs).to(dev), torch.from_numpy(sn).to(dev)
 
 
-def assert_pairs_turned(before: torch.Tensor, after: torch.Tensor, tables, dtype: str, what: str = "") -> None:
+def ulp_t(x: torch.Tensor, dtype: str) -> torch.Tensor:
+    """Device twin of the oracle's ulp(): the spacing of the storage dtype at |x| (fp64 tensor),
+    with zero and subnormals at the subnormal quantum."""
+    _, e = torch.frexp(x)
+    e = torch.where(x == 0, torch.full_like(e, -125), torch.clamp(e, min=-125))
+    return torch.ldexp(torch.ones_like(x), e - (8 if dtype == O.BF16 else 24))
+
+
+def assert_bands_rotated(before: torch.Tensor, after: torch.Tensor, tables, dtype: str, what: str = "") -> None:
     """before/after: rotary selections [rows, n_rot] of moved rows (device, storage dtype).  Every
-    pair p must have turned by its angle: p.p' = |p|^2 cos(phi) and p x p' = |p|^2 sin(phi),
-    within storage rounding (2^-7 |p|^2 for bf16, 1e-5 |p|^2 for fp32)."""
+    member of every pair must lie within 1.5 storage ulps of the exact rotation of its stored input
+    (fp64 products with the oracle's cos/sin of the pair's angle, `tables`), or within
+    2e-6 |pair| + 0.5 ulp where the pair nearly cancels.  An output within the oracle's bar (1 ulp
+    of the oracle's rounded value, or 2e-6 |pair|; assert_rows_match) always passes: the rounded
+    value lies within half an ulp of the exact one, and the ulp is taken of |exact| (1 + 2^-7) so
+    that a value rounded up into the next binade is covered."""
     ia, ib, cs, sn = tables
     bm, gm = before.double(), after.double()
-    a, b, a2, b2 = bm[:, ia], bm[:, ib], gm[:, ia], gm[:, ib]
-    n2 = a * a + b * b
-    tol = (2.0 ** -7 if dtype == O.BF16 else 1e-5) * n2 + 1e-30
-    assert bool(((a * a2 + b * b2 - n2 * cs).abs() <= tol).all()), f"{what}: pair angles (cos)"
-    assert bool(((a * b2 - b * a2 - n2 * sn).abs() <= tol).all()), f"{what}: pair angles (sin)"
+    a, b = bm[:, ia], bm[:, ib]
+    norm = torch.sqrt(a * a + b * b)
+    for name, want, got in (("first", a * cs - b * sn, gm[:, ia]), ("second", a * sn + b * cs, gm[:, ib])):
+        u = ulp_t(want.abs() * (1.0 + 2.0 ** -7), dtype)
+        tol = torch.maximum(1.5 * u, F32_PAIR_RTOL * norm + 0.5 * u)
+        err = (got - want).abs()
+        ok = err <= tol
+        if not bool(ok.all()):
+            bad = torch.nonzero(~ok)[:5].tolist()
+            raise AssertionError(f"{what}: {name} pair members beyond 1.5 ulp of the exact rotation at {bad} "
+                                 f"({int((~ok).sum())} total, max err/tol {float((err / tol).max()):.3g})")
 
 
 def bits(t: torch.Tensor) -> torch.Tensor:

@@ -105,7 +105,7 @@ def _check_every_layer(wl, before, after, stubs, n, odirs, new_len, label):
             if plane.rot_dim:
                 gr, sr = g[:, rot], s0[:, rot]
                 assert torch.equal(PU.bits(gr[~moved]), PU.bits(sr[~moved])), f"{what}: shift-0 rows"
-                PU.assert_pairs_turned(sr[moved], gr[moved], tables, wl.dtype, what)
+                PU.assert_bands_rotated(sr[moved], gr[moved], tables, wl.dtype, what)
     print(f"[info] {label}: every layer checked by properties ({new_len} rows x {wl.n_layers} layers)",
           flush=True)
 
@@ -340,8 +340,8 @@ def test_rotate_delta(L, kind, dtype, paged):
 @pytest.mark.parametrize("name", ["mla_dsv3_rotate_32k", "gqa_llama3_8b_rotate_16k"])
 def test_rotate_delta_full_size(L, name):
     """Re-anchoring in place at full size (the benchmark's rotate-only workloads): three whole
-    layers against the oracle; every layer by properties (listed rows' pairs turned by their
-    angle, every other element bit-identical)."""
+    layers against the oracle; every layer by properties (each member of the listed rows' pairs
+    within 1.5 ulps of the exact rotation of its input, every other element bit-identical)."""
     wl = W.WORKLOADS[name]()
     delta, row0, n = wl.rotate
     planes_dev, _ = W.alloc_contig(wl, DEV)
@@ -372,14 +372,15 @@ def test_rotate_delta_full_size(L, name):
             assert torch.equal(PU.bits(gl[:row0]), PU.bits(bl[:row0])), f"{what}: rows before"
             assert torch.equal(PU.bits(gl[row0 + n:]), PU.bits(bl[row0 + n:])), f"{what}: rows after"
             if plane.rot_dim:
-                PU.assert_pairs_turned(bl[rows][:, rot], gl[rows][:, rot], tables, wl.dtype, what)
+                PU.assert_bands_rotated(bl[rows][:, rot], gl[rows][:, rot], tables, wl.dtype, what)
 
 
 def test_rotate_delta_token_slots_full_size(L):
     """Re-anchoring in place on a token-slot cache at full size (the paper's own kernel operation:
     the K_pe bands of the 32K MLA splice's downstream slots, listed by physical slot, rotated
     where they are): three whole layers of the pool against the oracle; every layer by
-    properties (listed slots' pairs turned by their angle, every other element bit-identical)."""
+    properties (each member of the listed slots' pairs within 1.5 ulps of the exact rotation of
+    its input, every other element bit-identical)."""
     wl = W.WORKLOADS["mla_dsv3_slots_rotate_32k"]()
     delta, row0, n = wl.rotate
     pools, bt, _, _ = W.alloc_paged(wl, DEV)
@@ -411,7 +412,7 @@ def test_rotate_delta_token_slots_full_size(L):
         gl, bl = af[layer], b4[layer]
         assert torch.equal(PU.bits(gl[:, ~rot]), PU.bits(bl[:, ~rot])), f"{what}: non-rotary"
         assert torch.equal(PU.bits(gl[~listed]), PU.bits(bl[~listed])), f"{what}: slots not listed"
-        PU.assert_pairs_turned(bl[slots][:, rot], gl[slots][:, rot], tables, wl.dtype, what)
+        PU.assert_bands_rotated(bl[slots][:, rot], gl[slots][:, rot], tables, wl.dtype, what)
 
 
 def test_rotate_delta_flags_bad_rows(L):

@@ -10,7 +10,7 @@ import torch
 
 import workloads as W
 from oracle import splice_oracle as O
-from tests.parity_util import (angle_tables, assert_pairs_turned, assert_rows_match, bits, host,
+from tests.parity_util import (angle_tables, assert_bands_rotated, assert_rows_match, bits, host,
                                oracle_plane, rotary_mask)
 
 pytestmark = pytest.mark.gpu
@@ -313,9 +313,10 @@ def _sample_positions(rng, wl, b, new_len, extra=24):
 class _EveryRow:
     """Checks every row of every sequence, plane and layer at full size by properties:
     non-rotary elements equal their source row's bit for bit, replacement rows equal the
-    replacement bit for bit, rows with shift 0 are bit-identical, and every rotary pair p of a
-    moved row has turned by its angle phi (p.p' = |p|^2 cos phi, p x p' = |p|^2 sin phi, within
-    storage rounding), with cos phi and sin phi taken from the oracle once per distinct shift.
+    replacement bit for bit, rows with shift 0 are bit-identical, and every member of every
+    rotary pair of a moved row lies within 1.5 ulps of the exact rotation of its stored input by
+    its angle phi (assert_bands_rotated: fp64 products with cos phi and sin phi taken from the
+    oracle once per distinct shift; implied by the oracle bar of assert_rows_match).
     In three whole layers (first, middle, last) every row's rotary bands are also compared
     element by element with the oracle's rotation of its source bands (Eq. "rotate"), at the
     parity bar of assert_rows_match.
@@ -383,7 +384,7 @@ class _EveryRow:
                     continue
                 g, b0 = got[:, rot], self.before[pi][layer]
                 assert torch.equal(bits(g[~moved]), bits(b0[~moved])), f"plane {pi} layer {layer}: shift-0 rows"
-                assert_pairs_turned(b0[moved], g[moved], self.angles[pi], wl.dtype, f"plane {pi} layer {layer}")
+                assert_bands_rotated(b0[moved], g[moved], self.angles[pi], wl.dtype, f"plane {pi} layer {layer}")
                 if layer in oracle_layers:
                     self._against_oracle(plane, host(b0), host(g), f"plane {pi} layer {layer}", exact)
             rows += len(self.a_old) + len(self.q_stub)
