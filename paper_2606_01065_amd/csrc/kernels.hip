@@ -63,7 +63,12 @@ constexpr int TPB = LEYLINE_TPB;
 #ifndef LEYLINE_MOVE_TPB
 #define LEYLINE_MOVE_TPB 256
 #endif
-constexpr int CRPT = LEYLINE_CONTIG_RPT;   // rows per thread of the round / stub kernel
+constexpr int CRPT = LEYLINE_CONTIG_RPT;   // rows per thread of a rotating round item
+// Rows per thread of a round-kernel item: CRPT when it rotates; with fp32 pairs one when it only
+// copies (a V plane, a replacement copy), with fp64 pairs CRPT as well (there the rotating
+// workgroups are bound by their pair arithmetic, and the GQA splice runs 4 points slower with
+// one-row copies beside them).  The kernel and the launcher's grid both take it from here.
+LEYLINE_HD inline int round_rows_per_thread(bool rotates) { return rotates || LEYLINE_PAIR_F64 ? CRPT : 1; }
 constexpr int MOVE_TPB = LEYLINE_MOVE_TPB; // its workgroup size
 #ifndef LEYLINE_PAGED_TPB
 #define LEYLINE_PAGED_TPB 256
@@ -471,13 +476,19 @@ __device__ __forceinline__ void cs_commit(KCosSin* lcs, const CsReg& c, int32_t 
 
 // --------------------------------------------------------------------- contiguous splice ---
 
-// Rounds and replacement copies: rows laid end to end, one unit per thread for CRPT rows (the
-// same column of consecutive rows, so one cos/sin lookup serves them all); the (job, plane) items
-// of a launch own consecutive ranges of workgroups (blockIdx.x), so a small item (a replacement
-// copy) next to a round adds only its own workgroups.  A rotating item's workgroup stages its cos/sin block in LDS after the
+// Rounds and replacement copies: rows laid end to end, one unit per thread for CRPT rows of a
+// rotating item (the same column of consecutive rows, so one cos/sin lookup serves them all) and
+// for one row of an item that only copies; the (job, plane) items of a launch own consecutive
+// ranges of workgroups (blockIdx.x), so a small item (a replacement copy) next to a round adds only
+// its own workgroups.  A rotating item's workgroup stages its cos/sin block in LDS after the
 // threads have issued their data loads, so that the two latencies overlap.  Past the item's last
 // row a thread loads that last row again (every load issued without branching) and stores
 // nothing.
+//
+// Rows per thread: a plain copy runs at the rate of a bare copy with one row per thread (two rows
+// per thread, with twice the bytes in flight per workgroup, are slower in bare copies of both
+// workloads' geometries), while a rotating row's pair arithmetic between its load and its store
+// lengthens each workgroup's life, which the second row amortises.
 template <int ESZ>
 __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigParams P) {
     constexpr int EPC = Elt<ESZ>::EPC;
@@ -486,21 +497,27 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
     // The item as a value: its fields come in one level of independent scalar loads (through a
     // reference the compiler loaded them one by one between the branches below).
     // the item whose range holds this workgroup: the number of later items starting at or before
-    // it (independent reads, no loop-carried dependency)
-    int32_t it = 0;
+    // it, and that item's first workgroup, selected from the same reads (independent reads, no
+    // loop-carried dependency, no second load through the item index)
+    int32_t it = 0, b0 = P.block0[0];
 #pragma unroll
-    for (int i = 1; i < KMAX_LAUNCH_ITEMS; ++i) it += int32_t(blockIdx.x) >= P.block0[i] ? 1 : 0;
+    for (int i = 1; i < KMAX_LAUNCH_ITEMS; ++i) {
+        const bool ge = int32_t(blockIdx.x) >= P.block0[i];
+        it += ge ? 1 : 0;
+        b0 = ge ? P.block0[i] : b0;
+    }
     KItem I;
     __builtin_memcpy(&I, &P.items[it], sizeof(KItem));
-    const int32_t bx = int32_t(blockIdx.x) - P.block0[it];
+    const int32_t bx = int32_t(blockIdx.x) - b0;
     const KPlane& pl = I.pl;
-    const int64_t groups = (I.count + CRPT - 1) / CRPT;
+    const int rpt = round_rows_per_thread(I.cs >= 0);                      // block-uniform
+    const int64_t groups = rpt == 1 ? I.count : (I.count + CRPT - 1) / CRPT;
     if (int64_t(bx) * MOVE_TPB >= groups * pl.tpr) return;               // block past this item's rows
     const int layer = blockIdx.y;
     const int32_t t = bx * MOVE_TPB + int32_t(threadIdx.x);
     int32_t g, u;
     row_unit(pl, LEYLINE_ROUND_PACK, t, groups, g, u);
-    const int64_t r0 = int64_t(g) * CRPT;
+    const int64_t r0 = int64_t(g) * rpt;
     const bool active = r0 < I.count;
     char* lbase = pl.base + int64_t(layer) * pl.layer_stride;
     const bool stub = I.kind == KJOB_STUB;
@@ -515,7 +532,7 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
             __syncthreads();
         }
         if (!active) return;
-        for (int k = 0; k < CRPT; ++k) {
+        for (int k = 0; k < rpt; ++k) {
             const int64_t r = r0 + k;
             if (r < I.count)
                 move_row_unit<ESZ>(pl, src + r * src_step, dst + r * pl.token_stride, u, lcs, rot ? 0 : -1);
@@ -531,8 +548,10 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
     u32x4 v[CRPT];
 #pragma unroll
     for (int k = 0; k < CRPT; ++k) {
-        const int64_t r = min(r0 + k, I.count - 1);
-        v[k] = ld16(src + r * src_step + off);
+        if (k == 0 || k < rpt) {
+            const int64_t r = min(r0 + k, I.count - 1);
+            v[k] = ld16(src + r * src_step + off);
+        }
     }
     if (rot) {
         if (early) cs_commit(lcs, c, pl.n_pairs);
@@ -545,7 +564,7 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
     const bool in_band = rot && h < pl.n_heads && j >= 0 && j < pl.rot_chunks;
 #pragma unroll
     for (int k = 0; k < CRPT; ++k) {
-        if (r0 + k < I.count) {
+        if ((k == 0 || k < rpt) && r0 + k < I.count) {
             if (in_band) {
                 if (pl.rot == KROT_INTERLEAVED) {
                     rot_interleaved<ESZ>(v[k], lcs, j * (EPC / 2));
@@ -1508,16 +1527,21 @@ static int splice_contig_planned(const leyline_cache* cache, const ContigSchedul
         if (new_len_out) *new_len_out = sched.new_len;
         return LEYLINE_OK;
     }
-    // threads of one (job, plane) item; every count must fit a 31-bit index
+    // whether a (job, plane) item rotates (it then gets a cos/sin block: KItem::cs >= 0), and its
+    // threads; every count must fit a 31-bit index
+    const int32_t cs_need = cos_sin_per_shift(cache);
+    auto item_rotates = [&](const ContigJobHost& j, int p) {
+        return j.kind != KJOB_STUB && cs_need > 0 && planes[p].rot != KROT_NONE;
+    };
     auto item_threads = [&](const ContigJobHost& j, int p) -> int64_t {
         if (j.kind == KJOB_CHAIN) return std::min<int64_t>(j.count, abs64(j.delta)) * planes[p].units_all;
-        return (j.count + CRPT - 1) / CRPT * planes[p].tpr;
+        const int rpt = round_rows_per_thread(item_rotates(j, p));
+        return (j.count + rpt - 1) / rpt * planes[p].tpr;
     };
     for (const auto& jobs : sched.launches)
         for (const auto& j : jobs)
             for (int p = 0; p < n_planes; ++p)
                 if (item_threads(j, p) > INT32_MAX - TPB) return LEYLINE_E_INVAL;
-    const int32_t cs_need = cos_sin_per_shift(cache);
     for (const auto& group : sched.launches) {
         // the jobs of a group are independent; replacement copies, chains and rounds go to
         // separate launches, each a list of (job, plane) items selected by blockIdx.z
@@ -1569,7 +1593,7 @@ static int splice_contig_planned(const leyline_cache* cache, const ContigSchedul
                     it.delta = j.delta;
                     it.kind = j.kind;
                     it.chains = int32_t(kind == KJOB_CHAIN ? std::min<int64_t>(j.count, abs64(j.delta)) : 0);
-                    it.cs = (cs0 >= 0 && planes[p].rot != KROT_NONE) ? cs0 + planes[p].cs_off : -1;
+                    it.cs = item_rotates(j, p) ? cs0 + planes[p].cs_off : -1;
                     if (j.kind == KJOB_STUB) it.stub = static_cast<const char*>(dirs[j.dir].stub[p]);
                     const int block = kind == KJOB_CHAIN ? TPB : MOVE_TPB;
                     const int64_t blocks = (th + block - 1) / block;
