@@ -982,44 +982,73 @@ __device__ __forceinline__ void resolve_freed_entry(const KPagedParams& P, const
 // from one compute unit cost about 5 us per 15,000.
 constexpr int ORDER_TPB = 1024;
 constexpr int ORDER_STAGE = 24576;
-__global__ __launch_bounds__(ORDER_TPB) void paged_order_kernel(const KPagedParams P) {
-    __shared__ int32_t cnt[KORDER_BUCKETS];
-    __shared__ int32_t part[ORDER_TPB];
-    __shared__ int32_t stage[ORDER_STAGE];
-    const int tid = int(threadIdx.x);
-    for (int i = tid; i < KORDER_BUCKETS; i += ORDER_TPB) cnt[i] = 0;
-    __syncthreads();
-    auto bucket = [&](int32_t t) {
-        const int32_t pg = t < P.n_free ? P.free_pages[t] : -1;
-        return (pg < 0 || pg >= P.capacity) ? 0 : (pg >> P.order_shift);
-    };
-    for (int32_t t = tid; t < P.n_asm; t += ORDER_TPB) atomicAdd(&cnt[bucket(t)], 1);
-    __syncthreads();
-    // exclusive scan: each thread owns KORDER_BUCKETS / ORDER_TPB consecutive buckets
+constexpr int ORDER_PER = ORDER_STAGE / ORDER_TPB;   // fresh ordinals a thread holds
+
+// The counts cnt[KORDER_BUCKETS] replaced by their exclusive prefix sums, by a workgroup of
+// ORDER_TPB threads: each thread sums its KORDER_BUCKETS / ORDER_TPB consecutive buckets, the
+// wavefronts scan those sums with lane shuffles, and one barrier exchanges the wavefront totals
+// (wsum: ORDER_TPB / 64 entries).  Ends with a barrier, so cnt is ready for every thread.
+__device__ __forceinline__ void bucket_offsets(int32_t* cnt, int32_t* wsum) {
     constexpr int PER = KORDER_BUCKETS / ORDER_TPB;
+    const int tid = int(threadIdx.x), lane = tid & 63, wave = tid >> 6;
     int32_t own[PER], sum = 0;
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
         own[k] = cnt[tid * PER + k];
         sum += own[k];
     }
-    part[tid] = sum;
-    __syncthreads();
-    for (int off = 1; off < ORDER_TPB; off <<= 1) {
-        const int32_t v = tid >= off ? part[tid - off] : 0;
-        __syncthreads();
-        part[tid] += v;
-        __syncthreads();
+    int32_t x = sum;                                   // inclusive scan within the wavefront
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int32_t y = __shfl_up(x, off, 64);
+        if (lane >= off) x += y;
     }
-    int32_t run = part[tid] - sum;
+    if (lane == 63) wsum[wave] = x;
+    __syncthreads();
+    int32_t run = x - sum;
+    for (int w = 0; w < wave; ++w) run += wsum[w];
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
         cnt[tid * PER + k] = run;
         run += own[k];
     }
     __syncthreads();
-    if (P.n_asm <= ORDER_STAGE) {
-        for (int32_t t = tid; t < P.n_asm; t += ORDER_TPB) stage[atomicAdd(&cnt[bucket(t)], 1)] = t;
+}
+__global__ __launch_bounds__(ORDER_TPB) void paged_order_kernel(const KPagedParams P) {
+    __shared__ int32_t cnt[KORDER_BUCKETS];
+    __shared__ int32_t part[ORDER_TPB / 64];
+    __shared__ int32_t stage[ORDER_STAGE];
+    const int tid = int(threadIdx.x);
+    for (int i = tid; i < KORDER_BUCKETS; i += ORDER_TPB) cnt[i] = 0;
+    auto bucket = [&](int32_t t) {
+        const int32_t pg = t < P.n_free ? P.free_pages[t] : -1;
+        return (pg < 0 || pg >= P.capacity) ? 0 : (pg >> P.order_shift);
+    };
+    // up to ORDER_STAGE ordinals: every thread's buckets loaded at once and kept for the scatter
+    const bool held = P.n_asm <= ORDER_STAGE;                     // block-uniform
+    int32_t b[ORDER_PER];
+    if (held) {
+#pragma unroll
+        for (int k = 0; k < ORDER_PER; ++k) {
+            const int32_t t = tid + k * ORDER_TPB;
+            b[k] = t < P.n_asm ? bucket(t) : -1;
+        }
+    }
+    __syncthreads();
+    if (held) {
+#pragma unroll
+        for (int k = 0; k < ORDER_PER; ++k)
+            if (b[k] >= 0) atomicAdd(&cnt[b[k]], 1);
+    } else {
+        for (int32_t t = tid; t < P.n_asm; t += ORDER_TPB) atomicAdd(&cnt[bucket(t)], 1);
+    }
+    __syncthreads();
+    // exclusive scan: each thread owns KORDER_BUCKETS / ORDER_TPB consecutive buckets
+    bucket_offsets(cnt, part);
+    if (held) {
+#pragma unroll
+        for (int k = 0; k < ORDER_PER; ++k)
+            if (b[k] >= 0) stage[atomicAdd(&cnt[b[k]], 1)] = tid + k * ORDER_TPB;
         __syncthreads();
         for (int32_t j = tid; j < P.n_asm; j += ORDER_TPB) P.order[j] = stage[j];
     } else {
@@ -1045,7 +1074,7 @@ constexpr int REMAP_SORT_PER = 16;
 
 __global__ __launch_bounds__(ORDER_TPB) void paged_remap_order_kernel(const KPagedParams P) {
     __shared__ int32_t cnt[KORDER_BUCKETS];
-    __shared__ int32_t part[ORDER_TPB];
+    __shared__ int32_t part[ORDER_TPB / 64];
     __shared__ uint2 stage[ORDER_TPB * REMAP_SORT_PER];
     const PlanView V = plan_view(P);
     const int tid = int(threadIdx.x);
@@ -1069,28 +1098,7 @@ __global__ __launch_bounds__(ORDER_TPB) void paged_remap_order_kernel(const KPag
             atomicAdd(&cnt[remap_resolve(P, V, m).page >> P.remap_shift], 1);
     }
     __syncthreads();
-    constexpr int PER = KORDER_BUCKETS / ORDER_TPB;
-    int32_t own[PER], sum = 0;
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-        own[k] = cnt[tid * PER + k];
-        sum += own[k];
-    }
-    part[tid] = sum;
-    __syncthreads();
-    for (int off = 1; off < ORDER_TPB; off <<= 1) {
-        const int32_t v = tid >= off ? part[tid - off] : 0;
-        __syncthreads();
-        part[tid] += v;
-        __syncthreads();
-    }
-    int32_t run = part[tid] - sum;
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-        cnt[tid * PER + k] = run;
-        run += own[k];
-    }
-    __syncthreads();
+    bucket_offsets(cnt, part);
     if (held && P.remap_pack) {
 #pragma unroll
         for (int k = 0; k < REMAP_SORT_PER; ++k)
