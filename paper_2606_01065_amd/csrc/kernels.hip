@@ -12,11 +12,12 @@
 //
 // Access shape.  The 16-byte chunks of the moved rows are laid end to end over the threads, so
 // that every load and store instruction of a 64-wide wavefront covers about 1 KiB of whole rows
-// (a thread repeats its chunk position in a few rows or layers: two consecutive rows in the
-// round kernel, two layers in the paged kernels, eight strided chunks in a tile); that is the
-// shape that streams near the copy ceiling of the chip.  For a half-split (NEOX) band the partner half of a chunk lives in
-// another lane of the same wavefront and is exchanged with a lane shuffle instead of being
-// loaded twice.  Index arithmetic uses precomputed multiply-shift division.
+// (a thread repeats its chunk position in a few rows or layers: two consecutive rows of a
+// rotating round item and one row of a copy in the round kernel, two layers in the paged
+// kernels, eight strided chunks in a tile); that is the shape that streams near the copy ceiling
+// of the chip.  For a half-split (NEOX) band the partner half of a chunk lives in another lane of
+// the same wavefront and is exchanged with a lane shuffle instead of being loaded twice.  Index
+// arithmetic uses precomputed multiply-shift division.
 //
 // In-place contiguous compaction.  A segment moved left by m rows writes row x with the old
 // content of row x + m.  The host splits the segment into equal rounds of at most m rows taken
@@ -494,11 +495,11 @@ __global__ __launch_bounds__(MOVE_TPB) void contig_move_kernel(const KContigPara
     constexpr int EPC = Elt<ESZ>::EPC;
     static_assert(KMAX_CS <= MOVE_TPB, "one cos/sin entry per thread");
     __shared__ KCosSin lcs[KMAX_CS];
-    // The item as a value: its fields come in one level of independent scalar loads (through a
-    // reference the compiler loaded them one by one between the branches below).
-    // the item whose range holds this workgroup: the number of later items starting at or before
+    // The item whose range holds this workgroup: the number of later items starting at or before
     // it, and that item's first workgroup, selected from the same reads (independent reads, no
-    // loop-carried dependency, no second load through the item index)
+    // loop-carried dependency, no second load through the item index).  The item is then read as
+    // a value: its fields come in one level of independent scalar loads (through a reference the
+    // compiler loaded them one by one between the branches below).
     int32_t it = 0, b0 = P.block0[0];
 #pragma unroll
     for (int i = 1; i < KMAX_LAUNCH_ITEMS; ++i) {
@@ -874,15 +875,16 @@ __global__ __launch_bounds__(PAGED_TPB) void rotate_rows_kernel(const KRotatePar
 //
 // paged_data_kernel moves the data.  Its first blocks gather ASSEMBLE rows like the contiguous
 // kernel (rows laid end to end, one 16-byte chunk per thread, so a wavefront reads one row entry
-// and moves whole lines); the next blocks rotate the rotary bands of REMAP pages (re-used whole
-// pages) in place, each looking its pages up in the plan and the old block table.  The rows of a
-// small gather (token-slot splices: the replacement rows) are resolved by the gathering blocks
-// themselves and the new block tables and freed list are written by further blocks of the same
-// launch: one launch per call.  A large gather first runs paged_resolve_kernel, which expands the
-// page runs once for all layers and planes into a row table (for every row of every ASSEMBLE
-// page: which old physical page and row, or which replacement token, it comes from, which fresh
-// page it goes to, which shift re-anchors it) and writes the block tables and the freed list;
-// paged_order_kernel before it lays the row table out in destination-page order.
+// and moves whole lines); its last blocks rotate the rotary bands of REMAP pages (re-used whole
+// pages) in place, each looking its pages up in the plan and the old block table (or reading
+// them from paged_remap_order_kernel's physical-order list).  The rows of a small gather
+// (token-slot splices: the replacement rows) are resolved by the gathering blocks themselves, and
+// the new block tables and freed list are written by blocks between the two: one launch per call.
+// A large gather first runs paged_resolve_kernel, which expands the page runs once for all layers
+// and planes into a row table (for every row of every ASSEMBLE page: which old physical page and
+// row, or which replacement token, it comes from, which fresh page it goes to, which shift
+// re-anchors it) and writes the block tables and the freed list; paged_order_kernel before it
+// lays the row table out in destination-page order.
 // Nothing is written to an old page except the rotary bands of REMAP pages, which no ASSEMBLE
 // row reads.
 
