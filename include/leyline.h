@@ -275,7 +275,8 @@ int leyline_paged_plan(int32_t page_size, int32_t n_seqs, const int32_t* seq_len
  * Paged splice of a batch of sequences (all layers and planes), following the page plan above.
  *
  * cache->page_size > 0, cache->capacity = physical pages in the pool.
- * seq_lens: host [n_seqs].  block_table_in / block_table_out: device int32 [n_seqs][bt_stride];
+ * seq_lens: host [n_seqs].  block_table_in / block_table_out: device int32 [n_seqs][bt_stride]
+ * (bt_stride >= 0; 0 only when every sequence is and stays empty, and then the tables may be null);
  * on completion block_table_out holds every sequence's new table and -1 past its last page.
  * The old and new block tables, free_pages [n_free], freed_pages_out [freed_cap], the workspace
  * [workspace_bytes] and device_status [1] are read and written by the same launch: no two of

@@ -1780,14 +1780,16 @@ extern "C" int leyline_splice_paged(const leyline_cache* cache, int32_t n_seqs, 
     int n_planes = 0;
     int rc = describe_cache(cache, true, planes, &n_planes);
     if (rc) return rc;
-    if (bt_stride < 1 || n_free < 0 || freed_cap < 0 || workspace_bytes < 0) return LEYLINE_E_INVAL;
-    if (n_seqs > 0 && (!block_table_in || !block_table_out || block_table_in == block_table_out))
+    // bt_stride 0 (tables without columns) suits only sequences that stay empty, which the
+    // table-width check below enforces, as leyline_paged_query's does
+    if (bt_stride < 0 || n_free < 0 || freed_cap < 0 || workspace_bytes < 0) return LEYLINE_E_INVAL;
+    const int64_t bt_bytes = int64_t(n_seqs > 0 ? n_seqs : 0) * bt_stride * 4;
+    if (bt_bytes > 0 && (!block_table_in || !block_table_out || block_table_in == block_table_out))
         return LEYLINE_E_INVAL;
     if (flags & ~uint32_t(LEYLINE_PAGED_COPY_ON_WRITE)) return LEYLINE_E_INVAL;
     {
         // One launch reads the old tables and the free list while it writes the new tables, the
         // freed list, the workspace and the status word: no two of these may share a byte.
-        const int64_t bt_bytes = int64_t(n_seqs > 0 ? n_seqs : 0) * bt_stride * 4;
         const Span bufs[] = {{block_table_in, bt_bytes},    {block_table_out, bt_bytes},
                              {free_pages, int64_t(n_free) * 4}, {freed_pages_out, int64_t(freed_cap) * 4},
                              {workspace, workspace_bytes},  {device_status, 4}};

@@ -422,6 +422,28 @@ def test_paged_splice_validates_before_any_enqueue():
         assert e.value.code == L.E_INVAL, o
 
 
+def test_paged_splice_of_empty_sequences_with_empty_tables():
+    """A batch whose sequences are and stay empty needs block tables without columns
+    (bt_stride 0); the splice accepts what the query accepts, and with nothing to move, rotate or
+    write it returns the (empty) results without enqueueing anything."""
+    import torch
+    pool = _FakeTensor((2, 32, 48, 576), torch.bfloat16)
+    cache = L.make_cache([L.PlaneSpec(pool, 1, 576, 512, 64)], paged=True)
+    lens = [0, 0]
+    new, fresh, freed, ws_bytes = L.leyline_paged_query(cache, lens, 0, None, 0)
+    assert (new, fresh, freed) == ([0, 0], 0, 0)
+    bt_in = _FakeTensor((2, 0), torch.int32, ptr=0)                       # no columns, no memory
+    bt_out = _FakeTensor((2, 0), torch.int32, ptr=0)
+    free = _FakeTensor((4,), torch.int32, ptr=0x50000)
+    freed_out = _FakeTensor((1,), torch.int32, ptr=0x60000)
+    ws = _FakeTensor((max(256, ws_bytes),), torch.uint8, ptr=0x70000)
+    assert L.leyline_splice_paged(cache, lens, bt_in, bt_out, None, 0, free, freed_out, ws,
+                                  stream=0) == ([0, 0], 0, 0)
+    with pytest.raises(L.LeylineError) as e:                                # a page would be needed
+        L.leyline_splice_paged(cache, [1, 0], bt_in, bt_out, None, 0, free, freed_out, ws, stream=0)
+    assert e.value.code == L.E_CAPACITY
+
+
 def test_rotate_delta_validation():
     c = _mla_cache(cap=64)
     with pytest.raises(L.LeylineError) as e:
