@@ -22,7 +22,10 @@ What is computed, and where the paper defines it
 * Rotation arithmetic is carried out in higher precision than storage and rounded on the way
   back to the bf16 pool (Sec. 4.1 "bf16 K-storage precision floor"; App. "bf16 K-storage
   precision floor").  Here: float64 angles, float64 trig, float64 pair products, one
-  round-to-nearest-even to the storage dtype.
+  round-to-nearest-even to the storage dtype.  The frequencies, cosines and sines come from the
+  scalar functions of the platform's C math library (Python's ``math``), one value at a time:
+  numpy's vectorized ``power`` can differ from them in the last place, and a float64 result one
+  unit off can round to a different float32 when a pair nearly cancels.
 
 * A FORGET directive hands the edit to a prefix-trimmed re-prefill (Sec. 3.1, "The FORGET
   mode"): on the cache, the sequence is cut at the span's start after the earlier directives.
@@ -42,6 +45,8 @@ definition states.
 """
 
 from __future__ import annotations
+
+import math
 
 from dataclasses import dataclass, field
 from typing import List, Optional, Sequence, Tuple
@@ -129,9 +134,20 @@ def ulp(x64: np.ndarray, dtype: str) -> np.ndarray:
 # ----------------------------------------------------------------------------------------------
 
 def rope_frequencies(rot_dim: int, base: float) -> np.ndarray:
-    """theta_i = base ** (-2 i / d_rot), i in [0, d_rot/2)  (RoFormer schedule, Sec. 3.2)."""
-    i = np.arange(rot_dim // 2, dtype=np.float64)
-    return np.power(np.float64(base), -2.0 * i / rot_dim)
+    """theta_i = base ** (-2 i / d_rot), i in [0, d_rot/2)  (RoFormer schedule, Sec. 3.2), each
+    evaluated by the C math library's pow."""
+    return np.array([math.pow(float(base), -2.0 * i / rot_dim) for i in range(rot_dim // 2)],
+                    dtype=np.float64)
+
+
+def _cos_sin(phi: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """cos and sin of every angle, each evaluated by the C math library (once per distinct
+    angle)."""
+    phi = np.asarray(phi, dtype=np.float64)
+    u, inv = np.unique(phi, return_inverse=True)
+    c = np.array([math.cos(x) for x in u.tolist()], dtype=np.float64)
+    s = np.array([math.sin(x) for x in u.tolist()], dtype=np.float64)
+    return c[inv].reshape(phi.shape), s[inv].reshape(phi.shape)
 
 
 def pair_dims(rot_dim: int, style: int) -> Tuple[np.ndarray, np.ndarray]:
@@ -159,7 +175,7 @@ def rotate(band: np.ndarray, shift, freqs: np.ndarray, style: int) -> np.ndarray
     d_rot = band.shape[-1]
     ia, ib = pair_dims(d_rot, style)
     phi = np.asarray(shift, dtype=np.float64)[..., None] * freqs          # [..., d_rot/2]
-    c, s = np.cos(phi), np.sin(phi)
+    c, s = _cos_sin(phi)
     a, b = band[..., ia], band[..., ib]
     out = np.empty(np.broadcast_shapes(band.shape, phi.shape[:-1] + (d_rot,)), dtype=np.float64)
     out[..., ia] = a * c - b * s

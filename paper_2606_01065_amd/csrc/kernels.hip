@@ -120,9 +120,13 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
 // (a, b) -> (a c - b s, a s + b c) (Eq. "rotate").  BF16: the results are bf16-bound, and come back
 // as floats whose nearest-even bf16 is the stored value.  With fp64 pairs the products are fp64
 // and each result is rounded once (to odd for bf16, see f32_round_odd; to nearest-even for fp32).
+// fp64 pairs are computed without fused multiply-adds, as two rounded products and a rounded sum
+// (the plain evaluation of the formula): a fused form rounds differently in the last place, and
+// that can move a near-cancelling result across a rounding boundary of the storage type.
 template <bool BF16>
 __device__ __forceinline__ void rot_pair(float& a, float& b, const KCosSin& k) {
 #if LEYLINE_PAIR_F64
+#pragma clang fp contract(off)
     const double x = a, y = b;
     const double a2 = x * k.c - y * k.s;
     const double b2 = x * k.s + y * k.c;
@@ -141,6 +145,7 @@ __device__ __forceinline__ void rot_pair(float& a, float& b, const KCosSin& k) {
 template <bool BF16>
 __device__ __forceinline__ float rot_own(float mine, float partner, const KCosSin& k, bool lo) {
 #if LEYLINE_PAIR_F64
+#pragma clang fp contract(off)
     const double r = double(mine) * k.c + double(partner) * (lo ? -k.s : k.s);
     return BF16 ? f32_round_odd(r) : float(r);
 #else

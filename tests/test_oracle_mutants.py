@@ -21,7 +21,11 @@ MUTANTS = [
     ("rotate", "out[..., ib] = a * s + b * c", "out[..., ib] = a * s - b * c", "sign of the second component"),
     ("rotate", "out[..., ia] = a * c - b * s", "out[..., ia] = a * c + b * s", "sign of the first component"),
     ("rotate", "out[..., ia] = a * c - b * s", "out[..., ia] = a * c", "dropped cross term"),
-    ("rotate", "c, s = np.cos(phi), np.sin(phi)", "s, c = np.cos(phi), np.sin(phi)", "cos and sin swapped"),
+    ("rotate", "c, s = _cos_sin(phi)", "s, c = _cos_sin(phi)", "cos and sin swapped"),
+    ("_cos_sin", "s = np.array([math.sin(x) for x in u.tolist()], dtype=np.float64)",
+     "s = np.array([math.sin(-x) for x in u.tolist()], dtype=np.float64)", "sin of the negated angle"),
+    ("_cos_sin", "return c[inv].reshape(phi.shape), s[inv].reshape(phi.shape)",
+     "return c[inv[::-1]].reshape(phi.shape), s[inv].reshape(phi.shape)", "cos taken for other angles"),
     ("rotate", "a, b = band[..., ia], band[..., ib]", "b, a = band[..., ia], band[..., ib]", "pair operands transposed"),
     ("rotate", "[..., None] * freqs", "[..., None] * freqs[::-1]", "frequency index reversed"),
     # pairing convention (Sec. 3.3)
@@ -30,8 +34,8 @@ MUTANTS = [
     ("pair_dims", "return i, i + half", "return i + half, i", "half-split pair members swapped"),
     # frequency schedule
     ("rope_frequencies", "-2.0 * i / rot_dim", "-1.0 * i / rot_dim", "exponent missing its factor 2"),
-    ("rope_frequencies", "np.arange(rot_dim // 2, dtype=np.float64)",
-     "np.arange(1, rot_dim // 2 + 1, dtype=np.float64)", "frequency index off by one"),
+    ("rope_frequencies", "for i in range(rot_dim // 2)]",
+     "for i in range(1, rot_dim // 2 + 1)]", "frequency index off by one"),
     # the directive and its signed shift (Sec. 3.1)
     ("Directive", "return self.stub_len - (self.span_end - self.span_start)",
      "return (self.span_end - self.span_start) - self.stub_len", "sign of Delta"),
