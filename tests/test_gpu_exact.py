@@ -118,3 +118,36 @@ def test_paged_131k_full_is_bit_identical(L):
     """The 8-directive 131K-token paged splice at full size (gather through the row table, bands
     packed into wavefronts of their own, each XCD gathering its own eighth)."""
     _check_sampled(L, W.mla_dsv3_paged_131k(), seed=23, exact=True)
+
+
+@pytest.mark.parametrize("first", [20101, 20151])
+def test_random_sweep_is_bit_identical(L, first):
+    """The randomized sweep of test_gpu_random_sweep through the exact library, every element of
+    every compared row bit for bit; seed 20168 is an fp32 pair that nearly cancels, whose result
+    lies close to a float32 rounding boundary (it differed while the oracle's frequencies came from
+    numpy's vectorized power and the kernel fused its fp64 products)."""
+    from tests import test_gpu_contig as TC
+    from tests import test_gpu_random_sweep as RS
+    for seed in range(first, first + 50):
+        rng = random.Random(seed)
+        kind, dtype = RS.CONTIG_KINDS[seed % len(RS.CONTIG_KINDS)]
+        n = rng.choice([1, 5, 63, 64, 65, 300, 1000, 2047, 3000])
+        dirs = TC._random_dirs(rng, n, rng.randint(1, 8))
+        wl = TC._small_workload(rng, kind, dtype, rng.randint(1, 4), n, dirs, extra=rng.randint(0, 40))
+        print(f"[case] exact sweep contig seed {seed} {kind}/{dtype} n={n} dirs={dirs}", flush=True)
+        planes_dev, stubs_dev = W.alloc_contig(wl, DEV, seed=seed)
+        before = [host(t) for t in planes_dev]
+        stubs_h = [[host(s) for s in per] for per in stubs_dev]
+        cache = L.make_cache(TC._specs(L, wl, planes_dev))
+        new_len = L.leyline_splice_contig(cache, n, L.make_directives(TC._dir_dicts(wl, stubs_dev)), len(wl.dirs))
+        torch.cuda.synchronize()
+        odirs = [O.Directive(d.span_start, d.span_end, d.stub_len, mode=d.mode) for d in wl.dirs]
+        for pi, (desc, t) in enumerate(zip(wl.planes, planes_dev)):
+            plane = oracle_plane(desc)
+            shape = (wl.n_layers, wl.capacity, plane.row_elems)
+            stubs = [s[pi].reshape(wl.n_layers, s[pi].shape[1], plane.row_elems) for s in stubs_h]
+            want, n_want = O.splice_contig(before[pi].reshape(shape), n, odirs, stubs, plane, wl.dtype)
+            assert new_len == n_want
+            got = np.ascontiguousarray(host(t).reshape(shape)[:, :new_len])
+            want = np.ascontiguousarray(want[:, :new_len])
+            assert np.array_equal(got.view(np.uint8), want.view(np.uint8)), f"seed {seed} plane {pi}"
