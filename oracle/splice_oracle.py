@@ -140,14 +140,15 @@ def rope_frequencies(rot_dim: int, base: float) -> np.ndarray:
                     dtype=np.float64)
 
 
-def _cos_sin(phi: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
-    """cos and sin of every angle, each evaluated by the C math library (once per distinct
-    angle)."""
-    phi = np.asarray(phi, dtype=np.float64)
-    u, inv = np.unique(phi, return_inverse=True)
-    c = np.array([math.cos(x) for x in u.tolist()], dtype=np.float64)
-    s = np.array([math.sin(x) for x in u.tolist()], dtype=np.float64)
-    return c[inv].reshape(phi.shape), s[inv].reshape(phi.shape)
+def _cos_sin(shift, freqs: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """cos and sin of phi = shift * theta_i for every shift (scalar or array) and frequency:
+    [..., d_rot/2] each, every value evaluated by the C math library (once per distinct shift)."""
+    shift = np.asarray(shift, dtype=np.float64)
+    u, inv = np.unique(shift, return_inverse=True)
+    phi = u[:, None] * freqs                                              # [distinct shifts, d_rot/2]
+    c = np.array([[math.cos(x) for x in row] for row in phi.tolist()], dtype=np.float64).reshape(phi.shape)
+    s = np.array([[math.sin(x) for x in row] for row in phi.tolist()], dtype=np.float64).reshape(phi.shape)
+    return c[inv].reshape(shift.shape + freqs.shape), s[inv].reshape(shift.shape + freqs.shape)
 
 
 def pair_dims(rot_dim: int, style: int) -> Tuple[np.ndarray, np.ndarray]:
@@ -174,10 +175,9 @@ def rotate(band: np.ndarray, shift, freqs: np.ndarray, style: int) -> np.ndarray
     band = np.asarray(band, dtype=np.float64)
     d_rot = band.shape[-1]
     ia, ib = pair_dims(d_rot, style)
-    phi = np.asarray(shift, dtype=np.float64)[..., None] * freqs          # [..., d_rot/2]
-    c, s = _cos_sin(phi)
+    c, s = _cos_sin(shift, freqs)                                         # [..., d_rot/2]
     a, b = band[..., ia], band[..., ib]
-    out = np.empty(np.broadcast_shapes(band.shape, phi.shape[:-1] + (d_rot,)), dtype=np.float64)
+    out = np.empty(np.broadcast_shapes(band.shape, c.shape[:-1] + (d_rot,)), dtype=np.float64)
     out[..., ia] = a * c - b * s
     out[..., ib] = a * s + b * c
     return out

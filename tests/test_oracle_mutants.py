@@ -21,13 +21,14 @@ MUTANTS = [
     ("rotate", "out[..., ib] = a * s + b * c", "out[..., ib] = a * s - b * c", "sign of the second component"),
     ("rotate", "out[..., ia] = a * c - b * s", "out[..., ia] = a * c + b * s", "sign of the first component"),
     ("rotate", "out[..., ia] = a * c - b * s", "out[..., ia] = a * c", "dropped cross term"),
-    ("rotate", "c, s = _cos_sin(phi)", "s, c = _cos_sin(phi)", "cos and sin swapped"),
-    ("_cos_sin", "s = np.array([math.sin(x) for x in u.tolist()], dtype=np.float64)",
-     "s = np.array([math.sin(-x) for x in u.tolist()], dtype=np.float64)", "sin of the negated angle"),
-    ("_cos_sin", "return c[inv].reshape(phi.shape), s[inv].reshape(phi.shape)",
-     "return c[inv[::-1]].reshape(phi.shape), s[inv].reshape(phi.shape)", "cos taken for other angles"),
+    ("rotate", "c, s = _cos_sin(shift, freqs)", "s, c = _cos_sin(shift, freqs)", "cos and sin swapped"),
+    ("_cos_sin", "s = np.array([[math.sin(x) for x in row] for row in phi.tolist()], dtype=np.float64)",
+     "s = np.array([[math.sin(-x) for x in row] for row in phi.tolist()], dtype=np.float64)",
+     "sin of the negated angle"),
+    ("_cos_sin", "return c[inv].reshape(shift.shape + freqs.shape), s[inv]",
+     "return c[inv[::-1]].reshape(shift.shape + freqs.shape), s[inv]", "cos taken for other shifts"),
     ("rotate", "a, b = band[..., ia], band[..., ib]", "b, a = band[..., ia], band[..., ib]", "pair operands transposed"),
-    ("rotate", "[..., None] * freqs", "[..., None] * freqs[::-1]", "frequency index reversed"),
+    ("_cos_sin", "phi = u[:, None] * freqs", "phi = u[:, None] * freqs[::-1]", "frequency index reversed"),
     # pairing convention (Sec. 3.3)
     ("pair_dims", "return 2 * i, 2 * i + 1", "return i, i + half", "interleaved paired as half-split"),
     ("pair_dims", "return i, i + half", "return 2 * i, 2 * i + 1", "half-split paired as interleaved"),
