@@ -74,3 +74,27 @@ def test_random_sweep(L, first):
     for seed in range(first, first + 50):
         rng = _contig_case(L, seed)
         _paged_case(L, seed, rng)
+
+
+def _many_dirs(rng, n, k, seq=0):
+    cuts = sorted(rng.sample(range(n + 1), min(2 * k, n + 1)))
+    out = []
+    for i in range(0, len(cuts) - 1, 2):
+        s, e = cuts[i], cuts[i + 1]
+        r = rng.choice([0, 1, e - s, rng.randint(0, 2 * (e - s) + 3), max(0, e - s - 1), e - s + 1])
+        out.append(W.Dir(s, e, r, seq=seq))
+    return out
+
+
+@pytest.mark.parametrize("seed", [70001, 70002, 70003, 70004, 70005, 70006])
+def test_many_directives(L, seed):
+    """Calls of 20-400 directives on caches of 2,000-20,000 rows: many distinct shifts (the
+    cos/sin table written by several prep launches), several ordered-tile launches and rounds
+    (App. "Randomized edit-suite stress test" regime, at larger counts)."""
+    rng = random.Random(seed)
+    kind, dtype = [("mla", "bf16"), ("gqa", "bf16"), ("mla", "f32"), ("four", "bf16"), ("heads", "bf16")][seed % 5]
+    n = rng.choice([2000, 8000, 20000])
+    dirs = _many_dirs(rng, n, rng.randint(20, 400))
+    wl = TC._small_workload(rng, kind, dtype, rng.randint(1, 2), n, dirs, extra=rng.randint(0, 3000))
+    planes_dev, stubs_dev = W.alloc_contig(wl, DEV, seed=seed)
+    TC._run_and_check(L, wl, planes_dev, stubs_dev, f"many directives seed {seed} {kind}/{dtype} n={n} k={len(dirs)}")
