@@ -222,8 +222,9 @@ int leyline_splice_contig(const leyline_cache* cache, int64_t seq_len,
  * the counters and flags of, e.g., a small-shift splice of a 61-layer MLA cache of about 480K
  * tokens); use leyline_splice_contig with a caller workspace for those.  The call makes no
  * device allocation or free (no hipMalloc / hipFree, no allocating library routine) and clears
- * the counters and flags it needs with a kernel at its start.  Every call on one GPU shares that GPU's array: calls that may overlap
- * in time on one GPU (other streams, other threads) race and must be ordered by the caller.
+ * the counters and flags it needs with a kernel at its start.  Every call on one GPU shares that
+ * GPU's array: calls that may overlap in time on one GPU (other streams, other threads) race and
+ * must be ordered by the caller.
  */
 int leyline_splice_contig_noalloc(const leyline_cache* cache, int64_t seq_len,
                                   const leyline_directive* dirs, int32_t n_dirs,
