@@ -549,7 +549,7 @@ def cpu_leg(data, seconds, procs, out):
 
 
 def _host_cpus():
-    """CPUs this process may run on (the machine's CPU share, at most 16 on a one-GPU machine)."""
+    """CPUs this process may run on (its CPU affinity set)."""
     try:
         return len(os.sched_getaffinity(0))
     except AttributeError:
