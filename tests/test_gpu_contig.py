@@ -207,10 +207,13 @@ def test_small_random_splices(L, kind, dtype):
         _run_and_check(L, wl, planes_dev, stubs_dev, f"{kind}/{dtype} case {ci} n={n} dirs={dirs}")
 
 
-def test_mla_dsv3_32k_full(L):
-    wl = W.mla_dsv3_32k()
+@pytest.mark.parametrize("name", ["mla_dsv3_32k", "mla_dsv3_32k_split"])
+def test_mla_dsv3_32k_full(L, name):
+    """The 32K MLA splice, whole cache against the oracle; also on a cache that keeps K_pe and
+    c_kv in separate arrays."""
+    wl = W.WORKLOADS[name]()
     planes_dev, stubs_dev = W.alloc_contig(wl, DEV)
-    n_new = _run_and_check(L, wl, planes_dev, stubs_dev, "mla_dsv3_32k")
+    n_new = _run_and_check(L, wl, planes_dev, stubs_dev, name)
     assert n_new == 32768 - 4064
     print(f"[info] bf16 rotary elements bit-identical to the oracle: {PU.LAST_BF16_EXACT_FRACTION:.6f}")
 
@@ -337,7 +340,7 @@ def test_rotate_delta(L, kind, dtype, paged):
             before[pi] = g.reshape(before[pi].shape)
 
 
-@pytest.mark.parametrize("name", ["mla_dsv3_rotate_32k", "gqa_llama3_8b_rotate_16k"])
+@pytest.mark.parametrize("name", ["mla_dsv3_rotate_32k", "gqa_llama3_8b_rotate_16k", "mla_dsv3_rotate_split_32k"])
 def test_rotate_delta_full_size(L, name):
     """Re-anchoring in place at full size (the benchmark's rotate-only workloads): three whole
     layers against the oracle; every layer by properties (each member of the listed rows' pairs

@@ -551,10 +551,11 @@ def test_paged_131k_copy_on_write_full(L):
     assert kinds.count(O.REMAP) == 0 and kinds.count(O.ASSEMBLE) > 0
 
 
-@pytest.mark.parametrize("name", ["mla_dsv3_slots_32k", "gqa_llama3_8b_slots_16k"])
+@pytest.mark.parametrize("name", ["mla_dsv3_slots_32k", "gqa_llama3_8b_slots_16k", "mla_dsv3_slots_split_32k"])
 def test_token_slot_splice_full(L, name):
     """Full-size splices on token-slot caches: every downstream token keeps its slot (its
-    rotary band is rotated in place), only the replacement tokens take fresh slots."""
+    rotary band is rotated in place), only the replacement tokens take fresh slots.  The split
+    MLA layout keeps K_pe and c_kv in separate arrays."""
     wl = W.WORKLOADS[name]()
     pools, bt, bt_out, new_lens, plans = _check_sampled(L, wl, seed=17)
     kinds = [k for p in plans for k in p.kinds]

@@ -31,6 +31,9 @@ Workloads (MLA rows: latent c_kv[512] + K_pe[64]; GQA rows: 8 KV heads x 128):
   mla_dsv3_slots_rotate_32k
                       the same on a token-slot cache: the 32K MLA splice's downstream slots,
                       listed by physical slot, rotated in place
+  mla_dsv3_32k_split, mla_dsv3_slots_split_32k, mla_dsv3_rotate_split_32k
+                      the 32K MLA splice (contiguous, token slots) and in-place re-anchoring on a
+                      cache that keeps K_pe[64] and c_kv[512] in two arrays (layout study)
 """
 
 from __future__ import annotations
@@ -93,6 +96,11 @@ class Workload:
 def mla_plane(base=10000.0) -> PlaneDesc:
     row = MLA_LATENT + MLA_ROPE
     return PlaneDesc((row,), 1, row, MLA_LATENT, MLA_ROPE, 0, base)
+
+
+def mla_split_planes(base=10000.0) -> List[PlaneDesc]:
+    """The MLA row stored as two planes: K_pe[64] (all of it rotary) and the latent c_kv[512]."""
+    return [PlaneDesc((MLA_ROPE,), 1, MLA_ROPE, 0, MLA_ROPE, 0, base), PlaneDesc((MLA_LATENT,))]
 
 
 def gqa_planes(heads=8, dim=128, base=500000.0) -> List[PlaneDesc]:
@@ -238,6 +246,30 @@ def gqa_llama3_8b_rotate_16k() -> Workload:
                     capacity=w.capacity, rotate=(-2024, 6144, 16384 - 6144), seed=w.seed)
 
 
+def _split(w: Workload, name: str) -> Workload:
+    w.name = name
+    w.planes = mla_split_planes()
+    return w
+
+
+def mla_dsv3_32k_split() -> Workload:
+    """mla_dsv3_32k on a cache whose K_pe and c_kv live in separate arrays (same values, same
+    directive, same bytes)."""
+    return _split(mla_dsv3_32k(), "mla_dsv3_32k_split")
+
+
+def mla_dsv3_slots_split_32k() -> Workload:
+    """mla_dsv3_slots_32k with K_pe and c_kv in separate arrays: the in-place rotation of the
+    downstream slots reads and writes 128-byte K_pe rows of one array instead of 128-byte bands
+    of 1152-byte rows."""
+    return _split(mla_dsv3_slots_32k(), "mla_dsv3_slots_split_32k")
+
+
+def mla_dsv3_rotate_split_32k() -> Workload:
+    """mla_dsv3_rotate_32k with K_pe and c_kv in separate arrays."""
+    return _split(mla_dsv3_rotate_32k(), "mla_dsv3_rotate_split_32k")
+
+
 WORKLOADS = {
     "mla_1l_4k_f32": mla_1l_4k_f32,
     "mla_dsv3_32k": mla_dsv3_32k,
@@ -253,6 +285,9 @@ WORKLOADS = {
     "mla_dsv3_rotate_32k": mla_dsv3_rotate_32k,
     "gqa_llama3_8b_rotate_16k": gqa_llama3_8b_rotate_16k,
     "mla_dsv3_slots_rotate_32k": mla_dsv3_slots_rotate_32k,
+    "mla_dsv3_32k_split": mla_dsv3_32k_split,
+    "mla_dsv3_slots_split_32k": mla_dsv3_slots_split_32k,
+    "mla_dsv3_rotate_split_32k": mla_dsv3_rotate_split_32k,
 }
 
 
