@@ -131,6 +131,8 @@ def _small_workload(rng, kind, dtype, n_layers, n, dirs, extra=0):
         planes = [W.PlaneDesc((576,), 1, 576, 512, 64, 1, 10000.0)]
     elif kind == "four":      # the most planes a cache may have, both rotary styles and band widths
         planes = FOUR_PLANES
+    elif kind == "mla_split":  # K_pe and c_kv in two arrays: a plane that is all rotary band
+        planes = W.mla_split_planes()
     else:  # several interleaved heads with a partial rotary band, and a move-only plane
         planes = [W.PlaneDesc((4, 64), 4, 64, 32, 32, 0, 50000.0), W.PlaneDesc((128,))]
     cap = n + max(0, sum(d.stub_len - (d.span_end - d.span_start) for d in dirs)) + extra

@@ -69,6 +69,8 @@ def _random_workload(rng, page, kind, dtype, max_len=None):
         planes = [W.PlaneDesc((576,), 1, 576, 512, 64, 1, 10000.0)]
     elif kind == "gqa8":          # 2 KB rotated per row: re-used pages rotate in physical order
         planes = W.gqa_planes(heads=8, dim=128)
+    elif kind == "mla_split":     # K_pe and c_kv in two arrays: a plane that is all rotary band
+        planes = W.mla_split_planes()
     elif kind == "four":          # four planes, rotary bands of both access classes
         planes = [W.mla_plane(), W.PlaneDesc((2, 128), 2, 128, 0, 128, 1, 500000.0), W.PlaneDesc((256,)),
                   W.PlaneDesc((64,), 1, 64, 32, 32, 0, 10000.0)]

@@ -1,5 +1,6 @@
 """A wider randomized GPU parity sweep: for each seed one contiguous splice (1-8 directives of
-both signs on 1-3000 rows, 1-4 layers, seven plane layouts, bf16 and fp32) and one paged splice
+both signs on 1-3000 rows, 1-4 layers, seven plane layouts and the split MLA layout, bf16 and
+fp32) and one paged splice
 (1-4 sequences, page sizes 1 to 64 including 3 and 48, some with copy-on-write), each compared
 with the oracle as in the other GPU tests (Sec. 3.1 directive; Eq. "rotate")."""
 
@@ -29,9 +30,9 @@ def L():
     return leyline
 
 
-def _contig_case(L, seed):
+def _contig_case(L, seed, kinds=CONTIG_KINDS):
     rng = random.Random(seed)
-    kind, dtype = CONTIG_KINDS[seed % len(CONTIG_KINDS)]
+    kind, dtype = kinds[seed % len(kinds)]
     n = rng.choice([1, 5, 63, 64, 65, 300, 1000, 2047, 3000])
     dirs = TC._random_dirs(rng, n, rng.randint(1, 8))
     wl = TC._small_workload(rng, kind, dtype, rng.randint(1, 4), n, dirs, extra=rng.randint(0, 40))
@@ -40,8 +41,8 @@ def _contig_case(L, seed):
     return rng
 
 
-def _paged_case(L, seed, rng):
-    kind, dtype = PAGED_KINDS[seed % len(PAGED_KINDS)]
+def _paged_case(L, seed, rng, kinds=PAGED_KINDS):
+    kind, dtype = kinds[seed % len(kinds)]
     page = rng.choice([1, 2, 3, 4, 16, 48, 64])
     wl = TP._random_workload(rng, page, kind, dtype, max_len=rng.choice([200, 900, 3000]))
     cow = rng.random() < 0.3
@@ -74,6 +75,16 @@ def test_random_sweep(L, first):
     for seed in range(first, first + 50):
         rng = _contig_case(L, seed)
         _paged_case(L, seed, rng)
+
+
+@pytest.mark.parametrize("first", [6001])
+def test_random_sweep_split_layout(L, first):
+    """The same sweep on caches that keep K_pe and c_kv in two arrays (a plane that is all
+    rotary band next to a move-only plane), bf16 and fp32."""
+    kinds = [("mla_split", "bf16"), ("mla_split", "f32")]
+    for seed in range(first, first + 40):
+        rng = _contig_case(L, seed, kinds)
+        _paged_case(L, seed, rng, kinds)
 
 
 def _many_dirs(rng, n, k, seq=0):
