@@ -635,9 +635,9 @@ __global__ __launch_bounds__(TPB) void contig_chain_kernel(const KContigParams P
 }
 
 // Ordered tiles: every job of a call whose moves are too short-shifted for rounds.  Each
-// (job, plane) item is cut into tiles of tile_chunks chunks (KTILE_CHUNKS, or a whole number of
-// packed blocks for a packed item; counted from its first row) in
-// each layer.  Workgroups take tile tickets from a counter, in order; the items of a launch own
+// (job, plane) item is cut into tiles of tile_chunks chunks (KTILE_CHUNKS, a quarter of that in a
+// call of few tiles, or a whole number of packed blocks for a packed item; counted from its first
+// row) in each layer.  Workgroups take tile tickets from a counter, in order; the items of a launch own
 // consecutive ticket ranges in dependency order, and within an item ticket t is tile
 // t mod n_tiles of its processing order (a left shift ascending, a right shift descending) in
 // layer t / n_tiles, so that the tiles in flight cover one stretch of one layer (interleaving
@@ -678,6 +678,7 @@ struct TileCtx {
     int32_t total;           // chunks of the item in one layer
     int32_t end;             // end of the tile's chunks
     int32_t rows;            // rows of the item
+    int32_t slots;           // a thread's chunk slots that can fall inside the tile (tile-uniform)
     int32_t cs;              // first cos/sin entry (-1: copied unchanged)
     int32_t plane, flag0;
     bool move, pack;
@@ -701,6 +702,7 @@ __device__ __forceinline__ TileCtx tile_ctx(const KTileParams& P, int32_t ticket
     c.dst = lbase + I.dst0 * pl.token_stride;
     c.g0 = q * I.tile_chunks + int32_t(threadIdx.x);
     c.end = min(c.total, (q + 1) * I.tile_chunks);
+    c.slots = (c.end - q * I.tile_chunks + KTILE_TPB - 1) / KTILE_TPB;
     c.rows = int32_t(I.count);
     c.pack = LEYLINE_TILE_PACK && I.pack;
     c.cs = I.cs;
@@ -709,17 +711,21 @@ __device__ __forceinline__ TileCtx tile_ctx(const KTileParams& P, int32_t ticket
     return c;
 }
 
-// Every slot loads (past the end of the tile: the tile's last chunk, which stays unused), so
-// that the loads are issued back to back without branches between them.  A packed item's tiles
+// Every slot that can fall inside the tile loads (a thread past the end of the tile: the tile's
+// last chunk, which stays unused), so that the loads are issued back to back without divergent
+// branches between them; slots past every thread's share of a short tile (the quarter-size tiles
+// of small calls, an item's last tile) are skipped by a tile-uniform test.  A packed item's tiles
 // are whole packed blocks, so its units (row_unit) cover the same rows as in plain order.
 __device__ __forceinline__ void tile_load(const KTileParams& P, const TileCtx& c, u32x4 (&v)[KTILE_CPT]) {
     const KPlane& pl = P.planes[c.plane];
 #pragma unroll
     for (int i = 0; i < KTILE_CPT; ++i) {
-        const int32_t gc = min(c.g0 + i * KTILE_TPB, c.end - 1);
-        int32_t r, u;
-        row_unit(pl, c.pack, gc, c.rows, r, u);
-        v[i] = ld16(c.src + int64_t(r) * c.src_step + int64_t(u) * 16);
+        if (i == 0 || i < c.slots) {
+            const int32_t gc = min(c.g0 + i * KTILE_TPB, c.end - 1);
+            int32_t r, u;
+            row_unit(pl, c.pack, gc, c.rows, r, u);
+            v[i] = ld16(c.src + int64_t(r) * c.src_step + int64_t(u) * 16);
+        }
     }
 }
 
@@ -730,7 +736,7 @@ __device__ __forceinline__ void tile_store(const KTileParams& P, const TileCtx& 
 #pragma unroll
     for (int i = 0; i < KTILE_CPT; ++i) {
         const int32_t g = c.g0 + i * KTILE_TPB;
-        if (g < c.end) {
+        if ((i == 0 || i < c.slots) && g < c.end) {
             int32_t r, u;
             row_unit(pl, c.pack, g, c.rows, r, u);
             if (c.cs >= 0) rotate_chunk<ESZ, ROT>(pl, v[i], u, lcs, 0);

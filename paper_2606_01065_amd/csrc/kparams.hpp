@@ -163,6 +163,14 @@ struct KContigParams {
 constexpr int KTILE_CPT = LEYLINE_TILE_CPT;
 constexpr int KTILE_TPB = LEYLINE_TILE_TPB;
 constexpr int KTILE_CHUNKS = KTILE_TPB * KTILE_CPT;
+// A call whose full-size tiles number fewer than KTILE_SMALL_TICKETS (over all layers) runs in
+// tiles of KTILE_SMALL_CHUNKS chunks instead (the same kernel; a thread's slots past its tile's
+// end load the tile's last chunk and store nothing).
+#ifndef LEYLINE_TILE_SMALL_TICKETS
+#define LEYLINE_TILE_SMALL_TICKETS 256
+#endif
+constexpr int KTILE_SMALL_TICKETS = LEYLINE_TILE_SMALL_TICKETS;
+constexpr int KTILE_SMALL_CHUNKS = KTILE_CHUNKS / 4;
 
 // One (job, plane) item of an ordered-tile launch: a move (rows [src0, src0 + count) to
 // [dst0, dst0 + count), dst0 = src0 + delta) or a replacement copy (rows of `stub` to

@@ -215,10 +215,11 @@ int64_t align256(int64_t v) { return (v + 255) & ~int64_t(255); }
 // Every job of the call as ordered-tile items, in dependency-level order, packed into launches of
 // at most KTILE_MAX_ITEMS items.  An item waits (inside its launch) for the earlier moves of its
 // plane whose source rows it overwrites; items of earlier launches are finished by stream order.
-// One cos/sin block per distinct shift goes into the call's table.
+// One cos/sin block per distinct shift goes into the call's table.  Tiles hold tile_base chunks
+// (or a whole number of packed blocks up to that).
 int plan_tiles(const leyline_cache* cache, const leyline_directive* dirs, const KPlane* planes,
                int n_planes, const std::vector<ContigJobHost>& jobs, const std::vector<int>& level,
-               ContigSchedule* out) {
+               int32_t tile_base, ContigSchedule* out) {
     std::vector<size_t> order(jobs.size());
     for (size_t k = 0; k < order.size(); ++k) order[k] = k;
     std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return level[a] < level[b]; });
@@ -261,10 +262,10 @@ int plan_tiles(const leyline_cache* cache, const leyline_directive* dirs, const 
                 it.cs = -1;
             }
             // rotating narrow interleaved bands: tiles of whole packed blocks, units packed
-            it.tile_chunks = KTILE_CHUNKS;
+            it.tile_chunks = tile_base;
             const int32_t blk = planes[p].pack_groups * planes[p].tpr;
-            if (LEYLINE_TILE_PACK && move && it.cs >= 0 && planes[p].pack_groups && blk <= KTILE_CHUNKS) {
-                it.tile_chunks = (KTILE_CHUNKS / blk) * blk;
+            if (LEYLINE_TILE_PACK && move && it.cs >= 0 && planes[p].pack_groups && blk <= tile_base) {
+                it.tile_chunks = (tile_base / blk) * blk;
                 it.pack = 1;
             }
             const int64_t tiles = tile_count(x.count, planes[p].tpr, it.tile_chunks);
@@ -408,7 +409,20 @@ int plan_contig(const leyline_cache* cache, int64_t seq_len, const leyline_direc
         const bool big_rounds = nr == 1 || m * row_bytes_all * cache->n_layers >= ROUND_MIN_BYTES;
         if (nr > MAX_ROUNDS || !big_rounds) need_tiles = true;
     }
-    if (tiles_ok && need_tiles) return plan_tiles(cache, dirs, planes, n_planes, jobs, level, out);
+    if (tiles_ok && need_tiles) {
+        // A call of few full-size tiles cannot fill the device and is bound by each tile's chain
+        // of latencies (ticket, loads, flag, stores): it is planned again with quarter-size tiles.
+        const size_t cs_before = out->cs.size();
+        int rc = plan_tiles(cache, dirs, planes, n_planes, jobs, level, KTILE_CHUNKS, out);
+        int64_t tickets = 0;
+        for (const TileLaunchHost& tl : out->tile_launches) tickets += tl.tickets;
+        if (rc == LEYLINE_OK && tickets < KTILE_SMALL_TICKETS) {
+            out->cs.resize(cs_before);
+            out->tile_launches.clear();
+            rc = plan_tiles(cache, dirs, planes, n_planes, jobs, level, KTILE_SMALL_CHUNKS, out);
+        }
+        return rc;
+    }
 
     const int32_t cs_need = cos_sin_per_shift(cache);
     for (int lv = 0; lv < n_levels; ++lv) {

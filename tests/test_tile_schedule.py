@@ -37,6 +37,13 @@ def sim(tmp_path_factory):
 
 
 @pytest.fixture(scope="module")
+def sim_full_tiles(tmp_path_factory):
+    """The planner with the quarter-size tiles of small calls switched off: every call here is
+    small, so this build is the one that runs the full-size tiles of larger calls."""
+    return _build(tmp_path_factory, "tile_sim_full", ["-DLEYLINE_TILE_SMALL_TICKETS=0"])
+
+
+@pytest.fixture(scope="module")
 def sim_packed(tmp_path_factory):
     """The planner and unit layout of the fp64-pair build, whose tile launches pack narrow
     interleaved bands (MLA K_pe) and cut those items into tiles of whole packed blocks."""
@@ -49,6 +56,15 @@ def test_tile_schedules_are_race_free_and_complete(sim, seed):
     assert r.returncode == 0, r.stdout + r.stderr
     ok, cases, tiles, gave_up = r.stdout.split()
     assert ok == "ok" and int(cases) > 2000 and int(tiles) > 50000 and int(gave_up) == 0
+
+
+@pytest.mark.parametrize("persist", [0, 1])
+def test_full_size_tile_schedules_are_race_free_and_complete(sim_full_tiles, persist):
+    r = subprocess.run([sim_full_tiles, "19", "2500", "0", str(persist)], capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode == 0, r.stdout + r.stderr
+    ok, cases, tiles, gave_up = r.stdout.split()
+    assert ok == "ok" and int(cases) > 2000 and int(tiles) > 10000 and int(gave_up) == 0
 
 
 def test_persistent_workgroups_with_a_prefetched_tile_never_stall(sim):
