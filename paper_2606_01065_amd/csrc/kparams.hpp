@@ -167,7 +167,7 @@ constexpr int KTILE_CHUNKS = KTILE_TPB * KTILE_CPT;
 // tiles of KTILE_SMALL_CHUNKS chunks instead (the same kernel; a thread's slots past its tile's
 // end load the tile's last chunk and store nothing).
 #ifndef LEYLINE_TILE_SMALL_TICKETS
-#define LEYLINE_TILE_SMALL_TICKETS 256
+#define LEYLINE_TILE_SMALL_TICKETS 96
 #endif
 constexpr int KTILE_SMALL_TICKETS = LEYLINE_TILE_SMALL_TICKETS;
 constexpr int KTILE_SMALL_CHUNKS = KTILE_CHUNKS / 4;
