@@ -163,9 +163,9 @@ struct KContigParams {
 constexpr int KTILE_CPT = LEYLINE_TILE_CPT;
 constexpr int KTILE_TPB = LEYLINE_TILE_TPB;
 constexpr int KTILE_CHUNKS = KTILE_TPB * KTILE_CPT;
-// A call whose full-size tiles number fewer than KTILE_SMALL_TICKETS (over all layers) runs in
-// tiles of KTILE_SMALL_CHUNKS chunks instead (the same kernel; a thread's slots past its tile's
-// end load the tile's last chunk and store nothing).
+// A call whose full-size tiles number fewer than KTILE_SMALL_TICKETS (over all layers) cannot
+// fill the device and runs in tiles of KTILE_SMALL_CHUNKS chunks instead (the same kernel, which
+// skips the load slots that no thread of a short tile needs).
 #ifndef LEYLINE_TILE_SMALL_TICKETS
 #define LEYLINE_TILE_SMALL_TICKETS 96
 #endif
